@@ -1,0 +1,268 @@
+#!/usr/bin/env python3
+"""Throughput of the Hotline hot path on one MI355X.
+
+A step is one pass of the whole per-mini-batch path over one batch: global ids,
+classification, partition into popular / non-popular mu-batches, remap, cold
+gather for the non-popular mu-batch, forward of both mu-batches and one
+coalesced SGD step.  The learning phase (access counting over 16 profiling
+batches, top-K selection, hot-cache fill) runs once before and is reported
+separately.  Inputs (32 measured batches, their gradients, the host table) are
+resident before the timed region starts.
+
+Prints one JSON line on stdout; progress goes to stderr."""
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "embedding lookups/sec (fwd+bwd) + classify samples/sec; % of HBM peak GB/s"
+HBM_PEAK = 8.0e12          # MI355X HBM3E, bytes/s
+LINK_PEAK = 64.0e9         # PCIe Gen5 x16, one direction, bytes/s
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def kernel_bytes(name, st):
+    """Algorithmic bytes of one launch of kernel `name` (per-step statistics st)."""
+    L, nb, B, U, R, O = st["L"], st["n_bags"], st["B"], st["U"], st["R"], st["O"]
+    return {
+        "hl_k_gids": 4 * L + 4 * (nb + 1) + 4 * L,
+        "cl_kernel": 4 * L + 4 * (nb + 1) + B,
+        "pt_emit": B + 4 * B,
+        "rm_kernel": 8 * L,
+        # forward, both launches of a step together: codes, offsets, each referenced row once, outputs
+        "eb_fwd": (4 * L + 4 * (nb + 1) + U * R + nb * O) / 2.0,
+        "bw_prep": 4 * L + 4 * (nb + 1) + 8 * L,
+        "srt_pass": 16 * L,
+        "bw_reduce1": 8 * L + nb * O + 2 * U * R,
+    }.get(name)
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=64)
+    ap.add_argument("--warmup", type=int, default=8)
+    ap.add_argument("--workload", default="dlrm-large")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the oracle baseline")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py: this build measures one GPU only (asked for --gpus {args.gpus}); the path shards "
+              "by samples across GPUs but no multi-GPU run is part of it", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2204_05436_amd import configs, hotline as hl, workload as W
+    from paper_2204_05436_amd.runner import STAGES, HotPath, to_device
+
+    dev = "cuda:0"
+    torch.cuda.set_device(0)
+    w = configs.WORKLOADS[args.workload]
+    rows = W.table_rows(w)
+    n_rows = int(rows.sum(dtype=np.int64))
+    k_cap = w.k_cap(n_rows)
+    log(f"[bench] workload {w.name}: {w.n_tables} tables, {n_rows} rows, dim {w.dim} {w.dtype}, batch {w.batch}")
+    t0 = time.time()
+    prof = [W.make_batch(w, rows, i) for i in range(w.profile_batches)]
+    meas_idx = list(range(w.profile_batches, w.profile_batches + w.measured_batches))
+    meas = [W.make_batch(w, rows, i) for i in meas_idx]
+    log(f"[bench] batches generated in {time.time() - t0:.1f}s")
+    table = hl.HostTable(n_rows, w.dim, w.dtype)
+    t0 = time.time()
+    W.fill_weights_torch(w, table.torch_view(), dev)
+    torch.cuda.synchronize()
+    log(f"[bench] host table {table.nbytes / 2**30:.2f} GiB pinned+filled in {time.time() - t0:.1f}s")
+    dprof = [to_device(b, dev) for b in prof]
+    dmeas = []
+    for i, b in zip(meas_idx, meas):
+        dmeas.append(to_device(b, dev, W.make_dy(w, i, b.n_bags)))
+    max_l = max(b.n_lookups for b in prof + meas)
+    hp = HotPath(w, rows, table, max_l, w.batch, device=dev)
+    log(f"[bench] inputs resident; workspace {hp.ws.numel() / 2**20:.1f} MiB, hot cache {k_cap} rows")
+
+    # learning phase
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    n_hot = hp.learn(dprof)
+    e1.record()
+    torch.cuda.synchronize()
+    learn_ms = e0.elapsed_time(e1)
+    log(f"[bench] learning phase {learn_ms:.2f} ms, n_hot {n_hot}")
+
+    # per-batch statistics (untimed pass over every measured batch)
+    stats = []
+    for b in dmeas:
+        hp.step(b)
+        torch.cuda.synchronize()
+        L = b.n_lookups
+        U = int(torch.unique(hp.codes[:L]).numel())
+        c = hp.counts.cpu().numpy()
+        stats.append(dict(L=L, n_bags=b.n_bags, B=b.n_samples, U=U, n_pop=int(c[0]), n_cold=int(hp.n_cold.item()),
+                          R=hp.staging.element_size() * w.dim, O=4 * w.dim))
+    err = hp.device_error()
+    if err:
+        raise SystemExit(f"device error word {err:#x} after the statistics pass")
+    log("[bench] statistics pass done")
+    for i in range(args.warmup):
+        hp.step(dmeas[i % len(dmeas)])
+    torch.cuda.synchronize()
+    log(f"[bench] warmup {args.warmup} steps done")
+
+    # timed region: K steps, stage events every step, per-kernel event pairs
+    K = args.steps
+    hl.hl_trace_enable(hp.h, 64 * K + 64)
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(len(STAGES) + 1)] for _ in range(K)]
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    start = torch.cuda.Event(enable_timing=True)
+    stop = torch.cuda.Event(enable_timing=True)
+    start.record()
+    for i in range(K):
+        hp.step(dmeas[i % len(dmeas)], events=ev[i])
+    stop.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_start
+    total_ms = start.elapsed_time(stop)
+    log(f"[bench] timed {K} steps: {total_ms:.3f} ms (wall {wall * 1e3:.1f} ms)")
+    err = hp.device_error()
+    if err:
+        raise SystemExit(f"device error word {err:#x} in the timed region")
+
+    # per-stage and per-kernel times
+    stage_ms = {s: 0.0 for s in STAGES}
+    for i in range(K):
+        for j, s in enumerate(STAGES):
+            stage_ms[s] += ev[i][j].elapsed_time(ev[i][j + 1])
+    stage_ms = {s: v / K for s, v in stage_ms.items()}
+    kern = {}
+    for i in range(hl.hl_trace_count(hp.h)):
+        name, ms = hl.hl_trace_read(hp.h, i)
+        k = kern.setdefault(name, [0, 0.0])
+        k[0] += 1
+        k[1] += ms
+    hl.hl_trace_enable(hp.h, 0)
+    kernels = {n: {"launches_per_step": c / K, "ms_per_step": t / K, "avg_us": 1e3 * t / c}
+               for n, (c, t) in sorted(kern.items(), key=lambda x: -x[1][1])}
+
+    steps_stats = [stats[i % len(stats)] for i in range(K)]
+    avg = {k: float(np.mean([s[k] for s in steps_stats])) for k in steps_stats[0]}
+    L_tot = sum(s["L"] for s in steps_stats)
+    B_tot = sum(s["B"] for s in steps_stats)
+    value = L_tot / (total_ms / 1e3)
+    t_fb = stage_ms["fwd_pop"] + stage_ms["fwd_nonpop"] + stage_ms["bwd"]
+    fwd_b = 4 * avg["L"] + 4 * (avg["n_bags"] + 1) + avg["U"] * avg["R"] + avg["n_bags"] * avg["O"]
+    bwd_b = 4 * avg["L"] + 4 * (avg["n_bags"] + 1) + avg["n_bags"] * avg["O"] + 2 * avg["U"] * avg["R"]
+    fb_frac = (fwd_b + bwd_b) / (t_fb / 1e3) / HBM_PEAK
+
+    # roofline of the dominant HBM-bound kernel (the host-link-bound row copy excluded)
+    dom = None
+    for n, k in kernels.items():
+        if n in ("cg_finalize", "hl_k_gather"):
+            continue
+        if kernel_bytes(n, avg) is not None:
+            dom = n
+            break
+    kd = kernels[dom]
+    ach = kernel_bytes(dom, avg) / (kd["avg_us"] * 1e-6)
+    roof = {"kernel": dom, "bound": "hbm", "achieved": ach / 1e9, "peak": HBM_PEAK / 1e9, "unit": "GB/s",
+            "frac": ach / HBM_PEAK, "traffic": None, "avg_us": kd["avg_us"],
+            "algorithmic_bytes_per_launch": kernel_bytes(dom, avg)}
+    link = None
+    if "cg_finalize" in kernels:
+        gb = avg["n_cold"] * avg["R"]
+        link = {"kernel": "cg_finalize", "bytes_per_launch": gb, "avg_us": kernels["cg_finalize"]["avg_us"],
+                "achieved_GBps": gb / (kernels["cg_finalize"]["avg_us"] * 1e-6) / 1e9, "peak_GBps": LINK_PEAK / 1e9}
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(w, rows, prof, meas, meas_idx, table, k_cap, args.cpu_seconds)
+
+    res = {
+        "metric": METRIC, "value": value, "unit": "lookups/s", "n_gpus": 1, "steps": K, "warmup": args.warmup,
+        "ms_per_step": total_ms / K, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f32", "data": "synthetic",
+        "config": {"workload": w.name, "tables": w.n_tables, "rows": n_rows, "dim": w.dim, "storage": w.dtype,
+                   "batch": w.batch, "bags_per_sample": w.bags_per_sample, "lookups_per_batch": avg["L"],
+                   "zipf_alpha": w.alpha, "hot_cache_rows": k_cap, "n_hot": n_hot,
+                   "profile_batches": w.profile_batches, "measured_batches": w.measured_batches,
+                   "parallelism": "single-gpu"},
+        "fwd_bwd_lookups_per_s": avg["L"] / (t_fb / 1e3),
+        "fwd_bwd_hbm_frac": fb_frac,
+        "fwd_bwd_algorithmic_bytes": fwd_b + bwd_b,
+        "classify_samples_per_s": avg["B"] / ((stage_ms["classify"] + stage_ms["partition"]) / 1e3),
+        "popular_fraction": avg["n_pop"] / avg["B"],
+        "unique_rows_per_batch": avg["U"], "cold_rows_per_batch": avg["n_cold"],
+        "learning_phase_ms": learn_ms,
+        "stages_ms": stage_ms, "kernels": kernels,
+        "roofline": roof, "link_roofline": link, "cpu_baseline": cpu,
+    }
+    print(json.dumps(res), flush=True)
+    hp.close()
+    table.close()
+
+
+def cpu_baseline(w, rows, prof, meas, meas_idx, table, k_cap, budget_s):
+    """The oracle (single-threaded C, fp64) on the same batches: learning phase once
+    (untimed), then the per-batch steps timed batch by batch until the budget is spent."""
+    import oracle as O
+    from paper_2204_05436_amd import workload as W
+
+    n_rows = int(rows.sum(dtype=np.int64))
+    counts = np.zeros(n_rows, dtype=np.uint32)
+    for p in prof:
+        g, _ = O.gids(rows, p.rows, p.bag_ptr)
+        O.count(n_rows, [g], counts)
+    hot = O.topk(counts, k_cap)
+    w_hot = O.gather(table.array, hot)
+    done, L, B, t_all, t_cls = 0, 0, 0, 0.0, 0.0
+    log("[bench] cpu baseline (oracle) ...")
+    for i, mb in zip(meas_idx, meas):
+        dY = W.make_dy(w, i, mb.n_bags)
+        bps = mb.bags_per_sample
+        t0 = time.perf_counter()
+        g, _ = O.gids(rows, mb.rows, mb.bag_ptr)
+        flags = O.classify(hot, g, mb.bag_ptr, mb.n_samples, bps)
+        pop, nonpop = O.partition(flags)
+        t1 = time.perf_counter()
+        codes = O.remap(hot, g)
+        cold, codes = O.cold_plan(g, codes, mb.bag_ptr, nonpop, len(nonpop), bps, k_cap)
+        stg = O.gather(table.array, cold)
+        O.embbag_fwd(w.dtype, w_hot, k_cap, stg, codes, mb.bag_ptr, pop, len(pop), bps, mb.n_bags)
+        O.embbag_fwd(w.dtype, w_hot, k_cap, stg, codes, mb.bag_ptr, nonpop, len(nonpop), bps, mb.n_bags)
+        O.embbag_bwd_sgd(w.dtype, w_hot, k_cap, stg, codes, mb.bag_ptr, None, mb.n_samples, bps, dY, w.lr)
+        t2 = time.perf_counter()
+        t_all += t2 - t0
+        t_cls += t1 - t0
+        L += mb.n_lookups
+        B += mb.n_samples
+        done += 1
+        if t_all >= budget_s:
+            break
+    log(f"[bench] cpu baseline: {done} batches in {t_all:.1f}s")
+    return {"value": L / t_all, "unit": "lookups/s", "cores": 1, "kind": "oracle",
+            "classify_samples_per_s": B / t_cls,
+            "sample": f"{done} measured batches of {w.name}, every per-batch step, single-threaded fp64 oracle",
+            "host_cpu": _cpu_model(), "host_nproc": os.cpu_count()}
+
+
+def _cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,227 @@
+/*
+ * hotline.h -- C ABI of libhotline.so, the MI355X (gfx950) hot path of the
+ * Hotline heterogeneous recommendation-training pipeline ("Heterogeneous
+ * Acceleration Pipeline for Recommendation System Training", arXiv 2204.05436).
+ *
+ * Conventions (all entry points):
+ *  - Pointers are DEVICE pointers unless marked (host).  w_host is a pointer
+ *    the GPU can dereference to the pinned, device-mapped host table
+ *    (hl_host_alloc returns one).
+ *  - The caller owns every buffer, including workspaces; the handle owns only
+ *    its profiling and hot-set state.  No call allocates memory after
+ *    hl_create (hl_host_alloc / hl_workspace_* aside).
+ *  - Calls are asynchronous and stream-ordered on `stream` (a hipStream_t;
+ *    NULL = the null stream) unless stated otherwise.  A handle and a
+ *    workspace are not thread-safe and belong to one stream at a time.
+ *  - Argument errors found on the host return synchronously (HL_ERR_*) and
+ *    enqueue nothing.  Errors found by a kernel (an id outside the tables, a
+ *    code naming no row, staging overflow) set bits of the handle's device
+ *    error word (HL_DEVERR_*), read with hl_last_device_error; outputs of the
+ *    call are then unspecified, except where stated.
+ *  - Lookup layout (sample-major CSR): bag index = (b*steps + s)*n_tables + t;
+ *    sample b owns bags [b*bps, (b+1)*bps) where bps = bags_per_sample;
+ *    bag_ptr[n_bags+1] (int32) indexes the per-lookup arrays; the table of
+ *    bag j is j % n_tables.
+ *  - Row ids: gid = (rows of tables before t) + row, < 2^32-1.
+ *  - Slot codes (int32): [0, n_hot) = hot-cache slot (the row's rank among
+ *    the ascending hot ids); [k_cap, k_cap + staging rows) = staging row of a
+ *    gathered cold row; -1 = cold row not yet gathered (invalid for the
+ *    embedding calls).
+ *  - Embedding rows: dim elements of fp32 or bf16 (storage); pooled outputs
+ *    and gradients are always fp32, [n_bags, dim] row-major.
+ */
+#ifndef HOTLINE_H
+#define HOTLINE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  HL_OK = 0,
+  HL_ERR_INVALID_ARG = 1,  /* bad pointer/size/shape found on the host */
+  HL_ERR_OUT_OF_RANGE = 2, /* a value outside its table or capacity (host-checked) */
+  HL_ERR_CAPACITY = 3,     /* a buffer or workspace is too small */
+  HL_ERR_HIP = 4,          /* the HIP runtime reported an error */
+  HL_ERR_UNSUPPORTED = 5,  /* shape or dtype this build does not handle */
+  HL_ERR_DEVICE = 6        /* hl_last_device_error: the device error word is set */
+} hl_status;
+
+/* bits of the device error word */
+#define HL_DEVERR_OUT_OF_RANGE 0x1u /* a table row >= its table's rows, or a gid >= n_rows */
+#define HL_DEVERR_BAD_CODE 0x2u     /* a slot code naming no row in an embedding call */
+#define HL_DEVERR_CAPACITY 0x4u     /* cold rows exceed the staging capacity */
+#define HL_DEVERR_BAD_HOTSET 0x8u   /* hl_set_hot: ids not strictly ascending or >= n_rows */
+#define HL_DEVERR_STALL 0x10u       /* a cross-block wait hit its spin limit (never expected) */
+#define HL_DEVERR_SHAPE 0x20u       /* bag_ptr[n_bags] differs from the n_lookups passed */
+
+typedef enum { HL_F32 = 0, HL_BF16 = 1 } hl_dtype;
+
+typedef struct hl_handle hl_handle;
+typedef void* hl_stream; /* hipStream_t */
+
+const char* hl_status_string(hl_status s);
+
+/* ---------------------------------------------------------------- handle --
+ * Tables and their base registers: the accelerator's Address Registers hold
+ * each table's base (Sec. V-A "Data Dispatcher"; s_wr of the ISA table).
+ * rows_per_table (host, n_tables entries) fixes gid = base[t] + row; total
+ * rows must be < 2^32-1.  k_cap is the hot-cache capacity in rows (>= 1).
+ * Allocates the handle's device state on the current device: access counts
+ * (4 B/row), hot-set bitmap (1 bit/row) and rank directory (4 B per 256 rows).
+ * Synchronous. */
+hl_status hl_create(hl_handle** out, int32_t n_tables, const uint32_t* rows_per_table, int32_t dim,
+                    hl_dtype dtype, uint32_t k_cap);
+hl_status hl_destroy(hl_handle* h);
+uint64_t hl_n_rows(const hl_handle* h);
+uint32_t hl_n_hot(const hl_handle* h);   /* size of the current hot set (host copy) */
+uint32_t hl_k_cap(const hl_handle* h);
+
+/* Workspace bytes for calls with up to max_lookups lookups, max_bags bags and
+ * max_samples samples.  A workspace must be zero-filled once before its first
+ * use (hl_workspace_init, or any zero fill) and then belongs to this handle;
+ * the calls keep it reusable.  Used by hl_partition, hl_cold_gather and
+ * hl_embbag_bwd_sgd (never two of them concurrently). */
+size_t hl_workspace_bytes(const hl_handle* h, int64_t max_lookups, int64_t max_bags,
+                          int32_t max_samples);
+hl_status hl_workspace_init(void* workspace, size_t bytes, hl_stream stream);
+
+/* ----------------------------------------------------- address generation --
+ * gids[i] = base[table of lookup i] + rows[i] for the n_bags bags of bag_ptr
+ * (Sec. V-A: the memory controller forms row addresses from the Address
+ * Registers).  A row >= its table's size yields gid 0xFFFFFFFF and sets
+ * HL_DEVERR_OUT_OF_RANGE. */
+hl_status hl_lookup_gids(const hl_handle* h, const uint32_t* rows, const int32_t* bag_ptr,
+                         int64_t n_bags, uint32_t* gids, hl_stream stream);
+
+/* ------------------------------------------------------------- profiling --
+ * Learning phase (Sec. IV "The Learning Phase"; Sec. V-B Embedding Access
+ * Logger): counts[gid] += 1 for each of the n lookups of a sampled
+ * mini-batch, duplicates included.  Ids >= n_rows are skipped and set
+ * HL_DEVERR_OUT_OF_RANGE. */
+hl_status hl_profile_count(hl_handle* h, const uint32_t* gids, int64_t n, hl_stream stream);
+
+/* Copy the access counts (n_rows uint32) to counts_out. */
+hl_status hl_profile_counts(const hl_handle* h, uint32_t* counts_out, hl_stream stream);
+
+/* Hot set = the k most accessed rows (exact counts: the "Oracle LFU" the paper
+ * measures its tracker against, Sec. V-B), among rows accessed at least once,
+ * ties to the smaller id; n_hot = min(k, #accessed), k <= k_cap.  Writes the
+ * hot ids in ascending order to hot_ids_out (device, >= min(k, n_rows)
+ * entries), rebuilds the membership bitmap and rank directory, stores n_hot in
+ * the handle and in *n_hot_out (host).  reset_counts != 0 zeroes the counts
+ * afterwards.  Synchronous (waits for `stream`). */
+hl_status hl_profile_topk(hl_handle* h, uint32_t k, uint32_t* hot_ids_out, uint32_t* n_hot_out,
+                          int reset_counts, hl_stream stream);
+
+/* Install an explicit hot set: n_hot strictly ascending ids < n_rows (device).
+ * Rebuilds bitmap and rank directory; n_hot <= k_cap.  Violations set
+ * HL_DEVERR_BAD_HOTSET (the set is then unspecified). */
+hl_status hl_set_hot(hl_handle* h, const uint32_t* hot_ids, uint32_t n_hot, hl_stream stream);
+
+/* Fill the hot cache: w_hot[s] = w_host[hot_ids[s]] for s < n_hot (the hot
+ * rows are copied to GPU memory after learning, Sec. IV). */
+hl_status hl_hot_fill(const hl_handle* h, const uint32_t* hot_ids, const void* w_host, void* w_hot,
+                      hl_stream stream);
+
+/* Mini-batch shape used below: n_samples samples of bags_per_sample bags,
+ * bag_ptr[n_samples*bags_per_sample + 1] (device), and n_lookups (host) =
+ * bag_ptr[n_samples*bags_per_sample] (a mismatch sets HL_DEVERR_SHAPE).
+ * Sample selection (mu-batch calls): sample_ids == NULL selects every
+ * sample; otherwise sample_ids[0..n) with n = *n_sel_dev when n_sel_dev is
+ * not NULL (a device count, e.g. from hl_partition) else n_sel_max; n must
+ * not exceed n_sel_max. */
+
+/* -------------------------------------------------------- classification --
+ * flags[b] = 1 iff every lookup of sample b names a hot row, else 0 (a single
+ * non-hot lookup makes the input non-popular: Sec. I insight 2, Sec. V-C
+ * Lookup Engine).  A sample without lookups is popular. */
+hl_status hl_classify(const hl_handle* h, const uint32_t* gids, const int32_t* bag_ptr,
+                      int32_t n_samples, int32_t bags_per_sample, int64_t n_lookups, uint8_t* flags,
+                      hl_stream stream);
+
+/* Mini-batch fragmentation into the popular and non-popular mu-batches, with
+ * O u X = M and O n X = {} (Sec. IV-A, Eq. 3): pop_ids = ascending samples with
+ * flag 1, nonpop_ids = ascending samples with flag 0 (each list sized
+ * n_samples).  counts_dev[0] = |O|, counts_dev[1] = |X| (device). */
+hl_status hl_partition(const hl_handle* h, const uint8_t* flags, int32_t n_samples, int32_t* pop_ids,
+                       int32_t* nonpop_ids, int32_t* counts_dev, void* workspace, size_t ws_bytes,
+                       hl_stream stream);
+
+/* codes[i] = hot slot of gids[i], or -1 when the row is not hot. */
+hl_status hl_remap(const hl_handle* h, const uint32_t* gids, int64_t n, int32_t* codes,
+                   hl_stream stream);
+
+/* ------------------------------------------------------------ cold gather --
+ * Working parameters of a mu-batch (Sec. V-A: DMA reads of non-hot rows from
+ * CPU memory; dma_rd of the ISA).  Over the lookups of the selected samples
+ * whose code is -1: cold_ids_out = their distinct gids, ascending; each such
+ * code becomes k_cap + (index in cold_ids_out); staging[u] = w_host[cold_ids[u]]
+ * bit for bit (rows read by the GPU over the host link).  n_cold_dev (device)
+ * receives the number of cold rows.  If it exceeds staging_cap_rows the call
+ * sets HL_DEVERR_CAPACITY and writes nothing but n_cold_dev and workspace.
+ * Lookups whose code is neither -1 nor a hot slot are left alone. */
+hl_status hl_cold_gather(hl_handle* h, const uint32_t* gids, int32_t* codes, const int32_t* bag_ptr,
+                         int32_t n_samples, int32_t bags_per_sample, int64_t n_lookups,
+                         const int32_t* sample_ids, const int32_t* n_sel_dev, int32_t n_sel_max,
+                         const void* w_host, void* staging, int32_t staging_cap_rows,
+                         uint32_t* cold_ids_out, int32_t* n_cold_dev, void* workspace,
+                         size_t ws_bytes, hl_stream stream);
+
+/* -------------------------------------------------------------- embedding --
+ * Sum pooling (Sec. V-D Reducer, sparse-length element-wise sum; v_add of the
+ * ISA): out[bag] = sum over the bag's lookups of row(code) accumulated in fp32
+ * (bf16 rows widened exactly), for every bag of the selected samples,
+ * written at the bag's own position of out [n_samples*bags_per_sample, dim].  row(c) = w_hot[c] for c < n_hot, staging[c - k_cap]
+ * for k_cap <= c < k_cap + staging_rows; any other code sets HL_DEVERR_BAD_CODE
+ * and contributes nothing.  An empty bag pools to zero. */
+hl_status hl_embbag_fwd(const hl_handle* h, const void* w_hot, const void* staging,
+                        int32_t staging_rows, const int32_t* codes, const int32_t* bag_ptr,
+                        int32_t n_samples, int32_t bags_per_sample, int64_t n_lookups,
+                        const int32_t* sample_ids, const int32_t* n_sel_dev, int32_t n_sel_max,
+                        float* out, hl_stream stream);
+
+/* Backward of sum pooling plus one SGD step with duplicate rows coalesced
+ * (hot rows updated in GPU memory, Sec. IV): for every distinct code c among
+ * the selected bags' lookups, G_c = sum of dY[bag(i)] over its lookups and
+ * row(c) <- round_storage(row(c) - lr * G_c), round to nearest even.  Each
+ * row is written once; rows no lookup names are untouched.  Deterministic:
+ * the summation order depends only on the inputs.  dY: [n_samples *
+ * bags_per_sample, dim] fp32.  Invalid codes set HL_DEVERR_BAD_CODE and are
+ * skipped. */
+hl_status hl_embbag_bwd_sgd(hl_handle* h, void* w_hot, void* staging, int32_t staging_rows,
+                            const int32_t* codes, const int32_t* bag_ptr, int32_t n_samples,
+                            int32_t bags_per_sample, int64_t n_lookups, const int32_t* sample_ids,
+                            const int32_t* n_sel_dev, int32_t n_sel_max, const float* dY, float lr,
+                            void* workspace, size_t ws_bytes, hl_stream stream);
+
+/* ----------------------------------------------------------------- errors --
+ * Waits for the device, returns the error word (HL_DEVERR_* bits) in *err_out
+ * (host) and clears it.  Returns HL_ERR_DEVICE if any bit was set. */
+hl_status hl_last_device_error(hl_handle* h, uint32_t* err_out);
+
+/* ---------------------------------------------------------------- tracing --
+ * Per-kernel timing with HIP events.  hl_trace_enable(h, cap) creates cap
+ * event pairs and records one pair around every kernel the handle's calls
+ * launch (until cap records exist); cap = 0 turns tracing off.  hl_trace_read
+ * waits for record i and returns its kernel name (static string) and
+ * duration in ms.  hl_trace_reset forgets the records. */
+hl_status hl_trace_enable(hl_handle* h, int32_t cap);
+int32_t hl_trace_count(const hl_handle* h);
+hl_status hl_trace_read(const hl_handle* h, int32_t i, const char** name, float* ms);
+hl_status hl_trace_reset(hl_handle* h);
+
+/* ---------------------------------------------------- pinned host memory --
+ * Page-locked host memory mapped into the device address space (the host
+ * table the cold gather reads).  *host receives the host pointer, *dev (may be
+ * NULL) the pointer kernels use. */
+hl_status hl_host_alloc(size_t bytes, void** host, void** dev);
+hl_status hl_host_free(void* host);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* HOTLINE_H */

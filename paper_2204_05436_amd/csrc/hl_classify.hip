@@ -1,0 +1,185 @@
+// Popularity classification, mu-batch partition (stable compaction) and the
+// gid -> hot-slot remap.
+#include "hl_internal.h"
+
+// ----------------------------------------------------------------------------- classify
+// A block owns `spb` consecutive samples; their lookups are contiguous.  Threads
+// probe one lookup each (coalesced ids, one bitmap word per probe); a non-hot
+// lookup clears its sample's flag in LDS, the sample found by binary search
+// over the block's sample offsets.
+#define CL_MAX_SPB 1024
+__global__ void __launch_bounds__(256)
+cl_kernel(const uint32_t* __restrict__ gids, const int32_t* __restrict__ bag_ptr, int32_t n_samples,
+          int32_t bps, int32_t spb, const uint64_t* __restrict__ bitmap, uint64_t n_rows,
+          uint8_t* __restrict__ flags, int64_t n_lookups, uint32_t* err) {
+  __shared__ int32_t off[CL_MAX_SPB + 1];
+  __shared__ uint8_t fl[CL_MAX_SPB];
+  const int64_t s0 = (int64_t)blockIdx.x * spb;
+  const int ns = (int)min((int64_t)spb, (int64_t)n_samples - s0);
+  for (int j = threadIdx.x; j <= ns; j += blockDim.x) off[j] = bag_ptr[(s0 + j) * bps];
+  for (int j = threadIdx.x; j < ns; j += blockDim.x) fl[j] = 1;
+  if (blockIdx.x == 0 && threadIdx.x == 0 && bag_ptr[(int64_t)n_samples * bps] != n_lookups)
+    hl_flag(err, HL_DEVERR_SHAPE);
+  __syncthreads();
+  const int32_t lo = off[0], hi = off[ns];
+  for (int32_t i = lo + threadIdx.x; i < hi; i += blockDim.x) {
+    const uint32_t g = gids[i];
+    bool hot = false;
+    if (g < n_rows) hot = hl_is_hot(bitmap, g);
+    else hl_flag(err, HL_DEVERR_OUT_OF_RANGE);
+    if (!hot) {
+      int a = 0, b = ns;
+      while (b - a > 1) {
+        int m = (a + b) >> 1;
+        if (off[m] <= i) a = m; else b = m;
+      }
+      fl[a] = 0;
+    }
+  }
+  __syncthreads();
+  for (int j = threadIdx.x; j < ns; j += blockDim.x) flags[s0 + j] = fl[j];
+}
+
+extern "C" hl_status hl_classify(const hl_handle* h, const uint32_t* gids, const int32_t* bag_ptr,
+                                 int32_t n_samples, int32_t bps, int64_t n_lookups, uint8_t* flags,
+                                 hl_stream stream) {
+  if (!h || n_samples < 0 || bps < 1 || n_lookups < 0) return HL_ERR_INVALID_ARG;
+  if (n_samples == 0) return HL_OK;
+  if (!bag_ptr || !flags || (n_lookups > 0 && !gids)) return HL_ERR_INVALID_ARG;
+  if ((int64_t)n_samples * bps >= (1ll << 31)) return HL_ERR_UNSUPPORTED;
+  // about 512 lookups per block
+  int64_t spb = n_lookups > 0 ? (512ll * n_samples + n_lookups - 1) / n_lookups : CL_MAX_SPB;
+  spb = spb < 1 ? 1 : (spb > CL_MAX_SPB ? CL_MAX_SPB : spb);
+  hipStream_t s = (hipStream_t)stream;
+  HL_KERNEL(h, s, "cl_kernel", cl_kernel, dim3(hl_div_up(n_samples, spb)), dim3(256), 0, s, gids,
+                     bag_ptr, n_samples, bps, (int32_t)spb, h->d_bitmap, h->n_rows, flags, n_lookups,
+                     h->d_err);
+  HL_LAUNCHED();
+  return HL_OK;
+}
+
+// ----------------------------------------------------------------------------- partition
+// Stable compaction of sample ids by flag.  One block of 1024 threads handles a
+// tile of up to 64K samples in chunks of 1024: a wave ballot gives each lane's
+// rank among the wave's popular samples, the 16 wave totals are scanned in
+// LDS, and a running carry links the chunks.  A popular sample goes to
+// pop[p], a non-popular one to nonpop[i - p], p = popular samples before i.
+#define PT_TILE 65536
+__global__ void __launch_bounds__(1024)
+pt_count(const uint8_t* __restrict__ flags, int32_t n, uint32_t* tile_cnt) {
+  __shared__ uint32_t red[1024];
+  const int64_t base = (int64_t)blockIdx.x * PT_TILE;
+  uint32_t c = 0;
+  for (int k = 0; k < PT_TILE / 1024; ++k) {
+    const int64_t i = base + k * 1024 + threadIdx.x;
+    if (i < n) c += flags[i] != 0;
+  }
+  red[threadIdx.x] = c;
+  __syncthreads();
+  for (int o = 512; o > 0; o >>= 1) {
+    if (threadIdx.x < o) red[threadIdx.x] += red[threadIdx.x + o];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) tile_cnt[blockIdx.x] = red[0];
+}
+
+__global__ void __launch_bounds__(1024)
+pt_scan(uint32_t* tile_cnt, int32_t n_tiles) {
+  if (threadIdx.x == 0) {
+    uint32_t acc = 0;
+    for (int32_t t = 0; t < n_tiles; ++t) {
+      uint32_t v = tile_cnt[t];
+      tile_cnt[t] = acc;
+      acc += v;
+    }
+  }
+}
+
+__global__ void __launch_bounds__(1024)
+pt_emit(const uint8_t* __restrict__ flags, int32_t n, const uint32_t* tile_excl, int32_t* __restrict__ pop,
+        int32_t* __restrict__ nonpop, int32_t* counts) {
+  __shared__ uint32_t wtot[16];
+  __shared__ uint32_t carry;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int64_t base = (int64_t)blockIdx.x * PT_TILE;
+  if (threadIdx.x == 0) carry = tile_excl ? tile_excl[blockIdx.x] : 0u;
+  __syncthreads();
+  const uint64_t lt = (1ull << lane) - 1ull;
+  for (int k = 0; k < PT_TILE / 1024; ++k) {
+    const int64_t c0 = base + k * 1024;
+    if (c0 >= n) break;
+    const int64_t i = c0 + threadIdx.x;
+    const bool valid = i < n;
+    const bool p = valid && flags[i] != 0;
+    const uint64_t b = __ballot(p);
+    if (lane == 0) wtot[w] = __popcll(b);
+    __syncthreads();
+    uint32_t before = carry;
+    for (int j = 0; j < w; ++j) before += wtot[j];
+    before += __popcll(b & lt);
+    if (valid) {
+      if (p) pop[before] = (int32_t)i;
+      else nonpop[i - before] = (int32_t)i;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      uint32_t t = 0;
+      for (int j = 0; j < 16; ++j) t += wtot[j];
+      carry += t;
+    }
+    __syncthreads();
+  }
+  if (threadIdx.x == 0 && (blockIdx.x == gridDim.x - 1)) {
+    counts[0] = (int32_t)carry;
+    counts[1] = n - (int32_t)carry;
+  }
+}
+
+size_t hl_partition_ws_bytes(int32_t max_samples) {
+  return HL_WS_HEADER + 4 * ((size_t)(max_samples + PT_TILE - 1) / PT_TILE + 64);
+}
+
+extern "C" hl_status hl_partition(const hl_handle* h, const uint8_t* flags, int32_t n, int32_t* pop,
+                                  int32_t* nonpop, int32_t* counts, void* ws, size_t ws_bytes,
+                                  hl_stream stream) {
+  if (!h || n < 0 || !counts || (n > 0 && (!flags || !pop || !nonpop))) return HL_ERR_INVALID_ARG;
+  hipStream_t s = (hipStream_t)stream;
+  const int32_t tiles = n == 0 ? 1 : (int32_t)hl_div_up(n, PT_TILE);
+  uint32_t* tc = nullptr;
+  if (tiles > 1) {
+    if (!ws || ws_bytes < hl_partition_ws_bytes(n)) return HL_ERR_CAPACITY;
+    tc = (uint32_t*)((char*)ws + HL_WS_HEADER);
+    HL_KERNEL(h, s, "pt_count", pt_count, dim3(tiles), dim3(1024), 0, s, flags, n, tc);
+    HL_KERNEL(h, s, "pt_scan", pt_scan, dim3(1), dim3(1024), 0, s, tc, tiles);
+  }
+  HL_KERNEL(h, s, "pt_emit", pt_emit, dim3(tiles), dim3(1024), 0, s, flags, n, tc, pop, nonpop, counts);
+  HL_LAUNCHED();
+  return HL_OK;
+}
+
+// ----------------------------------------------------------------------------- remap
+__global__ void __launch_bounds__(256)
+rm_kernel(const uint32_t* __restrict__ gids, int64_t n, const uint64_t* __restrict__ bitmap,
+          const uint32_t* __restrict__ rank, uint64_t n_rows, int32_t* __restrict__ codes, uint32_t* err) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    const uint32_t g = gids[i];
+    int32_t c = -1;
+    if (g < n_rows) c = hl_hot_slot(bitmap, rank, g);
+    else hl_flag(err, HL_DEVERR_OUT_OF_RANGE);
+    codes[i] = c;
+  }
+}
+
+extern "C" hl_status hl_remap(const hl_handle* h, const uint32_t* gids, int64_t n, int32_t* codes,
+                              hl_stream stream) {
+  if (!h || n < 0 || (n > 0 && (!gids || !codes))) return HL_ERR_INVALID_ARG;
+  if (n == 0) return HL_OK;
+  uint32_t g = hl_div_up(n, 256);
+  if (g > 65535) g = 65535;
+  hipStream_t s = (hipStream_t)stream;
+  HL_KERNEL(h, s, "rm_kernel", rm_kernel, dim3(g), dim3(256), 0, s, gids, n, h->d_bitmap, h->d_rank,
+                     h->n_rows, codes, h->d_err);
+  HL_LAUNCHED();
+  return HL_OK;
+}

@@ -1,0 +1,643 @@
+// EmbeddingBag sum-pooling forward and the coalesced sparse-SGD backward over
+// the hot cache (HBM) and the staging buffer of gathered cold rows.
+//
+// Lane layout: a row is covered by G lanes holding VEC consecutive elements
+// each (fp32: 16-byte loads for VEC = 4; bf16: 8-byte loads widened to fp32),
+// G = min(dim/VEC, 64); a wave holds NG = 64/G row groups; rows wider than 64
+// vectors are split into column chunks over blockIdx.y.
+//
+// Backward: the lookups of the mini-batch are sorted by compressed row key
+// (hot slot, or n_hot + staging row) with their bag as payload; then tiles of
+// the sorted list are reduced by groups of E consecutive entries: a run of
+// equal keys entirely inside a group is a complete segment and its row is
+// updated at once; pieces of runs that cross group boundaries are combined in
+// LDS in group order, and pieces that cross tile boundaries are combined by a
+// second kernel in tile order.  Every row is read and written once and the
+// summation order depends only on the sorted order, so results are
+// deterministic.
+#include <initializer_list>
+
+#include "hl_internal.h"
+
+#define EB_SENT 0xFFFFFFFFu
+#define RB_E 8
+#define RB_WAVES 8
+#define RB_BLOCK (RB_WAVES * 64)
+
+// ----------------------------------------------------------------------------- row I/O
+template <int VEC, bool BF>
+struct RowIO;
+
+template <>
+struct RowIO<4, false> {
+  typedef float T;
+  static __device__ __forceinline__ void load(const T* p, float* v) {
+    float4 x = *reinterpret_cast<const float4*>(p);
+    v[0] = x.x; v[1] = x.y; v[2] = x.z; v[3] = x.w;
+  }
+  static __device__ __forceinline__ void store(T* p, const float* v) {
+    *reinterpret_cast<float4*>(p) = make_float4(v[0], v[1], v[2], v[3]);
+  }
+};
+template <>
+struct RowIO<2, false> {
+  typedef float T;
+  static __device__ __forceinline__ void load(const T* p, float* v) {
+    float2 x = *reinterpret_cast<const float2*>(p);
+    v[0] = x.x; v[1] = x.y;
+  }
+  static __device__ __forceinline__ void store(T* p, const float* v) {
+    *reinterpret_cast<float2*>(p) = make_float2(v[0], v[1]);
+  }
+};
+template <>
+struct RowIO<1, false> {
+  typedef float T;
+  static __device__ __forceinline__ void load(const T* p, float* v) { v[0] = *p; }
+  static __device__ __forceinline__ void store(T* p, const float* v) { *p = v[0]; }
+};
+
+__device__ __forceinline__ float bf2f(uint32_t b) { return __uint_as_float(b << 16); }
+__device__ __forceinline__ uint32_t f2bf(float f) {  // round to nearest even (finite values)
+  uint32_t u = __float_as_uint(f);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return u >> 16;
+}
+
+template <>
+struct RowIO<4, true> {
+  typedef uint16_t T;
+  static __device__ __forceinline__ void load(const T* p, float* v) {
+    uint2 x = *reinterpret_cast<const uint2*>(p);
+    v[0] = bf2f(x.x & 0xFFFFu); v[1] = bf2f(x.x >> 16); v[2] = bf2f(x.y & 0xFFFFu); v[3] = bf2f(x.y >> 16);
+  }
+  static __device__ __forceinline__ void store(T* p, const float* v) {
+    *reinterpret_cast<uint2*>(p) = make_uint2(f2bf(v[0]) | (f2bf(v[1]) << 16), f2bf(v[2]) | (f2bf(v[3]) << 16));
+  }
+};
+template <>
+struct RowIO<2, true> {
+  typedef uint16_t T;
+  static __device__ __forceinline__ void load(const T* p, float* v) {
+    uint32_t x = *reinterpret_cast<const uint32_t*>(p);
+    v[0] = bf2f(x & 0xFFFFu); v[1] = bf2f(x >> 16);
+  }
+  static __device__ __forceinline__ void store(T* p, const float* v) {
+    *reinterpret_cast<uint32_t*>(p) = f2bf(v[0]) | (f2bf(v[1]) << 16);
+  }
+};
+template <>
+struct RowIO<1, true> {
+  typedef uint16_t T;
+  static __device__ __forceinline__ void load(const T* p, float* v) { v[0] = bf2f(*p); }
+  static __device__ __forceinline__ void store(T* p, const float* v) { *p = (uint16_t)f2bf(v[0]); }
+};
+
+template <int VEC>
+__device__ __forceinline__ void ld_f32(const float* p, float* v) { RowIO<VEC, false>::load(p, v); }
+template <int VEC>
+__device__ __forceinline__ void st_f32(float* p, const float* v) { RowIO<VEC, false>::store(p, v); }
+
+struct eb_geom {
+  int32_t D, vpr, G, NG, cchunks, VEC;
+};
+
+static eb_geom eb_make_geom(int32_t D, int vec) {
+  eb_geom g;
+  g.D = D;
+  g.VEC = vec;
+  g.vpr = D / vec;
+  g.G = g.vpr < 64 ? g.vpr : 64;
+  g.NG = 64 / g.G;
+  g.cchunks = (g.vpr + 63) / 64;
+  return g;
+}
+
+static int eb_pick_vec(int32_t D, size_t esize, std::initializer_list<const void*> ptrs) {
+  int vec = D % 4 == 0 ? 4 : (D % 2 == 0 ? 2 : 1);
+  for (;;) {
+    bool ok = true;
+    for (const void* p : ptrs)
+      if (p && ((uintptr_t)p % (vec * esize) != 0 || (uintptr_t)p % (vec * 4) != 0)) ok = false;
+    if (ok || vec == 1) return vec;
+    vec >>= 1;
+  }
+}
+
+// selected-sample count
+__device__ __forceinline__ int32_t eb_nsel(const int32_t* ids, const int32_t* n_dev, int32_t n_max) {
+  if (ids && n_dev) return min(max(*n_dev, 0), n_max);
+  return n_max;
+}
+
+// ----------------------------------------------------------------------------- forward
+template <int VEC, bool BF>
+__global__ void __launch_bounds__(256)
+eb_fwd(const void* w_hot_, const void* stg_, int32_t stg_rows, uint32_t n_hot, uint32_t k_cap,
+       const int32_t* __restrict__ codes, const int32_t* __restrict__ bag_ptr, int32_t bps,
+       const int32_t* __restrict__ sample_ids, const int32_t* n_sel_dev, int32_t n_sel_max,
+       float* __restrict__ out, eb_geom g, int64_t n_lookups, int64_t n_bags_total, int32_t n_samples,
+       uint32_t* err) {
+  typedef typename RowIO<VEC, BF>::T T;
+  const T* w_hot = (const T*)w_hot_;
+  const T* stg = (const T*)stg_;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int gi = lane / g.G, gl = lane - gi * g.G;
+  if (blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0 && bag_ptr[n_bags_total] != n_lookups)
+    hl_flag(err, HL_DEVERR_SHAPE);
+  if (gi >= g.NG) return;
+  const int32_t colv = blockIdx.y * 64 + gl;
+  const bool cact = colv < g.vpr;
+  const int64_t col = (int64_t)colv * VEC;
+  const int64_t total = (int64_t)eb_nsel(sample_ids, n_sel_dev, n_sel_max) * bps;
+  const int64_t stride = (int64_t)gridDim.x * 4 * g.NG;
+  for (int64_t q = ((int64_t)blockIdx.x * 4 + w) * g.NG + gi; q < total; q += stride) {
+    const int64_t si = q / bps, j = q - si * bps;
+    const int64_t smp = sample_ids ? (int64_t)sample_ids[si] : si;
+    if (smp < 0 || smp >= n_samples) {
+      if (gl == 0) hl_flag(err, HL_DEVERR_OUT_OF_RANGE);
+      continue;
+    }
+    const int64_t bag = smp * bps + j;
+    const int32_t lo = bag_ptr[bag], hi = bag_ptr[bag + 1];
+    float acc[VEC];
+#pragma unroll
+    for (int v = 0; v < VEC; ++v) acc[v] = 0.f;
+    int32_t i = lo;
+    for (; i + 4 <= hi; i += 4) {
+      int32_t c[4];
+      const T* p[4];
+      bool ok[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) c[u] = codes[i + u];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const uint32_t cu = (uint32_t)c[u];
+        ok[u] = true;
+        if (cu < n_hot) p[u] = w_hot + (int64_t)cu * g.D;
+        else if (cu >= k_cap && cu - k_cap < (uint32_t)stg_rows) p[u] = stg + (int64_t)(cu - k_cap) * g.D;
+        else { ok[u] = false; p[u] = w_hot; }
+      }
+      float v[4][VEC];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        if (ok[u] && cact) RowIO<VEC, BF>::load(p[u] + col, v[u]);
+        else {
+#pragma unroll
+          for (int e = 0; e < VEC; ++e) v[u][e] = 0.f;
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) acc[e] += v[u][e];
+        if (!ok[u] && gl == 0) hl_flag(err, HL_DEVERR_BAD_CODE);
+      }
+    }
+    for (; i < hi; ++i) {
+      const uint32_t cu = (uint32_t)codes[i];
+      const T* p;
+      bool ok = true;
+      if (cu < n_hot) p = w_hot + (int64_t)cu * g.D;
+      else if (cu >= k_cap && cu - k_cap < (uint32_t)stg_rows) p = stg + (int64_t)(cu - k_cap) * g.D;
+      else { ok = false; p = w_hot; }
+      if (ok && cact) {
+        float v[VEC];
+        RowIO<VEC, BF>::load(p + col, v);
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) acc[e] += v[e];
+      }
+      if (!ok && gl == 0) hl_flag(err, HL_DEVERR_BAD_CODE);
+    }
+    if (cact) st_f32<VEC>(out + bag * g.D + col, acc);
+  }
+}
+
+// ----------------------------------------------------------------------------- backward
+struct bw_ws {
+  hl_sort_ws sort;
+  uint8_t* mask;     // [max_bags]
+  float* tfirst;     // [tiles][D]
+  float* tlast;      // [tiles][D]
+  uint32_t* tflag;   // [tiles]
+  uint32_t* tkey;    // [tiles]
+  uint32_t tiles;
+};
+
+static uint32_t bw_tile_entries(int32_t D, int vec) {
+  eb_geom g = eb_make_geom(D, vec);
+  return (uint32_t)(RB_WAVES * g.NG * RB_E);
+}
+
+static void bw_carve(hl_carver& c, bw_ws& ws, uint32_t n_max, int64_t max_bags, int32_t D) {
+  hl_sort_ws_carve(c, ws.sort, n_max);
+  ws.mask = c.take<uint8_t>((size_t)max_bags + 1);
+  // the smallest tile (largest count) over the vector widths the call may pick
+  uint32_t te = bw_tile_entries(D, 1);
+  uint32_t te2 = bw_tile_entries(D, D % 2 == 0 ? 2 : 1), te4 = bw_tile_entries(D, D % 4 == 0 ? 4 : 1);
+  te = te < te2 ? te : te2;
+  te = te < te4 ? te : te4;
+  ws.tiles = n_max ? hl_div_up(n_max, te) : 1;
+  ws.tfirst = c.take<float>((size_t)ws.tiles * D);
+  ws.tlast = c.take<float>((size_t)ws.tiles * D);
+  ws.tflag = c.take<uint32_t>(ws.tiles);
+  ws.tkey = c.take<uint32_t>(ws.tiles);
+}
+
+size_t hl_bwd_ws_bytes(const hl_handle* h, int64_t max_lookups, int64_t max_bags) {
+  hl_carver c = hl_carver::after_header(nullptr, 0);
+  bw_ws ws;
+  bw_carve(c, ws, (uint32_t)max_lookups, max_bags, h->dim);
+  return c.off;
+}
+
+__global__ void bw_mask(uint8_t* mask, int32_t n_samples, const int32_t* __restrict__ ids, const int32_t* n_dev,
+                        int32_t n_max, int phase) {
+  if (phase == 0) {
+    for (int32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < n_samples; i += gridDim.x * blockDim.x) mask[i] = 0;
+  } else {
+    const int32_t n = eb_nsel(ids, n_dev, n_max);
+    for (int32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) {
+      const int32_t s = ids[i];
+      if (s >= 0 && s < n_samples) mask[s] = 1;
+    }
+  }
+}
+
+// (compressed key, bag) for every lookup of the mini-batch; lookups of
+// unselected samples and invalid codes get the sentinel key (sorted last,
+// ignored).
+#define BP_BAGS 256
+__global__ void __launch_bounds__(256)
+bw_prep(const int32_t* __restrict__ codes, const int32_t* __restrict__ bag_ptr, int64_t n_bags, int32_t bps,
+        const uint8_t* __restrict__ mask, uint32_t n_hot, uint32_t k_cap, int32_t stg_rows,
+        uint32_t* __restrict__ keys, uint32_t* __restrict__ vals, int64_t n_lookups, uint32_t* err) {
+  __shared__ int32_t off[BP_BAGS + 1];
+  const int64_t b0 = (int64_t)blockIdx.x * BP_BAGS;
+  const int nb = (int)min((int64_t)BP_BAGS, n_bags - b0);
+  for (int j = threadIdx.x; j <= nb; j += blockDim.x) off[j] = bag_ptr[b0 + j];
+  if (blockIdx.x == 0 && threadIdx.x == 0 && bag_ptr[n_bags] != n_lookups) hl_flag(err, HL_DEVERR_SHAPE);
+  __syncthreads();
+  // positions the bags do not cover (only if bag_ptr disagrees with n_lookups) get the sentinel
+  const int64_t covered = min((int64_t)max(bag_ptr[n_bags], 0), n_lookups);
+  for (int64_t i = covered + (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n_lookups;
+       i += (int64_t)gridDim.x * blockDim.x)
+    keys[i] = EB_SENT;
+  const int32_t lo = off[0], hi = min((int64_t)off[nb], n_lookups);
+  for (int32_t i = lo + threadIdx.x; i < hi; i += blockDim.x) {
+    int a = 0, b = nb;
+    while (b - a > 1) {
+      int m = (a + b) >> 1;
+      if (off[m] <= i) a = m; else b = m;
+    }
+    const int64_t bag = b0 + a;
+    uint32_t key = EB_SENT;
+    if (!mask || mask[bag / bps]) {
+      const uint32_t c = (uint32_t)codes[i];
+      if (c < n_hot) key = c;
+      else if (c >= k_cap && c - k_cap < (uint32_t)stg_rows) key = n_hot + (c - k_cap);
+      else hl_flag(err, HL_DEVERR_BAD_CODE);
+    }
+    keys[i] = key;
+    vals[i] = (uint32_t)bag;
+  }
+}
+
+template <int VEC, bool BF>
+__device__ __forceinline__ typename RowIO<VEC, BF>::T* bw_row(void* w_hot, void* stg, uint32_t n_hot, int32_t D,
+                                                             uint32_t key) {
+  typedef typename RowIO<VEC, BF>::T T;
+  return key < n_hot ? (T*)w_hot + (int64_t)key * D : (T*)stg + (int64_t)(key - n_hot) * D;
+}
+
+#define GF_F 1u
+#define GF_W 2u
+#define GF_L 4u
+
+template <int VEC, bool BF>
+__global__ void __launch_bounds__(RB_BLOCK)
+bw_reduce1(const uint32_t* __restrict__ keys, const uint32_t* __restrict__ vals, uint32_t n,
+           const float* __restrict__ dY, eb_geom g, void* w_hot, void* stg, uint32_t n_hot, float lr,
+           float* __restrict__ tfirst, float* __restrict__ tlast, uint32_t* __restrict__ tflag,
+           uint32_t* __restrict__ tkey) {
+  typedef typename RowIO<VEC, BF>::T T;
+  __shared__ float pf[RB_WAVES * 64 * VEC], pl[RB_WAVES * 64 * VEC];
+  __shared__ uint32_t gflag[RB_WAVES * 64], gkey[RB_WAVES * 64];
+  __shared__ uint32_t s_tflag;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int gi = lane / g.G, gl = lane - gi * g.G;
+  const bool gact = gi < g.NG;
+  const int grp = w * g.NG + gi;           // group index inside the block
+  const int ngb = RB_WAVES * g.NG;         // groups per block
+  const uint32_t te = (uint32_t)ngb * RB_E;
+  const uint32_t tile = blockIdx.x;
+  const uint64_t tb = (uint64_t)tile * te;
+  const int32_t colv = blockIdx.y * 64 + gl;
+  const bool cact = gact && colv < g.vpr;
+  const int64_t col = (int64_t)colv * VEC;
+  const int lds_off = (grp * g.G + gl) * VEC;
+  if (threadIdx.x == 0) s_tflag = 0;
+  if (gact) {
+    const uint64_t e0 = tb + (uint64_t)grp * RB_E;
+    uint32_t kk[RB_E], bb[RB_E];
+#pragma unroll
+    for (int j = 0; j < RB_E; ++j) {
+      const uint64_t idx = e0 + j;
+      kk[j] = idx < n ? keys[idx] : EB_SENT;
+      bb[j] = idx < n ? vals[idx] : 0u;
+    }
+    const uint32_t prevk = (e0 > 0 && e0 - 1 < n) ? keys[e0 - 1] : EB_SENT;
+    const uint32_t nextk = (e0 + RB_E < n) ? keys[e0 + RB_E] : EB_SENT;
+    const bool cprev = kk[0] != EB_SENT && prevk == kk[0];
+    const bool cnext = kk[RB_E - 1] != EB_SENT && nextk == kk[RB_E - 1];
+    // gradient rows
+    float dv[RB_E][VEC];
+#pragma unroll
+    for (int j = 0; j < RB_E; ++j) {
+      if (kk[j] != EB_SENT && cact) ld_f32<VEC>(dY + (int64_t)bb[j] * g.D + col, dv[j]);
+      else {
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) dv[j][e] = 0.f;
+      }
+    }
+    // rows of complete runs (issued before the sums are formed)
+    float wr[RB_E][VEC];
+    bool cpl[RB_E];
+    bool from0 = true;
+#pragma unroll
+    for (int j = 0; j < RB_E; ++j) {
+      const bool valid = kk[j] != EB_SENT;
+      if (j > 0 && valid && kk[j - 1] != kk[j]) from0 = false;
+      const bool end = valid && (j == RB_E - 1 || kk[j + 1] != kk[j]);
+      cpl[j] = end && !(from0 && cprev) && !(j == RB_E - 1 && cnext);
+      if (cpl[j] && cact) RowIO<VEC, BF>::load(bw_row<VEC, BF>(w_hot, stg, n_hot, g.D, kk[j]) + col, wr[j]);
+    }
+    float acc[VEC];
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) acc[e] = 0.f;
+    uint32_t gf = 0;
+    from0 = true;
+#pragma unroll
+    for (int j = 0; j < RB_E; ++j) {
+      const bool valid = kk[j] != EB_SENT;
+      if (j > 0 && valid && kk[j - 1] != kk[j]) from0 = false;
+      if (valid) {
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) acc[e] += dv[j][e];
+      }
+      const bool end = valid && (j == RB_E - 1 || kk[j + 1] != kk[j]);
+      if (end) {
+        if (cpl[j]) {
+          if (cact) {
+            float nw[VEC];
+#pragma unroll
+            for (int e = 0; e < VEC; ++e) nw[e] = wr[j][e] - lr * acc[e];
+            RowIO<VEC, BF>::store(bw_row<VEC, BF>(w_hot, stg, n_hot, g.D, kk[j]) + col, nw);
+          }
+        } else {
+          const bool first = from0 && cprev, lastp = (j == RB_E - 1) && cnext;
+          if (first) {
+            gf |= GF_F | (lastp ? GF_W | GF_L : 0u);
+#pragma unroll
+            for (int e = 0; e < VEC; ++e) pf[lds_off + e] = acc[e];
+          } else if (lastp) {
+            gf |= GF_L;
+#pragma unroll
+            for (int e = 0; e < VEC; ++e) pl[lds_off + e] = acc[e];
+          }
+        }
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) acc[e] = 0.f;
+      }
+    }
+    if (gl == 0) {
+      gflag[grp] = gf;
+      gkey[grp] = kk[RB_E - 1];
+    }
+  }
+  __syncthreads();
+  if (gact) {
+    const uint32_t gf = gflag[grp];
+    // a segment that starts in this group and continues into the next ones
+    if ((gf & GF_L) && !(gf & GF_W)) {
+      float acc[VEC];
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) acc[e] = pl[lds_off + e];
+      bool done = false;
+      for (int g2 = grp + 1; g2 < ngb; ++g2) {
+        const int o2 = (g2 * g.G + gl) * VEC;
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) acc[e] += pf[o2 + e];
+        if (!(gflag[g2] & GF_W)) { done = true; break; }
+      }
+      const uint32_t key = gkey[grp];
+      if (done) {
+        if (cact) {
+          T* p = bw_row<VEC, BF>(w_hot, stg, n_hot, g.D, key) + col;
+          float wv[VEC];
+          RowIO<VEC, BF>::load(p, wv);
+#pragma unroll
+          for (int e = 0; e < VEC; ++e) wv[e] -= lr * acc[e];
+          RowIO<VEC, BF>::store(p, wv);
+        }
+      } else {
+        if (cact) st_f32<VEC>(tlast + (int64_t)tile * g.D + col, acc);
+        if (gl == 0) {
+          atomicOr(&s_tflag, GF_L);
+          if (blockIdx.y == 0) tkey[tile] = key;
+        }
+      }
+    }
+    // the piece of a segment that began in an earlier tile
+    if (grp == 0 && (gf & GF_F)) {
+      float acc[VEC];
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) acc[e] = pf[lds_off + e];
+      bool whole = (gf & GF_W) != 0;
+      if (whole) {
+        for (int g2 = 1; g2 < ngb; ++g2) {
+          const int o2 = (g2 * g.G + gl) * VEC;
+#pragma unroll
+          for (int e = 0; e < VEC; ++e) acc[e] += pf[o2 + e];
+          if (!(gflag[g2] & GF_W)) { whole = false; break; }
+        }
+      }
+      if (cact) st_f32<VEC>(tfirst + (int64_t)tile * g.D + col, acc);
+      if (gl == 0) atomicOr(&s_tflag, GF_F | (whole ? GF_W : 0u));
+    }
+  }
+  __syncthreads();
+  if (threadIdx.x == 0 && blockIdx.y == 0) tflag[tile] = s_tflag;
+}
+
+// Segments spanning tiles: the tile where a segment starts (flag L) sums its
+// own piece and the next tiles' first pieces up to the first tile that is not
+// wholly inside the segment.  Piece p is summed by group p % groups in
+// ascending p, then groups are added in order.
+template <int VEC, bool BF>
+__global__ void __launch_bounds__(RB_BLOCK)
+bw_reduce2(uint32_t n_tiles, eb_geom g, void* w_hot, void* stg, uint32_t n_hot, float lr,
+           const float* __restrict__ tfirst, const float* __restrict__ tlast, const uint32_t* __restrict__ tflag,
+           const uint32_t* __restrict__ tkey) {
+  typedef typename RowIO<VEC, BF>::T T;
+  const uint32_t t = blockIdx.x;
+  if (!(tflag[t] & GF_L)) return;
+  __shared__ uint32_t s_end;
+  __shared__ float part[RB_WAVES * 64 * VEC];
+  if (threadIdx.x == 0) s_end = n_tiles;
+  __syncthreads();
+  for (uint32_t t2 = t + 1 + threadIdx.x; t2 < n_tiles; t2 += RB_BLOCK) {
+    if (!(tflag[t2] & GF_W)) {
+      atomicMin(&s_end, t2);
+      break;
+    }
+    if (t2 >= s_end) break;
+  }
+  __syncthreads();
+  const uint32_t tend = s_end;  // last tile holding a piece (not whole)
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int gi = lane / g.G, gl = lane - gi * g.G;
+  const bool gact = gi < g.NG;
+  const int grp = w * g.NG + gi, ngb = RB_WAVES * g.NG;
+  const int32_t colv = blockIdx.y * 64 + gl;
+  const bool cact = gact && colv < g.vpr;
+  const int64_t col = (int64_t)colv * VEC;
+  const uint32_t npieces = (tend < n_tiles ? tend : n_tiles - 1) - t + 1;
+  if (gact) {
+    float acc[VEC];
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) acc[e] = 0.f;
+    if (cact) {
+      for (uint32_t p = grp; p < npieces; p += ngb) {
+        float v[VEC];
+        const float* src = p == 0 ? tlast + (int64_t)t * g.D : tfirst + (int64_t)(t + p) * g.D;
+        ld_f32<VEC>(src + col, v);
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) acc[e] += v[e];
+      }
+    }
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) part[(grp * g.G + gl) * VEC + e] = acc[e];
+  }
+  __syncthreads();
+  if (gact && grp == 0 && cact) {
+    float acc[VEC];
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) acc[e] = 0.f;
+    for (int q = 0; q < ngb; ++q)
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) acc[e] += part[(q * g.G + gl) * VEC + e];
+    T* p = bw_row<VEC, BF>(w_hot, stg, n_hot, g.D, tkey[t]) + col;
+    float wv[VEC];
+    RowIO<VEC, BF>::load(p, wv);
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) wv[e] -= lr * acc[e];
+    RowIO<VEC, BF>::store(p, wv);
+  }
+}
+
+// ----------------------------------------------------------------------------- host side
+static hl_status check_common(const hl_handle* h, const int32_t* codes, const int32_t* bag_ptr, int32_t n_samples,
+                              int32_t bps, int64_t n_lookups, const int32_t* sample_ids, int32_t n_sel_max,
+                              int32_t stg_rows) {
+  if (!h || n_samples < 0 || bps < 1 || n_lookups < 0 || n_sel_max < 0 || stg_rows < 0) return HL_ERR_INVALID_ARG;
+  if (!bag_ptr || (n_lookups > 0 && !codes)) return HL_ERR_INVALID_ARG;
+  if (!sample_ids && n_sel_max > n_samples) return HL_ERR_INVALID_ARG;
+  if ((int64_t)n_samples * bps >= (1ll << 31) || n_lookups >= (1ll << 30)) return HL_ERR_UNSUPPORTED;
+  if ((uint64_t)h->k_cap + (uint64_t)stg_rows >= (1ull << 31)) return HL_ERR_UNSUPPORTED;
+  return HL_OK;
+}
+
+template <int VEC, bool BF>
+static void launch_fwd(const hl_handle* h, dim3 grid, hipStream_t s, const void* w_hot, const void* stg,
+                       int32_t stg_rows, const int32_t* codes, const int32_t* bag_ptr, int32_t bps,
+                       const int32_t* ids, const int32_t* n_dev, int32_t n_max, float* out, eb_geom g,
+                       int64_t n_lookups, int64_t n_bags) {
+  HL_KERNEL(h, s, "eb_fwd", (eb_fwd<VEC, BF>), grid, dim3(256), 0, s, w_hot, stg, stg_rows, h->n_hot, h->k_cap, codes,
+                     bag_ptr, bps, ids, n_dev, n_max, out, g, n_lookups, n_bags, (int32_t)(n_bags / bps), h->d_err);
+}
+
+extern "C" hl_status hl_embbag_fwd(const hl_handle* h, const void* w_hot, const void* staging, int32_t stg_rows,
+                                   const int32_t* codes, const int32_t* bag_ptr, int32_t n_samples, int32_t bps,
+                                   int64_t n_lookups, const int32_t* sample_ids, const int32_t* n_sel_dev,
+                                   int32_t n_sel_max, float* out, hl_stream stream) {
+  hl_status st = check_common(h, codes, bag_ptr, n_samples, bps, n_lookups, sample_ids, n_sel_max, stg_rows);
+  if (st != HL_OK) return st;
+  if (n_sel_max == 0) return HL_OK;
+  if (!out || (h->n_hot && !w_hot) || (stg_rows && !staging)) return HL_ERR_INVALID_ARG;
+  const size_t es = h->dtype == HL_F32 ? 4 : 2;
+  const int vec = eb_pick_vec(h->dim, es, {w_hot, staging, out});
+  eb_geom g = eb_make_geom(h->dim, vec);
+  const int64_t total = (int64_t)n_sel_max * bps;
+  int64_t blocks = (total + 4 * g.NG - 1) / (4 * g.NG);
+  if (blocks > (1 << 20)) blocks = 1 << 20;
+  dim3 grid((uint32_t)blocks, g.cchunks);
+  hipStream_t s = (hipStream_t)stream;
+  const int64_t nb = (int64_t)n_samples * bps;
+  const bool bf = h->dtype == HL_BF16;
+#define FWD(V, B) launch_fwd<V, B>(h, grid, s, w_hot, staging, stg_rows, codes, bag_ptr, bps, sample_ids, n_sel_dev, \
+                                   n_sel_max, out, g, n_lookups, nb)
+  if (vec == 4) { if (bf) FWD(4, true); else FWD(4, false); }
+  else if (vec == 2) { if (bf) FWD(2, true); else FWD(2, false); }
+  else { if (bf) FWD(1, true); else FWD(1, false); }
+#undef FWD
+  HL_LAUNCHED();
+  return HL_OK;
+}
+
+template <int VEC, bool BF>
+static void launch_bwd(const hl_handle* h, uint32_t tiles, dim3 g2, hipStream_t s, const uint32_t* sk, const uint32_t* sv, uint32_t n,
+                       const float* dY, eb_geom g, void* w_hot, void* stg, uint32_t n_hot, float lr, bw_ws& ws) {
+  HL_KERNEL(h, s, "bw_reduce1", (bw_reduce1<VEC, BF>), dim3(tiles, g.cchunks), dim3(RB_BLOCK), 0, s, sk, sv, n, dY, g, w_hot, stg,
+                     n_hot, lr, ws.tfirst, ws.tlast, ws.tflag, ws.tkey);
+  HL_KERNEL(h, s, "bw_reduce2", (bw_reduce2<VEC, BF>), dim3(tiles, g.cchunks), dim3(RB_BLOCK), 0, s, tiles, g, w_hot, stg, n_hot,
+                     lr, ws.tfirst, ws.tlast, ws.tflag, ws.tkey);
+  (void)g2;
+}
+
+extern "C" hl_status hl_embbag_bwd_sgd(hl_handle* h, void* w_hot, void* staging, int32_t stg_rows,
+                                       const int32_t* codes, const int32_t* bag_ptr, int32_t n_samples, int32_t bps,
+                                       int64_t n_lookups, const int32_t* sample_ids, const int32_t* n_sel_dev,
+                                       int32_t n_sel_max, const float* dY, float lr, void* workspace, size_t ws_bytes,
+                                       hl_stream stream) {
+  hl_status st = check_common(h, codes, bag_ptr, n_samples, bps, n_lookups, sample_ids, n_sel_max, stg_rows);
+  if (st != HL_OK) return st;
+  if (n_samples == 0 || n_lookups == 0 || n_sel_max == 0) return HL_OK;
+  if (!dY || !workspace || (h->n_hot && !w_hot) || (stg_rows && !staging)) return HL_ERR_INVALID_ARG;
+  const int64_t n_bags = (int64_t)n_samples * bps;
+  if (ws_bytes < hl_bwd_ws_bytes(h, n_lookups, n_bags)) return HL_ERR_CAPACITY;
+  hipStream_t s = (hipStream_t)stream;
+  hl_carver c = hl_carver::after_header(workspace, ws_bytes);
+  bw_ws ws;
+  bw_carve(c, ws, (uint32_t)n_lookups, n_bags, h->dim);
+  const uint8_t* mask = nullptr;
+  if (sample_ids) {
+    uint32_t gb = hl_div_up(n_samples, 256);
+    if (gb > 4096) gb = 4096;
+    HL_KERNEL(h, s, "bw_mask", bw_mask, dim3(gb), dim3(256), 0, s, ws.mask, n_samples, sample_ids, n_sel_dev, n_sel_max, 0);
+    HL_KERNEL(h, s, "bw_mask", bw_mask, dim3(gb), dim3(256), 0, s, ws.mask, n_samples, sample_ids, n_sel_dev, n_sel_max, 1);
+    mask = ws.mask;
+  }
+  HL_KERNEL(h, s, "bw_prep", bw_prep, dim3(hl_div_up(n_bags, BP_BAGS)), dim3(256), 0, s, codes, bag_ptr, n_bags, bps, mask,
+                     h->n_hot, h->k_cap, stg_rows, ws.sort.k0, ws.sort.v0, n_lookups, h->d_err);
+  HL_LAUNCHED();
+  uint32_t *sk, *sv;
+  const uint32_t n = (uint32_t)n_lookups;
+  st = hl_sort_pairs(h, ws.sort, nullptr, n, hl_bit_width((uint64_t)h->n_hot + (uint64_t)stg_rows), s, &sk, &sv);
+  if (st != HL_OK) return st;
+  const size_t es = h->dtype == HL_F32 ? 4 : 2;
+  const int vec = eb_pick_vec(h->dim, es, {w_hot, staging, dY});
+  eb_geom g = eb_make_geom(h->dim, vec);
+  const uint32_t te = (uint32_t)(RB_WAVES * g.NG * RB_E);
+  const uint32_t tiles = hl_div_up(n, te);
+  if (tiles > ws.tiles) return HL_ERR_CAPACITY;
+  const bool bf = h->dtype == HL_BF16;
+  dim3 g2(tiles, g.cchunks);
+#define BWD(V, B) launch_bwd<V, B>(h, tiles, g2, s, sk, sv, n, dY, g, w_hot, staging, h->n_hot, lr, ws)
+  if (vec == 4) { if (bf) BWD(4, true); else BWD(4, false); }
+  else if (vec == 2) { if (bf) BWD(2, true); else BWD(2, false); }
+  else { if (bf) BWD(1, true); else BWD(1, false); }
+#undef BWD
+  HL_LAUNCHED();
+  return HL_OK;
+}

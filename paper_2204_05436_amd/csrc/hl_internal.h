@@ -1,0 +1,201 @@
+// Internal declarations shared by the HIP sources of libhotline (not installed).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/hotline.h"
+
+#define HL_WAVE 64
+
+// ----------------------------------------------------------------------------- tracing
+struct hl_trace_rec {
+  const char* name;
+  hipEvent_t a, b;
+};
+struct hl_trace {
+  int32_t cap = 0, n = 0;
+  hl_trace_rec* rec = nullptr;
+};
+// Index of the record opened for kernel `name` on stream s, or -1.
+int hl_trace_begin(const struct hl_handle* h, hipStream_t s, const char* name);
+void hl_trace_end(const struct hl_handle* h, hipStream_t s, int idx);
+#define HL_KERNEL(h, s, name, ...)                  \
+  do {                                              \
+    int _ti = hl_trace_begin((h), (s), (name));     \
+    hipLaunchKernelGGL(__VA_ARGS__);                \
+    hl_trace_end((h), (s), _ti);                    \
+  } while (0)
+
+// ----------------------------------------------------------------------------- handle
+struct hl_handle {
+  int device;
+  int32_t n_tables;
+  uint64_t n_rows;
+  int32_t dim;
+  hl_dtype dtype;
+  uint32_t k_cap;
+  uint32_t row_bytes;
+  uint32_t n_hot;
+  uint32_t epoch;        // tags cross-block status words of one call (see hl_sort.hip)
+  uint64_t n_tiles4k;    // ceil(n_rows / 4096): the bitmap and rank directory cover n_tiles4k*4096 ids
+  uint32_t* d_base;      // [n_tables] first gid of each table
+  uint32_t* d_rows;      // [n_tables] rows of each table
+  uint32_t* d_counts;    // [n_rows] access counts
+  uint64_t* d_bitmap;    // [n_tiles4k*64] hot-set membership, bit g of word g/64
+  uint32_t* d_rank;      // [n_tiles4k*16 + 1] hot ids below 256*j
+  uint32_t* d_err;       // device error word
+  uint32_t* d_tk;        // top-K scratch (state, histograms, tile counts)
+  size_t tk_bytes;
+  hl_trace* trace;       // per-kernel event records (owned)
+};
+
+// ----------------------------------------------------------------------------- errors
+#define HL_HIP(call)                                   \
+  do {                                                 \
+    hipError_t _e = (call);                            \
+    if (_e != hipSuccess) return HL_ERR_HIP;           \
+  } while (0)
+
+#define HL_LAUNCHED()                                  \
+  do {                                                 \
+    if (hipGetLastError() != hipSuccess) return HL_ERR_HIP; \
+  } while (0)
+
+__device__ __forceinline__ void hl_flag(uint32_t* err, uint32_t bit) { atomicOr(err, bit); }
+
+// ----------------------------------------------------------------------------- hot set probes
+// Membership: bit (g & 63) of word g >> 6.  Rank: rank[g >> 8] counts hot ids
+// below the 256-id block; the block's 4 words before g's word and the bits of
+// g's word below g add the rest.
+__device__ __forceinline__ bool hl_is_hot(const uint64_t* __restrict__ bm, uint32_t g) {
+  return (bm[g >> 6] >> (g & 63)) & 1ull;
+}
+
+__device__ __forceinline__ int32_t hl_hot_slot(const uint64_t* __restrict__ bm,
+                                               const uint32_t* __restrict__ rank, uint32_t g) {
+  const uint32_t blk = g >> 8;
+  const ulonglong2* p = reinterpret_cast<const ulonglong2*>(bm + (size_t)blk * 4);
+  ulonglong2 a = p[0], b = p[1];
+  uint64_t w[4] = {a.x, a.y, b.x, b.y};
+  const uint32_t wi = (g >> 6) & 3, bit = g & 63;
+  uint64_t word = w[wi];
+  if (!((word >> bit) & 1ull)) return -1;
+  uint32_t r = rank[blk];
+#pragma unroll
+  for (uint32_t k = 0; k < 3; ++k)
+    if (k < wi) r += __popcll(w[k]);
+  r += __popcll(word & ((1ull << bit) - 1ull));
+  return (int32_t)r;
+}
+
+// ----------------------------------------------------------------------------- workspace
+// Every workspace starts with a fixed header of self-resetting counters (their
+// place must not depend on the sizes of a call); buffers are carved after it
+// with 256-byte alignment.
+#define HL_WS_HEADER 4096
+#define HL_HDR_SORT 0    // 8 words: histogram done counter, per-pass tile counters
+#define HL_HDR_COLD 16   // 16 words: cold-gather counters
+// First and only place a new epoch is drawn: never 0 (zeroed status words) and
+// never all-ones.
+static inline uint32_t hl_next_epoch(hl_handle* h) {
+  do { ++h->epoch; } while (h->epoch == 0 || h->epoch == 0xFFFFFFFFu);
+  return h->epoch;
+}
+// Workspace carving with 256-byte alignment.
+struct hl_carver {
+  char* base;
+  size_t off, cap;
+  static hl_carver after_header(void* ws, size_t bytes) { return hl_carver{(char*)ws, HL_WS_HEADER, bytes}; }
+  uint32_t* header() const { return reinterpret_cast<uint32_t*>(base); }
+  template <class T>
+  T* take(size_t count) {
+    off = (off + 255) & ~(size_t)255;
+    T* p = reinterpret_cast<T*>(base ? base + off : nullptr);
+    off += count * sizeof(T);
+    return p;
+  }
+};
+
+// ----------------------------------------------------------------------------- sort
+// Stable LSD radix sort of (key, value) uint32 pairs, 8-bit digits, one
+// histogram kernel plus one kernel per digit with decoupled look-back for the
+// cross-tile digit offsets.  See hl_sort.hip.
+struct hl_sort_ws {
+  uint32_t *k0, *v0, *k1, *v1;  // ping-pong buffers, n_max each; input in k0/v0
+  uint32_t* part;               // [HL_SORT_HIST_BLOCKS][4*256]
+  uint32_t* gexcl;              // [4*256]
+  uint32_t* ctr;                // [8] self-resetting counters (in the workspace header)
+  uint64_t* status;             // [4][tiles_max][256]
+  uint32_t tiles_max;
+  uint32_t n_max;
+};
+
+#define HL_SORT_BLOCK 256
+#define HL_SORT_ITEMS 8
+#define HL_SORT_TILE (HL_SORT_BLOCK * HL_SORT_ITEMS)
+#define HL_SORT_HIST_BLOCKS 64
+
+void hl_sort_ws_carve(hl_carver& c, hl_sort_ws& ws, uint32_t n_max);
+// Sorts ws.k0/ws.v0 (first *n_dev items if n_dev != NULL, else n_host) by the
+// low `bits` bits of the key; returns in *out_k/*out_v the buffers holding the
+// result.  Keys must be < 2^bits - 1 except the all-ones sentinel, which sorts
+// last.
+hl_status hl_sort_pairs(hl_handle* h, hl_sort_ws& ws, const uint32_t* n_dev, uint32_t n_host,
+                        int bits, hipStream_t s, uint32_t** out_k, uint32_t** out_v);
+
+// Decoupled look-back helpers (epoch-tagged 64-bit status words).
+#define HL_ST_AGG 1ull
+#define HL_ST_PRE 2ull
+#define HL_SPIN_LIMIT (1u << 26)
+
+__device__ __forceinline__ uint64_t hl_st_pack(uint32_t epoch, uint64_t flag, uint32_t v) {
+  return ((uint64_t)epoch << 32) | (flag << 30) | (uint64_t)(v & 0x3FFFFFFFu);
+}
+__device__ __forceinline__ void hl_st_store(uint64_t* p, uint64_t w) {
+  __hip_atomic_store(p, w, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint64_t hl_st_load(const uint64_t* p) {
+  return __hip_atomic_load(const_cast<uint64_t*>(p), __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT);
+}
+// Exclusive prefix of tile `tile`'s value over tiles [0, tile) for one lane of
+// status words laid out with stride `stride` between tiles.
+__device__ __forceinline__ uint32_t hl_lookback(const uint64_t* st, uint32_t tile, size_t stride,
+                                                uint32_t epoch, uint32_t* err) {
+  uint32_t excl = 0;
+  int64_t j = (int64_t)tile - 1;
+  uint32_t spins = 0;
+  while (j >= 0) {
+    uint64_t w = hl_st_load(st + (size_t)j * stride);
+    uint32_t e = (uint32_t)(w >> 32);
+    uint64_t f = (w >> 30) & 3ull;
+    if (e != epoch || f == 0) {
+      if (++spins > HL_SPIN_LIMIT) {
+        hl_flag(err, HL_DEVERR_STALL);
+        break;
+      }
+      __builtin_amdgcn_s_sleep(1);
+      continue;
+    }
+    excl += (uint32_t)(w & 0x3FFFFFFFu);
+    if (f == HL_ST_PRE) break;
+    --j;
+  }
+  return excl;
+}
+
+// ----------------------------------------------------------------------------- misc
+static inline uint32_t hl_div_up(uint64_t a, uint64_t b) { return (uint32_t)((a + b - 1) / b); }
+static inline int hl_bit_width(uint64_t x) {
+  int b = 0;
+  while (x) { ++b; x >>= 1; }
+  return b;
+}
+
+// Row copy (bitwise) of n rows: dst[r] = src[ids[r]], rows of row_bytes; n is
+// *n_dev (clamped to n_host) when n_dev is given.  Ids >= n_src_rows are
+// skipped and flag HL_DEVERR_OUT_OF_RANGE.
+hl_status hl_launch_gather(const hl_handle* h, const uint32_t* ids, const int32_t* n_dev, uint32_t n_host,
+                           const void* src, uint64_t n_src_rows, void* dst, uint32_t row_bytes,
+                           uint32_t* err, hipStream_t s);
+hl_status hl_fill32(uint32_t* p, uint64_t n, uint32_t v, hipStream_t s);

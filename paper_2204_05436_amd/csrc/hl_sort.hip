@@ -1,0 +1,201 @@
+// Stable LSD radix sort of (key, value) uint32 pairs.
+//
+// One histogram kernel counts all digit positions in a single read of the keys
+// (the last block to finish merges the per-block counts and writes each
+// position's exclusive digit offsets).  Then one kernel per 8-bit digit: a
+// block takes the next tile (dynamic tile ids, so every lower tile is already
+// running), ranks its items by digit with wave ballots, publishes its digit
+// counts, and obtains the counts of all earlier tiles by decoupled look-back
+// over epoch-tagged status words (no clearing between calls).  Items are
+// reordered in LDS so the global writes of each digit run are contiguous.
+// Item order inside a tile is wave-major, then item, then lane, which is index
+// order, so the sort is stable.
+#include "hl_internal.h"
+
+void hl_sort_ws_carve(hl_carver& c, hl_sort_ws& ws, uint32_t n_max) {
+  ws.n_max = n_max;
+  ws.tiles_max = n_max ? hl_div_up(n_max, HL_SORT_TILE) : 1;
+  ws.k0 = c.take<uint32_t>(n_max);
+  ws.v0 = c.take<uint32_t>(n_max);
+  ws.k1 = c.take<uint32_t>(n_max);
+  ws.v1 = c.take<uint32_t>(n_max);
+  ws.part = c.take<uint32_t>((size_t)HL_SORT_HIST_BLOCKS * 1024);
+  ws.gexcl = c.take<uint32_t>(1024);
+  ws.ctr = c.base ? c.header() + HL_HDR_SORT : nullptr;
+  ws.status = c.take<uint64_t>((size_t)4 * ws.tiles_max * 256);
+}
+
+__device__ __forceinline__ uint32_t srt_n(const uint32_t* n_dev, uint32_t n_host) {
+  if (!n_dev) return n_host;
+  const uint32_t v = *n_dev;
+  return v < n_host ? v : n_host;
+}
+
+// Also clears the pass kernels' status words (n_status of them).
+__global__ void __launch_bounds__(256)
+srt_hist(const uint32_t* __restrict__ keys, const uint32_t* n_dev, uint32_t n_host, int passes,
+         uint32_t* part, uint32_t* gexcl, uint32_t* ctr, uint64_t* status, uint64_t n_status) {
+  __shared__ uint32_t h[4][256];
+  __shared__ bool last;
+  const uint32_t n = srt_n(n_dev, n_host);
+  for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n_status; i += (uint64_t)gridDim.x * blockDim.x)
+    status[i] = 0;
+#pragma unroll
+  for (int p = 0; p < 4; ++p) h[p][threadIdx.x] = 0;
+  __syncthreads();
+  for (uint32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) {
+    const uint32_t k = keys[i];
+    for (int p = 0; p < passes; ++p) atomicAdd(&h[p][(k >> (8 * p)) & 255u], 1u);
+  }
+  __syncthreads();
+  for (int p = 0; p < passes; ++p) part[blockIdx.x * 1024 + p * 256 + threadIdx.x] = h[p][threadIdx.x];
+  __threadfence();
+  __syncthreads();
+  if (threadIdx.x == 0) last = atomicInc(ctr, gridDim.x - 1) == gridDim.x - 1;
+  __syncthreads();
+  if (!last) return;
+  __threadfence();
+  __shared__ uint32_t wt[4];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  for (int p = 0; p < passes; ++p) {
+    uint32_t v = 0;
+    for (uint32_t b = 0; b < gridDim.x; ++b)
+      v += __hip_atomic_load(part + b * 1024 + p * 256 + threadIdx.x, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    uint32_t inc = v;
+    for (int o = 1; o < 64; o <<= 1) {
+      const uint32_t t = __shfl_up(inc, o);
+      if (lane >= o) inc += t;
+    }
+    if (lane == 63) wt[w] = inc;
+    __syncthreads();
+    uint32_t pre = 0;
+    for (int j = 0; j < w; ++j) pre += wt[j];
+    gexcl[p * 256 + threadIdx.x] = pre + inc - v;
+    __syncthreads();
+  }
+}
+
+__global__ void __launch_bounds__(HL_SORT_BLOCK)
+srt_pass(const uint32_t* __restrict__ kin, const uint32_t* __restrict__ vin, uint32_t* __restrict__ kout,
+         uint32_t* __restrict__ vout, const uint32_t* n_dev, uint32_t n_host, int shift,
+         const uint32_t* __restrict__ gexcl, uint64_t* status, uint32_t* tile_ctr, uint32_t epoch,
+         uint32_t* err) {
+  __shared__ uint32_t s_tile;
+  __shared__ uint32_t wcnt[4][256];
+  __shared__ uint32_t tdex[256], gbase[256], wt[4];
+  __shared__ uint32_t lk[HL_SORT_TILE], lv[HL_SORT_TILE];
+  const uint32_t n = srt_n(n_dev, n_host);
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  if (tid == 0) s_tile = atomicInc(tile_ctr, gridDim.x - 1);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) wcnt[j][tid] = 0;
+  __syncthreads();
+  const uint32_t tile = s_tile;
+  const uint64_t tb = (uint64_t)tile * HL_SORT_TILE;
+  if (tb >= n) return;
+  const uint64_t lt = (1ull << lane) - 1ull;
+  uint32_t key[HL_SORT_ITEMS], val[HL_SORT_ITEMS], lr[HL_SORT_ITEMS];
+#pragma unroll
+  for (int k = 0; k < HL_SORT_ITEMS; ++k) {
+    const uint64_t idx = tb + (uint64_t)w * (HL_SORT_ITEMS * 64) + k * 64 + lane;
+    const bool ok = idx < n;
+    key[k] = ok ? kin[idx] : 0xFFFFFFFFu;
+    val[k] = ok ? vin[idx] : 0u;
+  }
+#pragma unroll
+  for (int k = 0; k < HL_SORT_ITEMS; ++k) {
+    const uint64_t idx = tb + (uint64_t)w * (HL_SORT_ITEMS * 64) + k * 64 + lane;
+    const bool ok = idx < n;
+    const uint32_t d = (key[k] >> shift) & 255u;
+    uint64_t peers = __ballot(ok);
+#pragma unroll
+    for (int b = 0; b < 8; ++b) {
+      const bool bit = (d >> b) & 1u;
+      const uint64_t m = __ballot(bit);
+      peers &= bit ? m : ~m;
+    }
+    const int leader = peers ? (__ffsll((unsigned long long)peers) - 1) : 0;
+    uint32_t old = 0;
+    if (ok && lane == leader) {
+      old = wcnt[w][d];
+      wcnt[w][d] = old + (uint32_t)__popcll(peers);
+    }
+    old = __shfl(old, leader);
+    lr[k] = old + (uint32_t)__popcll(peers & lt);
+  }
+  __syncthreads();
+  // per digit (thread tid = digit): wave-exclusive prefixes and the tile count
+  uint32_t c0 = wcnt[0][tid], c1 = wcnt[1][tid], c2 = wcnt[2][tid], c3 = wcnt[3][tid];
+  const uint32_t tc = c0 + c1 + c2 + c3;
+  wcnt[0][tid] = 0;
+  wcnt[1][tid] = c0;
+  wcnt[2][tid] = c0 + c1;
+  wcnt[3][tid] = c0 + c1 + c2;
+  uint64_t* st = status + tid;
+  hl_st_store(st + (size_t)tile * 256, hl_st_pack(epoch, tile == 0 ? HL_ST_PRE : HL_ST_AGG, tc));
+  // tile-local exclusive scan of the digit counts
+  uint32_t inc = tc;
+  for (int o = 1; o < 64; o <<= 1) {
+    const uint32_t t = __shfl_up(inc, o);
+    if (lane >= o) inc += t;
+  }
+  if (lane == 63) wt[w] = inc;
+  __syncthreads();
+  uint32_t pre = 0;
+  for (int j = 0; j < w; ++j) pre += wt[j];
+  tdex[tid] = pre + inc - tc;
+  uint32_t excl = 0;
+  if (tile > 0) {
+    excl = hl_lookback(st, tile, 256, epoch, err);
+    hl_st_store(st + (size_t)tile * 256, hl_st_pack(epoch, HL_ST_PRE, excl + tc));
+  }
+  gbase[tid] = gexcl[tid] + excl;
+  __syncthreads();
+#pragma unroll
+  for (int k = 0; k < HL_SORT_ITEMS; ++k) {
+    const uint64_t idx = tb + (uint64_t)w * (HL_SORT_ITEMS * 64) + k * 64 + lane;
+    if (idx < n) {
+      const uint32_t d = (key[k] >> shift) & 255u;
+      const uint32_t p = tdex[d] + wcnt[w][d] + lr[k];
+      lk[p] = key[k];
+      lv[p] = val[k];
+    }
+  }
+  __syncthreads();
+  const uint32_t nv = (uint32_t)min((uint64_t)HL_SORT_TILE, (uint64_t)n - tb);
+  for (uint32_t i = tid; i < nv; i += HL_SORT_BLOCK) {
+    const uint32_t kk = lk[i];
+    const uint32_t d = (kk >> shift) & 255u;
+    const uint32_t p = gbase[d] + (i - tdex[d]);
+    kout[p] = kk;
+    vout[p] = lv[i];
+  }
+}
+
+hl_status hl_sort_pairs(hl_handle* h, hl_sort_ws& ws, const uint32_t* n_dev, uint32_t n_host, int bits,
+                        hipStream_t s, uint32_t** out_k, uint32_t** out_v) {
+  *out_k = ws.k0;
+  *out_v = ws.v0;
+  if (n_host == 0) return HL_OK;
+  if (n_host > ws.n_max || n_host >= (1u << 30)) return HL_ERR_CAPACITY;
+  if (bits < 1) bits = 1;
+  const int passes = (bits + 7) / 8;
+  if (passes > 4) return HL_ERR_UNSUPPORTED;
+  const uint32_t epoch = hl_next_epoch(h);
+  const uint32_t tiles = hl_div_up(n_host, HL_SORT_TILE);
+  const uint32_t hb = tiles < HL_SORT_HIST_BLOCKS ? tiles : HL_SORT_HIST_BLOCKS;
+  HL_KERNEL(h, s, "srt_hist", srt_hist, dim3(hb), dim3(256), 0, s, ws.k0, n_dev, n_host, passes, ws.part, ws.gexcl,
+                     ws.ctr, ws.status, (uint64_t)4 * ws.tiles_max * 256);
+  uint32_t *ki = ws.k0, *vi = ws.v0, *ko = ws.k1, *vo = ws.v1;
+  for (int p = 0; p < passes; ++p) {
+    HL_KERNEL(h, s, "srt_pass", srt_pass, dim3(tiles), dim3(HL_SORT_BLOCK), 0, s, ki, vi, ko, vo, n_dev, n_host, 8 * p,
+                       ws.gexcl + p * 256, ws.status + (size_t)p * ws.tiles_max * 256, ws.ctr + 1 + p, epoch,
+                       h->d_err);
+    uint32_t* t = ki; ki = ko; ko = t;
+    t = vi; vi = vo; vo = t;
+  }
+  HL_LAUNCHED();
+  *out_k = ki;
+  *out_v = vi;
+  return HL_OK;
+}

@@ -1,0 +1,265 @@
+"""GPU parity: every stage of the HIP path against the oracle on the same seeded
+inputs, through the C ABI.  Bit-exact for counts, hot set, gids, flags,
+partition, remap, cold ids/codes and gathered rows; within tolerance for pooled
+outputs (1e-5 of the summation scale) and updated rows (1e-5 fp32, 1e-2 bf16
+of |row| + lr*sum|dY|); untouched rows bitwise unchanged."""
+import numpy as np
+import pytest
+import torch
+
+from paper_2204_05436_amd import configs, hotline as hl, workload as W
+from paper_2204_05436_amd.runner import HotPath, to_device
+from parity_lib import as_f64, compare, log, make_table, run_gpu_stages, run_oracle
+
+pytestmark = pytest.mark.gpu
+
+
+def parity_case(w, n_prof=16, idx=16, k=None, hot_ids=None, batches=None):
+    rows = W.table_rows(w)
+    n_rows = int(rows.sum(dtype=np.int64))
+    k_cap = w.k_cap(n_rows)
+    if batches is None:
+        prof = [W.make_batch(w, rows, i) for i in range(n_prof)]
+        mb = W.make_batch(w, rows, idx)
+    else:
+        prof, mb = batches
+    dY = W.make_dy(w, idx, mb.n_bags)
+    log(f"[parity] {w.name}: rows={n_rows} B={mb.n_samples} L={mb.n_lookups} k_cap={k_cap} dim={w.dim} {w.dtype}")
+    table = make_table(w, n_rows)
+    max_l = max([p.n_lookups for p in prof] + [mb.n_lookups, 1])
+    hp = HotPath(w, rows, table, max_l, max(1, mb.n_samples))
+    try:
+        g = run_gpu_stages(hp, prof, mb, dY, k=k, hot_ids=hot_ids)
+        o = run_oracle(w, rows, prof, mb, dY, table.array, k_cap, k=k, hot_ids=hot_ids)
+        compare(w, g, o, k_cap, check_counts=hot_ids is None)
+        log(f"[parity] {w.name}: n_hot={len(o['hot'])} pop={len(o['pop'])} cold={len(o['cold'])} ok")
+    finally:
+        hp.close()
+        table.close()
+    return g, o
+
+
+@pytest.mark.parametrize("name", configs.ORDER)
+def test_full_size(name):
+    """Each workload at its full size, in the launch configuration the benchmark times."""
+    parity_case(configs.WORKLOADS[name])
+
+
+@pytest.mark.parametrize("name", configs.ORDER)
+def test_scaled_ragged(name):
+    """Smaller tables and a batch that is not a multiple of any tile size."""
+    w = configs.WORKLOADS[name]
+    w = configs.scaled(w, batch=777, row_scale=0.003 if name != "tiny" else 0.5, name=name + "-ragged")
+    parity_case(w, n_prof=4, idx=5)
+
+
+@pytest.mark.parametrize("k", [0, 1, 7, 10**9])
+def test_k_extremes(k):
+    w = configs.scaled(configs.WORKLOADS["tiny"], batch=300, row_scale=0.05, name="tiny-k")
+    rows = W.table_rows(w)
+    kk = min(k, w.k_cap(int(rows.sum())))
+    parity_case(w, n_prof=3, idx=3, k=kk)
+
+
+def test_all_rows_hot():
+    w = configs.scaled(configs.WORKLOADS["tbsm"], batch=200, row_scale=0.001, hot_frac=1.0, name="tbsm-allhot")
+    rows = W.table_rows(w)
+    g, o = parity_case(w, n_prof=2, idx=2, hot_ids=np.arange(int(rows.sum()), dtype=np.uint32))
+    assert len(o["nonpop"]) == 0 and len(o["cold"]) == 0
+
+
+def test_stale_hot_set():
+    """Profile one stream, run a batch from another seed: misclassification never changes results."""
+    w = configs.scaled(configs.WORKLOADS["dlrm-small"], batch=512, row_scale=0.01, name="small-stale")
+    rows = W.table_rows(w)
+    prof = [W.make_batch(w, rows, i) for i in range(3)]
+    other = configs.scaled(w, seed=w.seed + 99, name="small-other")
+    mb = W.make_batch(other, rows, 0)
+    parity_case(w, batches=(prof, mb))
+
+
+def _random_batch(rng, rows_per_table, B, steps, max_len, zero_frac=0.2):
+    T = len(rows_per_table)
+    bps = T * steps
+    lens = rng.integers(1, max_len + 1, B * bps)
+    lens[rng.random(B * bps) < zero_frac] = 0
+    ptr = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    rows = np.empty(int(ptr[-1]), np.uint32)
+    for j in range(B * bps):
+        t = j % T
+        # skewed draws so that rows repeat inside and across bags
+        r = (rng.zipf(1.3, lens[j]) - 1) % rows_per_table[t]
+        rows[ptr[j]:ptr[j + 1]] = r
+    return W.Batch(0, rows, ptr, B, bps)
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_random_shapes(seed):
+    rng = np.random.default_rng(1000 + seed)
+    dim = [1, 2, 3, 4, 6, 16, 64, 128, 136, 260, 24, 8][seed]
+    dtype = "bf16" if seed % 3 == 2 else "f32"
+    T = int(rng.integers(1, 5))
+    rows = rng.integers(1, 400, T).astype(np.uint32)
+    w = configs.Workload(name=f"rand{seed}", n_tables=T, dim=dim, dtype=dtype, batch=int(rng.integers(1, 300)),
+                         steps=int(rng.integers(1, 3)), rows_fixed=tuple(int(r) for r in rows),
+                         hot_frac=float(rng.uniform(0.05, 0.6)), seed=seed, lr=0.05)
+    prof = [_random_batch(rng, rows, w.batch, w.steps, 64) for _ in range(2)]
+    mb = _random_batch(rng, rows, w.batch, w.steps, 64)
+    parity_case(w, batches=(prof, mb))
+
+
+def test_determinism_and_split_equals_unsplit():
+    w = configs.scaled(configs.WORKLOADS["multi-hot"], batch=300, row_scale=0.002, name="mh-det")
+    rows = W.table_rows(w)
+    n_rows = int(rows.sum())
+    table = make_table(w, n_rows)
+    prof = [to_device(W.make_batch(w, rows, i), "cuda") for i in range(3)]
+    mb = W.make_batch(w, rows, 3)
+    dY = W.make_dy(w, 3, mb.n_bags)
+    results = []
+    for rep in range(2):
+        hp = HotPath(w, rows, table, max(p.n_lookups for p in prof + [to_device(mb, "cuda")]), w.batch)
+        hp.learn(prof)
+        b = to_device(mb, "cuda", dY)
+        hp.step(b, split_fwd=(rep == 0))
+        torch.cuda.synchronize()
+        results.append((hp.out[:mb.n_bags].cpu().numpy().copy(), hp.w_hot[:hp.n_hot].cpu().numpy().copy(),
+                        hp.staging.cpu().numpy().copy(), hp.device_error()))
+        hp.close()
+    table.close()
+    (o1, w1, s1, e1), (o2, w2, s2, e2) = results
+    assert e1 == 0 and e2 == 0
+    assert np.array_equal(o1.view(np.uint32), o2.view(np.uint32)), "pooled output not reproducible / split != unsplit"
+    assert np.array_equal(w1.view(np.uint8), w2.view(np.uint8)), "hot rows not reproducible"
+    assert np.array_equal(s1.view(np.uint8), s2.view(np.uint8)), "staging rows not reproducible"
+
+
+def test_sample_list_backward():
+    """Backward over one mu-batch (a sample list) against the oracle's selected update."""
+    import oracle as O
+    w = configs.scaled(configs.WORKLOADS["tbsm"], batch=256, row_scale=0.01, name="tbsm-sel")
+    rows = W.table_rows(w)
+    n_rows = int(rows.sum())
+    table = make_table(w, n_rows)
+    mb = W.make_batch(w, rows, 0)
+    dY = W.make_dy(w, 0, mb.n_bags)
+    hp = HotPath(w, rows, table, mb.n_lookups, w.batch)
+    try:
+        hot = np.arange(0, n_rows, 3, dtype=np.uint32)
+        hp.set_hot(torch.from_numpy(hot.view(np.int32)).cuda())
+        b = to_device(mb, "cuda", dY)
+        B, bps, L = b.n_samples, b.bps, b.n_lookups
+        sel = np.sort(np.random.default_rng(0).choice(B, B // 3, replace=False)).astype(np.int32)
+        dsel = torch.from_numpy(sel).cuda()
+        nsel = torch.tensor([len(sel)], dtype=torch.int32, device="cuda")
+        hl.hl_lookup_gids(hp.h, b.rows, b.bag_ptr, b.n_bags, hp.gids)
+        hl.hl_remap(hp.h, hp.gids, L, hp.codes)
+        hl.hl_cold_gather(hp.h, hp.gids, hp.codes, b.bag_ptr, B, bps, L, None, None, B, table.dev, hp.staging,
+                          hp.staging_cap, hp.cold_ids, hp.n_cold, hp.ws)
+        codes = hp.codes[:L].cpu().numpy().copy()
+        n_cold = int(hp.n_cold.item())
+        w0 = hp.w_hot[:len(hot)].cpu().numpy().copy()
+        s0 = hp.staging[:n_cold].cpu().numpy().copy()
+        hl.hl_embbag_bwd_sgd(hp.h, hp.w_hot, hp.staging, hp.staging_cap, hp.codes, b.bag_ptr, B, bps, L, dsel, nsel,
+                             B, b.dY, w.lr, hp.ws)
+        gw = hp.w_hot[:len(hot)].cpu().numpy()
+        gs = hp.staging[:n_cold].cpu().numpy()
+        assert hp.device_error() == 0
+        ow, os_ = w0.copy(), s0.copy()
+        uniq, sc, rc = O.embbag_bwd_sgd(w.dtype, ow, hp.k_cap, os_, codes, mb.bag_ptr, sel, len(sel), bps, dY, w.lr,
+                                        want_scale=True)
+        assert rc == 0
+        from parity_lib import check_close
+        th = uniq[uniq < hp.k_cap]
+        ts = uniq[uniq >= hp.k_cap] - hp.k_cap
+        check_close(gw[th], ow[th], sc[uniq < hp.k_cap], 1e-5, "selected update (hot)")
+        check_close(gs[ts], os_[ts], sc[uniq >= hp.k_cap], 1e-5, "selected update (staging)")
+        assert np.array_equal(np.delete(gw, th, axis=0), np.delete(w0, th, axis=0))
+    finally:
+        hp.close()
+        table.close()
+
+
+def test_capacity_and_range_errors():
+    w = configs.scaled(configs.WORKLOADS["tiny"], batch=64, row_scale=0.1, name="tiny-err")
+    rows = W.table_rows(w)
+    n_rows = int(rows.sum())
+    table = make_table(w, n_rows)
+    mb = W.make_batch(w, rows, 0)
+    hp = HotPath(w, rows, table, mb.n_lookups, w.batch, staging_cap=2)
+    try:
+        hp.set_hot(torch.arange(0, 5, dtype=torch.int32, device="cuda"))
+        b = to_device(mb, "cuda")
+        B, bps, L = b.n_samples, b.bps, b.n_lookups
+        hl.hl_lookup_gids(hp.h, b.rows, b.bag_ptr, b.n_bags, hp.gids)
+        hl.hl_remap(hp.h, hp.gids, L, hp.codes)
+        before = hp.codes[:L].clone()
+        stg_before = hp.staging.clone()
+        hl.hl_cold_gather(hp.h, hp.gids, hp.codes, b.bag_ptr, B, bps, L, None, None, B, table.dev, hp.staging,
+                          hp.staging_cap, hp.cold_ids, hp.n_cold, hp.ws)
+        err = hp.device_error()
+        assert err & hl.DEVERR["CAPACITY"]
+        assert int(hp.n_cold.item()) > 2                       # the count needed is reported
+        assert torch.equal(hp.codes[:L], before)               # nothing else written
+        assert torch.equal(hp.staging, stg_before)
+        # a row outside its table
+        bad = mb.rows.copy()
+        bad[3] = rows[3 % w.n_tables] + 5
+        db = to_device(W.Batch(0, bad, mb.bag_ptr, B, bps), "cuda")
+        hl.hl_lookup_gids(hp.h, db.rows, db.bag_ptr, db.n_bags, hp.gids)
+        assert hp.device_error() & hl.DEVERR["OUT_OF_RANGE"]
+        assert int(hp.gids[3].item()) == -1
+        # a code naming no row
+        hp.codes[:L] = -1
+        hl.hl_embbag_fwd(hp.h, hp.w_hot, hp.staging, hp.staging_cap, hp.codes, b.bag_ptr, B, bps, L, None, None, B,
+                         hp.out)
+        assert hp.device_error() & hl.DEVERR["BAD_CODE"]
+        # shape mismatch between bag_ptr and n_lookups
+        hl.hl_classify(hp.h, hp.gids, b.bag_ptr, B, bps, L + 1, hp.flags)
+        assert hp.device_error() & hl.DEVERR["SHAPE"]
+        # unsorted explicit hot set
+        hl.hl_set_hot(hp.h, torch.tensor([5, 3], dtype=torch.int32, device="cuda"), 2)
+        assert hp.device_error() & hl.DEVERR["BAD_HOTSET"]
+    finally:
+        hp.close()
+        table.close()
+
+
+def test_empty_batch():
+    w = configs.scaled(configs.WORKLOADS["tiny"], batch=0, row_scale=0.1, name="tiny-empty")
+    rows = W.table_rows(w)
+    table = make_table(w, int(rows.sum()))
+    hp = HotPath(w, rows, table, 1, 1)
+    try:
+        ptr = torch.zeros(1, dtype=torch.int32, device="cuda")
+        hl.hl_classify(hp.h, hp.gids, ptr, 0, w.bags_per_sample, 0, hp.flags)
+        hl.hl_partition(hp.h, hp.flags, 0, hp.pop, hp.nonpop, hp.counts, hp.ws)
+        hl.hl_cold_gather(hp.h, hp.gids, hp.codes, ptr, 0, w.bags_per_sample, 0, hp.nonpop, hp.counts[1:], 0,
+                          table.dev, hp.staging, hp.staging_cap, hp.cold_ids, hp.n_cold, hp.ws)
+        hl.hl_embbag_fwd(hp.h, hp.w_hot, hp.staging, hp.staging_cap, hp.codes, ptr, 0, w.bags_per_sample, 0, None,
+                         None, 0, hp.out)
+        assert hp.counts.cpu().tolist() == [0, 0] and int(hp.n_cold.item()) == 0
+        assert hp.device_error() == 0
+    finally:
+        hp.close()
+        table.close()
+
+
+def test_large_partition():
+    """More samples than one partition tile (multi-block path)."""
+    w = configs.scaled(configs.WORKLOADS["tiny"], batch=1, row_scale=0.1, name="tiny-part")
+    rows = W.table_rows(w)
+    table = make_table(w, int(rows.sum()))
+    n = 200_003
+    hp = HotPath(w, rows, table, 1, n)
+    try:
+        f = (np.random.default_rng(3).random(n) < 0.3).astype(np.uint8)
+        hp.flags.copy_(torch.from_numpy(f))
+        hl.hl_partition(hp.h, hp.flags, n, hp.pop, hp.nonpop, hp.counts, hp.ws)
+        c = hp.counts.cpu().numpy()
+        assert c[0] == f.sum() and c[1] == n - f.sum()
+        assert np.array_equal(hp.pop[:c[0]].cpu().numpy(), np.flatnonzero(f))
+        assert np.array_equal(hp.nonpop[:c[1]].cpu().numpy(), np.flatnonzero(f == 0))
+    finally:
+        hp.close()
+        table.close()
