@@ -59,18 +59,22 @@ extern "C" hl_status hl_classify(const hl_handle* h, const uint32_t* gids, const
 }
 
 // ----------------------------------------------------------------------------- partition
-// Stable compaction of sample ids by flag.  One block of 1024 threads handles a
-// tile of up to 64K samples in chunks of 1024: a wave ballot gives each lane's
+// Stable compaction of sample ids by flag.  A block of 1024 threads handles a
+// tile of `tile` samples in chunks of 1024: a wave ballot gives each lane's
 // rank among the wave's popular samples, the 16 wave totals are scanned in
 // LDS, and a running carry links the chunks.  A popular sample goes to
 // pop[p], a non-popular one to nonpop[i - p], p = popular samples before i.
-#define PT_TILE 65536
+// Tile prefixes: up to 1024 tiles of 1024 samples, every block adds up the
+// counts of the tiles before it; beyond that, 64K-sample tiles and a serial
+// scan of their counts.
+#define PT_SMALL 1024
+#define PT_BIG 65536
 __global__ void __launch_bounds__(1024)
-pt_count(const uint8_t* __restrict__ flags, int32_t n, uint32_t* tile_cnt) {
+pt_count(const uint8_t* __restrict__ flags, int32_t n, int32_t tile, uint32_t* tile_cnt) {
   __shared__ uint32_t red[1024];
-  const int64_t base = (int64_t)blockIdx.x * PT_TILE;
+  const int64_t base = (int64_t)blockIdx.x * tile;
   uint32_t c = 0;
-  for (int k = 0; k < PT_TILE / 1024; ++k) {
+  for (int k = 0; k < tile / 1024; ++k) {
     const int64_t i = base + k * 1024 + threadIdx.x;
     if (i < n) c += flags[i] != 0;
   }
@@ -95,17 +99,32 @@ pt_scan(uint32_t* tile_cnt, int32_t n_tiles) {
   }
 }
 
+// prefix_mode 0: no other tiles; 1: tile_cnt holds raw counts (sum those before
+// this tile); 2: tile_cnt holds exclusive prefixes.
 __global__ void __launch_bounds__(1024)
-pt_emit(const uint8_t* __restrict__ flags, int32_t n, const uint32_t* tile_excl, int32_t* __restrict__ pop,
-        int32_t* __restrict__ nonpop, int32_t* counts) {
+pt_emit(const uint8_t* __restrict__ flags, int32_t n, int32_t tile, const uint32_t* tile_cnt, int prefix_mode,
+        int32_t* __restrict__ pop, int32_t* __restrict__ nonpop, int32_t* counts) {
   __shared__ uint32_t wtot[16];
   __shared__ uint32_t carry;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int64_t base = (int64_t)blockIdx.x * PT_TILE;
-  if (threadIdx.x == 0) carry = tile_excl ? tile_excl[blockIdx.x] : 0u;
+  const int64_t base = (int64_t)blockIdx.x * tile;
+  if (prefix_mode == 1) {
+    uint32_t c = 0;
+    for (uint32_t t = threadIdx.x; t < blockIdx.x; t += blockDim.x) c += tile_cnt[t];
+    for (int o = 32; o > 0; o >>= 1) c += __shfl_down(c, o);
+    if (lane == 0) wtot[w] = c;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      uint32_t t = 0;
+      for (int j = 0; j < 16; ++j) t += wtot[j];
+      carry = t;
+    }
+  } else if (threadIdx.x == 0) {
+    carry = prefix_mode == 2 ? tile_cnt[blockIdx.x] : 0u;
+  }
   __syncthreads();
   const uint64_t lt = (1ull << lane) - 1ull;
-  for (int k = 0; k < PT_TILE / 1024; ++k) {
+  for (int k = 0; k < tile / 1024; ++k) {
     const int64_t c0 = base + k * 1024;
     if (c0 >= n) break;
     const int64_t i = c0 + threadIdx.x;
@@ -136,7 +155,7 @@ pt_emit(const uint8_t* __restrict__ flags, int32_t n, const uint32_t* tile_excl,
 }
 
 size_t hl_partition_ws_bytes(int32_t max_samples) {
-  return HL_WS_HEADER + 4 * ((size_t)(max_samples + PT_TILE - 1) / PT_TILE + 64);
+  return HL_WS_HEADER + 4 * ((size_t)(max_samples + PT_SMALL - 1) / PT_SMALL + 64);
 }
 
 extern "C" hl_status hl_partition(const hl_handle* h, const uint8_t* flags, int32_t n, int32_t* pop,
@@ -144,15 +163,23 @@ extern "C" hl_status hl_partition(const hl_handle* h, const uint8_t* flags, int3
                                   hl_stream stream) {
   if (!h || n < 0 || !counts || (n > 0 && (!flags || !pop || !nonpop))) return HL_ERR_INVALID_ARG;
   hipStream_t s = (hipStream_t)stream;
-  const int32_t tiles = n == 0 ? 1 : (int32_t)hl_div_up(n, PT_TILE);
+  const bool small = n <= PT_SMALL * 1024;
+  const int32_t tile = small ? PT_SMALL : PT_BIG;
+  const int32_t tiles = n == 0 ? 1 : (int32_t)hl_div_up(n, tile);
   uint32_t* tc = nullptr;
+  int mode = 0;
   if (tiles > 1) {
     if (!ws || ws_bytes < hl_partition_ws_bytes(n)) return HL_ERR_CAPACITY;
     tc = (uint32_t*)((char*)ws + HL_WS_HEADER);
-    HL_KERNEL(h, s, "pt_count", pt_count, dim3(tiles), dim3(1024), 0, s, flags, n, tc);
-    HL_KERNEL(h, s, "pt_scan", pt_scan, dim3(1), dim3(1024), 0, s, tc, tiles);
+    HL_KERNEL(h, s, "pt_count", pt_count, dim3(tiles), dim3(1024), 0, s, flags, n, tile, tc);
+    if (small) {
+      mode = 1;
+    } else {
+      HL_KERNEL(h, s, "pt_scan", pt_scan, dim3(1), dim3(1024), 0, s, tc, tiles);
+      mode = 2;
+    }
   }
-  HL_KERNEL(h, s, "pt_emit", pt_emit, dim3(tiles), dim3(1024), 0, s, flags, n, tc, pop, nonpop, counts);
+  HL_KERNEL(h, s, "pt_emit", pt_emit, dim3(tiles), dim3(1024), 0, s, flags, n, tile, tc, mode, pop, nonpop, counts);
   HL_LAUNCHED();
   return HL_OK;
 }

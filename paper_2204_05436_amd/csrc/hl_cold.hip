@@ -43,8 +43,11 @@ size_t hl_cold_ws_bytes(const hl_handle* h, int64_t max_lookups) {
 
 // A block owns `spb` selected samples; their lookup ranges are laid end to end
 // in LDS (start, exclusive prefix of lengths) and threads walk the
-// concatenation, finding their sample by binary search.
+// concatenation, finding their sample by binary search.  Candidates are
+// buffered in LDS and appended to the global list with one atomic per block
+// (per flush), which keeps same-address atomics rare.
 #define CG_MAX_SPB 512
+#define CG_BUF 2048
 __global__ void __launch_bounds__(256)
 cg_collect(const uint32_t* __restrict__ gids, const int32_t* __restrict__ codes,
            const int32_t* __restrict__ bag_ptr, int32_t n_samples, int32_t bps,
@@ -52,6 +55,8 @@ cg_collect(const uint32_t* __restrict__ gids, const int32_t* __restrict__ codes,
            uint64_t n_rows, uint32_t* __restrict__ out_k, uint32_t* __restrict__ out_v, uint32_t n_max,
            uint32_t* ctr, uint64_t* ustat, uint32_t utiles, uint32_t* err) {
   __shared__ int32_t st[CG_MAX_SPB], pre[CG_MAX_SPB + 1];
+  __shared__ uint32_t bk[CG_BUF], bv[CG_BUF];
+  __shared__ uint32_t bn, bbase;
   for (uint32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < utiles; i += gridDim.x * blockDim.x) ustat[i] = 0;
   int32_t n_sel = n_sel_max;
   if (sample_ids && n_sel_dev) n_sel = min(max(*n_sel_dev, 0), n_sel_max);
@@ -69,7 +74,10 @@ cg_collect(const uint32_t* __restrict__ gids, const int32_t* __restrict__ codes,
     st[j] = a;
     pre[j + 1] = b - a;
   }
-  if (threadIdx.x == 0) pre[0] = 0;
+  if (threadIdx.x == 0) {
+    pre[0] = 0;
+    bn = 0;
+  }
   __syncthreads();
   if (threadIdx.x == 0)
     for (int j = 0; j < ns; ++j) pre[j + 1] += pre[j];
@@ -77,7 +85,31 @@ cg_collect(const uint32_t* __restrict__ gids, const int32_t* __restrict__ codes,
   const int32_t total = pre[ns];
   const int lane = threadIdx.x & 63;
   const uint64_t lt = (1ull << lane) - 1ull;
-  for (int32_t t0 = 0; t0 < total; t0 += blockDim.x) {
+  for (int32_t t0 = 0; t0 < total + (int32_t)blockDim.x; t0 += blockDim.x) {
+    // flush when the next chunk might not fit, and once after the last chunk;
+    // the barrier makes every wave see the same buffer fill
+    __syncthreads();
+    const bool last = t0 >= total;
+    if (last || bn + blockDim.x > CG_BUF) {
+      const uint32_t cnt = bn;
+      if (threadIdx.x == 0 && cnt) bbase = atomicAdd(ctr + CG_C_COLLECT, cnt);
+      __syncthreads();
+      if (cnt) {
+        for (uint32_t j = threadIdx.x; j < cnt; j += blockDim.x) {
+          const uint32_t p = bbase + j;
+          if (p < n_max) {  // a sample listed twice could overflow the buffer
+            out_k[p] = bk[j];
+            out_v[p] = bv[j];
+          } else {
+            hl_flag(err, HL_DEVERR_OUT_OF_RANGE);
+          }
+        }
+      }
+      __syncthreads();
+      if (threadIdx.x == 0) bn = 0;
+      __syncthreads();
+    }
+    if (last) break;
     const int32_t t = t0 + threadIdx.x;
     bool take = false;
     uint32_t g = 0;
@@ -98,16 +130,12 @@ cg_collect(const uint32_t* __restrict__ gids, const int32_t* __restrict__ codes,
     const uint64_t m = __ballot(take);
     if (m) {
       uint32_t base = 0;
-      if (lane == 0) base = atomicAdd(ctr + CG_C_COLLECT, (uint32_t)__popcll(m));
+      if (lane == 0) base = atomicAdd(&bn, (uint32_t)__popcll(m));
       base = __shfl(base, 0);
       if (take) {
         const uint32_t p = base + (uint32_t)__popcll(m & lt);
-        if (p < n_max) {  // a sample listed twice could overflow the buffer
-          out_k[p] = g;
-          out_v[p] = (uint32_t)i;
-        } else {
-          hl_flag(err, HL_DEVERR_OUT_OF_RANGE);
-        }
+        bk[p] = g;
+        bv[p] = (uint32_t)i;
       }
     }
   }

@@ -131,6 +131,27 @@ __device__ __forceinline__ int32_t eb_nsel(const int32_t* ids, const int32_t* n_
 }
 
 // ----------------------------------------------------------------------------- forward
+// A row group takes FC consecutive bag slots of the selection (slot q = bag j of
+// selected sample q / bps) and issues the loads of all of them before using
+// any: offsets, then codes, then rows, so FC rows per lane are in flight.  When
+// every bag of the chunk holds one lookup (one-hot features) that is the whole
+// work; otherwise bags are pooled one by one with 4 rows in flight.
+#define FC 8
+__device__ __forceinline__ bool eb_code_row(uint32_t cu, uint32_t n_hot, uint32_t k_cap, int32_t stg_rows,
+                                            int64_t* row, bool* stg) {
+  if (cu < n_hot) {
+    *row = cu;
+    *stg = false;
+    return true;
+  }
+  if (cu >= k_cap && cu - k_cap < (uint32_t)stg_rows) {
+    *row = cu - k_cap;
+    *stg = true;
+    return true;
+  }
+  return false;
+}
+
 template <int VEC, bool BF>
 __global__ void __launch_bounds__(256)
 eb_fwd(const void* w_hot_, const void* stg_, int32_t stg_rows, uint32_t n_hot, uint32_t k_cap,
@@ -150,66 +171,89 @@ eb_fwd(const void* w_hot_, const void* stg_, int32_t stg_rows, uint32_t n_hot, u
   const bool cact = colv < g.vpr;
   const int64_t col = (int64_t)colv * VEC;
   const int64_t total = (int64_t)eb_nsel(sample_ids, n_sel_dev, n_sel_max) * bps;
+  const int64_t chunks = (total + FC - 1) / FC;
   const int64_t stride = (int64_t)gridDim.x * 4 * g.NG;
-  for (int64_t q = ((int64_t)blockIdx.x * 4 + w) * g.NG + gi; q < total; q += stride) {
-    const int64_t si = q / bps, j = q - si * bps;
-    const int64_t smp = sample_ids ? (int64_t)sample_ids[si] : si;
-    if (smp < 0 || smp >= n_samples) {
-      if (gl == 0) hl_flag(err, HL_DEVERR_OUT_OF_RANGE);
-      continue;
-    }
-    const int64_t bag = smp * bps + j;
-    const int32_t lo = bag_ptr[bag], hi = bag_ptr[bag + 1];
-    float acc[VEC];
+  for (int64_t c = ((int64_t)blockIdx.x * 4 + w) * g.NG + gi; c < chunks; c += stride) {
+    const int64_t q0 = c * FC;
+    int64_t si = q0 / bps, j = q0 - si * bps;
+    int64_t bag[FC];
+    bool val[FC];
 #pragma unroll
-    for (int v = 0; v < VEC; ++v) acc[v] = 0.f;
-    int32_t i = lo;
-    for (; i + 4 <= hi; i += 4) {
-      int32_t c[4];
-      const T* p[4];
-      bool ok[4];
-#pragma unroll
-      for (int u = 0; u < 4; ++u) c[u] = codes[i + u];
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const uint32_t cu = (uint32_t)c[u];
-        ok[u] = true;
-        if (cu < n_hot) p[u] = w_hot + (int64_t)cu * g.D;
-        else if (cu >= k_cap && cu - k_cap < (uint32_t)stg_rows) p[u] = stg + (int64_t)(cu - k_cap) * g.D;
-        else { ok[u] = false; p[u] = w_hot; }
+    for (int u = 0; u < FC; ++u) {
+      val[u] = q0 + u < total;
+      int64_t smp = si;
+      if (val[u] && sample_ids) smp = sample_ids[si];
+      if (val[u] && (smp < 0 || smp >= n_samples)) {
+        if (gl == 0) hl_flag(err, HL_DEVERR_OUT_OF_RANGE);
+        val[u] = false;
       }
-      float v[4][VEC];
+      bag[u] = smp * bps + j;
+      if (++j == bps) {
+        j = 0;
+        ++si;
+      }
+    }
+    int32_t lo[FC], hi[FC];
+    bool one = true;
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        if (ok[u] && cact) RowIO<VEC, BF>::load(p[u] + col, v[u]);
+    for (int u = 0; u < FC; ++u) {
+      lo[u] = val[u] ? bag_ptr[bag[u]] : 0;
+      hi[u] = val[u] ? bag_ptr[bag[u] + 1] : 1;
+    }
+#pragma unroll
+    for (int u = 0; u < FC; ++u) one = one && (hi[u] - lo[u] == 1);
+    if (one) {
+      uint32_t cu[FC];
+#pragma unroll
+      for (int u = 0; u < FC; ++u) cu[u] = val[u] ? (uint32_t)codes[lo[u]] : 0u;
+      float v[FC][VEC];
+#pragma unroll
+      for (int u = 0; u < FC; ++u) {
+        int64_t r = 0;
+        bool st = false;
+        const bool ok = val[u] && eb_code_row(cu[u], n_hot, k_cap, stg_rows, &r, &st);
+        if (ok && cact) RowIO<VEC, BF>::load((st ? stg : w_hot) + r * g.D + col, v[u]);
         else {
 #pragma unroll
           for (int e = 0; e < VEC; ++e) v[u][e] = 0.f;
         }
+        if (val[u] && !ok && gl == 0) hl_flag(err, HL_DEVERR_BAD_CODE);
       }
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-#pragma unroll
-        for (int e = 0; e < VEC; ++e) acc[e] += v[u][e];
-        if (!ok[u] && gl == 0) hl_flag(err, HL_DEVERR_BAD_CODE);
-      }
+      for (int u = 0; u < FC; ++u)
+        if (val[u] && cact) st_f32<VEC>(out + bag[u] * g.D + col, v[u]);
+      continue;
     }
-    for (; i < hi; ++i) {
-      const uint32_t cu = (uint32_t)codes[i];
-      const T* p;
-      bool ok = true;
-      if (cu < n_hot) p = w_hot + (int64_t)cu * g.D;
-      else if (cu >= k_cap && cu - k_cap < (uint32_t)stg_rows) p = stg + (int64_t)(cu - k_cap) * g.D;
-      else { ok = false; p = w_hot; }
-      if (ok && cact) {
-        float v[VEC];
-        RowIO<VEC, BF>::load(p + col, v);
+    for (int u = 0; u < FC; ++u) {
+      if (!val[u]) continue;
+      float acc[VEC];
 #pragma unroll
-        for (int e = 0; e < VEC; ++e) acc[e] += v[e];
+      for (int e = 0; e < VEC; ++e) acc[e] = 0.f;
+      for (int32_t i = lo[u]; i < hi[u]; i += 4) {
+        uint32_t cc[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) cc[k] = i + k < hi[u] ? (uint32_t)codes[i + k] : 0u;
+        float v[4][VEC];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          int64_t r = 0;
+          bool st = false;
+          const bool in = i + k < hi[u];
+          const bool ok = in && eb_code_row(cc[k], n_hot, k_cap, stg_rows, &r, &st);
+          if (ok && cact) RowIO<VEC, BF>::load((st ? stg : w_hot) + r * g.D + col, v[k]);
+          else {
+#pragma unroll
+            for (int e = 0; e < VEC; ++e) v[k][e] = 0.f;
+          }
+          if (in && !ok && gl == 0) hl_flag(err, HL_DEVERR_BAD_CODE);
+        }
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+#pragma unroll
+          for (int e = 0; e < VEC; ++e) acc[e] += v[k][e];
       }
-      if (!ok && gl == 0) hl_flag(err, HL_DEVERR_BAD_CODE);
+      if (cact) st_f32<VEC>(out + bag[u] * g.D + col, acc);
     }
-    if (cact) st_f32<VEC>(out + bag * g.D + col, acc);
   }
 }
 
@@ -568,8 +612,8 @@ extern "C" hl_status hl_embbag_fwd(const hl_handle* h, const void* w_hot, const 
   const size_t es = h->dtype == HL_F32 ? 4 : 2;
   const int vec = eb_pick_vec(h->dim, es, {w_hot, staging, out});
   eb_geom g = eb_make_geom(h->dim, vec);
-  const int64_t total = (int64_t)n_sel_max * bps;
-  int64_t blocks = (total + 4 * g.NG - 1) / (4 * g.NG);
+  const int64_t chunks = ((int64_t)n_sel_max * bps + FC - 1) / FC;
+  int64_t blocks = (chunks + 4 * g.NG - 1) / (4 * g.NG);
   if (blocks > (1 << 20)) blocks = 1 << 20;
   dim3 grid((uint32_t)blocks, g.cchunks);
   hipStream_t s = (hipStream_t)stream;

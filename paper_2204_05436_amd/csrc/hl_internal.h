@@ -132,9 +132,9 @@ struct hl_sort_ws {
 };
 
 #define HL_SORT_BLOCK 256
-#define HL_SORT_ITEMS 8
+#define HL_SORT_ITEMS 16
 #define HL_SORT_TILE (HL_SORT_BLOCK * HL_SORT_ITEMS)
-#define HL_SORT_HIST_BLOCKS 64
+#define HL_SORT_HIST_BLOCKS 32
 
 void hl_sort_ws_carve(hl_carver& c, hl_sort_ws& ws, uint32_t n_max);
 // Sorts ws.k0/ws.v0 (first *n_dev items if n_dev != NULL, else n_host) by the
@@ -144,42 +144,58 @@ void hl_sort_ws_carve(hl_carver& c, hl_sort_ws& ws, uint32_t n_max);
 hl_status hl_sort_pairs(hl_handle* h, hl_sort_ws& ws, const uint32_t* n_dev, uint32_t n_host,
                         int bits, hipStream_t s, uint32_t** out_k, uint32_t** out_v);
 
-// Decoupled look-back helpers (epoch-tagged 64-bit status words).
+// Decoupled look-back helpers (epoch-tagged 64-bit status words).  A status
+// word carries its own value, so relaxed agent-scope atomics suffice: no other
+// data is published through it.
 #define HL_ST_AGG 1ull
 #define HL_ST_PRE 2ull
-#define HL_SPIN_LIMIT (1u << 26)
+#define HL_SPIN_LIMIT (1u << 24)
+#define HL_LB_WIN 32
 
 __device__ __forceinline__ uint64_t hl_st_pack(uint32_t epoch, uint64_t flag, uint32_t v) {
   return ((uint64_t)epoch << 32) | (flag << 30) | (uint64_t)(v & 0x3FFFFFFFu);
 }
 __device__ __forceinline__ void hl_st_store(uint64_t* p, uint64_t w) {
-  __hip_atomic_store(p, w, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+  __hip_atomic_store(p, w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 __device__ __forceinline__ uint64_t hl_st_load(const uint64_t* p) {
-  return __hip_atomic_load(const_cast<uint64_t*>(p), __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT);
+  return __hip_atomic_load(const_cast<uint64_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 // Exclusive prefix of tile `tile`'s value over tiles [0, tile) for one lane of
-// status words laid out with stride `stride` between tiles.
+// status words laid out with stride `stride` between tiles.  Reads a window of
+// HL_LB_WIN predecessors per round trip.
 __device__ __forceinline__ uint32_t hl_lookback(const uint64_t* st, uint32_t tile, size_t stride,
                                                 uint32_t epoch, uint32_t* err) {
   uint32_t excl = 0;
   int64_t j = (int64_t)tile - 1;
   uint32_t spins = 0;
   while (j >= 0) {
-    uint64_t w = hl_st_load(st + (size_t)j * stride);
-    uint32_t e = (uint32_t)(w >> 32);
-    uint64_t f = (w >> 30) & 3ull;
-    if (e != epoch || f == 0) {
+    uint64_t w[HL_LB_WIN];
+#pragma unroll
+    for (int k = 0; k < HL_LB_WIN; ++k) w[k] = (j - k >= 0) ? hl_st_load(st + (size_t)(j - k) * stride) : 0ull;
+    int k = 0;
+    bool stall = false;
+#pragma unroll
+    for (int q = 0; q < HL_LB_WIN; ++q) {
+      if (stall || j - q < 0) continue;
+      const uint32_t e = (uint32_t)(w[q] >> 32);
+      const uint64_t f = (w[q] >> 30) & 3ull;
+      if (e != epoch || f == 0) {
+        stall = true;
+        continue;
+      }
+      excl += (uint32_t)(w[q] & 0x3FFFFFFFu);
+      if (f == HL_ST_PRE) return excl;
+      k = q + 1;
+    }
+    j -= k;
+    if (stall) {
       if (++spins > HL_SPIN_LIMIT) {
         hl_flag(err, HL_DEVERR_STALL);
-        break;
+        return excl;
       }
       __builtin_amdgcn_s_sleep(1);
-      continue;
     }
-    excl += (uint32_t)(w & 0x3FFFFFFFu);
-    if (f == HL_ST_PRE) break;
-    --j;
   }
   return excl;
 }

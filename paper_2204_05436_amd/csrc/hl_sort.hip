@@ -31,12 +31,13 @@ __device__ __forceinline__ uint32_t srt_n(const uint32_t* n_dev, uint32_t n_host
   return v < n_host ? v : n_host;
 }
 
-// Also clears the pass kernels' status words (n_status of them).
+// Per-block digit counts of every pass (no cross-block merge here: each pass
+// kernel block merges the few partials it needs), and clears the pass kernels'
+// status words (n_status of them).
 __global__ void __launch_bounds__(256)
 srt_hist(const uint32_t* __restrict__ keys, const uint32_t* n_dev, uint32_t n_host, int passes,
-         uint32_t* part, uint32_t* gexcl, uint32_t* ctr, uint64_t* status, uint64_t n_status) {
+         uint32_t* part, uint64_t* status, uint64_t n_status) {
   __shared__ uint32_t h[4][256];
-  __shared__ bool last;
   const uint32_t n = srt_n(n_dev, n_host);
   for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n_status; i += (uint64_t)gridDim.x * blockDim.x)
     status[i] = 0;
@@ -49,37 +50,13 @@ srt_hist(const uint32_t* __restrict__ keys, const uint32_t* n_dev, uint32_t n_ho
   }
   __syncthreads();
   for (int p = 0; p < passes; ++p) part[blockIdx.x * 1024 + p * 256 + threadIdx.x] = h[p][threadIdx.x];
-  __threadfence();
-  __syncthreads();
-  if (threadIdx.x == 0) last = atomicInc(ctr, gridDim.x - 1) == gridDim.x - 1;
-  __syncthreads();
-  if (!last) return;
-  __threadfence();
-  __shared__ uint32_t wt[4];
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  for (int p = 0; p < passes; ++p) {
-    uint32_t v = 0;
-    for (uint32_t b = 0; b < gridDim.x; ++b)
-      v += __hip_atomic_load(part + b * 1024 + p * 256 + threadIdx.x, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    uint32_t inc = v;
-    for (int o = 1; o < 64; o <<= 1) {
-      const uint32_t t = __shfl_up(inc, o);
-      if (lane >= o) inc += t;
-    }
-    if (lane == 63) wt[w] = inc;
-    __syncthreads();
-    uint32_t pre = 0;
-    for (int j = 0; j < w; ++j) pre += wt[j];
-    gexcl[p * 256 + threadIdx.x] = pre + inc - v;
-    __syncthreads();
-  }
 }
 
 __global__ void __launch_bounds__(HL_SORT_BLOCK)
 srt_pass(const uint32_t* __restrict__ kin, const uint32_t* __restrict__ vin, uint32_t* __restrict__ kout,
          uint32_t* __restrict__ vout, const uint32_t* n_dev, uint32_t n_host, int shift,
-         const uint32_t* __restrict__ gexcl, uint64_t* status, uint32_t* tile_ctr, uint32_t epoch,
-         uint32_t* err) {
+         const uint32_t* __restrict__ part, uint32_t n_part, uint64_t* status, uint32_t* tile_ctr,
+         uint32_t epoch, uint32_t* err) {
   __shared__ uint32_t s_tile;
   __shared__ uint32_t wcnt[4][256];
   __shared__ uint32_t tdex[256], gbase[256], wt[4];
@@ -94,6 +71,9 @@ srt_pass(const uint32_t* __restrict__ kin, const uint32_t* __restrict__ vin, uin
   const uint64_t tb = (uint64_t)tile * HL_SORT_TILE;
   if (tb >= n) return;
   const uint64_t lt = (1ull << lane) - 1ull;
+  // this pass's global count of digit tid, from the histogram kernel's partials
+  uint32_t dtot = 0;
+  for (uint32_t b = 0; b < n_part; ++b) dtot += part[b * 1024 + tid];
   uint32_t key[HL_SORT_ITEMS], val[HL_SORT_ITEMS], lr[HL_SORT_ITEMS];
 #pragma unroll
   for (int k = 0; k < HL_SORT_ITEMS; ++k) {
@@ -144,12 +124,23 @@ srt_pass(const uint32_t* __restrict__ kin, const uint32_t* __restrict__ vin, uin
   uint32_t pre = 0;
   for (int j = 0; j < w; ++j) pre += wt[j];
   tdex[tid] = pre + inc - tc;
+  // exclusive scan of the global digit counts
+  uint32_t ginc = dtot;
+  for (int o = 1; o < 64; o <<= 1) {
+    const uint32_t t = __shfl_up(ginc, o);
+    if (lane >= o) ginc += t;
+  }
+  __syncthreads();
+  if (lane == 63) wt[w] = ginc;
+  __syncthreads();
+  uint32_t gpre = 0;
+  for (int j = 0; j < w; ++j) gpre += wt[j];
   uint32_t excl = 0;
   if (tile > 0) {
     excl = hl_lookback(st, tile, 256, epoch, err);
     hl_st_store(st + (size_t)tile * 256, hl_st_pack(epoch, HL_ST_PRE, excl + tc));
   }
-  gbase[tid] = gexcl[tid] + excl;
+  gbase[tid] = gpre + ginc - dtot + excl;
   __syncthreads();
 #pragma unroll
   for (int k = 0; k < HL_SORT_ITEMS; ++k) {
@@ -184,13 +175,13 @@ hl_status hl_sort_pairs(hl_handle* h, hl_sort_ws& ws, const uint32_t* n_dev, uin
   const uint32_t epoch = hl_next_epoch(h);
   const uint32_t tiles = hl_div_up(n_host, HL_SORT_TILE);
   const uint32_t hb = tiles < HL_SORT_HIST_BLOCKS ? tiles : HL_SORT_HIST_BLOCKS;
-  HL_KERNEL(h, s, "srt_hist", srt_hist, dim3(hb), dim3(256), 0, s, ws.k0, n_dev, n_host, passes, ws.part, ws.gexcl,
-                     ws.ctr, ws.status, (uint64_t)4 * ws.tiles_max * 256);
+  HL_KERNEL(h, s, "srt_hist", srt_hist, dim3(hb), dim3(256), 0, s, ws.k0, n_dev, n_host, passes, ws.part,
+            ws.status, (uint64_t)4 * ws.tiles_max * 256);
   uint32_t *ki = ws.k0, *vi = ws.v0, *ko = ws.k1, *vo = ws.v1;
   for (int p = 0; p < passes; ++p) {
-    HL_KERNEL(h, s, "srt_pass", srt_pass, dim3(tiles), dim3(HL_SORT_BLOCK), 0, s, ki, vi, ko, vo, n_dev, n_host, 8 * p,
-                       ws.gexcl + p * 256, ws.status + (size_t)p * ws.tiles_max * 256, ws.ctr + 1 + p, epoch,
-                       h->d_err);
+    HL_KERNEL(h, s, "srt_pass", srt_pass, dim3(tiles), dim3(HL_SORT_BLOCK), 0, s, ki, vi, ko, vo, n_dev, n_host,
+              8 * p, ws.part + p * 256, hb, ws.status + (size_t)p * ws.tiles_max * 256, ws.ctr + 1 + p, epoch,
+              h->d_err);
     uint32_t* t = ki; ki = ko; ko = t;
     t = vi; vi = vo; vo = t;
   }

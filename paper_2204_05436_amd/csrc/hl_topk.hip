@@ -74,14 +74,13 @@ tk_level(const uint32_t* __restrict__ counts, uint64_t n, uint32_t* st, int leve
   if (!last) return;
   __threadfence();
   uint32_t tot = 0;
-  for (uint32_t b = 0; b < gridDim.x; ++b) tot += __hip_atomic_load(part + b * 257 + threadIdx.x, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  for (uint32_t b = 0; b < gridDim.x; ++b) tot += part[b * 257 + threadIdx.x];
   hist[threadIdx.x] = tot;
   __syncthreads();
   if (threadIdx.x != 0) return;
   if (level == 0) {
     uint32_t nonzero = 0;
-    for (uint32_t b = 0; b < gridDim.x; ++b)
-      nonzero += __hip_atomic_load(part + b * 257 + 256, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    for (uint32_t b = 0; b < gridDim.x; ++b) nonzero += part[b * 257 + 256];
     st[S_NONZERO] = nonzero;
     if (nonzero <= k) {  // every accessed row fits: select count >= 1
       st[S_TAU] = 1;

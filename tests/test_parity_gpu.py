@@ -137,7 +137,7 @@ def test_determinism_and_split_equals_unsplit():
 def test_sample_list_backward():
     """Backward over one mu-batch (a sample list) against the oracle's selected update."""
     import oracle as O
-    w = configs.scaled(configs.WORKLOADS["tbsm"], batch=256, row_scale=0.01, name="tbsm-sel")
+    w = configs.scaled(configs.WORKLOADS["tbsm"], batch=256, row_scale=0.01, hot_frac=0.5, name="tbsm-sel")
     rows = W.table_rows(w)
     n_rows = int(rows.sum())
     table = make_table(w, n_rows)
@@ -245,15 +245,15 @@ def test_empty_batch():
         table.close()
 
 
-def test_large_partition():
-    """More samples than one partition tile (multi-block path)."""
+@pytest.mark.parametrize("n", [1, 1023, 1025, 200_003, 1_300_007])
+def test_partition_sizes(n):
+    """One tile, several 1K tiles, and more than 1M samples (64K tiles)."""
     w = configs.scaled(configs.WORKLOADS["tiny"], batch=1, row_scale=0.1, name="tiny-part")
     rows = W.table_rows(w)
     table = make_table(w, int(rows.sum()))
-    n = 200_003
     hp = HotPath(w, rows, table, 1, n)
     try:
-        f = (np.random.default_rng(3).random(n) < 0.3).astype(np.uint8)
+        f = (np.random.default_rng(n).random(n) < 0.3).astype(np.uint8)
         hp.flags.copy_(torch.from_numpy(f))
         hl.hl_partition(hp.h, hp.flags, n, hp.pop, hp.nonpop, hp.counts, hp.ws)
         c = hp.counts.cpu().numpy()
