@@ -158,12 +158,14 @@ hl_status hl_remap(const hl_handle* h, const uint32_t* gids, int64_t n, int32_t*
 /* ------------------------------------------------------------ cold gather --
  * Working parameters of a mu-batch (Sec. V-A: DMA reads of non-hot rows from
  * CPU memory; dma_rd of the ISA).  Over the lookups of the selected samples
- * whose code is -1: cold_ids_out = their distinct gids, ascending; each such
- * code becomes k_cap + (index in cold_ids_out); staging[u] = w_host[cold_ids[u]]
- * bit for bit (rows read by the GPU over the host link).  n_cold_dev (device)
- * receives the number of cold rows.  If it exceeds staging_cap_rows the call
- * sets HL_DEVERR_CAPACITY and writes nothing but n_cold_dev and workspace.
- * Lookups whose code is neither -1 nor a hot slot are left alone. */
+ * whose code is -1: cold_ids_out = their distinct gids in order of first
+ * occurrence in the mini-batch's lookup (CSR) order, which for a selection in
+ * ascending sample order is the order a stream over the mu-batch meets them;
+ * each such code becomes k_cap + (index in cold_ids_out); staging[u] =
+ * w_host[cold_ids[u]] bit for bit (rows read by the GPU over the host link).
+ * n_cold_dev (device) receives the number of cold rows.  If it exceeds
+ * staging_cap_rows the call sets HL_DEVERR_CAPACITY and writes nothing but
+ * n_cold_dev and workspace.  Lookups whose code is not -1 are left alone. */
 hl_status hl_cold_gather(hl_handle* h, const uint32_t* gids, int32_t* codes, const int32_t* bag_ptr,
                          int32_t n_samples, int32_t bags_per_sample, int64_t n_lookups,
                          const int32_t* sample_ids, const int32_t* n_sel_dev, int32_t n_sel_max,

@@ -194,29 +194,70 @@ void ho_remap(const uint32_t* hot_ids, int64_t n_hot, const uint32_t* gids, int6
 }
 
 /* ------------------------------------------------------------------ 7. cold plan */
-/* Working parameters of a mu-batch (Sec. V-A: DMA reads for non-hot rows).
- * The cold rows are the distinct ids of the selected samples' lookups whose
- * slot is -1, in ascending id order; each such lookup's code becomes
- * k_cap + (position of its id in that list).  sel == NULL selects samples
- * 0..n_sel-1.  Returns the number of cold rows. */
+typedef struct { uint32_t gid; int64_t pos; } cpos_t;
+
+static int cmp_cpos_gid(const void* a, const void* b) {
+    const cpos_t* x = (const cpos_t*)a;
+    const cpos_t* y = (const cpos_t*)b;
+    if (x->gid != y->gid) return (x->gid > y->gid) - (x->gid < y->gid);
+    return (x->pos > y->pos) - (x->pos < y->pos);
+}
+
+static int cmp_cpos_pos(const void* a, const void* b) {
+    const cpos_t* x = (const cpos_t*)a;
+    const cpos_t* y = (const cpos_t*)b;
+    return (x->pos > y->pos) - (x->pos < y->pos);
+}
+
+/* Working parameters of a mu-batch (Sec. V-A: DMA reads for non-hot rows, in
+ * the order the dispatcher streams the mu-batch).  The cold rows are the
+ * distinct ids of the selected samples' lookups whose slot is -1, listed in
+ * order of first occurrence in the mini-batch's CSR lookup order (for a
+ * selection in ascending sample order, as the partition produces, that is the
+ * order a stream over the mu-batch meets them); each such lookup's code
+ * becomes k_cap + (position of its id in that list).  sel == NULL selects
+ * samples 0..n_sel-1.  Returns the number of cold rows. */
 int64_t ho_cold_plan(const uint32_t* gids, int32_t* codes, const int32_t* bag_ptr,
                      const int32_t* sel, int32_t n_sel, int32_t bps, uint32_t k_cap,
                      uint32_t* cold_ids) {
     int64_t m = 0;
     for (int32_t q = 0; q < n_sel; ++q) {
         int64_t b = sel ? sel[q] : q;
-        for (int64_t i = bag_ptr[b * bps]; i < bag_ptr[(b + 1) * bps]; ++i)
-            if (codes[i] == -1) cold_ids[m++] = gids[i];
+        m += bag_ptr[(b + 1) * bps] - bag_ptr[b * bps];
     }
-    qsort(cold_ids, (size_t)m, sizeof(uint32_t), cmp_u32);
-    int64_t u = 0;
-    for (int64_t i = 0; i < m; ++i)
-        if (i == 0 || cold_ids[i] != cold_ids[i - 1]) cold_ids[u++] = cold_ids[i];
+    cpos_t* c = (cpos_t*)malloc(sizeof(cpos_t) * (size_t)(m > 0 ? m : 1));
+    int64_t n = 0;
     for (int32_t q = 0; q < n_sel; ++q) {
         int64_t b = sel ? sel[q] : q;
         for (int64_t i = bag_ptr[b * bps]; i < bag_ptr[(b + 1) * bps]; ++i)
-            if (codes[i] == -1) codes[i] = (int32_t)((int64_t)k_cap + find_u32(cold_ids, u, gids[i]));
+            if (codes[i] == -1) { c[n].gid = gids[i]; c[n].pos = i; ++n; }
     }
+    /* first occurrence of each id: sort by (id, position), keep the first of each run */
+    qsort(c, (size_t)n, sizeof(cpos_t), cmp_cpos_gid);
+    int64_t u = 0;
+    for (int64_t i = 0; i < n; ++i)
+        if (i == 0 || c[i].gid != c[i - 1].gid) c[u++] = c[i];
+    /* list the distinct ids by first position */
+    qsort(c, (size_t)u, sizeof(cpos_t), cmp_cpos_pos);
+    for (int64_t i = 0; i < u; ++i) cold_ids[i] = c[i].gid;
+    /* id -> list position, through an id-sorted copy */
+    cpos_t* byid = (cpos_t*)malloc(sizeof(cpos_t) * (size_t)(u > 0 ? u : 1));
+    for (int64_t i = 0; i < u; ++i) { byid[i].gid = cold_ids[i]; byid[i].pos = i; }
+    qsort(byid, (size_t)u, sizeof(cpos_t), cmp_cpos_gid);
+    for (int32_t q = 0; q < n_sel; ++q) {
+        int64_t b = sel ? sel[q] : q;
+        for (int64_t i = bag_ptr[b * bps]; i < bag_ptr[(b + 1) * bps]; ++i) {
+            if (codes[i] != -1) continue;
+            int64_t lo = 0, hi = u;   /* binary search for the id */
+            while (lo < hi) {
+                int64_t mid = (lo + hi) / 2;
+                if (byid[mid].gid < gids[i]) lo = mid + 1; else hi = mid;
+            }
+            codes[i] = (int32_t)((int64_t)k_cap + byid[lo].pos);
+        }
+    }
+    free(byid);
+    free(c);
     return u;
 }
 

@@ -1,36 +1,55 @@
 // Cold-row gather of a mu-batch: the distinct non-hot rows its lookups need,
-// in ascending id order, fetched from the pinned host table by the GPU over the
-// host link, with the lookups' codes pointed at the staging rows.
+// in order of first occurrence in the mini-batch's lookup order, fetched from
+// the pinned host table by the GPU over the host link, with the lookups'
+// codes pointed at the staging rows.
 //
-//   collect  : (gid, lookup) of every selected lookup with code -1, appended
-//              with one atomic per wave (order irrelevant: the result depends
-//              only on the set of ids)
-//   sort     : radix sort by gid (hl_sort.hip)
-//   unique   : head flags in sorted order, decoupled look-back scan -> the
-//              staging index of every sorted entry, and the count of cold rows
-//   finalize : capacity check, then code rewrite, cold id list and row copy
+//   insert   : every selected lookup with code -1 enters an open-addressing
+//              hash table keyed by row id; a 64-bit atomic min keeps the
+//              smallest lookup index per id; the lookup is also appended to a
+//              list (one atomic per block)
+//   rank     : a scan over all lookups in index order (decoupled look-back)
+//              numbers the first occurrences: staging row u of each id
+//   finalize : capacity check, code rewrite, table clearing, cold id list and
+//              the row copy from host memory
+// The workspace is shared with other calls, so the table is cleared at the
+// start of every call.
 #include "hl_internal.h"
 
-#define CG_UTILE 2048  // 256 threads x 8 items
-#define CG_C_COLLECT 0
+#define CG_C_LIST 0
 #define CG_C_NCOLD 1
-#define CG_C_UTILE 2
+#define CG_C_RTILE 2
 #define CG_C_SNAP 3
+#define CG_RTILE 8192     // lookups per rank tile (512 threads x 16)
+#define CG_MAX_SPB 2048   // selected samples per insert block
+#define CG_FIRST 0x80000000u
 
 struct cg_ws {
-  hl_sort_ws sort;
-  uint32_t* ctr;     // [16]
-  uint32_t* uidx;    // [n_max]
-  uint64_t* ustat;   // [tiles]
-  uint32_t utiles;
+  uint32_t* ctr;      // header counters
+  uint64_t* table;    // [S] (id + 1) << 32 | smallest lookup index; 0 = empty
+  uint32_t* uidx;     // [S] staging row of the id in the slot
+  uint32_t* slotof;   // [n_max] slot of a cold lookup
+  uint32_t* list;     // [n_max] lookup indices of the cold lookups
+  uint32_t* fst;      // [n_max] id of staging row u
+  uint64_t* rstat;    // [rtiles] look-back status of the rank scan
+  uint32_t S, rtiles;
 };
 
+static uint32_t cg_table_slots(uint32_t n_max) {
+  uint32_t s = 1024;
+  while (s < 2u * n_max) s <<= 1;
+  return s;
+}
+
 static void cg_carve(hl_carver& c, cg_ws& ws, uint32_t n_max) {
-  hl_sort_ws_carve(c, ws.sort, n_max);
+  ws.S = cg_table_slots(n_max);
+  ws.rtiles = n_max ? hl_div_up(n_max, CG_RTILE) : 1;
   ws.ctr = c.base ? c.header() + HL_HDR_COLD : nullptr;
-  ws.uidx = c.take<uint32_t>(n_max);
-  ws.utiles = n_max ? hl_div_up(n_max, CG_UTILE) : 1;
-  ws.ustat = c.take<uint64_t>(ws.utiles);
+  ws.table = c.take<uint64_t>(ws.S);
+  ws.uidx = c.take<uint32_t>(ws.S);
+  ws.slotof = c.take<uint32_t>(n_max);
+  ws.list = c.take<uint32_t>(n_max);
+  ws.fst = c.take<uint32_t>(n_max);
+  ws.rstat = c.take<uint64_t>(ws.rtiles);
 }
 
 size_t hl_cold_ws_bytes(const hl_handle* h, int64_t max_lookups) {
@@ -41,23 +60,35 @@ size_t hl_cold_ws_bytes(const hl_handle* h, int64_t max_lookups) {
   return c.off;
 }
 
-// A block owns `spb` selected samples; their lookup ranges are laid end to end
-// in LDS (start, exclusive prefix of lengths) and threads walk the
-// concatenation, finding their sample by binary search.  Candidates are
-// buffered in LDS and appended to the global list with one atomic per block
-// (per flush), which keeps same-address atomics rare.
-#define CG_MAX_SPB 512
-#define CG_BUF 2048
+__device__ __forceinline__ uint32_t cg_hash(uint32_t x) {  // 32-bit finalising mix
+  x ^= x >> 16;
+  x *= 0x85EBCA6Bu;
+  x ^= x >> 13;
+  x *= 0xC2B2AE35u;
+  x ^= x >> 16;
+  return x;
+}
+
+__global__ void __launch_bounds__(256) cg_clear(cg_ws ws) {
+  for (uint32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < ws.S; i += gridDim.x * blockDim.x) ws.table[i] = 0;
+  for (uint32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < ws.rtiles; i += gridDim.x * blockDim.x)
+    ws.rstat[i] = 0;
+}
+
+// A block owns `spb` consecutive selected samples; their lookup ranges are laid
+// end to end in LDS (start, inclusive prefix of lengths) and threads walk the
+// concatenation in rounds of 8 positions per thread, finding their sample by
+// binary search.  Each round issues its loads stage by stage for all 8
+// positions (codes, then ids, then the first hash probe) so that they overlap.
+#define CG_IPT 8
 __global__ void __launch_bounds__(256)
-cg_collect(const uint32_t* __restrict__ gids, const int32_t* __restrict__ codes,
-           const int32_t* __restrict__ bag_ptr, int32_t n_samples, int32_t bps,
-           const int32_t* __restrict__ sample_ids, const int32_t* n_sel_dev, int32_t n_sel_max, int32_t spb,
-           uint64_t n_rows, uint32_t* __restrict__ out_k, uint32_t* __restrict__ out_v, uint32_t n_max,
-           uint32_t* ctr, uint64_t* ustat, uint32_t utiles, uint32_t* err) {
+cg_insert(const uint32_t* __restrict__ gids, const int32_t* __restrict__ codes,
+          const int32_t* __restrict__ bag_ptr, int32_t n_samples, int32_t bps,
+          const int32_t* __restrict__ sample_ids, const int32_t* n_sel_dev, int32_t n_sel_max, int32_t spb,
+          uint64_t n_rows, cg_ws ws, uint32_t n_max, uint32_t* err) {
   __shared__ int32_t st[CG_MAX_SPB], pre[CG_MAX_SPB + 1];
-  __shared__ uint32_t bk[CG_BUF], bv[CG_BUF];
-  __shared__ uint32_t bn, bbase;
-  for (uint32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < utiles; i += gridDim.x * blockDim.x) ustat[i] = 0;
+  __shared__ uint32_t buf[256 * CG_IPT];
+  __shared__ uint32_t bn, bbase, wsum[4];
   int32_t n_sel = n_sel_max;
   if (sample_ids && n_sel_dev) n_sel = min(max(*n_sel_dev, 0), n_sel_max);
   const int64_t q0 = (int64_t)blockIdx.x * spb;
@@ -74,165 +105,221 @@ cg_collect(const uint32_t* __restrict__ gids, const int32_t* __restrict__ codes,
     st[j] = a;
     pre[j + 1] = b - a;
   }
-  if (threadIdx.x == 0) {
-    pre[0] = 0;
-    bn = 0;
+  if (threadIdx.x == 0) pre[0] = 0;
+  __syncthreads();
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  {  // block-wide inclusive scan of the lengths (up to 8 per thread, blocked)
+    const int per = (ns + 255) / 256;
+    uint32_t loc = 0;
+    for (int k = 0; k < per; ++k) {
+      const int j = threadIdx.x * per + k;
+      if (j < ns) loc += (uint32_t)pre[j + 1];
+    }
+    uint32_t inc = loc;
+    for (int o = 1; o < 64; o <<= 1) {
+      const uint32_t t = __shfl_up(inc, o);
+      if (lane >= o) inc += t;
+    }
+    if (lane == 63) wsum[w] = inc;
+    __syncthreads();
+    uint32_t run = inc - loc;
+    for (int j = 0; j < w; ++j) run += wsum[j];
+    for (int k = 0; k < per; ++k) {
+      const int j = threadIdx.x * per + k;
+      if (j < ns) {
+        run += (uint32_t)pre[j + 1];
+        pre[j + 1] = (int32_t)run;
+      }
+    }
   }
   __syncthreads();
-  if (threadIdx.x == 0)
-    for (int j = 0; j < ns; ++j) pre[j + 1] += pre[j];
-  __syncthreads();
   const int32_t total = pre[ns];
-  const int lane = threadIdx.x & 63;
   const uint64_t lt = (1ull << lane) - 1ull;
-  for (int32_t t0 = 0; t0 < total + (int32_t)blockDim.x; t0 += blockDim.x) {
-    // flush when the next chunk might not fit, and once after the last chunk;
-    // the barrier makes every wave see the same buffer fill
-    __syncthreads();
-    const bool last = t0 >= total;
-    if (last || bn + blockDim.x > CG_BUF) {
-      const uint32_t cnt = bn;
-      if (threadIdx.x == 0 && cnt) bbase = atomicAdd(ctr + CG_C_COLLECT, cnt);
-      __syncthreads();
-      if (cnt) {
-        for (uint32_t j = threadIdx.x; j < cnt; j += blockDim.x) {
-          const uint32_t p = bbase + j;
-          if (p < n_max) {  // a sample listed twice could overflow the buffer
-            out_k[p] = bk[j];
-            out_v[p] = bv[j];
-          } else {
-            hl_flag(err, HL_DEVERR_OUT_OF_RANGE);
-          }
+  const uint32_t smask = ws.S - 1;
+  for (int32_t r0 = 0; r0 < total; r0 += 256 * CG_IPT) {
+    if (threadIdx.x == 0) bn = 0;
+    int32_t idx[CG_IPT];
+    int32_t cd[CG_IPT];
+    uint32_t g[CG_IPT], slot[CG_IPT];
+    uint64_t cur[CG_IPT];
+#pragma unroll
+    for (int k = 0; k < CG_IPT; ++k) {
+      const int32_t t = r0 + k * 256 + threadIdx.x;
+      idx[k] = -1;
+      if (t < total) {
+        int a = 0, b = ns;
+        while (b - a > 1) {
+          int m = (a + b) >> 1;
+          if (pre[m] <= t) a = m; else b = m;
         }
-      }
-      __syncthreads();
-      if (threadIdx.x == 0) bn = 0;
-      __syncthreads();
-    }
-    if (last) break;
-    const int32_t t = t0 + threadIdx.x;
-    bool take = false;
-    uint32_t g = 0;
-    int32_t i = 0;
-    if (t < total) {
-      int a = 0, b = ns;
-      while (b - a > 1) {
-        int m = (a + b) >> 1;
-        if (pre[m] <= t) a = m; else b = m;
-      }
-      i = st[a] + (t - pre[a]);
-      if (codes[i] == -1) {
-        g = gids[i];
-        if (g < n_rows) take = true;
-        else hl_flag(err, HL_DEVERR_OUT_OF_RANGE);
+        idx[k] = st[a] + (t - pre[a]);
       }
     }
-    const uint64_t m = __ballot(take);
-    if (m) {
-      uint32_t base = 0;
-      if (lane == 0) base = atomicAdd(&bn, (uint32_t)__popcll(m));
-      base = __shfl(base, 0);
-      if (take) {
-        const uint32_t p = base + (uint32_t)__popcll(m & lt);
-        bk[p] = g;
-        bv[p] = (uint32_t)i;
+#pragma unroll
+    for (int k = 0; k < CG_IPT; ++k) cd[k] = idx[k] >= 0 ? codes[idx[k]] : 0;
+#pragma unroll
+    for (int k = 0; k < CG_IPT; ++k) g[k] = (idx[k] >= 0 && cd[k] == -1) ? gids[idx[k]] : 0xFFFFFFFFu;
+#pragma unroll
+    for (int k = 0; k < CG_IPT; ++k) {
+      if (idx[k] >= 0 && cd[k] == -1 && g[k] >= n_rows) hl_flag(err, HL_DEVERR_OUT_OF_RANGE);
+      slot[k] = cg_hash(g[k]) & smask;
+      cur[k] = g[k] < n_rows ? ws.table[slot[k]] : 0ull;
+    }
+    bool take[CG_IPT];
+#pragma unroll
+    for (int k = 0; k < CG_IPT; ++k) {
+      take[k] = g[k] < n_rows;
+      if (!take[k]) continue;
+      const uint64_t want = ((uint64_t)(g[k] + 1) << 32) | (uint32_t)idx[k];
+      uint64_t c = cur[k];
+      for (uint32_t probe = 0; probe <= smask; ++probe) {
+        if ((c >> 32) == 0) {
+          c = atomicCAS((unsigned long long*)(ws.table + slot[k]), 0ull, (unsigned long long)want);
+          if (c == 0) break;
+        }
+        if ((uint32_t)(c >> 32) == g[k] + 1) {
+          atomicMin((unsigned long long*)(ws.table + slot[k]), (unsigned long long)want);
+          break;
+        }
+        slot[k] = (slot[k] + 1) & smask;
+        c = ws.table[slot[k]];
+      }
+      ws.slotof[idx[k]] = slot[k];
+    }
+    __syncthreads();  // bn reset visible
+#pragma unroll
+    for (int k = 0; k < CG_IPT; ++k) {
+      const uint64_t m = __ballot(take[k]);
+      if (m) {
+        uint32_t base = 0;
+        if (lane == 0) base = atomicAdd(&bn, (uint32_t)__popcll(m));
+        base = __shfl(base, 0);
+        if (take[k]) buf[base + (uint32_t)__popcll(m & lt)] = (uint32_t)idx[k];
       }
     }
+    __syncthreads();
+    const uint32_t cnt = bn;
+    if (threadIdx.x == 0 && cnt) bbase = atomicAdd(ws.ctr + CG_C_LIST, cnt);
+    __syncthreads();
+    for (uint32_t j = threadIdx.x; j < cnt; j += blockDim.x) {
+      const uint32_t p = bbase + j;
+      if (p < n_max) ws.list[p] = buf[j];
+      else hl_flag(err, HL_DEVERR_OUT_OF_RANGE);  // a sample listed twice
+    }
+    __syncthreads();
   }
 }
 
-__global__ void __launch_bounds__(256)
-cg_unique(const uint32_t* __restrict__ keys, uint32_t* ctr, uint32_t n_host, uint64_t* ustat,
-          uint32_t* __restrict__ uidx, int32_t* n_cold_dev, uint32_t epoch, uint32_t* err) {
-  __shared__ uint32_t s_tile, wt[4];
+// Scan over the mini-batch's lookups in index order.  Lookup i is a first
+// occurrence iff it is a cold lookup of this call whose slot holds (its id,
+// i); the running count of first occurrences numbers the staging rows.  Tiles
+// of 8192 lookups (512 threads x 16), so one look-back window reaches tile 0.
+#define CG_RT_THREADS 512
+#define CG_RT_ITEMS 16
+__global__ void __launch_bounds__(CG_RT_THREADS)
+cg_rank(const uint32_t* __restrict__ gids, const int32_t* __restrict__ codes, uint32_t n_lookups, cg_ws ws,
+        int32_t* n_cold_dev, uint32_t epoch, uint32_t* err) {
+  __shared__ uint32_t s_tile, wt[CG_RT_THREADS / 64], s_excl;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  if (tid == 0) s_tile = atomicInc(ctr + CG_C_UTILE, gridDim.x - 1);
+  if (tid == 0) s_tile = atomicInc(ws.ctr + CG_C_RTILE, gridDim.x - 1);
   __syncthreads();
-  const uint32_t n = min(__hip_atomic_load(ctr + CG_C_COLLECT, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT), n_host);
   const uint32_t tile = s_tile;
-  if (n == 0) {
+  if (tile == 0 && tid == 0) ws.ctr[CG_C_SNAP] = ws.ctr[CG_C_LIST];
+  if (n_lookups == 0) {
     if (tile == 0 && tid == 0) {
-      ctr[CG_C_NCOLD] = 0;
-      ctr[CG_C_SNAP] = 0;
+      ws.ctr[CG_C_NCOLD] = 0;
       *n_cold_dev = 0;
     }
     return;
   }
-  const uint64_t tb = (uint64_t)tile * CG_UTILE;
-  if (tb >= n) return;
+  const uint64_t tb = (uint64_t)tile * CG_RTILE;
+  if (tb >= n_lookups) return;
   const uint64_t lt = (1ull << lane) - 1ull;
-  bool hd[8];
+  bool first[CG_RT_ITEMS];
+  int32_t cd[CG_RT_ITEMS];
+  uint32_t slot[CG_RT_ITEMS], g[CG_RT_ITEMS];
+#pragma unroll
+  for (int k = 0; k < CG_RT_ITEMS; ++k) {
+    const uint64_t i = tb + (uint64_t)w * (64 * CG_RT_ITEMS) + k * 64 + lane;
+    cd[k] = i < n_lookups ? codes[i] : 0;
+  }
+#pragma unroll
+  for (int k = 0; k < CG_RT_ITEMS; ++k) {
+    const uint64_t i = tb + (uint64_t)w * (64 * CG_RT_ITEMS) + k * 64 + lane;
+    slot[k] = cd[k] == -1 ? ws.slotof[i] : 0xFFFFFFFFu;
+    g[k] = cd[k] == -1 ? gids[i] : 0u;
+  }
   uint32_t wsum = 0;
 #pragma unroll
-  for (int k = 0; k < 8; ++k) {
-    const uint64_t idx = tb + (uint64_t)w * 512 + k * 64 + lane;
-    bool h = false;
-    if (idx < n) h = idx == 0 || keys[idx] != keys[idx - 1];
-    hd[k] = h;
-    wsum += (uint32_t)__popcll(__ballot(h));
+  for (int k = 0; k < CG_RT_ITEMS; ++k) {
+    const uint64_t i = tb + (uint64_t)w * (64 * CG_RT_ITEMS) + k * 64 + lane;
+    bool f = false;
+    if (slot[k] < ws.S)  // a slot from an earlier call fails the test below
+      f = ws.table[slot[k]] == (((uint64_t)(g[k] + 1) << 32) | (uint32_t)i);
+    first[k] = f;
+    wsum += (uint32_t)__popcll(__ballot(f));
   }
   if (lane == 0) wt[w] = wsum;
   __syncthreads();
   uint32_t before = 0, tc = 0;
-  for (int j = 0; j < 4; ++j) {
+  for (int j = 0; j < CG_RT_THREADS / 64; ++j) {
     if (j < w) before += wt[j];
     tc += wt[j];
   }
-  __shared__ uint32_t s_excl;
   if (tid == 0) {
-    uint64_t* st = ustat;
-    hl_st_store(st + tile, hl_st_pack(epoch, tile == 0 ? HL_ST_PRE : HL_ST_AGG, tc));
+    hl_st_store(ws.rstat + tile, hl_st_pack(epoch, tile == 0 ? HL_ST_PRE : HL_ST_AGG, tc));
     uint32_t ex = 0;
     if (tile > 0) {
-      ex = hl_lookback(st, tile, 1, epoch, err);
-      hl_st_store(st + tile, hl_st_pack(epoch, HL_ST_PRE, ex + tc));
+      ex = hl_lookback(ws.rstat, tile, 1, epoch, err);
+      hl_st_store(ws.rstat + tile, hl_st_pack(epoch, HL_ST_PRE, ex + tc));
     }
     s_excl = ex;
   }
   __syncthreads();
   uint32_t run = s_excl + before;
 #pragma unroll
-  for (int k = 0; k < 8; ++k) {
-    const uint64_t idx = tb + (uint64_t)w * 512 + k * 64 + lane;
-    const uint64_t m = __ballot(hd[k]);
-    const uint32_t incl = run + (uint32_t)__popcll(m & lt) + (hd[k] ? 1u : 0u);
-    if (idx < n) uidx[idx] = incl - 1;
-    if (idx == (uint64_t)n - 1) {
-      ctr[CG_C_NCOLD] = incl;
-      ctr[CG_C_SNAP] = n;
-      *n_cold_dev = (int32_t)incl;
+  for (int k = 0; k < CG_RT_ITEMS; ++k) {
+    const uint64_t i = tb + (uint64_t)w * (64 * CG_RT_ITEMS) + k * 64 + lane;
+    const uint64_t m = __ballot(first[k]);
+    if (first[k]) {
+      const uint32_t u = run + (uint32_t)__popcll(m & lt);
+      ws.uidx[slot[k]] = u;
+      ws.fst[u] = g[k];
     }
     run += (uint32_t)__popcll(m);
+    if (i == (uint64_t)n_lookups - 1) {
+      ws.ctr[CG_C_NCOLD] = run;
+      *n_cold_dev = (int32_t)run;
+    }
   }
 }
 
-// Units of `U` bytes: thread (entry e, unit c).  Unit 0 of an entry rewrites the
-// lookup's code; heads (first entry of each id) also record the id and copy
-// their row from the host table.
+// Part (a): every listed cold lookup points its code at its staging row.
+// Part (b): thread (u, unit) copies one unit of row u.
 template <typename V>
 __global__ void __launch_bounds__(256)
-cg_finalize(const uint32_t* __restrict__ keys, const uint32_t* __restrict__ vals,
-            const uint32_t* __restrict__ uidx, uint32_t* ctr, int32_t cap, uint32_t k_cap,
-            int32_t* __restrict__ codes, uint32_t* __restrict__ cold_ids, const V* __restrict__ src,
-            V* __restrict__ dst, uint32_t upr, uint32_t* err) {
-  const uint32_t n = ctr[CG_C_SNAP], ncold = ctr[CG_C_NCOLD];
-  if (blockIdx.x == 0 && threadIdx.x == 0) ctr[CG_C_COLLECT] = 0;  // ready for the next call
-  if (ncold > (uint32_t)cap) {
-    if (blockIdx.x == 0 && threadIdx.x == 0) hl_flag(err, HL_DEVERR_CAPACITY);
-    return;
+cg_finalize(cg_ws ws, uint32_t n_max, int32_t cap, uint32_t k_cap, int32_t* __restrict__ codes,
+            uint32_t* __restrict__ cold_ids, const V* __restrict__ src, V* __restrict__ dst, uint32_t upr,
+            uint32_t* err) {
+  const uint32_t n_list = min(ws.ctr[CG_C_SNAP], n_max), ncold = ws.ctr[CG_C_NCOLD];
+  const bool fits = ncold <= (uint32_t)cap;
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    ws.ctr[CG_C_LIST] = 0;  // ready for the next call
+    if (!fits) hl_flag(err, HL_DEVERR_CAPACITY);
   }
-  const uint64_t total = (uint64_t)n * upr;
-  for (uint64_t t = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; t < total;
-       t += (uint64_t)gridDim.x * blockDim.x) {
-    const uint32_t e = (uint32_t)(t / upr), c = (uint32_t)(t - (uint64_t)e * upr);
-    const uint32_t g = keys[e];
-    const bool head = e == 0 || keys[e - 1] != g;
-    const uint32_t u = uidx[e];
-    if (c == 0) {
-      codes[vals[e]] = (int32_t)(k_cap + u);
-      if (head) cold_ids[u] = g;
-    }
-    if (head) dst[(uint64_t)u * upr + c] = src[(uint64_t)g * upr + c];
+  const uint64_t gs = (uint64_t)gridDim.x * blockDim.x, t0 = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  for (uint64_t e = t0; e < n_list; e += gs) {
+    const uint32_t i = ws.list[e];
+    const uint32_t sl = ws.slotof[i];
+    if (fits) codes[i] = (int32_t)(k_cap + ws.uidx[sl]);
+  }
+  if (!fits) return;
+  const uint64_t total = (uint64_t)ncold * upr;
+  for (uint64_t t = t0; t < total; t += gs) {
+    const uint32_t u = (uint32_t)(t / upr), c = (uint32_t)(t - (uint64_t)u * upr);
+    const uint32_t g = ws.fst[u];
+    if (c == 0) cold_ids[u] = g;
+    dst[(uint64_t)u * upr + c] = src[(uint64_t)g * upr + c];
   }
 }
 
@@ -254,29 +341,23 @@ extern "C" hl_status hl_cold_gather(hl_handle* h, const uint32_t* gids, int32_t*
   cg_ws ws;
   cg_carve(c, ws, (uint32_t)n_lookups);
   const uint32_t n_max = (uint32_t)n_lookups;
-  int64_t spb = n_lookups > 0 && n_samples > 0 ? (512ll * n_samples + n_lookups - 1) / n_lookups : CG_MAX_SPB;
+  // about 2048 lookups per insert block
+  int64_t spb = n_lookups > 0 && n_samples > 0 ? (2048ll * n_samples + n_lookups - 1) / n_lookups : CG_MAX_SPB;
   spb = spb < 1 ? 1 : (spb > CG_MAX_SPB ? CG_MAX_SPB : spb);
-  const uint32_t cblocks = n_sel_max > 0 ? hl_div_up(n_sel_max, spb) : 1;
-  HL_KERNEL(h, s, "cg_collect", cg_collect, dim3(cblocks), dim3(256), 0, s, gids, codes, bag_ptr, n_samples, bps, sample_ids,
-                     n_sel_dev, n_sel_max, (int32_t)spb, h->n_rows, ws.sort.k0, ws.sort.v0, n_max, ws.ctr, ws.ustat,
-                     ws.utiles, h->d_err);
-  HL_LAUNCHED();
-  uint32_t *sk, *sv;
-  hl_status st = hl_sort_pairs(h, ws.sort, ws.ctr + CG_C_COLLECT, n_max, hl_bit_width(h->n_rows), s, &sk, &sv);
-  if (st != HL_OK) return st;
+  const uint32_t iblocks = n_sel_max > 0 ? hl_div_up(n_sel_max, spb) : 1;
+  uint32_t cb = hl_div_up(ws.S, 256 * 4);
+  HL_KERNEL(h, s, "cg_clear", cg_clear, dim3(cb), dim3(256), 0, s, ws);
+  HL_KERNEL(h, s, "cg_insert", cg_insert, dim3(iblocks), dim3(256), 0, s, gids, codes, bag_ptr, n_samples, bps,
+            sample_ids, n_sel_dev, n_sel_max, (int32_t)spb, h->n_rows, ws, n_max, h->d_err);
   const uint32_t epoch = hl_next_epoch(h);
-  const uint32_t ut = n_max ? hl_div_up(n_max, CG_UTILE) : 1;
-  HL_KERNEL(h, s, "cg_unique", cg_unique, dim3(ut), dim3(256), 0, s, sk, ws.ctr, n_max, ws.ustat, ws.uidx, n_cold_dev,
-                     epoch, h->d_err);
+  HL_KERNEL(h, s, "cg_rank", cg_rank, dim3(ws.rtiles), dim3(CG_RT_THREADS), 0, s, gids, codes, n_max, ws, n_cold_dev, epoch,
+            h->d_err);
   const uint32_t rb = h->row_bytes;
-  uint64_t total;
-  uint32_t g;
-#define CG_FIN(V)                                                                                      \
-  total = (uint64_t)(n_max ? n_max : 1) * (rb / sizeof(V));                                            \
-  g = hl_div_up(total, 256);                                                                           \
-  if (g > 8192) g = 8192;                                                                              \
-  HL_KERNEL(h, s, "cg_finalize", cg_finalize<V>, dim3(g), dim3(256), 0, s, sk, sv, ws.uidx, ws.ctr, cap, h->k_cap, \
-                     codes, cold_ids_out, (const V*)w_host, (V*)staging, (uint32_t)(rb / sizeof(V)), h->d_err);
+  uint32_t g = hl_div_up((uint64_t)(n_max ? n_max : 1) * (rb / 4), 256);
+  if (g > 8192) g = 8192;
+#define CG_FIN(V)                                                                                     \
+  HL_KERNEL(h, s, "cg_finalize", cg_finalize<V>, dim3(g), dim3(256), 0, s, ws, n_max, cap, h->k_cap, codes, \
+            cold_ids_out, (const V*)w_host, (V*)staging, (uint32_t)(rb / sizeof(V)), h->d_err);
   if (rb % 16 == 0) { CG_FIN(uint4) }
   else if (rb % 8 == 0) { CG_FIN(uint2) }
   else if (rb % 4 == 0) { CG_FIN(uint32_t) }

@@ -131,10 +131,14 @@ struct hl_sort_ws {
   uint32_t n_max;
 };
 
-#define HL_SORT_BLOCK 256
+#define HL_SORT_BLOCK 512
+#define HL_SORT_WAVES (HL_SORT_BLOCK / 64)
+#ifndef HL_SORT_ITEMS
 #define HL_SORT_ITEMS 16
+#endif
 #define HL_SORT_TILE (HL_SORT_BLOCK * HL_SORT_ITEMS)
-#define HL_SORT_HIST_BLOCKS 32
+#define HL_SORT_HIST_BLOCKS 16
+#define HL_SORT_HIST_THREADS 1024
 
 void hl_sort_ws_carve(hl_carver& c, hl_sort_ws& ws, uint32_t n_max);
 // Sorts ws.k0/ws.v0 (first *n_dev items if n_dev != NULL, else n_host) by the
@@ -150,7 +154,9 @@ hl_status hl_sort_pairs(hl_handle* h, hl_sort_ws& ws, const uint32_t* n_dev, uin
 #define HL_ST_AGG 1ull
 #define HL_ST_PRE 2ull
 #define HL_SPIN_LIMIT (1u << 24)
+#ifndef HL_LB_WIN
 #define HL_LB_WIN 32
+#endif
 
 __device__ __forceinline__ uint64_t hl_st_pack(uint32_t epoch, uint64_t flag, uint32_t v) {
   return ((uint64_t)epoch << 32) | (flag << 30) | (uint64_t)(v & 0x3FFFFFFFu);

@@ -27,7 +27,8 @@ import oracle as O
 #   sample 2 -> (3, 0) -> {3, 4}.
 #   counts: id1 = 2, id4 = 2, id3 = 1, id6 = 1.
 #   K = 2: hot = {1, 4} (slots 0, 1); only sample 0 is all-hot -> O = [0], X = [1, 2].
-#   slots: s0 (0, 1), s1 (0, -1), s2 (-1, 1); cold ids of X = [3, 6] -> codes 2, 3.
+#   slots: s0 (0, 1), s1 (0, -1), s2 (-1, 1); cold ids of X in order of first
+#   occurrence (s1's id 6, then s2's id 3) = [6, 3] -> codes 2, 3.
 #   pooled (one row per bag): the rows themselves.
 #   dY per bag (1,0) (0,1) (1,1) (2,0) (0,-1) (1,1), lr = 0.5:
 #   G(id1) = (1,0)+(1,1) = (2,1) -> (3,4) - (1,0.5) = (2, 3.5)
@@ -35,7 +36,7 @@ import oracle as O
 #   G(id3) = (0,-1)              -> (7,8) - (0,-0.5) = (7, 8.5)
 #   G(id6) = (2,0)               -> (2,2) - (1,0)    = (1, 2)
 #   K = 1: the tie id1/id4 at count 2 goes to the smaller id -> hot = {1}; no
-#   sample is all-hot; cold ids = [3, 4, 6].
+#   sample is all-hot; cold ids by first occurrence = [4, 6, 3].
 HAND_ROWS_PER_TABLE = np.array([4, 3], np.uint32)
 HAND_TABLE = np.array([[1, 2], [3, 4], [5, 6], [7, 8], [-1, 0], [0, -1], [2, 2]], np.float32)
 HAND_ROWS = np.array([1, 0, 1, 2, 3, 0], np.uint32)
@@ -69,10 +70,10 @@ def test_hand_example_k2(dtype):
     codes0 = O.remap(hot, g)
     assert codes0.tolist() == [0, 1, 0, -1, -1, 1]
     cold, codes = O.cold_plan(g, codes0, HAND_PTR, nonpop, 2, 2, 2)
-    assert cold.tolist() == [3, 6] and codes.tolist() == [0, 1, 0, 3, 2, 1]
+    assert cold.tolist() == [6, 3] and codes.tolist() == [0, 1, 0, 2, 3, 1]
     table = _table(dtype)
     w_hot, stg = O.gather(table, hot), O.gather(table, cold)
-    assert _as_f64(stg, dtype).tolist() == [[7, 8], [2, 2]]
+    assert _as_f64(stg, dtype).tolist() == [[2, 2], [7, 8]]
     out, _, rc = O.embbag_fwd(dtype, w_hot, 2, stg, codes, HAND_PTR, None, 3, 2, 6)
     assert rc == 0
     assert out.tolist() == [[3, 4], [-1, 0], [3, 4], [2, 2], [7, 8], [-1, 0]]
@@ -80,7 +81,7 @@ def test_hand_example_k2(dtype):
                                        want_scale=True)
     assert rc == 0 and uniq.tolist() == [0, 1, 2, 3]
     assert _as_f64(w_hot, dtype).tolist() == [[2, 3.5], [-1.5, -1]]
-    assert _as_f64(stg, dtype).tolist() == [[7, 8.5], [1, 2]]
+    assert _as_f64(stg, dtype).tolist() == [[1, 2], [7, 8.5]]
     # error scale |row| + lr * sum|dY| for code 0 (id 1): (3 + 0.5*2, 4 + 0.5*1)
     assert scale[0].tolist() == [4.0, 4.5]
 
@@ -94,7 +95,8 @@ def test_hand_example_k1_tie_and_multihot():
     pop, nonpop = O.partition(flags)
     assert pop.tolist() == [] and nonpop.tolist() == [0, 1, 2]
     cold, codes = O.cold_plan(g, O.remap(hot, g), HAND_PTR, nonpop, 3, 2, 1)
-    assert cold.tolist() == [3, 4, 6]
+    assert cold.tolist() == [4, 6, 3]
+    assert codes.tolist() == [0, 1, 0, 2, 3, 1]
     # multi-hot bag {id1, id1, id2} pools to (3+3+5, 4+4+6)
     out = O.embbag_fwd_flat("f32", HAND_TABLE, np.array([1, 1, 2], np.uint32), np.array([0, 3], np.int32))
     assert out.tolist() == [[11, 14]]
@@ -184,8 +186,11 @@ def test_tiny_brute_force(seed):
                 assert hot[codes0[i]] == gi
         k_cap = max(k, 1)
         cold, codes = O.cold_plan(g, codes0, ptr, nonpop, len(nonpop), bps, k_cap)
-        cold_ref = sorted({g[i] for b in nonpop for i in range(ptr[b * bps], ptr[(b + 1) * bps])
-                           if g[i] not in H})
+        cold_ref = []
+        for b in nonpop:                       # first occurrence, streaming the mu-batch
+            for i in range(ptr[b * bps], ptr[(b + 1) * bps]):
+                if g[i] not in H and g[i] not in cold_ref:
+                    cold_ref.append(int(g[i]))
         assert cold.tolist() == cold_ref
         for i in range(len(g)):
             if codes[i] >= k_cap:

@@ -263,3 +263,65 @@ def test_partition_sizes(n):
     finally:
         hp.close()
         table.close()
+
+
+@pytest.mark.parametrize("name", ["dlrm-large", "multi-hot", "tbsm"])
+def test_multi_step(name):
+    """Several consecutive steps with one workspace and one hot cache (the hot
+    cache carries the updates from step to step).  Every step is checked against
+    the oracle run from the same pre-step state (the oracle's hot cache takes the
+    GPU's after each comparison), to the single-step tolerances."""
+    import oracle as O
+    from parity_lib import check_close
+    w = configs.scaled(configs.WORKLOADS[name], batch=600, row_scale=0.004, name=name + "-steps")
+    rows = W.table_rows(w)
+    n_rows = int(rows.sum())
+    k_cap = w.k_cap(n_rows)
+    rtol = {"f32": 1e-5, "bf16": 1e-2}[w.dtype]
+    table = make_table(w, n_rows)
+    prof = [W.make_batch(w, rows, i) for i in range(4)]
+    steps = [W.make_batch(w, rows, 4 + s) for s in range(4)]
+    hp = HotPath(w, rows, table, max(b.n_lookups for b in prof + steps), w.batch)
+    try:
+        hp.learn([to_device(p, "cuda") for p in prof])
+        counts = np.zeros(n_rows, np.uint32)
+        for p in prof:
+            O.count(n_rows, [O.gids(rows, p.rows, p.bag_ptr)[0]], counts)
+        hot = O.topk(counts, k_cap)
+        assert np.array_equal(hp.hot_ids[:hp.n_hot].cpu().numpy().view(np.uint32), hot)
+        w_hot = O.gather(table.array, hot)
+        for si, mb in enumerate(steps):
+            pre = hp.w_hot[:len(hot)].cpu().numpy().copy()
+            assert si > 0 or np.array_equal(pre.view(np.uint8), w_hot.view(np.uint8))
+            w_hot = pre.copy()
+            dY = W.make_dy(w, 4 + si, mb.n_bags)
+            hp.step(to_device(mb, "cuda", dY))
+            torch.cuda.synchronize()
+            assert hp.device_error() == 0, f"step {si}"
+            B, bps, L = mb.n_samples, mb.bags_per_sample, mb.n_lookups
+            g, _ = O.gids(rows, mb.rows, mb.bag_ptr)
+            flags = O.classify(hot, g, mb.bag_ptr, B, bps)
+            pop, nonpop = O.partition(flags)
+            cold, codes = O.cold_plan(g, O.remap(hot, g), mb.bag_ptr, nonpop, len(nonpop), bps, k_cap)
+            stg = O.gather(table.array, cold)
+            out, sc, _ = O.embbag_fwd(w.dtype, w_hot, k_cap, stg, codes, mb.bag_ptr, None, B, bps, B * bps,
+                                      want_scale=True)
+            assert np.array_equal(hp.flags[:B].cpu().numpy(), flags), f"step {si} flags"
+            assert np.array_equal(hp.codes[:L].cpu().numpy(), codes), f"step {si} codes"
+            n_cold = int(hp.n_cold.item())
+            assert np.array_equal(hp.cold_ids[:n_cold].cpu().numpy().view(np.uint32), cold), f"step {si} cold ids"
+            check_close(hp.out[:B * bps].cpu().numpy(), out, sc, 1e-5, f"step {si} pooled output")
+            uniq, usc, _ = O.embbag_bwd_sgd(w.dtype, w_hot, k_cap, stg, codes, mb.bag_ptr, None, B, bps, dY, w.lr,
+                                            want_scale=True)
+            hu = uniq < k_cap
+            gw = hp.w_hot[:len(hot)].cpu().numpy()
+            gst = hp.staging[:n_cold].cpu().numpy()
+            check_close(as_f64(gw[uniq[hu]], w.dtype), as_f64(w_hot[uniq[hu]], w.dtype), usc[hu], rtol,
+                        f"step {si} hot rows")
+            ts = uniq[~hu] - k_cap
+            check_close(as_f64(gst[ts], w.dtype), as_f64(stg[ts], w.dtype), usc[~hu], rtol, f"step {si} staging rows")
+            untouched = np.setdiff1d(np.arange(len(hot)), uniq[hu])
+            assert np.array_equal(gw[untouched].view(np.uint8), pre[untouched].view(np.uint8)), f"step {si}"
+    finally:
+        hp.close()
+        table.close()
