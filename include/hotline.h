@@ -83,8 +83,9 @@ uint32_t hl_k_cap(const hl_handle* h);
 /* Workspace bytes for calls with up to max_lookups lookups, max_bags bags and
  * max_samples samples.  A workspace must be zero-filled once before its first
  * use (hl_workspace_init, or any zero fill) and then belongs to this handle;
- * the calls keep it reusable.  Used by hl_partition, hl_cold_gather and
- * hl_embbag_bwd_sgd (never two of them concurrently). */
+ * the calls keep it reusable.  Used by hl_partition, hl_cold_plan /
+ * hl_cold_gather and hl_embbag_bwd_plan / _apply / _sgd, never two of them
+ * concurrently; hl_cold_fetch and hl_cold_scatter do not touch it. */
 size_t hl_workspace_bytes(const hl_handle* h, int64_t max_lookups, int64_t max_bags,
                           int32_t max_samples);
 hl_status hl_workspace_init(void* workspace, size_t bytes, hl_stream stream);
@@ -147,7 +148,7 @@ hl_status hl_classify(const hl_handle* h, const uint32_t* gids, const int32_t* b
  * O u X = M and O n X = {} (Sec. IV-A, Eq. 3): pop_ids = ascending samples with
  * flag 1, nonpop_ids = ascending samples with flag 0 (each list sized
  * n_samples).  counts_dev[0] = |O|, counts_dev[1] = |X| (device). */
-hl_status hl_partition(const hl_handle* h, const uint8_t* flags, int32_t n_samples, int32_t* pop_ids,
+hl_status hl_partition(hl_handle* h, const uint8_t* flags, int32_t n_samples, int32_t* pop_ids,
                        int32_t* nonpop_ids, int32_t* counts_dev, void* workspace, size_t ws_bytes,
                        hl_stream stream);
 
@@ -172,6 +173,34 @@ hl_status hl_cold_gather(hl_handle* h, const uint32_t* gids, int32_t* codes, con
                          const void* w_host, void* staging, int32_t staging_cap_rows,
                          uint32_t* cold_ids_out, int32_t* n_cold_dev, void* workspace,
                          size_t ws_bytes, hl_stream stream);
+
+/* The two halves of hl_cold_gather, for the paper's pipeline (Sec. IV and the
+ * pipeline figure: the working parameters of the non-popular mu-batch are
+ * gathered while the popular mu-batch runs).  hl_cold_plan does everything
+ * but the row copy: cold_ids_out, n_cold_dev and the code rewrite, with the
+ * same capacity rule.  hl_cold_fetch then copies staging[u] =
+ * w_host[cold_ids[u]] for u < *n_cold_dev (device count); it reads only its
+ * arguments, not the workspace, so once the plan has completed it may run on
+ * another stream concurrently with any other call except those that write
+ * cold_ids, n_cold_dev or staging.  A count above staging_cap_rows copies
+ * nothing and sets HL_DEVERR_CAPACITY; an id >= n_rows is skipped and sets
+ * HL_DEVERR_OUT_OF_RANGE. */
+hl_status hl_cold_plan(hl_handle* h, const uint32_t* gids, int32_t* codes, const int32_t* bag_ptr,
+                       int32_t n_samples, int32_t bags_per_sample, int64_t n_lookups,
+                       const int32_t* sample_ids, const int32_t* n_sel_dev, int32_t n_sel_max,
+                       int32_t staging_cap_rows, uint32_t* cold_ids_out, int32_t* n_cold_dev,
+                       void* workspace, size_t ws_bytes, hl_stream stream);
+hl_status hl_cold_fetch(hl_handle* h, const uint32_t* cold_ids, const int32_t* n_cold_dev,
+                        int32_t staging_cap_rows, const void* w_host, void* staging, hl_stream stream);
+
+/* Write-back of the updated working parameters (Sec. IV: non-hot rows are
+ * updated in CPU main memory by DMA; dma_wr of the ISA): w_host[cold_ids[u]] =
+ * staging[u] bit for bit, for u < *n_cold_dev, over the host link.  The ids
+ * must be distinct (hl_cold_plan's are).  Same count and id rules as
+ * hl_cold_fetch; reads no workspace. */
+hl_status hl_cold_scatter(hl_handle* h, const uint32_t* cold_ids, const int32_t* n_cold_dev,
+                          int32_t staging_cap_rows, const void* staging, void* w_host,
+                          hl_stream stream);
 
 /* -------------------------------------------------------------- embedding --
  * Sum pooling (Sec. V-D Reducer, sparse-length element-wise sum; v_add of the
@@ -199,6 +228,26 @@ hl_status hl_embbag_bwd_sgd(hl_handle* h, void* w_hot, void* staging, int32_t st
                             int32_t bags_per_sample, int64_t n_lookups, const int32_t* sample_ids,
                             const int32_t* n_sel_dev, int32_t n_sel_max, const float* dY, float lr,
                             void* workspace, size_t ws_bytes, hl_stream stream);
+
+/* The two halves of hl_embbag_bwd_sgd.  hl_embbag_bwd_plan groups the
+ * selected lookups by code (it reads codes and bag_ptr only, not the rows or
+ * dY) and leaves the grouping in the workspace; hl_embbag_bwd_apply reduces dY
+ * over each group and updates the rows.  The plan can therefore run while the
+ * working parameters are still being fetched and the forwards still read the
+ * rows; the apply must come after both forwards (they read the pre-update
+ * rows, Sec. IV-A Eq. 5) and after the fetch.  The apply takes the plan's
+ * staging_rows, n_samples, bags_per_sample and n_lookups and the same
+ * workspace, with no other call on that workspace in between; otherwise it
+ * returns HL_ERR_INVALID_ARG and changes nothing.  Applying one plan twice is
+ * two SGD steps with the same grouping. */
+hl_status hl_embbag_bwd_plan(hl_handle* h, int32_t staging_rows, const int32_t* codes,
+                             const int32_t* bag_ptr, int32_t n_samples, int32_t bags_per_sample,
+                             int64_t n_lookups, const int32_t* sample_ids, const int32_t* n_sel_dev,
+                             int32_t n_sel_max, void* workspace, size_t ws_bytes, hl_stream stream);
+hl_status hl_embbag_bwd_apply(hl_handle* h, void* w_hot, void* staging, int32_t staging_rows,
+                              int32_t n_samples, int32_t bags_per_sample, int64_t n_lookups,
+                              const float* dY, float lr, void* workspace, size_t ws_bytes,
+                              hl_stream stream);
 
 /* ----------------------------------------------------------------- errors --
  * Waits for the device, returns the error word (HL_DEVERR_* bits) in *err_out

@@ -47,6 +47,7 @@ def lib():
             "ho_remap": (None, [P, i64, P, i64, P]),
             "ho_cold_plan": (i64, [P, P, P, P, i32, i32, u32, P]),
             "ho_gather": (None, [P, u64, P, i64, P]),
+            "ho_scatter": (None, [P, u64, P, i64, P]),
             "ho_embbag_fwd": (C.c_int, [i32, i32, P, u32, i64, P, i64, P, P, P, i32, i32, P, P]),
             "ho_embbag_fwd_flat": (None, [i32, i32, P, P, P, i64, P]),
             "ho_embbag_bwd_sgd": (i64, [i32, i32, P, u32, i64, P, i64, P, P, P, i32, i32, P, f32,
@@ -151,6 +152,15 @@ def gather(table, ids):
     return out
 
 
+def scatter(table, ids, rows):
+    """table[ids] = rows in place via the oracle's write-back (ids distinct)."""
+    assert table.flags.c_contiguous
+    ids = _c(ids, np.uint32)
+    rows = np.ascontiguousarray(rows, dtype=table.dtype)
+    assert rows.shape == (len(ids),) + table.shape[1:]
+    lib().ho_scatter(_p(table), table.strides[0], _p(ids), len(ids), _p(rows))
+
+
 def gather_ptr(table_ptr: int, row_bytes: int, ids, dim: int, np_dtype):
     ids = _c(ids, np.uint32)
     out = np.empty((len(ids), dim), dtype=np_dtype)
@@ -220,10 +230,11 @@ def round_bf16(x: float) -> int:
 
 
 # ---------------------------------------------------------------------------- whole path
-def run_path(w, rows_per_table, prof_batches, batch, dY, table, k=None):
+def run_path(w, rows_per_table, prof_batches, batch, dY, table, k=None, writeback=False):
     """Every step of the hot path for one measured mini-batch, in the paper's order:
     profile (count + select), classify, partition, remap, cold plan + gather, forward
-    over both mu-batches, one coalesced SGD step.  `table` is the full host table
+    over both mu-batches, one coalesced SGD step [, write-back of the updated cold
+    rows into a copy of the table: key "table_new"].  `table` is the full host table
     [n_rows, dim] (float32 or uint16 bf16 bits); it is not modified.
     Returns a dict of every intermediate and final result."""
     n_rows = int(np.sum(rows_per_table, dtype=np.int64))
@@ -254,7 +265,11 @@ def run_path(w, rows_per_table, prof_batches, batch, dY, table, k=None):
     stg_new = stg.copy()
     uniq, scale_b, rc3 = embbag_bwd_sgd(w.dtype, w_hot_new, k_cap, stg_new, codes, batch.bag_ptr,
                                         None, B, bps, dY, w.lr, want_scale=True)
-    return dict(n_rows=n_rows, k_cap=k_cap, counts=counts, hot=hot, gids=g, flags=flags, pop=pop,
-                nonpop=nonpop, codes_remap=codes0, cold=cold, codes=codes, w_hot=w_hot, staging=stg,
-                out=out, out_scale=scale_f, w_hot_new=w_hot_new, staging_new=stg_new, uniq=uniq,
-                upd_scale=scale_b, rc=(rc_g, rc1, rc2, rc3))
+    r = dict(n_rows=n_rows, k_cap=k_cap, counts=counts, hot=hot, gids=g, flags=flags, pop=pop,
+             nonpop=nonpop, codes_remap=codes0, cold=cold, codes=codes, w_hot=w_hot, staging=stg,
+             out=out, out_scale=scale_f, w_hot_new=w_hot_new, staging_new=stg_new, uniq=uniq,
+             upd_scale=scale_b, rc=(rc_g, rc1, rc2, rc3))
+    if writeback:
+        r["table_new"] = np.array(table, copy=True)
+        scatter(r["table_new"], cold, stg_new)
+    return r

@@ -270,6 +270,15 @@ void ho_gather(const void* table, uint64_t row_bytes, const uint32_t* ids, int64
                (size_t)row_bytes);
 }
 
+/* Write-back of updated working parameters (non-hot rows are updated in CPU
+ * main memory, Sec. IV; dma_wr of the ISA table): table[ids[u]] = rows[u] bit
+ * for bit.  The ids are distinct. */
+void ho_scatter(void* table, uint64_t row_bytes, const uint32_t* ids, int64_t n, const void* rows) {
+    for (int64_t u = 0; u < n; ++u)
+        memcpy((char*)table + (size_t)ids[u] * row_bytes, (const char*)rows + (size_t)u * row_bytes,
+               (size_t)row_bytes);
+}
+
 /* ------------------------------------------------------------------ 9. forward */
 /* Sum pooling (the Reducer's sparse-length element-wise sum, Sec. V-D, v_add of
  * the ISA): out[bag] = sum of the bag's rows, in fp64 in CSR order, rounded once

@@ -158,7 +158,7 @@ size_t hl_partition_ws_bytes(int32_t max_samples) {
   return HL_WS_HEADER + 4 * ((size_t)(max_samples + PT_SMALL - 1) / PT_SMALL + 64);
 }
 
-extern "C" hl_status hl_partition(const hl_handle* h, const uint8_t* flags, int32_t n, int32_t* pop,
+extern "C" hl_status hl_partition(hl_handle* h, const uint8_t* flags, int32_t n, int32_t* pop,
                                   int32_t* nonpop, int32_t* counts, void* ws, size_t ws_bytes,
                                   hl_stream stream) {
   if (!h || n < 0 || !counts || (n > 0 && (!flags || !pop || !nonpop))) return HL_ERR_INVALID_ARG;
@@ -170,6 +170,7 @@ extern "C" hl_status hl_partition(const hl_handle* h, const uint8_t* flags, int3
   int mode = 0;
   if (tiles > 1) {
     if (!ws || ws_bytes < hl_partition_ws_bytes(n)) return HL_ERR_CAPACITY;
+    hl_ws_note(h, ws, HL_WSK_OTHER);
     tc = (uint32_t*)((char*)ws + HL_WS_HEADER);
     HL_KERNEL(h, s, "pt_count", pt_count, dim3(tiles), dim3(1024), 0, s, flags, n, tile, tc);
     if (small) {

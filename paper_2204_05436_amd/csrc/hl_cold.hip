@@ -9,10 +9,15 @@
 //              list (one atomic per block)
 //   rank     : a scan over all lookups in index order (decoupled look-back)
 //              numbers the first occurrences: staging row u of each id
-//   finalize : capacity check, code rewrite, table clearing, cold id list and
-//              the row copy from host memory
-// The workspace is shared with other calls, so the table is cleared at the
-// start of every call.
+//   codes    : capacity check, code rewrite and the cold id list
+//   copy     : the row copy between the pinned host table and the staging
+//              rows, in either direction (fetch before the mu-batch runs,
+//              write-back of the updated rows after it)
+// The plan (insert, rank, codes) uses the workspace, which is shared with
+// other calls, so its table is cleared at the start of every call.  The copy
+// reads only the cold id list and count, so it can run on a stream of its own
+// while the popular mu-batch and the backward's grouping proceed (the overlap
+// of the paper's pipeline, Sec. IV and Fig. "hotlinepipe").
 #include "hl_internal.h"
 
 #define CG_C_LIST 0
@@ -294,48 +299,104 @@ cg_rank(const uint32_t* __restrict__ gids, const int32_t* __restrict__ codes, ui
   }
 }
 
-// Part (a): every listed cold lookup points its code at its staging row.
-// Part (b): thread (u, unit) copies one unit of row u.
-template <typename V>
+// Every listed cold lookup points its code at its staging row; cold_ids[u] =
+// id of staging row u.  Nothing but the error bit and the list reset when the
+// rows do not fit.
 __global__ void __launch_bounds__(256)
-cg_finalize(cg_ws ws, uint32_t n_max, int32_t cap, uint32_t k_cap, int32_t* __restrict__ codes,
-            uint32_t* __restrict__ cold_ids, const V* __restrict__ src, V* __restrict__ dst, uint32_t upr,
-            uint32_t* err) {
+cg_codes(cg_ws ws, uint32_t n_max, int32_t cap, uint32_t k_cap, int32_t* __restrict__ codes,
+         uint32_t* __restrict__ cold_ids, uint32_t* err) {
   const uint32_t n_list = min(ws.ctr[CG_C_SNAP], n_max), ncold = ws.ctr[CG_C_NCOLD];
   const bool fits = ncold <= (uint32_t)cap;
   if (blockIdx.x == 0 && threadIdx.x == 0) {
     ws.ctr[CG_C_LIST] = 0;  // ready for the next call
     if (!fits) hl_flag(err, HL_DEVERR_CAPACITY);
   }
-  const uint64_t gs = (uint64_t)gridDim.x * blockDim.x, t0 = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  for (uint64_t e = t0; e < n_list; e += gs) {
-    const uint32_t i = ws.list[e];
-    const uint32_t sl = ws.slotof[i];
-    if (fits) codes[i] = (int32_t)(k_cap + ws.uidx[sl]);
-  }
   if (!fits) return;
-  const uint64_t total = (uint64_t)ncold * upr;
-  for (uint64_t t = t0; t < total; t += gs) {
-    const uint32_t u = (uint32_t)(t / upr), c = (uint32_t)(t - (uint64_t)u * upr);
-    const uint32_t g = ws.fst[u];
-    if (c == 0) cold_ids[u] = g;
-    dst[(uint64_t)u * upr + c] = src[(uint64_t)g * upr + c];
+  const uint32_t gs = gridDim.x * blockDim.x, t0 = blockIdx.x * blockDim.x + threadIdx.x;
+  for (uint32_t e = t0; e < n_list; e += gs) {
+    const uint32_t i = ws.list[e];
+    codes[i] = (int32_t)(k_cap + ws.uidx[ws.slotof[i]]);
+  }
+  for (uint32_t u = t0; u < ncold; u += gs) cold_ids[u] = ws.fst[u];
+}
+
+// Row copy between host table and staging rows: TO_HOST = 0 copies
+// staging[u] = host[ids[u]], TO_HOST = 1 copies host[ids[u]] = staging[u], for
+// u < *n_dev.  A count above cap copies nothing and sets the capacity bit; an
+// id >= n_rows is skipped and sets the range bit.  The grid is kept small (the
+// host link, not the CUs, bounds it) and each thread keeps 4 units in flight.
+template <typename V, bool TO_HOST>
+__global__ void __launch_bounds__(256)
+cg_copy(const uint32_t* __restrict__ ids, const int32_t* n_dev, int32_t cap, uint64_t n_rows, V* host, V* stg,
+        uint32_t upr, uint32_t* err) {
+  const int32_t nd = *n_dev;
+  if (nd < 0 || nd > cap) {
+    if (blockIdx.x == 0 && threadIdx.x == 0) hl_flag(err, nd < 0 ? HL_DEVERR_OUT_OF_RANGE : HL_DEVERR_CAPACITY);
+    return;
+  }
+  const uint64_t total = (uint64_t)nd * upr, gs = (uint64_t)gridDim.x * blockDim.x;
+  for (uint64_t t0 = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; t0 < total; t0 += 4 * gs) {
+    V v[4];
+    uint64_t dst[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const uint64_t t = t0 + k * gs;
+      dst[k] = ~0ull;
+      if (t < total) {
+        const uint32_t u = (uint32_t)(t / upr), c = (uint32_t)(t - (uint64_t)u * upr);
+        const uint32_t g = ids[u];
+        if (g < n_rows) {
+          const uint64_t hp = (uint64_t)g * upr + c, sp = (uint64_t)u * upr + c;
+          v[k] = TO_HOST ? stg[sp] : host[hp];
+          dst[k] = TO_HOST ? hp : sp;
+        } else if (c == 0) {
+          hl_flag(err, HL_DEVERR_OUT_OF_RANGE);
+        }
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      if (dst[k] != ~0ull) {
+        if (TO_HOST) host[dst[k]] = v[k];
+        else stg[dst[k]] = v[k];
+      }
+    }
   }
 }
 
-extern "C" hl_status hl_cold_gather(hl_handle* h, const uint32_t* gids, int32_t* codes, const int32_t* bag_ptr,
-                                    int32_t n_samples, int32_t bps, int64_t n_lookups,
-                                    const int32_t* sample_ids, const int32_t* n_sel_dev, int32_t n_sel_max,
-                                    const void* w_host, void* staging, int32_t cap, uint32_t* cold_ids_out,
-                                    int32_t* n_cold_dev, void* workspace, size_t ws_bytes,
-                                    hl_stream stream) {
+static hl_status cg_launch_copy(hl_handle* h, const uint32_t* ids, const int32_t* n_dev, int32_t cap, void* host,
+                                void* stg, bool to_host, hipStream_t s) {
+  const uint32_t rb = h->row_bytes;
+  uint64_t units = (uint64_t)(cap > 0 ? cap : 1) * (rb / 4);
+  uint32_t g = (uint32_t)((units + 1023) / 1024);
+  g = g < 1 ? 1 : (g > 512 ? 512 : g);
+#define CG_COPY(V)                                                                                             \
+  if (to_host)                                                                                                 \
+    HL_KERNEL(h, s, "cg_scatter", (cg_copy<V, true>), dim3(g), dim3(256), 0, s, ids, n_dev, cap, h->n_rows,     \
+              (V*)host, (V*)stg, (uint32_t)(rb / sizeof(V)), h->d_err);                                        \
+  else                                                                                                         \
+    HL_KERNEL(h, s, "cg_fetch", (cg_copy<V, false>), dim3(g), dim3(256), 0, s, ids, n_dev, cap, h->n_rows,      \
+              (V*)host, (V*)stg, (uint32_t)(rb / sizeof(V)), h->d_err);
+  if (rb % 16 == 0 && ((uintptr_t)host | (uintptr_t)stg) % 16 == 0) { CG_COPY(uint4) }
+  else if (rb % 8 == 0 && ((uintptr_t)host | (uintptr_t)stg) % 8 == 0) { CG_COPY(uint2) }
+  else if (rb % 4 == 0 && ((uintptr_t)host | (uintptr_t)stg) % 4 == 0) { CG_COPY(uint32_t) }
+  else { CG_COPY(uint16_t) }
+#undef CG_COPY
+  HL_LAUNCHED();
+  return HL_OK;
+}
+
+extern "C" hl_status hl_cold_plan(hl_handle* h, const uint32_t* gids, int32_t* codes, const int32_t* bag_ptr,
+                                  int32_t n_samples, int32_t bps, int64_t n_lookups, const int32_t* sample_ids,
+                                  const int32_t* n_sel_dev, int32_t n_sel_max, int32_t cap, uint32_t* cold_ids_out,
+                                  int32_t* n_cold_dev, void* workspace, size_t ws_bytes, hl_stream stream) {
   if (!h || n_samples < 0 || bps < 1 || n_lookups < 0 || n_sel_max < 0 || cap < 0) return HL_ERR_INVALID_ARG;
   if (!n_cold_dev || !bag_ptr || !workspace) return HL_ERR_INVALID_ARG;
   if (!sample_ids && n_sel_max > n_samples) return HL_ERR_INVALID_ARG;
-  if (n_lookups > 0 && (!gids || !codes || !w_host || (cap > 0 && (!staging || !cold_ids_out))))
-    return HL_ERR_INVALID_ARG;
+  if (n_lookups > 0 && (!gids || !codes || (cap > 0 && !cold_ids_out))) return HL_ERR_INVALID_ARG;
   if (n_lookups >= (1ll << 30) || (uint64_t)h->k_cap + (uint64_t)cap >= (1ull << 31)) return HL_ERR_UNSUPPORTED;
   if (ws_bytes < hl_cold_ws_bytes(h, n_lookups)) return HL_ERR_CAPACITY;
+  hl_ws_note(h, workspace, HL_WSK_OTHER);
   hipStream_t s = (hipStream_t)stream;
   hl_carver c = hl_carver::after_header(workspace, ws_bytes);
   cg_ws ws;
@@ -352,17 +413,39 @@ extern "C" hl_status hl_cold_gather(hl_handle* h, const uint32_t* gids, int32_t*
   const uint32_t epoch = hl_next_epoch(h);
   HL_KERNEL(h, s, "cg_rank", cg_rank, dim3(ws.rtiles), dim3(CG_RT_THREADS), 0, s, gids, codes, n_max, ws, n_cold_dev, epoch,
             h->d_err);
-  const uint32_t rb = h->row_bytes;
-  uint32_t g = hl_div_up((uint64_t)(n_max ? n_max : 1) * (rb / 4), 256);
-  if (g > 8192) g = 8192;
-#define CG_FIN(V)                                                                                     \
-  HL_KERNEL(h, s, "cg_finalize", cg_finalize<V>, dim3(g), dim3(256), 0, s, ws, n_max, cap, h->k_cap, codes, \
-            cold_ids_out, (const V*)w_host, (V*)staging, (uint32_t)(rb / sizeof(V)), h->d_err);
-  if (rb % 16 == 0) { CG_FIN(uint4) }
-  else if (rb % 8 == 0) { CG_FIN(uint2) }
-  else if (rb % 4 == 0) { CG_FIN(uint32_t) }
-  else { CG_FIN(uint16_t) }
-#undef CG_FIN
+  uint32_t g = hl_div_up(n_max ? n_max : 1, 256);
+  if (g > 1024) g = 1024;
+  HL_KERNEL(h, s, "cg_codes", cg_codes, dim3(g), dim3(256), 0, s, ws, n_max, cap, h->k_cap, codes, cold_ids_out,
+            h->d_err);
   HL_LAUNCHED();
   return HL_OK;
+}
+
+extern "C" hl_status hl_cold_fetch(hl_handle* h, const uint32_t* cold_ids, const int32_t* n_cold_dev, int32_t cap,
+                                   const void* w_host, void* staging, hl_stream stream) {
+  if (!h || cap < 0 || !n_cold_dev) return HL_ERR_INVALID_ARG;
+  if (cap > 0 && (!cold_ids || !w_host || !staging)) return HL_ERR_INVALID_ARG;
+  if (cap == 0) return HL_OK;
+  return cg_launch_copy(h, cold_ids, n_cold_dev, cap, const_cast<void*>(w_host), staging, false, (hipStream_t)stream);
+}
+
+extern "C" hl_status hl_cold_scatter(hl_handle* h, const uint32_t* cold_ids, const int32_t* n_cold_dev, int32_t cap,
+                                     const void* staging, void* w_host, hl_stream stream) {
+  if (!h || cap < 0 || !n_cold_dev) return HL_ERR_INVALID_ARG;
+  if (cap > 0 && (!cold_ids || !w_host || !staging)) return HL_ERR_INVALID_ARG;
+  if (cap == 0) return HL_OK;
+  return cg_launch_copy(h, cold_ids, n_cold_dev, cap, w_host, const_cast<void*>(staging), true, (hipStream_t)stream);
+}
+
+extern "C" hl_status hl_cold_gather(hl_handle* h, const uint32_t* gids, int32_t* codes, const int32_t* bag_ptr,
+                                    int32_t n_samples, int32_t bps, int64_t n_lookups,
+                                    const int32_t* sample_ids, const int32_t* n_sel_dev, int32_t n_sel_max,
+                                    const void* w_host, void* staging, int32_t cap, uint32_t* cold_ids_out,
+                                    int32_t* n_cold_dev, void* workspace, size_t ws_bytes,
+                                    hl_stream stream) {
+  if (h && n_lookups > 0 && cap > 0 && (!w_host || !staging)) return HL_ERR_INVALID_ARG;
+  hl_status st = hl_cold_plan(h, gids, codes, bag_ptr, n_samples, bps, n_lookups, sample_ids, n_sel_dev, n_sel_max,
+                              cap, cold_ids_out, n_cold_dev, workspace, ws_bytes, stream);
+  if (st != HL_OK || n_lookups == 0) return st;
+  return hl_cold_fetch(h, cold_ids_out, n_cold_dev, cap, w_host, staging, stream);
 }

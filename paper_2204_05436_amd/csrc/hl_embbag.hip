@@ -629,6 +629,11 @@ extern "C" hl_status hl_embbag_fwd(const hl_handle* h, const void* w_hot, const 
   return HL_OK;
 }
 
+// Keys are compressed codes: hot slot, or n_hot + staging row.
+static int bw_key_bits(const hl_handle* h, int32_t stg_rows) {
+  return hl_bit_width((uint64_t)h->n_hot + (uint64_t)stg_rows);
+}
+
 template <int VEC, bool BF>
 static void launch_bwd(const hl_handle* h, uint32_t tiles, dim3 g2, hipStream_t s, const uint32_t* sk, const uint32_t* sv, uint32_t n,
                        const float* dY, eb_geom g, void* w_hot, void* stg, uint32_t n_hot, float lr, bw_ws& ws) {
@@ -639,17 +644,20 @@ static void launch_bwd(const hl_handle* h, uint32_t tiles, dim3 g2, hipStream_t 
   (void)g2;
 }
 
-extern "C" hl_status hl_embbag_bwd_sgd(hl_handle* h, void* w_hot, void* staging, int32_t stg_rows,
-                                       const int32_t* codes, const int32_t* bag_ptr, int32_t n_samples, int32_t bps,
-                                       int64_t n_lookups, const int32_t* sample_ids, const int32_t* n_sel_dev,
-                                       int32_t n_sel_max, const float* dY, float lr, void* workspace, size_t ws_bytes,
-                                       hl_stream stream) {
+extern "C" hl_status hl_embbag_bwd_plan(hl_handle* h, int32_t stg_rows, const int32_t* codes, const int32_t* bag_ptr,
+                                        int32_t n_samples, int32_t bps, int64_t n_lookups, const int32_t* sample_ids,
+                                        const int32_t* n_sel_dev, int32_t n_sel_max, void* workspace, size_t ws_bytes,
+                                        hl_stream stream) {
   hl_status st = check_common(h, codes, bag_ptr, n_samples, bps, n_lookups, sample_ids, n_sel_max, stg_rows);
   if (st != HL_OK) return st;
-  if (n_samples == 0 || n_lookups == 0 || n_sel_max == 0) return HL_OK;
-  if (!dY || !workspace || (h->n_hot && !w_hot) || (stg_rows && !staging)) return HL_ERR_INVALID_ARG;
+  if (!workspace) return HL_ERR_INVALID_ARG;
   const int64_t n_bags = (int64_t)n_samples * bps;
   if (ws_bytes < hl_bwd_ws_bytes(h, n_lookups, n_bags)) return HL_ERR_CAPACITY;
+  hl_ws_note(h, workspace, HL_WSK_OTHER);
+  if (n_samples == 0 || n_lookups == 0 || n_sel_max == 0) {
+    hl_ws_note(h, workspace, HL_WSK_BWD_PLAN, 0, n_bags, stg_rows);
+    return HL_OK;
+  }
   hipStream_t s = (hipStream_t)stream;
   hl_carver c = hl_carver::after_header(workspace, ws_bytes);
   bw_ws ws;
@@ -666,9 +674,30 @@ extern "C" hl_status hl_embbag_bwd_sgd(hl_handle* h, void* w_hot, void* staging,
                      h->n_hot, h->k_cap, stg_rows, ws.sort.k0, ws.sort.v0, n_lookups, h->d_err);
   HL_LAUNCHED();
   uint32_t *sk, *sv;
-  const uint32_t n = (uint32_t)n_lookups;
-  st = hl_sort_pairs(h, ws.sort, nullptr, n, hl_bit_width((uint64_t)h->n_hot + (uint64_t)stg_rows), s, &sk, &sv);
+  st = hl_sort_pairs(h, ws.sort, nullptr, (uint32_t)n_lookups, bw_key_bits(h, stg_rows), s, &sk, &sv);
   if (st != HL_OK) return st;
+  hl_ws_note(h, workspace, HL_WSK_BWD_PLAN, n_lookups, n_bags, stg_rows);
+  return HL_OK;
+}
+
+extern "C" hl_status hl_embbag_bwd_apply(hl_handle* h, void* w_hot, void* staging, int32_t stg_rows, int32_t n_samples,
+                                         int32_t bps, int64_t n_lookups, const float* dY, float lr, void* workspace,
+                                         size_t ws_bytes, hl_stream stream) {
+  if (!h || n_samples < 0 || bps < 1 || n_lookups < 0 || stg_rows < 0 || !workspace) return HL_ERR_INVALID_ARG;
+  const int64_t n_bags = (int64_t)n_samples * bps;
+  if (h->ws_last != workspace || h->ws_kind != HL_WSK_BWD_PLAN || h->ws_n != n_lookups || h->ws_bags != n_bags ||
+      h->ws_stg != stg_rows)
+    return HL_ERR_INVALID_ARG;  // no matching plan is held by this workspace
+  if (n_lookups == 0 || n_samples == 0) return HL_OK;
+  if (!dY || (h->n_hot && !w_hot) || (stg_rows && !staging)) return HL_ERR_INVALID_ARG;
+  if (ws_bytes < hl_bwd_ws_bytes(h, n_lookups, n_bags)) return HL_ERR_CAPACITY;
+  hipStream_t s = (hipStream_t)stream;
+  hl_carver c = hl_carver::after_header(workspace, ws_bytes);
+  bw_ws ws;
+  bw_carve(c, ws, (uint32_t)n_lookups, n_bags, h->dim);
+  uint32_t *sk, *sv;
+  hl_sort_result(ws.sort, bw_key_bits(h, stg_rows), &sk, &sv);
+  const uint32_t n = (uint32_t)n_lookups;
   const size_t es = h->dtype == HL_F32 ? 4 : 2;
   const int vec = eb_pick_vec(h->dim, es, {w_hot, staging, dY});
   eb_geom g = eb_make_geom(h->dim, vec);
@@ -684,4 +713,20 @@ extern "C" hl_status hl_embbag_bwd_sgd(hl_handle* h, void* w_hot, void* staging,
 #undef BWD
   HL_LAUNCHED();
   return HL_OK;
+}
+
+extern "C" hl_status hl_embbag_bwd_sgd(hl_handle* h, void* w_hot, void* staging, int32_t stg_rows,
+                                       const int32_t* codes, const int32_t* bag_ptr, int32_t n_samples, int32_t bps,
+                                       int64_t n_lookups, const int32_t* sample_ids, const int32_t* n_sel_dev,
+                                       int32_t n_sel_max, const float* dY, float lr, void* workspace, size_t ws_bytes,
+                                       hl_stream stream) {
+  hl_status st = check_common(h, codes, bag_ptr, n_samples, bps, n_lookups, sample_ids, n_sel_max, stg_rows);
+  if (st != HL_OK) return st;
+  if (n_samples == 0 || n_lookups == 0 || n_sel_max == 0) return HL_OK;
+  if (!dY || !workspace || (h->n_hot && !w_hot) || (stg_rows && !staging)) return HL_ERR_INVALID_ARG;
+  st = hl_embbag_bwd_plan(h, stg_rows, codes, bag_ptr, n_samples, bps, n_lookups, sample_ids, n_sel_dev, n_sel_max,
+                          workspace, ws_bytes, stream);
+  if (st != HL_OK) return st;
+  return hl_embbag_bwd_apply(h, w_hot, staging, stg_rows, n_samples, bps, n_lookups, dY, lr, workspace, ws_bytes,
+                             stream);
 }

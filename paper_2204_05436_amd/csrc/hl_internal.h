@@ -48,7 +48,24 @@ struct hl_handle {
   uint32_t* d_tk;        // top-K scratch (state, histograms, tile counts)
   size_t tk_bytes;
   hl_trace* trace;       // per-kernel event records (owned)
+  // The last call that left state in a workspace for a later call: the
+  // backward's plan (grouping) is consumed by its apply step.
+  const void* ws_last;   // workspace of that call
+  int ws_kind;           // HL_WSK_*
+  int64_t ws_n, ws_bags; // its lookups and bags
+  int32_t ws_stg;        // its staging rows
 };
+#define HL_WSK_NONE 0
+#define HL_WSK_OTHER 1
+#define HL_WSK_BWD_PLAN 2
+static inline void hl_ws_note(hl_handle* h, const void* ws, int kind, int64_t n = 0, int64_t bags = 0,
+                              int32_t stg = 0) {
+  h->ws_last = ws;
+  h->ws_kind = kind;
+  h->ws_n = n;
+  h->ws_bags = bags;
+  h->ws_stg = stg;
+}
 
 // ----------------------------------------------------------------------------- errors
 #define HL_HIP(call)                                   \
@@ -118,27 +135,27 @@ struct hl_carver {
 };
 
 // ----------------------------------------------------------------------------- sort
-// Stable LSD radix sort of (key, value) uint32 pairs, 8-bit digits, one
-// histogram kernel plus one kernel per digit with decoupled look-back for the
-// cross-tile digit offsets.  See hl_sort.hip.
+// Stable LSD radix sort of (key, value) uint32 pairs with digits of up to 11
+// bits: one histogram kernel plus one kernel per digit with decoupled look-back
+// for the cross-tile digit offsets.  See hl_sort.hip.
+#define HL_SORT_THREADS 512
+#define HL_SORT_WAVES (HL_SORT_THREADS / 64)
+#ifndef HL_SORT_ITEMS
+#define HL_SORT_ITEMS 8
+#endif
+#define HL_SORT_TILE (HL_SORT_THREADS * HL_SORT_ITEMS)
+#define HL_SORT_MAXNB 2048        // bins of an 11-bit digit
+#define HL_SORT_MAXPASS 3
+#define HL_SORT_HIST_BLOCKS 16
+#define HL_SORT_HIST_THREADS 1024
 struct hl_sort_ws {
   uint32_t *k0, *v0, *k1, *v1;  // ping-pong buffers, n_max each; input in k0/v0
-  uint32_t* part;               // [HL_SORT_HIST_BLOCKS][4*256]
-  uint32_t* gexcl;              // [4*256]
-  uint32_t* ctr;                // [8] self-resetting counters (in the workspace header)
-  uint64_t* status;             // [4][tiles_max][256]
+  uint32_t* part;               // [HL_SORT_MAXPASS][HL_SORT_HIST_BLOCKS][HL_SORT_MAXNB] per-block digit counts
+  uint32_t* st[2];              // [tiles_max][HL_SORT_MAXNB] look-back status, alternating between passes
+  uint32_t* ctr;                // [8] self-resetting tile counters (in the workspace header)
   uint32_t tiles_max;
   uint32_t n_max;
 };
-
-#define HL_SORT_BLOCK 512
-#define HL_SORT_WAVES (HL_SORT_BLOCK / 64)
-#ifndef HL_SORT_ITEMS
-#define HL_SORT_ITEMS 16
-#endif
-#define HL_SORT_TILE (HL_SORT_BLOCK * HL_SORT_ITEMS)
-#define HL_SORT_HIST_BLOCKS 16
-#define HL_SORT_HIST_THREADS 1024
 
 void hl_sort_ws_carve(hl_carver& c, hl_sort_ws& ws, uint32_t n_max);
 // Sorts ws.k0/ws.v0 (first *n_dev items if n_dev != NULL, else n_host) by the
@@ -147,6 +164,9 @@ void hl_sort_ws_carve(hl_carver& c, hl_sort_ws& ws, uint32_t n_max);
 // last.
 hl_status hl_sort_pairs(hl_handle* h, hl_sort_ws& ws, const uint32_t* n_dev, uint32_t n_host,
                         int bits, hipStream_t s, uint32_t** out_k, uint32_t** out_v);
+// The buffers hl_sort_pairs leaves its result in for a sort of `bits` bits
+// with n_host > 0.
+void hl_sort_result(const hl_sort_ws& ws, int bits, uint32_t** out_k, uint32_t** out_v);
 
 // Decoupled look-back helpers (epoch-tagged 64-bit status words).  A status
 // word carries its own value, so relaxed agent-scope atomics suffice: no other

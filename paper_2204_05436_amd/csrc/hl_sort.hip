@@ -1,16 +1,18 @@
-// Stable LSD radix sort of (key, value) uint32 pairs, 8-bit digits.
+// Stable LSD radix sort of (key, value) uint32 pairs.
 //
-// One histogram kernel counts all digit positions in a single read of the keys
-// (per-block counts; each pass block adds up the few it needs).  Then one
-// kernel per digit: a block takes the next tile (dynamic tile ids, so every
-// lower tile is already running), counts its digits and publishes them at
-// once, ranks its items by digit with wave ballots, and obtains the counts of
-// all earlier tiles by decoupled look-back over epoch-tagged status words (no
-// clearing between calls beyond the histogram kernel's reset).  Items are
-// reordered in LDS so the global writes of each digit run are contiguous.
-// Item order inside a tile is wave-major, then item, then lane, which is index
-// order, so the sort is stable.  Tiles are large (8192 items) so that every
-// tile finds all its predecessors within one look-back window.
+// A sort of `bits` bits takes P = ceil(bits / 11) passes of b = ceil(bits / P)
+// bits (two passes of 10 bits for the backward's 20-bit keys).  One histogram
+// kernel counts every digit position in a single read of the keys (per-block
+// counts; each pass block adds up the few it needs) and clears the first
+// pass's look-back status.  Then one kernel per digit: a block takes the next
+// tile (dynamic tile ids, so every lower tile is already running), ranks its
+// items by digit with wave ballots and per-wave LDS counters (the counters'
+// totals are the tile's digit counts), publishes the counts, obtains those of
+// all earlier tiles by decoupled look-back, reorders the tile in LDS so that
+// each digit's run is contiguous and writes it out.  Each pass block also
+// clears its tile's status words for the next pass.  Item order inside a tile
+// is wave-major, then item, then lane, which is index order, so the sort is
+// stable.
 #include "hl_internal.h"
 
 void hl_sort_ws_carve(hl_carver& c, hl_sort_ws& ws, uint32_t n_max) {
@@ -20,10 +22,23 @@ void hl_sort_ws_carve(hl_carver& c, hl_sort_ws& ws, uint32_t n_max) {
   ws.v0 = c.take<uint32_t>(n_max);
   ws.k1 = c.take<uint32_t>(n_max);
   ws.v1 = c.take<uint32_t>(n_max);
-  ws.part = c.take<uint32_t>((size_t)HL_SORT_HIST_BLOCKS * 1024);
-  ws.gexcl = c.take<uint32_t>(1024);
+  ws.part = c.take<uint32_t>((size_t)HL_SORT_MAXPASS * HL_SORT_HIST_BLOCKS * HL_SORT_MAXNB);
+  ws.st[0] = c.take<uint32_t>((size_t)ws.tiles_max * HL_SORT_MAXNB);
+  ws.st[1] = c.take<uint32_t>((size_t)ws.tiles_max * HL_SORT_MAXNB);
   ws.ctr = c.base ? c.header() + HL_HDR_SORT : nullptr;
-  ws.status = c.take<uint64_t>((size_t)4 * ws.tiles_max * 256);
+}
+
+// Status word of (tile, digit): flag in the top two bits (0 = not yet
+// published), count below.  Relaxed agent-scope atomics: the word carries its
+// own value and no other data is published through it.
+#define SRT_AGG 0x40000000u
+#define SRT_PRE 0x80000000u
+#define SRT_VAL 0x3FFFFFFFu
+__device__ __forceinline__ void srt_st_store(uint32_t* p, uint32_t w) {
+  __hip_atomic_store(p, w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint32_t srt_st_load(const uint32_t* p) {
+  return __hip_atomic_load(const_cast<uint32_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 __device__ __forceinline__ uint32_t srt_n(const uint32_t* n_dev, uint32_t n_host) {
@@ -32,49 +47,111 @@ __device__ __forceinline__ uint32_t srt_n(const uint32_t* n_dev, uint32_t n_host
   return v < n_host ? v : n_host;
 }
 
-// Per-block digit counts of every pass, and a reset of the pass kernels'
-// status words (n_status of them).
-__global__ void __launch_bounds__(HL_SORT_HIST_THREADS)
-srt_hist(const uint32_t* __restrict__ keys, const uint32_t* n_dev, uint32_t n_host, int passes,
-         uint32_t* part, uint64_t* status, uint64_t n_status) {
-  __shared__ uint32_t h[4][256];
-  const uint32_t n = srt_n(n_dev, n_host);
-  const uint32_t gs = gridDim.x * blockDim.x;
-  for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n_status; i += gs) status[i] = 0;
-  for (int j = threadIdx.x; j < 1024; j += blockDim.x) (&h[0][0])[j] = 0;
-  __syncthreads();
-  for (uint32_t b = blockIdx.x * blockDim.x + threadIdx.x; b < n; b += 8 * gs) {
-    uint32_t k[8];
-#pragma unroll
-    for (int u = 0; u < 8; ++u) k[u] = b + u * gs < n ? keys[b + u * gs] : 0u;
-#pragma unroll
-    for (int u = 0; u < 8; ++u)
-      if (b + u * gs < n)
-        for (int p = 0; p < passes; ++p) atomicAdd(&h[p][(k[u] >> (8 * p)) & 255u], 1u);
-  }
-  __syncthreads();
-  for (int j = threadIdx.x; j < passes * 256; j += blockDim.x) part[blockIdx.x * 1024 + j] = (&h[0][0])[j];
+struct srt_plan {
+  int passes, b, nb;
+};
+static srt_plan srt_make_plan(int bits) {
+  if (bits < 1) bits = 1;
+  srt_plan p;
+  p.passes = (bits + 10) / 11;
+  p.b = (bits + p.passes - 1) / p.passes;
+  p.nb = p.b <= 8 ? 256 : (p.b <= 10 ? 1024 : 2048);
+  return p;
 }
 
-__global__ void __launch_bounds__(HL_SORT_BLOCK)
+// Per-block counts of every digit of every pass; clears n_zero status words.
+template <int NB>
+__global__ void __launch_bounds__(HL_SORT_HIST_THREADS)
+srt_hist(const uint32_t* __restrict__ keys, const uint32_t* n_dev, uint32_t n_host, int passes, int b,
+         uint32_t* __restrict__ part, uint32_t* __restrict__ zero, uint64_t n_zero) {
+  __shared__ uint32_t h[HL_SORT_MAXPASS][NB];
+  const uint32_t n = srt_n(n_dev, n_host);
+  const uint32_t gs = gridDim.x * blockDim.x;
+  for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n_zero; i += gs) zero[i] = 0;
+  for (int j = threadIdx.x; j < HL_SORT_MAXPASS * NB; j += blockDim.x) (&h[0][0])[j] = 0;
+  __syncthreads();
+  const uint32_t mask = (1u << b) - 1u;
+  for (uint32_t i0 = blockIdx.x * blockDim.x + threadIdx.x; i0 < n; i0 += 8 * gs) {
+    uint32_t k[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) k[u] = i0 + u * gs < n ? keys[i0 + u * gs] : 0u;
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      if (i0 + u * gs < n)
+        for (int p = 0; p < passes; ++p) atomicAdd(&h[p][(k[u] >> (b * p)) & mask], 1u);
+  }
+  __syncthreads();
+  for (int p = 0; p < passes; ++p)
+    for (int j = threadIdx.x; j < NB; j += blockDim.x)
+      part[((size_t)p * HL_SORT_HIST_BLOCKS + blockIdx.x) * NB + j] = h[p][j];
+}
+
+// Block-wide exclusive scans of two values per digit (each thread owns PER
+// consecutive digits).  Returns through a and c in place.
+template <int NB, int PER>
+__device__ __forceinline__ void srt_scan2(uint32_t (&a)[PER], uint32_t (&c)[PER], uint32_t (*ws)[2]) {
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  uint32_t sa = 0, sc = 0;
+#pragma unroll
+  for (int j = 0; j < PER; ++j) {
+    sa += a[j];
+    sc += c[j];
+  }
+  uint32_t ia = sa, ic = sc;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const uint32_t ta = __shfl_up(ia, o), tc = __shfl_up(ic, o);
+    if (lane >= o) {
+      ia += ta;
+      ic += tc;
+    }
+  }
+  if (lane == 63) {
+    ws[w][0] = ia;
+    ws[w][1] = ic;
+  }
+  __syncthreads();
+  uint32_t ra = ia - sa, rc = ic - sc;
+  for (int j = 0; j < w; ++j) {
+    ra += ws[j][0];
+    rc += ws[j][1];
+  }
+#pragma unroll
+  for (int j = 0; j < PER; ++j) {
+    const uint32_t ta = a[j], tc = c[j];
+    a[j] = ra;
+    c[j] = rc;
+    ra += ta;
+    rc += tc;
+  }
+}
+
+template <int NB>
+__global__ void __launch_bounds__(HL_SORT_THREADS)
 srt_pass(const uint32_t* __restrict__ kin, const uint32_t* __restrict__ vin, uint32_t* __restrict__ kout,
-         uint32_t* __restrict__ vout, const uint32_t* n_dev, uint32_t n_host, int shift,
-         const uint32_t* __restrict__ part, uint32_t n_part, uint64_t* status, uint32_t* tile_ctr,
-         uint32_t epoch, uint32_t* err) {
+         uint32_t* __restrict__ vout, const uint32_t* n_dev, uint32_t n_host, int shift, int b,
+         const uint32_t* __restrict__ part, uint32_t n_part, uint32_t* st, uint32_t* st_next, uint32_t* tile_ctr,
+         uint32_t* err) {
+  constexpr int PER = NB >= HL_SORT_THREADS ? NB / HL_SORT_THREADS : 1;
+  constexpr int OWNERS = NB / PER;       // threads that own digits
+  constexpr int WIN = PER >= 4 ? 8 : 16;  // look-back window per digit
   __shared__ uint32_t s_tile;
-  __shared__ uint32_t wcnt[HL_SORT_WAVES][256];
-  __shared__ uint32_t thist[256], tdex[256], gbase[256], wt[4], wg[4];
+  __shared__ uint32_t wcnt[HL_SORT_WAVES][NB];
+  __shared__ uint32_t tdex[NB], gbase[NB];
+  __shared__ uint32_t scan_ws[HL_SORT_WAVES][2];
   __shared__ uint32_t lk[HL_SORT_TILE], lv[HL_SORT_TILE];
   const uint32_t n = srt_n(n_dev, n_host);
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   if (tid == 0) s_tile = atomicInc(tile_ctr, gridDim.x - 1);
-  for (int j = tid; j < HL_SORT_WAVES * 256; j += HL_SORT_BLOCK) (&wcnt[0][0])[j] = 0;
-  if (tid < 256) thist[tid] = 0;
+  for (int j = tid; j < HL_SORT_WAVES * NB; j += HL_SORT_THREADS) (&wcnt[0][0])[j] = 0;
   __syncthreads();
   const uint32_t tile = s_tile;
+  if (st_next)  // this tile's status words of the next pass
+    for (int j = tid; j < NB; j += HL_SORT_THREADS) st_next[(size_t)tile * NB + j] = 0;
   const uint64_t tb = (uint64_t)tile * HL_SORT_TILE;
   if (tb >= n) return;
-  uint32_t key[HL_SORT_ITEMS], val[HL_SORT_ITEMS], lr[HL_SORT_ITEMS];
+  const uint32_t mask = (1u << b) - 1u;
+  uint32_t key[HL_SORT_ITEMS], val[HL_SORT_ITEMS];
 #pragma unroll
   for (int k = 0; k < HL_SORT_ITEMS; ++k) {
     const uint64_t idx = tb + (uint64_t)w * (HL_SORT_ITEMS * 64) + k * 64 + lane;
@@ -82,134 +159,172 @@ srt_pass(const uint32_t* __restrict__ kin, const uint32_t* __restrict__ vin, uin
     key[k] = ok ? kin[idx] : 0xFFFFFFFFu;
     val[k] = ok ? vin[idx] : 0u;
   }
-  // global count of digit tid over the histogram blocks (loads issued together)
-  uint32_t dtot = 0;
-  if (tid < 256) {
-    uint32_t pv[HL_SORT_HIST_BLOCKS];
+  // global counts of the owned digits (loads issued together)
+  const int d0 = tid * PER;
+  const bool owner = tid < OWNERS;
+  uint32_t dtot[PER];
+  {
+    uint32_t pv[PER][HL_SORT_HIST_BLOCKS];
 #pragma unroll
-    for (int b = 0; b < HL_SORT_HIST_BLOCKS; ++b) pv[b] = (uint32_t)b < n_part ? part[b * 1024 + tid] : 0u;
+    for (int j = 0; j < PER; ++j)
 #pragma unroll
-    for (int b = 0; b < HL_SORT_HIST_BLOCKS; ++b) dtot += pv[b];
-  }
-  // tile digit counts first, published before the ranking so that later tiles
-  // find them when they look back
+      for (int q = 0; q < HL_SORT_HIST_BLOCKS; ++q)
+        pv[j][q] = (owner && (uint32_t)q < n_part) ? part[(size_t)q * NB + d0 + j] : 0u;
 #pragma unroll
-  for (int k = 0; k < HL_SORT_ITEMS; ++k) {
-    const uint64_t idx = tb + (uint64_t)w * (HL_SORT_ITEMS * 64) + k * 64 + lane;
-    if (idx < n) atomicAdd(&thist[(key[k] >> shift) & 255u], 1u);
+    for (int j = 0; j < PER; ++j) {
+      dtot[j] = 0;
+#pragma unroll
+      for (int q = 0; q < HL_SORT_HIST_BLOCKS; ++q) dtot[j] += pv[j][q];
+    }
   }
-  __syncthreads();
-  uint64_t* st = status + (tid & 255);
-  uint32_t tc = 0;
-  if (tid < 256) {
-    tc = thist[tid];
-    hl_st_store(st + (size_t)tile * 256, hl_st_pack(epoch, tile == 0 ? HL_ST_PRE : HL_ST_AGG, tc));
-  }
+  // ranking: per item, the lanes with the same digit (ballots over its bits);
+  // the lowest of them adds the group size to the wave's counter (LDS atomics
+  // of one wave are applied in order, so the items pipeline) and the group
+  // shares the old value
   const uint64_t lt = (1ull << lane) - 1ull;
+  uint32_t dg[HL_SORT_ITEMS], lr[HL_SORT_ITEMS], old[HL_SORT_ITEMS];
+  uint64_t pm[HL_SORT_ITEMS];
+  int lead[HL_SORT_ITEMS];
 #pragma unroll
   for (int k = 0; k < HL_SORT_ITEMS; ++k) {
     const uint64_t idx = tb + (uint64_t)w * (HL_SORT_ITEMS * 64) + k * 64 + lane;
     const bool ok = idx < n;
-    const uint32_t d = (key[k] >> shift) & 255u;
+    const uint32_t d = (key[k] >> shift) & mask;
+    dg[k] = d;
     uint64_t peers = __ballot(ok);
-#pragma unroll
-    for (int b = 0; b < 8; ++b) {
-      const bool bit = (d >> b) & 1u;
+    for (int q = 0; q < b; ++q) {
+      const bool bit = (d >> q) & 1u;
       const uint64_t m = __ballot(bit);
       peers &= bit ? m : ~m;
     }
-    const int leader = peers ? (__ffsll((unsigned long long)peers) - 1) : 0;
-    uint32_t old = 0;
-    if (ok && lane == leader) {
-      old = wcnt[w][d];
-      wcnt[w][d] = old + (uint32_t)__popcll(peers);
-    }
-    old = __shfl(old, leader);
-    lr[k] = old + (uint32_t)__popcll(peers & lt);
+    pm[k] = peers;
+    lead[k] = peers ? (__ffsll((unsigned long long)peers) - 1) : 0;
+    old[k] = 0;
+    if (ok && lane == lead[k]) old[k] = atomicAdd(&wcnt[w][d], (uint32_t)__popcll(peers));
   }
-  __syncthreads();
-  if (tid < 256) {
-    // wave-exclusive prefixes of this digit
-    uint32_t run = 0;
 #pragma unroll
-    for (int j = 0; j < HL_SORT_WAVES; ++j) {
-      const uint32_t c = wcnt[j][tid];
-      wcnt[j][tid] = run;
-      run += c;
-    }
-    // tile-local and global exclusive scans over the digits (waves 0..3)
-    uint32_t inc = tc, ginc = dtot;
-    for (int o = 1; o < 64; o <<= 1) {
-      const uint32_t t1 = __shfl_up(inc, o), t2 = __shfl_up(ginc, o);
-      if (lane >= o) {
-        inc += t1;
-        ginc += t2;
-      }
-    }
-    if (lane == 63) {
-      wt[w] = inc;
-      wg[w] = ginc;
-    }
-    tdex[tid] = inc - tc;
-    gbase[tid] = ginc - dtot;
-  }
+  for (int k = 0; k < HL_SORT_ITEMS; ++k) lr[k] = __shfl(old[k], lead[k]) + (uint32_t)__popcll(pm[k] & lt);
   __syncthreads();
-  if (tid < 256) {
-    uint32_t pre = 0, gpre = 0;
-    for (int j = 0; j < w; ++j) {
-      pre += wt[j];
-      gpre += wg[j];
+  // wave-exclusive offsets of each owned digit; the totals are the tile's counts
+  uint32_t tc[PER], tx[PER];
+#pragma unroll
+  for (int j = 0; j < PER; ++j) {
+    uint32_t run = 0;
+    if (owner)
+#pragma unroll
+      for (int q = 0; q < HL_SORT_WAVES; ++q) {
+        const uint32_t c = wcnt[q][d0 + j];
+        wcnt[q][d0 + j] = run;
+        run += c;
+      }
+    tc[j] = run;
+    tx[j] = run;
+    if (owner) srt_st_store(st + (size_t)tile * NB + d0 + j, (tile == 0 ? SRT_PRE : SRT_AGG) | run);
+  }
+  uint32_t gx[PER];
+#pragma unroll
+  for (int j = 0; j < PER; ++j) gx[j] = dtot[j];
+  srt_scan2<NB, PER>(tx, gx, scan_ws);
+  // decoupled look-back: counts of this digit in all earlier tiles
+  uint32_t excl[PER];
+  int64_t jj[PER];
+#pragma unroll
+  for (int j = 0; j < PER; ++j) {
+    excl[j] = 0;
+    jj[j] = owner ? (int64_t)tile - 1 : -1;
+  }
+  uint32_t spins = 0;
+  while (true) {
+    uint32_t wv[PER][WIN];
+#pragma unroll
+    for (int j = 0; j < PER; ++j)
+#pragma unroll
+      for (int q = 0; q < WIN; ++q)
+        wv[j][q] = jj[j] - q >= 0 ? srt_st_load(st + (size_t)(jj[j] - q) * NB + d0 + j) : SRT_PRE;
+    bool any = false, stall = false;
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+      if (jj[j] < 0) continue;
+      int used = 0;
+      bool stop = false;
+#pragma unroll
+      for (int q = 0; q < WIN; ++q) {
+        if (stop) continue;
+        const uint32_t x = wv[j][q];
+        if ((x & (SRT_AGG | SRT_PRE)) == 0) {  // not yet published
+          stop = true;
+          stall = true;
+          continue;
+        }
+        if (jj[j] - q >= 0) excl[j] += x & SRT_VAL;
+        if (x & SRT_PRE) {
+          used = -1;
+          stop = true;
+          continue;
+        }
+        used = q + 1;
+      }
+      jj[j] = used < 0 ? -1 : jj[j] - used;
+      any |= jj[j] >= 0;
     }
-    tdex[tid] += pre;
-    uint32_t excl = 0;
-    if (tile > 0) {
-      excl = hl_lookback(st, tile, 256, epoch, err);
-      hl_st_store(st + (size_t)tile * 256, hl_st_pack(epoch, HL_ST_PRE, excl + tc));
+    if (!any) break;
+    if (stall) {
+      if (++spins > HL_SPIN_LIMIT) {
+        hl_flag(err, HL_DEVERR_STALL);
+        break;
+      }
+      __builtin_amdgcn_s_sleep(1);
     }
-    gbase[tid] += gpre + excl;
+  }
+  if (owner) {
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+      if (tile > 0) srt_st_store(st + (size_t)tile * NB + d0 + j, SRT_PRE | (excl[j] + tc[j]));
+      tdex[d0 + j] = tx[j];
+      gbase[d0 + j] = gx[j] + excl[j];
+    }
   }
   __syncthreads();
 #pragma unroll
   for (int k = 0; k < HL_SORT_ITEMS; ++k) {
     const uint64_t idx = tb + (uint64_t)w * (HL_SORT_ITEMS * 64) + k * 64 + lane;
     if (idx < n) {
-      const uint32_t d = (key[k] >> shift) & 255u;
-      const uint32_t p = tdex[d] + wcnt[w][d] + lr[k];
+      const uint32_t p = tdex[dg[k]] + wcnt[w][dg[k]] + lr[k];
       lk[p] = key[k];
       lv[p] = val[k];
     }
   }
   __syncthreads();
   const uint32_t nv = (uint32_t)min((uint64_t)HL_SORT_TILE, (uint64_t)n - tb);
-  for (uint32_t i = tid; i < nv; i += HL_SORT_BLOCK) {
+#pragma unroll 4
+  for (uint32_t i = tid; i < nv; i += HL_SORT_THREADS) {
     const uint32_t kk = lk[i];
-    const uint32_t d = (kk >> shift) & 255u;
+    const uint32_t d = (kk >> shift) & mask;
     const uint32_t p = gbase[d] + (i - tdex[d]);
     kout[p] = kk;
     vout[p] = lv[i];
   }
 }
 
-hl_status hl_sort_pairs(hl_handle* h, hl_sort_ws& ws, const uint32_t* n_dev, uint32_t n_host, int bits,
-                        hipStream_t s, uint32_t** out_k, uint32_t** out_v) {
-  *out_k = ws.k0;
-  *out_v = ws.v0;
-  if (n_host == 0) return HL_OK;
-  if (n_host > ws.n_max || n_host >= (1u << 30)) return HL_ERR_CAPACITY;
-  if (bits < 1) bits = 1;
-  const int passes = (bits + 7) / 8;
-  if (passes > 4) return HL_ERR_UNSUPPORTED;
-  const uint32_t epoch = hl_next_epoch(h);
+void hl_sort_result(const hl_sort_ws& ws, int bits, uint32_t** out_k, uint32_t** out_v) {
+  const bool odd = srt_make_plan(bits).passes & 1;
+  *out_k = odd ? ws.k1 : ws.k0;
+  *out_v = odd ? ws.v1 : ws.v0;
+}
+
+template <int NB>
+static hl_status srt_launch(hl_handle* h, hl_sort_ws& ws, const uint32_t* n_dev, uint32_t n_host, srt_plan pl,
+                            hipStream_t s) {
   const uint32_t tiles = hl_div_up(n_host, HL_SORT_TILE);
   uint32_t hb = hl_div_up(n_host, HL_SORT_HIST_THREADS * 8);
   hb = hb < 1 ? 1 : (hb > HL_SORT_HIST_BLOCKS ? HL_SORT_HIST_BLOCKS : hb);
-  HL_KERNEL(h, s, "srt_hist", srt_hist, dim3(hb), dim3(HL_SORT_HIST_THREADS), 0, s, ws.k0, n_dev, n_host, passes,
-            ws.part, ws.status, (uint64_t)4 * ws.tiles_max * 256);
+  HL_KERNEL(h, s, "srt_hist", srt_hist<NB>, dim3(hb), dim3(HL_SORT_HIST_THREADS), 0, s, ws.k0, n_dev, n_host,
+            pl.passes, pl.b, ws.part, ws.st[0], (uint64_t)tiles * NB);
   uint32_t *ki = ws.k0, *vi = ws.v0, *ko = ws.k1, *vo = ws.v1;
-  for (int p = 0; p < passes; ++p) {
-    HL_KERNEL(h, s, "srt_pass", srt_pass, dim3(tiles), dim3(HL_SORT_BLOCK), 0, s, ki, vi, ko, vo, n_dev, n_host,
-              8 * p, ws.part + p * 256, hb, ws.status + (size_t)p * ws.tiles_max * 256, ws.ctr + 1 + p, epoch,
-              h->d_err);
+  for (int p = 0; p < pl.passes; ++p) {
+    HL_KERNEL(h, s, "srt_pass", srt_pass<NB>, dim3(tiles), dim3(HL_SORT_THREADS), 0, s, ki, vi, ko, vo, n_dev,
+              n_host, pl.b * p, pl.b, ws.part + (size_t)p * HL_SORT_HIST_BLOCKS * NB, hb, ws.st[p & 1],
+              p + 1 < pl.passes ? ws.st[(p + 1) & 1] : nullptr, ws.ctr + 1 + p, h->d_err);
     uint32_t* t = ki;
     ki = ko;
     ko = t;
@@ -218,7 +333,22 @@ hl_status hl_sort_pairs(hl_handle* h, hl_sort_ws& ws, const uint32_t* n_dev, uin
     vo = t;
   }
   HL_LAUNCHED();
-  *out_k = ki;
-  *out_v = vi;
+  return HL_OK;
+}
+
+hl_status hl_sort_pairs(hl_handle* h, hl_sort_ws& ws, const uint32_t* n_dev, uint32_t n_host, int bits,
+                        hipStream_t s, uint32_t** out_k, uint32_t** out_v) {
+  *out_k = ws.k0;
+  *out_v = ws.v0;
+  if (n_host == 0) return HL_OK;
+  if (n_host > ws.n_max || n_host >= (1u << 30)) return HL_ERR_CAPACITY;
+  if (bits > 32) return HL_ERR_UNSUPPORTED;
+  const srt_plan pl = srt_make_plan(bits);
+  hl_status st;
+  if (pl.nb == 256) st = srt_launch<256>(h, ws, n_dev, n_host, pl, s);
+  else if (pl.nb == 1024) st = srt_launch<1024>(h, ws, n_dev, n_host, pl, s);
+  else st = srt_launch<2048>(h, ws, n_dev, n_host, pl, s);
+  if (st != HL_OK) return st;
+  hl_sort_result(ws, bits, out_k, out_v);
   return HL_OK;
 }

@@ -47,8 +47,13 @@ _SIGS = {
     "hl_partition": (C.c_int, [P, P, I32, P, P, P, P, SZ, P]),
     "hl_remap": (C.c_int, [P, P, I64, P, P]),
     "hl_cold_gather": (C.c_int, [P, P, P, P, I32, I32, I64, P, P, I32, P, P, I32, P, P, P, SZ, P]),
+    "hl_cold_plan": (C.c_int, [P, P, P, P, I32, I32, I64, P, P, I32, I32, P, P, P, SZ, P]),
+    "hl_cold_fetch": (C.c_int, [P, P, P, I32, P, P, P]),
+    "hl_cold_scatter": (C.c_int, [P, P, P, I32, P, P, P]),
     "hl_embbag_fwd": (C.c_int, [P, P, P, I32, P, P, I32, I32, I64, P, P, I32, P, P]),
     "hl_embbag_bwd_sgd": (C.c_int, [P, P, P, I32, P, P, I32, I32, I64, P, P, I32, P, F32, P, SZ, P]),
+    "hl_embbag_bwd_plan": (C.c_int, [P, I32, P, P, I32, I32, I64, P, P, I32, P, SZ, P]),
+    "hl_embbag_bwd_apply": (C.c_int, [P, P, P, I32, I32, I32, I64, P, F32, P, SZ, P]),
     "hl_last_device_error": (C.c_int, [P, C.POINTER(U32)]),
     "hl_trace_enable": (C.c_int, [P, I32]),
     "hl_trace_count": (I32, [P]),
@@ -207,6 +212,24 @@ def hl_cold_gather(h, gids, codes, bag_ptr, n_samples, bags_per_sample, n_lookup
         _p(cold_ids_out), _p(n_cold_dev), _p(ws), _nbytes(ws), _s(stream)))
 
 
+def hl_cold_plan(h, gids, codes, bag_ptr, n_samples, bags_per_sample, n_lookups, sample_ids, n_sel_dev, n_sel_max,
+                 staging_cap_rows, cold_ids_out, n_cold_dev, ws, stream=None):
+    _ck("hl_cold_plan", lib().hl_cold_plan(
+        h.ptr, _p(gids), _p(codes), _p(bag_ptr), int(n_samples), int(bags_per_sample), int(n_lookups),
+        _p(sample_ids), _p(n_sel_dev), int(n_sel_max), int(staging_cap_rows), _p(cold_ids_out), _p(n_cold_dev),
+        _p(ws), _nbytes(ws), _s(stream)))
+
+
+def hl_cold_fetch(h, cold_ids, n_cold_dev, staging_cap_rows, w_host_dev, staging, stream=None):
+    _ck("hl_cold_fetch", lib().hl_cold_fetch(h.ptr, _p(cold_ids), _p(n_cold_dev), int(staging_cap_rows),
+                                             _p(w_host_dev), _p(staging), _s(stream)))
+
+
+def hl_cold_scatter(h, cold_ids, n_cold_dev, staging_cap_rows, staging, w_host_dev, stream=None):
+    _ck("hl_cold_scatter", lib().hl_cold_scatter(h.ptr, _p(cold_ids), _p(n_cold_dev), int(staging_cap_rows),
+                                                 _p(staging), _p(w_host_dev), _s(stream)))
+
+
 def hl_embbag_fwd(h, w_hot, staging, staging_rows, codes, bag_ptr, n_samples, bags_per_sample, n_lookups,
                   sample_ids, n_sel_dev, n_sel_max, out, stream=None):
     _ck("hl_embbag_fwd", lib().hl_embbag_fwd(
@@ -220,6 +243,20 @@ def hl_embbag_bwd_sgd(h, w_hot, staging, staging_rows, codes, bag_ptr, n_samples
         h.ptr, _p(w_hot), _p(staging), int(staging_rows), _p(codes), _p(bag_ptr), int(n_samples),
         int(bags_per_sample), int(n_lookups), _p(sample_ids), _p(n_sel_dev), int(n_sel_max), _p(dY), float(lr),
         _p(ws), _nbytes(ws), _s(stream)))
+
+
+def hl_embbag_bwd_plan(h, staging_rows, codes, bag_ptr, n_samples, bags_per_sample, n_lookups, sample_ids, n_sel_dev,
+                       n_sel_max, ws, stream=None):
+    _ck("hl_embbag_bwd_plan", lib().hl_embbag_bwd_plan(
+        h.ptr, int(staging_rows), _p(codes), _p(bag_ptr), int(n_samples), int(bags_per_sample), int(n_lookups),
+        _p(sample_ids), _p(n_sel_dev), int(n_sel_max), _p(ws), _nbytes(ws), _s(stream)))
+
+
+def hl_embbag_bwd_apply(h, w_hot, staging, staging_rows, n_samples, bags_per_sample, n_lookups, dY, lr, ws,
+                        stream=None):
+    _ck("hl_embbag_bwd_apply", lib().hl_embbag_bwd_apply(
+        h.ptr, _p(w_hot), _p(staging), int(staging_rows), int(n_samples), int(bags_per_sample), int(n_lookups),
+        _p(dY), float(lr), _p(ws), _nbytes(ws), _s(stream)))
 
 
 def hl_last_device_error(h):

@@ -3,7 +3,18 @@ the library calls in the order the paper's pipeline runs them (Sec. IV: the
 learning phase, then per mini-batch classification, fragmentation into the
 popular and non-popular mu-batches, working-parameter gather for the
 non-popular one, forward of both, and the update).  No arithmetic here: every
-step is a call into libhotline."""
+step is a call into libhotline.
+
+The pipelined schedule (the paper's pipeline figure: the popular mu-batch runs
+while the non-popular one's working parameters are gathered) uses three
+streams of default priority:
+  main  : ids, classify, partition, remap, cold plan | fwd(popular) |
+          wait fetch, fwd(non-popular) | wait grouping, backward apply
+  fetch : wait cold plan, row fetch over the host link [, write-back after
+          the apply]
+  group : wait cold plan, the backward's grouping of lookups by code
+The cold id list and count are double-buffered so that a step's write-back
+can still read them while the next step plans."""
 from __future__ import annotations
 
 from dataclasses import dataclass
@@ -37,11 +48,12 @@ def to_device(batch, device, dY=None) -> DevBatch:
 
 
 STAGES = ("gids", "classify", "partition", "remap", "cold_gather", "fwd_pop", "fwd_nonpop", "bwd")
+MODES = ("pipelined", "sequential", "fwdbwd")
 
 
 class HotPath:
     def __init__(self, w: Workload, rows_per_table, table: hl.HostTable, max_lookups: int, max_samples: int,
-                 device="cuda", k_cap: int | None = None, staging_cap: int | None = None):
+                 device="cuda", k_cap: int | None = None, staging_cap: int | None = None, writeback: bool = False):
         self.w = w
         self.device = device
         self.rows_per_table = np.asarray(rows_per_table, dtype=np.uint32)
@@ -68,8 +80,16 @@ class HotPath:
         self.pop = torch.zeros(B, **i32)
         self.nonpop = torch.zeros(B, **i32)
         self.counts = torch.zeros(2, **i32)
-        self.cold_ids = torch.zeros(self.staging_cap, **i32)
-        self.n_cold = torch.zeros(1, **i32)
+        self._cold = [torch.zeros(self.staging_cap, **i32) for _ in range(2)]
+        self._ncold = [torch.zeros(1, **i32) for _ in range(2)]
+        self._par = 0
+        self.cold_ids, self.n_cold = self._cold[0], self._ncold[0]
+        self.writeback = bool(writeback)
+        self.s_fetch = torch.cuda.Stream(device=device)
+        self.s_group = torch.cuda.Stream(device=device)
+        ev = lambda: torch.cuda.Event()
+        self.ev_plan, self.ev_fetch, self.ev_group, self.ev_apply = ev(), ev(), ev(), ev()
+        self.ev_wb = [ev(), ev()]
         self.out = torch.zeros((max(1, max_bags), w.dim), dtype=torch.float32, device=device)
         self.n_hot = 0
 
@@ -90,13 +110,77 @@ class HotPath:
         hl.hl_hot_fill(self.h, self.hot_ids, self.table.dev, self.w_hot)
 
     # ------------------------------------------------------------------ one mini-batch
-    def step(self, b: DevBatch, lr: float | None = None, events=None, split_fwd=True):
+    def step(self, b: DevBatch, lr: float | None = None, events=None, mode: str = "pipelined", split_fwd=True):
         """classify -> partition -> remap -> cold gather (non-popular) -> forward of
-        both mu-batches -> one coalesced SGD step.  `events`: optional list of
-        len(STAGES)+1 torch.cuda.Event recorded around the stages."""
+        both mu-batches -> one coalesced SGD step [-> write-back of the cold rows].
+
+        mode "pipelined": the three-stream schedule of the module docstring.
+        mode "sequential": the fused calls in order on the current stream;
+          `events`: optional list of len(STAGES)+1 torch.cuda.Event recorded
+          around the stages.
+        mode "fwdbwd": as pipelined, but the fetch is awaited before the
+          forward/backward section, which `events` (two events) brackets."""
+        if mode not in MODES:
+            raise ValueError(mode)
         lr = self.w.lr if lr is None else lr
         B, bps, L = b.n_samples, b.bps, b.n_lookups
+        if mode == "sequential":
+            return self._step_sequential(b, lr, events, split_fwd)
+        h, w = self.h, self.w
+        main = torch.cuda.current_stream(self.device)
+        p = self._par
+        self._par ^= 1
+        cold, ncold = self._cold[p], self._ncold[p]
+        self.cold_ids, self.n_cold = cold, ncold
+        hl.hl_lookup_gids(h, b.rows, b.bag_ptr, b.n_bags, self.gids)
+        hl.hl_classify(h, self.gids, b.bag_ptr, B, bps, L, self.flags)
+        hl.hl_partition(h, self.flags, B, self.pop, self.nonpop, self.counts, self.ws)
+        hl.hl_remap(h, self.gids, L, self.codes)
+        if self.writeback:
+            main.wait_event(self.ev_wb[p])  # the write-back two steps ago read this list
+        hl.hl_cold_plan(h, self.gids, self.codes, b.bag_ptr, B, bps, L, self.nonpop, self.counts[1:], B,
+                        self.staging_cap, cold, ncold, self.ws)
+        self.ev_plan.record(main)
+        # working parameters of the non-popular mu-batch over the host link
+        self.s_fetch.wait_event(self.ev_plan)
+        hl.hl_cold_fetch(h, cold, ncold, self.staging_cap, self.table.dev, self.staging, stream=self.s_fetch)
+        self.ev_fetch.record(self.s_fetch)
+        if mode == "fwdbwd":
+            main.wait_event(self.ev_fetch)
+            if events is not None:
+                events[0].record(main)
+        # the backward's grouping needs only the codes
+        self.s_group.wait_event(self.ev_fetch if mode == "fwdbwd" else self.ev_plan)
+        if b.dY is not None:
+            hl.hl_embbag_bwd_plan(h, self.staging_cap, self.codes, b.bag_ptr, B, bps, L, None, None, B, self.ws,
+                                  stream=self.s_group)
+        self.ev_group.record(self.s_group)
+        # popular mu-batch while the fetch runs
+        hl.hl_embbag_fwd(h, self.w_hot, self.staging, self.staging_cap, self.codes, b.bag_ptr, B, bps, L,
+                         self.pop, self.counts[0:], B, self.out)
+        main.wait_event(self.ev_fetch)
+        hl.hl_embbag_fwd(h, self.w_hot, self.staging, self.staging_cap, self.codes, b.bag_ptr, B, bps, L,
+                         self.nonpop, self.counts[1:], B, self.out)
+        main.wait_event(self.ev_group)
+        if b.dY is not None:
+            hl.hl_embbag_bwd_apply(h, self.w_hot, self.staging, self.staging_cap, B, bps, L, b.dY, lr, self.ws)
+        if mode == "fwdbwd" and events is not None:
+            events[1].record(main)
+        if self.writeback:
+            self.ev_apply.record(main)
+            self.s_fetch.wait_event(self.ev_apply)
+            hl.hl_cold_scatter(h, cold, ncold, self.staging_cap, self.staging, self.table.dev, stream=self.s_fetch)
+            self.ev_wb[p].record(self.s_fetch)
+
+    def _step_sequential(self, b, lr, events, split_fwd):
+        B, bps, L = b.n_samples, b.bps, b.n_lookups
         ev = events
+        p = self._par
+        self._par ^= 1
+        self.cold_ids, self.n_cold = self._cold[p], self._ncold[p]
+        main = torch.cuda.current_stream(self.device)
+        if self.writeback:
+            main.wait_event(self.ev_wb[p])
 
         def mark(i):
             if ev is not None:
@@ -129,6 +213,9 @@ class HotPath:
             hl.hl_embbag_bwd_sgd(self.h, self.w_hot, self.staging, self.staging_cap, self.codes, b.bag_ptr, B, bps, L,
                                  None, None, B, b.dY, lr, self.ws)
         mark(8)
+        if self.writeback:
+            hl.hl_cold_scatter(self.h, self.cold_ids, self.n_cold, self.staging_cap, self.staging, self.table.dev)
+            self.ev_wb[p].record(main)
 
     def device_error(self):
         return hl.hl_last_device_error(self.h)

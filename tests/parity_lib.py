@@ -54,8 +54,24 @@ def check_close(got, ref, scale, rtol, what):
                              f"got {got[tuple(i)]!r} ref {ref[tuple(i)]!r} tol {tol[tuple(i)]!r}")
 
 
-def run_gpu_stages(hp: HotPath, prof, mb, dY, k=None, hot_ids=None):
-    """All stages on the GPU, with snapshots.  Either profiles (k) or installs hot_ids."""
+def _on_side(fn):
+    """Run fn(stream) on a fresh side stream ordered after the current stream's
+    work; the current stream then waits for it."""
+    main = torch.cuda.current_stream()
+    side = torch.cuda.Stream()
+    e0, e1 = torch.cuda.Event(), torch.cuda.Event()
+    e0.record(main)
+    side.wait_event(e0)
+    fn(side)
+    e1.record(side)
+    main.wait_event(e1)
+
+
+def run_gpu_stages(hp: HotPath, prof, mb, dY, k=None, hot_ids=None, split=False):
+    """All stages on the GPU, with snapshots.  Either profiles (k) or installs hot_ids.
+    split: the cold gather as plan + fetch and the backward as plan + apply, the
+    fetch and the backward's plan each on a side stream (the pipelined
+    schedule's entry points)."""
     h = hp.h
     r = {}
     dprof = [to_device(p, hp.device) for p in prof]
@@ -86,8 +102,14 @@ def run_gpu_stages(hp: HotPath, prof, mb, dY, k=None, hot_ids=None):
     r["nonpop"] = hp.nonpop[:r["n_nonpop"]].cpu().numpy().copy()
     hl.hl_remap(h, hp.gids, L, hp.codes)
     r["codes_remap"] = hp.codes[:L].cpu().numpy().copy()
-    hl.hl_cold_gather(h, hp.gids, hp.codes, b.bag_ptr, B, bps, L, hp.nonpop, hp.counts[1:], B, hp.table.dev,
-                      hp.staging, hp.staging_cap, hp.cold_ids, hp.n_cold, hp.ws)
+    if split:
+        hl.hl_cold_plan(h, hp.gids, hp.codes, b.bag_ptr, B, bps, L, hp.nonpop, hp.counts[1:], B, hp.staging_cap,
+                        hp.cold_ids, hp.n_cold, hp.ws)
+        _on_side(lambda st: hl.hl_cold_fetch(h, hp.cold_ids, hp.n_cold, hp.staging_cap, hp.table.dev, hp.staging,
+                                             stream=st))
+    else:
+        hl.hl_cold_gather(h, hp.gids, hp.codes, b.bag_ptr, B, bps, L, hp.nonpop, hp.counts[1:], B, hp.table.dev,
+                          hp.staging, hp.staging_cap, hp.cold_ids, hp.n_cold, hp.ws)
     n_cold = int(hp.n_cold.cpu().item())
     r["n_cold"] = n_cold
     r["cold"] = u32(hp.cold_ids[:min(n_cold, hp.staging_cap)])
@@ -99,8 +121,13 @@ def run_gpu_stages(hp: HotPath, prof, mb, dY, k=None, hot_ids=None):
     hl.hl_embbag_fwd(h, hp.w_hot, hp.staging, hp.staging_cap, hp.codes, b.bag_ptr, B, bps, L, hp.nonpop,
                      hp.counts[1:], B, hp.out)
     r["out"] = hp.out[:B * bps].cpu().numpy().copy()
-    hl.hl_embbag_bwd_sgd(h, hp.w_hot, hp.staging, hp.staging_cap, hp.codes, b.bag_ptr, B, bps, L, None, None, B,
-                         b.dY, hp.w.lr, hp.ws)
+    if split:
+        _on_side(lambda st: hl.hl_embbag_bwd_plan(h, hp.staging_cap, hp.codes, b.bag_ptr, B, bps, L, None, None, B,
+                                                  hp.ws, stream=st))
+        hl.hl_embbag_bwd_apply(h, hp.w_hot, hp.staging, hp.staging_cap, B, bps, L, b.dY, hp.w.lr, hp.ws)
+    else:
+        hl.hl_embbag_bwd_sgd(h, hp.w_hot, hp.staging, hp.staging_cap, hp.codes, b.bag_ptr, B, bps, L, None, None,
+                             B, b.dY, hp.w.lr, hp.ws)
     r["w_hot_new"] = hp.w_hot[:n_hot].cpu().numpy().copy()
     r["staging_new"] = hp.staging[:min(n_cold, hp.staging_cap)].cpu().numpy().copy()
     r["deverr"] = hp.device_error()

@@ -86,6 +86,27 @@ def test_hand_example_k2(dtype):
     assert scale[0].tolist() == [4.0, 4.5]
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_hand_example_writeback(dtype):
+    """After the K=2 step, writing the updated cold rows back and taking the hot
+    rows from the cache gives the whole table updated by one SGD step (hand
+    values above); rows no lookup names keep their bits."""
+    g, _ = O.gids(HAND_ROWS_PER_TABLE, HAND_ROWS, HAND_PTR)
+    hot = np.array([1, 4], np.uint32)
+    _, nonpop = O.partition(O.classify(hot, g, HAND_PTR, 3, 2))
+    cold, codes = O.cold_plan(g, O.remap(hot, g), HAND_PTR, nonpop, 2, 2, 2)
+    table = _table(dtype)
+    w_hot, stg = O.gather(table, hot), O.gather(table, cold)
+    O.embbag_bwd_sgd(dtype, w_hot, 2, stg, codes, HAND_PTR, None, 3, 2, HAND_DY, 0.5)
+    host = table.copy()
+    O.scatter(host, cold, stg)
+    assert _as_f64(host[[6, 3]], dtype).tolist() == [[1, 2], [7, 8.5]]
+    for r in (0, 1, 2, 4, 5):
+        assert (host[r] == table[r]).all()
+    host[hot] = w_hot
+    assert _as_f64(host, dtype).tolist() == [[1, 2], [2, 3.5], [5, 6], [7, 8.5], [-1.5, -1], [0, -1], [1, 2]]
+
+
 def test_hand_example_k1_tie_and_multihot():
     g, _ = O.gids(HAND_ROWS_PER_TABLE, HAND_ROWS, HAND_PTR)
     counts, _ = O.count(7, [g])
@@ -261,6 +282,41 @@ def test_forward_backward_vs_torch(seed):
         gid = ids_of_code[code]
         got = w_hot[code] if code < k_cap else stg[code - k_cap]
         assert (got == flat[gid]).all()
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_writeback_round_trip_and_composition(seed):
+    """The write-back against numpy fancy assignment; gather then write-back is the
+    identity; hot cache + written-back staging == the flat-table update (Eq. 5),
+    bit for bit."""
+    c = tiny_case(seed + 300, max_bag=5, dim=3)
+    g, ptr, B, bps, n = c["gids"], c["ptr"], c["B"], c["bps"], c["n_rows"]
+    rng = np.random.default_rng(seed)
+    tab = rng.standard_normal((n, 3)).astype(np.float32)
+    ids = rng.permutation(n)[: max(1, n // 2)].astype(np.uint32)
+    rows = rng.standard_normal((len(ids), 3)).astype(np.float32)
+    a = tab.copy()
+    O.scatter(a, ids, rows)
+    b = tab.copy()
+    b[ids.astype(np.int64)] = rows
+    assert (a == b).all()
+    a = tab.copy()
+    O.scatter(a, ids, O.gather(tab, ids))
+    assert (a == tab).all()
+    counts, _ = O.count(n, [g])
+    hot = O.topk(counts, max(1, n // 4))
+    _, nonpop = O.partition(O.classify(hot, g, ptr, B, bps))
+    k_cap = len(hot) + 1
+    cold, codes = O.cold_plan(g, O.remap(hot, g), ptr, nonpop, len(nonpop), bps, k_cap)
+    dY = rng.standard_normal((B * bps, 3)).astype(np.float32)
+    w_hot, stg = O.gather(tab, hot), O.gather(tab, cold)
+    O.embbag_bwd_sgd("f32", w_hot, k_cap, stg, codes, ptr, None, B, bps, dY, 0.1)
+    host = tab.copy()
+    O.scatter(host, cold, stg)
+    host[hot.astype(np.int64)] = w_hot
+    flat = tab.copy()
+    O.embbag_bwd_sgd_flat("f32", flat, g, ptr, dY, 0.1)
+    assert (host == flat).all()
 
 
 @pytest.mark.parametrize("seed", range(10))

@@ -14,7 +14,7 @@ from parity_lib import as_f64, compare, log, make_table, run_gpu_stages, run_ora
 pytestmark = pytest.mark.gpu
 
 
-def parity_case(w, n_prof=16, idx=16, k=None, hot_ids=None, batches=None):
+def parity_case(w, n_prof=16, idx=16, k=None, hot_ids=None, batches=None, split=False, staging_cap=None):
     rows = W.table_rows(w)
     n_rows = int(rows.sum(dtype=np.int64))
     k_cap = w.k_cap(n_rows)
@@ -27,9 +27,9 @@ def parity_case(w, n_prof=16, idx=16, k=None, hot_ids=None, batches=None):
     log(f"[parity] {w.name}: rows={n_rows} B={mb.n_samples} L={mb.n_lookups} k_cap={k_cap} dim={w.dim} {w.dtype}")
     table = make_table(w, n_rows)
     max_l = max([p.n_lookups for p in prof] + [mb.n_lookups, 1])
-    hp = HotPath(w, rows, table, max_l, max(1, mb.n_samples))
+    hp = HotPath(w, rows, table, max_l, max(1, mb.n_samples), staging_cap=staging_cap)
     try:
-        g = run_gpu_stages(hp, prof, mb, dY, k=k, hot_ids=hot_ids)
+        g = run_gpu_stages(hp, prof, mb, dY, k=k, hot_ids=hot_ids, split=split)
         o = run_oracle(w, rows, prof, mb, dY, table.array, k_cap, k=k, hot_ids=hot_ids)
         compare(w, g, o, k_cap, check_counts=hot_ids is None)
         log(f"[parity] {w.name}: n_hot={len(o['hot'])} pop={len(o['pop'])} cold={len(o['cold'])} ok")
@@ -41,16 +41,19 @@ def parity_case(w, n_prof=16, idx=16, k=None, hot_ids=None, batches=None):
 
 @pytest.mark.parametrize("name", configs.ORDER)
 def test_full_size(name):
-    """Each workload at its full size, in the launch configuration the benchmark times."""
-    parity_case(configs.WORKLOADS[name])
+    """Each workload at its full size, through the entry points the benchmark's
+    pipelined step calls (cold plan + fetch, backward plan + apply, on side
+    streams)."""
+    parity_case(configs.WORKLOADS[name], split=True)
 
 
+@pytest.mark.parametrize("split", [False, True])
 @pytest.mark.parametrize("name", configs.ORDER)
-def test_scaled_ragged(name):
+def test_scaled_ragged(name, split):
     """Smaller tables and a batch that is not a multiple of any tile size."""
     w = configs.WORKLOADS[name]
     w = configs.scaled(w, batch=777, row_scale=0.003 if name != "tiny" else 0.5, name=name + "-ragged")
-    parity_case(w, n_prof=4, idx=5)
+    parity_case(w, n_prof=4, idx=5, split=split)
 
 
 @pytest.mark.parametrize("k", [0, 1, 7, 10**9])
@@ -108,6 +111,22 @@ def test_random_shapes(seed):
     parity_case(w, batches=(prof, mb))
 
 
+@pytest.mark.parametrize("bits", [9, 10, 11, 12, 17, 19, 20, 21, 22, 23])
+def test_backward_key_widths(bits):
+    """The backward's sort keys span n_hot + staging rows: the staging capacity
+    sets their width, and with it the digit width and pass count of the sort
+    (one pass of 9-11 bits; two of 6, 9, 10 or 11; three of 8).  Heavily
+    repeated rows over many tiles."""
+    rng = np.random.default_rng(bits)
+    rows = np.array([64, 40, 100], np.uint32)
+    w = configs.Workload(name=f"keys{bits}", n_tables=3, dim=16, dtype="f32", batch=3000, steps=1,
+                         rows_fixed=tuple(int(r) for r in rows), hot_frac=0.05, seed=bits, lr=0.05)
+    mb = _random_batch(rng, rows, w.batch, 1, 8)
+    hot = np.arange(0, 16, 2, dtype=np.uint32)
+    cap = (1 << (bits - 1)) - len(hot)
+    parity_case(w, batches=([], mb), hot_ids=hot, split=bits % 2 == 0, staging_cap=cap)
+
+
 def test_determinism_and_split_equals_unsplit():
     w = configs.scaled(configs.WORKLOADS["multi-hot"], batch=300, row_scale=0.002, name="mh-det")
     rows = W.table_rows(w)
@@ -117,21 +136,22 @@ def test_determinism_and_split_equals_unsplit():
     mb = W.make_batch(w, rows, 3)
     dY = W.make_dy(w, 3, mb.n_bags)
     results = []
-    for rep in range(2):
+    for mode, split in (("sequential", True), ("sequential", False), ("pipelined", True)):
         hp = HotPath(w, rows, table, max(p.n_lookups for p in prof + [to_device(mb, "cuda")]), w.batch)
         hp.learn(prof)
         b = to_device(mb, "cuda", dY)
-        hp.step(b, split_fwd=(rep == 0))
+        hp.step(b, mode=mode, split_fwd=split)
         torch.cuda.synchronize()
         results.append((hp.out[:mb.n_bags].cpu().numpy().copy(), hp.w_hot[:hp.n_hot].cpu().numpy().copy(),
                         hp.staging.cpu().numpy().copy(), hp.device_error()))
         hp.close()
     table.close()
-    (o1, w1, s1, e1), (o2, w2, s2, e2) = results
-    assert e1 == 0 and e2 == 0
-    assert np.array_equal(o1.view(np.uint32), o2.view(np.uint32)), "pooled output not reproducible / split != unsplit"
-    assert np.array_equal(w1.view(np.uint8), w2.view(np.uint8)), "hot rows not reproducible"
-    assert np.array_equal(s1.view(np.uint8), s2.view(np.uint8)), "staging rows not reproducible"
+    o1, w1, s1, e1 = results[0]
+    for i, (o2, w2, s2, e2) in enumerate(results[1:]):
+        assert e1 == 0 and e2 == 0
+        assert np.array_equal(o1.view(np.uint32), o2.view(np.uint32)), f"pooled output differs (run {i + 1})"
+        assert np.array_equal(w1.view(np.uint8), w2.view(np.uint8)), f"hot rows differ (run {i + 1})"
+        assert np.array_equal(s1.view(np.uint8), s2.view(np.uint8)), f"staging rows differ (run {i + 1})"
 
 
 def test_sample_list_backward():
@@ -225,6 +245,64 @@ def test_capacity_and_range_errors():
         table.close()
 
 
+def test_plan_apply_contract():
+    """The backward's apply needs its plan in the workspace: refused without one,
+    after another workspace call, or with other sizes; applying one plan twice is
+    two SGD steps (against the oracle run twice)."""
+    import oracle as O
+    from parity_lib import check_close
+    w = configs.scaled(configs.WORKLOADS["tiny"], batch=128, row_scale=0.2, name="tiny-contract")
+    rows = W.table_rows(w)
+    n_rows = int(rows.sum())
+    table = make_table(w, n_rows)
+    mb = W.make_batch(w, rows, 0)
+    dY = W.make_dy(w, 0, mb.n_bags)
+    hp = HotPath(w, rows, table, mb.n_lookups, w.batch)
+    try:
+        hot = np.arange(0, n_rows, 2, dtype=np.uint32)[:hp.k_cap]
+        hp.set_hot(torch.from_numpy(hot.view(np.int32)).cuda())
+        b = to_device(mb, "cuda", dY)
+        B, bps, L = b.n_samples, b.bps, b.n_lookups
+        h = hp.h
+        with pytest.raises(hl.HotlineError):
+            hl.hl_embbag_bwd_apply(h, hp.w_hot, hp.staging, hp.staging_cap, B, bps, L, b.dY, w.lr, hp.ws)
+        hl.hl_lookup_gids(h, b.rows, b.bag_ptr, b.n_bags, hp.gids)
+        hl.hl_remap(h, hp.gids, L, hp.codes)
+        hl.hl_embbag_bwd_plan(h, hp.staging_cap, hp.codes, b.bag_ptr, B, bps, L, None, None, B, hp.ws)
+        with pytest.raises(hl.HotlineError):   # other sizes
+            hl.hl_embbag_bwd_apply(h, hp.w_hot, hp.staging, hp.staging_cap, B, bps, L - 1, b.dY, w.lr, hp.ws)
+        # the cold lookups still have code -1 here: the plan reports them
+        assert hp.device_error() & hl.DEVERR["BAD_CODE"]
+        hl.hl_cold_plan(h, hp.gids, hp.codes, b.bag_ptr, B, bps, L, None, None, B, hp.staging_cap, hp.cold_ids,
+                        hp.n_cold, hp.ws)
+        with pytest.raises(hl.HotlineError):   # the cold plan reused the workspace
+            hl.hl_embbag_bwd_apply(h, hp.w_hot, hp.staging, hp.staging_cap, B, bps, L, b.dY, w.lr, hp.ws)
+        hl.hl_cold_fetch(h, hp.cold_ids, hp.n_cold, hp.staging_cap, table.dev, hp.staging)
+        codes = hp.codes[:L].cpu().numpy().copy()
+        n_cold = int(hp.n_cold.item())
+        w0 = hp.w_hot[:len(hot)].cpu().numpy().copy()
+        s0 = hp.staging[:n_cold].cpu().numpy().copy()
+        hl.hl_embbag_bwd_plan(h, hp.staging_cap, hp.codes, b.bag_ptr, B, bps, L, None, None, B, hp.ws)
+        for _ in range(2):
+            hl.hl_embbag_bwd_apply(h, hp.w_hot, hp.staging, hp.staging_cap, B, bps, L, b.dY, w.lr, hp.ws)
+        assert hp.device_error() == 0
+        ow, os_ = w0.copy(), s0.copy()
+        sc = None
+        for _ in range(2):
+            uniq, s1, rc = O.embbag_bwd_sgd(w.dtype, ow, hp.k_cap, os_, codes, mb.bag_ptr, None, B, bps, dY, w.lr,
+                                            want_scale=True)
+            assert rc == 0
+            sc = s1 if sc is None else sc + s1
+        th = uniq[uniq < hp.k_cap]
+        ts = uniq[uniq >= hp.k_cap] - hp.k_cap
+        check_close(hp.w_hot[:len(hot)].cpu().numpy()[th], ow[th], sc[uniq < hp.k_cap], 1e-5, "two applies (hot)")
+        check_close(hp.staging[:n_cold].cpu().numpy()[ts], os_[ts], sc[uniq >= hp.k_cap], 1e-5,
+                    "two applies (staging)")
+    finally:
+        hp.close()
+        table.close()
+
+
 def test_empty_batch():
     w = configs.scaled(configs.WORKLOADS["tiny"], batch=0, row_scale=0.1, name="tiny-empty")
     rows = W.table_rows(w)
@@ -265,12 +343,16 @@ def test_partition_sizes(n):
         table.close()
 
 
+@pytest.mark.parametrize("mode,writeback", [("pipelined", True), ("pipelined", False), ("sequential", True)])
 @pytest.mark.parametrize("name", ["dlrm-large", "multi-hot", "tbsm"])
-def test_multi_step(name):
+def test_multi_step(name, mode, writeback):
     """Several consecutive steps with one workspace and one hot cache (the hot
     cache carries the updates from step to step).  Every step is checked against
-    the oracle run from the same pre-step state (the oracle's hot cache takes the
-    GPU's after each comparison), to the single-step tolerances."""
+    the oracle run from the same pre-step state (the oracle's hot cache, and with
+    write-back its host table, take the GPU's after each comparison), to the
+    single-step tolerances.  With write-back, the host table after a step holds
+    the step's updated staging rows bit for bit at the cold ids and is unchanged
+    elsewhere."""
     import oracle as O
     from parity_lib import check_close
     w = configs.scaled(configs.WORKLOADS[name], batch=600, row_scale=0.004, name=name + "-steps")
@@ -281,7 +363,7 @@ def test_multi_step(name):
     table = make_table(w, n_rows)
     prof = [W.make_batch(w, rows, i) for i in range(4)]
     steps = [W.make_batch(w, rows, 4 + s) for s in range(4)]
-    hp = HotPath(w, rows, table, max(b.n_lookups for b in prof + steps), w.batch)
+    hp = HotPath(w, rows, table, max(b.n_lookups for b in prof + steps), w.batch, writeback=writeback)
     try:
         hp.learn([to_device(p, "cuda") for p in prof])
         counts = np.zeros(n_rows, np.uint32)
@@ -294,8 +376,9 @@ def test_multi_step(name):
             pre = hp.w_hot[:len(hot)].cpu().numpy().copy()
             assert si > 0 or np.array_equal(pre.view(np.uint8), w_hot.view(np.uint8))
             w_hot = pre.copy()
+            tab_pre = table.array.copy()
             dY = W.make_dy(w, 4 + si, mb.n_bags)
-            hp.step(to_device(mb, "cuda", dY))
+            hp.step(to_device(mb, "cuda", dY), mode=mode)
             torch.cuda.synchronize()
             assert hp.device_error() == 0, f"step {si}"
             B, bps, L = mb.n_samples, mb.bags_per_sample, mb.n_lookups
@@ -303,7 +386,7 @@ def test_multi_step(name):
             flags = O.classify(hot, g, mb.bag_ptr, B, bps)
             pop, nonpop = O.partition(flags)
             cold, codes = O.cold_plan(g, O.remap(hot, g), mb.bag_ptr, nonpop, len(nonpop), bps, k_cap)
-            stg = O.gather(table.array, cold)
+            stg = O.gather(tab_pre, cold)
             out, sc, _ = O.embbag_fwd(w.dtype, w_hot, k_cap, stg, codes, mb.bag_ptr, None, B, bps, B * bps,
                                       want_scale=True)
             assert np.array_equal(hp.flags[:B].cpu().numpy(), flags), f"step {si} flags"
@@ -322,6 +405,13 @@ def test_multi_step(name):
             check_close(as_f64(gst[ts], w.dtype), as_f64(stg[ts], w.dtype), usc[~hu], rtol, f"step {si} staging rows")
             untouched = np.setdiff1d(np.arange(len(hot)), uniq[hu])
             assert np.array_equal(gw[untouched].view(np.uint8), pre[untouched].view(np.uint8)), f"step {si}"
+            tab = table.array
+            if writeback:
+                ref_tab = tab_pre.copy()
+                O.scatter(ref_tab, cold, gst)
+                assert np.array_equal(tab.view(np.uint8), ref_tab.view(np.uint8)), f"step {si} write-back"
+            else:
+                assert np.array_equal(tab.view(np.uint8), tab_pre.view(np.uint8)), f"step {si} host table changed"
     finally:
         hp.close()
         table.close()
