@@ -131,10 +131,11 @@ hl_status hl_hot_fill(const hl_handle* h, const uint32_t* hot_ids, const void* w
 /* Mini-batch shape used below: n_samples samples of bags_per_sample bags,
  * bag_ptr[n_samples*bags_per_sample + 1] (device), and n_lookups (host) =
  * bag_ptr[n_samples*bags_per_sample] (a mismatch sets HL_DEVERR_SHAPE).
- * Sample selection (mu-batch calls): sample_ids == NULL selects every
- * sample; otherwise sample_ids[0..n) with n = *n_sel_dev when n_sel_dev is
- * not NULL (a device count, e.g. from hl_partition) else n_sel_max; n must
- * not exceed n_sel_max. */
+ * Sample selection (mu-batch calls): sample_ids == NULL selects samples
+ * 0..n_sel_max-1 (every sample when n_sel_max = n_samples); otherwise
+ * sample_ids[0..n) with n = *n_sel_dev when n_sel_dev is not NULL (a device
+ * count, e.g. from hl_partition) else n_sel_max; n must not exceed
+ * n_sel_max. */
 
 /* -------------------------------------------------------- classification --
  * flags[b] = 1 iff every lookup of sample b names a hot row, else 0 (a single

@@ -3,40 +3,42 @@
 // the pinned host table by the GPU over the host link, with the lookups'
 // codes pointed at the staging rows.
 //
-//   insert   : every selected lookup with code -1 enters an open-addressing
-//              hash table keyed by row id; a 64-bit atomic min keeps the
-//              smallest lookup index per id; the lookup is also appended to a
-//              list (one atomic per block)
-//   rank     : a scan over all lookups in index order (decoupled look-back)
-//              numbers the first occurrences: staging row u of each id
-//   codes    : capacity check, code rewrite and the cold id list
-//   copy     : the row copy between the pinned host table and the staging
-//              rows, in either direction (fetch before the mu-batch runs,
-//              write-back of the updated rows after it)
-// The plan (insert, rank, codes) uses the workspace, which is shared with
-// other calls, so its table is cleared at the start of every call.  The copy
-// reads only the cold id list and count, so it can run on a stream of its own
-// while the popular mu-batch and the backward's grouping proceed (the overlap
-// of the paper's pipeline, Sec. IV and Fig. "hotlinepipe").
+//   insert : a block per 256 bags; each round a wave compacts its cold
+//            lookups (code -1, sample selected) so that a lane handles about
+//            one, which enters an open-addressing hash table keyed by row id
+//            with one CAS (a 64-bit atomic min keeps the smallest lookup index
+//            per id); the block lists its cold lookups in its own lookup range
+//   rank   : a scan over all lookups in index order (tiles of 1024, decoupled
+//            look-back read by a whole wave) numbers the first occurrences:
+//            staging row u of each id
+//   codes  : capacity check, code rewrite, the cold id list, and the clearing
+//            of the table slots this call used
+//   copy   : the row copy between the pinned host table and the staging rows,
+//            in either direction (fetch before the mu-batch runs, write-back
+//            of the updated rows after it)
+// The hash table belongs to the handle (cleared once, then left clean by every
+// call); the rest lives in the workspace.  The copy reads only the cold id
+// list and count, so it can run on a stream of its own while the popular
+// mu-batch and the backward's grouping proceed (the overlap of the paper's
+// pipeline, Sec. IV and Fig. "hotlinepipe").
 #include "hl_internal.h"
 
-#define CG_C_LIST 0
 #define CG_C_NCOLD 1
 #define CG_C_RTILE 2
-#define CG_C_SNAP 3
-#define CG_RTILE 8192     // lookups per rank tile (512 threads x 16)
-#define CG_MAX_SPB 2048   // selected samples per insert block
-#define CG_FIRST 0x80000000u
+#define CG_BAGS 256      // bags per insert block
+#define CG_IR 1024       // lookup positions per insert round (256 threads x 4)
+#define CG_RT 1024       // lookups per rank tile (256 threads x 4)
 
 struct cg_ws {
   uint32_t* ctr;      // header counters
-  uint64_t* table;    // [S] (id + 1) << 32 | smallest lookup index; 0 = empty
   uint32_t* uidx;     // [S] staging row of the id in the slot
   uint32_t* slotof;   // [n_max] slot of a cold lookup
-  uint32_t* list;     // [n_max] lookup indices of the cold lookups
+  uint32_t* blist;    // [n_max] cold lookups of insert block b at [bag_ptr[b * CG_BAGS], ...)
+  uint32_t* bcnt;     // [iblocks] their number
   uint32_t* fst;      // [n_max] id of staging row u
   uint64_t* rstat;    // [rtiles] look-back status of the rank scan
-  uint32_t S, rtiles;
+  uint8_t* mask;      // [max_samples] selected samples (when a sample list is given)
+  uint32_t S, rtiles, iblocks;
 };
 
 static uint32_t cg_table_slots(uint32_t n_max) {
@@ -45,24 +47,43 @@ static uint32_t cg_table_slots(uint32_t n_max) {
   return s;
 }
 
-static void cg_carve(hl_carver& c, cg_ws& ws, uint32_t n_max) {
+static void cg_carve(hl_carver& c, cg_ws& ws, uint32_t n_max, int64_t n_bags, int32_t n_samples) {
   ws.S = cg_table_slots(n_max);
-  ws.rtiles = n_max ? hl_div_up(n_max, CG_RTILE) : 1;
+  ws.rtiles = n_max ? hl_div_up(n_max, CG_RT) : 1;
+  ws.iblocks = n_bags > 0 ? hl_div_up((uint64_t)n_bags, CG_BAGS) : 1;
   ws.ctr = c.base ? c.header() + HL_HDR_COLD : nullptr;
-  ws.table = c.take<uint64_t>(ws.S);
   ws.uidx = c.take<uint32_t>(ws.S);
   ws.slotof = c.take<uint32_t>(n_max);
-  ws.list = c.take<uint32_t>(n_max);
+  ws.blist = c.take<uint32_t>(n_max);
+  ws.bcnt = c.take<uint32_t>(ws.iblocks);
   ws.fst = c.take<uint32_t>(n_max);
   ws.rstat = c.take<uint64_t>(ws.rtiles);
+  ws.mask = c.take<uint8_t>((size_t)n_samples + 1);
 }
 
-size_t hl_cold_ws_bytes(const hl_handle* h, int64_t max_lookups) {
+size_t hl_cold_ws_bytes(const hl_handle* h, int64_t max_lookups, int64_t max_bags, int32_t max_samples) {
   (void)h;
   hl_carver c = hl_carver::after_header(nullptr, 0);
   cg_ws ws;
-  cg_carve(c, ws, (uint32_t)max_lookups);
+  cg_carve(c, ws, (uint32_t)max_lookups, max_bags, max_samples);
   return c.off;
+}
+
+// The handle's hash table, (id + 1) << 32 | smallest lookup index per slot, 0
+// = empty; grown (and zeroed) when a call needs more slots.
+static hl_status cg_table(hl_handle* h, uint32_t S, hipStream_t s, uint64_t** out) {
+  if (h->cg_slots < S) {
+    if (h->cg_table) {
+      if (hipFree(h->cg_table) != hipSuccess) return HL_ERR_HIP;
+      h->cg_table = nullptr;
+      h->cg_slots = 0;
+    }
+    if (hipMalloc(&h->cg_table, (size_t)S * 8) != hipSuccess) return HL_ERR_HIP;
+    if (hipMemsetAsync(h->cg_table, 0, (size_t)S * 8, s) != hipSuccess) return HL_ERR_HIP;
+    h->cg_slots = S;
+  }
+  *out = h->cg_table;
+  return HL_OK;
 }
 
 __device__ __forceinline__ uint32_t cg_hash(uint32_t x) {  // 32-bit finalising mix
@@ -74,162 +95,152 @@ __device__ __forceinline__ uint32_t cg_hash(uint32_t x) {  // 32-bit finalising 
   return x;
 }
 
-__global__ void __launch_bounds__(256) cg_clear(cg_ws ws) {
-  for (uint32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < ws.S; i += gridDim.x * blockDim.x) ws.table[i] = 0;
-  for (uint32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < ws.rtiles; i += gridDim.x * blockDim.x)
-    ws.rstat[i] = 0;
+__global__ void cg_mask(uint8_t* mask, int32_t n_samples, const int32_t* __restrict__ ids, const int32_t* n_dev,
+                        int32_t n_max, int phase, uint32_t* err) {
+  if (phase == 0) {
+    for (int32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < n_samples; i += gridDim.x * blockDim.x) mask[i] = 0;
+  } else {
+    int32_t n = n_max;
+    if (n_dev) n = min(max(*n_dev, 0), n_max);
+    for (int32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) {
+      const int32_t s = ids[i];
+      if (s >= 0 && s < n_samples) mask[s] = 1;
+      else hl_flag(err, HL_DEVERR_OUT_OF_RANGE);
+    }
+  }
 }
 
-// A block owns `spb` consecutive selected samples; their lookup ranges are laid
-// end to end in LDS (start, inclusive prefix of lengths) and threads walk the
-// concatenation in rounds of 8 positions per thread, finding their sample by
-// binary search.  Each round issues its loads stage by stage for all 8
-// positions (codes, then ids, then the first hash probe) so that they overlap.
-#define CG_IPT 8
 __global__ void __launch_bounds__(256)
-cg_insert(const uint32_t* __restrict__ gids, const int32_t* __restrict__ codes,
-          const int32_t* __restrict__ bag_ptr, int32_t n_samples, int32_t bps,
-          const int32_t* __restrict__ sample_ids, const int32_t* n_sel_dev, int32_t n_sel_max, int32_t spb,
-          uint64_t n_rows, cg_ws ws, uint32_t n_max, uint32_t* err) {
-  __shared__ int32_t st[CG_MAX_SPB], pre[CG_MAX_SPB + 1];
-  __shared__ uint32_t buf[256 * CG_IPT];
-  __shared__ uint32_t bn, bbase, wsum[4];
-  int32_t n_sel = n_sel_max;
-  if (sample_ids && n_sel_dev) n_sel = min(max(*n_sel_dev, 0), n_sel_max);
-  const int64_t q0 = (int64_t)blockIdx.x * spb;
-  const int ns = (int)max((int64_t)0, min((int64_t)spb, (int64_t)n_sel - q0));
-  for (int j = threadIdx.x; j < ns; j += blockDim.x) {
-    const int64_t s = sample_ids ? sample_ids[q0 + j] : q0 + j;
-    int32_t a = 0, b = 0;
-    if (s >= 0 && s < n_samples) {
-      a = bag_ptr[s * bps];
-      b = bag_ptr[(s + 1) * bps];
-    } else {
-      hl_flag(err, HL_DEVERR_OUT_OF_RANGE);
-    }
-    st[j] = a;
-    pre[j + 1] = b - a;
-  }
-  if (threadIdx.x == 0) pre[0] = 0;
+cg_insert(const uint32_t* __restrict__ gids, const int32_t* __restrict__ codes, const int32_t* __restrict__ bag_ptr,
+          int64_t n_bags, int32_t bps, const uint8_t* __restrict__ mask, uint32_t n_lookups, uint64_t n_rows,
+          uint64_t* table, cg_ws ws, uint32_t* err) {
+  __shared__ int32_t off[CG_BAGS + 1];
+  __shared__ uint32_t cl[CG_IR];
+  __shared__ uint32_t wn[4], s_total;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int64_t b0 = (int64_t)blockIdx.x * CG_BAGS;
+  const int nb = (int)min((int64_t)CG_BAGS, n_bags - b0);
+  for (int j = tid; j <= nb; j += 256) off[j] = bag_ptr[b0 + j];
   __syncthreads();
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  {  // block-wide inclusive scan of the lengths (up to 8 per thread, blocked)
-    const int per = (ns + 255) / 256;
-    uint32_t loc = 0;
-    for (int k = 0; k < per; ++k) {
-      const int j = threadIdx.x * per + k;
-      if (j < ns) loc += (uint32_t)pre[j + 1];
-    }
-    uint32_t inc = loc;
-    for (int o = 1; o < 64; o <<= 1) {
-      const uint32_t t = __shfl_up(inc, o);
-      if (lane >= o) inc += t;
-    }
-    if (lane == 63) wsum[w] = inc;
-    __syncthreads();
-    uint32_t run = inc - loc;
-    for (int j = 0; j < w; ++j) run += wsum[j];
-    for (int k = 0; k < per; ++k) {
-      const int j = threadIdx.x * per + k;
-      if (j < ns) {
-        run += (uint32_t)pre[j + 1];
-        pre[j + 1] = (int32_t)run;
-      }
-    }
-  }
-  __syncthreads();
-  const int32_t total = pre[ns];
+  const int32_t lo = off[0], hi = (int32_t)min((int64_t)off[nb], (int64_t)n_lookups);
   const uint64_t lt = (1ull << lane) - 1ull;
   const uint32_t smask = ws.S - 1;
-  for (int32_t r0 = 0; r0 < total; r0 += 256 * CG_IPT) {
-    if (threadIdx.x == 0) bn = 0;
-    int32_t idx[CG_IPT];
-    int32_t cd[CG_IPT];
-    uint32_t g[CG_IPT], slot[CG_IPT];
-    uint64_t cur[CG_IPT];
+  uint32_t listed = 0;  // block-wide count so far (uniform)
+  for (int32_t r0 = lo; r0 < hi; r0 += CG_IR) {
+    // positions r0 + k*256 + tid: cold and selected?
+    bool cold[4];
+    int32_t pos[4];
 #pragma unroll
-    for (int k = 0; k < CG_IPT; ++k) {
-      const int32_t t = r0 + k * 256 + threadIdx.x;
-      idx[k] = -1;
-      if (t < total) {
-        int a = 0, b = ns;
+    for (int k = 0; k < 4; ++k) {
+      pos[k] = r0 + k * 256 + tid;
+      cold[k] = pos[k] < hi && codes[pos[k]] == -1;
+    }
+    if (mask) {
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        if (!cold[k]) continue;
+        int a = 0, b = nb;
         while (b - a > 1) {
-          int m = (a + b) >> 1;
-          if (pre[m] <= t) a = m; else b = m;
+          const int m = (a + b) >> 1;
+          if (off[m] <= pos[k]) a = m; else b = m;
         }
-        idx[k] = st[a] + (t - pre[a]);
+        cold[k] = mask[(b0 + a) / bps] != 0;
       }
     }
+    // compact the round's cold positions into cl (wave-major, then item, then lane)
+    uint32_t c = 0;
+    uint64_t m[4];
 #pragma unroll
-    for (int k = 0; k < CG_IPT; ++k) cd[k] = idx[k] >= 0 ? codes[idx[k]] : 0;
-#pragma unroll
-    for (int k = 0; k < CG_IPT; ++k) g[k] = (idx[k] >= 0 && cd[k] == -1) ? gids[idx[k]] : 0xFFFFFFFFu;
-#pragma unroll
-    for (int k = 0; k < CG_IPT; ++k) {
-      if (idx[k] >= 0 && cd[k] == -1 && g[k] >= n_rows) hl_flag(err, HL_DEVERR_OUT_OF_RANGE);
-      slot[k] = cg_hash(g[k]) & smask;
-      cur[k] = g[k] < n_rows ? ws.table[slot[k]] : 0ull;
+    for (int k = 0; k < 4; ++k) {
+      m[k] = __ballot(cold[k]);
+      c += (uint32_t)__popcll(m[k]);
     }
-    bool take[CG_IPT];
+    if (lane == 0) wn[w] = c;
+    __syncthreads();
+    uint32_t base = 0, tot = 0;
+    for (int q = 0; q < 4; ++q) {
+      if (q < w) base += wn[q];
+      tot += wn[q];
+    }
 #pragma unroll
-    for (int k = 0; k < CG_IPT; ++k) {
-      take[k] = g[k] < n_rows;
-      if (!take[k]) continue;
-      const uint64_t want = ((uint64_t)(g[k] + 1) << 32) | (uint32_t)idx[k];
-      uint64_t c = cur[k];
+    for (int k = 0; k < 4; ++k) {
+      if (cold[k]) cl[base + (uint32_t)__popcll(m[k] & lt)] = (uint32_t)pos[k];
+      base += (uint32_t)__popcll(m[k]);
+    }
+    __syncthreads();
+    // each thread inserts about one lookup
+    for (uint32_t e = tid; e < tot; e += 256) {
+      const uint32_t i = cl[e];
+      const uint32_t g = gids[i];
+      if (g >= n_rows) {
+        hl_flag(err, HL_DEVERR_OUT_OF_RANGE);
+        ws.slotof[i] = 0xFFFFFFFFu;
+        continue;
+      }
+      const uint64_t want = ((uint64_t)(g + 1) << 32) | i;
+      uint32_t slot = cg_hash(g) & smask;
       for (uint32_t probe = 0; probe <= smask; ++probe) {
-        if ((c >> 32) == 0) {
-          c = atomicCAS((unsigned long long*)(ws.table + slot[k]), 0ull, (unsigned long long)want);
-          if (c == 0) break;
-        }
-        if ((uint32_t)(c >> 32) == g[k] + 1) {
-          atomicMin((unsigned long long*)(ws.table + slot[k]), (unsigned long long)want);
+        const uint64_t prev = atomicCAS((unsigned long long*)(table + slot), 0ull, (unsigned long long)want);
+        if (prev == 0) break;
+        if ((uint32_t)(prev >> 32) == g + 1) {
+          atomicMin((unsigned long long*)(table + slot), (unsigned long long)want);
           break;
         }
-        slot[k] = (slot[k] + 1) & smask;
-        c = ws.table[slot[k]];
+        slot = (slot + 1) & smask;
       }
-      ws.slotof[idx[k]] = slot[k];
+      ws.slotof[i] = slot;
+      ws.blist[lo + listed + e] = i;
     }
-    __syncthreads();  // bn reset visible
-#pragma unroll
-    for (int k = 0; k < CG_IPT; ++k) {
-      const uint64_t m = __ballot(take[k]);
-      if (m) {
-        uint32_t base = 0;
-        if (lane == 0) base = atomicAdd(&bn, (uint32_t)__popcll(m));
-        base = __shfl(base, 0);
-        if (take[k]) buf[base + (uint32_t)__popcll(m & lt)] = (uint32_t)idx[k];
-      }
-    }
-    __syncthreads();
-    const uint32_t cnt = bn;
-    if (threadIdx.x == 0 && cnt) bbase = atomicAdd(ws.ctr + CG_C_LIST, cnt);
-    __syncthreads();
-    for (uint32_t j = threadIdx.x; j < cnt; j += blockDim.x) {
-      const uint32_t p = bbase + j;
-      if (p < n_max) ws.list[p] = buf[j];
-      else hl_flag(err, HL_DEVERR_OUT_OF_RANGE);  // a sample listed twice
-    }
-    __syncthreads();
+    listed += tot;
+    __syncthreads();  // cl and wn reused
   }
+  if (tid == 0) ws.bcnt[blockIdx.x] = listed;
 }
 
-// Scan over the mini-batch's lookups in index order.  Lookup i is a first
-// occurrence iff it is a cold lookup of this call whose slot holds (its id,
-// i); the running count of first occurrences numbers the staging rows.  Tiles
-// of 8192 lookups (512 threads x 16), so one look-back window reaches tile 0.
-#define CG_RT_THREADS 512
-#define CG_RT_ITEMS 16
-__global__ void __launch_bounds__(CG_RT_THREADS)
-cg_rank(const uint32_t* __restrict__ gids, const int32_t* __restrict__ codes, uint32_t n_lookups, cg_ws ws,
-        int32_t* n_cold_dev, uint32_t epoch, uint32_t* err) {
-  __shared__ uint32_t s_tile, wt[CG_RT_THREADS / 64], s_excl;
+// Exclusive prefix of this tile's count over earlier tiles, read by all 64
+// lanes of one wave: lane j looks at tile (tile - 1 - j) of the current window.
+__device__ __forceinline__ uint32_t cg_wave_lookback(const uint64_t* st, uint32_t tile, uint32_t epoch, uint32_t* err) {
+  const int lane = threadIdx.x & 63;
+  uint32_t excl = 0, spins = 0;
+  int64_t j = (int64_t)tile - 1;
+  while (j >= 0) {
+    const int64_t p = j - lane;
+    const uint64_t wd = p >= 0 ? hl_st_load(st + p) : hl_st_pack(epoch, HL_ST_PRE, 0);
+    const uint32_t e = (uint32_t)(wd >> 32);
+    const uint32_t f = (uint32_t)((wd >> 30) & 3ull);
+    const bool ok = e == epoch && f != 0;
+    const uint64_t pre = __ballot(ok && f == HL_ST_PRE), bad = __ballot(!ok);
+    const int fp = pre ? __ffsll((unsigned long long)pre) - 1 : 64;
+    const int fb = bad ? __ffsll((unsigned long long)bad) - 1 : 64;
+    const int use = fb < fp ? fb : (fp < 64 ? fp + 1 : 64);  // lanes [0, use) are consumed
+    uint32_t v = lane < use ? (uint32_t)(wd & 0x3FFFFFFFu) : 0u;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+    excl += v;
+    if (fb >= fp && fp < 64) break;  // reached a tile with its inclusive prefix
+    j -= use;
+    if (fb < fp) {
+      if (++spins > HL_SPIN_LIMIT) {
+        hl_flag(err, HL_DEVERR_STALL);
+        break;
+      }
+      __builtin_amdgcn_s_sleep(1);
+    }
+  }
+  return excl;
+}
+
+// Lookup i is a first occurrence iff it is a cold lookup of this call whose
+// slot holds (its id, i); the running count of first occurrences numbers the
+// staging rows.
+__global__ void __launch_bounds__(256)
+cg_rank(const uint32_t* __restrict__ gids, const int32_t* __restrict__ codes, uint32_t n_lookups,
+        const uint64_t* __restrict__ table, cg_ws ws, int32_t* n_cold_dev, uint32_t epoch, uint32_t* err) {
+  __shared__ uint32_t s_tile, wt[4], s_excl;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   if (tid == 0) s_tile = atomicInc(ws.ctr + CG_C_RTILE, gridDim.x - 1);
   __syncthreads();
   const uint32_t tile = s_tile;
-  if (tile == 0 && tid == 0) ws.ctr[CG_C_SNAP] = ws.ctr[CG_C_LIST];
   if (n_lookups == 0) {
     if (tile == 0 && tid == 0) {
       ws.ctr[CG_C_NCOLD] = 0;
@@ -237,54 +248,54 @@ cg_rank(const uint32_t* __restrict__ gids, const int32_t* __restrict__ codes, ui
     }
     return;
   }
-  const uint64_t tb = (uint64_t)tile * CG_RTILE;
+  const uint64_t tb = (uint64_t)tile * CG_RT;
   if (tb >= n_lookups) return;
   const uint64_t lt = (1ull << lane) - 1ull;
-  bool first[CG_RT_ITEMS];
-  int32_t cd[CG_RT_ITEMS];
-  uint32_t slot[CG_RT_ITEMS], g[CG_RT_ITEMS];
+  int32_t cd[4];
+  uint32_t slot[4], g[4];
+  bool first[4];
 #pragma unroll
-  for (int k = 0; k < CG_RT_ITEMS; ++k) {
-    const uint64_t i = tb + (uint64_t)w * (64 * CG_RT_ITEMS) + k * 64 + lane;
+  for (int k = 0; k < 4; ++k) {
+    const uint64_t i = tb + w * 256 + k * 64 + lane;
     cd[k] = i < n_lookups ? codes[i] : 0;
   }
 #pragma unroll
-  for (int k = 0; k < CG_RT_ITEMS; ++k) {
-    const uint64_t i = tb + (uint64_t)w * (64 * CG_RT_ITEMS) + k * 64 + lane;
+  for (int k = 0; k < 4; ++k) {
+    const uint64_t i = tb + w * 256 + k * 64 + lane;
     slot[k] = cd[k] == -1 ? ws.slotof[i] : 0xFFFFFFFFu;
     g[k] = cd[k] == -1 ? gids[i] : 0u;
   }
   uint32_t wsum = 0;
 #pragma unroll
-  for (int k = 0; k < CG_RT_ITEMS; ++k) {
-    const uint64_t i = tb + (uint64_t)w * (64 * CG_RT_ITEMS) + k * 64 + lane;
+  for (int k = 0; k < 4; ++k) {
+    const uint64_t i = tb + w * 256 + k * 64 + lane;
     bool f = false;
-    if (slot[k] < ws.S)  // a slot from an earlier call fails the test below
-      f = ws.table[slot[k]] == (((uint64_t)(g[k] + 1) << 32) | (uint32_t)i);
+    if (slot[k] < ws.S)  // a slot left by an earlier call fails the test below
+      f = table[slot[k]] == (((uint64_t)(g[k] + 1) << 32) | (uint32_t)i);
     first[k] = f;
     wsum += (uint32_t)__popcll(__ballot(f));
   }
   if (lane == 0) wt[w] = wsum;
   __syncthreads();
   uint32_t before = 0, tc = 0;
-  for (int j = 0; j < CG_RT_THREADS / 64; ++j) {
-    if (j < w) before += wt[j];
-    tc += wt[j];
+  for (int q = 0; q < 4; ++q) {
+    if (q < w) before += wt[q];
+    tc += wt[q];
   }
-  if (tid == 0) {
-    hl_st_store(ws.rstat + tile, hl_st_pack(epoch, tile == 0 ? HL_ST_PRE : HL_ST_AGG, tc));
+  if (w == 0) {
+    if (lane == 0) hl_st_store(ws.rstat + tile, hl_st_pack(epoch, tile == 0 ? HL_ST_PRE : HL_ST_AGG, tc));
     uint32_t ex = 0;
     if (tile > 0) {
-      ex = hl_lookback(ws.rstat, tile, 1, epoch, err);
-      hl_st_store(ws.rstat + tile, hl_st_pack(epoch, HL_ST_PRE, ex + tc));
+      ex = cg_wave_lookback(ws.rstat, tile, epoch, err);
+      if (lane == 0) hl_st_store(ws.rstat + tile, hl_st_pack(epoch, HL_ST_PRE, ex + tc));
     }
-    s_excl = ex;
+    if (lane == 0) s_excl = ex;
   }
   __syncthreads();
   uint32_t run = s_excl + before;
 #pragma unroll
-  for (int k = 0; k < CG_RT_ITEMS; ++k) {
-    const uint64_t i = tb + (uint64_t)w * (64 * CG_RT_ITEMS) + k * 64 + lane;
+  for (int k = 0; k < 4; ++k) {
+    const uint64_t i = tb + w * 256 + k * 64 + lane;
     const uint64_t m = __ballot(first[k]);
     if (first[k]) {
       const uint32_t u = run + (uint32_t)__popcll(m & lt);
@@ -299,25 +310,27 @@ cg_rank(const uint32_t* __restrict__ gids, const int32_t* __restrict__ codes, ui
   }
 }
 
-// Every listed cold lookup points its code at its staging row; cold_ids[u] =
-// id of staging row u.  Nothing but the error bit and the list reset when the
-// rows do not fit.
+// Insert block b's listed cold lookups point their codes at their staging
+// rows and free their table slots; cold_ids[u] = id of staging row u.  When
+// the rows do not fit: only the capacity bit and the slot clearing.
 __global__ void __launch_bounds__(256)
-cg_codes(cg_ws ws, uint32_t n_max, int32_t cap, uint32_t k_cap, int32_t* __restrict__ codes,
-         uint32_t* __restrict__ cold_ids, uint32_t* err) {
-  const uint32_t n_list = min(ws.ctr[CG_C_SNAP], n_max), ncold = ws.ctr[CG_C_NCOLD];
+cg_codes(const int32_t* __restrict__ bag_ptr, uint64_t* table, cg_ws ws, int32_t cap, uint32_t k_cap,
+         int32_t* __restrict__ codes, uint32_t* __restrict__ cold_ids, uint32_t* err) {
+  const uint32_t ncold = ws.ctr[CG_C_NCOLD];
   const bool fits = ncold <= (uint32_t)cap;
-  if (blockIdx.x == 0 && threadIdx.x == 0) {
-    ws.ctr[CG_C_LIST] = 0;  // ready for the next call
-    if (!fits) hl_flag(err, HL_DEVERR_CAPACITY);
+  if (blockIdx.x == 0 && threadIdx.x == 0 && !fits) hl_flag(err, HL_DEVERR_CAPACITY);
+  const uint32_t cnt = ws.bcnt[blockIdx.x];
+  const int32_t lo = bag_ptr[(int64_t)blockIdx.x * CG_BAGS];
+  for (uint32_t e = threadIdx.x; e < cnt; e += 256) {
+    const uint32_t i = ws.blist[lo + e];
+    const uint32_t sl = ws.slotof[i];
+    if (sl >= ws.S) continue;
+    if (fits) codes[i] = (int32_t)(k_cap + ws.uidx[sl]);
+    table[sl] = 0;
   }
   if (!fits) return;
-  const uint32_t gs = gridDim.x * blockDim.x, t0 = blockIdx.x * blockDim.x + threadIdx.x;
-  for (uint32_t e = t0; e < n_list; e += gs) {
-    const uint32_t i = ws.list[e];
-    codes[i] = (int32_t)(k_cap + ws.uidx[ws.slotof[i]]);
-  }
-  for (uint32_t u = t0; u < ncold; u += gs) cold_ids[u] = ws.fst[u];
+  const uint32_t gs = gridDim.x * blockDim.x;
+  for (uint32_t u = blockIdx.x * blockDim.x + threadIdx.x; u < ncold; u += gs) cold_ids[u] = ws.fst[u];
 }
 
 // Row copy between host table and staging rows: TO_HOST = 0 copies
@@ -395,28 +408,42 @@ extern "C" hl_status hl_cold_plan(hl_handle* h, const uint32_t* gids, int32_t* c
   if (!sample_ids && n_sel_max > n_samples) return HL_ERR_INVALID_ARG;
   if (n_lookups > 0 && (!gids || !codes || (cap > 0 && !cold_ids_out))) return HL_ERR_INVALID_ARG;
   if (n_lookups >= (1ll << 30) || (uint64_t)h->k_cap + (uint64_t)cap >= (1ull << 31)) return HL_ERR_UNSUPPORTED;
-  if (ws_bytes < hl_cold_ws_bytes(h, n_lookups)) return HL_ERR_CAPACITY;
+  if ((int64_t)n_samples * bps >= (1ll << 31)) return HL_ERR_UNSUPPORTED;
+  const int64_t n_bags = (int64_t)n_samples * bps;
+  if (ws_bytes < hl_cold_ws_bytes(h, n_lookups, n_bags, n_samples)) return HL_ERR_CAPACITY;
   hl_ws_note(h, workspace, HL_WSK_OTHER);
   hipStream_t s = (hipStream_t)stream;
   hl_carver c = hl_carver::after_header(workspace, ws_bytes);
   cg_ws ws;
-  cg_carve(c, ws, (uint32_t)n_lookups);
-  const uint32_t n_max = (uint32_t)n_lookups;
-  // about 2048 lookups per insert block
-  int64_t spb = n_lookups > 0 && n_samples > 0 ? (2048ll * n_samples + n_lookups - 1) / n_lookups : CG_MAX_SPB;
-  spb = spb < 1 ? 1 : (spb > CG_MAX_SPB ? CG_MAX_SPB : spb);
-  const uint32_t iblocks = n_sel_max > 0 ? hl_div_up(n_sel_max, spb) : 1;
-  uint32_t cb = hl_div_up(ws.S, 256 * 4);
-  HL_KERNEL(h, s, "cg_clear", cg_clear, dim3(cb), dim3(256), 0, s, ws);
-  HL_KERNEL(h, s, "cg_insert", cg_insert, dim3(iblocks), dim3(256), 0, s, gids, codes, bag_ptr, n_samples, bps,
-            sample_ids, n_sel_dev, n_sel_max, (int32_t)spb, h->n_rows, ws, n_max, h->d_err);
+  cg_carve(c, ws, (uint32_t)n_lookups, n_bags, n_samples);
+  uint64_t* table = nullptr;
+  hl_status st = cg_table(h, ws.S, s, &table);
+  if (st != HL_OK) return st;
+  const uint32_t n = (uint32_t)n_lookups;
+  // selection: every sample (no list) or the listed ones (a mask over samples);
+  // an empty selection inserts nothing
+  const uint8_t* mask = nullptr;
+  if (sample_ids) {
+    uint32_t gb = hl_div_up(n_samples > 0 ? n_samples : 1, 256);
+    if (gb > 4096) gb = 4096;
+    HL_KERNEL(h, s, "cg_mask", cg_mask, dim3(gb), dim3(256), 0, s, ws.mask, n_samples, sample_ids, n_sel_dev,
+              n_sel_max, 0, h->d_err);
+    HL_KERNEL(h, s, "cg_mask", cg_mask, dim3(gb), dim3(256), 0, s, ws.mask, n_samples, sample_ids, n_sel_dev,
+              n_sel_max, 1, h->d_err);
+    mask = ws.mask;
+  }
+  // without a list the first n_sel_max samples are selected: their bags come first
+  const int64_t sel_bags = sample_ids ? n_bags : (int64_t)n_sel_max * bps;
+  const uint32_t ib = sel_bags > 0 ? hl_div_up((uint64_t)sel_bags, CG_BAGS) : 0;
+  if (ib > 0)
+    HL_KERNEL(h, s, "cg_insert", cg_insert, dim3(ib), dim3(256), 0, s, gids, codes, bag_ptr, sel_bags, bps, mask, n,
+              h->n_rows, table, ws, h->d_err);
   const uint32_t epoch = hl_next_epoch(h);
-  HL_KERNEL(h, s, "cg_rank", cg_rank, dim3(ws.rtiles), dim3(CG_RT_THREADS), 0, s, gids, codes, n_max, ws, n_cold_dev, epoch,
-            h->d_err);
-  uint32_t g = hl_div_up(n_max ? n_max : 1, 256);
-  if (g > 1024) g = 1024;
-  HL_KERNEL(h, s, "cg_codes", cg_codes, dim3(g), dim3(256), 0, s, ws, n_max, cap, h->k_cap, codes, cold_ids_out,
-            h->d_err);
+  HL_KERNEL(h, s, "cg_rank", cg_rank, dim3(ws.rtiles), dim3(256), 0, s, gids, codes, ib > 0 ? n : 0u, table, ws,
+            n_cold_dev, epoch, h->d_err);
+  if (ib > 0)
+    HL_KERNEL(h, s, "cg_codes", cg_codes, dim3(ib), dim3(256), 0, s, bag_ptr, table, ws, cap, h->k_cap, codes,
+              cold_ids_out, h->d_err);
   HL_LAUNCHED();
   return HL_OK;
 }

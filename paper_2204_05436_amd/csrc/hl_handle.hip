@@ -9,7 +9,7 @@
 
 size_t hl_topk_scratch_bytes(uint64_t n_rows);
 size_t hl_partition_ws_bytes(int32_t max_samples);
-size_t hl_cold_ws_bytes(const hl_handle* h, int64_t max_lookups);
+size_t hl_cold_ws_bytes(const hl_handle* h, int64_t max_lookups, int64_t max_bags, int32_t max_samples);
 size_t hl_bwd_ws_bytes(const hl_handle* h, int64_t max_lookups, int64_t max_bags);
 
 extern "C" const char* hl_status_string(hl_status s) {
@@ -161,7 +161,7 @@ extern "C" hl_status hl_create(hl_handle** out, int32_t n_tables, const uint32_t
 
 extern "C" hl_status hl_destroy(hl_handle* h) {
   if (!h) return HL_ERR_INVALID_ARG;
-  void* ps[] = {h->d_base, h->d_rows, h->d_counts, h->d_bitmap, h->d_rank, h->d_err, h->d_tk};
+  void* ps[] = {h->d_base, h->d_rows, h->d_counts, h->d_bitmap, h->d_rank, h->d_err, h->d_tk, h->cg_table};
   hl_status st = HL_OK;
   if (h->trace) {
     trace_free(h->trace);
@@ -181,7 +181,7 @@ extern "C" size_t hl_workspace_bytes(const hl_handle* h, int64_t max_lookups, in
                                      int32_t max_samples) {
   if (!h || max_lookups < 0 || max_bags < 0 || max_samples < 0) return 0;
   size_t a = hl_partition_ws_bytes(max_samples);
-  size_t b = hl_cold_ws_bytes(h, max_lookups);
+  size_t b = hl_cold_ws_bytes(h, max_lookups, max_bags, max_samples);
   size_t c = hl_bwd_ws_bytes(h, max_lookups, max_bags);
   size_t m = a > b ? a : b;
   m = m > c ? m : c;

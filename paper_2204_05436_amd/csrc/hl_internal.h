@@ -54,6 +54,8 @@ struct hl_handle {
   int ws_kind;           // HL_WSK_*
   int64_t ws_n, ws_bags; // its lookups and bags
   int32_t ws_stg;        // its staging rows
+  uint64_t* cg_table;    // cold-gather hash table (kept clean between calls)
+  uint32_t cg_slots;     // its slots
 };
 #define HL_WSK_NONE 0
 #define HL_WSK_OTHER 1

@@ -138,8 +138,10 @@ class HotPath:
         hl.hl_remap(h, self.gids, L, self.codes)
         if self.writeback:
             main.wait_event(self.ev_wb[p])  # the write-back two steps ago read this list
-        hl.hl_cold_plan(h, self.gids, self.codes, b.bag_ptr, B, bps, L, self.nonpop, self.counts[1:], B,
-                        self.staging_cap, cold, ncold, self.ws)
+        # a cold lookup makes its sample non-popular, so the cold lookups of all
+        # samples are those of the non-popular mu-batch: no sample list needed
+        hl.hl_cold_plan(h, self.gids, self.codes, b.bag_ptr, B, bps, L, None, None, B, self.staging_cap, cold, ncold,
+                        self.ws)
         self.ev_plan.record(main)
         # working parameters of the non-popular mu-batch over the host link
         self.s_fetch.wait_event(self.ev_plan)

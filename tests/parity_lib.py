@@ -103,7 +103,9 @@ def run_gpu_stages(hp: HotPath, prof, mb, dY, k=None, hot_ids=None, split=False)
     hl.hl_remap(h, hp.gids, L, hp.codes)
     r["codes_remap"] = hp.codes[:L].cpu().numpy().copy()
     if split:
-        hl.hl_cold_plan(h, hp.gids, hp.codes, b.bag_ptr, B, bps, L, hp.nonpop, hp.counts[1:], B, hp.staging_cap,
+        # as the pipelined step calls it: no sample list (cold lookups occur only
+        # in non-popular samples)
+        hl.hl_cold_plan(h, hp.gids, hp.codes, b.bag_ptr, B, bps, L, None, None, B, hp.staging_cap,
                         hp.cold_ids, hp.n_cold, hp.ws)
         _on_side(lambda st: hl.hl_cold_fetch(h, hp.cold_ids, hp.n_cold, hp.staging_cap, hp.table.dev, hp.staging,
                                              stream=st))
