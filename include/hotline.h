@@ -157,6 +157,17 @@ hl_status hl_partition(hl_handle* h, const uint8_t* flags, int32_t n_samples, in
 hl_status hl_remap(const hl_handle* h, const uint32_t* gids, int64_t n, int32_t* codes,
                    hl_stream stream);
 
+/* The Data Dispatcher of Sec. V-A in one pass over the mini-batch: the
+ * results of hl_lookup_gids (gids), hl_classify (flags), hl_partition
+ * (pop_ids, nonpop_ids, counts_dev) and hl_remap (codes), bit for bit, with
+ * the same error behaviour.  The workspace (hl_workspace_bytes) holds its
+ * cross-block state in the header; mini-batches too large for that state take
+ * the four calls in turn. */
+hl_status hl_dispatch(hl_handle* h, const uint32_t* rows, const int32_t* bag_ptr, int32_t n_samples,
+                      int32_t bags_per_sample, int64_t n_lookups, uint32_t* gids, int32_t* codes,
+                      uint8_t* flags, int32_t* pop_ids, int32_t* nonpop_ids, int32_t* counts_dev,
+                      void* workspace, size_t ws_bytes, hl_stream stream);
+
 /* ------------------------------------------------------------ cold gather --
  * Working parameters of a mu-batch (Sec. V-A: DMA reads of non-hot rows from
  * CPU memory; dma_rd of the ISA).  Over the lookups of the selected samples

@@ -70,7 +70,9 @@ size_t hl_cold_ws_bytes(const hl_handle* h, int64_t max_lookups, int64_t max_bag
 }
 
 // The handle's hash table, (id + 1) << 32 | smallest lookup index per slot, 0
-// = empty; grown (and zeroed) when a call needs more slots.
+// = empty; grown (and zeroed) when a call needs more slots.  The growth
+// allocates, so a caller that captures calls into a graph makes one call of
+// the largest size first.
 static hl_status cg_table(hl_handle* h, uint32_t S, hipStream_t s, uint64_t** out) {
   if (h->cg_slots < S) {
     if (h->cg_table) {
@@ -79,8 +81,9 @@ static hl_status cg_table(hl_handle* h, uint32_t S, hipStream_t s, uint64_t** ou
       h->cg_slots = 0;
     }
     if (hipMalloc(&h->cg_table, (size_t)S * 8) != hipSuccess) return HL_ERR_HIP;
-    if (hipMemsetAsync(h->cg_table, 0, (size_t)S * 8, s) != hipSuccess) return HL_ERR_HIP;
     h->cg_slots = S;
+    hl_status st = hl_fill32((uint32_t*)h->cg_table, (uint64_t)S * 2, 0, s);
+    if (st != HL_OK) return st;
   }
   *out = h->cg_table;
   return HL_OK;
@@ -123,6 +126,8 @@ cg_insert(const uint32_t* __restrict__ gids, const int32_t* __restrict__ codes, 
   for (int j = tid; j <= nb; j += 256) off[j] = bag_ptr[b0 + j];
   __syncthreads();
   const int32_t lo = off[0], hi = (int32_t)min((int64_t)off[nb], (int64_t)n_lookups);
+  // the rank scan's status words, cleared for the kernel that follows
+  for (uint32_t j = blockIdx.x * 256 + tid; j < ws.rtiles; j += gridDim.x * 256) ws.rstat[j] = 0;
   const uint64_t lt = (1ull << lane) - 1ull;
   const uint32_t smask = ws.S - 1;
   uint32_t listed = 0;  // block-wide count so far (uniform)
@@ -336,8 +341,12 @@ cg_codes(const int32_t* __restrict__ bag_ptr, uint64_t* table, cg_ws ws, int32_t
 // Row copy between host table and staging rows: TO_HOST = 0 copies
 // staging[u] = host[ids[u]], TO_HOST = 1 copies host[ids[u]] = staging[u], for
 // u < *n_dev.  A count above cap copies nothing and sets the capacity bit; an
-// id >= n_rows is skipped and sets the range bit.  The grid is kept small (the
-// host link, not the CUs, bounds it) and each thread keeps 4 units in flight.
+// id >= n_rows is skipped and sets the range bit.  Each thread keeps 4 units in
+// flight.  64 blocks already hold enough reads in flight to fill the host link
+// (measured: fewer blocks lose bandwidth, more gain none); more blocks only fill
+// the shared memory pipeline with slow host reads, which then stall the HBM
+// traffic of kernels running beside the copy on other streams (a concurrent
+// streaming kernel ran 5.5x slower beside 512 copy blocks, 1.5x beside 64).
 template <typename V, bool TO_HOST>
 __global__ void __launch_bounds__(256)
 cg_copy(const uint32_t* __restrict__ ids, const int32_t* n_dev, int32_t cap, uint64_t n_rows, V* host, V* stg,
@@ -382,7 +391,7 @@ static hl_status cg_launch_copy(hl_handle* h, const uint32_t* ids, const int32_t
   const uint32_t rb = h->row_bytes;
   uint64_t units = (uint64_t)(cap > 0 ? cap : 1) * (rb / 4);
   uint32_t g = (uint32_t)((units + 1023) / 1024);
-  g = g < 1 ? 1 : (g > 512 ? 512 : g);
+  g = g < 1 ? 1 : (g > 64 ? 64 : g);
 #define CG_COPY(V)                                                                                             \
   if (to_host)                                                                                                 \
     HL_KERNEL(h, s, "cg_scatter", (cg_copy<V, true>), dim3(g), dim3(256), 0, s, ids, n_dev, cap, h->n_rows,     \
@@ -438,7 +447,9 @@ extern "C" hl_status hl_cold_plan(hl_handle* h, const uint32_t* gids, int32_t* c
   if (ib > 0)
     HL_KERNEL(h, s, "cg_insert", cg_insert, dim3(ib), dim3(256), 0, s, gids, codes, bag_ptr, sel_bags, bps, mask, n,
               h->n_rows, table, ws, h->d_err);
-  const uint32_t epoch = hl_next_epoch(h);
+  // the insert kernel cleared the status words, so one fixed tag serves every
+  // call (and every replay of a captured graph)
+  const uint32_t epoch = 1;
   HL_KERNEL(h, s, "cg_rank", cg_rank, dim3(ws.rtiles), dim3(256), 0, s, gids, codes, ib > 0 ? n : 0u, table, ws,
             n_cold_dev, epoch, h->d_err);
   if (ib > 0)

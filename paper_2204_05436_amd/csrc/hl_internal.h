@@ -112,9 +112,12 @@ __device__ __forceinline__ int32_t hl_hot_slot(const uint64_t* __restrict__ bm,
 // Every workspace starts with a fixed header of self-resetting counters (their
 // place must not depend on the sizes of a call); buffers are carved after it
 // with 256-byte alignment.
-#define HL_WS_HEADER 4096
+#define HL_WS_HEADER 16384
 #define HL_HDR_SORT 0    // 8 words: histogram done counter, per-pass tile counters
 #define HL_HDR_COLD 16   // 16 words: cold-gather counters
+#define HL_HDR_DISP 64   // 8 words: dispatch epoch, done counter, tile counter
+#define HL_HDR_DSTAT 128 // dispatch look-back status words (64-bit), to the header's end
+#define HL_DISP_MAX_TILES ((HL_WS_HEADER - 4 * HL_HDR_DSTAT) / 8)
 // First and only place a new epoch is drawn: never 0 (zeroed status words) and
 // never all-ones.
 static inline uint32_t hl_next_epoch(hl_handle* h) {

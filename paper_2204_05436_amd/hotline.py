@@ -46,6 +46,7 @@ _SIGS = {
     "hl_classify": (C.c_int, [P, P, P, I32, I32, I64, P, P]),
     "hl_partition": (C.c_int, [P, P, I32, P, P, P, P, SZ, P]),
     "hl_remap": (C.c_int, [P, P, I64, P, P]),
+    "hl_dispatch": (C.c_int, [P, P, P, I32, I32, I64, P, P, P, P, P, P, P, SZ, P]),
     "hl_cold_gather": (C.c_int, [P, P, P, P, I32, I32, I64, P, P, I32, P, P, I32, P, P, P, SZ, P]),
     "hl_cold_plan": (C.c_int, [P, P, P, P, I32, I32, I64, P, P, I32, I32, P, P, P, SZ, P]),
     "hl_cold_fetch": (C.c_int, [P, P, P, I32, P, P, P]),
@@ -202,6 +203,14 @@ def hl_partition(h, flags, n_samples, pop_ids, nonpop_ids, counts_dev, ws, strea
 
 def hl_remap(h, gids, n, codes, stream=None):
     _ck("hl_remap", lib().hl_remap(h.ptr, _p(gids), int(n), _p(codes), _s(stream)))
+
+
+def hl_dispatch(h, rows, bag_ptr, n_samples, bags_per_sample, n_lookups, gids, codes, flags, pop_ids, nonpop_ids,
+                counts_dev, ws, stream=None):
+    _ck("hl_dispatch", lib().hl_dispatch(
+        h.ptr, _p(rows), _p(bag_ptr), int(n_samples), int(bags_per_sample), int(n_lookups), _p(gids), _p(codes),
+        _p(flags), _p(pop_ids), _p(nonpop_ids), _p(counts_dev), _p(ws), 0 if ws is None else _nbytes(ws),
+        _s(stream)))
 
 
 def hl_cold_gather(h, gids, codes, bag_ptr, n_samples, bags_per_sample, n_lookups, sample_ids, n_sel_dev, n_sel_max,

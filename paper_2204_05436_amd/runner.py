@@ -8,7 +8,7 @@ step is a call into libhotline.
 The pipelined schedule (the paper's pipeline figure: the popular mu-batch runs
 while the non-popular one's working parameters are gathered) uses three
 streams of default priority:
-  main  : ids, classify, partition, remap, cold plan | fwd(popular) |
+  main  : dispatch (ids, classify, partition, remap), cold plan | fwd(popular) |
           wait fetch, fwd(non-popular) | wait grouping, backward apply
   fetch : wait cold plan, row fetch over the host link [, write-back after
           the apply]
@@ -128,15 +128,14 @@ class HotPath:
             return self._step_sequential(b, lr, events, split_fwd)
         h, w = self.h, self.w
         main = torch.cuda.current_stream(self.device)
+        capturing = torch.cuda.is_current_stream_capturing()
         p = self._par
         self._par ^= 1
         cold, ncold = self._cold[p], self._ncold[p]
         self.cold_ids, self.n_cold = cold, ncold
-        hl.hl_lookup_gids(h, b.rows, b.bag_ptr, b.n_bags, self.gids)
-        hl.hl_classify(h, self.gids, b.bag_ptr, B, bps, L, self.flags)
-        hl.hl_partition(h, self.flags, B, self.pop, self.nonpop, self.counts, self.ws)
-        hl.hl_remap(h, self.gids, L, self.codes)
-        if self.writeback:
+        hl.hl_dispatch(h, b.rows, b.bag_ptr, B, bps, L, self.gids, self.codes, self.flags, self.pop, self.nonpop,
+                       self.counts, self.ws)
+        if self.writeback and not capturing:
             main.wait_event(self.ev_wb[p])  # the write-back two steps ago read this list
         # a cold lookup makes its sample non-popular, so the cold lookups of all
         # samples are those of the non-popular mu-batch: no sample list needed
@@ -173,6 +172,19 @@ class HotPath:
             self.s_fetch.wait_event(self.ev_apply)
             hl.hl_cold_scatter(h, cold, ncold, self.staging_cap, self.staging, self.table.dev, stream=self.s_fetch)
             self.ev_wb[p].record(self.s_fetch)
+            if capturing:  # a graph joins every stream it forked
+                main.wait_event(self.ev_wb[p])
+
+    def capture(self, b: DevBatch, lr: float | None = None):
+        """A HIP graph of one pipelined step over batch b: replaying it runs the
+        whole step (all three streams, joined) with one launch.  Run one eager
+        step of at least this size first (the cold plan's hash table is
+        allocated on first use).  Returns (graph, cold_ids, n_cold): the
+        buffers the graph's cold plan writes."""
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            self.step(b, lr=lr, mode="pipelined")
+        return g, self.cold_ids, self.n_cold
 
     def _step_sequential(self, b, lr, events, split_fwd):
         B, bps, L = b.n_samples, b.bps, b.n_lookups

@@ -69,9 +69,10 @@ def _on_side(fn):
 
 def run_gpu_stages(hp: HotPath, prof, mb, dY, k=None, hot_ids=None, split=False):
     """All stages on the GPU, with snapshots.  Either profiles (k) or installs hot_ids.
-    split: the cold gather as plan + fetch and the backward as plan + apply, the
-    fetch and the backward's plan each on a side stream (the pipelined
-    schedule's entry points)."""
+    split: the dispatch kernel for ids, classify, partition and remap, the cold
+    gather as plan + fetch and the backward as plan + apply, the fetch and the
+    backward's plan each on a side stream (the pipelined schedule's entry
+    points)."""
     h = hp.h
     r = {}
     dprof = [to_device(p, hp.device) for p in prof]
@@ -91,16 +92,23 @@ def run_gpu_stages(hp: HotPath, prof, mb, dY, k=None, hot_ids=None, split=False)
     r["w_hot_pre"] = hp.w_hot[:n_hot].cpu().numpy().copy()
     b = to_device(mb, hp.device, dY)
     B, bps, L = b.n_samples, b.bps, b.n_lookups
-    hl.hl_lookup_gids(h, b.rows, b.bag_ptr, b.n_bags, hp.gids)
-    r["gids"] = u32(hp.gids[:L])
-    hl.hl_classify(h, hp.gids, b.bag_ptr, B, bps, L, hp.flags)
-    r["flags"] = hp.flags[:B].cpu().numpy().copy()
-    hl.hl_partition(h, hp.flags, B, hp.pop, hp.nonpop, hp.counts, hp.ws)
+    if split:  # the dispatch kernel, as the pipelined step calls it
+        hl.hl_dispatch(h, b.rows, b.bag_ptr, B, bps, L, hp.gids, hp.codes, hp.flags, hp.pop, hp.nonpop, hp.counts,
+                       hp.ws)
+        r["gids"] = u32(hp.gids[:L])
+        r["flags"] = hp.flags[:B].cpu().numpy().copy()
+    else:
+        hl.hl_lookup_gids(h, b.rows, b.bag_ptr, b.n_bags, hp.gids)
+        r["gids"] = u32(hp.gids[:L])
+        hl.hl_classify(h, hp.gids, b.bag_ptr, B, bps, L, hp.flags)
+        r["flags"] = hp.flags[:B].cpu().numpy().copy()
+        hl.hl_partition(h, hp.flags, B, hp.pop, hp.nonpop, hp.counts, hp.ws)
     cnts = hp.counts.cpu().numpy()
     r["n_pop"], r["n_nonpop"] = int(cnts[0]), int(cnts[1])
     r["pop"] = hp.pop[:r["n_pop"]].cpu().numpy().copy()
     r["nonpop"] = hp.nonpop[:r["n_nonpop"]].cpu().numpy().copy()
-    hl.hl_remap(h, hp.gids, L, hp.codes)
+    if not split:
+        hl.hl_remap(h, hp.gids, L, hp.codes)
     r["codes_remap"] = hp.codes[:L].cpu().numpy().copy()
     if split:
         # as the pipelined step calls it: no sample list (cold lookups occur only

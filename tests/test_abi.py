@@ -24,7 +24,7 @@ def test_header_declares_the_path():
     names = declared()
     for n in ["hl_create", "hl_profile_count", "hl_profile_topk", "hl_classify", "hl_partition", "hl_remap",
               "hl_cold_gather", "hl_cold_plan", "hl_cold_fetch", "hl_cold_scatter", "hl_embbag_fwd",
-              "hl_embbag_bwd_sgd", "hl_embbag_bwd_plan", "hl_embbag_bwd_apply", "hl_last_device_error"]:
+              "hl_embbag_bwd_sgd", "hl_embbag_bwd_plan", "hl_embbag_bwd_apply", "hl_dispatch", "hl_last_device_error"]:
         assert n in names
 
 
@@ -54,6 +54,7 @@ def test_host_side_validation():
     assert L.hl_embbag_fwd(None, None, None, 0, None, None, 1, 1, 1, None, None, 1, None, None) == 1
     assert L.hl_last_device_error(None, None) == 1
     assert L.hl_cold_fetch(None, None, None, 1, None, None, None) == 1
+    assert L.hl_dispatch(None, None, None, 1, 1, 1, None, None, None, None, None, None, None, 0, None) == 1
     assert L.hl_cold_scatter(None, None, None, 1, None, None, None) == 1
     assert L.hl_cold_plan(None, None, None, None, 1, 1, 1, None, None, 1, 1, None, None, None, 0, None) == 1
     assert L.hl_embbag_bwd_plan(None, 0, None, None, 1, 1, 1, None, None, 1, None, 0, None) == 1

@@ -303,6 +303,46 @@ def test_plan_apply_contract():
         table.close()
 
 
+@pytest.mark.parametrize("B,T,max_len", [(1, 3, 4), (777, 26, 1), (5000, 26, 1), (100_000, 1, 1), (3000, 8, 40),
+                                         (1_300_000, 1, 1), (60_000, 26, 1)])
+def test_dispatch_shapes(B, T, max_len):
+    """The dispatch kernel against the oracle's ids, classify, partition and remap:
+    one tile to ~2000 tiles, ragged tails, multi-hot bags, and sizes beyond its
+    look-back state (which take the four calls in turn); three calls in a row
+    (the device-side epoch advances)."""
+    import oracle as O
+    rng = np.random.default_rng(B + T)
+    rows = rng.integers(50, 5000, T).astype(np.uint32)
+    w = configs.Workload(name=f"disp{B}", n_tables=T, dim=4, dtype="f32", batch=B, steps=1,
+                         rows_fixed=tuple(int(r) for r in rows), hot_frac=0.3, seed=B)
+    n_rows = int(rows.sum())
+    table = make_table(w, n_rows)
+    batches = [_random_batch(rng, rows, B, 1, max_len, zero_frac=0.05 if max_len > 1 else 0.0) for _ in range(3)]
+    hp = HotPath(w, rows, table, max(b.n_lookups for b in batches), B)
+    try:
+        hot = np.sort(rng.choice(n_rows, int(0.7 * n_rows), replace=False)).astype(np.uint32)[:hp.k_cap]
+        hp.set_hot(torch.from_numpy(hot.view(np.int32)).cuda())
+        for mb in batches:
+            b = to_device(mb, "cuda")
+            L = b.n_lookups
+            hl.hl_dispatch(hp.h, b.rows, b.bag_ptr, B, T, L, hp.gids, hp.codes, hp.flags, hp.pop, hp.nonpop,
+                           hp.counts, hp.ws)
+            g, _ = O.gids(rows, mb.rows, mb.bag_ptr)
+            flags = O.classify(hot, g, mb.bag_ptr, B, T)
+            pop, nonpop = O.partition(flags)
+            c = hp.counts.cpu().numpy()
+            assert np.array_equal(hp.gids[:L].cpu().numpy().view(np.uint32), g)
+            assert np.array_equal(hp.codes[:L].cpu().numpy(), O.remap(hot, g))
+            assert np.array_equal(hp.flags[:B].cpu().numpy(), flags)
+            assert c[0] == len(pop) and c[1] == len(nonpop)
+            assert np.array_equal(hp.pop[:c[0]].cpu().numpy(), pop)
+            assert np.array_equal(hp.nonpop[:c[1]].cpu().numpy(), nonpop)
+            assert hp.device_error() == 0
+    finally:
+        hp.close()
+        table.close()
+
+
 def test_empty_batch():
     w = configs.scaled(configs.WORKLOADS["tiny"], batch=0, row_scale=0.1, name="tiny-empty")
     rows = W.table_rows(w)
@@ -338,6 +378,60 @@ def test_partition_sizes(n):
         assert c[0] == f.sum() and c[1] == n - f.sum()
         assert np.array_equal(hp.pop[:c[0]].cpu().numpy(), np.flatnonzero(f))
         assert np.array_equal(hp.nonpop[:c[1]].cpu().numpy(), np.flatnonzero(f == 0))
+    finally:
+        hp.close()
+        table.close()
+
+
+@pytest.mark.parametrize("name,writeback", [("dlrm-large", False), ("multi-hot", True), ("tbsm", True)])
+def test_graph_replay(name, writeback):
+    """A HIP graph of the pipelined step (the benchmark's timed unit) replays to
+    the eager step's results bit for bit, three times, with eager steps on
+    another batch and synchronizations between the replays."""
+    w = configs.scaled(configs.WORKLOADS[name], batch=600, row_scale=0.004, name=name + "-graph")
+    rows = W.table_rows(w)
+    n_rows = int(rows.sum())
+    table = make_table(w, n_rows)
+    prof = [W.make_batch(w, rows, i) for i in range(3)]
+    mba, mbb = W.make_batch(w, rows, 3), W.make_batch(w, rows, 4)
+    da = to_device(mba, "cuda", W.make_dy(w, 3, mba.n_bags))
+    db = to_device(mbb, "cuda", W.make_dy(w, 4, mbb.n_bags))
+    hp = HotPath(w, rows, table, max(b.n_lookups for b in prof + [mba, mbb]), w.batch, writeback=writeback)
+    try:
+        hp.learn([to_device(p, "cuda") for p in prof])
+        torch.cuda.synchronize()
+        w0, tab0 = hp.w_hot.clone(), table.array.copy()
+
+        def state():
+            torch.cuda.synchronize()
+            n = int(hp.n_cold.item())
+            return dict(out=hp.out[:mba.n_bags].cpu().numpy().copy(), w_hot=hp.w_hot[:hp.n_hot].cpu().numpy().copy(),
+                        stg=hp.staging[:n].cpu().numpy().copy(), cold=hp.cold_ids[:n].cpu().numpy().copy(),
+                        codes=hp.codes[:mba.n_lookups].cpu().numpy().copy(), tab=table.array.copy())
+
+        def reset():
+            torch.cuda.synchronize()
+            hp.w_hot.copy_(w0)
+            table.array[:] = tab0
+            torch.cuda.synchronize()
+
+        hp.step(da)
+        ref = state()
+        assert hp.device_error() == 0
+        reset()
+        g, cold, ncold = hp.capture(da)
+        for rep in range(3):
+            reset()
+            g.replay()
+            torch.cuda.synchronize()
+            hp.cold_ids, hp.n_cold = cold, ncold
+            got = state()
+            assert hp.device_error() == 0, f"replay {rep}"
+            for k in ref:
+                assert np.array_equal(got[k].view(np.uint8), ref[k].view(np.uint8)), f"replay {rep}: {k} differs"
+            hp.step(db)  # eager work between replays
+            torch.cuda.synchronize()
+            assert hp.device_error() == 0
     finally:
         hp.close()
         table.close()
