@@ -205,6 +205,12 @@ hl_status hl_cold_plan(hl_handle* h, const uint32_t* gids, int32_t* codes, const
 hl_status hl_cold_fetch(hl_handle* h, const uint32_t* cold_ids, const int32_t* n_cold_dev,
                         int32_t staging_cap_rows, const void* w_host, void* staging, hl_stream stream);
 
+/* Allocates now (and zero-fills on `stream`) the handle's cold-gather hash
+ * table for calls of up to max_lookups lookups, which hl_cold_plan would
+ * otherwise allocate on first use; callers that capture the plan into a graph
+ * reserve first. */
+hl_status hl_cold_reserve(hl_handle* h, int64_t max_lookups, hl_stream stream);
+
 /* Write-back of the updated working parameters (Sec. IV: non-hot rows are
  * updated in CPU main memory by DMA; dma_wr of the ISA): w_host[cold_ids[u]] =
  * staging[u] bit for bit, for u < *n_cold_dev, over the host link.  The ids
@@ -226,6 +232,19 @@ hl_status hl_embbag_fwd(const hl_handle* h, const void* w_hot, const void* stagi
                         int32_t n_samples, int32_t bags_per_sample, int64_t n_lookups,
                         const int32_t* sample_ids, const int32_t* n_sel_dev, int32_t n_sel_max,
                         float* out, hl_stream stream);
+
+/* hl_embbag_fwd in halves (the non-popular mu-batch's hot rows are in GPU
+ * memory before its working parameters arrive, Sec. IV): a bag's sum takes its
+ * hot rows first, then its staging rows, each in lookup order, so that part 1
+ * (hot rows only; out = the partial sum, 0 for a bag without hot rows) followed
+ * by part 2 (staging rows only, added onto out; bags without staging rows are
+ * not touched) gives out bit for bit as part 0 (hl_embbag_fwd) does.  Part 1
+ * reads no staging row. */
+hl_status hl_embbag_fwd_part(const hl_handle* h, const void* w_hot, const void* staging,
+                             int32_t staging_rows, const int32_t* codes, const int32_t* bag_ptr,
+                             int32_t n_samples, int32_t bags_per_sample, int64_t n_lookups,
+                             const int32_t* sample_ids, const int32_t* n_sel_dev, int32_t n_sel_max,
+                             float* out, int32_t part, hl_stream stream);
 
 /* Backward of sum pooling plus one SGD step with duplicate rows coalesced
  * (hot rows updated in GPU memory, Sec. IV): for every distinct code c among
@@ -261,6 +280,17 @@ hl_status hl_embbag_bwd_apply(hl_handle* h, void* w_hot, void* staging, int32_t 
                               const float* dY, float lr, void* workspace, size_t ws_bytes,
                               hl_stream stream);
 
+/* hl_embbag_bwd_apply in halves, bit for bit the same updates: part 1 reduces
+ * dY for every group, updates the hot rows and keeps the sums of the staging
+ * rows below n_lookups in the workspace without reading those rows (so it can
+ * run while they are fetched, once the forwards have read the hot rows);
+ * part 2 updates those staging rows from the kept sums (reads no dY).  Part 2
+ * needs part 1 on the same plan (else HL_ERR_INVALID_ARG); part 0 is both. */
+hl_status hl_embbag_bwd_apply_part(hl_handle* h, void* w_hot, void* staging, int32_t staging_rows,
+                                   int32_t n_samples, int32_t bags_per_sample, int64_t n_lookups,
+                                   const float* dY, float lr, int32_t part, void* workspace,
+                                   size_t ws_bytes, hl_stream stream);
+
 /* ----------------------------------------------------------------- errors --
  * Waits for the device, returns the error word (HL_DEVERR_* bits) in *err_out
  * (host) and clears it.  Returns HL_ERR_DEVICE if any bit was set. */
@@ -276,6 +306,80 @@ hl_status hl_trace_enable(hl_handle* h, int32_t cap);
 int32_t hl_trace_count(const hl_handle* h);
 hl_status hl_trace_read(const hl_handle* h, int32_t i, const char** name, float* ms);
 hl_status hl_trace_reset(hl_handle* h);
+
+/* ---------------------------------------------------------------- streams --
+ * A stream of default priority whose kernels run only on compute units
+ * [first_cu, first_cu + n_cu) of the current device (complement != 0: on all
+ * the others; n_cu = 0: no restriction).  The host-link copy keeps its compute
+ * units' memory queues full of slow host reads, which stalls any kernel that
+ * shares those units, so the pipelined schedule gives the copy a few units of
+ * its own and the rest of the step the others. */
+hl_status hl_stream_create(int32_t first_cu, int32_t n_cu, int32_t complement, hl_stream* out);
+hl_status hl_stream_destroy(hl_stream stream);
+
+/* --------------------------------------------------------------- pipeline --
+ * The pipelined schedule of one mini-batch (Sec. IV and the pipeline figure:
+ * the popular mu-batch runs on the GPU while the non-popular mu-batch's working
+ * parameters are gathered), enqueued by one host call on three streams of the
+ * pipeline's own: the host-link copy on compute units [0, fetch_cus) (0 = no
+ * restriction), everything else on the other units.  The step runs
+ * hl_dispatch, hl_cold_plan (no sample list: a cold lookup makes its sample
+ * non-popular), hl_cold_fetch beside hl_embbag_fwd_part 0 of the popular and
+ * part 1 of the non-popular mu-batch, hl_embbag_bwd_plan and apply part 1 on a
+ * third stream, then part 2 of both (and with write_back, hl_cold_scatter
+ * after the updates).  It is ordered after the work already on `stream`, and
+ * `stream` waits for it (the write-back excepted: it is ordered before the
+ * next step's fetch and before any later step's plan that rewrites the same
+ * cold_ids, so callers that write back may alternate two cold_ids / n_cold
+ * buffers between steps; hl_pipeline_sync_writeback makes `stream` wait for
+ * the last write-backs).
+ * One pipeline serves one handle; steps on it do not overlap other calls on
+ * the same workspace.  Every buffer keeps the meaning it has in the calls
+ * above; counts has 2 entries.  Refused (HL_ERR_UNSUPPORTED) while `stream` is
+ * being captured into a graph: a graph keeps no stream's compute-unit mask. */
+typedef struct hl_pipeline hl_pipeline;
+typedef struct hl_step_io {
+  const uint32_t* rows;       /* mini-batch (device) */
+  const int32_t* bag_ptr;
+  int32_t n_samples;
+  int32_t bags_per_sample;
+  int64_t n_lookups;
+  const float* dY;            /* NULL: forward only */
+  float lr;
+  uint32_t* gids;             /* per-step results (device) */
+  int32_t* codes;
+  uint8_t* flags;
+  int32_t* pop_ids;
+  int32_t* nonpop_ids;
+  int32_t* counts;
+  uint32_t* cold_ids;
+  int32_t* n_cold;
+  const void* w_host;         /* parameters */
+  void* w_hot;
+  void* staging;
+  int32_t staging_cap;
+  float* out;
+  void* workspace;
+  size_t ws_bytes;
+  int32_t write_back;
+  uint32_t step_flags;        /* HL_STEP_* */
+} hl_step_io;
+/* Step flag: no ordering with `stream` (no wait before, no wait after); the
+ * caller has the inputs ready on the device and later calls
+ * hl_pipeline_sync.  Back-to-back steps then run without two cross-stream
+ * hops per step. */
+#define HL_STEP_UNTIED 1u
+hl_status hl_pipeline_create(hl_handle* h, int32_t fetch_cus, hl_pipeline** out);
+hl_status hl_pipeline_destroy(hl_pipeline* p);
+hl_status hl_pipeline_step(hl_pipeline* p, const hl_step_io* io, hl_stream stream);
+hl_status hl_pipeline_sync_writeback(hl_pipeline* p, hl_stream stream);
+/* `stream` waits for every step enqueued so far (and their write-backs). */
+hl_status hl_pipeline_sync(hl_pipeline* p, hl_stream stream);
+/* The pipeline's streams (main and group on the compute units the copy leaves
+ * free, fetch on the copy's own), for callers that enqueue more work in the
+ * same arrangement instead of creating streams of their own (a process has a
+ * few hardware queues; streams beyond them share queues). */
+hl_status hl_pipeline_streams(const hl_pipeline* p, hl_stream* main, hl_stream* fetch, hl_stream* group);
 
 /* ---------------------------------------------------- pinned host memory --
  * Page-locked host memory mapped into the device address space (the host

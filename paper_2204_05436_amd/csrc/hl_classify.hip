@@ -224,12 +224,13 @@ extern "C" hl_status hl_remap(const hl_handle* h, const uint32_t* gids, int64_t 
 // the workspace header, tagged with an epoch kept on the device: the last block
 // to finish advances it, so no clearing is needed between calls (nor between
 // replays of a captured graph).
-#define DS_MAX_BAGS 2048
-#define DS_MAX_SPB 1024
+#define DS_THREADS 512
+#define DS_MAX_BAGS 4096
+#define DS_MAX_SPB 2048
 #define DS_EPOCH 0
 #define DS_DONE 1
 #define DS_TILE 2
-__global__ void __launch_bounds__(256)
+__global__ void __launch_bounds__(DS_THREADS)
 ds_kernel(const uint32_t* __restrict__ rows, const int32_t* __restrict__ bag_ptr, int32_t n_samples, int32_t bps,
           int32_t spb, const uint32_t* __restrict__ base, const uint32_t* __restrict__ nrow, int32_t n_tables,
           const uint64_t* __restrict__ bitmap, const uint32_t* __restrict__ rank, uint64_t n_rows,
@@ -237,7 +238,7 @@ ds_kernel(const uint32_t* __restrict__ rows, const int32_t* __restrict__ bag_ptr
           int32_t* nonpop, int32_t* counts, int64_t n_lookups, uint32_t* hdr, uint64_t* st, uint32_t* err) {
   __shared__ int32_t off[DS_MAX_BAGS + 1];
   __shared__ uint8_t fl[DS_MAX_SPB];
-  __shared__ uint32_t s_tile, s_epoch, s_excl, wsum[4];
+  __shared__ uint32_t s_tile, s_epoch, wsum[DS_THREADS / 64];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   if (tid == 0) {
     s_tile = atomicInc(hdr + DS_TILE, gridDim.x - 1);
@@ -250,30 +251,47 @@ ds_kernel(const uint32_t* __restrict__ rows, const int32_t* __restrict__ bag_ptr
   const int ns = (int)min((int64_t)spb, (int64_t)n_samples - s0);
   const int64_t bg0 = s0 * bps;
   const int nbg = ns * bps;
-  for (int j = tid; j <= nbg; j += 256) off[j] = bag_ptr[bg0 + j];
-  for (int j = tid; j < ns; j += 256) fl[j] = 1;
+  for (int j = tid; j <= nbg; j += DS_THREADS) off[j] = bag_ptr[bg0 + j];
+  for (int j = tid; j < ns; j += DS_THREADS) fl[j] = 1;
   if (tile == 0 && tid == 0 && bag_ptr[(int64_t)n_samples * bps] != n_lookups) hl_flag(err, HL_DEVERR_SHAPE);
   __syncthreads();
   const int32_t lo = off[0], hi = (int32_t)min((int64_t)off[nbg], n_lookups);
-  for (int32_t i = lo + tid; i < hi; i += 256) {
-    int a = 0, b = nbg;  // off[a] <= i < off[b]
-    while (b - a > 1) {
-      const int m = (a + b) >> 1;
-      if (off[m] <= i) a = m; else b = m;
+  // 4 lookups per thread per round, their loads issued together
+  for (int32_t i0 = lo + tid; i0 < hi; i0 += 4 * DS_THREADS) {
+    int a[4];
+    uint32_t r[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int32_t i = i0 + k * DS_THREADS;
+      int x = 0, y = nbg;  // off[x] <= i < off[y]
+      if (i < hi)
+        while (y - x > 1) {
+          const int m = (x + y) >> 1;
+          if (off[m] <= i) x = m; else y = m;
+        }
+      a[k] = x;
+      r[k] = i < hi ? rows[i] : 0u;
     }
-    const int32_t t = (int32_t)((bg0 + a) % n_tables);
-    const uint32_t r = rows[i];
-    uint32_t g = 0xFFFFFFFFu;
-    int32_t c = -1;
-    if (r < nrow[t]) {
-      g = base[t] + r;
-      c = hl_hot_slot(bitmap, rank, g);
-    } else {
-      hl_flag(err, HL_DEVERR_OUT_OF_RANGE);
+    uint32_t g[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int32_t t = (int32_t)((bg0 + a[k]) % n_tables);
+      const bool in = i0 + k * DS_THREADS < hi;
+      g[k] = 0xFFFFFFFFu;
+      if (in) {
+        if (r[k] < nrow[t]) g[k] = base[t] + r[k];
+        else hl_flag(err, HL_DEVERR_OUT_OF_RANGE);
+      }
     }
-    gids[i] = g;
-    codes[i] = c;
-    if (c < 0) fl[a / bps] = 0;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int32_t i = i0 + k * DS_THREADS;
+      if (i >= hi) continue;
+      const int32_t c = g[k] < n_rows ? hl_hot_slot(bitmap, rank, g[k]) : -1;
+      gids[i] = g[k];
+      codes[i] = c;
+      if (c < 0) fl[a[k] / bps] = 0;
+    }
   }
   __syncthreads();
   // popular samples of this block: exclusive ranks over its samples (4 per thread)
@@ -293,46 +311,13 @@ ds_kernel(const uint32_t* __restrict__ rows, const int32_t* __restrict__ bag_ptr
   if (lane == 63) wsum[w] = inc;
   __syncthreads();
   uint32_t before = inc - loc, tc = 0;
-  for (int q = 0; q < 4; ++q) {
+  for (int q = 0; q < DS_THREADS / 64; ++q) {
     if (q < w) before += wsum[q];
     tc += wsum[q];
   }
-  if (w == 0) {
-    if (lane == 0) hl_st_store(st + tile, hl_st_pack(epoch, tile == 0 ? HL_ST_PRE : HL_ST_AGG, tc));
-    uint32_t ex = 0;
-    if (tile > 0) {
-      // lane j reads tile (t - 1 - j) of the window; stop at the nearest inclusive prefix
-      uint32_t spins = 0;
-      int64_t jj = (int64_t)tile - 1;
-      while (jj >= 0) {
-        const int64_t p = jj - lane;
-        const uint64_t wd = p >= 0 ? hl_st_load(st + p) : hl_st_pack(epoch, HL_ST_PRE, 0);
-        const uint32_t f = (uint32_t)((wd >> 30) & 3ull);
-        const bool ok = (uint32_t)(wd >> 32) == epoch && f != 0;
-        const uint64_t pre = __ballot(ok && f == HL_ST_PRE), bad = __ballot(!ok);
-        const int fp = pre ? __ffsll((unsigned long long)pre) - 1 : 64;
-        const int fb = bad ? __ffsll((unsigned long long)bad) - 1 : 64;
-        const int use = fb < fp ? fb : (fp < 64 ? fp + 1 : 64);
-        uint32_t v = lane < use ? (uint32_t)(wd & 0x3FFFFFFFu) : 0u;
-#pragma unroll
-        for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
-        ex += v;
-        if (fb >= fp && fp < 64) break;
-        jj -= use;
-        if (fb < fp) {
-          if (++spins > HL_SPIN_LIMIT) {
-            hl_flag(err, HL_DEVERR_STALL);
-            break;
-          }
-          __builtin_amdgcn_s_sleep(1);
-        }
-      }
-      if (lane == 0) hl_st_store(st + tile, hl_st_pack(epoch, HL_ST_PRE, ex + tc));
-    }
-    if (lane == 0) s_excl = ex;
-  }
-  __syncthreads();
-  const uint32_t ex = s_excl;
+  if (tid == 0) hl_st_store(st + tile, hl_st_pack(epoch, tile == 0 ? HL_ST_PRE : HL_ST_AGG, tc));
+  const uint32_t ex = tile > 0 ? hl_block_lookback(st, tile, epoch, err) : 0u;
+  if (tid == 0 && tile > 0) hl_st_store(st + tile, hl_st_pack(epoch, HL_ST_PRE, ex + tc));
   uint32_t pp = ex + before;
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
@@ -361,8 +346,8 @@ extern "C" hl_status hl_dispatch(hl_handle* h, const uint32_t* rows, const int32
   if (n_lookups > 0 && (!rows || !gids || !codes)) return HL_ERR_INVALID_ARG;
   if ((int64_t)n_samples * bps >= (1ll << 31) || n_lookups >= (1ll << 31)) return HL_ERR_UNSUPPORTED;
   hipStream_t s = (hipStream_t)stream;
-  // about 512 lookups per block, at most DS_MAX_BAGS bags
-  int64_t spb = n_lookups > 0 ? (512ll * n_samples + n_lookups - 1) / n_lookups : DS_MAX_SPB;
+  // about 2048 lookups per block, at most DS_MAX_BAGS bags
+  int64_t spb = n_lookups > 0 ? (2048ll * n_samples + n_lookups - 1) / n_lookups : DS_MAX_SPB;
   const int64_t bag_cap = DS_MAX_BAGS / bps;
   if (spb > bag_cap) spb = bag_cap;
   if (spb > DS_MAX_SPB) spb = DS_MAX_SPB;
@@ -378,7 +363,7 @@ extern "C" hl_status hl_dispatch(hl_handle* h, const uint32_t* rows, const int32
   }
   uint32_t* hdr = (uint32_t*)workspace + HL_HDR_DISP;
   uint64_t* stw = (uint64_t*)((uint32_t*)workspace + HL_HDR_DSTAT);
-  HL_KERNEL(h, s, "ds_kernel", ds_kernel, dim3((uint32_t)tiles), dim3(256), 0, s, rows, bag_ptr, n_samples, bps,
+  HL_KERNEL(h, s, "ds_kernel", ds_kernel, dim3((uint32_t)tiles), dim3(DS_THREADS), 0, s, rows, bag_ptr, n_samples, bps,
             (int32_t)spb, h->d_base, h->d_rows, h->n_tables, h->d_bitmap, h->d_rank, h->n_rows, gids, codes, flags,
             pop_ids, nonpop_ids, counts_dev, n_lookups, hdr, stw, h->d_err);
   HL_LAUNCHED();

@@ -8,8 +8,8 @@
 //            one, which enters an open-addressing hash table keyed by row id
 //            with one CAS (a 64-bit atomic min keeps the smallest lookup index
 //            per id); the block lists its cold lookups in its own lookup range
-//   rank   : a scan over all lookups in index order (tiles of 1024, decoupled
-//            look-back read by a whole wave) numbers the first occurrences:
+//   rank   : a scan over all lookups in index order (tiles of 2048, decoupled
+//            look-back read by the whole block) numbers the first occurrences:
 //            staging row u of each id
 //   codes  : capacity check, code rewrite, the cold id list, and the clearing
 //            of the table slots this call used
@@ -27,7 +27,8 @@
 #define CG_C_RTILE 2
 #define CG_BAGS 256      // bags per insert block
 #define CG_IR 1024       // lookup positions per insert round (256 threads x 4)
-#define CG_RT 1024       // lookups per rank tile (256 threads x 4)
+#define CG_RT_THREADS 512
+#define CG_RT (CG_RT_THREADS * 4)  // lookups per rank tile
 
 struct cg_ws {
   uint32_t* ctr;      // header counters
@@ -71,8 +72,8 @@ size_t hl_cold_ws_bytes(const hl_handle* h, int64_t max_lookups, int64_t max_bag
 
 // The handle's hash table, (id + 1) << 32 | smallest lookup index per slot, 0
 // = empty; grown (and zeroed) when a call needs more slots.  The growth
-// allocates, so a caller that captures calls into a graph makes one call of
-// the largest size first.
+// allocates, so a caller that captures calls into a graph reserves the largest
+// size first (hl_cold_reserve).
 static hl_status cg_table(hl_handle* h, uint32_t S, hipStream_t s, uint64_t** out) {
   if (h->cg_slots < S) {
     if (h->cg_table) {
@@ -202,46 +203,13 @@ cg_insert(const uint32_t* __restrict__ gids, const int32_t* __restrict__ codes, 
   if (tid == 0) ws.bcnt[blockIdx.x] = listed;
 }
 
-// Exclusive prefix of this tile's count over earlier tiles, read by all 64
-// lanes of one wave: lane j looks at tile (tile - 1 - j) of the current window.
-__device__ __forceinline__ uint32_t cg_wave_lookback(const uint64_t* st, uint32_t tile, uint32_t epoch, uint32_t* err) {
-  const int lane = threadIdx.x & 63;
-  uint32_t excl = 0, spins = 0;
-  int64_t j = (int64_t)tile - 1;
-  while (j >= 0) {
-    const int64_t p = j - lane;
-    const uint64_t wd = p >= 0 ? hl_st_load(st + p) : hl_st_pack(epoch, HL_ST_PRE, 0);
-    const uint32_t e = (uint32_t)(wd >> 32);
-    const uint32_t f = (uint32_t)((wd >> 30) & 3ull);
-    const bool ok = e == epoch && f != 0;
-    const uint64_t pre = __ballot(ok && f == HL_ST_PRE), bad = __ballot(!ok);
-    const int fp = pre ? __ffsll((unsigned long long)pre) - 1 : 64;
-    const int fb = bad ? __ffsll((unsigned long long)bad) - 1 : 64;
-    const int use = fb < fp ? fb : (fp < 64 ? fp + 1 : 64);  // lanes [0, use) are consumed
-    uint32_t v = lane < use ? (uint32_t)(wd & 0x3FFFFFFFu) : 0u;
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
-    excl += v;
-    if (fb >= fp && fp < 64) break;  // reached a tile with its inclusive prefix
-    j -= use;
-    if (fb < fp) {
-      if (++spins > HL_SPIN_LIMIT) {
-        hl_flag(err, HL_DEVERR_STALL);
-        break;
-      }
-      __builtin_amdgcn_s_sleep(1);
-    }
-  }
-  return excl;
-}
-
 // Lookup i is a first occurrence iff it is a cold lookup of this call whose
 // slot holds (its id, i); the running count of first occurrences numbers the
 // staging rows.
-__global__ void __launch_bounds__(256)
+__global__ void __launch_bounds__(CG_RT_THREADS)
 cg_rank(const uint32_t* __restrict__ gids, const int32_t* __restrict__ codes, uint32_t n_lookups,
         const uint64_t* __restrict__ table, cg_ws ws, int32_t* n_cold_dev, uint32_t epoch, uint32_t* err) {
-  __shared__ uint32_t s_tile, wt[4], s_excl;
+  __shared__ uint32_t s_tile, wt[CG_RT_THREADS / 64];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   if (tid == 0) s_tile = atomicInc(ws.ctr + CG_C_RTILE, gridDim.x - 1);
   __syncthreads();
@@ -283,21 +251,14 @@ cg_rank(const uint32_t* __restrict__ gids, const int32_t* __restrict__ codes, ui
   if (lane == 0) wt[w] = wsum;
   __syncthreads();
   uint32_t before = 0, tc = 0;
-  for (int q = 0; q < 4; ++q) {
+  for (int q = 0; q < CG_RT_THREADS / 64; ++q) {
     if (q < w) before += wt[q];
     tc += wt[q];
   }
-  if (w == 0) {
-    if (lane == 0) hl_st_store(ws.rstat + tile, hl_st_pack(epoch, tile == 0 ? HL_ST_PRE : HL_ST_AGG, tc));
-    uint32_t ex = 0;
-    if (tile > 0) {
-      ex = cg_wave_lookback(ws.rstat, tile, epoch, err);
-      if (lane == 0) hl_st_store(ws.rstat + tile, hl_st_pack(epoch, HL_ST_PRE, ex + tc));
-    }
-    if (lane == 0) s_excl = ex;
-  }
-  __syncthreads();
-  uint32_t run = s_excl + before;
+  if (tid == 0) hl_st_store(ws.rstat + tile, hl_st_pack(epoch, tile == 0 ? HL_ST_PRE : HL_ST_AGG, tc));
+  const uint32_t ex = tile > 0 ? hl_block_lookback(ws.rstat, tile, epoch, err) : 0u;
+  if (tid == 0 && tile > 0) hl_st_store(ws.rstat + tile, hl_st_pack(epoch, HL_ST_PRE, ex + tc));
+  uint32_t run = ex + before;
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
     const uint64_t i = tb + w * 256 + k * 64 + lane;
@@ -450,13 +411,20 @@ extern "C" hl_status hl_cold_plan(hl_handle* h, const uint32_t* gids, int32_t* c
   // the insert kernel cleared the status words, so one fixed tag serves every
   // call (and every replay of a captured graph)
   const uint32_t epoch = 1;
-  HL_KERNEL(h, s, "cg_rank", cg_rank, dim3(ws.rtiles), dim3(256), 0, s, gids, codes, ib > 0 ? n : 0u, table, ws,
+  HL_KERNEL(h, s, "cg_rank", cg_rank, dim3(ws.rtiles), dim3(CG_RT_THREADS), 0, s, gids, codes, ib > 0 ? n : 0u, table, ws,
             n_cold_dev, epoch, h->d_err);
   if (ib > 0)
     HL_KERNEL(h, s, "cg_codes", cg_codes, dim3(ib), dim3(256), 0, s, bag_ptr, table, ws, cap, h->k_cap, codes,
               cold_ids_out, h->d_err);
   HL_LAUNCHED();
   return HL_OK;
+}
+
+extern "C" hl_status hl_cold_reserve(hl_handle* h, int64_t max_lookups, hl_stream stream) {
+  if (!h || max_lookups < 0) return HL_ERR_INVALID_ARG;
+  if (max_lookups >= (1ll << 30)) return HL_ERR_UNSUPPORTED;
+  uint64_t* t = nullptr;
+  return cg_table(h, cg_table_slots((uint32_t)max_lookups), (hipStream_t)stream, &t);
 }
 
 extern "C" hl_status hl_cold_fetch(hl_handle* h, const uint32_t* cold_ids, const int32_t* n_cold_dev, int32_t cap,

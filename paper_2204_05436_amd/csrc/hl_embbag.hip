@@ -136,6 +136,13 @@ __device__ __forceinline__ int32_t eb_nsel(const int32_t* ids, const int32_t* n_
 // any: offsets, then codes, then rows, so FC rows per lane are in flight.  When
 // every bag of the chunk holds one lookup (one-hot features) that is the whole
 // work; otherwise bags are pooled one by one with 4 rows in flight.
+//
+// A bag's sum takes its hot rows first, then its staging (cold) rows, each in
+// CSR order, so that the two halves can run apart with identical results:
+// PART 0 does both, PART 1 only the hot rows (writing the partial sum), PART 2
+// adds the cold rows onto the stored partial sum (bags without cold rows are
+// left alone).  The hot half needs no fetched row, so it runs while the
+// working parameters still travel over the host link.
 #define FC 8
 __device__ __forceinline__ bool eb_code_row(uint32_t cu, uint32_t n_hot, uint32_t k_cap, int32_t stg_rows,
                                             int64_t* row, bool* stg) {
@@ -152,7 +159,38 @@ __device__ __forceinline__ bool eb_code_row(uint32_t cu, uint32_t n_hot, uint32_
   return false;
 }
 
-template <int VEC, bool BF>
+// acc += the bag's rows of one kind (hot, or staging when COLD), in CSR order,
+// 4 rows in flight.  Invalid codes are flagged by the hot pass only.
+template <int VEC, bool BF, bool COLD>
+__device__ __forceinline__ void eb_pass(float* acc, const typename RowIO<VEC, BF>::T* w_hot,
+                                        const typename RowIO<VEC, BF>::T* stg, int32_t stg_rows, uint32_t n_hot,
+                                        uint32_t k_cap, const int32_t* __restrict__ codes, int32_t lo, int32_t hi,
+                                        eb_geom g, int64_t col, bool cact, int gl, uint32_t* err) {
+  for (int32_t i = lo; i < hi; i += 4) {
+    uint32_t cc[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) cc[k] = i + k < hi ? (uint32_t)codes[i + k] : 0u;
+    float v[4][VEC];
+    bool use[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      int64_t r = 0;
+      bool st = false;
+      const bool in = i + k < hi;
+      const bool ok = in && eb_code_row(cc[k], n_hot, k_cap, stg_rows, &r, &st);
+      use[k] = ok && st == COLD;
+      if (use[k] && cact) RowIO<VEC, BF>::load((COLD ? stg : w_hot) + r * g.D + col, v[k]);
+      if (!COLD && in && !ok && gl == 0) hl_flag(err, HL_DEVERR_BAD_CODE);
+    }
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+      if (use[k] && cact)
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) acc[e] += v[k][e];
+  }
+}
+
+template <int VEC, bool BF, int PART>
 __global__ void __launch_bounds__(256)
 eb_fwd(const void* w_hot_, const void* stg_, int32_t stg_rows, uint32_t n_hot, uint32_t k_cap,
        const int32_t* __restrict__ codes, const int32_t* __restrict__ bag_ptr, int32_t bps,
@@ -184,7 +222,7 @@ eb_fwd(const void* w_hot_, const void* stg_, int32_t stg_rows, uint32_t n_hot, u
       int64_t smp = si;
       if (val[u] && sample_ids) smp = sample_ids[si];
       if (val[u] && (smp < 0 || smp >= n_samples)) {
-        if (gl == 0) hl_flag(err, HL_DEVERR_OUT_OF_RANGE);
+        if (gl == 0 && PART != 2) hl_flag(err, HL_DEVERR_OUT_OF_RANGE);
         val[u] = false;
       }
       bag[u] = smp * bps + j;
@@ -207,21 +245,35 @@ eb_fwd(const void* w_hot_, const void* stg_, int32_t stg_rows, uint32_t n_hot, u
 #pragma unroll
       for (int u = 0; u < FC; ++u) cu[u] = val[u] ? (uint32_t)codes[lo[u]] : 0u;
       float v[FC][VEC];
+      bool wr[FC];
 #pragma unroll
       for (int u = 0; u < FC; ++u) {
         int64_t r = 0;
         bool st = false;
         const bool ok = val[u] && eb_code_row(cu[u], n_hot, k_cap, stg_rows, &r, &st);
-        if (ok && cact) RowIO<VEC, BF>::load((st ? stg : w_hot) + r * g.D + col, v[u]);
+        // PART 0 and 1 write every valid bag (PART 1 a zero for a cold row); PART 2 only cold ones
+        const bool take = ok && (PART == 0 || (PART == 1 ? !st : st));
+        wr[u] = val[u] && (PART == 2 ? take : true);
+        if (take && cact) RowIO<VEC, BF>::load((st ? stg : w_hot) + r * g.D + col, v[u]);
         else {
 #pragma unroll
           for (int e = 0; e < VEC; ++e) v[u][e] = 0.f;
         }
-        if (val[u] && !ok && gl == 0) hl_flag(err, HL_DEVERR_BAD_CODE);
+        if (PART != 2 && val[u] && !ok && gl == 0) hl_flag(err, HL_DEVERR_BAD_CODE);
       }
+      // the sum starts from 0 (PART 2: from the stored hot partial sum, which is 0)
 #pragma unroll
       for (int u = 0; u < FC; ++u)
-        if (val[u] && cact) st_f32<VEC>(out + bag[u] * g.D + col, v[u]);
+        if (wr[u] && cact) {
+          float o[VEC];
+          if (PART == 2) ld_f32<VEC>(out + bag[u] * g.D + col, o);
+          else
+#pragma unroll
+            for (int e = 0; e < VEC; ++e) o[e] = 0.f;
+#pragma unroll
+          for (int e = 0; e < VEC; ++e) o[e] += v[u][e];
+          st_f32<VEC>(out + bag[u] * g.D + col, o);
+        }
       continue;
     }
     for (int u = 0; u < FC; ++u) {
@@ -229,29 +281,19 @@ eb_fwd(const void* w_hot_, const void* stg_, int32_t stg_rows, uint32_t n_hot, u
       float acc[VEC];
 #pragma unroll
       for (int e = 0; e < VEC; ++e) acc[e] = 0.f;
-      for (int32_t i = lo[u]; i < hi[u]; i += 4) {
-        uint32_t cc[4];
-#pragma unroll
-        for (int k = 0; k < 4; ++k) cc[k] = i + k < hi[u] ? (uint32_t)codes[i + k] : 0u;
-        float v[4][VEC];
-#pragma unroll
-        for (int k = 0; k < 4; ++k) {
-          int64_t r = 0;
-          bool st = false;
-          const bool in = i + k < hi[u];
-          const bool ok = in && eb_code_row(cc[k], n_hot, k_cap, stg_rows, &r, &st);
-          if (ok && cact) RowIO<VEC, BF>::load((st ? stg : w_hot) + r * g.D + col, v[k]);
-          else {
-#pragma unroll
-            for (int e = 0; e < VEC; ++e) v[k][e] = 0.f;
-          }
-          if (in && !ok && gl == 0) hl_flag(err, HL_DEVERR_BAD_CODE);
+      if (PART == 2) {
+        bool any = false;
+        for (int32_t i = lo[u]; i < hi[u] && !any; ++i) {
+          const uint32_t cc = (uint32_t)codes[i];
+          any = cc >= k_cap && cc - k_cap < (uint32_t)stg_rows;
         }
-#pragma unroll
-        for (int k = 0; k < 4; ++k)
-#pragma unroll
-          for (int e = 0; e < VEC; ++e) acc[e] += v[k][e];
+        if (!any) continue;
+        if (cact) ld_f32<VEC>(out + bag[u] * g.D + col, acc);
       }
+      if (PART != 2)
+        eb_pass<VEC, BF, false>(acc, w_hot, stg, stg_rows, n_hot, k_cap, codes, lo[u], hi[u], g, col, cact, gl, err);
+      if (PART != 1)
+        eb_pass<VEC, BF, true>(acc, w_hot, stg, stg_rows, n_hot, k_cap, codes, lo[u], hi[u], g, col, cact, gl, err);
       if (cact) st_f32<VEC>(out + bag[u] * g.D + col, acc);
     }
   }
@@ -265,7 +307,8 @@ struct bw_ws {
   float* tlast;      // [tiles][D]
   uint32_t* tflag;   // [tiles]
   uint32_t* tkey;    // [tiles]
-  uint32_t tiles;
+  float* gc;         // [n_max][D] gradient sums of staging rows, kept between the two halves of the apply
+  uint32_t tiles, gc_rows;
 };
 
 static uint32_t bw_tile_entries(int32_t D, int vec) {
@@ -286,6 +329,8 @@ static void bw_carve(hl_carver& c, bw_ws& ws, uint32_t n_max, int64_t max_bags, 
   ws.tlast = c.take<float>((size_t)ws.tiles * D);
   ws.tflag = c.take<uint32_t>(ws.tiles);
   ws.tkey = c.take<uint32_t>(ws.tiles);
+  ws.gc_rows = n_max;
+  ws.gc = c.take<float>((size_t)n_max * D);
 }
 
 size_t hl_bwd_ws_bytes(const hl_handle* h, int64_t max_lookups, int64_t max_bags) {
@@ -358,12 +403,19 @@ __device__ __forceinline__ typename RowIO<VEC, BF>::T* bw_row(void* w_hot, void*
 #define GF_W 2u
 #define GF_L 4u
 
-template <int VEC, bool BF>
+// SPLIT: the run of a staging row (key n_hot + u, u < gc_rows) stores its sum
+// G in gc[u] instead of updating the row, and the row is not read; bw_cold
+// applies it later (the staging rows may still be in flight then).
+__device__ __forceinline__ bool bw_deferred(uint32_t key, uint32_t n_hot, uint32_t gc_rows) {
+  return key >= n_hot && key != EB_SENT && key - n_hot < gc_rows;
+}
+
+template <int VEC, bool BF, bool SPLIT>
 __global__ void __launch_bounds__(RB_BLOCK)
 bw_reduce1(const uint32_t* __restrict__ keys, const uint32_t* __restrict__ vals, uint32_t n,
            const float* __restrict__ dY, eb_geom g, void* w_hot, void* stg, uint32_t n_hot, float lr,
            float* __restrict__ tfirst, float* __restrict__ tlast, uint32_t* __restrict__ tflag,
-           uint32_t* __restrict__ tkey) {
+           uint32_t* __restrict__ tkey, float* __restrict__ gc, uint32_t gc_rows) {
   typedef typename RowIO<VEC, BF>::T T;
   __shared__ float pf[RB_WAVES * 64 * VEC], pl[RB_WAVES * 64 * VEC];
   __shared__ uint32_t gflag[RB_WAVES * 64], gkey[RB_WAVES * 64];
@@ -414,7 +466,8 @@ bw_reduce1(const uint32_t* __restrict__ keys, const uint32_t* __restrict__ vals,
       if (j > 0 && valid && kk[j - 1] != kk[j]) from0 = false;
       const bool end = valid && (j == RB_E - 1 || kk[j + 1] != kk[j]);
       cpl[j] = end && !(from0 && cprev) && !(j == RB_E - 1 && cnext);
-      if (cpl[j] && cact) RowIO<VEC, BF>::load(bw_row<VEC, BF>(w_hot, stg, n_hot, g.D, kk[j]) + col, wr[j]);
+      if (cpl[j] && cact && !(SPLIT && bw_deferred(kk[j], n_hot, gc_rows)))
+        RowIO<VEC, BF>::load(bw_row<VEC, BF>(w_hot, stg, n_hot, g.D, kk[j]) + col, wr[j]);
     }
     float acc[VEC];
 #pragma unroll
@@ -433,10 +486,14 @@ bw_reduce1(const uint32_t* __restrict__ keys, const uint32_t* __restrict__ vals,
       if (end) {
         if (cpl[j]) {
           if (cact) {
-            float nw[VEC];
+            if (SPLIT && bw_deferred(kk[j], n_hot, gc_rows)) {
+              st_f32<VEC>(gc + (int64_t)(kk[j] - n_hot) * g.D + col, acc);
+            } else {
+              float nw[VEC];
 #pragma unroll
-            for (int e = 0; e < VEC; ++e) nw[e] = wr[j][e] - lr * acc[e];
-            RowIO<VEC, BF>::store(bw_row<VEC, BF>(w_hot, stg, n_hot, g.D, kk[j]) + col, nw);
+              for (int e = 0; e < VEC; ++e) nw[e] = wr[j][e] - lr * acc[e];
+              RowIO<VEC, BF>::store(bw_row<VEC, BF>(w_hot, stg, n_hot, g.D, kk[j]) + col, nw);
+            }
           }
         } else {
           const bool first = from0 && cprev, lastp = (j == RB_E - 1) && cnext;
@@ -476,7 +533,9 @@ bw_reduce1(const uint32_t* __restrict__ keys, const uint32_t* __restrict__ vals,
       }
       const uint32_t key = gkey[grp];
       if (done) {
-        if (cact) {
+        if (cact && SPLIT && bw_deferred(key, n_hot, gc_rows)) {
+          st_f32<VEC>(gc + (int64_t)(key - n_hot) * g.D + col, acc);
+        } else if (cact) {
           T* p = bw_row<VEC, BF>(w_hot, stg, n_hot, g.D, key) + col;
           float wv[VEC];
           RowIO<VEC, BF>::load(p, wv);
@@ -518,11 +577,11 @@ bw_reduce1(const uint32_t* __restrict__ keys, const uint32_t* __restrict__ vals,
 // own piece and the next tiles' first pieces up to the first tile that is not
 // wholly inside the segment.  Piece p is summed by group p % groups in
 // ascending p, then groups are added in order.
-template <int VEC, bool BF>
+template <int VEC, bool BF, bool SPLIT>
 __global__ void __launch_bounds__(RB_BLOCK)
 bw_reduce2(uint32_t n_tiles, eb_geom g, void* w_hot, void* stg, uint32_t n_hot, float lr,
            const float* __restrict__ tfirst, const float* __restrict__ tlast, const uint32_t* __restrict__ tflag,
-           const uint32_t* __restrict__ tkey) {
+           const uint32_t* __restrict__ tkey, float* __restrict__ gc, uint32_t gc_rows) {
   typedef typename RowIO<VEC, BF>::T T;
   const uint32_t t = blockIdx.x;
   if (!(tflag[t] & GF_L)) return;
@@ -571,12 +630,56 @@ bw_reduce2(uint32_t n_tiles, eb_geom g, void* w_hot, void* stg, uint32_t n_hot, 
     for (int q = 0; q < ngb; ++q)
 #pragma unroll
       for (int e = 0; e < VEC; ++e) acc[e] += part[(q * g.G + gl) * VEC + e];
-    T* p = bw_row<VEC, BF>(w_hot, stg, n_hot, g.D, tkey[t]) + col;
+    const uint32_t key = tkey[t];
+    if (SPLIT && bw_deferred(key, n_hot, gc_rows)) {
+      st_f32<VEC>(gc + (int64_t)(key - n_hot) * g.D + col, acc);
+      return;
+    }
+    T* p = bw_row<VEC, BF>(w_hot, stg, n_hot, g.D, key) + col;
     float wv[VEC];
     RowIO<VEC, BF>::load(p, wv);
 #pragma unroll
     for (int e = 0; e < VEC; ++e) wv[e] -= lr * acc[e];
     RowIO<VEC, BF>::store(p, wv);
+  }
+}
+
+// The deferred staging-row updates: every run end in the sorted keys whose key
+// is a staging row below gc_rows applies row <- round(row - lr * gc[u]), the
+// same arithmetic as the one-pass update.  A wave tests 64 positions, then its
+// row groups take the run ends it found, a group per row.
+template <int VEC, bool BF>
+__global__ void __launch_bounds__(256)
+bw_cold(const uint32_t* __restrict__ keys, uint32_t n, eb_geom g, void* stg, uint32_t n_hot, float lr,
+        const float* __restrict__ gc, uint32_t gc_rows) {
+  typedef typename RowIO<VEC, BF>::T T;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int gi = lane / g.G, gl = lane - gi * g.G;
+  const int32_t colv = blockIdx.y * 64 + gl;
+  const bool cact = gi < g.NG && colv < g.vpr;
+  const int64_t col = (int64_t)colv * VEC;
+  for (uint64_t base = ((uint64_t)blockIdx.x * 4 + w) * 64; base < n; base += (uint64_t)gridDim.x * 256) {
+    const uint64_t p = base + lane;
+    const uint32_t k = p < n ? keys[p] : EB_SENT;
+    const uint32_t kn = p + 1 < n ? keys[p + 1] : EB_SENT;
+    uint64_t m = __ballot(k != kn && bw_deferred(k, n_hot, gc_rows));
+    while (m) {
+      uint64_t mm = m;
+      for (int q = 0; q < gi; ++q) mm &= mm - 1;
+      const int src = mm ? __ffsll((unsigned long long)mm) - 1 : 0;
+      const uint32_t key = __shfl(k, src);
+      if (mm && cact) {
+        const int64_t u = key - n_hot;
+        T* row = (T*)stg + u * g.D + col;
+        float wv[VEC], gv[VEC];
+        RowIO<VEC, BF>::load(row, wv);
+        ld_f32<VEC>(gc + u * g.D + col, gv);
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) wv[e] = wv[e] - lr * gv[e];
+        RowIO<VEC, BF>::store(row, wv);
+      }
+      for (int q = 0; q < g.NG && m; ++q) m &= m - 1;
+    }
   }
 }
 
@@ -596,17 +699,24 @@ template <int VEC, bool BF>
 static void launch_fwd(const hl_handle* h, dim3 grid, hipStream_t s, const void* w_hot, const void* stg,
                        int32_t stg_rows, const int32_t* codes, const int32_t* bag_ptr, int32_t bps,
                        const int32_t* ids, const int32_t* n_dev, int32_t n_max, float* out, eb_geom g,
-                       int64_t n_lookups, int64_t n_bags) {
-  HL_KERNEL(h, s, "eb_fwd", (eb_fwd<VEC, BF>), grid, dim3(256), 0, s, w_hot, stg, stg_rows, h->n_hot, h->k_cap, codes,
-                     bag_ptr, bps, ids, n_dev, n_max, out, g, n_lookups, n_bags, (int32_t)(n_bags / bps), h->d_err);
+                       int64_t n_lookups, int64_t n_bags, int part) {
+#define EBF(P)                                                                                                   \
+  HL_KERNEL(h, s, P == 0 ? "eb_fwd" : (P == 1 ? "eb_fwd_hot" : "eb_fwd_cold"), (eb_fwd<VEC, BF, P>), grid,       \
+            dim3(256), 0, s, w_hot, stg, stg_rows, h->n_hot, h->k_cap, codes, bag_ptr, bps, ids, n_dev, n_max, out, \
+            g, n_lookups, n_bags, (int32_t)(n_bags / bps), h->d_err);
+  if (part == 0) { EBF(0) }
+  else if (part == 1) { EBF(1) }
+  else { EBF(2) }
+#undef EBF
 }
 
-extern "C" hl_status hl_embbag_fwd(const hl_handle* h, const void* w_hot, const void* staging, int32_t stg_rows,
-                                   const int32_t* codes, const int32_t* bag_ptr, int32_t n_samples, int32_t bps,
-                                   int64_t n_lookups, const int32_t* sample_ids, const int32_t* n_sel_dev,
-                                   int32_t n_sel_max, float* out, hl_stream stream) {
+extern "C" hl_status hl_embbag_fwd_part(const hl_handle* h, const void* w_hot, const void* staging, int32_t stg_rows,
+                                        const int32_t* codes, const int32_t* bag_ptr, int32_t n_samples, int32_t bps,
+                                        int64_t n_lookups, const int32_t* sample_ids, const int32_t* n_sel_dev,
+                                        int32_t n_sel_max, float* out, int32_t part, hl_stream stream) {
   hl_status st = check_common(h, codes, bag_ptr, n_samples, bps, n_lookups, sample_ids, n_sel_max, stg_rows);
   if (st != HL_OK) return st;
+  if (part < 0 || part > 2) return HL_ERR_INVALID_ARG;
   if (n_sel_max == 0) return HL_OK;
   if (!out || (h->n_hot && !w_hot) || (stg_rows && !staging)) return HL_ERR_INVALID_ARG;
   const size_t es = h->dtype == HL_F32 ? 4 : 2;
@@ -620,7 +730,7 @@ extern "C" hl_status hl_embbag_fwd(const hl_handle* h, const void* w_hot, const 
   const int64_t nb = (int64_t)n_samples * bps;
   const bool bf = h->dtype == HL_BF16;
 #define FWD(V, B) launch_fwd<V, B>(h, grid, s, w_hot, staging, stg_rows, codes, bag_ptr, bps, sample_ids, n_sel_dev, \
-                                   n_sel_max, out, g, n_lookups, nb)
+                                   n_sel_max, out, g, n_lookups, nb, part)
   if (vec == 4) { if (bf) FWD(4, true); else FWD(4, false); }
   else if (vec == 2) { if (bf) FWD(2, true); else FWD(2, false); }
   else { if (bf) FWD(1, true); else FWD(1, false); }
@@ -629,19 +739,40 @@ extern "C" hl_status hl_embbag_fwd(const hl_handle* h, const void* w_hot, const 
   return HL_OK;
 }
 
+extern "C" hl_status hl_embbag_fwd(const hl_handle* h, const void* w_hot, const void* staging, int32_t stg_rows,
+                                   const int32_t* codes, const int32_t* bag_ptr, int32_t n_samples, int32_t bps,
+                                   int64_t n_lookups, const int32_t* sample_ids, const int32_t* n_sel_dev,
+                                   int32_t n_sel_max, float* out, hl_stream stream) {
+  return hl_embbag_fwd_part(h, w_hot, staging, stg_rows, codes, bag_ptr, n_samples, bps, n_lookups, sample_ids,
+                            n_sel_dev, n_sel_max, out, 0, stream);
+}
+
 // Keys are compressed codes: hot slot, or n_hot + staging row.
 static int bw_key_bits(const hl_handle* h, int32_t stg_rows) {
   return hl_bit_width((uint64_t)h->n_hot + (uint64_t)stg_rows);
 }
 
 template <int VEC, bool BF>
-static void launch_bwd(const hl_handle* h, uint32_t tiles, dim3 g2, hipStream_t s, const uint32_t* sk, const uint32_t* sv, uint32_t n,
-                       const float* dY, eb_geom g, void* w_hot, void* stg, uint32_t n_hot, float lr, bw_ws& ws) {
-  HL_KERNEL(h, s, "bw_reduce1", (bw_reduce1<VEC, BF>), dim3(tiles, g.cchunks), dim3(RB_BLOCK), 0, s, sk, sv, n, dY, g, w_hot, stg,
-                     n_hot, lr, ws.tfirst, ws.tlast, ws.tflag, ws.tkey);
-  HL_KERNEL(h, s, "bw_reduce2", (bw_reduce2<VEC, BF>), dim3(tiles, g.cchunks), dim3(RB_BLOCK), 0, s, tiles, g, w_hot, stg, n_hot,
-                     lr, ws.tfirst, ws.tlast, ws.tflag, ws.tkey);
-  (void)g2;
+static void launch_bwd(const hl_handle* h, uint32_t tiles, hipStream_t s, const uint32_t* sk, const uint32_t* sv,
+                       uint32_t n, const float* dY, eb_geom g, void* w_hot, void* stg, uint32_t n_hot, float lr,
+                       bw_ws& ws, int part) {
+  const dim3 grid(tiles, g.cchunks);
+  if (part == 0) {
+    HL_KERNEL(h, s, "bw_reduce1", (bw_reduce1<VEC, BF, false>), grid, dim3(RB_BLOCK), 0, s, sk, sv, n, dY, g, w_hot,
+              stg, n_hot, lr, ws.tfirst, ws.tlast, ws.tflag, ws.tkey, ws.gc, ws.gc_rows);
+    HL_KERNEL(h, s, "bw_reduce2", (bw_reduce2<VEC, BF, false>), grid, dim3(RB_BLOCK), 0, s, tiles, g, w_hot, stg,
+              n_hot, lr, ws.tfirst, ws.tlast, ws.tflag, ws.tkey, ws.gc, ws.gc_rows);
+  } else if (part == 1) {
+    HL_KERNEL(h, s, "bw_reduce1", (bw_reduce1<VEC, BF, true>), grid, dim3(RB_BLOCK), 0, s, sk, sv, n, dY, g, w_hot,
+              stg, n_hot, lr, ws.tfirst, ws.tlast, ws.tflag, ws.tkey, ws.gc, ws.gc_rows);
+    HL_KERNEL(h, s, "bw_reduce2", (bw_reduce2<VEC, BF, true>), grid, dim3(RB_BLOCK), 0, s, tiles, g, w_hot, stg,
+              n_hot, lr, ws.tfirst, ws.tlast, ws.tflag, ws.tkey, ws.gc, ws.gc_rows);
+  } else {
+    uint32_t b = hl_div_up(n, 256);
+    if (b > 4096) b = 4096;
+    HL_KERNEL(h, s, "bw_cold", (bw_cold<VEC, BF>), dim3(b, g.cchunks), dim3(256), 0, s, sk, n, g, stg, n_hot, lr,
+              ws.gc, ws.gc_rows);
+  }
 }
 
 extern "C" hl_status hl_embbag_bwd_plan(hl_handle* h, int32_t stg_rows, const int32_t* codes, const int32_t* bag_ptr,
@@ -680,16 +811,22 @@ extern "C" hl_status hl_embbag_bwd_plan(hl_handle* h, int32_t stg_rows, const in
   return HL_OK;
 }
 
-extern "C" hl_status hl_embbag_bwd_apply(hl_handle* h, void* w_hot, void* staging, int32_t stg_rows, int32_t n_samples,
-                                         int32_t bps, int64_t n_lookups, const float* dY, float lr, void* workspace,
-                                         size_t ws_bytes, hl_stream stream) {
+extern "C" hl_status hl_embbag_bwd_apply_part(hl_handle* h, void* w_hot, void* staging, int32_t stg_rows,
+                                              int32_t n_samples, int32_t bps, int64_t n_lookups, const float* dY,
+                                              float lr, int32_t part, void* workspace, size_t ws_bytes,
+                                              hl_stream stream) {
   if (!h || n_samples < 0 || bps < 1 || n_lookups < 0 || stg_rows < 0 || !workspace) return HL_ERR_INVALID_ARG;
+  if (part < 0 || part > 2) return HL_ERR_INVALID_ARG;
   const int64_t n_bags = (int64_t)n_samples * bps;
   if (h->ws_last != workspace || h->ws_kind != HL_WSK_BWD_PLAN || h->ws_n != n_lookups || h->ws_bags != n_bags ||
       h->ws_stg != stg_rows)
     return HL_ERR_INVALID_ARG;  // no matching plan is held by this workspace
-  if (n_lookups == 0 || n_samples == 0) return HL_OK;
-  if (!dY || (h->n_hot && !w_hot) || (stg_rows && !staging)) return HL_ERR_INVALID_ARG;
+  if (part == 2 && !h->ws_part1) return HL_ERR_INVALID_ARG;  // the first half has not run on this plan
+  if (n_lookups == 0 || n_samples == 0) {
+    if (part == 1) h->ws_part1 = 1;
+    return HL_OK;
+  }
+  if ((part != 2 && (!dY || (h->n_hot && !w_hot))) || (stg_rows && !staging)) return HL_ERR_INVALID_ARG;
   if (ws_bytes < hl_bwd_ws_bytes(h, n_lookups, n_bags)) return HL_ERR_CAPACITY;
   hipStream_t s = (hipStream_t)stream;
   hl_carver c = hl_carver::after_header(workspace, ws_bytes);
@@ -699,20 +836,27 @@ extern "C" hl_status hl_embbag_bwd_apply(hl_handle* h, void* w_hot, void* stagin
   hl_sort_result(ws.sort, bw_key_bits(h, stg_rows), &sk, &sv);
   const uint32_t n = (uint32_t)n_lookups;
   const size_t es = h->dtype == HL_F32 ? 4 : 2;
-  const int vec = eb_pick_vec(h->dim, es, {w_hot, staging, dY});
+  const int vec = eb_pick_vec(h->dim, es, {w_hot, staging, part == 2 ? nullptr : dY});
   eb_geom g = eb_make_geom(h->dim, vec);
   const uint32_t te = (uint32_t)(RB_WAVES * g.NG * RB_E);
   const uint32_t tiles = hl_div_up(n, te);
   if (tiles > ws.tiles) return HL_ERR_CAPACITY;
   const bool bf = h->dtype == HL_BF16;
-  dim3 g2(tiles, g.cchunks);
-#define BWD(V, B) launch_bwd<V, B>(h, tiles, g2, s, sk, sv, n, dY, g, w_hot, staging, h->n_hot, lr, ws)
+#define BWD(V, B) launch_bwd<V, B>(h, tiles, s, sk, sv, n, dY, g, w_hot, staging, h->n_hot, lr, ws, part)
   if (vec == 4) { if (bf) BWD(4, true); else BWD(4, false); }
   else if (vec == 2) { if (bf) BWD(2, true); else BWD(2, false); }
   else { if (bf) BWD(1, true); else BWD(1, false); }
 #undef BWD
   HL_LAUNCHED();
+  if (part == 1) h->ws_part1 = 1;
   return HL_OK;
+}
+
+extern "C" hl_status hl_embbag_bwd_apply(hl_handle* h, void* w_hot, void* staging, int32_t stg_rows, int32_t n_samples,
+                                         int32_t bps, int64_t n_lookups, const float* dY, float lr, void* workspace,
+                                         size_t ws_bytes, hl_stream stream) {
+  return hl_embbag_bwd_apply_part(h, w_hot, staging, stg_rows, n_samples, bps, n_lookups, dY, lr, 0, workspace,
+                                  ws_bytes, stream);
 }
 
 extern "C" hl_status hl_embbag_bwd_sgd(hl_handle* h, void* w_hot, void* staging, int32_t stg_rows,

@@ -348,3 +348,34 @@ extern "C" hl_status hl_hot_fill(const hl_handle* h, const uint32_t* hot_ids, co
   return hl_launch_gather(h, hot_ids, nullptr, h->n_hot, w_host, h->n_rows, w_hot, h->row_bytes, h->d_err,
                           (hipStream_t)stream);
 }
+
+// ----------------------------------------------------------------------------- streams
+extern "C" hl_status hl_stream_create(int32_t first_cu, int32_t n_cu, int32_t complement, hl_stream* out) {
+  if (!out || first_cu < 0 || n_cu < 0) return HL_ERR_INVALID_ARG;
+  int dev = 0, ncu = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+    return HL_ERR_HIP;
+  if (n_cu == 0) {  // no mask
+    hipStream_t s;
+    if (hipStreamCreateWithFlags(&s, hipStreamNonBlocking) != hipSuccess) return HL_ERR_HIP;
+    *out = (hl_stream)s;
+    return HL_OK;
+  }
+  if (first_cu + n_cu > ncu || (complement && n_cu >= ncu)) return HL_ERR_INVALID_ARG;
+  const int words = (ncu + 31) / 32;
+  std::vector<uint32_t> mask((size_t)words, 0u);
+  for (int c = 0; c < ncu; ++c) {
+    const bool in = c >= first_cu && c < first_cu + n_cu;
+    if (in != (complement != 0)) mask[(size_t)c / 32] |= 1u << (c % 32);
+  }
+  hipStream_t s;
+  if (hipExtStreamCreateWithCUMask(&s, (uint32_t)words, mask.data()) != hipSuccess) return HL_ERR_HIP;
+  *out = (hl_stream)s;
+  return HL_OK;
+}
+
+extern "C" hl_status hl_stream_destroy(hl_stream s) {
+  if (!s) return HL_ERR_INVALID_ARG;
+  return hipStreamDestroy((hipStream_t)s) == hipSuccess ? HL_OK : HL_ERR_HIP;
+}

@@ -54,6 +54,7 @@ struct hl_handle {
   int ws_kind;           // HL_WSK_*
   int64_t ws_n, ws_bags; // its lookups and bags
   int32_t ws_stg;        // its staging rows
+  int ws_part1;          // the first half of the backward's apply ran on that plan
   uint64_t* cg_table;    // cold-gather hash table (kept clean between calls)
   uint32_t cg_slots;     // its slots
 };
@@ -67,6 +68,7 @@ static inline void hl_ws_note(hl_handle* h, const void* ws, int kind, int64_t n 
   h->ws_n = n;
   h->ws_bags = bags;
   h->ws_stg = stg;
+  h->ws_part1 = 0;
 }
 
 // ----------------------------------------------------------------------------- errors
@@ -224,6 +226,57 @@ __device__ __forceinline__ uint32_t hl_lookback(const uint64_t* st, uint32_t til
       if (++spins > HL_SPIN_LIMIT) {
         hl_flag(err, HL_DEVERR_STALL);
         return excl;
+      }
+      __builtin_amdgcn_s_sleep(1);
+    }
+  }
+  return excl;
+}
+
+// Exclusive prefix of `tile` over tiles [0, tile) from single-value status
+// words (hl_st_pack), read by the whole block: thread t looks at tile j - t of
+// the current window, so one round trip covers blockDim.x predecessors, and the
+// walk stops at the nearest inclusive prefix.  Every thread of the block calls
+// it (uniform control flow) and receives the result.
+__device__ __forceinline__ uint32_t hl_block_lookback(const uint64_t* st, uint32_t tile, uint32_t epoch,
+                                                      uint32_t* err) {
+  __shared__ int s_first, s_first_pre;
+  __shared__ uint32_t s_part[16];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, nw = (int)(blockDim.x >> 6);
+  uint32_t excl = 0, spins = 0;
+  int64_t j = (int64_t)tile - 1;
+  while (j >= 0) {
+    const int64_t p = j - tid;
+    const uint64_t wd = p >= 0 ? hl_st_load(st + p) : hl_st_pack(epoch, HL_ST_PRE, 0);
+    const uint32_t f = (uint32_t)((wd >> 30) & 3ull);
+    const bool ok = (uint32_t)(wd >> 32) == epoch && f != 0;
+    const bool stop = !ok || f == HL_ST_PRE;
+    if (tid == 0) s_first = 0x7FFFFFFF;
+    __syncthreads();
+    const uint64_t sm = __ballot(stop);
+    if (lane == 0 && sm) atomicMin(&s_first, w * 64 + __ffsll((unsigned long long)sm) - 1);
+    __syncthreads();
+    const int first = s_first;
+    if (tid == first) s_first_pre = ok ? 1 : 0;
+    __syncthreads();
+    const bool none = first == 0x7FFFFFFF;
+    const bool pre = !none && s_first_pre;
+    const int use = none ? (int)blockDim.x : (pre ? first + 1 : first);  // words [0, use) are summed
+    uint32_t v = tid < use ? (uint32_t)(wd & 0x3FFFFFFFu) : 0u;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+    if (lane == 0) s_part[w] = v;
+    __syncthreads();
+    uint32_t tot = 0;
+    for (int q = 0; q < nw; ++q) tot += s_part[q];
+    __syncthreads();  // s_first, s_first_pre and s_part are reused
+    excl += tot;
+    if (pre) break;
+    j -= use;
+    if (!none) {  // an unpublished predecessor: wait for it
+      if (++spins > HL_SPIN_LIMIT) {
+        if (tid == 0) hl_flag(err, HL_DEVERR_STALL);
+        break;
       }
       __builtin_amdgcn_s_sleep(1);
     }

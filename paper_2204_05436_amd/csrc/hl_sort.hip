@@ -133,8 +133,12 @@ srt_pass(const uint32_t* __restrict__ kin, const uint32_t* __restrict__ vin, uin
          const uint32_t* __restrict__ part, uint32_t n_part, uint32_t* st, uint32_t* st_next, uint32_t* tile_ctr,
          uint32_t* err) {
   constexpr int PER = NB >= HL_SORT_THREADS ? NB / HL_SORT_THREADS : 1;
-  constexpr int OWNERS = NB / PER;       // threads that own digits
-  constexpr int WIN = PER >= 4 ? 8 : 16;  // look-back window per digit
+  constexpr int OWNERS = NB / PER;         // threads that own digits
+  // look-back window per digit; every predecessor read costs a load per digit
+  // (NB x tiles^2 / 2 loads when no inclusive prefix is found early), so the
+  // window stays short and the walk stops at the first inclusive prefix
+  constexpr int WIN = PER >= 4 ? 8 : 16;
+  constexpr int LOGNB = NB == 256 ? 8 : (NB == 1024 ? 10 : 11);
   __shared__ uint32_t s_tile;
   __shared__ uint32_t wcnt[HL_SORT_WAVES][NB];
   __shared__ uint32_t tdex[NB], gbase[NB];
@@ -192,7 +196,9 @@ srt_pass(const uint32_t* __restrict__ kin, const uint32_t* __restrict__ vin, uin
     const uint32_t d = (key[k] >> shift) & mask;
     dg[k] = d;
     uint64_t peers = __ballot(ok);
-    for (int q = 0; q < b; ++q) {
+    // digits are below 2^b <= NB: the bits above b match for every lane
+#pragma unroll
+    for (int q = 0; q < LOGNB; ++q) {
       const bool bit = (d >> q) & 1u;
       const uint64_t m = __ballot(bit);
       peers &= bit ? m : ~m;

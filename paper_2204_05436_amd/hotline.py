@@ -28,6 +28,18 @@ class HotlineError(RuntimeError):
 _lib = None
 P, I32, I64, U32, U64, F32, SZ = (C.c_void_p, C.c_int32, C.c_int64, C.c_uint32, C.c_uint64, C.c_float,
                                   C.c_size_t)
+
+
+class StepIO(C.Structure):
+    """hl_step_io of include/hotline.h, field for field."""
+    _fields_ = [("rows", P), ("bag_ptr", P), ("n_samples", I32), ("bags_per_sample", I32), ("n_lookups", I64),
+                ("dY", P), ("lr", F32), ("gids", P), ("codes", P), ("flags", P), ("pop_ids", P),
+                ("nonpop_ids", P), ("counts", P), ("cold_ids", P), ("n_cold", P), ("w_host", P), ("w_hot", P),
+                ("staging", P), ("staging_cap", I32), ("out", P), ("workspace", P), ("ws_bytes", SZ),
+                ("write_back", I32), ("step_flags", U32)]
+
+
+HL_STEP_UNTIED = 1
 _SIGS = {
     "hl_status_string": (C.c_char_p, [C.c_int]),
     "hl_create": (C.c_int, [C.POINTER(P), I32, P, I32, C.c_int, U32]),
@@ -50,17 +62,28 @@ _SIGS = {
     "hl_cold_gather": (C.c_int, [P, P, P, P, I32, I32, I64, P, P, I32, P, P, I32, P, P, P, SZ, P]),
     "hl_cold_plan": (C.c_int, [P, P, P, P, I32, I32, I64, P, P, I32, I32, P, P, P, SZ, P]),
     "hl_cold_fetch": (C.c_int, [P, P, P, I32, P, P, P]),
+    "hl_cold_reserve": (C.c_int, [P, I64, P]),
     "hl_cold_scatter": (C.c_int, [P, P, P, I32, P, P, P]),
     "hl_embbag_fwd": (C.c_int, [P, P, P, I32, P, P, I32, I32, I64, P, P, I32, P, P]),
+    "hl_embbag_fwd_part": (C.c_int, [P, P, P, I32, P, P, I32, I32, I64, P, P, I32, P, I32, P]),
     "hl_embbag_bwd_sgd": (C.c_int, [P, P, P, I32, P, P, I32, I32, I64, P, P, I32, P, F32, P, SZ, P]),
     "hl_embbag_bwd_plan": (C.c_int, [P, I32, P, P, I32, I32, I64, P, P, I32, P, SZ, P]),
     "hl_embbag_bwd_apply": (C.c_int, [P, P, P, I32, I32, I32, I64, P, F32, P, SZ, P]),
+    "hl_embbag_bwd_apply_part": (C.c_int, [P, P, P, I32, I32, I32, I64, P, F32, I32, P, SZ, P]),
     "hl_last_device_error": (C.c_int, [P, C.POINTER(U32)]),
     "hl_trace_enable": (C.c_int, [P, I32]),
     "hl_trace_count": (I32, [P]),
     "hl_trace_read": (C.c_int, [P, I32, C.POINTER(C.c_char_p), C.POINTER(C.c_float)]),
     "hl_trace_reset": (C.c_int, [P]),
     "hl_host_alloc": (C.c_int, [SZ, C.POINTER(P), C.POINTER(P)]),
+    "hl_stream_create": (C.c_int, [I32, I32, I32, C.POINTER(P)]),
+    "hl_pipeline_create": (C.c_int, [P, I32, C.POINTER(P)]),
+    "hl_pipeline_destroy": (C.c_int, [P]),
+    "hl_pipeline_step": (C.c_int, [P, C.POINTER(StepIO), P]),
+    "hl_pipeline_sync_writeback": (C.c_int, [P, P]),
+    "hl_pipeline_sync": (C.c_int, [P, P]),
+    "hl_pipeline_streams": (C.c_int, [P, C.POINTER(P), C.POINTER(P), C.POINTER(P)]),
+    "hl_stream_destroy": (C.c_int, [P]),
     "hl_host_free": (C.c_int, [P]),
 }
 
@@ -229,6 +252,10 @@ def hl_cold_plan(h, gids, codes, bag_ptr, n_samples, bags_per_sample, n_lookups,
         _p(ws), _nbytes(ws), _s(stream)))
 
 
+def hl_cold_reserve(h, max_lookups, stream=None):
+    _ck("hl_cold_reserve", lib().hl_cold_reserve(h.ptr, int(max_lookups), _s(stream)))
+
+
 def hl_cold_fetch(h, cold_ids, n_cold_dev, staging_cap_rows, w_host_dev, staging, stream=None):
     _ck("hl_cold_fetch", lib().hl_cold_fetch(h.ptr, _p(cold_ids), _p(n_cold_dev), int(staging_cap_rows),
                                              _p(w_host_dev), _p(staging), _s(stream)))
@@ -244,6 +271,14 @@ def hl_embbag_fwd(h, w_hot, staging, staging_rows, codes, bag_ptr, n_samples, ba
     _ck("hl_embbag_fwd", lib().hl_embbag_fwd(
         h.ptr, _p(w_hot), _p(staging), int(staging_rows), _p(codes), _p(bag_ptr), int(n_samples),
         int(bags_per_sample), int(n_lookups), _p(sample_ids), _p(n_sel_dev), int(n_sel_max), _p(out), _s(stream)))
+
+
+def hl_embbag_fwd_part(h, w_hot, staging, staging_rows, codes, bag_ptr, n_samples, bags_per_sample, n_lookups,
+                       sample_ids, n_sel_dev, n_sel_max, out, part, stream=None):
+    _ck("hl_embbag_fwd_part", lib().hl_embbag_fwd_part(
+        h.ptr, _p(w_hot), _p(staging), int(staging_rows), _p(codes), _p(bag_ptr), int(n_samples),
+        int(bags_per_sample), int(n_lookups), _p(sample_ids), _p(n_sel_dev), int(n_sel_max), _p(out), int(part),
+        _s(stream)))
 
 
 def hl_embbag_bwd_sgd(h, w_hot, staging, staging_rows, codes, bag_ptr, n_samples, bags_per_sample, n_lookups,
@@ -266,6 +301,13 @@ def hl_embbag_bwd_apply(h, w_hot, staging, staging_rows, n_samples, bags_per_sam
     _ck("hl_embbag_bwd_apply", lib().hl_embbag_bwd_apply(
         h.ptr, _p(w_hot), _p(staging), int(staging_rows), int(n_samples), int(bags_per_sample), int(n_lookups),
         _p(dY), float(lr), _p(ws), _nbytes(ws), _s(stream)))
+
+
+def hl_embbag_bwd_apply_part(h, w_hot, staging, staging_rows, n_samples, bags_per_sample, n_lookups, dY, lr, part,
+                             ws, stream=None):
+    _ck("hl_embbag_bwd_apply_part", lib().hl_embbag_bwd_apply_part(
+        h.ptr, _p(w_hot), _p(staging), int(staging_rows), int(n_samples), int(bags_per_sample), int(n_lookups),
+        _p(dY), float(lr), int(part), _p(ws), _nbytes(ws), _s(stream)))
 
 
 def hl_last_device_error(h):
@@ -292,6 +334,45 @@ def hl_trace_read(h, i):
 
 def hl_trace_reset(h):
     _ck("hl_trace_reset", lib().hl_trace_reset(h.ptr))
+
+
+def hl_stream_create(first_cu, n_cu, complement=False):
+    """Returns the raw stream handle (wrap it with torch.cuda.ExternalStream)."""
+    s = P()
+    _ck("hl_stream_create", lib().hl_stream_create(int(first_cu), int(n_cu), int(bool(complement)), C.byref(s)))
+    return s.value
+
+
+def hl_stream_destroy(stream):
+    _ck("hl_stream_destroy", lib().hl_stream_destroy(stream))
+
+
+def hl_pipeline_create(h, fetch_cus):
+    p = P()
+    _ck("hl_pipeline_create", lib().hl_pipeline_create(h.ptr, int(fetch_cus), C.byref(p)))
+    return p.value
+
+
+def hl_pipeline_destroy(p):
+    _ck("hl_pipeline_destroy", lib().hl_pipeline_destroy(p))
+
+
+def hl_pipeline_step(p, io: StepIO, stream=None):
+    _ck("hl_pipeline_step", lib().hl_pipeline_step(p, C.byref(io), _s(stream)))
+
+
+def hl_pipeline_sync_writeback(p, stream=None):
+    _ck("hl_pipeline_sync_writeback", lib().hl_pipeline_sync_writeback(p, _s(stream)))
+
+
+def hl_pipeline_sync(p, stream=None):
+    _ck("hl_pipeline_sync", lib().hl_pipeline_sync(p, _s(stream)))
+
+
+def hl_pipeline_streams(p):
+    m, f, g = P(), P(), P()
+    _ck("hl_pipeline_streams", lib().hl_pipeline_streams(p, C.byref(m), C.byref(f), C.byref(g)))
+    return m.value, f.value, g.value
 
 
 def hl_host_alloc(nbytes):

@@ -8,11 +8,16 @@ step is a call into libhotline.
 The pipelined schedule (the paper's pipeline figure: the popular mu-batch runs
 while the non-popular one's working parameters are gathered) uses three
 streams of default priority:
-  main  : dispatch (ids, classify, partition, remap), cold plan | fwd(popular) |
-          wait fetch, fwd(non-popular) | wait grouping, backward apply
+  main  : dispatch (ids, classify, partition, remap), cold plan | fwd(popular),
+          hot half of fwd(non-popular) | wait fetch, cold half of
+          fwd(non-popular) | wait group, staging-row updates
   fetch : wait cold plan, row fetch over the host link [, write-back after
-          the apply]
-  group : wait cold plan, the backward's grouping of lookups by code
+          the updates]
+  group : wait cold plan, the backward's grouping of lookups by code | wait
+          the hot halves of the forwards, reduction of dY and hot-row updates
+          (the staging rows' sums are kept for the main stream)
+Only the cold half of the non-popular forward and the staging-row updates
+wait for the host link.
 The cold id list and count are double-buffered so that a step's write-back
 can still read them while the next step plans."""
 from __future__ import annotations
@@ -53,7 +58,8 @@ MODES = ("pipelined", "sequential", "fwdbwd")
 
 class HotPath:
     def __init__(self, w: Workload, rows_per_table, table: hl.HostTable, max_lookups: int, max_samples: int,
-                 device="cuda", k_cap: int | None = None, staging_cap: int | None = None, writeback: bool = False):
+                 device="cuda", k_cap: int | None = None, staging_cap: int | None = None, writeback: bool = False,
+                 fetch_cus: int = 32):
         self.w = w
         self.device = device
         self.rows_per_table = np.asarray(rows_per_table, dtype=np.uint32)
@@ -85,10 +91,18 @@ class HotPath:
         self._par = 0
         self.cold_ids, self.n_cold = self._cold[0], self._ncold[0]
         self.writeback = bool(writeback)
-        self.s_fetch = torch.cuda.Stream(device=device)
-        self.s_group = torch.cuda.Stream(device=device)
+        hl.hl_cold_reserve(self.h, self.max_lookups)  # no allocation inside a captured step
+        # the native pipeline (its own streams; the host-link copy on compute units
+        # of its own, since its slow host reads would stall kernels sharing them)
+        self.fetch_cus = int(fetch_cus)
+        self.pipe = hl.hl_pipeline_create(self.h, self.fetch_cus)
+        self.io = hl.StepIO()
+        # a process has a few hardware queues (streams beyond them share queues):
+        # the Python rendering's streams are created only when it is used
+        self._py_streams = None
         ev = lambda: torch.cuda.Event()
         self.ev_plan, self.ev_fetch, self.ev_group, self.ev_apply = ev(), ev(), ev(), ev()
+        self.ev_fwdhot = ev()
         self.ev_wb = [ev(), ev()]
         self.out = torch.zeros((max(1, max_bags), w.dim), dtype=torch.float32, device=device)
         self.n_hot = 0
@@ -110,11 +124,15 @@ class HotPath:
         hl.hl_hot_fill(self.h, self.hot_ids, self.table.dev, self.w_hot)
 
     # ------------------------------------------------------------------ one mini-batch
-    def step(self, b: DevBatch, lr: float | None = None, events=None, mode: str = "pipelined", split_fwd=True):
+    def step(self, b: DevBatch, lr: float | None = None, events=None, mode: str = "pipelined", split_fwd=True,
+             untied=False):
         """classify -> partition -> remap -> cold gather (non-popular) -> forward of
         both mu-batches -> one coalesced SGD step [-> write-back of the cold rows].
 
-        mode "pipelined": the three-stream schedule of the module docstring.
+        mode "pipelined": the three-stream schedule of the module docstring,
+          enqueued by the native pipeline (hl_pipeline_step).  untied: no
+          ordering with the current stream (inputs already resident; call
+          sync() before using the results).
         mode "sequential": the fused calls in order on the current stream;
           `events`: optional list of len(STAGES)+1 torch.cuda.Event recorded
           around the stages.
@@ -126,9 +144,34 @@ class HotPath:
         B, bps, L = b.n_samples, b.bps, b.n_lookups
         if mode == "sequential":
             return self._step_sequential(b, lr, events, split_fwd)
-        h, w = self.h, self.w
-        main = torch.cuda.current_stream(self.device)
+        caller = torch.cuda.current_stream(self.device)
         capturing = torch.cuda.is_current_stream_capturing()
+        if mode == "fwdbwd" or capturing:  # the Python rendering of the schedule (a graph keeps no CU mask)
+            return self._step_pipelined(b, lr, events, mode, caller, capturing)
+        p = self._par
+        self._par ^= 1
+        self.cold_ids, self.n_cold = self._cold[p], self._ncold[p]
+        io = self.io
+        io.rows, io.bag_ptr, io.n_samples, io.bags_per_sample, io.n_lookups = (
+            b.rows.data_ptr(), b.bag_ptr.data_ptr(), B, bps, L)
+        io.dY, io.lr = (b.dY.data_ptr() if b.dY is not None else None), float(lr)
+        io.gids, io.codes, io.flags = self.gids.data_ptr(), self.codes.data_ptr(), self.flags.data_ptr()
+        io.pop_ids, io.nonpop_ids, io.counts = self.pop.data_ptr(), self.nonpop.data_ptr(), self.counts.data_ptr()
+        io.cold_ids, io.n_cold = self.cold_ids.data_ptr(), self.n_cold.data_ptr()
+        io.w_host, io.w_hot, io.staging, io.staging_cap = (
+            self.table.dev, self.w_hot.data_ptr(), self.staging.data_ptr(), self.staging_cap)
+        io.out, io.workspace, io.ws_bytes = self.out.data_ptr(), self.ws.data_ptr(), self.ws.numel()
+        io.write_back = int(self.writeback)
+        io.step_flags = hl.HL_STEP_UNTIED if untied else 0
+        hl.hl_pipeline_step(self.pipe, io, caller)
+
+    def sync(self, stream=None):
+        """The stream (default: current) waits for every step enqueued so far."""
+        hl.hl_pipeline_sync(self.pipe, torch.cuda.current_stream(self.device) if stream is None else stream)
+
+    def _step_pipelined(self, b, lr, events, mode, main, capturing):
+        h, w = self.h, self.w
+        B, bps, L = b.n_samples, b.bps, b.n_lookups
         p = self._par
         self._par ^= 1
         cold, ncold = self._cold[p], self._ncold[p]
@@ -155,16 +198,26 @@ class HotPath:
         if b.dY is not None:
             hl.hl_embbag_bwd_plan(h, self.staging_cap, self.codes, b.bag_ptr, B, bps, L, None, None, B, self.ws,
                                   stream=self.s_group)
+        # popular mu-batch, and the hot rows of the non-popular one, while the fetch runs
+        hl.hl_embbag_fwd_part(h, self.w_hot, self.staging, self.staging_cap, self.codes, b.bag_ptr, B, bps, L,
+                              self.pop, self.counts[0:], B, self.out, 0)
+        hl.hl_embbag_fwd_part(h, self.w_hot, self.staging, self.staging_cap, self.codes, b.bag_ptr, B, bps, L,
+                              self.nonpop, self.counts[1:], B, self.out, 1)
+        self.ev_fwdhot.record(main)
+        # the backward's reduction and hot-row updates once both forwards have read the hot rows
+        self.s_group.wait_event(self.ev_fwdhot)
+        if b.dY is not None:
+            hl.hl_embbag_bwd_apply_part(h, self.w_hot, self.staging, self.staging_cap, B, bps, L, b.dY, lr, 1,
+                                        self.ws, stream=self.s_group)
         self.ev_group.record(self.s_group)
-        # popular mu-batch while the fetch runs
-        hl.hl_embbag_fwd(h, self.w_hot, self.staging, self.staging_cap, self.codes, b.bag_ptr, B, bps, L,
-                         self.pop, self.counts[0:], B, self.out)
+        # the staging rows: cold half of the non-popular forward, then their updates
         main.wait_event(self.ev_fetch)
-        hl.hl_embbag_fwd(h, self.w_hot, self.staging, self.staging_cap, self.codes, b.bag_ptr, B, bps, L,
-                         self.nonpop, self.counts[1:], B, self.out)
+        hl.hl_embbag_fwd_part(h, self.w_hot, self.staging, self.staging_cap, self.codes, b.bag_ptr, B, bps, L,
+                              self.nonpop, self.counts[1:], B, self.out, 2)
         main.wait_event(self.ev_group)
         if b.dY is not None:
-            hl.hl_embbag_bwd_apply(h, self.w_hot, self.staging, self.staging_cap, B, bps, L, b.dY, lr, self.ws)
+            hl.hl_embbag_bwd_apply_part(h, self.w_hot, self.staging, self.staging_cap, B, bps, L, b.dY, lr, 2,
+                                        self.ws)
         if mode == "fwdbwd" and events is not None:
             events[1].record(main)
         if self.writeback:
@@ -176,8 +229,9 @@ class HotPath:
                 main.wait_event(self.ev_wb[p])
 
     def capture(self, b: DevBatch, lr: float | None = None):
-        """A HIP graph of one pipelined step over batch b: replaying it runs the
-        whole step (all three streams, joined) with one launch.  Run one eager
+        """A HIP graph of one pipelined step over batch b (the Python rendering
+        of the schedule, on unmasked streams): replaying it runs the whole step
+        (all three streams, joined) with one launch.  Run one eager
         step of at least this size first (the cold plan's hash table is
         allocated on first use).  Returns (graph, cold_ids, n_cold): the
         buffers the graph's cold plan writes."""
@@ -234,5 +288,24 @@ class HotPath:
     def device_error(self):
         return hl.hl_last_device_error(self.h)
 
+    @property
+    def s_fetch(self):
+        return self._pystreams()[0]
+
+    @property
+    def s_group(self):
+        return self._pystreams()[1]
+
+    def _pystreams(self):
+        """Streams of the Python rendering of the schedule (graph capture and the
+        fwd+bwd timing mode), created on first use."""
+        if self._py_streams is None:
+            self._py_streams = (torch.cuda.Stream(device=self.device), torch.cuda.Stream(device=self.device))
+        return self._py_streams
+
     def close(self):
+        torch.cuda.synchronize()
+        if self.pipe:
+            hl.hl_pipeline_destroy(self.pipe)
+            self.pipe = None
         self.h.close()

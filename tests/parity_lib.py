@@ -126,16 +126,27 @@ def run_gpu_stages(hp: HotPath, prof, mb, dY, k=None, hot_ids=None, split=False)
     r["codes"] = hp.codes[:L].cpu().numpy().copy()
     r["staging_pre"] = hp.staging[:min(n_cold, hp.staging_cap)].cpu().numpy().copy()
     hp.out.zero_()
-    hl.hl_embbag_fwd(h, hp.w_hot, hp.staging, hp.staging_cap, hp.codes, b.bag_ptr, B, bps, L, hp.pop,
-                     hp.counts[0:], B, hp.out)
-    hl.hl_embbag_fwd(h, hp.w_hot, hp.staging, hp.staging_cap, hp.codes, b.bag_ptr, B, bps, L, hp.nonpop,
-                     hp.counts[1:], B, hp.out)
-    r["out"] = hp.out[:B * bps].cpu().numpy().copy()
     if split:
+        # as the pipelined step: popular forward, hot half of the non-popular one, the
+        # backward's plan and first half on side streams, then the staging rows
+        hl.hl_embbag_fwd_part(h, hp.w_hot, hp.staging, hp.staging_cap, hp.codes, b.bag_ptr, B, bps, L, hp.pop,
+                              hp.counts[0:], B, hp.out, 0)
+        hl.hl_embbag_fwd_part(h, hp.w_hot, hp.staging, hp.staging_cap, hp.codes, b.bag_ptr, B, bps, L, hp.nonpop,
+                              hp.counts[1:], B, hp.out, 1)
         _on_side(lambda st: hl.hl_embbag_bwd_plan(h, hp.staging_cap, hp.codes, b.bag_ptr, B, bps, L, None, None, B,
                                                   hp.ws, stream=st))
-        hl.hl_embbag_bwd_apply(h, hp.w_hot, hp.staging, hp.staging_cap, B, bps, L, b.dY, hp.w.lr, hp.ws)
+        _on_side(lambda st: hl.hl_embbag_bwd_apply_part(h, hp.w_hot, hp.staging, hp.staging_cap, B, bps, L, b.dY,
+                                                        hp.w.lr, 1, hp.ws, stream=st))
+        hl.hl_embbag_fwd_part(h, hp.w_hot, hp.staging, hp.staging_cap, hp.codes, b.bag_ptr, B, bps, L, hp.nonpop,
+                              hp.counts[1:], B, hp.out, 2)
+        r["out"] = hp.out[:B * bps].cpu().numpy().copy()
+        hl.hl_embbag_bwd_apply_part(h, hp.w_hot, hp.staging, hp.staging_cap, B, bps, L, b.dY, hp.w.lr, 2, hp.ws)
     else:
+        hl.hl_embbag_fwd(h, hp.w_hot, hp.staging, hp.staging_cap, hp.codes, b.bag_ptr, B, bps, L, hp.pop,
+                         hp.counts[0:], B, hp.out)
+        hl.hl_embbag_fwd(h, hp.w_hot, hp.staging, hp.staging_cap, hp.codes, b.bag_ptr, B, bps, L, hp.nonpop,
+                         hp.counts[1:], B, hp.out)
+        r["out"] = hp.out[:B * bps].cpu().numpy().copy()
         hl.hl_embbag_bwd_sgd(h, hp.w_hot, hp.staging, hp.staging_cap, hp.codes, b.bag_ptr, B, bps, L, None, None,
                              B, b.dY, hp.w.lr, hp.ws)
     r["w_hot_new"] = hp.w_hot[:n_hot].cpu().numpy().copy()

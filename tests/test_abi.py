@@ -24,7 +24,9 @@ def test_header_declares_the_path():
     names = declared()
     for n in ["hl_create", "hl_profile_count", "hl_profile_topk", "hl_classify", "hl_partition", "hl_remap",
               "hl_cold_gather", "hl_cold_plan", "hl_cold_fetch", "hl_cold_scatter", "hl_embbag_fwd",
-              "hl_embbag_bwd_sgd", "hl_embbag_bwd_plan", "hl_embbag_bwd_apply", "hl_dispatch", "hl_last_device_error"]:
+              "hl_embbag_bwd_sgd", "hl_embbag_bwd_plan", "hl_embbag_bwd_apply", "hl_dispatch", "hl_embbag_fwd_part",
+              "hl_embbag_bwd_apply_part", "hl_cold_reserve", "hl_pipeline_step", "hl_stream_create",
+              "hl_last_device_error"]:
         assert n in names
 
 

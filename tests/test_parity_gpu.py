@@ -343,6 +343,66 @@ def test_dispatch_shapes(B, T, max_len):
         table.close()
 
 
+@pytest.mark.parametrize("seed", range(6))
+def test_halves_equal_whole(seed):
+    """Forward part 1 + part 2 == part 0 and backward apply part 1 + part 2 ==
+    part 0, bit for bit, on random shapes (multi-hot bags mixing hot and staging
+    rows, empty bags, fp32 and bf16, dims needing every vector width); and the
+    staging rows are not read by the halves that run before the fetch (they are
+    poisoned with NaN meanwhile)."""
+    rng = np.random.default_rng(500 + seed)
+    dim = int(rng.choice([1, 3, 16, 64, 130]))
+    dtype = "bf16" if seed % 2 else "f32"
+    T = int(rng.integers(1, 4))
+    rows = rng.integers(20, 300, T).astype(np.uint32)
+    w = configs.Workload(name=f"halves{seed}", n_tables=T, dim=dim, dtype=dtype, batch=int(rng.integers(50, 400)),
+                         steps=1, rows_fixed=tuple(int(r) for r in rows), hot_frac=0.4, seed=seed, lr=0.05)
+    n_rows = int(rows.sum())
+    table = make_table(w, n_rows)
+    mb = _random_batch(rng, rows, w.batch, 1, 12)
+    dY = W.make_dy(w, seed, mb.n_bags)
+    hp = HotPath(w, rows, table, mb.n_lookups, w.batch)
+    try:
+        hot = np.sort(rng.choice(n_rows, hp.k_cap, replace=False)).astype(np.uint32)
+        hp.set_hot(torch.from_numpy(hot.view(np.int32)).cuda())
+        b = to_device(mb, "cuda", dY)
+        B, bps, L, h = b.n_samples, b.bps, b.n_lookups, hp.h
+        hl.hl_dispatch(h, b.rows, b.bag_ptr, B, bps, L, hp.gids, hp.codes, hp.flags, hp.pop, hp.nonpop, hp.counts,
+                       hp.ws)
+        hl.hl_cold_gather(h, hp.gids, hp.codes, b.bag_ptr, B, bps, L, None, None, B, table.dev, hp.staging,
+                          hp.staging_cap, hp.cold_ids, hp.n_cold, hp.ws)
+        w0, s0 = hp.w_hot.clone(), hp.staging.clone()
+        args = (h, hp.w_hot, hp.staging, hp.staging_cap, hp.codes, b.bag_ptr, B, bps, L, None, None, B)
+        hl.hl_embbag_fwd_part(*args, hp.out, 0)
+        whole = hp.out[:mb.n_bags].clone()
+        hp.out.fill_(7.0)
+        poison = torch.full_like(hp.staging, -1) if dtype == "bf16" else torch.full_like(hp.staging, float("nan"))
+        hp.staging.copy_(poison)
+        hl.hl_embbag_fwd_part(*args, hp.out, 1)
+        hp.staging.copy_(s0)
+        hl.hl_embbag_fwd_part(*args, hp.out, 2)
+        assert torch.equal(hp.out[:mb.n_bags].view(torch.int32), whole.view(torch.int32)), "forward halves differ"
+        hl.hl_embbag_bwd_sgd(h, hp.w_hot, hp.staging, hp.staging_cap, hp.codes, b.bag_ptr, B, bps, L, None, None, B,
+                             b.dY, w.lr, hp.ws)
+        w1, s1 = hp.w_hot.clone(), hp.staging.clone()
+        hp.w_hot.copy_(w0)
+        hl.hl_embbag_bwd_plan(h, hp.staging_cap, hp.codes, b.bag_ptr, B, bps, L, None, None, B, hp.ws)
+        with pytest.raises(hl.HotlineError):  # part 2 needs part 1
+            hl.hl_embbag_bwd_apply_part(h, hp.w_hot, hp.staging, hp.staging_cap, B, bps, L, b.dY, w.lr, 2, hp.ws)
+        hp.staging.copy_(poison)
+        hl.hl_embbag_bwd_apply_part(h, hp.w_hot, hp.staging, hp.staging_cap, B, bps, L, b.dY, w.lr, 1, hp.ws)
+        torch.cuda.synchronize()
+        assert torch.equal(hp.staging.view(torch.int16), poison.view(torch.int16)), "part 1 touched staging rows"
+        hp.staging.copy_(s0)
+        hl.hl_embbag_bwd_apply_part(h, hp.w_hot, hp.staging, hp.staging_cap, B, bps, L, b.dY, w.lr, 2, hp.ws)
+        assert torch.equal(hp.w_hot.view(torch.int16), w1.view(torch.int16)), "hot rows differ"
+        assert torch.equal(hp.staging.view(torch.int16), s1.view(torch.int16)), "staging rows differ"
+        assert hp.device_error() == 0
+    finally:
+        hp.close()
+        table.close()
+
+
 def test_empty_batch():
     w = configs.scaled(configs.WORKLOADS["tiny"], batch=0, row_scale=0.1, name="tiny-empty")
     rows = W.table_rows(w)
