@@ -369,11 +369,31 @@ typedef struct hl_step_io {
  * hl_pipeline_sync.  Back-to-back steps then run without two cross-stream
  * hops per step. */
 #define HL_STEP_UNTIED 1u
+/* Step flag: the step's hl_dispatch and hl_cold_plan were enqueued ahead by
+ * hl_pipeline_plan with the same inputs, sizes and per-step buffers (gids,
+ * codes, flags, pop_ids, nonpop_ids, counts, cold_ids, n_cold, workspace);
+ * the step skips them.  HL_ERR_INVALID_ARG if no such plan is pending. */
+#define HL_STEP_PLANNED 2u
 hl_status hl_pipeline_create(hl_handle* h, int32_t fetch_cus, hl_pipeline** out);
 hl_status hl_pipeline_destroy(hl_pipeline* p);
 hl_status hl_pipeline_step(hl_pipeline* p, const hl_step_io* io, hl_stream stream);
+/* Look-ahead segregation (Sec. IV and the pipeline figure: the accelerator
+ * classifies and segregates a mini-batch while the GPUs train the one before):
+ * enqueues hl_dispatch and hl_cold_plan of io's mini-batch on a fourth stream
+ * of the pipeline, to be consumed by a later hl_pipeline_step with
+ * HL_STEP_PLANNED and the same io.  The plan waits for every step enqueued
+ * before it (it rewrites per-step buffers and the workspace, and shares the
+ * cold-gather hash table with them) and for the write-back that last read its
+ * cold_ids, so one step ahead needs two sets of per-step buffers, alternated;
+ * the step's row fetch still waits for the previous step to end.  dY, lr,
+ * w_host, w_hot, staging, out and write_back are not read.  HL_STEP_UNTIED in
+ * io->step_flags: no wait for `stream` first.  HL_ERR_INVALID_ARG: a plan on
+ * the same workspace is still pending, or four plans are; HL_ERR_UNSUPPORTED:
+ * a pipeline without compute-unit masks (fetch_cus = 0), whose streams may
+ * share hardware queues, or `stream` under capture. */
+hl_status hl_pipeline_plan(hl_pipeline* p, const hl_step_io* io, hl_stream stream);
 hl_status hl_pipeline_sync_writeback(hl_pipeline* p, hl_stream stream);
-/* `stream` waits for every step enqueued so far (and their write-backs). */
+/* `stream` waits for every step and plan enqueued so far (and the write-backs). */
 hl_status hl_pipeline_sync(hl_pipeline* p, hl_stream stream);
 /* The pipeline's streams (main and group on the compute units the copy leaves
  * free, fetch on the copy's own), for callers that enqueue more work in the

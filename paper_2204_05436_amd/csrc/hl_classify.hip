@@ -225,6 +225,7 @@ extern "C" hl_status hl_remap(const hl_handle* h, const uint32_t* gids, int64_t 
 // to finish advances it, so no clearing is needed between calls (nor between
 // replays of a captured graph).
 #define DS_THREADS 512
+#define DS_MAX_TABLES 1024  // table bases and sizes in LDS up to this many tables
 #define DS_MAX_BAGS 4096
 #define DS_MAX_SPB 2048
 #define DS_EPOCH 0
@@ -237,6 +238,7 @@ ds_kernel(const uint32_t* __restrict__ rows, const int32_t* __restrict__ bag_ptr
           uint32_t* __restrict__ gids, int32_t* __restrict__ codes, uint8_t* __restrict__ flags, int32_t* pop,
           int32_t* nonpop, int32_t* counts, int64_t n_lookups, uint32_t* hdr, uint64_t* st, uint32_t* err) {
   __shared__ int32_t off[DS_MAX_BAGS + 1];
+  __shared__ uint32_t tb_base[DS_MAX_TABLES], tb_rows[DS_MAX_TABLES];
   __shared__ uint8_t fl[DS_MAX_SPB];
   __shared__ uint32_t s_tile, s_epoch, wsum[DS_THREADS / 64];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
@@ -253,6 +255,10 @@ ds_kernel(const uint32_t* __restrict__ rows, const int32_t* __restrict__ bag_ptr
   const int nbg = ns * bps;
   for (int j = tid; j <= nbg; j += DS_THREADS) off[j] = bag_ptr[bg0 + j];
   for (int j = tid; j < ns; j += DS_THREADS) fl[j] = 1;
+  for (int j = tid; j < n_tables; j += DS_THREADS) {
+    tb_base[j] = base[j];
+    tb_rows[j] = nrow[j];
+  }
   if (tile == 0 && tid == 0 && bag_ptr[(int64_t)n_samples * bps] != n_lookups) hl_flag(err, HL_DEVERR_SHAPE);
   __syncthreads();
   const int32_t lo = off[0], hi = (int32_t)min((int64_t)off[nbg], n_lookups);
@@ -279,7 +285,7 @@ ds_kernel(const uint32_t* __restrict__ rows, const int32_t* __restrict__ bag_ptr
       const bool in = i0 + k * DS_THREADS < hi;
       g[k] = 0xFFFFFFFFu;
       if (in) {
-        if (r[k] < nrow[t]) g[k] = base[t] + r[k];
+        if (r[k] < tb_rows[t]) g[k] = tb_base[t] + r[k];
         else hl_flag(err, HL_DEVERR_OUT_OF_RANGE);
       }
     }
@@ -353,7 +359,8 @@ extern "C" hl_status hl_dispatch(hl_handle* h, const uint32_t* rows, const int32
   if (spb > DS_MAX_SPB) spb = DS_MAX_SPB;
   if (spb < 1) spb = 1;
   const int64_t tiles = n_samples > 0 ? (n_samples + spb - 1) / spb : 0;
-  if (tiles == 0 || bps > DS_MAX_BAGS || tiles > HL_DISP_MAX_TILES || !workspace || ws_bytes < HL_WS_HEADER) {
+  if (tiles == 0 || bps > DS_MAX_BAGS || tiles > HL_DISP_MAX_TILES || h->n_tables > DS_MAX_TABLES || !workspace ||
+      ws_bytes < HL_WS_HEADER) {
     // the step by step calls (also for an empty batch)
     hl_status st = hl_lookup_gids(h, rows, bag_ptr, (int64_t)n_samples * bps, gids, stream);
     if (st == HL_OK) st = hl_classify(h, gids, bag_ptr, n_samples, bps, n_lookups, flags, stream);

@@ -119,7 +119,7 @@ cg_insert(const uint32_t* __restrict__ gids, const int32_t* __restrict__ codes, 
           int64_t n_bags, int32_t bps, const uint8_t* __restrict__ mask, uint32_t n_lookups, uint64_t n_rows,
           uint64_t* table, cg_ws ws, uint32_t* err) {
   __shared__ int32_t off[CG_BAGS + 1];
-  __shared__ uint32_t cl[CG_IR];
+  __shared__ uint32_t cl[CG_IR], cg_[CG_IR];
   __shared__ uint32_t wn[4], s_total;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int64_t b0 = (int64_t)blockIdx.x * CG_BAGS;
@@ -136,10 +136,13 @@ cg_insert(const uint32_t* __restrict__ gids, const int32_t* __restrict__ codes, 
     // positions r0 + k*256 + tid: cold and selected?
     bool cold[4];
     int32_t pos[4];
+    uint32_t gg[4];
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
+    for (int k = 0; k < 4; ++k) {  // codes and ids loaded together
       pos[k] = r0 + k * 256 + tid;
-      cold[k] = pos[k] < hi && codes[pos[k]] == -1;
+      const bool in = pos[k] < hi;
+      cold[k] = in && codes[pos[k]] == -1;
+      gg[k] = in ? gids[pos[k]] : 0u;
     }
     if (mask) {
 #pragma unroll
@@ -170,14 +173,17 @@ cg_insert(const uint32_t* __restrict__ gids, const int32_t* __restrict__ codes, 
     }
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
-      if (cold[k]) cl[base + (uint32_t)__popcll(m[k] & lt)] = (uint32_t)pos[k];
+      if (cold[k]) {
+        cl[base + (uint32_t)__popcll(m[k] & lt)] = (uint32_t)pos[k];
+        cg_[base + (uint32_t)__popcll(m[k] & lt)] = gg[k];
+      }
       base += (uint32_t)__popcll(m[k]);
     }
     __syncthreads();
     // each thread inserts about one lookup
     for (uint32_t e = tid; e < tot; e += 256) {
       const uint32_t i = cl[e];
-      const uint32_t g = gids[i];
+      const uint32_t g = cg_[e];
       if (g >= n_rows) {
         hl_flag(err, HL_DEVERR_OUT_OF_RANGE);
         ws.slotof[i] = 0xFFFFFFFFu;
@@ -227,17 +233,18 @@ cg_rank(const uint32_t* __restrict__ gids, const int32_t* __restrict__ codes, ui
   int32_t cd[4];
   uint32_t slot[4], g[4];
   bool first[4];
+  // codes, slots and ids loaded together (the slot and id only matter for code -1)
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
     const uint64_t i = tb + w * 256 + k * 64 + lane;
-    cd[k] = i < n_lookups ? codes[i] : 0;
+    const bool in = i < n_lookups;
+    cd[k] = in ? codes[i] : 0;
+    slot[k] = in ? ws.slotof[i] : 0xFFFFFFFFu;
+    g[k] = in ? gids[i] : 0u;
   }
 #pragma unroll
-  for (int k = 0; k < 4; ++k) {
-    const uint64_t i = tb + w * 256 + k * 64 + lane;
-    slot[k] = cd[k] == -1 ? ws.slotof[i] : 0xFFFFFFFFu;
-    g[k] = cd[k] == -1 ? gids[i] : 0u;
-  }
+  for (int k = 0; k < 4; ++k)
+    if (cd[k] != -1) slot[k] = 0xFFFFFFFFu;
   uint32_t wsum = 0;
 #pragma unroll
   for (int k = 0; k < 4; ++k) {

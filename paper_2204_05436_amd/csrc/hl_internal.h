@@ -63,6 +63,8 @@ struct hl_handle {
 #define HL_WSK_BWD_PLAN 2
 static inline void hl_ws_note(hl_handle* h, const void* ws, int kind, int64_t n = 0, int64_t bags = 0,
                               int32_t stg = 0) {
+  // a call on another workspace leaves the recorded one intact
+  if (kind == HL_WSK_OTHER && ws != h->ws_last) return;
   h->ws_last = ws;
   h->ws_kind = kind;
   h->ws_n = n;
@@ -97,12 +99,13 @@ __device__ __forceinline__ int32_t hl_hot_slot(const uint64_t* __restrict__ bm,
                                                const uint32_t* __restrict__ rank, uint32_t g) {
   const uint32_t blk = g >> 8;
   const ulonglong2* p = reinterpret_cast<const ulonglong2*>(bm + (size_t)blk * 4);
+  // the rank word is loaded with the bitmap words, not after the membership test
   ulonglong2 a = p[0], b = p[1];
+  uint32_t r = rank[blk];
   uint64_t w[4] = {a.x, a.y, b.x, b.y};
   const uint32_t wi = (g >> 6) & 3, bit = g & 63;
   uint64_t word = w[wi];
   if (!((word >> bit) & 1ull)) return -1;
-  uint32_t r = rank[blk];
 #pragma unroll
   for (uint32_t k = 0; k < 3; ++k)
     if (k < wi) r += __popcll(w[k]);

@@ -13,14 +13,76 @@
 // The fetch stream runs on a few compute units of its own and the others on
 // the rest: the copy keeps its units' memory queues full of slow host reads,
 // and a kernel with a block on such a unit would wait for them.
+//
+// Streams hand over through flags in device memory rather than events: after
+// the producing kernel, a one-wave kernel stores the step's sequence number
+// into the flag (the producer's writes are complete and written back at its
+// kernel boundary); before the consuming kernels, a one-wave kernel waits until
+// the flag reaches that number (a bounded wait: past the limit it sets
+// HL_DEVERR_STALL and returns).  A handover costs two small kernels (~3 us
+// each) instead of an event dependency between streams (~17 us measured).
+// Flags need streams that progress independently: a stream with a compute-unit
+// mask has a hardware queue of its own.  Without masks (fetch_cus = 0) streams
+// may share a hardware queue, where a wait ahead of its signal would stall, so
+// the handovers are events then.
+//
+// Look-ahead (hl_pipeline_plan): the dispatch and cold plan of the next
+// mini-batch, which read only its inputs and the fixed hot set, run on a
+// fourth stream while the current step trains, as the accelerator segregates
+// the next mini-batch while the GPUs train (Sec. IV, pipeline figure).  Only
+// that work moves ahead: the next step's row fetch still waits for the end of
+// the current step (its staging rows and, with write-back, their write-back),
+// so no row is read before the update that precedes it.  A plan waits for
+// every step enqueued before it (their per-step buffers and workspace are the
+// plan's to rewrite), so two alternating sets of per-step buffers suffice.
 #include <vector>
 
 #include "hl_internal.h"
 
+#define PF_PLAN 0
+#define PF_FETCH 1
+#define PF_FWDHOT 2
+#define PF_GROUP 3
+#define PF_WB 5   // two: one per cold list
+#define PF_LOOK 7 // a look-ahead plan: its own sequence
+#define PF_DONE 8 // the end of a step on the main stream
+#define PF_N 16
+#define PL_PLANS 4 // look-ahead plans not yet stepped
+
+__global__ void pl_signal(uint32_t* flag, uint32_t v) {
+  if (threadIdx.x == 0) __hip_atomic_store(flag, v, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__global__ void pl_wait(const uint32_t* flag, uint32_t v, uint32_t* err) {
+  if (threadIdx.x != 0) return;
+  uint32_t spins = 0;
+  // (int32_t)(x - v) >= 0: x has reached v (sequence numbers wrap)
+  while ((int32_t)(__hip_atomic_load(flag, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT) - v) < 0) {
+    if (++spins > HL_SPIN_LIMIT) {
+      hl_flag(err, HL_DEVERR_STALL);
+      return;
+    }
+    __builtin_amdgcn_s_sleep(8);
+  }
+}
+
+struct pl_plan {
+  hl_step_io io;      // the inputs and per-step buffers it ran with
+  uint32_t seq;       // its PF_LOOK value
+  bool pending;       // enqueued, not yet consumed by a step
+};
+
 struct hl_pipeline {
   hl_handle* h;
-  hipStream_t main, fetch, group;
-  hipEvent_t ev_in, ev_plan, ev_fetch, ev_fwdhot, ev_group, ev_apply, ev_out, ev_wb[2];
+  hipStream_t main, fetch, group, plan;
+  pl_plan plans[PL_PLANS];
+  uint32_t plan_seq;      // sequence number of the last look-ahead plan
+  uint32_t* flags;        // [PF_N] device
+  uint32_t seq;           // sequence number of the last step
+  uint32_t wb_seq[2];     // step whose write-back last read each cold list
+  bool use_flags;         // handovers through device flags (masked streams)
+  hipEvent_t ev[PF_N];    // the same handovers as events; ev[PF_WB + i] always
+  hipEvent_t ev_in, ev_out, ev_pin, ev_plan;
   const void* wb_ids[2];  // the cold list each write-back event covers
   int wb_next;
 };
@@ -29,13 +91,14 @@ extern "C" hl_status hl_pipeline_destroy(hl_pipeline* p) {
   if (!p) return HL_ERR_INVALID_ARG;
   hl_status st = HL_OK;
   if (hipDeviceSynchronize() != hipSuccess) st = HL_ERR_HIP;
-  hipEvent_t evs[] = {p->ev_in, p->ev_plan, p->ev_fetch, p->ev_fwdhot, p->ev_group, p->ev_apply, p->ev_out,
-                      p->ev_wb[0], p->ev_wb[1]};
-  for (hipEvent_t e : evs)
+  for (hipEvent_t e : p->ev)
     if (e && hipEventDestroy(e) != hipSuccess) st = HL_ERR_HIP;
-  hipStream_t ss[] = {p->main, p->fetch, p->group};
+  for (hipEvent_t e : {p->ev_in, p->ev_out, p->ev_pin, p->ev_plan})
+    if (e && hipEventDestroy(e) != hipSuccess) st = HL_ERR_HIP;
+  hipStream_t ss[] = {p->main, p->fetch, p->group, p->plan};
   for (hipStream_t s : ss)
     if (s && hipStreamDestroy(s) != hipSuccess) st = HL_ERR_HIP;
+  if (p->flags && hipFree(p->flags) != hipSuccess) st = HL_ERR_HIP;
   delete p;
   return st;
 }
@@ -44,24 +107,30 @@ extern "C" hl_status hl_pipeline_create(hl_handle* h, int32_t fetch_cus, hl_pipe
   if (!h || !out || fetch_cus < 0) return HL_ERR_INVALID_ARG;
   hl_pipeline* p = new hl_pipeline();
   p->h = h;
-  hl_stream s[3] = {nullptr, nullptr, nullptr};
+  hl_stream s[4] = {nullptr, nullptr, nullptr, nullptr};
   hl_status st = hl_stream_create(0, fetch_cus, 0, &s[0]);
-  if (st == HL_OK) st = hl_stream_create(0, fetch_cus, 1, &s[1]);
-  if (st == HL_OK) st = hl_stream_create(0, fetch_cus, 1, &s[2]);
+  for (int i = 1; i < 4; ++i)
+    if (st == HL_OK) st = hl_stream_create(0, fetch_cus, 1, &s[i]);
   p->fetch = (hipStream_t)s[0];
   p->main = (hipStream_t)s[1];
   p->group = (hipStream_t)s[2];
-  hipEvent_t* evs[] = {&p->ev_in, &p->ev_plan, &p->ev_fetch, &p->ev_fwdhot, &p->ev_group, &p->ev_apply,
-                       &p->ev_out, &p->ev_wb[0], &p->ev_wb[1]};
-  for (hipEvent_t* e : evs)
+  p->plan = (hipStream_t)s[3];
+  p->use_flags = fetch_cus > 0;
+  hipEvent_t* extra[] = {&p->ev_in, &p->ev_out, &p->ev_pin, &p->ev_plan};
+  for (int i = 0; i < PF_N + 4; ++i) {
+    hipEvent_t* e = i < PF_N ? &p->ev[i] : extra[i - PF_N];
     if (st == HL_OK && hipEventCreateWithFlags(e, hipEventDisableTiming) != hipSuccess) st = HL_ERR_HIP;
+  }
+  if (st == HL_OK && hipMalloc(&p->flags, PF_N * sizeof(uint32_t)) != hipSuccess) st = HL_ERR_HIP;
+  if (st == HL_OK && hipMemset(p->flags, 0, PF_N * sizeof(uint32_t)) != hipSuccess) st = HL_ERR_HIP;
   if (st != HL_OK) {
     hl_pipeline_destroy(p);
     return st;
   }
-  // the write-back events start recorded (nothing to wait for)
+  // the write-back and plan events start recorded (nothing to wait for)
   for (int i = 0; i < 2; ++i)
-    if (hipEventRecord(p->ev_wb[i], p->fetch) != hipSuccess) st = HL_ERR_HIP;
+    if (hipEventRecord(p->ev[PF_WB + i], p->fetch) != hipSuccess) st = HL_ERR_HIP;
+  if (hipEventRecord(p->ev_plan, p->plan) != hipSuccess) st = HL_ERR_HIP;
   *out = p;
   return st;
 }
@@ -76,68 +145,166 @@ extern "C" hl_status hl_pipeline_create(hl_handle* h, int32_t fetch_cus, hl_pipe
     if ((x) != hipSuccess) return HL_ERR_HIP;       \
   } while (0)
 
+// handover f of step v: stream s has enqueued the producer
+static hl_status pl_sig(hl_pipeline* p, hipStream_t s, int f, uint32_t v) {
+  if (p->use_flags) {
+    hipLaunchKernelGGL(pl_signal, dim3(1), dim3(64), 0, s, p->flags + f, v);
+    if (hipGetLastError() != hipSuccess) return HL_ERR_HIP;
+    if (f < PF_WB) return HL_OK;  // the write-back events also serve the host-side syncs
+  }
+  return hipEventRecord(p->ev[f], s) == hipSuccess ? HL_OK : HL_ERR_HIP;
+}
+// stream s waits for handover f of step v
+static hl_status pl_wt(hl_pipeline* p, hipStream_t s, int f, uint32_t v) {
+  if (!p->use_flags) return hipStreamWaitEvent(s, p->ev[f], 0) == hipSuccess ? HL_OK : HL_ERR_HIP;
+  hipLaunchKernelGGL(pl_wait, dim3(1), dim3(64), 0, s, p->flags + f, v, p->h->d_err);
+  return hipGetLastError() == hipSuccess ? HL_OK : HL_ERR_HIP;
+}
+
+static hl_status pl_not_capturing(hipStream_t s) {
+  // a graph keeps no stream's compute-unit mask, and capturing these masked
+  // streams is not supported
+  hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+  if (hipStreamIsCapturing(s, &cs) != hipSuccess) return HL_ERR_HIP;
+  return cs == hipStreamCaptureStatusNone ? HL_OK : HL_ERR_UNSUPPORTED;
+}
+
+// the inputs, sizes and per-step buffers that a plan reads or writes
+static bool pl_same_plan(const hl_step_io& a, const hl_step_io& b) {
+  return a.rows == b.rows && a.bag_ptr == b.bag_ptr && a.n_samples == b.n_samples &&
+         a.bags_per_sample == b.bags_per_sample && a.n_lookups == b.n_lookups && a.gids == b.gids &&
+         a.codes == b.codes && a.flags == b.flags && a.pop_ids == b.pop_ids && a.nonpop_ids == b.nonpop_ids &&
+         a.counts == b.counts && a.cold_ids == b.cold_ids && a.n_cold == b.n_cold &&
+         a.staging_cap == b.staging_cap && a.workspace == b.workspace && a.ws_bytes == b.ws_bytes;
+}
+
+static pl_plan* pl_pending(hl_pipeline* p, const void* ws) {
+  for (pl_plan& e : p->plans)
+    if (e.pending && e.io.workspace == ws) return &e;
+  return nullptr;
+}
+
+// the write-back slot whose last write-back read this cold list, or -1
+static int pl_wb_slot(const hl_pipeline* p, const uint32_t* cold_ids) {
+  for (int i = 0; i < 2; ++i)
+    if (p->wb_ids[i] == cold_ids) return i;
+  return -1;
+}
+
+extern "C" hl_status hl_pipeline_plan(hl_pipeline* p, const hl_step_io* io, hl_stream stream) {
+  if (!p || !io) return HL_ERR_INVALID_ARG;
+  if (!p->use_flags) return HL_ERR_UNSUPPORTED;
+  HL_TRY(pl_not_capturing((hipStream_t)stream));
+  if (pl_pending(p, io->workspace)) return HL_ERR_INVALID_ARG;  // that plan has not been stepped yet
+  pl_plan* e = nullptr;
+  for (pl_plan& c : p->plans)
+    if (!c.pending) e = &c;
+  if (!e) return HL_ERR_INVALID_ARG;  // too many plans ahead
+  hl_handle* h = p->h;
+  hipStream_t P = p->plan;
+  const hl_stream PS = (hl_stream)P;
+  if (!(io->step_flags & HL_STEP_UNTIED)) {
+    HL_HIPTRY(hipEventRecord(p->ev_pin, (hipStream_t)stream));
+    HL_HIPTRY(hipStreamWaitEvent(P, p->ev_pin, 0));
+  }
+  // every step enqueued so far has finished with its per-step buffers and
+  // workspace (and with the cold-gather hash table, which plans share)
+  if (p->seq) HL_TRY(pl_wt(p, P, PF_DONE, p->seq));
+  const int wb = pl_wb_slot(p, io->cold_ids);
+  if (wb >= 0) HL_TRY(pl_wt(p, P, PF_WB + wb, p->wb_seq[wb]));
+  const int32_t B = io->n_samples, bps = io->bags_per_sample;
+  HL_TRY(hl_dispatch(h, io->rows, io->bag_ptr, B, bps, io->n_lookups, io->gids, io->codes, io->flags, io->pop_ids,
+                     io->nonpop_ids, io->counts, io->workspace, io->ws_bytes, PS));
+  HL_TRY(hl_cold_plan(h, io->gids, io->codes, io->bag_ptr, B, bps, io->n_lookups, nullptr, nullptr, B,
+                      io->staging_cap, io->cold_ids, io->n_cold, io->workspace, io->ws_bytes, PS));
+  const uint32_t v = ++p->plan_seq;
+  HL_TRY(pl_sig(p, P, PF_LOOK, v));
+  HL_HIPTRY(hipEventRecord(p->ev_plan, P));
+  e->io = *io;
+  e->seq = v;
+  e->pending = true;
+  return HL_OK;
+}
+
 extern "C" hl_status hl_pipeline_step(hl_pipeline* p, const hl_step_io* io, hl_stream stream) {
   if (!p || !io) return HL_ERR_INVALID_ARG;
   hl_handle* h = p->h;
-  // not under stream capture: a graph keeps no stream's compute-unit mask, and
-  // capturing these masked streams is not supported
-  hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
-  if (hipStreamIsCapturing((hipStream_t)stream, &cs) != hipSuccess) return HL_ERR_HIP;
-  if (cs != hipStreamCaptureStatusNone) return HL_ERR_UNSUPPORTED;
+  HL_TRY(pl_not_capturing((hipStream_t)stream));
+  const bool planned = io->step_flags & HL_STEP_PLANNED;
+  pl_plan* e = pl_pending(p, io->workspace);
+  if (planned ? !e || !pl_same_plan(e->io, *io) : e != nullptr) return HL_ERR_INVALID_ARG;
   const int32_t B = io->n_samples, bps = io->bags_per_sample, cap = io->staging_cap;
   const int64_t L = io->n_lookups;
   hipStream_t caller = (hipStream_t)stream, m = p->main, f = p->fetch, g = p->group;
   const hl_stream M = (hl_stream)m, F = (hl_stream)f, G = (hl_stream)g;
-  // the write-back that last read this cold list (if any) must end before the plan rewrites it
-  int slot = -1;
-  for (int i = 0; i < 2; ++i)
-    if (p->wb_ids[i] == io->cold_ids) slot = i;
+  const uint32_t q = ++p->seq;
+  int slot = pl_wb_slot(p, io->cold_ids);
   const bool tie = !(io->step_flags & HL_STEP_UNTIED);
   if (tie) {
     HL_HIPTRY(hipEventRecord(p->ev_in, caller));
     HL_HIPTRY(hipStreamWaitEvent(m, p->ev_in, 0));
+    HL_HIPTRY(hipStreamWaitEvent(g, p->ev_in, 0));
+    if (planned) HL_HIPTRY(hipStreamWaitEvent(f, p->ev_in, 0));
   }
-  HL_TRY(hl_dispatch(h, io->rows, io->bag_ptr, B, bps, L, io->gids, io->codes, io->flags, io->pop_ids,
-                     io->nonpop_ids, io->counts, io->workspace, io->ws_bytes, M));
-  if (slot >= 0) HL_HIPTRY(hipStreamWaitEvent(m, p->ev_wb[slot], 0));
-  // a cold lookup makes its sample non-popular: no sample list needed
-  HL_TRY(hl_cold_plan(h, io->gids, io->codes, io->bag_ptr, B, bps, L, nullptr, nullptr, B, cap, io->cold_ids,
-                      io->n_cold, io->workspace, io->ws_bytes, M));
-  HL_HIPTRY(hipEventRecord(p->ev_plan, m));
-  HL_HIPTRY(hipStreamWaitEvent(f, p->ev_plan, 0));
+  if (planned) {
+    e->pending = false;
+    HL_TRY(pl_wt(p, m, PF_LOOK, e->seq));
+    // the fetch rewrites the staging rows: after the previous step (and its write-back)
+    HL_TRY(pl_wt(p, f, PF_LOOK, e->seq));
+    if (q > 1) HL_TRY(pl_wt(p, f, PF_DONE, q - 1));
+    HL_TRY(pl_wt(p, g, PF_LOOK, e->seq));
+  } else {
+    // the look-ahead plans use the same cold-gather hash table
+    if (p->plan_seq) HL_TRY(pl_wt(p, m, PF_LOOK, p->plan_seq));
+    HL_TRY(hl_dispatch(h, io->rows, io->bag_ptr, B, bps, L, io->gids, io->codes, io->flags, io->pop_ids,
+                       io->nonpop_ids, io->counts, io->workspace, io->ws_bytes, M));
+    // the write-back that last read this cold list must end before the plan rewrites it
+    if (slot >= 0) HL_TRY(pl_wt(p, m, PF_WB + slot, p->wb_seq[slot]));
+    // a cold lookup makes its sample non-popular: no sample list needed
+    HL_TRY(hl_cold_plan(h, io->gids, io->codes, io->bag_ptr, B, bps, L, nullptr, nullptr, B, cap, io->cold_ids,
+                        io->n_cold, io->workspace, io->ws_bytes, M));
+    HL_TRY(pl_sig(p, m, PF_PLAN, q));
+    HL_TRY(pl_wt(p, f, PF_PLAN, q));
+    HL_TRY(pl_wt(p, g, PF_PLAN, q));
+  }
+  // the working parameters of the non-popular mu-batch over the host link
   HL_TRY(hl_cold_fetch(h, io->cold_ids, io->n_cold, cap, io->w_host, io->staging, F));
-  HL_HIPTRY(hipEventRecord(p->ev_fetch, f));
-  HL_HIPTRY(hipStreamWaitEvent(g, p->ev_plan, 0));
+  HL_TRY(pl_sig(p, f, PF_FETCH, q));
+  // the backward's grouping needs only the codes
   if (io->dY)
     HL_TRY(hl_embbag_bwd_plan(h, cap, io->codes, io->bag_ptr, B, bps, L, nullptr, nullptr, B, io->workspace,
                               io->ws_bytes, G));
+  // the popular mu-batch and the hot rows of the non-popular one while the fetch runs
   HL_TRY(hl_embbag_fwd_part(h, io->w_hot, io->staging, cap, io->codes, io->bag_ptr, B, bps, L, io->pop_ids,
                             io->counts, B, io->out, 0, M));
   HL_TRY(hl_embbag_fwd_part(h, io->w_hot, io->staging, cap, io->codes, io->bag_ptr, B, bps, L, io->nonpop_ids,
                             io->counts + 1, B, io->out, 1, M));
-  HL_HIPTRY(hipEventRecord(p->ev_fwdhot, m));
-  HL_HIPTRY(hipStreamWaitEvent(g, p->ev_fwdhot, 0));
+  HL_TRY(pl_sig(p, m, PF_FWDHOT, q));
+  // the reduction and the hot-row updates once both forwards have read the hot rows
+  HL_TRY(pl_wt(p, g, PF_FWDHOT, q));
   if (io->dY)
     HL_TRY(hl_embbag_bwd_apply_part(h, io->w_hot, io->staging, cap, B, bps, L, io->dY, io->lr, 1, io->workspace,
                                     io->ws_bytes, G));
-  HL_HIPTRY(hipEventRecord(p->ev_group, g));
-  HL_HIPTRY(hipStreamWaitEvent(m, p->ev_fetch, 0));
+  HL_TRY(pl_sig(p, g, PF_GROUP, q));
+  // the staging rows: cold half of the non-popular forward, then their updates
+  HL_TRY(pl_wt(p, m, PF_FETCH, q));
   HL_TRY(hl_embbag_fwd_part(h, io->w_hot, io->staging, cap, io->codes, io->bag_ptr, B, bps, L, io->nonpop_ids,
                             io->counts + 1, B, io->out, 2, M));
-  HL_HIPTRY(hipStreamWaitEvent(m, p->ev_group, 0));
+  HL_TRY(pl_wt(p, m, PF_GROUP, q));
   if (io->dY)
     HL_TRY(hl_embbag_bwd_apply_part(h, io->w_hot, io->staging, cap, B, bps, L, io->dY, io->lr, 2, io->workspace,
                                     io->ws_bytes, M));
+  HL_TRY(pl_sig(p, m, PF_DONE, q));
   if (io->write_back) {
-    HL_HIPTRY(hipEventRecord(p->ev_apply, m));
-    HL_HIPTRY(hipStreamWaitEvent(f, p->ev_apply, 0));
+    HL_TRY(pl_wt(p, f, PF_DONE, q));
     HL_TRY(hl_cold_scatter(h, io->cold_ids, io->n_cold, cap, io->staging, const_cast<void*>(io->w_host), F));
     if (slot < 0) {
       slot = p->wb_next;
       p->wb_next ^= 1;
     }
     p->wb_ids[slot] = io->cold_ids;
-    HL_HIPTRY(hipEventRecord(p->ev_wb[slot], f));
+    p->wb_seq[slot] = q;
+    HL_TRY(pl_sig(p, f, PF_WB + slot, q));
   }
   HL_HIPTRY(hipEventRecord(p->ev_out, m));
   if (tie) HL_HIPTRY(hipStreamWaitEvent(caller, p->ev_out, 0));
@@ -146,8 +313,8 @@ extern "C" hl_status hl_pipeline_step(hl_pipeline* p, const hl_step_io* io, hl_s
 
 extern "C" hl_status hl_pipeline_sync_writeback(hl_pipeline* p, hl_stream stream) {
   if (!p) return HL_ERR_INVALID_ARG;
-  HL_HIPTRY(hipStreamWaitEvent((hipStream_t)stream, p->ev_wb[0], 0));
-  HL_HIPTRY(hipStreamWaitEvent((hipStream_t)stream, p->ev_wb[1], 0));
+  HL_HIPTRY(hipStreamWaitEvent((hipStream_t)stream, p->ev[PF_WB], 0));
+  HL_HIPTRY(hipStreamWaitEvent((hipStream_t)stream, p->ev[PF_WB + 1], 0));
   return HL_OK;
 }
 
@@ -162,5 +329,6 @@ extern "C" hl_status hl_pipeline_streams(const hl_pipeline* p, hl_stream* main, 
 extern "C" hl_status hl_pipeline_sync(hl_pipeline* p, hl_stream stream) {
   if (!p) return HL_ERR_INVALID_ARG;
   HL_HIPTRY(hipStreamWaitEvent((hipStream_t)stream, p->ev_out, 0));
+  HL_HIPTRY(hipStreamWaitEvent((hipStream_t)stream, p->ev_plan, 0));
   return hl_pipeline_sync_writeback(p, stream);
 }

@@ -40,6 +40,7 @@ class StepIO(C.Structure):
 
 
 HL_STEP_UNTIED = 1
+HL_STEP_PLANNED = 2
 _SIGS = {
     "hl_status_string": (C.c_char_p, [C.c_int]),
     "hl_create": (C.c_int, [C.POINTER(P), I32, P, I32, C.c_int, U32]),
@@ -80,6 +81,7 @@ _SIGS = {
     "hl_pipeline_create": (C.c_int, [P, I32, C.POINTER(P)]),
     "hl_pipeline_destroy": (C.c_int, [P]),
     "hl_pipeline_step": (C.c_int, [P, C.POINTER(StepIO), P]),
+    "hl_pipeline_plan": (C.c_int, [P, C.POINTER(StepIO), P]),
     "hl_pipeline_sync_writeback": (C.c_int, [P, P]),
     "hl_pipeline_sync": (C.c_int, [P, P]),
     "hl_pipeline_streams": (C.c_int, [P, C.POINTER(P), C.POINTER(P), C.POINTER(P)]),
@@ -359,6 +361,10 @@ def hl_pipeline_destroy(p):
 
 def hl_pipeline_step(p, io: StepIO, stream=None):
     _ck("hl_pipeline_step", lib().hl_pipeline_step(p, C.byref(io), _s(stream)))
+
+
+def hl_pipeline_plan(p, io: StepIO, stream=None):
+    _ck("hl_pipeline_plan", lib().hl_pipeline_plan(p, C.byref(io), _s(stream)))
 
 
 def hl_pipeline_sync_writeback(p, stream=None):

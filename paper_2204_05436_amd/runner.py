@@ -24,6 +24,8 @@ from __future__ import annotations
 
 from dataclasses import dataclass
 
+from types import SimpleNamespace
+
 import numpy as np
 import torch
 
@@ -71,7 +73,6 @@ class HotPath:
         self.max_samples = int(max_samples)
         max_bags = self.max_samples * w.bags_per_sample
         wsb = hl.hl_workspace_bytes(self.h, self.max_lookups, max_bags, self.max_samples)
-        self.ws = torch.zeros(wsb, dtype=torch.uint8, device=device)
         sdt = torch.float32 if w.dtype == "f32" else torch.int16
         self.sdt = sdt
         self.w_hot = torch.zeros((self.k_cap, w.dim), dtype=sdt, device=device)
@@ -80,16 +81,22 @@ class HotPath:
         self.hot_ids = torch.zeros(max(1, min(self.k_cap, n_rows)), dtype=torch.int32, device=device)
         L, B = max(1, self.max_lookups), max(1, self.max_samples)
         i32 = dict(dtype=torch.int32, device=device)
-        self.gids = torch.zeros(L, **i32)
-        self.codes = torch.zeros(L, **i32)
-        self.flags = torch.zeros(B, dtype=torch.uint8, device=device)
-        self.pop = torch.zeros(B, **i32)
-        self.nonpop = torch.zeros(B, **i32)
-        self.counts = torch.zeros(2, **i32)
-        self._cold = [torch.zeros(self.staging_cap, **i32) for _ in range(2)]
-        self._ncold = [torch.zeros(1, **i32) for _ in range(2)]
+
+        def bufs():
+            return SimpleNamespace(
+                gids=torch.zeros(L, **i32), codes=torch.zeros(L, **i32),
+                flags=torch.zeros(B, dtype=torch.uint8, device=device), pop=torch.zeros(B, **i32),
+                nonpop=torch.zeros(B, **i32), counts=torch.zeros(2, **i32),
+                cold_ids=torch.zeros(self.staging_cap, **i32), n_cold=torch.zeros(1, **i32),
+                ws=torch.zeros(wsb, dtype=torch.uint8, device=device))
+
+        # two sets of per-step buffers, alternated between steps: a write-back
+        # still reading one step's cold list, or a look-ahead plan of the next
+        # mini-batch, uses the other set
+        self._sets = [bufs(), bufs()]
         self._par = 0
-        self.cold_ids, self.n_cold = self._cold[0], self._ncold[0]
+        self._use(0)
+        self._pending = []  # look-ahead plans: (batch, set)
         self.writeback = bool(writeback)
         hl.hl_cold_reserve(self.h, self.max_lookups)  # no allocation inside a captured step
         # the native pipeline (its own streams; the host-link copy on compute units
@@ -106,6 +113,46 @@ class HotPath:
         self.ev_wb = [ev(), ev()]
         self.out = torch.zeros((max(1, max_bags), w.dim), dtype=torch.float32, device=device)
         self.n_hot = 0
+
+    def _use(self, p):
+        """The public per-step buffers (gids, codes, ..., ws) are set p's."""
+        for k, v in vars(self._sets[p]).items():
+            setattr(self, k, v)
+
+    def _next_set(self):
+        if self._pending:
+            raise RuntimeError("a look-ahead plan is pending: step that batch first")
+        p = self._par
+        self._par ^= 1
+        self._use(p)
+        return p
+
+    def _fill_io(self, io, b, s, lr, flags):
+        io.rows, io.bag_ptr, io.n_samples, io.bags_per_sample, io.n_lookups = (
+            b.rows.data_ptr(), b.bag_ptr.data_ptr(), b.n_samples, b.bps, b.n_lookups)
+        io.dY, io.lr = (b.dY.data_ptr() if b.dY is not None else None), float(lr)
+        io.gids, io.codes, io.flags = s.gids.data_ptr(), s.codes.data_ptr(), s.flags.data_ptr()
+        io.pop_ids, io.nonpop_ids, io.counts = s.pop.data_ptr(), s.nonpop.data_ptr(), s.counts.data_ptr()
+        io.cold_ids, io.n_cold = s.cold_ids.data_ptr(), s.n_cold.data_ptr()
+        io.w_host, io.w_hot, io.staging, io.staging_cap = (
+            self.table.dev, self.w_hot.data_ptr(), self.staging.data_ptr(), self.staging_cap)
+        io.out, io.workspace, io.ws_bytes = self.out.data_ptr(), s.ws.data_ptr(), s.ws.numel()
+        io.write_back = int(self.writeback)
+        io.step_flags = flags
+        return io
+
+    def plan(self, b: DevBatch, untied=False):
+        """Look-ahead segregation of batch b (hl_pipeline_plan): its dispatch and
+        cold plan run on the pipeline's plan stream while the steps enqueued
+        before it train; the step of b (the next pipelined step) skips them.
+        At most one plan ahead of the next step."""
+        if len(self._pending) >= 2:
+            raise RuntimeError("two look-ahead plans are already pending")
+        p = self._par
+        self._par ^= 1
+        io = self._fill_io(hl.StepIO(), b, self._sets[p], 0.0, hl.HL_STEP_UNTIED if untied else 0)
+        hl.hl_pipeline_plan(self.pipe, io, torch.cuda.current_stream(self.device))
+        self._pending.append((b, p))
 
     # ------------------------------------------------------------------ learning phase
     def learn(self, prof_batches, k: int | None = None, reset=True):
@@ -125,14 +172,16 @@ class HotPath:
 
     # ------------------------------------------------------------------ one mini-batch
     def step(self, b: DevBatch, lr: float | None = None, events=None, mode: str = "pipelined", split_fwd=True,
-             untied=False):
+             untied=False, next: DevBatch | None = None):
         """classify -> partition -> remap -> cold gather (non-popular) -> forward of
         both mu-batches -> one coalesced SGD step [-> write-back of the cold rows].
 
         mode "pipelined": the three-stream schedule of the module docstring,
           enqueued by the native pipeline (hl_pipeline_step).  untied: no
           ordering with the current stream (inputs already resident; call
-          sync() before using the results).
+          sync() before using the results).  next: the following batch,
+          whose dispatch and cold plan are then enqueued ahead (plan()) to
+          run while this step trains; its own step finds them done.
         mode "sequential": the fused calls in order on the current stream;
           `events`: optional list of len(STAGES)+1 torch.cuda.Event recorded
           around the stages.
@@ -142,28 +191,30 @@ class HotPath:
             raise ValueError(mode)
         lr = self.w.lr if lr is None else lr
         B, bps, L = b.n_samples, b.bps, b.n_lookups
+        if next is not None and mode != "pipelined":
+            raise ValueError("look-ahead needs the native pipelined step")
         if mode == "sequential":
             return self._step_sequential(b, lr, events, split_fwd)
         caller = torch.cuda.current_stream(self.device)
         capturing = torch.cuda.is_current_stream_capturing()
         if mode == "fwdbwd" or capturing:  # the Python rendering of the schedule (a graph keeps no CU mask)
+            if next is not None:
+                raise ValueError("no look-ahead under capture")
             return self._step_pipelined(b, lr, events, mode, caller, capturing)
-        p = self._par
-        self._par ^= 1
-        self.cold_ids, self.n_cold = self._cold[p], self._ncold[p]
-        io = self.io
-        io.rows, io.bag_ptr, io.n_samples, io.bags_per_sample, io.n_lookups = (
-            b.rows.data_ptr(), b.bag_ptr.data_ptr(), B, bps, L)
-        io.dY, io.lr = (b.dY.data_ptr() if b.dY is not None else None), float(lr)
-        io.gids, io.codes, io.flags = self.gids.data_ptr(), self.codes.data_ptr(), self.flags.data_ptr()
-        io.pop_ids, io.nonpop_ids, io.counts = self.pop.data_ptr(), self.nonpop.data_ptr(), self.counts.data_ptr()
-        io.cold_ids, io.n_cold = self.cold_ids.data_ptr(), self.n_cold.data_ptr()
-        io.w_host, io.w_hot, io.staging, io.staging_cap = (
-            self.table.dev, self.w_hot.data_ptr(), self.staging.data_ptr(), self.staging_cap)
-        io.out, io.workspace, io.ws_bytes = self.out.data_ptr(), self.ws.data_ptr(), self.ws.numel()
-        io.write_back = int(self.writeback)
-        io.step_flags = hl.HL_STEP_UNTIED if untied else 0
-        hl.hl_pipeline_step(self.pipe, io, caller)
+        flags = hl.HL_STEP_UNTIED if untied else 0
+        if next is not None and not self._pending:
+            self.plan(b, untied)
+        if self._pending:
+            if self._pending[0][0] is not b:
+                raise RuntimeError("steps must take the batches in the order they were planned")
+            if next is not None:
+                self.plan(next, untied)
+            _, p = self._pending.pop(0)
+            self._use(p)
+            flags |= hl.HL_STEP_PLANNED
+        else:
+            p = self._next_set()
+        hl.hl_pipeline_step(self.pipe, self._fill_io(self.io, b, self._sets[p], lr, flags), caller)
 
     def sync(self, stream=None):
         """The stream (default: current) waits for every step enqueued so far."""
@@ -172,10 +223,8 @@ class HotPath:
     def _step_pipelined(self, b, lr, events, mode, main, capturing):
         h, w = self.h, self.w
         B, bps, L = b.n_samples, b.bps, b.n_lookups
-        p = self._par
-        self._par ^= 1
-        cold, ncold = self._cold[p], self._ncold[p]
-        self.cold_ids, self.n_cold = cold, ncold
+        p = self._next_set()
+        cold, ncold = self.cold_ids, self.n_cold
         hl.hl_dispatch(h, b.rows, b.bag_ptr, B, bps, L, self.gids, self.codes, self.flags, self.pop, self.nonpop,
                        self.counts, self.ws)
         if self.writeback and not capturing:
@@ -233,19 +282,18 @@ class HotPath:
         of the schedule, on unmasked streams): replaying it runs the whole step
         (all three streams, joined) with one launch.  Run one eager
         step of at least this size first (the cold plan's hash table is
-        allocated on first use).  Returns (graph, cold_ids, n_cold): the
-        buffers the graph's cold plan writes."""
+        allocated on first use).  Returns (graph, bufs): bufs holds the
+        per-step buffers the graph writes (gids, codes, flags, pop, nonpop,
+        counts, cold_ids, n_cold, ws); later eager steps alternate sets."""
         g = torch.cuda.CUDAGraph()
         with torch.cuda.graph(g):
             self.step(b, lr=lr, mode="pipelined")
-        return g, self.cold_ids, self.n_cold
+        return g, next(s for s in self._sets if s.codes is self.codes)
 
     def _step_sequential(self, b, lr, events, split_fwd):
         B, bps, L = b.n_samples, b.bps, b.n_lookups
         ev = events
-        p = self._par
-        self._par ^= 1
-        self.cold_ids, self.n_cold = self._cold[p], self._ncold[p]
+        p = self._next_set()
         main = torch.cuda.current_stream(self.device)
         if self.writeback:
             main.wait_event(self.ev_wb[p])

@@ -462,12 +462,12 @@ def test_graph_replay(name, writeback):
         torch.cuda.synchronize()
         w0, tab0 = hp.w_hot.clone(), table.array.copy()
 
-        def state():
+        def state(bufs):
             torch.cuda.synchronize()
-            n = int(hp.n_cold.item())
+            n = int(bufs.n_cold.item())
             return dict(out=hp.out[:mba.n_bags].cpu().numpy().copy(), w_hot=hp.w_hot[:hp.n_hot].cpu().numpy().copy(),
-                        stg=hp.staging[:n].cpu().numpy().copy(), cold=hp.cold_ids[:n].cpu().numpy().copy(),
-                        codes=hp.codes[:mba.n_lookups].cpu().numpy().copy(), tab=table.array.copy())
+                        stg=hp.staging[:n].cpu().numpy().copy(), cold=bufs.cold_ids[:n].cpu().numpy().copy(),
+                        codes=bufs.codes[:mba.n_lookups].cpu().numpy().copy(), tab=table.array.copy())
 
         def reset():
             torch.cuda.synchronize()
@@ -476,16 +476,15 @@ def test_graph_replay(name, writeback):
             torch.cuda.synchronize()
 
         hp.step(da)
-        ref = state()
+        ref = state(hp)
         assert hp.device_error() == 0
         reset()
-        g, cold, ncold = hp.capture(da)
+        g, bufs = hp.capture(da)
         for rep in range(3):
             reset()
             g.replay()
             torch.cuda.synchronize()
-            hp.cold_ids, hp.n_cold = cold, ncold
-            got = state()
+            got = state(bufs)
             assert hp.device_error() == 0, f"replay {rep}"
             for k in ref:
                 assert np.array_equal(got[k].view(np.uint8), ref[k].view(np.uint8)), f"replay {rep}: {k} differs"
@@ -497,7 +496,8 @@ def test_graph_replay(name, writeback):
         table.close()
 
 
-@pytest.mark.parametrize("mode,writeback", [("pipelined", True), ("pipelined", False), ("sequential", True)])
+@pytest.mark.parametrize("mode,writeback", [("pipelined", True), ("pipelined", False), ("sequential", True),
+                                           ("lookahead", True), ("lookahead", False)])
 @pytest.mark.parametrize("name", ["dlrm-large", "multi-hot", "tbsm"])
 def test_multi_step(name, mode, writeback):
     """Several consecutive steps with one workspace and one hot cache (the hot
@@ -506,7 +506,8 @@ def test_multi_step(name, mode, writeback):
     write-back its host table, take the GPU's after each comparison), to the
     single-step tolerances.  With write-back, the host table after a step holds
     the step's updated staging rows bit for bit at the cold ids and is unchanged
-    elsewhere."""
+    elsewhere.  "lookahead": each step also plans the next batch, whose
+    dispatch and cold plan run on the plan stream while the step trains."""
     import oracle as O
     from parity_lib import check_close
     w = configs.scaled(configs.WORKLOADS[name], batch=600, row_scale=0.004, name=name + "-steps")
@@ -526,13 +527,18 @@ def test_multi_step(name, mode, writeback):
         hot = O.topk(counts, k_cap)
         assert np.array_equal(hp.hot_ids[:hp.n_hot].cpu().numpy().view(np.uint32), hot)
         w_hot = O.gather(table.array, hot)
+        dYs = [W.make_dy(w, 4 + si, mb.n_bags) for si, mb in enumerate(steps)]
+        dbs = [to_device(mb, "cuda", dY) for mb, dY in zip(steps, dYs)]
         for si, mb in enumerate(steps):
             pre = hp.w_hot[:len(hot)].cpu().numpy().copy()
             assert si > 0 or np.array_equal(pre.view(np.uint8), w_hot.view(np.uint8))
             w_hot = pre.copy()
             tab_pre = table.array.copy()
-            dY = W.make_dy(w, 4 + si, mb.n_bags)
-            hp.step(to_device(mb, "cuda", dY), mode=mode)
+            dY = dYs[si]
+            if mode == "lookahead":
+                hp.step(dbs[si], next=dbs[si + 1] if si + 1 < len(dbs) else None)
+            else:
+                hp.step(dbs[si], mode=mode)
             torch.cuda.synchronize()
             assert hp.device_error() == 0, f"step {si}"
             B, bps, L = mb.n_samples, mb.bags_per_sample, mb.n_lookups
@@ -569,3 +575,69 @@ def test_multi_step(name, mode, writeback):
     finally:
         hp.close()
         table.close()
+
+
+@pytest.mark.parametrize("writeback", [False, True])
+@pytest.mark.parametrize("name", ["dlrm-large", "multi-hot"])
+def test_lookahead_chain(name, writeback):
+    """Six untied back-to-back steps, each planning the next batch ahead, with
+    one sync at the end: the hot cache (and with write-back the host table) ends
+    bit for bit where six plain pipelined steps leave it, and within the
+    single-step tolerance, compounded, of the oracle's six steps in order."""
+    import oracle as O
+    from parity_lib import check_close
+    w = configs.scaled(configs.WORKLOADS[name], batch=700, row_scale=0.004, name=name + "-chain")
+    rows = W.table_rows(w)
+    n_rows = int(rows.sum())
+    k_cap = w.k_cap(n_rows)
+    prof = [W.make_batch(w, rows, i) for i in range(4)]
+    steps = [W.make_batch(w, rows, 4 + s) for s in range(6)]
+    dYs = [W.make_dy(w, 4 + si, mb.n_bags) for si, mb in enumerate(steps)]
+    finals = {}
+    for variant in ("plain", "lookahead"):
+        table = make_table(w, n_rows)
+        hp = HotPath(w, rows, table, max(b.n_lookups for b in prof + steps), w.batch, writeback=writeback)
+        try:
+            hp.learn([to_device(p, "cuda") for p in prof])
+            hot = hp.hot_ids[:hp.n_hot].cpu().numpy().view(np.uint32).copy()
+            w0 = hp.w_hot[:len(hot)].cpu().numpy().copy()
+            tab0 = table.array.copy()
+            dbs = [to_device(mb, "cuda", dY) for mb, dY in zip(steps, dYs)]
+            side = torch.cuda.Stream()
+            side.wait_stream(torch.cuda.current_stream())
+            with torch.cuda.stream(side):
+                for si in range(len(dbs)):
+                    if variant == "plain":
+                        hp.step(dbs[si], untied=True)
+                    else:
+                        hp.step(dbs[si], untied=True, next=dbs[si + 1] if si + 1 < len(dbs) else None)
+                hp.sync()
+            torch.cuda.synchronize()
+            assert hp.device_error() == 0, variant
+            finals[variant] = (hp.w_hot[:len(hot)].cpu().numpy().copy(), table.array.copy())
+        finally:
+            hp.close()
+            table.close()
+    assert np.array_equal(finals["plain"][0].view(np.uint8), finals["lookahead"][0].view(np.uint8)), "hot cache"
+    assert np.array_equal(finals["plain"][1].view(np.uint8), finals["lookahead"][1].view(np.uint8)), "host table"
+    # the oracle's six steps in order, updating its hot cache and staging rows in
+    # place (a step's staging rows are dropped after it unless written back)
+    w_hot, tab = np.ascontiguousarray(w0.copy()), tab0.copy()
+    B, bps = w.batch, w.bags_per_sample
+    for mb, dY in zip(steps, dYs):
+        g, _ = O.gids(rows, mb.rows, mb.bag_ptr)
+        flags = O.classify(hot, g, mb.bag_ptr, B, bps)
+        _, nonpop = O.partition(flags)
+        cold, codes = O.cold_plan(g, O.remap(hot, g), mb.bag_ptr, nonpop, len(nonpop), bps, k_cap)
+        stg = np.ascontiguousarray(O.gather(tab, cold))
+        _, _, rc = O.embbag_bwd_sgd(w.dtype, w_hot, k_cap, stg, codes, mb.bag_ptr, None, B, bps, dY, w.lr)
+        assert rc == 0
+        if writeback:
+            O.scatter(tab, cold, stg)
+    rtol = {"f32": 1e-5, "bf16": 1e-2}[w.dtype] * len(steps)
+    got = finals["lookahead"][0]
+    scale = np.maximum(np.abs(as_f64(w0, w.dtype)), 1e-3)
+    check_close(as_f64(got, w.dtype), as_f64(w_hot, w.dtype), scale, rtol, "hot cache after the chain")
+    if writeback:
+        check_close(as_f64(finals["lookahead"][1], w.dtype), as_f64(tab, w.dtype),
+                    np.maximum(np.abs(as_f64(tab0, w.dtype)), 1e-3), rtol, "host table after the chain")
