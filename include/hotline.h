@@ -57,6 +57,7 @@ typedef enum {
 #define HL_DEVERR_BAD_HOTSET 0x8u   /* hl_set_hot: ids not strictly ascending or >= n_rows */
 #define HL_DEVERR_STALL 0x10u       /* a cross-block wait hit its spin limit (never expected) */
 #define HL_DEVERR_SHAPE 0x20u       /* bag_ptr[n_bags] differs from the n_lookups passed */
+#define HL_DEVERR_INTERNAL 0x40u    /* an internal bound check failed (never expected); the write was skipped */
 
 typedef enum { HL_F32 = 0, HL_BF16 = 1 } hl_dtype;
 
@@ -324,10 +325,11 @@ hl_status hl_stream_destroy(hl_stream stream);
  * pipeline's own: the host-link copy on compute units [0, fetch_cus) (0 = no
  * restriction), everything else on the other units.  The step runs
  * hl_dispatch, hl_cold_plan (no sample list: a cold lookup makes its sample
- * non-popular), hl_cold_fetch beside hl_embbag_fwd_part 0 of the popular and
- * part 1 of the non-popular mu-batch, hl_embbag_bwd_plan and apply part 1 on a
- * third stream, then part 2 of both (and with write_back, hl_cold_scatter
- * after the updates).  It is ordered after the work already on `stream`, and
+ * non-popular), hl_cold_fetch beside hl_embbag_fwd_part 1 over every sample
+ * (the popular mu-batch's forward and the non-popular one's hot half in one
+ * launch: the same sums), hl_embbag_bwd_plan and apply part 1 on a third
+ * stream, then part 2 of the forward over the non-popular mu-batch and of the
+ * apply (and with write_back, hl_cold_scatter after the updates).  It is ordered after the work already on `stream`, and
  * `stream` waits for it (the write-back excepted: it is ordered before the
  * next step's fetch and before any later step's plan that rewrites the same
  * cold_ids, so callers that write back may alternate two cold_ids / n_cold
@@ -379,18 +381,20 @@ hl_status hl_pipeline_destroy(hl_pipeline* p);
 hl_status hl_pipeline_step(hl_pipeline* p, const hl_step_io* io, hl_stream stream);
 /* Look-ahead segregation (Sec. IV and the pipeline figure: the accelerator
  * classifies and segregates a mini-batch while the GPUs train the one before):
- * enqueues hl_dispatch and hl_cold_plan of io's mini-batch on a fourth stream
- * of the pipeline, to be consumed by a later hl_pipeline_step with
- * HL_STEP_PLANNED and the same io.  The plan waits for every step enqueued
- * before it (it rewrites per-step buffers and the workspace, and shares the
- * cold-gather hash table with them) and for the write-back that last read its
- * cold_ids, so one step ahead needs two sets of per-step buffers, alternated;
- * the step's row fetch still waits for the previous step to end.  dY, lr,
- * w_host, w_hot, staging, out and write_back are not read.  HL_STEP_UNTIED in
- * io->step_flags: no wait for `stream` first.  HL_ERR_INVALID_ARG: a plan on
- * the same workspace is still pending, or four plans are; HL_ERR_UNSUPPORTED:
- * a pipeline without compute-unit masks (fetch_cus = 0), whose streams may
- * share hardware queues, or `stream` under capture. */
+ * enqueues hl_dispatch, hl_cold_plan and, when io->dY is not NULL,
+ * hl_embbag_bwd_plan of io's mini-batch on a fourth stream of the pipeline, to
+ * be consumed by a later hl_pipeline_step with HL_STEP_PLANNED and the same io
+ * (dY NULL or not alike).  The plan waits for every step enqueued before it
+ * (it rewrites per-step buffers and the workspace, and shares the cold-gather
+ * hash table with them) and for the write-back that last read its cold_ids, so
+ * one step ahead needs two sets of per-step buffers, alternated; the planned
+ * step's row fetch still waits for the previous step to end, and its forwards
+ * and backward run on one stream.  lr, w_host, w_hot, staging, out and
+ * write_back are not read.  HL_STEP_UNTIED in io->step_flags: no wait for
+ * `stream` first.  HL_ERR_INVALID_ARG: a plan on the same workspace is still
+ * pending, or four plans are; HL_ERR_UNSUPPORTED: a pipeline without
+ * compute-unit masks (fetch_cus = 0), whose streams may share hardware queues,
+ * or `stream` under capture. */
 hl_status hl_pipeline_plan(hl_pipeline* p, const hl_step_io* io, hl_stream stream);
 hl_status hl_pipeline_sync_writeback(hl_pipeline* p, hl_stream stream);
 /* `stream` waits for every step and plan enqueued so far (and the write-backs). */

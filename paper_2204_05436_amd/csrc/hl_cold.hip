@@ -120,7 +120,7 @@ cg_insert(const uint32_t* __restrict__ gids, const int32_t* __restrict__ codes, 
           uint64_t* table, cg_ws ws, uint32_t* err) {
   __shared__ int32_t off[CG_BAGS + 1];
   __shared__ uint32_t cl[CG_IR], cg_[CG_IR];
-  __shared__ uint32_t wn[4], s_total;
+  __shared__ uint32_t wn[4];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int64_t b0 = (int64_t)blockIdx.x * CG_BAGS;
   const int nb = (int)min((int64_t)CG_BAGS, n_bags - b0);

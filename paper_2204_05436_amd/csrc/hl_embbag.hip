@@ -308,6 +308,7 @@ struct bw_ws {
   uint32_t* tflag;   // [tiles]
   uint32_t* tkey;    // [tiles]
   float* gc;         // [n_max][D] gradient sums of staging rows, kept between the two halves of the apply
+  uint32_t* bnd;     // [1] first sorted position whose key is not a hot slot (set by the first half)
   uint32_t tiles, gc_rows;
 };
 
@@ -331,6 +332,7 @@ static void bw_carve(hl_carver& c, bw_ws& ws, uint32_t n_max, int64_t max_bags, 
   ws.tkey = c.take<uint32_t>(ws.tiles);
   ws.gc_rows = n_max;
   ws.gc = c.take<float>((size_t)n_max * D);
+  ws.bnd = c.take<uint32_t>(1);
 }
 
 size_t hl_bwd_ws_bytes(const hl_handle* h, int64_t max_lookups, int64_t max_bags) {
@@ -415,7 +417,7 @@ __global__ void __launch_bounds__(RB_BLOCK)
 bw_reduce1(const uint32_t* __restrict__ keys, const uint32_t* __restrict__ vals, uint32_t n,
            const float* __restrict__ dY, eb_geom g, void* w_hot, void* stg, uint32_t n_hot, float lr,
            float* __restrict__ tfirst, float* __restrict__ tlast, uint32_t* __restrict__ tflag,
-           uint32_t* __restrict__ tkey, float* __restrict__ gc, uint32_t gc_rows) {
+           uint32_t* __restrict__ tkey, float* __restrict__ gc, uint32_t gc_rows, uint32_t* __restrict__ bnd) {
   typedef typename RowIO<VEC, BF>::T T;
   __shared__ float pf[RB_WAVES * 64 * VEC], pl[RB_WAVES * 64 * VEC];
   __shared__ uint32_t gflag[RB_WAVES * 64], gkey[RB_WAVES * 64];
@@ -444,6 +446,16 @@ bw_reduce1(const uint32_t* __restrict__ keys, const uint32_t* __restrict__ vals,
     }
     const uint32_t prevk = (e0 > 0 && e0 - 1 < n) ? keys[e0 - 1] : EB_SENT;
     const uint32_t nextk = (e0 + RB_E < n) ? keys[e0 + RB_E] : EB_SENT;
+    if (SPLIT && blockIdx.y == 0 && gl == 0) {
+      // the one position where the hot slots end (keys are sorted; n if they never do)
+#pragma unroll
+      for (int j = 0; j < RB_E; ++j) {
+        const uint64_t idx = e0 + j;
+        const uint32_t kp = j == 0 ? (e0 > 0 ? prevk : 0u) : kk[j - 1];
+        if (idx < n && kk[j] >= n_hot && (idx == 0 || kp < n_hot)) *bnd = (uint32_t)idx;
+        if (idx + 1 == n && kk[j] < n_hot) *bnd = (uint32_t)n;
+      }
+    }
     const bool cprev = kk[0] != EB_SENT && prevk == kk[0];
     const bool cnext = kk[RB_E - 1] != EB_SENT && nextk == kk[RB_E - 1];
     // gradient rows
@@ -646,19 +658,21 @@ bw_reduce2(uint32_t n_tiles, eb_geom g, void* w_hot, void* stg, uint32_t n_hot, 
 
 // The deferred staging-row updates: every run end in the sorted keys whose key
 // is a staging row below gc_rows applies row <- round(row - lr * gc[u]), the
-// same arithmetic as the one-pass update.  A wave tests 64 positions, then its
-// row groups take the run ends it found, a group per row.
+// same arithmetic as the one-pass update.  Only the sorted tail from *bnd (the
+// end of the hot slots, found by the first half) is scanned.  A wave tests 64
+// positions, then its row groups take the run ends it found, a group per row.
 template <int VEC, bool BF>
 __global__ void __launch_bounds__(256)
 bw_cold(const uint32_t* __restrict__ keys, uint32_t n, eb_geom g, void* stg, uint32_t n_hot, float lr,
-        const float* __restrict__ gc, uint32_t gc_rows) {
+        const float* __restrict__ gc, uint32_t gc_rows, const uint32_t* __restrict__ bnd) {
   typedef typename RowIO<VEC, BF>::T T;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int gi = lane / g.G, gl = lane - gi * g.G;
   const int32_t colv = blockIdx.y * 64 + gl;
   const bool cact = gi < g.NG && colv < g.vpr;
   const int64_t col = (int64_t)colv * VEC;
-  for (uint64_t base = ((uint64_t)blockIdx.x * 4 + w) * 64; base < n; base += (uint64_t)gridDim.x * 256) {
+  const uint32_t b0 = min(*bnd, n);
+  for (uint64_t base = b0 + ((uint64_t)blockIdx.x * 4 + w) * 64; base < n; base += (uint64_t)gridDim.x * 256) {
     const uint64_t p = base + lane;
     const uint32_t k = p < n ? keys[p] : EB_SENT;
     const uint32_t kn = p + 1 < n ? keys[p + 1] : EB_SENT;
@@ -759,19 +773,21 @@ static void launch_bwd(const hl_handle* h, uint32_t tiles, hipStream_t s, const 
   const dim3 grid(tiles, g.cchunks);
   if (part == 0) {
     HL_KERNEL(h, s, "bw_reduce1", (bw_reduce1<VEC, BF, false>), grid, dim3(RB_BLOCK), 0, s, sk, sv, n, dY, g, w_hot,
-              stg, n_hot, lr, ws.tfirst, ws.tlast, ws.tflag, ws.tkey, ws.gc, ws.gc_rows);
+              stg, n_hot, lr, ws.tfirst, ws.tlast, ws.tflag, ws.tkey, ws.gc, ws.gc_rows, ws.bnd);
     HL_KERNEL(h, s, "bw_reduce2", (bw_reduce2<VEC, BF, false>), grid, dim3(RB_BLOCK), 0, s, tiles, g, w_hot, stg,
               n_hot, lr, ws.tfirst, ws.tlast, ws.tflag, ws.tkey, ws.gc, ws.gc_rows);
   } else if (part == 1) {
     HL_KERNEL(h, s, "bw_reduce1", (bw_reduce1<VEC, BF, true>), grid, dim3(RB_BLOCK), 0, s, sk, sv, n, dY, g, w_hot,
-              stg, n_hot, lr, ws.tfirst, ws.tlast, ws.tflag, ws.tkey, ws.gc, ws.gc_rows);
+              stg, n_hot, lr, ws.tfirst, ws.tlast, ws.tflag, ws.tkey, ws.gc, ws.gc_rows, ws.bnd);
     HL_KERNEL(h, s, "bw_reduce2", (bw_reduce2<VEC, BF, true>), grid, dim3(RB_BLOCK), 0, s, tiles, g, w_hot, stg,
               n_hot, lr, ws.tfirst, ws.tlast, ws.tflag, ws.tkey, ws.gc, ws.gc_rows);
   } else {
+    // the tail (cold lookups: about a tenth of a mini-batch here) is short; a
+    // small grid strides over it
     uint32_t b = hl_div_up(n, 256);
-    if (b > 4096) b = 4096;
+    if (b > 128) b = 128;
     HL_KERNEL(h, s, "bw_cold", (bw_cold<VEC, BF>), dim3(b, g.cchunks), dim3(256), 0, s, sk, n, g, stg, n_hot, lr,
-              ws.gc, ws.gc_rows);
+              ws.gc, ws.gc_rows, ws.bnd);
   }
 }
 
@@ -818,12 +834,12 @@ extern "C" hl_status hl_embbag_bwd_apply_part(hl_handle* h, void* w_hot, void* s
   if (!h || n_samples < 0 || bps < 1 || n_lookups < 0 || stg_rows < 0 || !workspace) return HL_ERR_INVALID_ARG;
   if (part < 0 || part > 2) return HL_ERR_INVALID_ARG;
   const int64_t n_bags = (int64_t)n_samples * bps;
-  if (h->ws_last != workspace || h->ws_kind != HL_WSK_BWD_PLAN || h->ws_n != n_lookups || h->ws_bags != n_bags ||
-      h->ws_stg != stg_rows)
+  hl_ws_rec* rec = hl_ws_find(h, workspace);
+  if (!rec || rec->n != n_lookups || rec->bags != n_bags || rec->stg != stg_rows)
     return HL_ERR_INVALID_ARG;  // no matching plan is held by this workspace
-  if (part == 2 && !h->ws_part1) return HL_ERR_INVALID_ARG;  // the first half has not run on this plan
+  if (part == 2 && !rec->part1) return HL_ERR_INVALID_ARG;  // the first half has not run on this plan
   if (n_lookups == 0 || n_samples == 0) {
-    if (part == 1) h->ws_part1 = 1;
+    if (part == 1) rec->part1 = 1;
     return HL_OK;
   }
   if ((part != 2 && (!dY || (h->n_hot && !w_hot))) || (stg_rows && !staging)) return HL_ERR_INVALID_ARG;
@@ -848,7 +864,7 @@ extern "C" hl_status hl_embbag_bwd_apply_part(hl_handle* h, void* w_hot, void* s
   else { if (bf) BWD(1, true); else BWD(1, false); }
 #undef BWD
   HL_LAUNCHED();
-  if (part == 1) h->ws_part1 = 1;
+  if (part == 1) rec->part1 = 1;
   return HL_OK;
 }
 

@@ -124,7 +124,6 @@ extern "C" hl_status hl_create(hl_handle** out, int32_t n_tables, const uint32_t
   h->dtype = dtype;
   h->k_cap = k_cap;
   h->row_bytes = (uint32_t)dim * (dtype == HL_F32 ? 4u : 2u);
-  h->epoch = 1;
   h->n_tiles4k = (total + 4095) / 4096;
   h->tk_bytes = hl_topk_scratch_bytes(total);
   h->trace = new hl_trace();

@@ -28,6 +28,13 @@ void hl_trace_end(const struct hl_handle* h, hipStream_t s, int idx);
   } while (0)
 
 // ----------------------------------------------------------------------------- handle
+// A workspace holding a backward plan (grouping) for a later apply step.
+struct hl_ws_rec {
+  const void* ws;      // NULL: free
+  int64_t n, bags;     // the plan's lookups and bags
+  int32_t stg;         // its staging rows
+  int part1;           // the first half of the apply ran on it
+};
 struct hl_handle {
   int device;
   int32_t n_tables;
@@ -37,7 +44,6 @@ struct hl_handle {
   uint32_t k_cap;
   uint32_t row_bytes;
   uint32_t n_hot;
-  uint32_t epoch;        // tags cross-block status words of one call (see hl_sort.hip)
   uint64_t n_tiles4k;    // ceil(n_rows / 4096): the bitmap and rank directory cover n_tiles4k*4096 ids
   uint32_t* d_base;      // [n_tables] first gid of each table
   uint32_t* d_rows;      // [n_tables] rows of each table
@@ -48,29 +54,33 @@ struct hl_handle {
   uint32_t* d_tk;        // top-K scratch (state, histograms, tile counts)
   size_t tk_bytes;
   hl_trace* trace;       // per-kernel event records (owned)
-  // The last call that left state in a workspace for a later call: the
-  // backward's plan (grouping) is consumed by its apply step.
-  const void* ws_last;   // workspace of that call
-  int ws_kind;           // HL_WSK_*
-  int64_t ws_n, ws_bags; // its lookups and bags
-  int32_t ws_stg;        // its staging rows
-  int ws_part1;          // the first half of the backward's apply ran on that plan
+  // Workspaces that hold a backward plan (grouping) for a later apply step;
+  // any other call on a workspace clears its record.
+  hl_ws_rec ws_rec[4];
+  int ws_next;           // next record to reuse when all are taken
   uint64_t* cg_table;    // cold-gather hash table (kept clean between calls)
   uint32_t cg_slots;     // its slots
 };
-#define HL_WSK_NONE 0
 #define HL_WSK_OTHER 1
 #define HL_WSK_BWD_PLAN 2
 static inline void hl_ws_note(hl_handle* h, const void* ws, int kind, int64_t n = 0, int64_t bags = 0,
                               int32_t stg = 0) {
-  // a call on another workspace leaves the recorded one intact
-  if (kind == HL_WSK_OTHER && ws != h->ws_last) return;
-  h->ws_last = ws;
-  h->ws_kind = kind;
-  h->ws_n = n;
-  h->ws_bags = bags;
-  h->ws_stg = stg;
-  h->ws_part1 = 0;
+  for (auto& r : h->ws_rec)
+    if (r.ws == ws) r.ws = nullptr;
+  if (kind != HL_WSK_BWD_PLAN) return;
+  hl_ws_rec* r = nullptr;
+  for (auto& c : h->ws_rec)
+    if (!c.ws && !r) r = &c;
+  if (!r) {  // more plans than records: the oldest is forgotten
+    r = &h->ws_rec[h->ws_next];
+    h->ws_next = (h->ws_next + 1) % 4;
+  }
+  *r = {ws, n, bags, stg, 0};
+}
+static inline hl_ws_rec* hl_ws_find(hl_handle* h, const void* ws) {
+  for (auto& r : h->ws_rec)
+    if (ws && r.ws == ws) return &r;
+  return nullptr;
 }
 
 // ----------------------------------------------------------------------------- errors
@@ -118,17 +128,11 @@ __device__ __forceinline__ int32_t hl_hot_slot(const uint64_t* __restrict__ bm,
 // place must not depend on the sizes of a call); buffers are carved after it
 // with 256-byte alignment.
 #define HL_WS_HEADER 16384
-#define HL_HDR_SORT 0    // 8 words: histogram done counter, per-pass tile counters
+#define HL_HDR_SORT 0    // 8 words: per-pass tile counters
 #define HL_HDR_COLD 16   // 16 words: cold-gather counters
 #define HL_HDR_DISP 64   // 8 words: dispatch epoch, done counter, tile counter
 #define HL_HDR_DSTAT 128 // dispatch look-back status words (64-bit), to the header's end
 #define HL_DISP_MAX_TILES ((HL_WS_HEADER - 4 * HL_HDR_DSTAT) / 8)
-// First and only place a new epoch is drawn: never 0 (zeroed status words) and
-// never all-ones.
-static inline uint32_t hl_next_epoch(hl_handle* h) {
-  do { ++h->epoch; } while (h->epoch == 0 || h->epoch == 0xFFFFFFFFu);
-  return h->epoch;
-}
 // Workspace carving with 256-byte alignment.
 struct hl_carver {
   char* base;
@@ -151,7 +155,7 @@ struct hl_carver {
 #define HL_SORT_THREADS 512
 #define HL_SORT_WAVES (HL_SORT_THREADS / 64)
 #ifndef HL_SORT_ITEMS
-#define HL_SORT_ITEMS 8
+#define HL_SORT_ITEMS 12
 #endif
 #define HL_SORT_TILE (HL_SORT_THREADS * HL_SORT_ITEMS)
 #define HL_SORT_MAXNB 2048        // bins of an 11-bit digit

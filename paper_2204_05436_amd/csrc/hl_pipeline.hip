@@ -26,15 +26,19 @@
 // may share a hardware queue, where a wait ahead of its signal would stall, so
 // the handovers are events then.
 //
-// Look-ahead (hl_pipeline_plan): the dispatch and cold plan of the next
-// mini-batch, which read only its inputs and the fixed hot set, run on a
-// fourth stream while the current step trains, as the accelerator segregates
-// the next mini-batch while the GPUs train (Sec. IV, pipeline figure).  Only
-// that work moves ahead: the next step's row fetch still waits for the end of
-// the current step (its staging rows and, with write-back, their write-back),
-// so no row is read before the update that precedes it.  A plan waits for
-// every step enqueued before it (their per-step buffers and workspace are the
-// plan's to rewrite), so two alternating sets of per-step buffers suffice.
+// Look-ahead (hl_pipeline_plan): the dispatch, the cold plan and the
+// backward's grouping of the next mini-batch, which read only its inputs and
+// the fixed hot set, run on a fourth stream while the current step trains, as
+// the accelerator segregates the next mini-batch while the GPUs train (Sec. IV,
+// pipeline figure).  Only that work moves ahead: the next step's row fetch
+// still waits for the end of the current step (its staging rows and, with
+// write-back, their write-back), so no row is read before the update that
+// precedes it.  A plan waits for every step enqueued before it (their per-step
+// buffers and workspace are the plan's to rewrite), so two alternating sets of
+// per-step buffers suffice.  The planned step's main stream runs the forwards
+// and the backward's apply, the fetch stream the copy.  (The grouping on a
+// stream of its own, beside the next plan, measured slower: four busy streams
+// slowed every kernel.)
 #include <vector>
 
 #include "hl_internal.h"
@@ -175,7 +179,8 @@ static bool pl_same_plan(const hl_step_io& a, const hl_step_io& b) {
          a.bags_per_sample == b.bags_per_sample && a.n_lookups == b.n_lookups && a.gids == b.gids &&
          a.codes == b.codes && a.flags == b.flags && a.pop_ids == b.pop_ids && a.nonpop_ids == b.nonpop_ids &&
          a.counts == b.counts && a.cold_ids == b.cold_ids && a.n_cold == b.n_cold &&
-         a.staging_cap == b.staging_cap && a.workspace == b.workspace && a.ws_bytes == b.ws_bytes;
+         a.staging_cap == b.staging_cap && a.workspace == b.workspace && a.ws_bytes == b.ws_bytes &&
+         (a.dY != nullptr) == (b.dY != nullptr);
 }
 
 static pl_plan* pl_pending(hl_pipeline* p, const void* ws) {
@@ -189,6 +194,16 @@ static int pl_wb_slot(const hl_pipeline* p, const uint32_t* cold_ids) {
   for (int i = 0; i < 2; ++i)
     if (p->wb_ids[i] == cold_ids) return i;
   return -1;
+}
+
+// The popular mu-batch and the hot rows of the non-popular one in one launch:
+// the hot half of the forward over every sample equals the popular mu-batch's
+// whole forward (its rows are all hot) and the non-popular one's hot half, bit
+// for bit (the same sums in the same order), so one pass over the samples
+// replaces two over the two lists.
+static hl_status pl_fwd_hot(hl_handle* h, const hl_step_io* io, hl_stream s) {
+  return hl_embbag_fwd_part(h, io->w_hot, io->staging, io->staging_cap, io->codes, io->bag_ptr, io->n_samples,
+                            io->bags_per_sample, io->n_lookups, nullptr, nullptr, io->n_samples, io->out, 1, s);
 }
 
 extern "C" hl_status hl_pipeline_plan(hl_pipeline* p, const hl_step_io* io, hl_stream stream) {
@@ -217,6 +232,10 @@ extern "C" hl_status hl_pipeline_plan(hl_pipeline* p, const hl_step_io* io, hl_s
                      io->nonpop_ids, io->counts, io->workspace, io->ws_bytes, PS));
   HL_TRY(hl_cold_plan(h, io->gids, io->codes, io->bag_ptr, B, bps, io->n_lookups, nullptr, nullptr, B,
                       io->staging_cap, io->cold_ids, io->n_cold, io->workspace, io->ws_bytes, PS));
+  // the backward's grouping needs only the codes
+  if (io->dY)
+    HL_TRY(hl_embbag_bwd_plan(h, io->staging_cap, io->codes, io->bag_ptr, B, bps, io->n_lookups, nullptr, nullptr, B,
+                              io->workspace, io->ws_bytes, PS));
   const uint32_t v = ++p->plan_seq;
   HL_TRY(pl_sig(p, P, PF_LOOK, v));
   HL_HIPTRY(hipEventRecord(p->ev_plan, P));
@@ -248,11 +267,23 @@ extern "C" hl_status hl_pipeline_step(hl_pipeline* p, const hl_step_io* io, hl_s
   }
   if (planned) {
     e->pending = false;
-    HL_TRY(pl_wt(p, m, PF_LOOK, e->seq));
-    // the fetch rewrites the staging rows: after the previous step (and its write-back)
+    // main: the forwards and the backward on the planned grouping; fetch: the
+    // copy, after the previous step (and its write-back) released the staging rows
     HL_TRY(pl_wt(p, f, PF_LOOK, e->seq));
     if (q > 1) HL_TRY(pl_wt(p, f, PF_DONE, q - 1));
-    HL_TRY(pl_wt(p, g, PF_LOOK, e->seq));
+    HL_TRY(hl_cold_fetch(h, io->cold_ids, io->n_cold, cap, io->w_host, io->staging, F));
+    HL_TRY(pl_sig(p, f, PF_FETCH, q));
+    HL_TRY(pl_wt(p, m, PF_LOOK, e->seq));
+    HL_TRY(pl_fwd_hot(h, io, M));
+    if (io->dY)
+      HL_TRY(hl_embbag_bwd_apply_part(h, io->w_hot, io->staging, cap, B, bps, L, io->dY, io->lr, 1, io->workspace,
+                                      io->ws_bytes, M));
+    HL_TRY(pl_wt(p, m, PF_FETCH, q));
+    HL_TRY(hl_embbag_fwd_part(h, io->w_hot, io->staging, cap, io->codes, io->bag_ptr, B, bps, L, io->nonpop_ids,
+                              io->counts + 1, B, io->out, 2, M));
+    if (io->dY)
+      HL_TRY(hl_embbag_bwd_apply_part(h, io->w_hot, io->staging, cap, B, bps, L, io->dY, io->lr, 2, io->workspace,
+                                      io->ws_bytes, M));
   } else {
     // the look-ahead plans use the same cold-gather hash table
     if (p->plan_seq) HL_TRY(pl_wt(p, m, PF_LOOK, p->plan_seq));
@@ -264,36 +295,33 @@ extern "C" hl_status hl_pipeline_step(hl_pipeline* p, const hl_step_io* io, hl_s
     HL_TRY(hl_cold_plan(h, io->gids, io->codes, io->bag_ptr, B, bps, L, nullptr, nullptr, B, cap, io->cold_ids,
                         io->n_cold, io->workspace, io->ws_bytes, M));
     HL_TRY(pl_sig(p, m, PF_PLAN, q));
+    // the working parameters of the non-popular mu-batch over the host link
     HL_TRY(pl_wt(p, f, PF_PLAN, q));
+    HL_TRY(hl_cold_fetch(h, io->cold_ids, io->n_cold, cap, io->w_host, io->staging, F));
+    HL_TRY(pl_sig(p, f, PF_FETCH, q));
+    // the backward's grouping needs only the codes
     HL_TRY(pl_wt(p, g, PF_PLAN, q));
+    if (io->dY)
+      HL_TRY(hl_embbag_bwd_plan(h, cap, io->codes, io->bag_ptr, B, bps, L, nullptr, nullptr, B, io->workspace,
+                                io->ws_bytes, G));
+    // the popular mu-batch and the hot rows of the non-popular one while the fetch runs
+    HL_TRY(pl_fwd_hot(h, io, M));
+    HL_TRY(pl_sig(p, m, PF_FWDHOT, q));
+    // the reduction and the hot-row updates once both forwards have read the hot rows
+    HL_TRY(pl_wt(p, g, PF_FWDHOT, q));
+    if (io->dY)
+      HL_TRY(hl_embbag_bwd_apply_part(h, io->w_hot, io->staging, cap, B, bps, L, io->dY, io->lr, 1, io->workspace,
+                                      io->ws_bytes, G));
+    HL_TRY(pl_sig(p, g, PF_GROUP, q));
+    // the staging rows: cold half of the non-popular forward, then their updates
+    HL_TRY(pl_wt(p, m, PF_FETCH, q));
+    HL_TRY(hl_embbag_fwd_part(h, io->w_hot, io->staging, cap, io->codes, io->bag_ptr, B, bps, L, io->nonpop_ids,
+                              io->counts + 1, B, io->out, 2, M));
+    HL_TRY(pl_wt(p, m, PF_GROUP, q));
+    if (io->dY)
+      HL_TRY(hl_embbag_bwd_apply_part(h, io->w_hot, io->staging, cap, B, bps, L, io->dY, io->lr, 2, io->workspace,
+                                      io->ws_bytes, M));
   }
-  // the working parameters of the non-popular mu-batch over the host link
-  HL_TRY(hl_cold_fetch(h, io->cold_ids, io->n_cold, cap, io->w_host, io->staging, F));
-  HL_TRY(pl_sig(p, f, PF_FETCH, q));
-  // the backward's grouping needs only the codes
-  if (io->dY)
-    HL_TRY(hl_embbag_bwd_plan(h, cap, io->codes, io->bag_ptr, B, bps, L, nullptr, nullptr, B, io->workspace,
-                              io->ws_bytes, G));
-  // the popular mu-batch and the hot rows of the non-popular one while the fetch runs
-  HL_TRY(hl_embbag_fwd_part(h, io->w_hot, io->staging, cap, io->codes, io->bag_ptr, B, bps, L, io->pop_ids,
-                            io->counts, B, io->out, 0, M));
-  HL_TRY(hl_embbag_fwd_part(h, io->w_hot, io->staging, cap, io->codes, io->bag_ptr, B, bps, L, io->nonpop_ids,
-                            io->counts + 1, B, io->out, 1, M));
-  HL_TRY(pl_sig(p, m, PF_FWDHOT, q));
-  // the reduction and the hot-row updates once both forwards have read the hot rows
-  HL_TRY(pl_wt(p, g, PF_FWDHOT, q));
-  if (io->dY)
-    HL_TRY(hl_embbag_bwd_apply_part(h, io->w_hot, io->staging, cap, B, bps, L, io->dY, io->lr, 1, io->workspace,
-                                    io->ws_bytes, G));
-  HL_TRY(pl_sig(p, g, PF_GROUP, q));
-  // the staging rows: cold half of the non-popular forward, then their updates
-  HL_TRY(pl_wt(p, m, PF_FETCH, q));
-  HL_TRY(hl_embbag_fwd_part(h, io->w_hot, io->staging, cap, io->codes, io->bag_ptr, B, bps, L, io->nonpop_ids,
-                            io->counts + 1, B, io->out, 2, M));
-  HL_TRY(pl_wt(p, m, PF_GROUP, q));
-  if (io->dY)
-    HL_TRY(hl_embbag_bwd_apply_part(h, io->w_hot, io->staging, cap, B, bps, L, io->dY, io->lr, 2, io->workspace,
-                                    io->ws_bytes, M));
   HL_TRY(pl_sig(p, m, PF_DONE, q));
   if (io->write_back) {
     HL_TRY(pl_wt(p, f, PF_DONE, q));

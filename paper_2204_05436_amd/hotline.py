@@ -16,7 +16,7 @@ HL_F32, HL_BF16 = 0, 1
 STATUS = {0: "ok", 1: "invalid argument", 2: "out of range", 3: "capacity exceeded", 4: "HIP runtime error",
           5: "unsupported", 6: "device error word set"}
 DEVERR = {"OUT_OF_RANGE": 0x1, "BAD_CODE": 0x2, "CAPACITY": 0x4, "BAD_HOTSET": 0x8, "STALL": 0x10,
-          "SHAPE": 0x20}
+          "SHAPE": 0x20, "INTERNAL": 0x40}
 
 
 class HotlineError(RuntimeError):

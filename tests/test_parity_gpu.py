@@ -247,8 +247,9 @@ def test_capacity_and_range_errors():
 
 def test_plan_apply_contract():
     """The backward's apply needs its plan in the workspace: refused without one,
-    after another workspace call, or with other sizes; applying one plan twice is
-    two SGD steps (against the oracle run twice)."""
+    after another call on that workspace, or with other sizes; calls on another
+    workspace leave it; applying one plan twice is two SGD steps (against the
+    oracle run twice)."""
     import oracle as O
     from parity_lib import check_close
     w = configs.scaled(configs.WORKLOADS["tiny"], batch=128, row_scale=0.2, name="tiny-contract")
@@ -283,6 +284,10 @@ def test_plan_apply_contract():
         w0 = hp.w_hot[:len(hot)].cpu().numpy().copy()
         s0 = hp.staging[:n_cold].cpu().numpy().copy()
         hl.hl_embbag_bwd_plan(h, hp.staging_cap, hp.codes, b.bag_ptr, B, bps, L, None, None, B, hp.ws)
+        # calls on another workspace (a plan of its own included) leave this plan intact
+        ws2 = torch.zeros_like(hp.ws)
+        hl.hl_embbag_bwd_plan(h, hp.staging_cap, hp.codes, b.bag_ptr, B, bps, L, None, None, B, ws2)
+        hl.hl_partition(h, hp.flags, B, hp.pop, hp.nonpop, hp.counts, ws2)
         for _ in range(2):
             hl.hl_embbag_bwd_apply(h, hp.w_hot, hp.staging, hp.staging_cap, B, bps, L, b.dY, w.lr, hp.ws)
         assert hp.device_error() == 0
