@@ -678,21 +678,118 @@ bw_cold(const uint32_t* __restrict__ keys, uint32_t n, eb_geom g, void* stg, uin
     const uint32_t kn = p + 1 < n ? keys[p + 1] : EB_SENT;
     uint64_t m = __ballot(k != kn && bw_deferred(k, n_hot, gc_rows));
     while (m) {
+      // run end gi + NG j of the remaining ones goes to group gi, 4 per group in flight
       uint64_t mm = m;
       for (int q = 0; q < gi; ++q) mm &= mm - 1;
-      const int src = mm ? __ffsll((unsigned long long)mm) - 1 : 0;
-      const uint32_t key = __shfl(k, src);
-      if (mm && cact) {
-        const int64_t u = key - n_hot;
-        T* row = (T*)stg + u * g.D + col;
-        float wv[VEC], gv[VEC];
-        RowIO<VEC, BF>::load(row, wv);
-        ld_f32<VEC>(gc + u * g.D + col, gv);
+      int src[4];
+      bool has[4];
 #pragma unroll
-        for (int e = 0; e < VEC; ++e) wv[e] = wv[e] - lr * gv[e];
-        RowIO<VEC, BF>::store(row, wv);
+      for (int j = 0; j < 4; ++j) {
+        has[j] = mm != 0;
+        src[j] = has[j] ? __ffsll((unsigned long long)mm) - 1 : 0;
+        for (int q = 0; q < g.NG && mm; ++q) mm &= mm - 1;
       }
-      for (int q = 0; q < g.NG && m; ++q) m &= m - 1;
+      int64_t u[4];
+      float wv[4][VEC], gv[4][VEC];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        u[j] = (int64_t)__shfl(k, src[j]) - n_hot;
+        if (has[j] && cact) {
+          RowIO<VEC, BF>::load((T*)stg + u[j] * g.D + col, wv[j]);
+          ld_f32<VEC>(gc + u[j] * g.D + col, gv[j]);
+        }
+      }
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        if (has[j] && cact) {
+#pragma unroll
+          for (int e = 0; e < VEC; ++e) wv[j][e] = wv[j][e] - lr * gv[j][e];
+          RowIO<VEC, BF>::store((T*)stg + u[j] * g.D + col, wv[j]);
+        }
+      for (int q = 0; q < 4 * g.NG && m; ++q) m &= m - 1;
+    }
+  }
+}
+
+// The cold half of the forward from the backward's grouping: the sorted tail
+// from *bnd holds a (staging key, bag) pair for every cold lookup.  A bag is
+// completed by the pair of its first cold lookup in CSR order (the first copy
+// of that pair): out[bag] += its staging rows in CSR order, the same sums as
+// the forward's cold half over the non-popular mu-batch.  A group of lanes
+// takes FT pairs at once.
+#define FT 4
+template <int VEC, bool BF>
+__global__ void __launch_bounds__(256)
+eb_fwd_tail(const uint32_t* __restrict__ keys, const uint32_t* __restrict__ vals, uint32_t n,
+            const uint32_t* __restrict__ bnd, eb_geom g, const void* stg_, int32_t stg_rows, uint32_t n_hot,
+            uint32_t k_cap, const int32_t* __restrict__ codes, const int32_t* __restrict__ bag_ptr,
+            float* __restrict__ out, uint32_t* err) {
+  typedef typename RowIO<VEC, BF>::T T;
+  const T* stg = (const T*)stg_;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int gi = lane / g.G, gl = lane - gi * g.G;
+  if (gi >= g.NG) return;
+  const int32_t colv = blockIdx.y * 64 + gl;
+  const bool cact = colv < g.vpr;
+  const int64_t col = (int64_t)colv * VEC;
+  const uint32_t b0 = min(*bnd, n);
+  const uint64_t stride = (uint64_t)gridDim.x * 4 * g.NG * FT;
+  for (uint64_t p0 = b0 + ((uint64_t)(blockIdx.x * 4 + w) * g.NG + gi) * FT; p0 < n; p0 += stride) {
+    uint32_t key[FT], bag[FT];
+    bool take[FT];
+#pragma unroll
+    for (int j = 0; j < FT; ++j) {
+      const uint64_t p = p0 + j;
+      key[j] = p < n ? keys[p] : EB_SENT;
+      bag[j] = p < n ? vals[p] : 0u;
+      const uint32_t kp = p > b0 && p < n ? keys[p - 1] : EB_SENT;
+      const uint32_t bp = p > b0 && p < n ? vals[p - 1] : 0u;
+      take[j] = key[j] != EB_SENT && key[j] >= n_hot && key[j] - n_hot < (uint32_t)stg_rows &&
+                !(kp == key[j] && bp == bag[j]);
+    }
+    int32_t lo[FT], hi[FT];
+#pragma unroll
+    for (int j = 0; j < FT; ++j) {
+      lo[j] = take[j] ? bag_ptr[bag[j]] : 0;
+      hi[j] = take[j] ? bag_ptr[bag[j] + 1] : 0;
+    }
+#pragma unroll
+    for (int j = 0; j < FT; ++j) {
+      if (!take[j]) continue;
+      const uint32_t u = key[j] - n_hot;
+      if (hi[j] - lo[j] != 1) {
+        // the bag's first cold lookup in CSR order names the pair that completes it
+        bool mine = false;
+        for (int32_t i = lo[j]; i < hi[j]; ++i) {
+          const uint32_t c = (uint32_t)codes[i];
+          if (c >= k_cap && c - k_cap < (uint32_t)stg_rows) {
+            mine = c - k_cap == u;
+            break;
+          }
+        }
+        if (!mine) take[j] = false;
+      }
+    }
+    float o[FT][VEC], v[FT][VEC];
+#pragma unroll
+    for (int j = 0; j < FT; ++j)
+      if (take[j] && cact) {
+        ld_f32<VEC>(out + (int64_t)bag[j] * g.D + col, o[j]);
+        if (hi[j] - lo[j] == 1) RowIO<VEC, BF>::load(stg + (int64_t)(key[j] - n_hot) * g.D + col, v[j]);
+      }
+#pragma unroll
+    for (int j = 0; j < FT; ++j) {
+      if (!take[j]) continue;
+      if (hi[j] - lo[j] == 1) {
+        if (cact) {
+#pragma unroll
+          for (int e = 0; e < VEC; ++e) o[j][e] += v[j][e];
+        }
+      } else {
+        eb_pass<VEC, BF, true>(o[j], nullptr, stg, stg_rows, n_hot, k_cap, codes, lo[j], hi[j], g, col, cact, gl,
+                               err);
+      }
+      if (cact) st_f32<VEC>(out + (int64_t)bag[j] * g.D + col, o[j]);
     }
   }
 }
@@ -865,6 +962,42 @@ extern "C" hl_status hl_embbag_bwd_apply_part(hl_handle* h, void* w_hot, void* s
 #undef BWD
   HL_LAUNCHED();
   if (part == 1) rec->part1 = 1;
+  return HL_OK;
+}
+
+hl_status hl_embbag_fwd_cold_sorted(hl_handle* h, const void* staging, int32_t stg_rows, const int32_t* codes,
+                                    const int32_t* bag_ptr, int32_t n_samples, int32_t bps, int64_t n_lookups,
+                                    float* out, void* workspace, size_t ws_bytes, hl_stream stream) {
+  hl_status st = check_common(h, codes, bag_ptr, n_samples, bps, n_lookups, nullptr, n_samples, stg_rows);
+  if (st != HL_OK) return st;
+  if (!workspace || !out || (stg_rows && !staging)) return HL_ERR_INVALID_ARG;
+  const int64_t n_bags = (int64_t)n_samples * bps;
+  hl_ws_rec* rec = hl_ws_find(h, workspace);
+  if (!rec || rec->n != n_lookups || rec->bags != n_bags || rec->stg != stg_rows || !rec->part1)
+    return HL_ERR_INVALID_ARG;  // the grouping and the first apply half must be in this workspace
+  if (n_lookups == 0 || n_samples == 0) return HL_OK;
+  if (ws_bytes < hl_bwd_ws_bytes(h, n_lookups, n_bags)) return HL_ERR_CAPACITY;
+  hl_carver c = hl_carver::after_header(workspace, ws_bytes);
+  bw_ws ws;
+  bw_carve(c, ws, (uint32_t)n_lookups, n_bags, h->dim);
+  uint32_t *sk, *sv;
+  hl_sort_result(ws.sort, bw_key_bits(h, stg_rows), &sk, &sv);
+  const size_t es = h->dtype == HL_F32 ? 4 : 2;
+  const int vec = eb_pick_vec(h->dim, es, {staging, out});
+  eb_geom g = eb_make_geom(h->dim, vec);
+  const uint32_t n = (uint32_t)n_lookups;
+  uint32_t b = hl_div_up(n, 4 * g.NG * FT);
+  if (b > 512) b = 512;
+  hipStream_t s = (hipStream_t)stream;
+  const bool bf = h->dtype == HL_BF16;
+#define TAIL(V, B)                                                                                                  \
+  HL_KERNEL(h, s, "eb_fwd_tail", (eb_fwd_tail<V, B>), dim3(b, g.cchunks), dim3(256), 0, s, sk, sv, n, ws.bnd, g, \
+            staging, stg_rows, h->n_hot, h->k_cap, codes, bag_ptr, out, h->d_err)
+  if (vec == 4) { if (bf) TAIL(4, true); else TAIL(4, false); }
+  else if (vec == 2) { if (bf) TAIL(2, true); else TAIL(2, false); }
+  else { if (bf) TAIL(1, true); else TAIL(1, false); }
+#undef TAIL
+  HL_LAUNCHED();
   return HL_OK;
 }
 

@@ -148,6 +148,14 @@ struct hl_carver {
   }
 };
 
+// The cold half of the forward (hl_embbag_fwd_part 2 over the non-popular
+// mu-batch) read from the backward's grouping held in `workspace`: the same
+// sums, over the cold lookups only.  Needs a plan over every sample and the
+// first apply half (which marks where the cold keys start) on that workspace.
+hl_status hl_embbag_fwd_cold_sorted(hl_handle* h, const void* staging, int32_t stg_rows, const int32_t* codes,
+                                    const int32_t* bag_ptr, int32_t n_samples, int32_t bps, int64_t n_lookups,
+                                    float* out, void* workspace, size_t ws_bytes, hl_stream stream);
+
 // ----------------------------------------------------------------------------- sort
 // Stable LSD radix sort of (key, value) uint32 pairs with digits of up to 11
 // bits: one histogram kernel plus one kernel per digit with decoupled look-back

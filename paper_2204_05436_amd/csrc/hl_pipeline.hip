@@ -50,6 +50,7 @@
 #define PF_WB 5   // two: one per cold list
 #define PF_LOOK 7 // a look-ahead plan: its own sequence
 #define PF_DONE 8 // the end of a step on the main stream
+#define PF_SORT 9 // a look-ahead plan's grouping (plan sequence)
 #define PF_N 16
 #define PL_PLANS 4 // look-ahead plans not yet stepped
 
@@ -79,16 +80,20 @@ struct pl_plan {
 struct hl_pipeline {
   hl_handle* h;
   hipStream_t main, fetch, group, plan;
+  int32_t fetch_cus;
   pl_plan plans[PL_PLANS];
   uint32_t plan_seq;      // sequence number of the last look-ahead plan
   uint32_t* flags;        // [PF_N] device
   uint32_t seq;           // sequence number of the last step
   uint32_t wb_seq[2];     // step whose write-back last read each cold list
   bool use_flags;         // handovers through device flags (masked streams)
-  hipEvent_t ev[PF_N];    // the same handovers as events; ev[PF_WB + i] always
-  hipEvent_t ev_in, ev_out, ev_pin, ev_plan;
+  hipEvent_t ev[PF_N];    // the same handovers as events (pipelines without masks)
+  hipEvent_t ev_in, ev_out, ev_pin, ev_plan, ev_f, ev_g;
   const void* wb_ids[2];  // the cold list each write-back event covers
   int wb_next;
+  const void* stg_ptr[4]; // staging buffers of recent steps, and the last step that used each
+  uint32_t stg_seq[4];
+  int stg_next;
 };
 
 extern "C" hl_status hl_pipeline_destroy(hl_pipeline* p) {
@@ -97,7 +102,7 @@ extern "C" hl_status hl_pipeline_destroy(hl_pipeline* p) {
   if (hipDeviceSynchronize() != hipSuccess) st = HL_ERR_HIP;
   for (hipEvent_t e : p->ev)
     if (e && hipEventDestroy(e) != hipSuccess) st = HL_ERR_HIP;
-  for (hipEvent_t e : {p->ev_in, p->ev_out, p->ev_pin, p->ev_plan})
+  for (hipEvent_t e : {p->ev_in, p->ev_out, p->ev_pin, p->ev_plan, p->ev_f, p->ev_g})
     if (e && hipEventDestroy(e) != hipSuccess) st = HL_ERR_HIP;
   hipStream_t ss[] = {p->main, p->fetch, p->group, p->plan};
   for (hipStream_t s : ss)
@@ -111,17 +116,19 @@ extern "C" hl_status hl_pipeline_create(hl_handle* h, int32_t fetch_cus, hl_pipe
   if (!h || !out || fetch_cus < 0) return HL_ERR_INVALID_ARG;
   hl_pipeline* p = new hl_pipeline();
   p->h = h;
-  hl_stream s[4] = {nullptr, nullptr, nullptr, nullptr};
+  // the group stream is created on first use: look-ahead steps leave it idle,
+  // and every stream takes a hardware queue
+  hl_stream s[3] = {nullptr, nullptr, nullptr};
   hl_status st = hl_stream_create(0, fetch_cus, 0, &s[0]);
-  for (int i = 1; i < 4; ++i)
+  for (int i = 1; i < 3; ++i)
     if (st == HL_OK) st = hl_stream_create(0, fetch_cus, 1, &s[i]);
   p->fetch = (hipStream_t)s[0];
   p->main = (hipStream_t)s[1];
-  p->group = (hipStream_t)s[2];
-  p->plan = (hipStream_t)s[3];
+  p->plan = (hipStream_t)s[2];
+  p->fetch_cus = fetch_cus;
   p->use_flags = fetch_cus > 0;
-  hipEvent_t* extra[] = {&p->ev_in, &p->ev_out, &p->ev_pin, &p->ev_plan};
-  for (int i = 0; i < PF_N + 4; ++i) {
+  hipEvent_t* extra[] = {&p->ev_in, &p->ev_out, &p->ev_pin, &p->ev_plan, &p->ev_f, &p->ev_g};
+  for (int i = 0; i < PF_N + 6; ++i) {
     hipEvent_t* e = i < PF_N ? &p->ev[i] : extra[i - PF_N];
     if (st == HL_OK && hipEventCreateWithFlags(e, hipEventDisableTiming) != hipSuccess) st = HL_ERR_HIP;
   }
@@ -131,10 +138,9 @@ extern "C" hl_status hl_pipeline_create(hl_handle* h, int32_t fetch_cus, hl_pipe
     hl_pipeline_destroy(p);
     return st;
   }
-  // the write-back and plan events start recorded (nothing to wait for)
+  // the write-back events start recorded (nothing to wait for)
   for (int i = 0; i < 2; ++i)
-    if (hipEventRecord(p->ev[PF_WB + i], p->fetch) != hipSuccess) st = HL_ERR_HIP;
-  if (hipEventRecord(p->ev_plan, p->plan) != hipSuccess) st = HL_ERR_HIP;
+    if (!p->use_flags && hipEventRecord(p->ev[PF_WB + i], p->fetch) != hipSuccess) st = HL_ERR_HIP;
   *out = p;
   return st;
 }
@@ -149,12 +155,12 @@ extern "C" hl_status hl_pipeline_create(hl_handle* h, int32_t fetch_cus, hl_pipe
     if ((x) != hipSuccess) return HL_ERR_HIP;       \
   } while (0)
 
-// handover f of step v: stream s has enqueued the producer
+// handover f of step v: stream s has enqueued the producer.  (Flag mode
+// records no event: event records in every step measured ~12 us slower steps.)
 static hl_status pl_sig(hl_pipeline* p, hipStream_t s, int f, uint32_t v) {
   if (p->use_flags) {
     hipLaunchKernelGGL(pl_signal, dim3(1), dim3(64), 0, s, p->flags + f, v);
-    if (hipGetLastError() != hipSuccess) return HL_ERR_HIP;
-    if (f < PF_WB) return HL_OK;  // the write-back events also serve the host-side syncs
+    return hipGetLastError() == hipSuccess ? HL_OK : HL_ERR_HIP;
   }
   return hipEventRecord(p->ev[f], s) == hipSuccess ? HL_OK : HL_ERR_HIP;
 }
@@ -163,6 +169,14 @@ static hl_status pl_wt(hl_pipeline* p, hipStream_t s, int f, uint32_t v) {
   if (!p->use_flags) return hipStreamWaitEvent(s, p->ev[f], 0) == hipSuccess ? HL_OK : HL_ERR_HIP;
   hipLaunchKernelGGL(pl_wait, dim3(1), dim3(64), 0, s, p->flags + f, v, p->h->d_err);
   return hipGetLastError() == hipSuccess ? HL_OK : HL_ERR_HIP;
+}
+
+static hl_status pl_group(hl_pipeline* p) {
+  if (p->group) return HL_OK;
+  hl_stream g = nullptr;
+  HL_TRY(hl_stream_create(0, p->fetch_cus, 1, &g));
+  p->group = (hipStream_t)g;
+  return HL_OK;
 }
 
 static hl_status pl_not_capturing(hipStream_t s) {
@@ -187,6 +201,23 @@ static pl_plan* pl_pending(hl_pipeline* p, const void* ws) {
   for (pl_plan& e : p->plans)
     if (e.pending && e.io.workspace == ws) return &e;
   return nullptr;
+}
+
+// the last step that used this staging buffer (0: none seen)
+static uint32_t pl_stg_last(const hl_pipeline* p, const void* stg) {
+  for (int i = 0; i < 4; ++i)
+    if (p->stg_ptr[i] == stg) return p->stg_seq[i];
+  return 0;
+}
+static void pl_stg_note(hl_pipeline* p, const void* stg, uint32_t q) {
+  for (int i = 0; i < 4; ++i)
+    if (p->stg_ptr[i] == stg) {
+      p->stg_seq[i] = q;
+      return;
+    }
+  p->stg_ptr[p->stg_next] = stg;
+  p->stg_seq[p->stg_next] = q;
+  p->stg_next = (p->stg_next + 1) % 4;
 }
 
 // the write-back slot whose last write-back read this cold list, or -1
@@ -232,13 +263,14 @@ extern "C" hl_status hl_pipeline_plan(hl_pipeline* p, const hl_step_io* io, hl_s
                      io->nonpop_ids, io->counts, io->workspace, io->ws_bytes, PS));
   HL_TRY(hl_cold_plan(h, io->gids, io->codes, io->bag_ptr, B, bps, io->n_lookups, nullptr, nullptr, B,
                       io->staging_cap, io->cold_ids, io->n_cold, io->workspace, io->ws_bytes, PS));
+  // the cold list is ready: the fetch may start while the grouping runs
+  const uint32_t v = ++p->plan_seq;
+  HL_TRY(pl_sig(p, P, PF_LOOK, v));
   // the backward's grouping needs only the codes
   if (io->dY)
     HL_TRY(hl_embbag_bwd_plan(h, io->staging_cap, io->codes, io->bag_ptr, B, bps, io->n_lookups, nullptr, nullptr, B,
                               io->workspace, io->ws_bytes, PS));
-  const uint32_t v = ++p->plan_seq;
-  HL_TRY(pl_sig(p, P, PF_LOOK, v));
-  HL_HIPTRY(hipEventRecord(p->ev_plan, P));
+  HL_TRY(pl_sig(p, P, PF_SORT, v));
   e->io = *io;
   e->seq = v;
   e->pending = true;
@@ -252,6 +284,7 @@ extern "C" hl_status hl_pipeline_step(hl_pipeline* p, const hl_step_io* io, hl_s
   const bool planned = io->step_flags & HL_STEP_PLANNED;
   pl_plan* e = pl_pending(p, io->workspace);
   if (planned ? !e || !pl_same_plan(e->io, *io) : e != nullptr) return HL_ERR_INVALID_ARG;
+  if (!planned) HL_TRY(pl_group(p));
   const int32_t B = io->n_samples, bps = io->bags_per_sample, cap = io->staging_cap;
   const int64_t L = io->n_lookups;
   hipStream_t caller = (hipStream_t)stream, m = p->main, f = p->fetch, g = p->group;
@@ -262,28 +295,37 @@ extern "C" hl_status hl_pipeline_step(hl_pipeline* p, const hl_step_io* io, hl_s
   if (tie) {
     HL_HIPTRY(hipEventRecord(p->ev_in, caller));
     HL_HIPTRY(hipStreamWaitEvent(m, p->ev_in, 0));
-    HL_HIPTRY(hipStreamWaitEvent(g, p->ev_in, 0));
-    if (planned) HL_HIPTRY(hipStreamWaitEvent(f, p->ev_in, 0));
+    HL_HIPTRY(hipStreamWaitEvent(planned ? f : g, p->ev_in, 0));
   }
   if (planned) {
     e->pending = false;
     // main: the forwards and the backward on the planned grouping; fetch: the
-    // copy, after the previous step (and its write-back) released the staging rows
+    // copy, once the last step that used these staging rows has ended (a
+    // write-back of the previous step precedes it on the fetch stream).  With
+    // two staging buffers alternating, the copy overlaps the previous step.
     HL_TRY(pl_wt(p, f, PF_LOOK, e->seq));
-    if (q > 1) HL_TRY(pl_wt(p, f, PF_DONE, q - 1));
+    const uint32_t last = pl_stg_last(p, io->staging);
+    if (last) HL_TRY(pl_wt(p, f, PF_DONE, last));
     HL_TRY(hl_cold_fetch(h, io->cold_ids, io->n_cold, cap, io->w_host, io->staging, F));
     HL_TRY(pl_sig(p, f, PF_FETCH, q));
     HL_TRY(pl_wt(p, m, PF_LOOK, e->seq));
     HL_TRY(pl_fwd_hot(h, io, M));
-    if (io->dY)
+    if (io->dY) {
+      HL_TRY(pl_wt(p, m, PF_SORT, e->seq));
       HL_TRY(hl_embbag_bwd_apply_part(h, io->w_hot, io->staging, cap, B, bps, L, io->dY, io->lr, 1, io->workspace,
                                       io->ws_bytes, M));
+    }
     HL_TRY(pl_wt(p, m, PF_FETCH, q));
-    HL_TRY(hl_embbag_fwd_part(h, io->w_hot, io->staging, cap, io->codes, io->bag_ptr, B, bps, L, io->nonpop_ids,
-                              io->counts + 1, B, io->out, 2, M));
-    if (io->dY)
+    if (io->dY) {
+      // the cold half of the forward from the grouping's tail (cold lookups only)
+      HL_TRY(hl_embbag_fwd_cold_sorted(h, io->staging, cap, io->codes, io->bag_ptr, B, bps, L, io->out, io->workspace,
+                                       io->ws_bytes, M));
       HL_TRY(hl_embbag_bwd_apply_part(h, io->w_hot, io->staging, cap, B, bps, L, io->dY, io->lr, 2, io->workspace,
                                       io->ws_bytes, M));
+    } else {
+      HL_TRY(hl_embbag_fwd_part(h, io->w_hot, io->staging, cap, io->codes, io->bag_ptr, B, bps, L, io->nonpop_ids,
+                                io->counts + 1, B, io->out, 2, M));
+    }
   } else {
     // the look-ahead plans use the same cold-gather hash table
     if (p->plan_seq) HL_TRY(pl_wt(p, m, PF_LOOK, p->plan_seq));
@@ -323,6 +365,7 @@ extern "C" hl_status hl_pipeline_step(hl_pipeline* p, const hl_step_io* io, hl_s
                                       io->ws_bytes, M));
   }
   HL_TRY(pl_sig(p, m, PF_DONE, q));
+  pl_stg_note(p, io->staging, q);
   if (io->write_back) {
     HL_TRY(pl_wt(p, f, PF_DONE, q));
     HL_TRY(hl_cold_scatter(h, io->cold_ids, io->n_cold, cap, io->staging, const_cast<void*>(io->w_host), F));
@@ -334,15 +377,23 @@ extern "C" hl_status hl_pipeline_step(hl_pipeline* p, const hl_step_io* io, hl_s
     p->wb_seq[slot] = q;
     HL_TRY(pl_sig(p, f, PF_WB + slot, q));
   }
-  HL_HIPTRY(hipEventRecord(p->ev_out, m));
-  if (tie) HL_HIPTRY(hipStreamWaitEvent(caller, p->ev_out, 0));
+  if (tie) {
+    HL_HIPTRY(hipEventRecord(p->ev_out, m));
+    HL_HIPTRY(hipStreamWaitEvent(caller, p->ev_out, 0));
+  }
   return HL_OK;
 }
 
 extern "C" hl_status hl_pipeline_sync_writeback(hl_pipeline* p, hl_stream stream) {
   if (!p) return HL_ERR_INVALID_ARG;
-  HL_HIPTRY(hipStreamWaitEvent((hipStream_t)stream, p->ev[PF_WB], 0));
-  HL_HIPTRY(hipStreamWaitEvent((hipStream_t)stream, p->ev[PF_WB + 1], 0));
+  if (!p->use_flags) {
+    HL_HIPTRY(hipStreamWaitEvent((hipStream_t)stream, p->ev[PF_WB], 0));
+    HL_HIPTRY(hipStreamWaitEvent((hipStream_t)stream, p->ev[PF_WB + 1], 0));
+    return HL_OK;
+  }
+  // the write-backs run in order on the fetch stream
+  HL_HIPTRY(hipEventRecord(p->ev_f, p->fetch));
+  HL_HIPTRY(hipStreamWaitEvent((hipStream_t)stream, p->ev_f, 0));
   return HL_OK;
 }
 
@@ -350,13 +401,26 @@ extern "C" hl_status hl_pipeline_streams(const hl_pipeline* p, hl_stream* main, 
   if (!p) return HL_ERR_INVALID_ARG;
   if (main) *main = (hl_stream)p->main;
   if (fetch) *fetch = (hl_stream)p->fetch;
-  if (group) *group = (hl_stream)p->group;
+  if (group) {
+    HL_TRY(pl_group(const_cast<hl_pipeline*>(p)));
+    *group = (hl_stream)p->group;
+  }
   return HL_OK;
 }
 
 extern "C" hl_status hl_pipeline_sync(hl_pipeline* p, hl_stream stream) {
   if (!p) return HL_ERR_INVALID_ARG;
-  HL_HIPTRY(hipStreamWaitEvent((hipStream_t)stream, p->ev_out, 0));
-  HL_HIPTRY(hipStreamWaitEvent((hipStream_t)stream, p->ev_plan, 0));
-  return hl_pipeline_sync_writeback(p, stream);
+  hipStream_t c = (hipStream_t)stream;
+  // events recorded now, behind everything enqueued on each stream
+  HL_HIPTRY(hipEventRecord(p->ev_out, p->main));
+  HL_HIPTRY(hipEventRecord(p->ev_plan, p->plan));
+  HL_HIPTRY(hipEventRecord(p->ev_f, p->fetch));
+  HL_HIPTRY(hipStreamWaitEvent(c, p->ev_out, 0));
+  HL_HIPTRY(hipStreamWaitEvent(c, p->ev_plan, 0));
+  HL_HIPTRY(hipStreamWaitEvent(c, p->ev_f, 0));
+  if (p->group) {
+    HL_HIPTRY(hipEventRecord(p->ev_g, p->group));
+    HL_HIPTRY(hipStreamWaitEvent(c, p->ev_g, 0));
+  }
+  return HL_OK;
 }

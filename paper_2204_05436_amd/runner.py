@@ -77,7 +77,6 @@ class HotPath:
         self.sdt = sdt
         self.w_hot = torch.zeros((self.k_cap, w.dim), dtype=sdt, device=device)
         self.staging_cap = int(staging_cap if staging_cap is not None else max(1, self.max_lookups))
-        self.staging = torch.zeros((self.staging_cap, w.dim), dtype=sdt, device=device)
         self.hot_ids = torch.zeros(max(1, min(self.k_cap, n_rows)), dtype=torch.int32, device=device)
         L, B = max(1, self.max_lookups), max(1, self.max_samples)
         i32 = dict(dtype=torch.int32, device=device)
@@ -88,11 +87,12 @@ class HotPath:
                 flags=torch.zeros(B, dtype=torch.uint8, device=device), pop=torch.zeros(B, **i32),
                 nonpop=torch.zeros(B, **i32), counts=torch.zeros(2, **i32),
                 cold_ids=torch.zeros(self.staging_cap, **i32), n_cold=torch.zeros(1, **i32),
+                staging=torch.zeros((self.staging_cap, w.dim), dtype=sdt, device=device),
                 ws=torch.zeros(wsb, dtype=torch.uint8, device=device))
 
         # two sets of per-step buffers, alternated between steps: a write-back
-        # still reading one step's cold list, or a look-ahead plan of the next
-        # mini-batch, uses the other set
+        # still reading one step's cold list, a look-ahead plan of the next
+        # mini-batch, or the next step's row fetch, uses the other set
         self._sets = [bufs(), bufs()]
         self._par = 0
         self._use(0)
@@ -135,7 +135,7 @@ class HotPath:
         io.pop_ids, io.nonpop_ids, io.counts = s.pop.data_ptr(), s.nonpop.data_ptr(), s.counts.data_ptr()
         io.cold_ids, io.n_cold = s.cold_ids.data_ptr(), s.n_cold.data_ptr()
         io.w_host, io.w_hot, io.staging, io.staging_cap = (
-            self.table.dev, self.w_hot.data_ptr(), self.staging.data_ptr(), self.staging_cap)
+            self.table.dev, self.w_hot.data_ptr(), s.staging.data_ptr(), self.staging_cap)
         io.out, io.workspace, io.ws_bytes = self.out.data_ptr(), s.ws.data_ptr(), s.ws.numel()
         io.write_back = int(self.writeback)
         io.step_flags = flags

@@ -471,7 +471,7 @@ def test_graph_replay(name, writeback):
             torch.cuda.synchronize()
             n = int(bufs.n_cold.item())
             return dict(out=hp.out[:mba.n_bags].cpu().numpy().copy(), w_hot=hp.w_hot[:hp.n_hot].cpu().numpy().copy(),
-                        stg=hp.staging[:n].cpu().numpy().copy(), cold=bufs.cold_ids[:n].cpu().numpy().copy(),
+                        stg=bufs.staging[:n].cpu().numpy().copy(), cold=bufs.cold_ids[:n].cpu().numpy().copy(),
                         codes=bufs.codes[:mba.n_lookups].cpu().numpy().copy(), tab=table.array.copy())
 
         def reset():
