@@ -228,6 +228,7 @@ extern "C" hl_status hl_remap(const hl_handle* h, const uint32_t* gids, int64_t 
 #define DS_MAX_TABLES 1024  // table bases and sizes in LDS up to this many tables
 #define DS_MAX_BAGS 4096
 #define DS_MAX_SPB 2048
+#define DS_MAP 8192         // lookups per block mapped to their bag in LDS
 #define DS_EPOCH 0
 #define DS_DONE 1
 #define DS_TILE 2
@@ -240,6 +241,7 @@ ds_kernel(const uint32_t* __restrict__ rows, const int32_t* __restrict__ bag_ptr
   __shared__ int32_t off[DS_MAX_BAGS + 1];
   __shared__ uint32_t tb_base[DS_MAX_TABLES], tb_rows[DS_MAX_TABLES];
   __shared__ uint8_t fl[DS_MAX_SPB];
+  __shared__ uint16_t bmap[DS_MAP];  // lookup - lo -> bag within the block
   __shared__ uint32_t s_tile, s_epoch, wsum[DS_THREADS / 64];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   if (tid == 0) {
@@ -262,6 +264,19 @@ ds_kernel(const uint32_t* __restrict__ rows, const int32_t* __restrict__ bag_ptr
   if (tile == 0 && tid == 0 && bag_ptr[(int64_t)n_samples * bps] != n_lookups) hl_flag(err, HL_DEVERR_SHAPE);
   __syncthreads();
   const int32_t lo = off[0], hi = (int32_t)min((int64_t)off[nbg], n_lookups);
+  // each lookup's bag from an LDS map built bag by bag (a binary search over the
+  // offsets when the block holds more lookups than the map)
+  const bool mapped = hi - lo <= DS_MAP;
+  if (mapped) {
+    for (int j = tid; j < nbg; j += DS_THREADS) {
+      const int32_t e = min(off[j + 1], hi);
+      for (int32_t q = max(off[j], lo); q < e; ++q) bmap[q - lo] = (uint16_t)j;
+    }
+    __syncthreads();
+  }
+  // the table of bag j is (t0 + j) % n_tables, its sample j / bps
+  const uint32_t t0 = (uint32_t)(bg0 % n_tables);
+  const float inv_t = 1.0f / (float)n_tables, inv_b = 1.0f / (float)bps;
   // 4 lookups per thread per round, their loads issued together
   for (int32_t i0 = lo + tid; i0 < hi; i0 += 4 * DS_THREADS) {
     int a[4];
@@ -270,18 +285,22 @@ ds_kernel(const uint32_t* __restrict__ rows, const int32_t* __restrict__ bag_ptr
     for (int k = 0; k < 4; ++k) {
       const int32_t i = i0 + k * DS_THREADS;
       int x = 0, y = nbg;  // off[x] <= i < off[y]
-      if (i < hi)
-        while (y - x > 1) {
-          const int m = (x + y) >> 1;
-          if (off[m] <= i) x = m; else y = m;
-        }
+      if (i < hi) {
+        if (mapped) x = bmap[i - lo];
+        else
+          while (y - x > 1) {
+            const int m = (x + y) >> 1;
+            if (off[m] <= i) x = m; else y = m;
+          }
+      }
       a[k] = x;
       r[k] = i < hi ? rows[i] : 0u;
     }
     uint32_t g[4];
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
-      const int32_t t = (int32_t)((bg0 + a[k]) % n_tables);
+      uint32_t t;
+      (void)hl_fdiv(t0 + (uint32_t)a[k], (uint32_t)n_tables, inv_t, &t);
       const bool in = i0 + k * DS_THREADS < hi;
       g[k] = 0xFFFFFFFFu;
       if (in) {
@@ -296,7 +315,8 @@ ds_kernel(const uint32_t* __restrict__ rows, const int32_t* __restrict__ bag_ptr
       const int32_t c = g[k] < n_rows ? hl_hot_slot(bitmap, rank, g[k]) : -1;
       gids[i] = g[k];
       codes[i] = c;
-      if (c < 0) fl[a[k] / bps] = 0;
+      uint32_t rm;
+      if (c < 0) fl[hl_fdiv((uint32_t)a[k], (uint32_t)bps, inv_b, &rm)] = 0;
     }
   }
   __syncthreads();

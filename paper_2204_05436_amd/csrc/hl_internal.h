@@ -83,6 +83,23 @@ static inline hl_ws_rec* hl_ws_find(hl_handle* h, const void* ws) {
   return nullptr;
 }
 
+// n / d and n % d for 0 <= n < 2^22, d >= 1, with inv = 1.0f / d: the float
+// quotient is off by at most one, and the remainder check corrects it (no
+// integer division, which takes tens of instructions).
+__device__ __forceinline__ uint32_t hl_fdiv(uint32_t n, uint32_t d, float inv, uint32_t* rem) {
+  uint32_t q = (uint32_t)((float)n * inv);
+  int32_t r = (int32_t)(n - q * d);
+  if (r < 0) {
+    --q;
+    r += (int32_t)d;
+  } else if (r >= (int32_t)d) {
+    ++q;
+    r -= (int32_t)d;
+  }
+  *rem = (uint32_t)r;
+  return q;
+}
+
 // ----------------------------------------------------------------------------- errors
 #define HL_HIP(call)                                   \
   do {                                                 \
