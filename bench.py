@@ -33,18 +33,32 @@ def log(*a):
 
 
 def kernel_bytes(name, st):
-    """Algorithmic bytes of one launch of kernel `name` (per-step statistics st)."""
+    """Algorithmic bytes of one launch of kernel `name` in the pipelined step
+    (per-step statistics st): each input read once, each output written once.
+    L lookups, nb bags, B samples, U distinct rows, C distinct cold rows, Lc
+    cold lookups, R bytes per stored row, O bytes per pooled output row."""
     L, nb, B, U, R, O = st["L"], st["n_bags"], st["B"], st["U"], st["R"], st["O"]
+    C, Lc = st["n_cold"], st["Lc"]
     return {
-        "hl_k_gids": 4 * L + 4 * (nb + 1) + 4 * L,
-        "cl_kernel": 4 * L + 4 * (nb + 1) + B,
-        "pt_emit": B + 4 * B,
-        "rm_kernel": 8 * L,
-        # forward, both launches of a step together: codes, offsets, each referenced row once, outputs
-        "eb_fwd": (4 * L + 4 * (nb + 1) + U * R + nb * O) / 2.0,
+        # rows, offsets, a bitmap word per lookup; gids, codes, flags, the two lists
+        "ds_kernel": 4 * L + 4 * (nb + 1) + 8 * L + 8 * L + 5 * B,
+        # cold plan: gids and codes of every lookup, table slot per cold lookup, the cold list
+        "cg_insert": 8 * L + 8 * Lc,
+        "cg_rank": 8 * L + 4 * C,
+        "cg_codes": 8 * Lc + 4 * C,
+        # the host-link copy (also reported against the link's peak)
+        "cg_fetch": 4 * C + 2 * C * R,
+        # grouping: keys and bags out, a histogram read, two passes of keys and bags in and out
         "bw_prep": 4 * L + 4 * (nb + 1) + 8 * L,
+        "srt_hist": 4 * L,
         "srt_pass": 16 * L,
-        "bw_reduce1": 8 * L + nb * O + 2 * U * R,
+        # hot half of the forward over every bag: codes, offsets, each referenced row once, outputs
+        "eb_fwd_hot": 4 * L + 4 * (nb + 1) + (U - C) * R + nb * O,
+        # cold half: tail keys and bags, offsets, staging rows, outputs read and written
+        "eb_fwd_tail": 8 * Lc + 8 * Lc + C * R + 2 * Lc * O,
+        # reduction: sorted keys and bags, dY, each updated row read and written
+        "bw_reduce1": 8 * L + nb * O + 2 * (U - C) * R + C * O,
+        "bw_cold": 4 * Lc + 2 * C * R + C * O,
     }.get(name)
 
 
@@ -101,48 +115,31 @@ def main():
     log(f"[bench] learning phase {learn_ms:.2f} ms, n_hot {n_hot}")
 
     # per-batch statistics (untimed pass over every measured batch)
+    # steps are issued from a stream of their own (work on the default stream
+    # would serialize with the pipeline's streams)
+    side = torch.cuda.Stream()
     stats = []
-    for b in dmeas:
-        hp.step(b)
+    for j, b in enumerate(dmeas):
+        with torch.cuda.stream(side):
+            hp.step(b, next=dmeas[j + 1] if j + 1 < len(dmeas) else None)
         torch.cuda.synchronize()
         L = b.n_lookups
         U = int(torch.unique(hp.codes[:L]).numel())
         c = hp.counts.cpu().numpy()
+        Lc = int((hp.codes[:L] >= hp.k_cap).sum().item())
         stats.append(dict(L=L, n_bags=b.n_bags, B=b.n_samples, U=U, n_pop=int(c[0]), n_cold=int(hp.n_cold.item()),
-                          R=hp.staging.element_size() * w.dim, O=4 * w.dim))
+                          Lc=Lc, R=hp.staging.element_size() * w.dim, O=4 * w.dim))
     err = hp.device_error()
     if err:
         raise SystemExit(f"device error word {err:#x} after the statistics pass")
     log("[bench] statistics pass done")
-    for i in range(args.warmup):
-        hp.step(dmeas[i % len(dmeas)])
+    with torch.cuda.stream(side):
+        for i in range(args.warmup):
+            hp.step(dmeas[i % len(dmeas)], untied=True, next=dmeas[(i + 1) % len(dmeas)] if i + 1 < args.warmup else None)
+        hp.sync()
     torch.cuda.synchronize()
     log(f"[bench] warmup {args.warmup} steps done")
-
-    # steps are issued from a stream of their own (work on the default stream
-    # would serialize with the pipeline's streams)
     K = args.steps
-    side = torch.cuda.Stream()
-    torch.cuda.synchronize()
-    with torch.cuda.stream(side):
-        # steps tied to the issuing stream (each waits for it and it for each), for reference
-        e0.record()
-        for i in range(K):
-            hp.step(dmeas[i % len(dmeas)])
-        e1.record()
-    torch.cuda.synchronize()
-    tied_ms = e0.elapsed_time(e1)
-    log(f"[bench] {K} tied steps: {tied_ms:.3f} ms")
-    with torch.cuda.stream(side):
-        # untied steps without look-ahead, for reference
-        e0.record()
-        for i in range(K):
-            hp.step(dmeas[i % len(dmeas)], untied=True)
-        hp.sync()
-        e1.record()
-    torch.cuda.synchronize()
-    untied_ms = e0.elapsed_time(e1)
-    log(f"[bench] {K} untied steps without look-ahead: {untied_ms:.3f} ms")
 
     # timed region: K pipelined steps back to back (inputs resident, so the steps
     # are not tied to the issuing stream; one wait for all of them at the end),
@@ -167,6 +164,26 @@ def main():
     if err:
         raise SystemExit(f"device error word {err:#x} in the timed region")
 
+    # for reference: steps tied to the issuing stream (each waits for it and it
+    # for each), and untied steps without look-ahead
+    with torch.cuda.stream(side):
+        e0.record()
+        for i in range(K):
+            hp.step(dmeas[i % len(dmeas)])
+        e1.record()
+    torch.cuda.synchronize()
+    tied_ms = e0.elapsed_time(e1)
+    log(f"[bench] {K} tied steps: {tied_ms:.3f} ms")
+    with torch.cuda.stream(side):
+        e0.record()
+        for i in range(K):
+            hp.step(dmeas[i % len(dmeas)], untied=True)
+        hp.sync()
+        e1.record()
+    torch.cuda.synchronize()
+    untied_ms = e0.elapsed_time(e1)
+    log(f"[bench] {K} untied steps without look-ahead: {untied_ms:.3f} ms")
+
     # forward + backward section alone: the fetch is awaited first, then events
     # bracket fwd(popular), fwd(non-popular) and the backward (its grouping on
     # its own stream, overlapped with the forwards)
@@ -178,27 +195,22 @@ def main():
     t_fb = float(np.mean(fb_ms))
     log(f"[bench] fwd+bwd section: {t_fb * 1e3:.1f} us per step (median {np.median(fb_ms) * 1e3:.1f})")
 
-    # third region of K steps, sequential on one stream, with HIP events around
-    # every stage and kernel (the breakdown)
+    # third region: the timed configuration again (K look-ahead steps, untied)
+    # with HIP events around every kernel on the stream it is launched on: the
+    # per-kernel durations of the roofline (the events slow the steps a little)
     hl.hl_trace_enable(hp.h, 64 * K + 64)
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(len(STAGES) + 1)] for _ in range(K)]
     torch.cuda.synchronize()
     start2 = torch.cuda.Event(enable_timing=True)
     stop2 = torch.cuda.Event(enable_timing=True)
-    start2.record()
-    for i in range(K):
-        hp.step(dmeas[i % len(dmeas)], events=ev[i], mode="sequential")
-    stop2.record()
+    with torch.cuda.stream(side):
+        start2.record()
+        for i in range(K):
+            hp.step(dmeas[i % len(dmeas)], untied=True, next=dmeas[(i + 1) % len(dmeas)] if i + 1 < K else None)
+        hp.sync()
+        stop2.record()
     torch.cuda.synchronize()
     traced_ms = start2.elapsed_time(stop2)
-    log(f"[bench] traced sequential {K} steps: {traced_ms:.3f} ms")
-
-    # per-stage and per-kernel times
-    stage_ms = {s: 0.0 for s in STAGES}
-    for i in range(K):
-        for j, s in enumerate(STAGES):
-            stage_ms[s] += ev[i][j].elapsed_time(ev[i][j + 1])
-    stage_ms = {s: v / K for s, v in stage_ms.items()}
+    log(f"[bench] traced pipelined {K} steps: {traced_ms:.3f} ms")
     kern = {}
     for i in range(hl.hl_trace_count(hp.h)):
         name, ms = hl.hl_trace_read(hp.h, i)
@@ -208,6 +220,18 @@ def main():
     hl.hl_trace_enable(hp.h, 0)
     kernels = {n: {"launches_per_step": c / K, "ms_per_step": t / K, "avg_us": 1e3 * t / c}
                for n, (c, t) in sorted(kern.items(), key=lambda x: -x[1][1])}
+
+    # fourth region: the calls in order on one stream, HIP events between the
+    # stages (the stage breakdown)
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(len(STAGES) + 1)] for _ in range(K)]
+    for i in range(K):
+        hp.step(dmeas[i % len(dmeas)], events=ev[i], mode="sequential")
+    torch.cuda.synchronize()
+    stage_ms = {s: 0.0 for s in STAGES}
+    for i in range(K):
+        for j, s in enumerate(STAGES):
+            stage_ms[s] += ev[i][j].elapsed_time(ev[i][j + 1])
+    stage_ms = {s: v / K for s, v in stage_ms.items()}
 
     steps_stats = [stats[i % len(stats)] for i in range(K)]
     avg = {k: float(np.mean([s[k] for s in steps_stats])) for k in steps_stats[0]}
@@ -219,14 +243,15 @@ def main():
     bwd_b = 4 * avg["L"] + 4 * (avg["n_bags"] + 1) + avg["n_bags"] * avg["O"] + 2 * avg["U"] * avg["R"]
     fb_frac = (fwd_b + bwd_b) / (t_fb / 1e3) / HBM_PEAK
 
-    # roofline of the dominant HBM-bound kernel (the host-link-bound row copy excluded)
-    dom = None
+    # roofline of the dominant kernel by time per step (the host-link-bound row
+    # copy excluded: it is reported against the link)
     for n, k in kernels.items():
-        if n in ("cg_fetch", "cg_scatter", "hl_k_gather"):
-            continue
-        if kernel_bytes(n, avg) is not None:
-            dom = n
-            break
+        kb = kernel_bytes(n, avg)
+        if kb is not None:
+            k["algorithmic_GBps"] = kb / (k["avg_us"] * 1e-6) / 1e9
+    dom = next(n for n in kernels if n not in ("cg_fetch", "cg_scatter"))
+    if kernel_bytes(dom, avg) is None:
+        raise SystemExit(f"no byte model for the dominant kernel {dom}")
     kd = kernels[dom]
     ach = kernel_bytes(dom, avg) / (kd["avg_us"] * 1e-6)
     roof = {"kernel": dom, "bound": "hbm", "achieved": ach / 1e9, "peak": HBM_PEAK / 1e9, "unit": "GB/s",
@@ -251,9 +276,9 @@ def main():
                    "zipf_alpha": w.alpha, "hot_cache_rows": k_cap, "n_hot": n_hot,
                    "profile_batches": w.profile_batches, "measured_batches": w.measured_batches,
                    "parallelism": "single-gpu"},
-        "schedule": "pipelined by the native scheduler: main, backward and look-ahead plan streams on 224 compute "
-                    "units, the host-link fetch on 32 compute units of its own; each step's dispatch and cold "
-                    "plan run during the step before",
+        "schedule": "pipelined by the native scheduler: the host-link fetch on 32 compute units, the look-ahead "
+                    "plans (dispatch, cold plan, grouping of the next mini-batch, during the step before) on 64, "
+                    "the forwards and the backward on the other 160",
         "tied_ms_per_step": tied_ms / K,
         "untied_no_lookahead_ms_per_step": untied_ms / K,
         "host_enqueue_ms_per_step": host_ms / K,
@@ -265,7 +290,7 @@ def main():
         "classify_samples_per_s": avg["B"] / ((stage_ms["classify"] + stage_ms["partition"]) / 1e3),
         "popular_fraction": avg["n_pop"] / avg["B"],
         "unique_rows_per_batch": avg["U"], "cold_rows_per_batch": avg["n_cold"],
-        "learning_phase_ms": learn_ms, "traced_sequential_ms_per_step": traced_ms / K,
+        "learning_phase_ms": learn_ms, "traced_pipelined_ms_per_step": traced_ms / K,
         "stages_ms": stage_ms, "kernels": kernels,
         "roofline": roof, "link_roofline": link, "cpu_baseline": cpu,
     }

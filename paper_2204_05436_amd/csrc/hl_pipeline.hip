@@ -80,7 +80,7 @@ struct pl_plan {
 struct hl_pipeline {
   hl_handle* h;
   hipStream_t main, fetch, group, plan;
-  int32_t fetch_cus;
+  int32_t fetch_cus, plan_cus;
   pl_plan plans[PL_PLANS];
   uint32_t plan_seq;      // sequence number of the last look-ahead plan
   uint32_t* flags;        // [PF_N] device
@@ -112,20 +112,24 @@ extern "C" hl_status hl_pipeline_destroy(hl_pipeline* p) {
   return st;
 }
 
-extern "C" hl_status hl_pipeline_create(hl_handle* h, int32_t fetch_cus, hl_pipeline** out) {
-  if (!h || !out || fetch_cus < 0) return HL_ERR_INVALID_ARG;
+extern "C" hl_status hl_pipeline_create(hl_handle* h, int32_t fetch_cus, int32_t plan_cus, hl_pipeline** out) {
+  if (!h || !out || fetch_cus < 0 || plan_cus < 0 || (plan_cus > 0 && fetch_cus == 0)) return HL_ERR_INVALID_ARG;
   hl_pipeline* p = new hl_pipeline();
   p->h = h;
   // the group stream is created on first use: look-ahead steps leave it idle,
   // and every stream takes a hardware queue
+  // compute units [0, fetch_cus) for the copy, the next plan_cus for the
+  // look-ahead plans (0: with main), the rest for main (and group)
   hl_stream s[3] = {nullptr, nullptr, nullptr};
   hl_status st = hl_stream_create(0, fetch_cus, 0, &s[0]);
-  for (int i = 1; i < 3; ++i)
-    if (st == HL_OK) st = hl_stream_create(0, fetch_cus, 1, &s[i]);
+  if (st == HL_OK) st = hl_stream_create(0, fetch_cus + plan_cus, 1, &s[1]);
+  if (st == HL_OK)
+    st = plan_cus ? hl_stream_create(fetch_cus, plan_cus, 0, &s[2]) : hl_stream_create(0, fetch_cus, 1, &s[2]);
   p->fetch = (hipStream_t)s[0];
   p->main = (hipStream_t)s[1];
   p->plan = (hipStream_t)s[2];
   p->fetch_cus = fetch_cus;
+  p->plan_cus = plan_cus;
   p->use_flags = fetch_cus > 0;
   hipEvent_t* extra[] = {&p->ev_in, &p->ev_out, &p->ev_pin, &p->ev_plan, &p->ev_f, &p->ev_g};
   for (int i = 0; i < PF_N + 6; ++i) {
@@ -174,7 +178,7 @@ static hl_status pl_wt(hl_pipeline* p, hipStream_t s, int f, uint32_t v) {
 static hl_status pl_group(hl_pipeline* p) {
   if (p->group) return HL_OK;
   hl_stream g = nullptr;
-  HL_TRY(hl_stream_create(0, p->fetch_cus, 1, &g));
+  HL_TRY(hl_stream_create(0, p->fetch_cus + p->plan_cus, 1, &g));
   p->group = (hipStream_t)g;
   return HL_OK;
 }

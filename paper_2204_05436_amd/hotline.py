@@ -78,7 +78,7 @@ _SIGS = {
     "hl_trace_reset": (C.c_int, [P]),
     "hl_host_alloc": (C.c_int, [SZ, C.POINTER(P), C.POINTER(P)]),
     "hl_stream_create": (C.c_int, [I32, I32, I32, C.POINTER(P)]),
-    "hl_pipeline_create": (C.c_int, [P, I32, C.POINTER(P)]),
+    "hl_pipeline_create": (C.c_int, [P, I32, I32, C.POINTER(P)]),
     "hl_pipeline_destroy": (C.c_int, [P]),
     "hl_pipeline_step": (C.c_int, [P, C.POINTER(StepIO), P]),
     "hl_pipeline_plan": (C.c_int, [P, C.POINTER(StepIO), P]),
@@ -349,9 +349,9 @@ def hl_stream_destroy(stream):
     _ck("hl_stream_destroy", lib().hl_stream_destroy(stream))
 
 
-def hl_pipeline_create(h, fetch_cus):
+def hl_pipeline_create(h, fetch_cus, plan_cus=0):
     p = P()
-    _ck("hl_pipeline_create", lib().hl_pipeline_create(h.ptr, int(fetch_cus), C.byref(p)))
+    _ck("hl_pipeline_create", lib().hl_pipeline_create(h.ptr, int(fetch_cus), int(plan_cus), C.byref(p)))
     return p.value
 
 

@@ -61,7 +61,7 @@ MODES = ("pipelined", "sequential", "fwdbwd")
 class HotPath:
     def __init__(self, w: Workload, rows_per_table, table: hl.HostTable, max_lookups: int, max_samples: int,
                  device="cuda", k_cap: int | None = None, staging_cap: int | None = None, writeback: bool = False,
-                 fetch_cus: int = 32):
+                 fetch_cus: int = 32, plan_cus: int = 64):
         self.w = w
         self.device = device
         self.rows_per_table = np.asarray(rows_per_table, dtype=np.uint32)
@@ -102,7 +102,8 @@ class HotPath:
         # the native pipeline (its own streams; the host-link copy on compute units
         # of its own, since its slow host reads would stall kernels sharing them)
         self.fetch_cus = int(fetch_cus)
-        self.pipe = hl.hl_pipeline_create(self.h, self.fetch_cus)
+        self.plan_cus = int(plan_cus) if self.fetch_cus else 0
+        self.pipe = hl.hl_pipeline_create(self.h, self.fetch_cus, self.plan_cus)
         self.io = hl.StepIO()
         # a process has a few hardware queues (streams beyond them share queues):
         # the Python rendering's streams are created only when it is used
