@@ -4,12 +4,19 @@
 A step is one pass of the whole per-mini-batch path over one batch: global ids,
 classification, partition into popular / non-popular mu-batches, remap, cold
 gather for the non-popular mu-batch, forward of both mu-batches and one
-coalesced SGD step, in the paper's pipelined schedule (the cold-row fetch over
-the host link, on compute units of its own, and the backward's grouping run on
-streams of their own while the popular mu-batch runs).  The learning phase (access counting over 16 profiling
+coalesced SGD step, in the paper's pipelined schedule: the host-link fetch on
+compute units of its own, the next mini-batch's segregation (dispatch, cold
+plan, grouping) during the step before on others, the forwards and the
+backward on the rest.  The learning phase (access counting over 16 profiling
 batches, top-K selection, hot-cache fill) runs once before and is reported
 separately.  Inputs (32 measured batches, their gradients, the host table) are
 resident before the timed region starts.
+
+Regions, in order: a statistics pass, warmup, the timed region (K steps, no
+events inside), then the same steps with HIP events around the kernels of one
+name at a time (per-kernel durations for the roofline and the fwd+bwd
+fraction), and the oracle's CPU baseline.  --breakdown adds reference
+schedules and a per-stage breakdown.
 
 Prints one JSON line on stdout; progress goes to stderr."""
 import argparse
@@ -62,6 +69,49 @@ def kernel_bytes(name, st):
     }.get(name)
 
 
+def reference_regions(hp, dmeas, side, K):
+    """--breakdown: steps tied to the issuing stream, untied steps without
+    look-ahead, the fwd+bwd section of the Python rendering (events after the
+    fetch and after the backward), and the calls in order on one stream with
+    events between the stages."""
+    import torch
+    from paper_2204_05436_amd.runner import STAGES
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    out = {}
+    with torch.cuda.stream(side):
+        e0.record()
+        for i in range(K):
+            hp.step(dmeas[i % len(dmeas)])
+        e1.record()
+    torch.cuda.synchronize()
+    out["tied_ms_per_step"] = e0.elapsed_time(e1) / K
+    with torch.cuda.stream(side):
+        e0.record()
+        for i in range(K):
+            hp.step(dmeas[i % len(dmeas)], untied=True)
+        hp.sync()
+        e1.record()
+    torch.cuda.synchronize()
+    out["untied_no_lookahead_ms_per_step"] = e0.elapsed_time(e1) / K
+    evf = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(K)]
+    for i in range(K):
+        hp.step(dmeas[i % len(dmeas)], events=evf[i], mode="fwdbwd")
+    torch.cuda.synchronize()
+    fb = [e[0].elapsed_time(e[1]) for e in evf]
+    out["fwd_bwd_section_us_mean"], out["fwd_bwd_section_us_median"] = 1e3 * np.mean(fb), 1e3 * np.median(fb)
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(len(STAGES) + 1)] for _ in range(K)]
+    for i in range(K):
+        hp.step(dmeas[i % len(dmeas)], events=ev[i], mode="sequential")
+    torch.cuda.synchronize()
+    st = {s: 0.0 for s in STAGES}
+    for i in range(K):
+        for j, s in enumerate(STAGES):
+            st[s] += ev[i][j].elapsed_time(ev[i][j + 1])
+    out["sequential_stages_ms"] = {s: v / K for s, v in st.items()}
+    log(f"[bench] breakdown: {out}")
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -70,6 +120,7 @@ def main():
     ap.add_argument("--workload", default="dlrm-large")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the oracle baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--breakdown", action="store_true", help="also time reference schedules and the stages")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build measures one GPU only (asked for --gpus {args.gpus}); the path shards "
@@ -78,7 +129,7 @@ def main():
 
     import torch
     from paper_2204_05436_amd import configs, hotline as hl, workload as W
-    from paper_2204_05436_amd.runner import STAGES, HotPath, to_device
+    from paper_2204_05436_amd.runner import HotPath, to_device
 
     dev = "cuda:0"
     torch.cuda.set_device(0)
@@ -164,91 +215,61 @@ def main():
     if err:
         raise SystemExit(f"device error word {err:#x} in the timed region")
 
-    # for reference: steps tied to the issuing stream (each waits for it and it
-    # for each), and untied steps without look-ahead
-    with torch.cuda.stream(side):
-        e0.record()
-        for i in range(K):
-            hp.step(dmeas[i % len(dmeas)])
-        e1.record()
-    torch.cuda.synchronize()
-    tied_ms = e0.elapsed_time(e1)
-    log(f"[bench] {K} tied steps: {tied_ms:.3f} ms")
-    with torch.cuda.stream(side):
-        e0.record()
-        for i in range(K):
-            hp.step(dmeas[i % len(dmeas)], untied=True)
-        hp.sync()
-        e1.record()
-    torch.cuda.synchronize()
-    untied_ms = e0.elapsed_time(e1)
-    log(f"[bench] {K} untied steps without look-ahead: {untied_ms:.3f} ms")
-
-    # forward + backward section alone: the fetch is awaited first, then events
-    # bracket fwd(popular), fwd(non-popular) and the backward (its grouping on
-    # its own stream, overlapped with the forwards)
-    evf = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(K)]
-    for i in range(K):
-        hp.step(dmeas[i % len(dmeas)], events=evf[i], mode="fwdbwd")
-    torch.cuda.synchronize()
-    fb_ms = [e[0].elapsed_time(e[1]) for e in evf]
-    t_fb = float(np.mean(fb_ms))
-    log(f"[bench] fwd+bwd section: {t_fb * 1e3:.1f} us per step (median {np.median(fb_ms) * 1e3:.1f})")
-
-    # third region: the timed configuration again (K look-ahead steps, untied)
-    # with HIP events around every kernel on the stream it is launched on: the
-    # per-kernel durations of the roofline (the events slow the steps a little)
-    hl.hl_trace_enable(hp.h, 64 * K + 64)
-    torch.cuda.synchronize()
-    start2 = torch.cuda.Event(enable_timing=True)
-    stop2 = torch.cuda.Event(enable_timing=True)
-    with torch.cuda.stream(side):
-        start2.record()
-        for i in range(K):
-            hp.step(dmeas[i % len(dmeas)], untied=True, next=dmeas[(i + 1) % len(dmeas)] if i + 1 < K else None)
-        hp.sync()
-        stop2.record()
-    torch.cuda.synchronize()
-    traced_ms = start2.elapsed_time(stop2)
-    log(f"[bench] traced pipelined {K} steps: {traced_ms:.3f} ms")
-    kern = {}
-    for i in range(hl.hl_trace_count(hp.h)):
-        name, ms = hl.hl_trace_read(hp.h, i)
-        k = kern.setdefault(name, [0, 0.0])
-        k[0] += 1
-        k[1] += ms
-    hl.hl_trace_enable(hp.h, 0)
-    kernels = {n: {"launches_per_step": c / K, "ms_per_step": t / K, "avg_us": 1e3 * t / c}
-               for n, (c, t) in sorted(kern.items(), key=lambda x: -x[1][1])}
-
-    # fourth region: the calls in order on one stream, HIP events between the
-    # stages (the stage breakdown)
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(len(STAGES) + 1)] for _ in range(K)]
-    for i in range(K):
-        hp.step(dmeas[i % len(dmeas)], events=ev[i], mode="sequential")
-    torch.cuda.synchronize()
-    stage_ms = {s: 0.0 for s in STAGES}
-    for i in range(K):
-        for j, s in enumerate(STAGES):
-            stage_ms[s] += ev[i][j].elapsed_time(ev[i][j + 1])
-    stage_ms = {s: v / K for s, v in stage_ms.items()}
-
     steps_stats = [stats[i % len(stats)] for i in range(K)]
     avg = {k: float(np.mean([s[k] for s in steps_stats])) for k in steps_stats[0]}
     L_tot = sum(s["L"] for s in steps_stats)
-    B_tot = sum(s["B"] for s in steps_stats)
     value = L_tot / (total_ms / 1e3)
-    t_fb_seq = stage_ms["fwd_pop"] + stage_ms["fwd_nonpop"] + stage_ms["bwd"]
+
+    def look_ahead_steps():
+        with torch.cuda.stream(side):
+            for i in range(K):
+                hp.step(dmeas[i % len(dmeas)], untied=True, next=dmeas[(i + 1) % len(dmeas)] if i + 1 < K else None)
+            hp.sync()
+        torch.cuda.synchronize()
+
+    def traced(only):
+        """K look-ahead steps with HIP events around every kernel named `only`
+        (None: every kernel) on the stream it is launched on; per name: launches
+        and total ms."""
+        hl.hl_trace_enable(hp.h, 64 * K + 64)
+        hl.hl_trace_only(hp.h, only)
+        look_ahead_steps()
+        kern = {}
+        for i in range(hl.hl_trace_count(hp.h)):
+            name, ms = hl.hl_trace_read(hp.h, i)
+            k = kern.setdefault(name, [0, 0.0])
+            k[0] += 1
+            k[1] += ms
+        hl.hl_trace_only(hp.h, None)
+        hl.hl_trace_enable(hp.h, 0)
+        return kern
+
+    # per-kernel durations in the timed configuration: which kernels run (events
+    # around all of them), then each kernel timed alone (events around its
+    # launches only, so the others run as in the timed region)
+    names = list(traced(None))
+    kernels = {}
+    for n in names:
+        c, t = traced(n)[n]
+        kernels[n] = {"launches_per_step": c / K, "ms_per_step": t / K, "avg_us": 1e3 * t / c}
+        kb = kernel_bytes(n, avg)
+        if kb is not None:
+            kernels[n]["algorithmic_GBps"] = kb / (kernels[n]["avg_us"] * 1e-6) / 1e9
+    kernels = dict(sorted(kernels.items(), key=lambda x: -x[1]["ms_per_step"]))
+    log("[bench] per-kernel times: " + ", ".join(f"{n} {k['avg_us']:.1f}us x{k['launches_per_step']:.0f}"
+                                               for n, k in kernels.items()))
+
+    # the embedding forward and backward: their kernels' time per step (the
+    # grouping included), against the algorithmic bytes of both passes
+    fb_kernels = ("eb_fwd_hot", "eb_fwd_tail", "bw_prep", "srt_hist", "srt_pass", "bw_reduce1", "bw_reduce2",
+                  "bw_cold")
+    t_fb = sum(kernels[n]["ms_per_step"] for n in fb_kernels if n in kernels)
     fwd_b = 4 * avg["L"] + 4 * (avg["n_bags"] + 1) + avg["U"] * avg["R"] + avg["n_bags"] * avg["O"]
     bwd_b = 4 * avg["L"] + 4 * (avg["n_bags"] + 1) + avg["n_bags"] * avg["O"] + 2 * avg["U"] * avg["R"]
     fb_frac = (fwd_b + bwd_b) / (t_fb / 1e3) / HBM_PEAK
 
     # roofline of the dominant kernel by time per step (the host-link-bound row
     # copy excluded: it is reported against the link)
-    for n, k in kernels.items():
-        kb = kernel_bytes(n, avg)
-        if kb is not None:
-            k["algorithmic_GBps"] = kb / (k["avg_us"] * 1e-6) / 1e9
     dom = next(n for n in kernels if n not in ("cg_fetch", "cg_scatter"))
     if kernel_bytes(dom, avg) is None:
         raise SystemExit(f"no byte model for the dominant kernel {dom}")
@@ -262,6 +283,10 @@ def main():
         gb = avg["n_cold"] * avg["R"]
         link = {"kernel": "cg_fetch", "bytes_per_launch": gb, "avg_us": kernels["cg_fetch"]["avg_us"],
                 "achieved_GBps": gb / (kernels["cg_fetch"]["avg_us"] * 1e-6) / 1e9, "peak_GBps": LINK_PEAK / 1e9}
+
+    breakdown = None
+    if args.breakdown:
+        breakdown = reference_regions(hp, dmeas, side, K)
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -279,20 +304,17 @@ def main():
         "schedule": "pipelined by the native scheduler: the host-link fetch on 32 compute units, the look-ahead "
                     "plans (dispatch, cold plan, grouping of the next mini-batch, during the step before) on 64, "
                     "the forwards and the backward on the other 160",
-        "tied_ms_per_step": tied_ms / K,
-        "untied_no_lookahead_ms_per_step": untied_ms / K,
         "host_enqueue_ms_per_step": host_ms / K,
-        "fwd_bwd_us": t_fb * 1e3,
+        "fwd_bwd_kernel_us": t_fb * 1e3,
         "fwd_bwd_lookups_per_s": avg["L"] / (t_fb / 1e3),
         "fwd_bwd_hbm_frac": fb_frac,
-        "fwd_bwd_sequential_us": t_fb_seq * 1e3,
         "fwd_bwd_algorithmic_bytes": fwd_b + bwd_b,
-        "classify_samples_per_s": avg["B"] / ((stage_ms["classify"] + stage_ms["partition"]) / 1e3),
+        # the dispatch kernel classifies, partitions and remaps a mini-batch
+        "classify_samples_per_s": avg["B"] / (kernels["ds_kernel"]["avg_us"] * 1e-6),
         "popular_fraction": avg["n_pop"] / avg["B"],
         "unique_rows_per_batch": avg["U"], "cold_rows_per_batch": avg["n_cold"],
-        "learning_phase_ms": learn_ms, "traced_pipelined_ms_per_step": traced_ms / K,
-        "stages_ms": stage_ms, "kernels": kernels,
-        "roofline": roof, "link_roofline": link, "cpu_baseline": cpu,
+        "learning_phase_ms": learn_ms, "kernels": kernels,
+        "roofline": roof, "link_roofline": link, "cpu_baseline": cpu, "breakdown": breakdown,
     }
     print(json.dumps(res), flush=True)
     hp.close()

@@ -302,8 +302,11 @@ hl_status hl_last_device_error(hl_handle* h, uint32_t* err_out);
  * event pairs and records one pair around every kernel the handle's calls
  * launch (until cap records exist); cap = 0 turns tracing off.  hl_trace_read
  * waits for record i and returns its kernel name (static string) and
- * duration in ms.  hl_trace_reset forgets the records. */
+ * duration in ms.  hl_trace_reset forgets the records.  hl_trace_only(h,
+ * name) records only kernels of that name (NULL: all again), so one kernel
+ * can be timed without events around all the others. */
 hl_status hl_trace_enable(hl_handle* h, int32_t cap);
+hl_status hl_trace_only(hl_handle* h, const char* name);
 int32_t hl_trace_count(const hl_handle* h);
 hl_status hl_trace_read(const hl_handle* h, int32_t i, const char** name, float* ms);
 hl_status hl_trace_reset(hl_handle* h);

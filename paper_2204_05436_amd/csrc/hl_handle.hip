@@ -5,6 +5,8 @@
 
 #include <vector>
 
+#include <cstring>
+
 #include "hl_internal.h"
 
 size_t hl_topk_scratch_bytes(uint64_t n_rows);
@@ -47,6 +49,7 @@ hl_status hl_fill32(uint32_t* p, uint64_t n, uint32_t v, hipStream_t s) { return
 int hl_trace_begin(const hl_handle* h, hipStream_t s, const char* name) {
   hl_trace* t = h ? h->trace : nullptr;
   if (!t || t->n >= t->cap) return -1;
+  if (t->only[0] && strcmp(t->only, name) != 0) return -1;
   const int i = t->n++;
   t->rec[i].name = name;
   if (hipEventRecord(t->rec[i].a, s) != hipSuccess) return -1;
@@ -75,13 +78,22 @@ extern "C" hl_status hl_trace_enable(hl_handle* h, int32_t cap) {
   h->trace->rec = (hl_trace_rec*)calloc((size_t)cap, sizeof(hl_trace_rec));
   if (!h->trace->rec) return HL_ERR_CAPACITY;
   for (int i = 0; i < cap; ++i) {
-    if (hipEventCreate(&h->trace->rec[i].a) != hipSuccess || hipEventCreate(&h->trace->rec[i].b) != hipSuccess) {
+    // timing only: no system-scope fence (cache write-back and invalidate) at
+    // each record, which would lengthen and perturb what is measured
+    if (hipEventCreateWithFlags(&h->trace->rec[i].a, hipEventDisableSystemFence) != hipSuccess ||
+        hipEventCreateWithFlags(&h->trace->rec[i].b, hipEventDisableSystemFence) != hipSuccess) {
       h->trace->cap = i + 1;
       trace_free(h->trace);
       return HL_ERR_HIP;
     }
   }
   h->trace->cap = cap;
+  return HL_OK;
+}
+
+extern "C" hl_status hl_trace_only(hl_handle* h, const char* name) {
+  if (!h || (name && strlen(name) >= sizeof(h->trace->only))) return HL_ERR_INVALID_ARG;
+  strcpy(h->trace->only, name ? name : "");
   return HL_OK;
 }
 

@@ -16,6 +16,7 @@ struct hl_trace_rec {
 struct hl_trace {
   int32_t cap = 0, n = 0;
   hl_trace_rec* rec = nullptr;
+  char only[64] = {0};  // record only kernels of this name (empty: all)
 };
 // Index of the record opened for kernel `name` on stream s, or -1.
 int hl_trace_begin(const struct hl_handle* h, hipStream_t s, const char* name);

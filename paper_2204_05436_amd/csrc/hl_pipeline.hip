@@ -134,7 +134,9 @@ extern "C" hl_status hl_pipeline_create(hl_handle* h, int32_t fetch_cus, int32_t
   hipEvent_t* extra[] = {&p->ev_in, &p->ev_out, &p->ev_pin, &p->ev_plan, &p->ev_f, &p->ev_g};
   for (int i = 0; i < PF_N + 6; ++i) {
     hipEvent_t* e = i < PF_N ? &p->ev[i] : extra[i - PF_N];
-    if (st == HL_OK && hipEventCreateWithFlags(e, hipEventDisableTiming) != hipSuccess) st = HL_ERR_HIP;
+    // ordering between streams of this device: a device-scope release suffices
+    if (st == HL_OK && hipEventCreateWithFlags(e, hipEventDisableTiming | hipEventReleaseToDevice) != hipSuccess)
+      st = HL_ERR_HIP;
   }
   if (st == HL_OK && hipMalloc(&p->flags, PF_N * sizeof(uint32_t)) != hipSuccess) st = HL_ERR_HIP;
   if (st == HL_OK && hipMemset(p->flags, 0, PF_N * sizeof(uint32_t)) != hipSuccess) st = HL_ERR_HIP;

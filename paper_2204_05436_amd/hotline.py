@@ -74,6 +74,7 @@ _SIGS = {
     "hl_last_device_error": (C.c_int, [P, C.POINTER(U32)]),
     "hl_trace_enable": (C.c_int, [P, I32]),
     "hl_trace_count": (I32, [P]),
+    "hl_trace_only": (C.c_int, [P, C.c_char_p]),
     "hl_trace_read": (C.c_int, [P, I32, C.POINTER(C.c_char_p), C.POINTER(C.c_float)]),
     "hl_trace_reset": (C.c_int, [P]),
     "hl_host_alloc": (C.c_int, [SZ, C.POINTER(P), C.POINTER(P)]),
@@ -322,6 +323,10 @@ def hl_last_device_error(h):
 
 def hl_trace_enable(h, cap):
     _ck("hl_trace_enable", lib().hl_trace_enable(h.ptr, int(cap)))
+
+
+def hl_trace_only(h, name=None):
+    _ck("hl_trace_only", lib().hl_trace_only(h.ptr, None if name is None else name.encode()))
 
 
 def hl_trace_count(h):
