@@ -3,13 +3,14 @@
 // A sort of `bits` bits takes P = ceil(bits / 11) passes of b = ceil(bits / P)
 // bits (two passes of 10 bits for the backward's 20-bit keys).  One histogram
 // kernel counts every digit position in a single read of the keys (per-block
-// counts; each pass block adds up the few it needs) and clears the first
-// pass's look-back status.  Then one kernel per digit: a block takes the next
-// tile (dynamic tile ids, so every lower tile is already running), ranks its
-// items by digit with per-wave LDS counters (the counters' totals are the
-// tile's digit counts), publishes the counts, obtains those of
-// all earlier tiles by decoupled look-back, reorders the tile in LDS so that
-// each digit's run is contiguous and writes it out.  Each pass block also
+// counts) and clears the first pass's look-back status.  Then one kernel per
+// digit: a block takes the next tile (dynamic tile ids, so every lower tile is
+// already running), ranks its items by digit with per-wave LDS counters (the
+// counters' totals are the tile's digit counts), publishes the counts, obtains
+// those of all earlier tiles by decoupled look-back, reorders the tile in LDS
+// so that each digit's run is contiguous and writes it out.  Only tile 0 adds
+// up the histogram: its published prefix starts from each digit's global
+// offset, so the look-back hands the offsets to every later tile.  Each pass block also
 // clears its tile's status words for the next pass.  Item order inside a tile
 // is wave-major, then item, then lane, which is index order, so the sort is
 // stable.
@@ -138,6 +139,7 @@ srt_pass(const uint32_t* __restrict__ kin, const uint32_t* __restrict__ vin, uin
   // (NB x tiles^2 / 2 loads when no inclusive prefix is found early), so the
   // window stays short and the walk stops at the first inclusive prefix
   constexpr int WIN = PER >= 4 ? 8 : 16;
+  constexpr int WIN0 = 4;
   __shared__ uint32_t s_tile;
   __shared__ uint32_t wcnt[HL_SORT_WAVES][NB];
   __shared__ uint32_t tdex[NB], gbase[NB];
@@ -162,17 +164,20 @@ srt_pass(const uint32_t* __restrict__ kin, const uint32_t* __restrict__ vin, uin
     key[k] = ok ? kin[idx] : 0xFFFFFFFFu;
     val[k] = ok ? vin[idx] : 0u;
   }
-  // global counts of the owned digits (loads issued together)
+  // global counts of the owned digits (loads issued together), read by tile 0
+  // only: its published prefix carries the digits' global offsets, so every
+  // later tile obtains them through the look-back
   const int d0 = tid * PER;
   const bool owner = tid < OWNERS;
   uint32_t dtot[PER];
   {
+    const uint32_t np = tile == 0 ? n_part : 0u;
     uint32_t pv[PER][HL_SORT_HIST_BLOCKS];
 #pragma unroll
     for (int j = 0; j < PER; ++j)
 #pragma unroll
       for (int q = 0; q < HL_SORT_HIST_BLOCKS; ++q)
-        pv[j][q] = (owner && (uint32_t)q < n_part) ? part[(size_t)q * NB + d0 + j] : 0u;
+        pv[j][q] = (owner && (uint32_t)q < np) ? part[(size_t)q * NB + d0 + j] : 0u;
 #pragma unroll
     for (int j = 0; j < PER; ++j) {
       dtot[j] = 0;
@@ -208,12 +213,16 @@ srt_pass(const uint32_t* __restrict__ kin, const uint32_t* __restrict__ vin, uin
       }
     tc[j] = run;
     tx[j] = run;
-    if (owner) srt_st_store(st + (size_t)tile * NB + d0 + j, (tile == 0 ? SRT_PRE : SRT_AGG) | run);
+    if (owner && tile > 0) srt_st_store(st + (size_t)tile * NB + d0 + j, SRT_AGG | run);
   }
   uint32_t gx[PER];
 #pragma unroll
   for (int j = 0; j < PER; ++j) gx[j] = dtot[j];
   srt_scan2<NB, PER>(tx, gx, scan_ws);
+  // tile 0: inclusive prefix = the digit's global offset + its own count
+  if (owner && tile == 0)
+#pragma unroll
+    for (int j = 0; j < PER; ++j) srt_st_store(st + d0 + j, SRT_PRE | (gx[j] + tc[j]));
   // decoupled look-back: counts of this digit in all earlier tiles
   uint32_t excl[PER];
   int64_t jj[PER];
@@ -223,13 +232,16 @@ srt_pass(const uint32_t* __restrict__ kin, const uint32_t* __restrict__ vin, uin
     jj[j] = owner ? (int64_t)tile - 1 : -1;
   }
   uint32_t spins = 0;
+  // the first window is short: the nearest tiles have most likely published
+  // their inclusive prefix by then, and each word read costs bandwidth
+  int win = WIN0;
   while (true) {
     uint32_t wv[PER][WIN];
 #pragma unroll
     for (int j = 0; j < PER; ++j)
 #pragma unroll
       for (int q = 0; q < WIN; ++q)
-        wv[j][q] = jj[j] - q >= 0 ? srt_st_load(st + (size_t)(jj[j] - q) * NB + d0 + j) : SRT_PRE;
+        wv[j][q] = q < win && jj[j] - q >= 0 ? srt_st_load(st + (size_t)(jj[j] - q) * NB + d0 + j) : SRT_PRE;
     bool any = false, stall = false;
 #pragma unroll
     for (int j = 0; j < PER; ++j) {
@@ -239,6 +251,10 @@ srt_pass(const uint32_t* __restrict__ kin, const uint32_t* __restrict__ vin, uin
 #pragma unroll
       for (int q = 0; q < WIN; ++q) {
         if (stop) continue;
+        if (q >= win) {  // beyond this round's window
+          stop = true;
+          continue;
+        }
         const uint32_t x = wv[j][q];
         if ((x & (SRT_AGG | SRT_PRE)) == 0) {  // not yet published
           stop = true;
@@ -257,6 +273,7 @@ srt_pass(const uint32_t* __restrict__ kin, const uint32_t* __restrict__ vin, uin
       any |= jj[j] >= 0;
     }
     if (!any) break;
+    win = WIN;
     if (stall) {
       if (++spins > HL_SPIN_LIMIT) {
         hl_flag(err, HL_DEVERR_STALL);
@@ -270,7 +287,7 @@ srt_pass(const uint32_t* __restrict__ kin, const uint32_t* __restrict__ vin, uin
     for (int j = 0; j < PER; ++j) {
       if (tile > 0) srt_st_store(st + (size_t)tile * NB + d0 + j, SRT_PRE | (excl[j] + tc[j]));
       tdex[d0 + j] = tx[j];
-      gbase[d0 + j] = gx[j] + excl[j];
+      gbase[d0 + j] = tile == 0 ? gx[j] : excl[j];
     }
   }
   __syncthreads();
