@@ -58,6 +58,7 @@ def kernel_bytes(name, st):
         # grouping: keys and bags out, a histogram read, two passes of keys and bags in and out
         "bw_prep": 4 * L + 4 * (nb + 1) + 8 * L,
         "srt_hist": 4 * L,
+        "bw_prep_hist": 4 * L + 4 * (nb + 1) + 8 * L,
         "srt_pass": 16 * L,
         # hot half of the forward over every bag: codes, offsets, each referenced row once, outputs
         "eb_fwd_hot": 4 * L + 4 * (nb + 1) + (U - C) * R + nb * O,
@@ -261,7 +262,7 @@ def main():
 
     # the embedding forward and backward: their kernels' time per step (the
     # grouping included), against the algorithmic bytes of both passes
-    fb_kernels = ("eb_fwd_hot", "eb_fwd_tail", "bw_prep", "srt_hist", "srt_pass", "bw_reduce1", "bw_reduce2",
+    fb_kernels = ("eb_fwd_hot", "eb_fwd_tail", "bw_prep", "bw_prep_hist", "srt_hist", "srt_pass", "bw_reduce1", "bw_reduce2",
                   "bw_cold")
     t_fb = sum(kernels[n]["ms_per_step"] for n in fb_kernels if n in kernels)
     fwd_b = 4 * avg["L"] + 4 * (avg["n_bags"] + 1) + avg["U"] * avg["R"] + avg["n_bags"] * avg["O"]

@@ -357,7 +357,45 @@ __global__ void bw_mask(uint8_t* mask, int32_t n_samples, const int32_t* __restr
 
 // (compressed key, bag) for every lookup of the mini-batch; lookups of
 // unselected samples and invalid codes get the sentinel key (sorted last,
-// ignored).
+// ignored), and so do positions outside [bag_ptr[0], bag_ptr[n_bags]) (only if
+// bag_ptr disagrees with n_lookups; bag_ptr is non-decreasing).
+__device__ __forceinline__ uint32_t bw_key(uint32_t c, uint32_t n_hot, uint32_t k_cap, int32_t stg_rows) {
+  if (c < n_hot) return c;
+  if (c >= k_cap && c - k_cap < (uint32_t)stg_rows) return n_hot + (c - k_cap);
+  return EB_SENT;
+}
+
+// the lookup positions no bag covers: [0, bag_ptr[0]) and [bag_ptr[n_bags], n)
+__device__ __forceinline__ void bw_uncovered(const int32_t* bag_ptr, int64_t n_bags, int64_t n_lookups,
+                                             int64_t* first, int64_t* covered) {
+  *first = min((int64_t)max(bag_ptr[0], 0), n_lookups);
+  *covered = max(min((int64_t)max(bag_ptr[n_bags], 0), n_lookups), *first);
+}
+
+// the bags [b0, b0 + nb) of one block: off[] holds their offsets
+template <int NT>
+__device__ __forceinline__ void bw_prep_bags(const int32_t* __restrict__ codes, const int32_t* off, int64_t b0,
+                                             int nb, int32_t bps, const uint8_t* __restrict__ mask, uint32_t n_hot,
+                                             uint32_t k_cap, int32_t stg_rows, uint32_t* __restrict__ keys,
+                                             uint32_t* __restrict__ vals, int64_t n_lookups, uint32_t* err) {
+  const int32_t lo = off[0], hi = min((int64_t)off[nb], n_lookups);
+  for (int32_t i = lo + threadIdx.x; i < hi; i += NT) {
+    int a = 0, b = nb;
+    while (b - a > 1) {
+      int m = (a + b) >> 1;
+      if (off[m] <= i) a = m; else b = m;
+    }
+    const int64_t bag = b0 + a;
+    uint32_t key = EB_SENT;
+    if (!mask || mask[bag / bps]) {
+      key = bw_key((uint32_t)codes[i], n_hot, k_cap, stg_rows);
+      if (key == EB_SENT) hl_flag(err, HL_DEVERR_BAD_CODE);
+    }
+    keys[i] = key;
+    vals[i] = (uint32_t)bag;
+  }
+}
+
 #define BP_BAGS 256
 __global__ void __launch_bounds__(256)
 bw_prep(const int32_t* __restrict__ codes, const int32_t* __restrict__ bag_ptr, int64_t n_bags, int32_t bps,
@@ -369,29 +407,68 @@ bw_prep(const int32_t* __restrict__ codes, const int32_t* __restrict__ bag_ptr, 
   for (int j = threadIdx.x; j <= nb; j += blockDim.x) off[j] = bag_ptr[b0 + j];
   if (blockIdx.x == 0 && threadIdx.x == 0 && bag_ptr[n_bags] != n_lookups) hl_flag(err, HL_DEVERR_SHAPE);
   __syncthreads();
-  // positions the bags do not cover (only if bag_ptr disagrees with n_lookups) get the sentinel
-  const int64_t covered = min((int64_t)max(bag_ptr[n_bags], 0), n_lookups);
-  for (int64_t i = covered + (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n_lookups;
-       i += (int64_t)gridDim.x * blockDim.x)
-    keys[i] = EB_SENT;
-  const int32_t lo = off[0], hi = min((int64_t)off[nb], n_lookups);
-  for (int32_t i = lo + threadIdx.x; i < hi; i += blockDim.x) {
-    int a = 0, b = nb;
-    while (b - a > 1) {
-      int m = (a + b) >> 1;
-      if (off[m] <= i) a = m; else b = m;
+  int64_t first, covered;
+  bw_uncovered(bag_ptr, n_bags, n_lookups, &first, &covered);
+  const int64_t gs = (int64_t)gridDim.x * blockDim.x, t0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  for (int64_t i = t0; i < first; i += gs) keys[i] = EB_SENT;
+  for (int64_t i = covered + t0; i < n_lookups; i += gs) keys[i] = EB_SENT;
+  bw_prep_bags<256>(codes, off, b0, nb, bps, mask, n_hot, k_cap, stg_rows, keys, vals, n_lookups, err);
+}
+
+// bw_prep and the sort's digit histogram in one launch (no sample selection):
+// blocks [0, hb) count the digits of every key, taking the keys from the codes
+// by the same rule as the writers, and clear the first pass's status words;
+// the other blocks write the (key, bag) pairs, BPH_BAGS bags each.
+#define BPH_THREADS 1024
+#define BPH_BAGS 1024
+template <int NB>
+__global__ void __launch_bounds__(BPH_THREADS)
+bw_prep_hist(const int32_t* __restrict__ codes, const int32_t* __restrict__ bag_ptr, int64_t n_bags, int32_t bps,
+             uint32_t n_hot, uint32_t k_cap, int32_t stg_rows, uint32_t* __restrict__ keys,
+             uint32_t* __restrict__ vals, int64_t n_lookups, uint32_t hb, int passes, int b,
+             uint32_t* __restrict__ part, uint32_t* __restrict__ zero, uint64_t n_zero, uint32_t* err) {
+  __shared__ uint32_t hst[HL_SORT_MAXPASS][NB];
+  __shared__ int32_t off[BPH_BAGS + 1];
+  int64_t first, covered;
+  bw_uncovered(bag_ptr, n_bags, n_lookups, &first, &covered);
+  if (blockIdx.x < hb) {
+    const uint32_t gs = hb * BPH_THREADS;
+    for (uint64_t i = (uint64_t)blockIdx.x * BPH_THREADS + threadIdx.x; i < n_zero; i += gs) zero[i] = 0;
+    for (int j = threadIdx.x; j < HL_SORT_MAXPASS * NB; j += BPH_THREADS) (&hst[0][0])[j] = 0;
+    __syncthreads();
+    const uint32_t mask = (1u << b) - 1u;
+    const uint32_t n = (uint32_t)n_lookups;
+    for (uint32_t i0 = blockIdx.x * BPH_THREADS + threadIdx.x; i0 < n; i0 += 8 * gs) {
+      uint32_t k[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const uint32_t i = i0 + u * gs;
+        k[u] = i < n ? (uint32_t)codes[i] : 0u;
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const uint32_t i = i0 + u * gs;
+        if (i >= n) continue;
+        const uint32_t key = (int64_t)i < first || (int64_t)i >= covered ? EB_SENT : bw_key(k[u], n_hot, k_cap, stg_rows);
+        for (int p = 0; p < passes; ++p) atomicAdd(&hst[p][(key >> (b * p)) & mask], 1u);
+      }
     }
-    const int64_t bag = b0 + a;
-    uint32_t key = EB_SENT;
-    if (!mask || mask[bag / bps]) {
-      const uint32_t c = (uint32_t)codes[i];
-      if (c < n_hot) key = c;
-      else if (c >= k_cap && c - k_cap < (uint32_t)stg_rows) key = n_hot + (c - k_cap);
-      else hl_flag(err, HL_DEVERR_BAD_CODE);
-    }
-    keys[i] = key;
-    vals[i] = (uint32_t)bag;
+    __syncthreads();
+    for (int p = 0; p < passes; ++p)
+      for (int j = threadIdx.x; j < NB; j += BPH_THREADS)
+        part[((size_t)p * HL_SORT_HIST_BLOCKS + blockIdx.x) * NB + j] = hst[p][j];
+    return;
   }
+  const uint32_t blk = blockIdx.x - hb;
+  const int64_t b0 = (int64_t)blk * BPH_BAGS;
+  const int nb = (int)min((int64_t)BPH_BAGS, n_bags - b0);
+  for (int j = threadIdx.x; j <= nb; j += BPH_THREADS) off[j] = bag_ptr[b0 + j];
+  if (blk == 0 && threadIdx.x == 0 && bag_ptr[n_bags] != n_lookups) hl_flag(err, HL_DEVERR_SHAPE);
+  __syncthreads();
+  const int64_t gs = (int64_t)(gridDim.x - hb) * BPH_THREADS, t0 = (int64_t)blk * BPH_THREADS + threadIdx.x;
+  for (int64_t i = t0; i < first; i += gs) keys[i] = EB_SENT;
+  for (int64_t i = covered + t0; i < n_lookups; i += gs) keys[i] = EB_SENT;
+  bw_prep_bags<BPH_THREADS>(codes, off, b0, nb, bps, nullptr, n_hot, k_cap, stg_rows, keys, vals, n_lookups, err);
 }
 
 template <int VEC, bool BF>
@@ -914,11 +991,28 @@ extern "C" hl_status hl_embbag_bwd_plan(hl_handle* h, int32_t stg_rows, const in
     HL_KERNEL(h, s, "bw_mask", bw_mask, dim3(gb), dim3(256), 0, s, ws.mask, n_samples, sample_ids, n_sel_dev, n_sel_max, 1);
     mask = ws.mask;
   }
-  HL_KERNEL(h, s, "bw_prep", bw_prep, dim3(hl_div_up(n_bags, BP_BAGS)), dim3(256), 0, s, codes, bag_ptr, n_bags, bps, mask,
-                     h->n_hot, h->k_cap, stg_rows, ws.sort.k0, ws.sort.v0, n_lookups, h->d_err);
-  HL_LAUNCHED();
   uint32_t *sk, *sv;
-  st = hl_sort_pairs(h, ws.sort, nullptr, (uint32_t)n_lookups, bw_key_bits(h, stg_rows), s, &sk, &sv);
+  const int bits = bw_key_bits(h, stg_rows);
+  if (mask) {
+    HL_KERNEL(h, s, "bw_prep", bw_prep, dim3(hl_div_up(n_bags, BP_BAGS)), dim3(256), 0, s, codes, bag_ptr, n_bags,
+              bps, mask, h->n_hot, h->k_cap, stg_rows, ws.sort.k0, ws.sort.v0, n_lookups, h->d_err);
+    HL_LAUNCHED();
+    st = hl_sort_pairs(h, ws.sort, nullptr, (uint32_t)n_lookups, bits, s, &sk, &sv);
+  } else {
+    if ((uint64_t)n_lookups > ws.sort.n_max) return HL_ERR_CAPACITY;
+    const hl_sort_geom sg = hl_sort_geometry((uint32_t)n_lookups, bits);
+    const dim3 grid(sg.hist_blocks + (uint32_t)hl_div_up(n_bags, BPH_BAGS));
+#define BPH(NB)                                                                                                  \
+  HL_KERNEL(h, s, "bw_prep_hist", bw_prep_hist<NB>, grid, dim3(BPH_THREADS), 0, s, codes, bag_ptr, n_bags, bps, h->n_hot, \
+            h->k_cap, stg_rows, ws.sort.k0, ws.sort.v0, n_lookups, sg.hist_blocks, sg.passes, sg.b, ws.sort.part,   \
+            ws.sort.st[0], sg.n_zero, h->d_err)
+    if (sg.nb == 256) BPH(256);
+    else if (sg.nb == 1024) BPH(1024);
+    else BPH(2048);
+#undef BPH
+    HL_LAUNCHED();
+    st = hl_sort_passes(h, ws.sort, nullptr, (uint32_t)n_lookups, bits, s, &sk, &sv);
+  }
   if (st != HL_OK) return st;
   hl_ws_note(h, workspace, HL_WSK_BWD_PLAN, n_lookups, n_bags, stg_rows);
   return HL_OK;

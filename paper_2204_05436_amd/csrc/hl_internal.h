@@ -207,6 +207,22 @@ hl_status hl_sort_pairs(hl_handle* h, hl_sort_ws& ws, const uint32_t* n_dev, uin
 // The buffers hl_sort_pairs leaves its result in for a sort of `bits` bits
 // with n_host > 0.
 void hl_sort_result(const hl_sort_ws& ws, int bits, uint32_t** out_k, uint32_t** out_v);
+// A producer of the keys may count their digits itself (in the same launch
+// that writes them) and then run only the digit passes.  Geometry of a sort
+// of n_host items and `bits` bits: `passes` digits of `b` bits, nb bins,
+// hist_blocks partial counts per pass (ws.part[(p * HL_SORT_HIST_BLOCKS +
+// block) * nb + digit], digit p = (key >> (b * p)) & (nb - 1)), and the first
+// pass's status words ws.st[0][0 .. n_zero) to clear.
+struct hl_sort_geom {
+  int passes, b, nb;
+  uint32_t hist_blocks;
+  uint64_t n_zero;
+};
+hl_sort_geom hl_sort_geometry(uint32_t n_host, int bits);
+// The digit passes of hl_sort_pairs, once the counts and the cleared status
+// words are in place (hl_sort_geometry); same contract otherwise.
+hl_status hl_sort_passes(hl_handle* h, hl_sort_ws& ws, const uint32_t* n_dev, uint32_t n_host, int bits,
+                         hipStream_t s, uint32_t** out_k, uint32_t** out_v);
 
 // Decoupled look-back helpers (epoch-tagged 64-bit status words).  A status
 // word carries its own value, so relaxed agent-scope atomics suffice: no other

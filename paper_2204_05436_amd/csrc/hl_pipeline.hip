@@ -21,6 +21,8 @@
 // the flag reaches that number (a bounded wait: past the limit it sets
 // HL_DEVERR_STALL and returns).  A handover costs two small kernels (~3 us
 // each) instead of an event dependency between streams (~17 us measured).
+// Handovers that meet at one point of a stream share one launch (pl_hand): the
+// fetch's two waits, and a plan's grouping signal with the next plan's waits.
 // Flags need streams that progress independently: a stream with a compute-unit
 // mask has a hardware queue of its own.  Without masks (fetch_cus = 0) streams
 // may share a hardware queue, where a wait ahead of its signal would stall, so
@@ -71,6 +73,28 @@ __global__ void pl_wait(const uint32_t* flag, uint32_t v, uint32_t* err) {
   }
 }
 
+// Several handovers of one stream at one point in a single launch: the
+// signal (if any), then each wait in turn.  The signal tells that the kernels
+// before it on the stream are complete, as a separate pl_signal would.
+__global__ void pl_hand(uint32_t* sflag, uint32_t sv, const uint32_t* w1, uint32_t v1, const uint32_t* w2,
+                        uint32_t v2, uint32_t* err) {
+  if (threadIdx.x != 0) return;
+  if (sflag) __hip_atomic_store(sflag, sv, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+  const uint32_t* wf[2] = {w1, w2};
+  const uint32_t wv[2] = {v1, v2};
+  for (int k = 0; k < 2; ++k) {
+    if (!wf[k]) continue;
+    uint32_t spins = 0;
+    while ((int32_t)(__hip_atomic_load(wf[k], __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT) - wv[k]) < 0) {
+      if (++spins > HL_SPIN_LIMIT) {
+        hl_flag(err, HL_DEVERR_STALL);
+        return;
+      }
+      __builtin_amdgcn_s_sleep(8);
+    }
+  }
+}
+
 struct pl_plan {
   hl_step_io io;      // the inputs and per-step buffers it ran with
   uint32_t seq;       // its PF_LOOK value
@@ -94,11 +118,15 @@ struct hl_pipeline {
   const void* stg_ptr[4]; // staging buffers of recent steps, and the last step that used each
   uint32_t stg_seq[4];
   int stg_next;
+  bool sort_pend;         // the last plan's grouping signal (value sort_v) is not enqueued yet: it
+  uint32_t sort_v;        // rides on the next plan's first wait, or is enqueued alone when awaited
 };
+
+static hl_status pl_flush(hl_pipeline* p);
 
 extern "C" hl_status hl_pipeline_destroy(hl_pipeline* p) {
   if (!p) return HL_ERR_INVALID_ARG;
-  hl_status st = HL_OK;
+  hl_status st = pl_flush(p);
   if (hipDeviceSynchronize() != hipSuccess) st = HL_ERR_HIP;
   for (hipEvent_t e : p->ev)
     if (e && hipEventDestroy(e) != hipSuccess) st = HL_ERR_HIP;
@@ -175,6 +203,21 @@ static hl_status pl_wt(hl_pipeline* p, hipStream_t s, int f, uint32_t v) {
   if (!p->use_flags) return hipStreamWaitEvent(s, p->ev[f], 0) == hipSuccess ? HL_OK : HL_ERR_HIP;
   hipLaunchKernelGGL(pl_wait, dim3(1), dim3(64), 0, s, p->flags + f, v, p->h->d_err);
   return hipGetLastError() == hipSuccess ? HL_OK : HL_ERR_HIP;
+}
+
+// flag mode: stream s signals flag sf = sv (sf < 0: none), then waits for
+// flags w1 >= v1 and w2 >= v2 (w < 0: none), in one launch
+static hl_status pl_hw(hl_pipeline* p, hipStream_t s, int sf, uint32_t sv, int w1, uint32_t v1, int w2, uint32_t v2) {
+  if (sf < 0 && w1 < 0 && w2 < 0) return HL_OK;
+  hipLaunchKernelGGL(pl_hand, dim3(1), dim3(64), 0, s, sf >= 0 ? p->flags + sf : nullptr, sv,
+                     w1 >= 0 ? p->flags + w1 : nullptr, v1, w2 >= 0 ? p->flags + w2 : nullptr, v2, p->h->d_err);
+  return hipGetLastError() == hipSuccess ? HL_OK : HL_ERR_HIP;
+}
+// the pending grouping signal, enqueued alone
+static hl_status pl_flush(hl_pipeline* p) {
+  if (!p->sort_pend) return HL_OK;
+  p->sort_pend = false;
+  return pl_sig(p, p->plan, PF_SORT, p->sort_v);
 }
 
 static hl_status pl_group(hl_pipeline* p) {
@@ -260,10 +303,13 @@ extern "C" hl_status hl_pipeline_plan(hl_pipeline* p, const hl_step_io* io, hl_s
     HL_HIPTRY(hipStreamWaitEvent(P, p->ev_pin, 0));
   }
   // every step enqueued so far has finished with its per-step buffers and
-  // workspace (and with the cold-gather hash table, which plans share)
-  if (p->seq) HL_TRY(pl_wt(p, P, PF_DONE, p->seq));
+  // workspace (and with the cold-gather hash table, which plans share); the
+  // previous plan's grouping signal goes in the same launch
   const int wb = pl_wb_slot(p, io->cold_ids);
-  if (wb >= 0) HL_TRY(pl_wt(p, P, PF_WB + wb, p->wb_seq[wb]));
+  const bool sp = p->sort_pend;
+  p->sort_pend = false;
+  HL_TRY(pl_hw(p, P, sp ? PF_SORT : -1, p->sort_v, p->seq ? PF_DONE : -1, p->seq, wb >= 0 ? PF_WB + wb : -1,
+               wb >= 0 ? p->wb_seq[wb] : 0));
   const int32_t B = io->n_samples, bps = io->bags_per_sample;
   HL_TRY(hl_dispatch(h, io->rows, io->bag_ptr, B, bps, io->n_lookups, io->gids, io->codes, io->flags, io->pop_ids,
                      io->nonpop_ids, io->counts, io->workspace, io->ws_bytes, PS));
@@ -276,7 +322,8 @@ extern "C" hl_status hl_pipeline_plan(hl_pipeline* p, const hl_step_io* io, hl_s
   if (io->dY)
     HL_TRY(hl_embbag_bwd_plan(h, io->staging_cap, io->codes, io->bag_ptr, B, bps, io->n_lookups, nullptr, nullptr, B,
                               io->workspace, io->ws_bytes, PS));
-  HL_TRY(pl_sig(p, P, PF_SORT, v));
+  p->sort_pend = true;
+  p->sort_v = v;
   e->io = *io;
   e->seq = v;
   e->pending = true;
@@ -309,14 +356,14 @@ extern "C" hl_status hl_pipeline_step(hl_pipeline* p, const hl_step_io* io, hl_s
     // copy, once the last step that used these staging rows has ended (a
     // write-back of the previous step precedes it on the fetch stream).  With
     // two staging buffers alternating, the copy overlaps the previous step.
-    HL_TRY(pl_wt(p, f, PF_LOOK, e->seq));
     const uint32_t last = pl_stg_last(p, io->staging);
-    if (last) HL_TRY(pl_wt(p, f, PF_DONE, last));
+    HL_TRY(pl_hw(p, f, -1, 0, PF_LOOK, e->seq, last ? PF_DONE : -1, last));
     HL_TRY(hl_cold_fetch(h, io->cold_ids, io->n_cold, cap, io->w_host, io->staging, F));
     HL_TRY(pl_sig(p, f, PF_FETCH, q));
     HL_TRY(pl_wt(p, m, PF_LOOK, e->seq));
     HL_TRY(pl_fwd_hot(h, io, M));
     if (io->dY) {
+      if (p->sort_pend && p->sort_v == e->seq) HL_TRY(pl_flush(p));
       HL_TRY(pl_wt(p, m, PF_SORT, e->seq));
       HL_TRY(hl_embbag_bwd_apply_part(h, io->w_hot, io->staging, cap, B, bps, L, io->dY, io->lr, 1, io->workspace,
                                       io->ws_bytes, M));
@@ -416,6 +463,7 @@ extern "C" hl_status hl_pipeline_streams(const hl_pipeline* p, hl_stream* main, 
 
 extern "C" hl_status hl_pipeline_sync(hl_pipeline* p, hl_stream stream) {
   if (!p) return HL_ERR_INVALID_ARG;
+  HL_TRY(pl_flush(p));
   hipStream_t c = (hipStream_t)stream;
   // events recorded now, behind everything enqueued on each stream
   HL_HIPTRY(hipEventRecord(p->ev_out, p->main));

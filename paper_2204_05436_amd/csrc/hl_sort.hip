@@ -318,19 +318,38 @@ void hl_sort_result(const hl_sort_ws& ws, int bits, uint32_t** out_k, uint32_t**
   *out_v = odd ? ws.v1 : ws.v0;
 }
 
+hl_sort_geom hl_sort_geometry(uint32_t n_host, int bits) {
+  const srt_plan pl = srt_make_plan(bits);
+  hl_sort_geom g;
+  g.passes = pl.passes;
+  g.b = pl.b;
+  g.nb = pl.nb;
+  const uint32_t hb = hl_div_up(n_host, HL_SORT_HIST_THREADS * 8);
+  g.hist_blocks = hb < 1 ? 1 : (hb > HL_SORT_HIST_BLOCKS ? HL_SORT_HIST_BLOCKS : hb);
+  g.n_zero = (uint64_t)hl_div_up(n_host, HL_SORT_TILE) * pl.nb;
+  return g;
+}
+
 template <int NB>
-static hl_status srt_launch(hl_handle* h, hl_sort_ws& ws, const uint32_t* n_dev, uint32_t n_host, srt_plan pl,
+static hl_status srt_hist_launch(hl_handle* h, hl_sort_ws& ws, const uint32_t* n_dev, uint32_t n_host, int bits,
+                                 hipStream_t s) {
+  const hl_sort_geom g = hl_sort_geometry(n_host, bits);
+  HL_KERNEL(h, s, "srt_hist", srt_hist<NB>, dim3(g.hist_blocks), dim3(HL_SORT_HIST_THREADS), 0, s, ws.k0, n_dev,
+            n_host, g.passes, g.b, ws.part, ws.st[0], g.n_zero);
+  HL_LAUNCHED();
+  return HL_OK;
+}
+
+template <int NB>
+static hl_status srt_launch(hl_handle* h, hl_sort_ws& ws, const uint32_t* n_dev, uint32_t n_host, int bits,
                             hipStream_t s) {
   const uint32_t tiles = hl_div_up(n_host, HL_SORT_TILE);
-  uint32_t hb = hl_div_up(n_host, HL_SORT_HIST_THREADS * 8);
-  hb = hb < 1 ? 1 : (hb > HL_SORT_HIST_BLOCKS ? HL_SORT_HIST_BLOCKS : hb);
-  HL_KERNEL(h, s, "srt_hist", srt_hist<NB>, dim3(hb), dim3(HL_SORT_HIST_THREADS), 0, s, ws.k0, n_dev, n_host,
-            pl.passes, pl.b, ws.part, ws.st[0], (uint64_t)tiles * NB);
+  const hl_sort_geom g = hl_sort_geometry(n_host, bits);
   uint32_t *ki = ws.k0, *vi = ws.v0, *ko = ws.k1, *vo = ws.v1;
-  for (int p = 0; p < pl.passes; ++p) {
+  for (int p = 0; p < g.passes; ++p) {
     HL_KERNEL(h, s, "srt_pass", srt_pass<NB>, dim3(tiles), dim3(HL_SORT_THREADS), 0, s, ki, vi, ko, vo, n_dev,
-              n_host, pl.b * p, pl.b, ws.part + (size_t)p * HL_SORT_HIST_BLOCKS * NB, hb, ws.st[p & 1],
-              p + 1 < pl.passes ? ws.st[(p + 1) & 1] : nullptr, ws.ctr + 1 + p, h->d_err);
+              n_host, g.b * p, g.b, ws.part + (size_t)p * HL_SORT_HIST_BLOCKS * NB, g.hist_blocks, ws.st[p & 1],
+              p + 1 < g.passes ? ws.st[(p + 1) & 1] : nullptr, ws.ctr + 1 + p, h->d_err);
     uint32_t* t = ki;
     ki = ko;
     ko = t;
@@ -342,19 +361,39 @@ static hl_status srt_launch(hl_handle* h, hl_sort_ws& ws, const uint32_t* n_dev,
   return HL_OK;
 }
 
+static hl_status srt_check(const hl_sort_ws& ws, uint32_t n_host, int bits) {
+  if (n_host > ws.n_max || n_host >= (1u << 30)) return HL_ERR_CAPACITY;
+  if (bits > 32) return HL_ERR_UNSUPPORTED;
+  return HL_OK;
+}
+
+hl_status hl_sort_passes(hl_handle* h, hl_sort_ws& ws, const uint32_t* n_dev, uint32_t n_host, int bits,
+                         hipStream_t s, uint32_t** out_k, uint32_t** out_v) {
+  *out_k = ws.k0;
+  *out_v = ws.v0;
+  if (n_host == 0) return HL_OK;
+  hl_status st = srt_check(ws, n_host, bits);
+  if (st != HL_OK) return st;
+  const srt_plan pl = srt_make_plan(bits);
+  if (pl.nb == 256) st = srt_launch<256>(h, ws, n_dev, n_host, bits, s);
+  else if (pl.nb == 1024) st = srt_launch<1024>(h, ws, n_dev, n_host, bits, s);
+  else st = srt_launch<2048>(h, ws, n_dev, n_host, bits, s);
+  if (st != HL_OK) return st;
+  hl_sort_result(ws, bits, out_k, out_v);
+  return HL_OK;
+}
+
 hl_status hl_sort_pairs(hl_handle* h, hl_sort_ws& ws, const uint32_t* n_dev, uint32_t n_host, int bits,
                         hipStream_t s, uint32_t** out_k, uint32_t** out_v) {
   *out_k = ws.k0;
   *out_v = ws.v0;
   if (n_host == 0) return HL_OK;
-  if (n_host > ws.n_max || n_host >= (1u << 30)) return HL_ERR_CAPACITY;
-  if (bits > 32) return HL_ERR_UNSUPPORTED;
-  const srt_plan pl = srt_make_plan(bits);
-  hl_status st;
-  if (pl.nb == 256) st = srt_launch<256>(h, ws, n_dev, n_host, pl, s);
-  else if (pl.nb == 1024) st = srt_launch<1024>(h, ws, n_dev, n_host, pl, s);
-  else st = srt_launch<2048>(h, ws, n_dev, n_host, pl, s);
+  hl_status st = srt_check(ws, n_host, bits);
   if (st != HL_OK) return st;
-  hl_sort_result(ws, bits, out_k, out_v);
-  return HL_OK;
+  const srt_plan pl = srt_make_plan(bits);
+  if (pl.nb == 256) st = srt_hist_launch<256>(h, ws, n_dev, n_host, bits, s);
+  else if (pl.nb == 1024) st = srt_hist_launch<1024>(h, ws, n_dev, n_host, bits, s);
+  else st = srt_hist_launch<2048>(h, ws, n_dev, n_host, bits, s);
+  if (st != HL_OK) return st;
+  return hl_sort_passes(h, ws, n_dev, n_host, bits, s, out_k, out_v);
 }
