@@ -393,11 +393,15 @@ hl_status hl_pipeline_step(hl_pipeline* p, const hl_step_io* io, hl_stream strea
  * hl_embbag_bwd_plan of io's mini-batch on a fourth stream of the pipeline, to
  * be consumed by a later hl_pipeline_step with HL_STEP_PLANNED and the same io
  * (dY NULL or not alike).  The plan waits for every step enqueued before it
- * (it rewrites per-step buffers and the workspace, and shares the cold-gather
- * hash table with them) and for the write-back that last read its cold_ids, so
- * one step ahead needs two sets of per-step buffers, alternated; the planned
- * step's row fetch still waits for the previous step to end, and its forwards
- * and backward run on one stream.  lr, w_host, w_hot, staging, out and
+ * that used one of its per-step buffers (gids, codes, flags, pop_ids,
+ * nonpop_ids, counts, cold_ids, n_cold) or its workspace, which it rewrites,
+ * for every step enqueued before it that ran its own dispatch (the cold-gather
+ * hash table is shared), and for the write-back that last read its cold_ids;
+ * one step ahead thus needs two sets of per-step buffers, alternated, and
+ * enqueuing a step before the plan of the batch after it lets the plan run
+ * beside that step.  The planned step's row fetch still waits for the last
+ * step that used its staging rows to end, and its forwards and backward run on
+ * one stream.  lr, w_host, w_hot, staging, out and
  * write_back are not read.  HL_STEP_UNTIED in io->step_flags: no wait for
  * `stream` first.  HL_ERR_INVALID_ARG: a plan on the same workspace is still
  * pending, or four plans are; HL_ERR_UNSUPPORTED: a pipeline without

@@ -396,12 +396,22 @@ __device__ __forceinline__ void bw_prep_bags(const int32_t* __restrict__ codes, 
   }
 }
 
+// A kernel starts only once the kernels before it on its stream are complete
+// and their writes visible: a store at its start is a handover signal for
+// them (block 0 makes it, with release order at agent scope).
+__device__ __forceinline__ void bw_start_signal(uint32_t* sflag, uint32_t sv) {
+  if (sflag && blockIdx.x == 0 && threadIdx.x == 0)
+    __hip_atomic_store(sflag, sv, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 #define BP_BAGS 256
 __global__ void __launch_bounds__(256)
 bw_prep(const int32_t* __restrict__ codes, const int32_t* __restrict__ bag_ptr, int64_t n_bags, int32_t bps,
         const uint8_t* __restrict__ mask, uint32_t n_hot, uint32_t k_cap, int32_t stg_rows,
-        uint32_t* __restrict__ keys, uint32_t* __restrict__ vals, int64_t n_lookups, uint32_t* err) {
+        uint32_t* __restrict__ keys, uint32_t* __restrict__ vals, int64_t n_lookups, uint32_t* sflag, uint32_t sv,
+        uint32_t* err) {
   __shared__ int32_t off[BP_BAGS + 1];
+  bw_start_signal(sflag, sv);
   const int64_t b0 = (int64_t)blockIdx.x * BP_BAGS;
   const int nb = (int)min((int64_t)BP_BAGS, n_bags - b0);
   for (int j = threadIdx.x; j <= nb; j += blockDim.x) off[j] = bag_ptr[b0 + j];
@@ -426,9 +436,11 @@ __global__ void __launch_bounds__(BPH_THREADS)
 bw_prep_hist(const int32_t* __restrict__ codes, const int32_t* __restrict__ bag_ptr, int64_t n_bags, int32_t bps,
              uint32_t n_hot, uint32_t k_cap, int32_t stg_rows, uint32_t* __restrict__ keys,
              uint32_t* __restrict__ vals, int64_t n_lookups, uint32_t hb, int passes, int b,
-             uint32_t* __restrict__ part, uint32_t* __restrict__ zero, uint64_t n_zero, uint32_t* err) {
+             uint32_t* __restrict__ part, uint32_t* __restrict__ zero, uint64_t n_zero, uint32_t* sflag, uint32_t sv,
+             uint32_t* err) {
   __shared__ uint32_t hst[HL_SORT_MAXPASS][NB];
   __shared__ int32_t off[BPH_BAGS + 1];
+  bw_start_signal(sflag, sv);
   int64_t first, covered;
   bw_uncovered(bag_ptr, n_bags, n_lookups, &first, &covered);
   if (blockIdx.x < hb) {
@@ -969,6 +981,16 @@ extern "C" hl_status hl_embbag_bwd_plan(hl_handle* h, int32_t stg_rows, const in
                                         int32_t n_samples, int32_t bps, int64_t n_lookups, const int32_t* sample_ids,
                                         const int32_t* n_sel_dev, int32_t n_sel_max, void* workspace, size_t ws_bytes,
                                         hl_stream stream) {
+  bool sent = false;
+  return hl_embbag_bwd_plan_signal(h, stg_rows, codes, bag_ptr, n_samples, bps, n_lookups, sample_ids, n_sel_dev,
+                                   n_sel_max, workspace, ws_bytes, stream, nullptr, 0, &sent);
+}
+
+hl_status hl_embbag_bwd_plan_signal(hl_handle* h, int32_t stg_rows, const int32_t* codes, const int32_t* bag_ptr,
+                                    int32_t n_samples, int32_t bps, int64_t n_lookups, const int32_t* sample_ids,
+                                    const int32_t* n_sel_dev, int32_t n_sel_max, void* workspace, size_t ws_bytes,
+                                    hl_stream stream, uint32_t* sflag, uint32_t sval, bool* sent) {
+  *sent = false;
   hl_status st = check_common(h, codes, bag_ptr, n_samples, bps, n_lookups, sample_ids, n_sel_max, stg_rows);
   if (st != HL_OK) return st;
   if (!workspace) return HL_ERR_INVALID_ARG;
@@ -995,8 +1017,9 @@ extern "C" hl_status hl_embbag_bwd_plan(hl_handle* h, int32_t stg_rows, const in
   const int bits = bw_key_bits(h, stg_rows);
   if (mask) {
     HL_KERNEL(h, s, "bw_prep", bw_prep, dim3(hl_div_up(n_bags, BP_BAGS)), dim3(256), 0, s, codes, bag_ptr, n_bags,
-              bps, mask, h->n_hot, h->k_cap, stg_rows, ws.sort.k0, ws.sort.v0, n_lookups, h->d_err);
+              bps, mask, h->n_hot, h->k_cap, stg_rows, ws.sort.k0, ws.sort.v0, n_lookups, sflag, sval, h->d_err);
     HL_LAUNCHED();
+    *sent = sflag != nullptr;
     st = hl_sort_pairs(h, ws.sort, nullptr, (uint32_t)n_lookups, bits, s, &sk, &sv);
   } else {
     if ((uint64_t)n_lookups > ws.sort.n_max) return HL_ERR_CAPACITY;
@@ -1005,12 +1028,13 @@ extern "C" hl_status hl_embbag_bwd_plan(hl_handle* h, int32_t stg_rows, const in
 #define BPH(NB)                                                                                                  \
   HL_KERNEL(h, s, "bw_prep_hist", bw_prep_hist<NB>, grid, dim3(BPH_THREADS), 0, s, codes, bag_ptr, n_bags, bps, h->n_hot, \
             h->k_cap, stg_rows, ws.sort.k0, ws.sort.v0, n_lookups, sg.hist_blocks, sg.passes, sg.b, ws.sort.part,   \
-            ws.sort.st[0], sg.n_zero, h->d_err)
+            ws.sort.st[0], sg.n_zero, sflag, sval, h->d_err)
     if (sg.nb == 256) BPH(256);
     else if (sg.nb == 1024) BPH(1024);
     else BPH(2048);
 #undef BPH
     HL_LAUNCHED();
+    *sent = sflag != nullptr;
     st = hl_sort_passes(h, ws.sort, nullptr, (uint32_t)n_lookups, bits, s, &sk, &sv);
   }
   if (st != HL_OK) return st;

@@ -174,6 +174,14 @@ hl_status hl_embbag_fwd_cold_sorted(hl_handle* h, const void* staging, int32_t s
                                     const int32_t* bag_ptr, int32_t n_samples, int32_t bps, int64_t n_lookups,
                                     float* out, void* workspace, size_t ws_bytes, hl_stream stream);
 
+// hl_embbag_bwd_plan whose first kernel, when it launches one (*sent), also
+// stores sv into *sflag as it starts: a handover signal for the kernels
+// enqueued before it on the stream.
+hl_status hl_embbag_bwd_plan_signal(hl_handle* h, int32_t stg_rows, const int32_t* codes, const int32_t* bag_ptr,
+                                    int32_t n_samples, int32_t bps, int64_t n_lookups, const int32_t* sample_ids,
+                                    const int32_t* n_sel_dev, int32_t n_sel_max, void* workspace, size_t ws_bytes,
+                                    hl_stream stream, uint32_t* sflag, uint32_t sv, bool* sent);
+
 // ----------------------------------------------------------------------------- sort
 // Stable LSD radix sort of (key, value) uint32 pairs with digits of up to 11
 // bits: one histogram kernel plus one kernel per digit with decoupled look-back

@@ -77,12 +77,12 @@ __global__ void pl_wait(const uint32_t* flag, uint32_t v, uint32_t* err) {
 // signal (if any), then each wait in turn.  The signal tells that the kernels
 // before it on the stream are complete, as a separate pl_signal would.
 __global__ void pl_hand(uint32_t* sflag, uint32_t sv, const uint32_t* w1, uint32_t v1, const uint32_t* w2,
-                        uint32_t v2, uint32_t* err) {
+                        uint32_t v2, const uint32_t* w3, uint32_t v3, uint32_t* err) {
   if (threadIdx.x != 0) return;
   if (sflag) __hip_atomic_store(sflag, sv, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
-  const uint32_t* wf[2] = {w1, w2};
-  const uint32_t wv[2] = {v1, v2};
-  for (int k = 0; k < 2; ++k) {
+  const uint32_t* wf[3] = {w1, w2, w3};
+  const uint32_t wv[3] = {v1, v2, v3};
+  for (int k = 0; k < 3; ++k) {
     if (!wf[k]) continue;
     uint32_t spins = 0;
     while ((int32_t)(__hip_atomic_load(wf[k], __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT) - wv[k]) < 0) {
@@ -120,6 +120,12 @@ struct hl_pipeline {
   int stg_next;
   bool sort_pend;         // the last plan's grouping signal (value sort_v) is not enqueued yet: it
   uint32_t sort_v;        // rides on the next plan's first wait, or is enqueued alone when awaited
+  bool done_pend;         // the last step's end signal (value done_v) likewise: it rides on the
+  uint32_t done_v;        // next step's first main-stream wait
+  const void* use_ptr[32];  // per-step buffers of recent steps, and the last step that used each
+  uint32_t use_seq[32];
+  int use_next;
+  uint32_t np_last;       // last step that ran its own dispatch and cold plan (cold-gather hash table)
 };
 
 static hl_status pl_flush(hl_pipeline* p);
@@ -207,17 +213,60 @@ static hl_status pl_wt(hl_pipeline* p, hipStream_t s, int f, uint32_t v) {
 
 // flag mode: stream s signals flag sf = sv (sf < 0: none), then waits for
 // flags w1 >= v1 and w2 >= v2 (w < 0: none), in one launch
-static hl_status pl_hw(hl_pipeline* p, hipStream_t s, int sf, uint32_t sv, int w1, uint32_t v1, int w2, uint32_t v2) {
-  if (sf < 0 && w1 < 0 && w2 < 0) return HL_OK;
-  hipLaunchKernelGGL(pl_hand, dim3(1), dim3(64), 0, s, sf >= 0 ? p->flags + sf : nullptr, sv,
-                     w1 >= 0 ? p->flags + w1 : nullptr, v1, w2 >= 0 ? p->flags + w2 : nullptr, v2, p->h->d_err);
+static hl_status pl_hw(hl_pipeline* p, hipStream_t s, int sf, uint32_t sv, int w1, uint32_t v1, int w2, uint32_t v2,
+                       int w3 = -1, uint32_t v3 = 0) {
+  if (sf < 0 && w1 < 0 && w2 < 0 && w3 < 0) return HL_OK;
+  if (!p->use_flags) {
+    if (sf >= 0) HL_TRY(pl_sig(p, s, sf, sv));
+    if (w1 >= 0) HL_TRY(pl_wt(p, s, w1, v1));
+    if (w2 >= 0) HL_TRY(pl_wt(p, s, w2, v2));
+    if (w3 >= 0) HL_TRY(pl_wt(p, s, w3, v3));
+    return HL_OK;
+  }
+  uint32_t* F = p->flags;
+  hipLaunchKernelGGL(pl_hand, dim3(1), dim3(64), 0, s, sf >= 0 ? F + sf : nullptr, sv, w1 >= 0 ? F + w1 : nullptr, v1,
+                     w2 >= 0 ? F + w2 : nullptr, v2, w3 >= 0 ? F + w3 : nullptr, v3, p->h->d_err);
   return hipGetLastError() == hipSuccess ? HL_OK : HL_ERR_HIP;
 }
-// the pending grouping signal, enqueued alone
-static hl_status pl_flush(hl_pipeline* p) {
+// the pending signals, enqueued alone
+static hl_status pl_flush_sort(hl_pipeline* p) {
   if (!p->sort_pend) return HL_OK;
   p->sort_pend = false;
   return pl_sig(p, p->plan, PF_SORT, p->sort_v);
+}
+static hl_status pl_flush_done(hl_pipeline* p) {
+  if (!p->done_pend) return HL_OK;
+  p->done_pend = false;
+  return pl_sig(p, p->main, PF_DONE, p->done_v);
+}
+static hl_status pl_flush(hl_pipeline* p) {
+  HL_TRY(pl_flush_sort(p));
+  return pl_flush_done(p);
+}
+// a before b in sequence order (sequence numbers wrap)
+static bool pl_before(uint32_t a, uint32_t b) { return (int32_t)(a - b) < 0; }
+// the last step that used buffer x (0: none seen)
+static uint32_t pl_use_last(const hl_pipeline* p, const void* x) {
+  for (int i = 0; i < 32; ++i)
+    if (p->use_ptr[i] == x) return p->use_seq[i];
+  return 0;
+}
+static void pl_use_note(hl_pipeline* p, const void* x, uint32_t q) {
+  if (!x) return;
+  for (int i = 0; i < 32; ++i)
+    if (p->use_ptr[i] == x) {
+      p->use_seq[i] = q;
+      return;
+    }
+  p->use_ptr[p->use_next] = x;
+  p->use_seq[p->use_next] = q;
+  p->use_next = (p->use_next + 1) % 32;
+}
+// the per-step buffers a plan rewrites (and a step uses)
+static void pl_step_bufs(const hl_step_io* io, const void* (&b)[9]) {
+  const void* v[9] = {io->gids, io->codes, io->flags, io->pop_ids, io->nonpop_ids, io->counts, io->cold_ids,
+                      io->n_cold, io->workspace};
+  for (int i = 0; i < 9; ++i) b[i] = v[i];
 }
 
 static hl_status pl_group(hl_pipeline* p) {
@@ -302,26 +351,37 @@ extern "C" hl_status hl_pipeline_plan(hl_pipeline* p, const hl_step_io* io, hl_s
     HL_HIPTRY(hipEventRecord(p->ev_pin, (hipStream_t)stream));
     HL_HIPTRY(hipStreamWaitEvent(P, p->ev_pin, 0));
   }
-  // every step enqueued so far has finished with its per-step buffers and
-  // workspace (and with the cold-gather hash table, which plans share); the
-  // previous plan's grouping signal goes in the same launch
+  // every step that used one of the plan's per-step buffers or workspace has
+  // finished with it, and so has every step that ran its own cold plan (the
+  // cold-gather hash table, which plans share; steps are in order on the main
+  // stream, so one wait covers them all); the previous plan's grouping signal
+  // goes in the same launch
+  const void* bufs[9];
+  pl_step_bufs(io, bufs);
+  uint32_t need = p->np_last;
+  for (const void* b : bufs) {
+    const uint32_t u = pl_use_last(p, b);
+    if (u && (!need || pl_before(need, u))) need = u;
+  }
+  if (need && p->done_pend && p->done_v == need) HL_TRY(pl_flush_done(p));
   const int wb = pl_wb_slot(p, io->cold_ids);
   const bool sp = p->sort_pend;
   p->sort_pend = false;
-  HL_TRY(pl_hw(p, P, sp ? PF_SORT : -1, p->sort_v, p->seq ? PF_DONE : -1, p->seq, wb >= 0 ? PF_WB + wb : -1,
+  HL_TRY(pl_hw(p, P, sp ? PF_SORT : -1, p->sort_v, need ? PF_DONE : -1, need, wb >= 0 ? PF_WB + wb : -1,
                wb >= 0 ? p->wb_seq[wb] : 0));
   const int32_t B = io->n_samples, bps = io->bags_per_sample;
   HL_TRY(hl_dispatch(h, io->rows, io->bag_ptr, B, bps, io->n_lookups, io->gids, io->codes, io->flags, io->pop_ids,
                      io->nonpop_ids, io->counts, io->workspace, io->ws_bytes, PS));
   HL_TRY(hl_cold_plan(h, io->gids, io->codes, io->bag_ptr, B, bps, io->n_lookups, nullptr, nullptr, B,
                       io->staging_cap, io->cold_ids, io->n_cold, io->workspace, io->ws_bytes, PS));
-  // the cold list is ready: the fetch may start while the grouping runs
+  // the cold list is ready: the fetch may start while the grouping runs (the
+  // grouping's first kernel gives the signal as it starts)
   const uint32_t v = ++p->plan_seq;
-  HL_TRY(pl_sig(p, P, PF_LOOK, v));
-  // the backward's grouping needs only the codes
+  bool sent = false;
   if (io->dY)
-    HL_TRY(hl_embbag_bwd_plan(h, io->staging_cap, io->codes, io->bag_ptr, B, bps, io->n_lookups, nullptr, nullptr, B,
-                              io->workspace, io->ws_bytes, PS));
+    HL_TRY(hl_embbag_bwd_plan_signal(h, io->staging_cap, io->codes, io->bag_ptr, B, bps, io->n_lookups, nullptr,
+                                     nullptr, B, io->workspace, io->ws_bytes, PS, p->flags + PF_LOOK, v, &sent));
+  if (!sent) HL_TRY(pl_sig(p, P, PF_LOOK, v));
   p->sort_pend = true;
   p->sort_v = v;
   e->io = *io;
@@ -356,14 +416,21 @@ extern "C" hl_status hl_pipeline_step(hl_pipeline* p, const hl_step_io* io, hl_s
     // copy, once the last step that used these staging rows has ended (a
     // write-back of the previous step precedes it on the fetch stream).  With
     // two staging buffers alternating, the copy overlaps the previous step.
+    // (a pending end signal of the previous step is given by this step's
+    // first main-stream launch, enqueued below)
     const uint32_t last = pl_stg_last(p, io->staging);
     HL_TRY(pl_hw(p, f, -1, 0, PF_LOOK, e->seq, last ? PF_DONE : -1, last));
     HL_TRY(hl_cold_fetch(h, io->cold_ids, io->n_cold, cap, io->w_host, io->staging, F));
     HL_TRY(pl_sig(p, f, PF_FETCH, q));
-    HL_TRY(pl_wt(p, m, PF_LOOK, e->seq));
+    // main: the previous step's end signal and the wait for the plan in one
+    // launch; the grouping is awaited after the hot forward (awaiting it
+    // before measured slower)
+    const bool dp = p->done_pend;
+    p->done_pend = false;
+    HL_TRY(pl_hw(p, m, dp ? PF_DONE : -1, p->done_v, PF_LOOK, e->seq, -1, 0));
     HL_TRY(pl_fwd_hot(h, io, M));
     if (io->dY) {
-      if (p->sort_pend && p->sort_v == e->seq) HL_TRY(pl_flush(p));
+      if (p->sort_pend && p->sort_v == e->seq) HL_TRY(pl_flush_sort(p));
       HL_TRY(pl_wt(p, m, PF_SORT, e->seq));
       HL_TRY(hl_embbag_bwd_apply_part(h, io->w_hot, io->staging, cap, B, bps, L, io->dY, io->lr, 1, io->workspace,
                                       io->ws_bytes, M));
@@ -381,7 +448,10 @@ extern "C" hl_status hl_pipeline_step(hl_pipeline* p, const hl_step_io* io, hl_s
     }
   } else {
     // the look-ahead plans use the same cold-gather hash table
-    if (p->plan_seq) HL_TRY(pl_wt(p, m, PF_LOOK, p->plan_seq));
+    const bool dp = p->done_pend;
+    p->done_pend = false;
+    HL_TRY(pl_hw(p, m, dp ? PF_DONE : -1, p->done_v, p->plan_seq ? PF_LOOK : -1, p->plan_seq, -1, 0));
+    p->np_last = q;
     HL_TRY(hl_dispatch(h, io->rows, io->bag_ptr, B, bps, L, io->gids, io->codes, io->flags, io->pop_ids,
                        io->nonpop_ids, io->counts, io->workspace, io->ws_bytes, M));
     // the write-back that last read this cold list must end before the plan rewrites it
@@ -417,8 +487,20 @@ extern "C" hl_status hl_pipeline_step(hl_pipeline* p, const hl_step_io* io, hl_s
       HL_TRY(hl_embbag_bwd_apply_part(h, io->w_hot, io->staging, cap, B, bps, L, io->dY, io->lr, 2, io->workspace,
                                       io->ws_bytes, M));
   }
-  HL_TRY(pl_sig(p, m, PF_DONE, q));
+  // the end signal waits for the next step's first main-stream launch, unless
+  // the write-back below needs it now
+  if (io->write_back || !p->use_flags) {
+    HL_TRY(pl_sig(p, m, PF_DONE, q));
+  } else {
+    p->done_pend = true;
+    p->done_v = q;
+  }
   pl_stg_note(p, io->staging, q);
+  {
+    const void* bufs[9];
+    pl_step_bufs(io, bufs);
+    for (const void* b : bufs) pl_use_note(p, b, q);
+  }
   if (io->write_back) {
     HL_TRY(pl_wt(p, f, PF_DONE, q));
     HL_TRY(hl_cold_scatter(h, io->cold_ids, io->n_cold, cap, io->staging, const_cast<void*>(io->w_host), F));
@@ -439,6 +521,7 @@ extern "C" hl_status hl_pipeline_step(hl_pipeline* p, const hl_step_io* io, hl_s
 
 extern "C" hl_status hl_pipeline_sync_writeback(hl_pipeline* p, hl_stream stream) {
   if (!p) return HL_ERR_INVALID_ARG;
+  HL_TRY(pl_flush(p));
   if (!p->use_flags) {
     HL_HIPTRY(hipStreamWaitEvent((hipStream_t)stream, p->ev[PF_WB], 0));
     HL_HIPTRY(hipStreamWaitEvent((hipStream_t)stream, p->ev[PF_WB + 1], 0));

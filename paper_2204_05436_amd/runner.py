@@ -208,14 +208,16 @@ class HotPath:
         if self._pending:
             if self._pending[0][0] is not b:
                 raise RuntimeError("steps must take the batches in the order they were planned")
-            if next is not None:
-                self.plan(next, untied)
             _, p = self._pending.pop(0)
             self._use(p)
             flags |= hl.HL_STEP_PLANNED
         else:
             p = self._next_set()
         hl.hl_pipeline_step(self.pipe, self._fill_io(self.io, b, self._sets[p], lr, flags), caller)
+        # the next plan after this step: it waits only for the steps that used
+        # its own buffers, and this step's end signal rides on the next step
+        if next is not None:
+            self.plan(next, untied)
 
     def sync(self, stream=None):
         """The stream (default: current) waits for every step enqueued so far."""
