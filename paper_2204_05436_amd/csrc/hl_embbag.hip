@@ -679,12 +679,12 @@ bw_reduce1(const uint32_t* __restrict__ keys, const uint32_t* __restrict__ vals,
 // wholly inside the segment.  Piece p is summed by group p % groups in
 // ascending p, then groups are added in order.
 template <int VEC, bool BF, bool SPLIT>
-__global__ void __launch_bounds__(RB_BLOCK)
-bw_reduce2(uint32_t n_tiles, eb_geom g, void* w_hot, void* stg, uint32_t n_hot, float lr,
-           const float* __restrict__ tfirst, const float* __restrict__ tlast, const uint32_t* __restrict__ tflag,
-           const uint32_t* __restrict__ tkey, float* __restrict__ gc, uint32_t gc_rows) {
+__device__ __forceinline__ void bw_reduce2_body(uint32_t t, uint32_t n_tiles, eb_geom g, void* w_hot, void* stg,
+                                                uint32_t n_hot, float lr, const float* __restrict__ tfirst,
+                                                const float* __restrict__ tlast, const uint32_t* __restrict__ tflag,
+                                                const uint32_t* __restrict__ tkey, float* __restrict__ gc,
+                                                uint32_t gc_rows) {
   typedef typename RowIO<VEC, BF>::T T;
-  const uint32_t t = blockIdx.x;
   if (!(tflag[t] & GF_L)) return;
   __shared__ uint32_t s_end;
   __shared__ float part[RB_WAVES * 64 * VEC];
@@ -743,6 +743,15 @@ bw_reduce2(uint32_t n_tiles, eb_geom g, void* w_hot, void* stg, uint32_t n_hot, 
     for (int e = 0; e < VEC; ++e) wv[e] -= lr * acc[e];
     RowIO<VEC, BF>::store(p, wv);
   }
+}
+
+template <int VEC, bool BF, bool SPLIT>
+__global__ void __launch_bounds__(RB_BLOCK)
+bw_reduce2(uint32_t n_tiles, eb_geom g, void* w_hot, void* stg, uint32_t n_hot, float lr,
+           const float* __restrict__ tfirst, const float* __restrict__ tlast, const uint32_t* __restrict__ tflag,
+           const uint32_t* __restrict__ tkey, float* __restrict__ gc, uint32_t gc_rows) {
+  bw_reduce2_body<VEC, BF, SPLIT>(blockIdx.x, n_tiles, g, w_hot, stg, n_hot, lr, tfirst, tlast, tflag, tkey, gc,
+                                  gc_rows);
 }
 
 // The deferred staging-row updates: every run end in the sorted keys whose key
@@ -807,12 +816,14 @@ bw_cold(const uint32_t* __restrict__ keys, uint32_t n, eb_geom g, void* stg, uin
 // the forward's cold half over the non-popular mu-batch.  A group of lanes
 // takes FT pairs at once.
 #define FT 4
-template <int VEC, bool BF>
-__global__ void __launch_bounds__(256)
-eb_fwd_tail(const uint32_t* __restrict__ keys, const uint32_t* __restrict__ vals, uint32_t n,
-            const uint32_t* __restrict__ bnd, eb_geom g, const void* stg_, int32_t stg_rows, uint32_t n_hot,
-            uint32_t k_cap, const int32_t* __restrict__ codes, const int32_t* __restrict__ bag_ptr,
-            float* __restrict__ out, uint32_t* err) {
+// (block bid of nblk, WAVES waves per block)
+template <int VEC, bool BF, int WAVES>
+__device__ __forceinline__ void eb_tail_body(uint32_t bid, uint32_t nblk, const uint32_t* __restrict__ keys,
+                                             const uint32_t* __restrict__ vals, uint32_t n,
+                                             const uint32_t* __restrict__ bnd, eb_geom g, const void* stg_,
+                                             int32_t stg_rows, uint32_t n_hot, uint32_t k_cap,
+                                             const int32_t* __restrict__ codes, const int32_t* __restrict__ bag_ptr,
+                                             float* __restrict__ out, uint32_t* err) {
   typedef typename RowIO<VEC, BF>::T T;
   const T* stg = (const T*)stg_;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
@@ -822,8 +833,8 @@ eb_fwd_tail(const uint32_t* __restrict__ keys, const uint32_t* __restrict__ vals
   const bool cact = colv < g.vpr;
   const int64_t col = (int64_t)colv * VEC;
   const uint32_t b0 = min(*bnd, n);
-  const uint64_t stride = (uint64_t)gridDim.x * 4 * g.NG * FT;
-  for (uint64_t p0 = b0 + ((uint64_t)(blockIdx.x * 4 + w) * g.NG + gi) * FT; p0 < n; p0 += stride) {
+  const uint64_t stride = (uint64_t)nblk * WAVES * g.NG * FT;
+  for (uint64_t p0 = b0 + ((uint64_t)(bid * WAVES + w) * g.NG + gi) * FT; p0 < n; p0 += stride) {
     uint32_t key[FT], bag[FT];
     bool take[FT];
 #pragma unroll
@@ -881,6 +892,38 @@ eb_fwd_tail(const uint32_t* __restrict__ keys, const uint32_t* __restrict__ vals
       if (cact) st_f32<VEC>(out + (int64_t)bag[j] * g.D + col, o[j]);
     }
   }
+}
+
+template <int VEC, bool BF>
+__global__ void __launch_bounds__(256)
+eb_fwd_tail(const uint32_t* __restrict__ keys, const uint32_t* __restrict__ vals, uint32_t n,
+            const uint32_t* __restrict__ bnd, eb_geom g, const void* stg_, int32_t stg_rows, uint32_t n_hot,
+            uint32_t k_cap, const int32_t* __restrict__ codes, const int32_t* __restrict__ bag_ptr,
+            float* __restrict__ out, uint32_t* err) {
+  eb_tail_body<VEC, BF, 4>(blockIdx.x, gridDim.x, keys, vals, n, bnd, g, stg_, stg_rows, n_hot, k_cap, codes, bag_ptr,
+                           out, err);
+}
+
+// The cold half of the forward and the backward's segments that span tiles
+// (bw_reduce2, split form) in one launch: blocks [0, n_tiles) take the
+// segments, the others the sorted tail.  They share no data (the segments
+// write hot rows and staging-row sums, the tail reads staging rows and
+// writes pooled outputs).
+template <int VEC, bool BF>
+__global__ void __launch_bounds__(RB_BLOCK)
+eb_tail_r2(uint32_t n_tiles, void* w_hot, uint32_t n_hot, float lr, const float* __restrict__ tfirst,
+           const float* __restrict__ tlast, const uint32_t* __restrict__ tflag, const uint32_t* __restrict__ tkey,
+           float* __restrict__ gc, uint32_t gc_rows, const uint32_t* __restrict__ keys,
+           const uint32_t* __restrict__ vals, uint32_t n, const uint32_t* __restrict__ bnd, eb_geom g, void* stg,
+           int32_t stg_rows, uint32_t k_cap, const int32_t* __restrict__ codes, const int32_t* __restrict__ bag_ptr,
+           float* __restrict__ out, uint32_t* err) {
+  if (blockIdx.x < n_tiles) {
+    bw_reduce2_body<VEC, BF, true>(blockIdx.x, n_tiles, g, w_hot, stg, n_hot, lr, tfirst, tlast, tflag, tkey, gc,
+                                   gc_rows);
+    return;
+  }
+  eb_tail_body<VEC, BF, RB_WAVES>(blockIdx.x - n_tiles, gridDim.x - n_tiles, keys, vals, n, bnd, g, stg, stg_rows,
+                                  n_hot, k_cap, codes, bag_ptr, out, err);
 }
 
 // ----------------------------------------------------------------------------- host side
@@ -962,11 +1005,12 @@ static void launch_bwd(const hl_handle* h, uint32_t tiles, hipStream_t s, const 
               stg, n_hot, lr, ws.tfirst, ws.tlast, ws.tflag, ws.tkey, ws.gc, ws.gc_rows, ws.bnd);
     HL_KERNEL(h, s, "bw_reduce2", (bw_reduce2<VEC, BF, false>), grid, dim3(RB_BLOCK), 0, s, tiles, g, w_hot, stg,
               n_hot, lr, ws.tfirst, ws.tlast, ws.tflag, ws.tkey, ws.gc, ws.gc_rows);
-  } else if (part == 1) {
+  } else if (part == 1 || part == 3) {
     HL_KERNEL(h, s, "bw_reduce1", (bw_reduce1<VEC, BF, true>), grid, dim3(RB_BLOCK), 0, s, sk, sv, n, dY, g, w_hot,
               stg, n_hot, lr, ws.tfirst, ws.tlast, ws.tflag, ws.tkey, ws.gc, ws.gc_rows, ws.bnd);
-    HL_KERNEL(h, s, "bw_reduce2", (bw_reduce2<VEC, BF, true>), grid, dim3(RB_BLOCK), 0, s, tiles, g, w_hot, stg,
-              n_hot, lr, ws.tfirst, ws.tlast, ws.tflag, ws.tkey, ws.gc, ws.gc_rows);
+    if (part == 1)
+      HL_KERNEL(h, s, "bw_reduce2", (bw_reduce2<VEC, BF, true>), grid, dim3(RB_BLOCK), 0, s, tiles, g, w_hot, stg,
+                n_hot, lr, ws.tfirst, ws.tlast, ws.tflag, ws.tkey, ws.gc, ws.gc_rows);
   } else {
     // the tail (cold lookups: about a tenth of a mini-batch here) is short; a
     // small grid strides over it
@@ -1046,15 +1090,25 @@ extern "C" hl_status hl_embbag_bwd_apply_part(hl_handle* h, void* w_hot, void* s
                                               int32_t n_samples, int32_t bps, int64_t n_lookups, const float* dY,
                                               float lr, int32_t part, void* workspace, size_t ws_bytes,
                                               hl_stream stream) {
-  if (!h || n_samples < 0 || bps < 1 || n_lookups < 0 || stg_rows < 0 || !workspace) return HL_ERR_INVALID_ARG;
   if (part < 0 || part > 2) return HL_ERR_INVALID_ARG;
+  return hl_embbag_bwd_apply_any(h, w_hot, staging, stg_rows, n_samples, bps, n_lookups, dY, lr, part, workspace,
+                                 ws_bytes, stream);
+}
+
+// parts 0-2 of hl_embbag_bwd_apply_part, and 3: the first half without its
+// spanning segments (hl_embbag_finish_cold completes them)
+hl_status hl_embbag_bwd_apply_any(hl_handle* h, void* w_hot, void* staging, int32_t stg_rows, int32_t n_samples,
+                                  int32_t bps, int64_t n_lookups, const float* dY, float lr, int32_t part,
+                                  void* workspace, size_t ws_bytes, hl_stream stream) {
+  if (!h || n_samples < 0 || bps < 1 || n_lookups < 0 || stg_rows < 0 || !workspace) return HL_ERR_INVALID_ARG;
+  if (part < 0 || part > 3) return HL_ERR_INVALID_ARG;
   const int64_t n_bags = (int64_t)n_samples * bps;
   hl_ws_rec* rec = hl_ws_find(h, workspace);
   if (!rec || rec->n != n_lookups || rec->bags != n_bags || rec->stg != stg_rows)
     return HL_ERR_INVALID_ARG;  // no matching plan is held by this workspace
-  if (part == 2 && !rec->part1) return HL_ERR_INVALID_ARG;  // the first half has not run on this plan
+  if (part == 2 && rec->part1 != 1) return HL_ERR_INVALID_ARG;  // the first half has not run on this plan
   if (n_lookups == 0 || n_samples == 0) {
-    if (part == 1) rec->part1 = 1;
+    if (part == 1 || part == 3) rec->part1 = part == 1 ? 1 : 3;
     return HL_OK;
   }
   if ((part != 2 && (!dY || (h->n_hot && !w_hot))) || (stg_rows && !staging)) return HL_ERR_INVALID_ARG;
@@ -1079,7 +1133,10 @@ extern "C" hl_status hl_embbag_bwd_apply_part(hl_handle* h, void* w_hot, void* s
   else { if (bf) BWD(1, true); else BWD(1, false); }
 #undef BWD
   HL_LAUNCHED();
-  if (part == 1) rec->part1 = 1;
+  if (part == 1 || part == 3) {
+    rec->part1 = part == 1 ? 1 : 3;
+    rec->vec = vec;
+  }
   return HL_OK;
 }
 
@@ -1115,6 +1172,58 @@ hl_status hl_embbag_fwd_cold_sorted(hl_handle* h, const void* staging, int32_t s
   else if (vec == 2) { if (bf) TAIL(2, true); else TAIL(2, false); }
   else { if (bf) TAIL(1, true); else TAIL(1, false); }
 #undef TAIL
+  HL_LAUNCHED();
+  return HL_OK;
+}
+
+// After apply part 3 and the fetch: the cold half of the forward from the
+// sorted tail together with the first half's spanning segments, then the
+// staging-row updates (part 2's kernel).
+hl_status hl_embbag_finish_cold(hl_handle* h, void* w_hot, void* staging, int32_t stg_rows, const int32_t* codes,
+                                const int32_t* bag_ptr, int32_t n_samples, int32_t bps, int64_t n_lookups, float lr,
+                                float* out, void* workspace, size_t ws_bytes, hl_stream stream) {
+  hl_status st = check_common(h, codes, bag_ptr, n_samples, bps, n_lookups, nullptr, n_samples, stg_rows);
+  if (st != HL_OK) return st;
+  if (!workspace || !out || (stg_rows && !staging) || (h->n_hot && !w_hot)) return HL_ERR_INVALID_ARG;
+  const int64_t n_bags = (int64_t)n_samples * bps;
+  hl_ws_rec* rec = hl_ws_find(h, workspace);
+  if (!rec || rec->n != n_lookups || rec->bags != n_bags || rec->stg != stg_rows || rec->part1 != 3)
+    return HL_ERR_INVALID_ARG;  // the grouping and apply part 3 must be in this workspace
+  rec->part1 = 0;  // the plan is used up: no part 2 or second finish on it
+  if (n_lookups == 0 || n_samples == 0) return HL_OK;
+  if (ws_bytes < hl_bwd_ws_bytes(h, n_lookups, n_bags)) return HL_ERR_CAPACITY;
+  hl_carver c = hl_carver::after_header(workspace, ws_bytes);
+  bw_ws ws;
+  bw_carve(c, ws, (uint32_t)n_lookups, n_bags, h->dim);
+  uint32_t *sk, *sv;
+  hl_sort_result(ws.sort, bw_key_bits(h, stg_rows), &sk, &sv);
+  // the first half's vector width (its tile sums' layout); out and the rows must allow it
+  const size_t es = h->dtype == HL_F32 ? 4 : 2;
+  const int vec = rec->vec;
+  if (eb_pick_vec(h->dim, es, {w_hot, staging, out}) < vec) return HL_ERR_INVALID_ARG;
+  eb_geom g = eb_make_geom(h->dim, vec);
+  const uint32_t n = (uint32_t)n_lookups;
+  const uint32_t te = (uint32_t)(RB_WAVES * g.NG * RB_E);
+  const uint32_t tiles = hl_div_up(n, te);
+  if (tiles > ws.tiles) return HL_ERR_CAPACITY;
+  uint32_t tb = hl_div_up(n, RB_WAVES * g.NG * FT);
+  if (tb > 256) tb = 256;
+  uint32_t cb = hl_div_up(n, 256);  // (as part 2: the tail is short, a small grid strides over it)
+  if (cb > 128) cb = 128;
+  hipStream_t s = (hipStream_t)stream;
+  const bool bf = h->dtype == HL_BF16;
+#define FIN(V, B)                                                                                                   \
+  do {                                                                                                             \
+    HL_KERNEL(h, s, "eb_tail_r2", (eb_tail_r2<V, B>), dim3(tiles + tb, g.cchunks), dim3(RB_BLOCK), 0, s, tiles,    \
+              w_hot, h->n_hot, lr, ws.tfirst, ws.tlast, ws.tflag, ws.tkey, ws.gc, ws.gc_rows, sk, sv, n, ws.bnd, g, \
+              staging, stg_rows, h->k_cap, codes, bag_ptr, out, h->d_err);                                         \
+    HL_KERNEL(h, s, "bw_cold", (bw_cold<V, B>), dim3(cb, g.cchunks), dim3(256), 0, s, sk, n, g, staging, h->n_hot, \
+              lr, ws.gc, ws.gc_rows, ws.bnd);                                                                      \
+  } while (0)
+  if (vec == 4) { if (bf) FIN(4, true); else FIN(4, false); }
+  else if (vec == 2) { if (bf) FIN(2, true); else FIN(2, false); }
+  else { if (bf) FIN(1, true); else FIN(1, false); }
+#undef FIN
   HL_LAUNCHED();
   return HL_OK;
 }

@@ -34,7 +34,8 @@ struct hl_ws_rec {
   const void* ws;      // NULL: free
   int64_t n, bags;     // the plan's lookups and bags
   int32_t stg;         // its staging rows
-  int part1;           // the first half of the apply ran on it
+  int part1;           // the first half of the apply ran on it (3: without its spanning segments)
+  int vec;             // the row vector width that half used (its tile layout depends on it)
 };
 struct hl_handle {
   int device;
@@ -174,6 +175,17 @@ hl_status hl_embbag_fwd_cold_sorted(hl_handle* h, const void* staging, int32_t s
                                     const int32_t* bag_ptr, int32_t n_samples, int32_t bps, int64_t n_lookups,
                                     float* out, void* workspace, size_t ws_bytes, hl_stream stream);
 
+// hl_embbag_bwd_apply_part with one more part: 3, the first half without the
+// segments that span tiles, which hl_embbag_finish_cold then completes.
+hl_status hl_embbag_bwd_apply_any(hl_handle* h, void* w_hot, void* staging, int32_t stg_rows, int32_t n_samples,
+                                  int32_t bps, int64_t n_lookups, const float* dY, float lr, int32_t part,
+                                  void* workspace, size_t ws_bytes, hl_stream stream);
+// After part 3, once the staging rows are fetched: the cold half of the
+// forward (as hl_embbag_fwd_cold_sorted) with part 3's spanning segments in one
+// launch, then the staging-row updates (as part 2).
+hl_status hl_embbag_finish_cold(hl_handle* h, void* w_hot, void* staging, int32_t stg_rows, const int32_t* codes,
+                                const int32_t* bag_ptr, int32_t n_samples, int32_t bps, int64_t n_lookups, float lr,
+                                float* out, void* workspace, size_t ws_bytes, hl_stream stream);
 // hl_embbag_bwd_plan whose first kernel, when it launches one (*sent), also
 // stores sv into *sflag as it starts: a handover signal for the kernels
 // enqueued before it on the stream.
@@ -219,8 +231,8 @@ void hl_sort_result(const hl_sort_ws& ws, int bits, uint32_t** out_k, uint32_t**
 // that writes them) and then run only the digit passes.  Geometry of a sort
 // of n_host items and `bits` bits: `passes` digits of `b` bits, nb bins,
 // hist_blocks partial counts per pass (ws.part[(p * HL_SORT_HIST_BLOCKS +
-// block) * nb + digit], digit p = (key >> (b * p)) & (nb - 1)), and the first
-// pass's status words ws.st[0][0 .. n_zero) to clear.
+// block) * nb + digit], digit p = (key >> (b * p)) & ((1 << b) - 1)), and the
+// first pass's status words ws.st[0][0 .. n_zero) to clear.
 struct hl_sort_geom {
   int passes, b, nb;
   uint32_t hist_blocks;

@@ -432,16 +432,16 @@ extern "C" hl_status hl_pipeline_step(hl_pipeline* p, const hl_step_io* io, hl_s
     if (io->dY) {
       if (p->sort_pend && p->sort_v == e->seq) HL_TRY(pl_flush_sort(p));
       HL_TRY(pl_wt(p, m, PF_SORT, e->seq));
-      HL_TRY(hl_embbag_bwd_apply_part(h, io->w_hot, io->staging, cap, B, bps, L, io->dY, io->lr, 1, io->workspace,
-                                      io->ws_bytes, M));
+      // the reduction of the hot runs and of the staging runs inside a tile
+      HL_TRY(hl_embbag_bwd_apply_any(h, io->w_hot, io->staging, cap, B, bps, L, io->dY, io->lr, 3, io->workspace,
+                                     io->ws_bytes, M));
     }
     HL_TRY(pl_wt(p, m, PF_FETCH, q));
     if (io->dY) {
-      // the cold half of the forward from the grouping's tail (cold lookups only)
-      HL_TRY(hl_embbag_fwd_cold_sorted(h, io->staging, cap, io->codes, io->bag_ptr, B, bps, L, io->out, io->workspace,
-                                       io->ws_bytes, M));
-      HL_TRY(hl_embbag_bwd_apply_part(h, io->w_hot, io->staging, cap, B, bps, L, io->dY, io->lr, 2, io->workspace,
-                                      io->ws_bytes, M));
+      // the cold half of the forward from the grouping's tail (cold lookups
+      // only) with the runs that span tiles, then the staging-row updates
+      HL_TRY(hl_embbag_finish_cold(h, io->w_hot, io->staging, cap, io->codes, io->bag_ptr, B, bps, L, io->lr, io->out,
+                                   io->workspace, io->ws_bytes, M));
     } else {
       HL_TRY(hl_embbag_fwd_part(h, io->w_hot, io->staging, cap, io->codes, io->bag_ptr, B, bps, L, io->nonpop_ids,
                                 io->counts + 1, B, io->out, 2, M));
