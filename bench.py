@@ -64,6 +64,9 @@ def kernel_bytes(name, st):
         "eb_fwd_hot": 4 * L + 4 * (nb + 1) + (U - C) * R + nb * O,
         # cold half: tail keys and bags, offsets, staging rows, outputs read and written
         "eb_fwd_tail": 8 * Lc + 8 * Lc + C * R + 2 * Lc * O,
+        # the same with the reduction's spanning segments (their partial sums are
+        # workspace, not algorithmic bytes)
+        "eb_tail_r2": 8 * Lc + 8 * Lc + C * R + 2 * Lc * O,
         # reduction: sorted keys and bags, dY, each updated row read and written
         "bw_reduce1": 8 * L + nb * O + 2 * (U - C) * R + C * O,
         "bw_cold": 4 * Lc + 2 * C * R + C * O,
@@ -262,8 +265,8 @@ def main():
 
     # the embedding forward and backward: their kernels' time per step (the
     # grouping included), against the algorithmic bytes of both passes
-    fb_kernels = ("eb_fwd_hot", "eb_fwd_tail", "bw_prep", "bw_prep_hist", "srt_hist", "srt_pass", "bw_reduce1", "bw_reduce2",
-                  "bw_cold")
+    fb_kernels = ("eb_fwd_hot", "eb_fwd_tail", "eb_tail_r2", "bw_prep", "bw_prep_hist", "srt_hist", "srt_pass",
+                  "bw_reduce1", "bw_reduce2", "bw_cold")
     t_fb = sum(kernels[n]["ms_per_step"] for n in fb_kernels if n in kernels)
     fwd_b = 4 * avg["L"] + 4 * (avg["n_bags"] + 1) + avg["U"] * avg["R"] + avg["n_bags"] * avg["O"]
     bwd_b = 4 * avg["L"] + 4 * (avg["n_bags"] + 1) + avg["n_bags"] * avg["O"] + 2 * avg["U"] * avg["R"]
