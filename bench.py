@@ -173,10 +173,14 @@ def main():
     # steps are issued from a stream of their own (work on the default stream
     # would serialize with the pipeline's streams)
     side = torch.cuda.Stream()
+
+    def ahead(i, n):
+        """the batches after step i of n that the runner plans ahead"""
+        return [dmeas[(i + j) % len(dmeas)] for j in range(1, hp.n_sets) if i + j < n]
     stats = []
     for j, b in enumerate(dmeas):
         with torch.cuda.stream(side):
-            hp.step(b, next=dmeas[j + 1] if j + 1 < len(dmeas) else None)
+            hp.step(b, next=ahead(j, len(dmeas)))
         torch.cuda.synchronize()
         L = b.n_lookups
         U = int(torch.unique(hp.codes[:L]).numel())
@@ -190,7 +194,7 @@ def main():
     log("[bench] statistics pass done")
     with torch.cuda.stream(side):
         for i in range(args.warmup):
-            hp.step(dmeas[i % len(dmeas)], untied=True, next=dmeas[(i + 1) % len(dmeas)] if i + 1 < args.warmup else None)
+            hp.step(dmeas[i % len(dmeas)], untied=True, next=ahead(i, args.warmup))
         hp.sync()
     torch.cuda.synchronize()
     log(f"[bench] warmup {args.warmup} steps done")
@@ -207,7 +211,7 @@ def main():
         t_start = time.perf_counter()
         start.record()  # the side stream is idle: the event completes before the first step is issued
         for i in range(K):
-            hp.step(dmeas[i % len(dmeas)], untied=True, next=dmeas[(i + 1) % len(dmeas)] if i + 1 < K else None)
+            hp.step(dmeas[i % len(dmeas)], untied=True, next=ahead(i, K))
         host_ms = (time.perf_counter() - t_start) * 1e3
         hp.sync()
         stop.record()
@@ -227,7 +231,7 @@ def main():
     def look_ahead_steps():
         with torch.cuda.stream(side):
             for i in range(K):
-                hp.step(dmeas[i % len(dmeas)], untied=True, next=dmeas[(i + 1) % len(dmeas)] if i + 1 < K else None)
+                hp.step(dmeas[i % len(dmeas)], untied=True, next=ahead(i, K))
             hp.sync()
         torch.cuda.synchronize()
 

@@ -49,7 +49,7 @@
 #define PF_FETCH 1
 #define PF_FWDHOT 2
 #define PF_GROUP 3
-#define PF_WB 5   // two: one per cold list
+#define PF_WB 5   // the last step whose write-back has ended (write-backs run in order)
 #define PF_LOOK 7 // a look-ahead plan: its own sequence
 #define PF_DONE 8 // the end of a step on the main stream
 #define PF_SORT 9 // a look-ahead plan's grouping (plan sequence)
@@ -109,12 +109,12 @@ struct hl_pipeline {
   uint32_t plan_seq;      // sequence number of the last look-ahead plan
   uint32_t* flags;        // [PF_N] device
   uint32_t seq;           // sequence number of the last step
-  uint32_t wb_seq[2];     // step whose write-back last read each cold list
+  const void* wb_ids[8];  // cold lists of recent write-backs, and the step of each one's last
+  uint32_t wb_seq[8];     // (a list not among them was last written back before all of these)
+  int wb_next;
   bool use_flags;         // handovers through device flags (masked streams)
   hipEvent_t ev[PF_N];    // the same handovers as events (pipelines without masks)
   hipEvent_t ev_in, ev_out, ev_pin, ev_plan, ev_f, ev_g;
-  const void* wb_ids[2];  // the cold list each write-back event covers
-  int wb_next;
   const void* stg_ptr[4]; // staging buffers of recent steps, and the last step that used each
   uint32_t stg_seq[4];
   int stg_next;
@@ -178,9 +178,8 @@ extern "C" hl_status hl_pipeline_create(hl_handle* h, int32_t fetch_cus, int32_t
     hl_pipeline_destroy(p);
     return st;
   }
-  // the write-back events start recorded (nothing to wait for)
-  for (int i = 0; i < 2; ++i)
-    if (!p->use_flags && hipEventRecord(p->ev[PF_WB + i], p->fetch) != hipSuccess) st = HL_ERR_HIP;
+  // the write-back event starts recorded (nothing to wait for)
+  if (!p->use_flags && hipEventRecord(p->ev[PF_WB], p->fetch) != hipSuccess) st = HL_ERR_HIP;
   *out = p;
   return st;
 }
@@ -318,11 +317,27 @@ static void pl_stg_note(hl_pipeline* p, const void* stg, uint32_t q) {
   p->stg_next = (p->stg_next + 1) % 4;
 }
 
-// the write-back slot whose last write-back read this cold list, or -1
-static int pl_wb_slot(const hl_pipeline* p, const uint32_t* cold_ids) {
-  for (int i = 0; i < 2; ++i)
-    if (p->wb_ids[i] == cold_ids) return i;
-  return -1;
+// the step of the last write-back that read this cold list (0: none): a list
+// not among the recent ones was written back before all of them, so the
+// oldest recent one bounds it
+static uint32_t pl_wb_last(const hl_pipeline* p, const uint32_t* cold_ids) {
+  uint32_t oldest = 0;
+  for (int i = 0; i < 8; ++i) {
+    if (!p->wb_ids[i]) continue;
+    if (p->wb_ids[i] == cold_ids) return p->wb_seq[i];
+    if (!oldest || pl_before(p->wb_seq[i], oldest)) oldest = p->wb_seq[i];
+  }
+  return oldest;
+}
+static void pl_wb_note(hl_pipeline* p, const uint32_t* cold_ids, uint32_t q) {
+  for (int i = 0; i < 8; ++i)
+    if (p->wb_ids[i] == cold_ids) {
+      p->wb_seq[i] = q;
+      return;
+    }
+  p->wb_ids[p->wb_next] = cold_ids;
+  p->wb_seq[p->wb_next] = q;
+  p->wb_next = (p->wb_next + 1) % 8;
 }
 
 // The popular mu-batch and the hot rows of the non-popular one in one launch:
@@ -364,11 +379,10 @@ extern "C" hl_status hl_pipeline_plan(hl_pipeline* p, const hl_step_io* io, hl_s
     if (u && (!need || pl_before(need, u))) need = u;
   }
   if (need && p->done_pend && p->done_v == need) HL_TRY(pl_flush_done(p));
-  const int wb = pl_wb_slot(p, io->cold_ids);
+  const uint32_t wb = pl_wb_last(p, io->cold_ids);
   const bool sp = p->sort_pend;
   p->sort_pend = false;
-  HL_TRY(pl_hw(p, P, sp ? PF_SORT : -1, p->sort_v, need ? PF_DONE : -1, need, wb >= 0 ? PF_WB + wb : -1,
-               wb >= 0 ? p->wb_seq[wb] : 0));
+  HL_TRY(pl_hw(p, P, sp ? PF_SORT : -1, p->sort_v, need ? PF_DONE : -1, need, wb ? PF_WB : -1, wb));
   const int32_t B = io->n_samples, bps = io->bags_per_sample;
   HL_TRY(hl_dispatch(h, io->rows, io->bag_ptr, B, bps, io->n_lookups, io->gids, io->codes, io->flags, io->pop_ids,
                      io->nonpop_ids, io->counts, io->workspace, io->ws_bytes, PS));
@@ -403,7 +417,7 @@ extern "C" hl_status hl_pipeline_step(hl_pipeline* p, const hl_step_io* io, hl_s
   hipStream_t caller = (hipStream_t)stream, m = p->main, f = p->fetch, g = p->group;
   const hl_stream M = (hl_stream)m, F = (hl_stream)f, G = (hl_stream)g;
   const uint32_t q = ++p->seq;
-  int slot = pl_wb_slot(p, io->cold_ids);
+  const uint32_t wbl = pl_wb_last(p, io->cold_ids);
   const bool tie = !(io->step_flags & HL_STEP_UNTIED);
   if (tie) {
     HL_HIPTRY(hipEventRecord(p->ev_in, caller));
@@ -423,14 +437,15 @@ extern "C" hl_status hl_pipeline_step(hl_pipeline* p, const hl_step_io* io, hl_s
     HL_TRY(hl_cold_fetch(h, io->cold_ids, io->n_cold, cap, io->w_host, io->staging, F));
     HL_TRY(pl_sig(p, f, PF_FETCH, q));
     // main: the previous step's end signal and the wait for the plan in one
-    // launch; the grouping is awaited after the hot forward (awaiting it
-    // before measured slower)
+    // launch; the grouping is awaited after the hot forward (the plan stream
+    // carries as much work per step as main: awaiting the grouping before the
+    // forward measured slower, also with plans two steps ahead)
+    if (io->dY && p->sort_pend && p->sort_v == e->seq) HL_TRY(pl_flush_sort(p));
     const bool dp = p->done_pend;
     p->done_pend = false;
     HL_TRY(pl_hw(p, m, dp ? PF_DONE : -1, p->done_v, PF_LOOK, e->seq, -1, 0));
     HL_TRY(pl_fwd_hot(h, io, M));
     if (io->dY) {
-      if (p->sort_pend && p->sort_v == e->seq) HL_TRY(pl_flush_sort(p));
       HL_TRY(pl_wt(p, m, PF_SORT, e->seq));
       // the reduction of the hot runs and of the staging runs inside a tile
       HL_TRY(hl_embbag_bwd_apply_any(h, io->w_hot, io->staging, cap, B, bps, L, io->dY, io->lr, 3, io->workspace,
@@ -455,7 +470,7 @@ extern "C" hl_status hl_pipeline_step(hl_pipeline* p, const hl_step_io* io, hl_s
     HL_TRY(hl_dispatch(h, io->rows, io->bag_ptr, B, bps, L, io->gids, io->codes, io->flags, io->pop_ids,
                        io->nonpop_ids, io->counts, io->workspace, io->ws_bytes, M));
     // the write-back that last read this cold list must end before the plan rewrites it
-    if (slot >= 0) HL_TRY(pl_wt(p, m, PF_WB + slot, p->wb_seq[slot]));
+    if (wbl) HL_TRY(pl_wt(p, m, PF_WB, wbl));
     // a cold lookup makes its sample non-popular: no sample list needed
     HL_TRY(hl_cold_plan(h, io->gids, io->codes, io->bag_ptr, B, bps, L, nullptr, nullptr, B, cap, io->cold_ids,
                         io->n_cold, io->workspace, io->ws_bytes, M));
@@ -504,13 +519,8 @@ extern "C" hl_status hl_pipeline_step(hl_pipeline* p, const hl_step_io* io, hl_s
   if (io->write_back) {
     HL_TRY(pl_wt(p, f, PF_DONE, q));
     HL_TRY(hl_cold_scatter(h, io->cold_ids, io->n_cold, cap, io->staging, const_cast<void*>(io->w_host), F));
-    if (slot < 0) {
-      slot = p->wb_next;
-      p->wb_next ^= 1;
-    }
-    p->wb_ids[slot] = io->cold_ids;
-    p->wb_seq[slot] = q;
-    HL_TRY(pl_sig(p, f, PF_WB + slot, q));
+    pl_wb_note(p, io->cold_ids, q);
+    HL_TRY(pl_sig(p, f, PF_WB, q));
   }
   if (tie) {
     HL_HIPTRY(hipEventRecord(p->ev_out, m));
@@ -524,7 +534,6 @@ extern "C" hl_status hl_pipeline_sync_writeback(hl_pipeline* p, hl_stream stream
   HL_TRY(pl_flush(p));
   if (!p->use_flags) {
     HL_HIPTRY(hipStreamWaitEvent((hipStream_t)stream, p->ev[PF_WB], 0));
-    HL_HIPTRY(hipStreamWaitEvent((hipStream_t)stream, p->ev[PF_WB + 1], 0));
     return HL_OK;
   }
   // the write-backs run in order on the fetch stream

@@ -61,7 +61,7 @@ MODES = ("pipelined", "sequential", "fwdbwd")
 class HotPath:
     def __init__(self, w: Workload, rows_per_table, table: hl.HostTable, max_lookups: int, max_samples: int,
                  device="cuda", k_cap: int | None = None, staging_cap: int | None = None, writeback: bool = False,
-                 fetch_cus: int = 32, plan_cus: int = 64):
+                 fetch_cus: int = 32, plan_cus: int = 64, n_sets: int = 3):
         self.w = w
         self.device = device
         self.rows_per_table = np.asarray(rows_per_table, dtype=np.uint32)
@@ -90,10 +90,14 @@ class HotPath:
                 staging=torch.zeros((self.staging_cap, w.dim), dtype=sdt, device=device),
                 ws=torch.zeros(wsb, dtype=torch.uint8, device=device))
 
-        # two sets of per-step buffers, alternated between steps: a write-back
-        # still reading one step's cold list, a look-ahead plan of the next
-        # mini-batch, or the next step's row fetch, uses the other set
-        self._sets = [bufs(), bufs()]
+        # n_sets >= 2 sets of per-step buffers, taken in turn by the steps: a
+        # write-back still reading one step's cold list, the look-ahead plans of
+        # the next n_sets - 1 mini-batches, or the next step's row fetch, use the
+        # others
+        if n_sets < 2:
+            raise ValueError("at least two sets of per-step buffers")
+        self.n_sets = int(n_sets)
+        self._sets = [bufs() for _ in range(self.n_sets)]
         self._par = 0
         self._use(0)
         self._pending = []  # look-ahead plans: (batch, set)
@@ -111,7 +115,7 @@ class HotPath:
         ev = lambda: torch.cuda.Event()
         self.ev_plan, self.ev_fetch, self.ev_group, self.ev_apply = ev(), ev(), ev(), ev()
         self.ev_fwdhot = ev()
-        self.ev_wb = [ev(), ev()]
+        self.ev_wb = [ev() for _ in range(self.n_sets)]
         self.out = torch.zeros((max(1, max_bags), w.dim), dtype=torch.float32, device=device)
         self.n_hot = 0
 
@@ -124,7 +128,7 @@ class HotPath:
         if self._pending:
             raise RuntimeError("a look-ahead plan is pending: step that batch first")
         p = self._par
-        self._par ^= 1
+        self._par = (p + 1) % self.n_sets
         self._use(p)
         return p
 
@@ -143,14 +147,14 @@ class HotPath:
         return io
 
     def plan(self, b: DevBatch, untied=False):
-        """Look-ahead segregation of batch b (hl_pipeline_plan): its dispatch and
-        cold plan run on the pipeline's plan stream while the steps enqueued
-        before it train; the step of b (the next pipelined step) skips them.
-        At most one plan ahead of the next step."""
-        if len(self._pending) >= 2:
-            raise RuntimeError("two look-ahead plans are already pending")
+        """Look-ahead segregation of batch b (hl_pipeline_plan): its dispatch,
+        cold plan and grouping run on the pipeline's plan stream while the steps
+        enqueued before it train; the step of b skips them.  Up to n_sets - 1
+        plans ahead of the steps."""
+        if len(self._pending) >= self.n_sets - 1:
+            raise RuntimeError(f"{len(self._pending)} look-ahead plans are already pending")
         p = self._par
-        self._par ^= 1
+        self._par = (p + 1) % self.n_sets
         io = self._fill_io(hl.StepIO(), b, self._sets[p], 0.0, hl.HL_STEP_UNTIED if untied else 0)
         hl.hl_pipeline_plan(self.pipe, io, torch.cuda.current_stream(self.device))
         self._pending.append((b, p))
@@ -173,16 +177,17 @@ class HotPath:
 
     # ------------------------------------------------------------------ one mini-batch
     def step(self, b: DevBatch, lr: float | None = None, events=None, mode: str = "pipelined", split_fwd=True,
-             untied=False, next: DevBatch | None = None):
+             untied=False, next=None):
         """classify -> partition -> remap -> cold gather (non-popular) -> forward of
         both mu-batches -> one coalesced SGD step [-> write-back of the cold rows].
 
         mode "pipelined": the three-stream schedule of the module docstring,
           enqueued by the native pipeline (hl_pipeline_step).  untied: no
           ordering with the current stream (inputs already resident; call
-          sync() before using the results).  next: the following batch,
-          whose dispatch and cold plan are then enqueued ahead (plan()) to
-          run while this step trains; its own step finds them done.
+          sync() before using the results).  next: the following batch, or
+          a list of the following batches, planned ahead (plan()) up to
+          n_sets - 1 of them, to run while this step trains; their own steps
+          find them done.
         mode "sequential": the fused calls in order on the current stream;
           `events`: optional list of len(STAGES)+1 torch.cuda.Event recorded
           around the stages.
@@ -203,7 +208,8 @@ class HotPath:
                 raise ValueError("no look-ahead under capture")
             return self._step_pipelined(b, lr, events, mode, caller, capturing)
         flags = hl.HL_STEP_UNTIED if untied else 0
-        if next is not None and not self._pending:
+        nexts = [] if next is None else (list(next) if isinstance(next, (list, tuple)) else [next])
+        if nexts and not self._pending:
             self.plan(b, untied)
         if self._pending:
             if self._pending[0][0] is not b:
@@ -214,10 +220,13 @@ class HotPath:
         else:
             p = self._next_set()
         hl.hl_pipeline_step(self.pipe, self._fill_io(self.io, b, self._sets[p], lr, flags), caller)
-        # the next plan after this step: it waits only for the steps that used
-        # its own buffers, and this step's end signal rides on the next step
-        if next is not None:
-            self.plan(next, untied)
+        # the next plans after this step: a plan waits only for the steps that
+        # used its own buffers, and this step's end signal rides on the next step
+        for nb in nexts:
+            if len(self._pending) >= self.n_sets - 1:
+                break
+            if not any(nb is pb for pb, _ in self._pending):
+                self.plan(nb, untied)
 
     def sync(self, stream=None):
         """The stream (default: current) waits for every step enqueued so far."""
