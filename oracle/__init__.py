@@ -54,6 +54,7 @@ def lib():
                                         P, P]),
             "ho_embbag_bwd_sgd_flat": (None, [i32, i32, P, P, P, i64, P, f32]),
             "ho_round_bf16": (C.c_uint16, [C.c_double]),
+            "ho_migrate": (i64, [u64, P, i64, P, P, i64, P, P]),
         }
         for name, (res, args) in sig.items():
             fn = getattr(L, name)
@@ -159,6 +160,19 @@ def scatter(table, ids, rows):
     rows = np.ascontiguousarray(rows, dtype=table.dtype)
     assert rows.shape == (len(ids),) + table.shape[1:]
     lib().ho_scatter(_p(table), table.strides[0], _p(ids), len(ids), _p(rows))
+
+
+def migrate(old_ids, w_hot_old, new_ids, host):
+    """Hot-set migration (re-learning): returns (w_hot_new, n_written_back);
+    host ([n_rows, dim], C-contiguous) is updated in place.  w_hot_old holds the
+    old set's rows by slot (at least len(old_ids) rows)."""
+    assert host.flags.c_contiguous
+    old_ids, new_ids = _c(old_ids, np.uint32), _c(new_ids, np.uint32)
+    w_hot_old = np.ascontiguousarray(w_hot_old, dtype=host.dtype)
+    out = np.empty((len(new_ids),) + host.shape[1:], dtype=host.dtype)
+    n = lib().ho_migrate(host.strides[0], _p(old_ids), len(old_ids), _p(w_hot_old), _p(new_ids), len(new_ids),
+                         _p(out), _p(host))
+    return out, int(n)
 
 
 def gather_ptr(table_ptr: int, row_bytes: int, ids, dim: int, np_dtype):

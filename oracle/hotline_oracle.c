@@ -445,5 +445,36 @@ void ho_embbag_bwd_sgd_flat(int32_t dim, int32_t dtype, void* table, const uint3
     free(o);
 }
 
+/* ------------------------------------------------------------------ 11. re-learning */
+/* The learning phase recurs during training (Sec. V-B: the EAL periodically
+ * switches back to learning; Sec. VI: twice per epoch; Sec. IV: hot rows are
+ * updated on the GPU, the others in CPU memory).  When a new hot set
+ * new_ids replaces old_ids (both ascending, distinct; slot = position):
+ *   - a row that leaves the cache (in old_ids, not in new_ids) goes back to the
+ *     host table with its trained value: host[id] = w_hot_old[old slot];
+ *   - a row that stays moves to its new slot with its trained value;
+ *   - a row that enters is read from the host table.
+ * Reading: nothing else changes, so the table as the path sees it (a hot row
+ * from the cache, any other from the host table) is the same before and after,
+ * bit for bit.  w_hot_new receives n_new rows; host is updated in place.
+ * Returns the number of rows written back. */
+int64_t ho_migrate(uint64_t row_bytes, const uint32_t* old_ids, int64_t n_old, const void* w_hot_old,
+                   const uint32_t* new_ids, int64_t n_new, void* w_hot_new, void* host) {
+    int64_t wb = 0;
+    for (int64_t s = 0; s < n_old; ++s)
+        if (find_u32(new_ids, n_new, old_ids[s]) < 0) {
+            memcpy((char*)host + (size_t)old_ids[s] * row_bytes, (const char*)w_hot_old + (size_t)s * row_bytes,
+                   (size_t)row_bytes);
+            ++wb;
+        }
+    for (int64_t s = 0; s < n_new; ++s) {
+        const int64_t o = find_u32(old_ids, n_old, new_ids[s]);
+        const char* src = o >= 0 ? (const char*)w_hot_old + (size_t)o * row_bytes
+                                 : (const char*)host + (size_t)new_ids[s] * row_bytes;
+        memcpy((char*)w_hot_new + (size_t)s * row_bytes, src, (size_t)row_bytes);
+    }
+    return wb;
+}
+
 /* bf16 rounding exposed for its own pin (ties-to-even cases). */
 uint16_t ho_round_bf16(double x) { return round_bf16(x); }

@@ -359,3 +359,66 @@ def test_empty_inputs():
     assert O.classify(np.zeros(0, np.uint32), np.zeros(0, np.uint32), np.zeros(3, np.int32), 2, 1).tolist() == [1, 1]
     pop, nonpop = O.partition(np.zeros(0, np.uint8))
     assert len(pop) == len(nonpop) == 0
+
+
+# ---------------------------------------------------------------------------- re-learning (hot-set migration)
+# Hand example: six rows of dim 2, row r of the host table holds (r, r); the old
+# hot set {1, 3} was trained to (10, 10) and (30, 30) in slots 0 and 1; the new
+# hot set is {3, 4}.  Row 1 leaves: the host gets (10, 10).  Row 3 stays: it
+# moves to slot 0 with (30, 30), and its stale host copy (3, 3) is left alone.
+# Row 4 enters from the host: (4, 4) in slot 1.  One row written back.
+def test_migrate_hand_example():
+    host = np.repeat(np.arange(6, dtype=np.float32)[:, None], 2, axis=1).copy()
+    w_old = np.array([[10, 10], [30, 30]], np.float32)
+    w_new, n = O.migrate([1, 3], w_old, [3, 4], host)
+    assert n == 1
+    assert np.array_equal(w_new, np.array([[30, 30], [4, 4]], np.float32))
+    expect = np.repeat(np.arange(6, dtype=np.float32)[:, None], 2, axis=1)
+    expect[1] = 10
+    assert np.array_equal(host, expect)
+
+
+def _logical(host, ids, w_hot):
+    """The table as the path reads it: a hot row from the cache, any other from the host."""
+    t = host.copy()
+    t[np.asarray(ids, np.int64)] = w_hot[: len(ids)]
+    return t
+
+
+@pytest.mark.parametrize("seed", range(6))
+@pytest.mark.parametrize("dtype", [np.float32, np.uint16])
+def test_migrate_keeps_the_logical_table(seed, dtype):
+    """Re-learning moves rows between the cache and the host but changes no row
+    of the table the path reads (bit for bit), keeps the trained values of the
+    rows that stay, and writes back exactly the rows that leave."""
+    rng = np.random.default_rng(seed)
+    n_rows, dim = int(rng.integers(8, 300)), int(rng.integers(1, 5))
+    host = rng.integers(0, 1 << 15, size=(n_rows, dim)).astype(dtype)
+    old = np.sort(rng.choice(n_rows, size=int(rng.integers(0, n_rows // 2 + 1)), replace=False)).astype(np.uint32)
+    new = np.sort(rng.choice(n_rows, size=int(rng.integers(0, n_rows // 2 + 1)), replace=False)).astype(np.uint32)
+    w_old = rng.integers(1 << 15, 1 << 16, size=(len(old), dim)).astype(dtype)  # trained: unlike any host row
+    before = _logical(host, old, w_old)
+    host0 = host.copy()
+    w_new, n = O.migrate(old, w_old, new, host)
+    assert np.array_equal(_logical(host, new, w_new), before)
+    leave, stay = set(old.tolist()) - set(new.tolist()), set(old.tolist()) & set(new.tolist())
+    assert n == len(leave)
+    slot_old = {int(g): s for s, g in enumerate(old)}
+    for s, g in enumerate(new.tolist()):
+        src = w_old[slot_old[g]] if g in stay else host0[g]
+        assert np.array_equal(w_new[s], src)
+    untouched = np.setdiff1d(np.arange(n_rows), np.fromiter(leave, dtype=np.int64, count=len(leave)))
+    assert np.array_equal(host[untouched], host0[untouched])
+
+
+def test_migrate_same_and_disjoint_sets():
+    rng = np.random.default_rng(7)
+    host = rng.standard_normal((50, 3)).astype(np.float32)
+    ids = np.array([2, 9, 17, 40], np.uint32)
+    w_old = rng.standard_normal((4, 3)).astype(np.float32) + 100
+    h0 = host.copy()
+    w_new, n = O.migrate(ids, w_old, ids, host)  # the same set: nothing moves
+    assert n == 0 and np.array_equal(w_new, w_old) and np.array_equal(host, h0)
+    other = np.array([0, 5, 41], np.uint32)       # disjoint: every old row leaves, every new one enters
+    w_new, n = O.migrate(ids, w_old, other, host)
+    assert n == 4 and np.array_equal(host[ids], w_old) and np.array_equal(w_new, h0[other])
