@@ -125,6 +125,7 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the oracle baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--breakdown", action="store_true", help="also time reference schedules and the stages")
+    ap.add_argument("--no-relearn", action="store_true", help="skip the timed re-learning (hot-set migration)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build measures one GPU only (asked for --gpus {args.gpus}); the path shards "
@@ -296,6 +297,28 @@ def main():
     if args.breakdown:
         breakdown = reference_regions(hp, dmeas, side, K)
 
+    # the learning phase again (after the measured steps, so it changes nothing
+    # above): counts over a sample of batches whose popularity has drifted (the
+    # same Zipf ranks on other rows), the new top-K, and the hot-cache migration
+    relearn = None
+    if not args.no_relearn:
+        drift = [to_device(W.make_batch(w, rows, 1000 + i, phase=1), dev) for i in range(w.profile_batches)]
+        old = hp.hot_ids[:hp.n_hot].cpu().numpy()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        n_new = hp.relearn(drift)
+        torch.cuda.synchronize()
+        rl_ms = (time.perf_counter() - t0) * 1e3
+        new = hp.hot_ids[:n_new].cpu().numpy()
+        err = hp.device_error()
+        if err:
+            raise SystemExit(f"device error word {err:#x} in the re-learning")
+        leave, enter = int(np.setdiff1d(old, new).size), int(np.setdiff1d(new, old).size)
+        relearn = {"ms": rl_ms, "sampled_batches": len(drift), "n_hot_before": int(old.size), "n_hot": int(n_new),
+                   "rows_written_back": leave, "rows_entered": enter, "steps_equivalent": rl_ms / (total_ms / K)}
+        log(f"[bench] re-learning over {len(drift)} drifted batches: {rl_ms:.2f} ms, {leave} rows left the cache, "
+            f"{enter} entered")
+
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(w, rows, prof, meas, meas_idx, table, k_cap, args.cpu_seconds)
@@ -322,7 +345,7 @@ def main():
         "popular_fraction": avg["n_pop"] / avg["B"],
         "unique_rows_per_batch": avg["U"], "cold_rows_per_batch": avg["n_cold"],
         "learning_phase_ms": learn_ms, "kernels": kernels,
-        "roofline": roof, "link_roofline": link, "cpu_baseline": cpu, "breakdown": breakdown,
+        "roofline": roof, "link_roofline": link, "cpu_baseline": cpu, "breakdown": breakdown, "relearn": relearn,
     }
     print(json.dumps(res), flush=True)
     hp.close()

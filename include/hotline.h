@@ -128,6 +128,23 @@ hl_status hl_set_hot(hl_handle* h, const uint32_t* hot_ids, uint32_t n_hot, hl_s
  * rows are copied to GPU memory after learning, Sec. IV). */
 hl_status hl_hot_fill(const hl_handle* h, const uint32_t* hot_ids, const void* w_host, void* w_hot,
                       hl_stream stream);
+/* Hot-set migration of the recurring learning phase (Sec. V-B: the EAL
+ * switches back to learning from time to time; Sec. VI: twice per epoch;
+ * Sec. IV: hot rows are trained on the GPU, the others in CPU memory).  Call
+ * it after hl_profile_topk (or hl_set_hot) has replaced the hot set
+ * old_ids[0..n_old) (device, ascending: the set w_hot_old holds, row s in slot
+ * s) by new_ids[0..hl_n_hot(h)) (device, ascending: that call's hot ids).  It
+ * fills w_hot_new (device, at least hl_n_hot(h) rows, not overlapping
+ * w_hot_old): a row in both sets is copied from its old slot, a row only in
+ * the new set is read from w_host; and every row only in the old set is
+ * written back to w_host (the pinned host table, device-visible pointer, as in
+ * hl_cold_fetch).  The table as the path reads it, a hot row from the cache
+ * and any other from w_host, is thus unchanged, bit for bit.  Asynchronous on
+ * `stream`; nothing else may use the three tables meanwhile.  HL_ERR_CAPACITY:
+ * n_old > k_cap; HL_ERR_INVALID_ARG: NULL where rows are needed, or the caches
+ * overlap.  An id >= n_rows sets HL_DEVERR_BAD_HOTSET and its row is skipped. */
+hl_status hl_hot_migrate(const hl_handle* h, const uint32_t* old_ids, uint32_t n_old, const uint32_t* new_ids,
+                         const void* w_hot_old, void* w_hot_new, void* w_host, hl_stream stream);
 
 /* Mini-batch shape used below: n_samples samples of bags_per_sample bags,
  * bag_ptr[n_samples*bags_per_sample + 1] (device), and n_lookups (host) =

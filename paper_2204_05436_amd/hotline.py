@@ -56,6 +56,7 @@ _SIGS = {
     "hl_profile_topk": (C.c_int, [P, U32, P, C.POINTER(U32), C.c_int, P]),
     "hl_set_hot": (C.c_int, [P, P, U32, P]),
     "hl_hot_fill": (C.c_int, [P, P, P, P, P]),
+    "hl_hot_migrate": (C.c_int, [P, P, U32, P, P, P, P, P]),
     "hl_classify": (C.c_int, [P, P, P, I32, I32, I64, P, P]),
     "hl_partition": (C.c_int, [P, P, I32, P, P, P, P, SZ, P]),
     "hl_remap": (C.c_int, [P, P, I64, P, P]),
@@ -215,6 +216,11 @@ def hl_set_hot(h, hot_ids, n_hot, stream=None):
 
 def hl_hot_fill(h, hot_ids, w_host_dev, w_hot, stream=None):
     _ck("hl_hot_fill", lib().hl_hot_fill(h.ptr, _p(hot_ids), _p(w_host_dev), _p(w_hot), _s(stream)))
+
+
+def hl_hot_migrate(h, old_ids, n_old, new_ids, w_hot_old, w_hot_new, w_host_dev, stream=None):
+    _ck("hl_hot_migrate", lib().hl_hot_migrate(h.ptr, _p(old_ids), int(n_old), _p(new_ids), _p(w_hot_old),
+                                               _p(w_hot_new), _p(w_host_dev), _s(stream)))
 
 
 def hl_classify(h, gids, bag_ptr, n_samples, bags_per_sample, n_lookups, flags, stream=None):

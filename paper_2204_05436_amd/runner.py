@@ -168,6 +168,30 @@ class HotPath:
         hl.hl_hot_fill(self.h, self.hot_ids, self.table.dev, self.w_hot)
         return self.n_hot
 
+    def relearn(self, batches, k: int | None = None):
+        """The learning phase again (Sec. V-B: the accelerator switches back to
+        learning from time to time; Sec. VI: twice per epoch): access counts
+        over `batches` (a sample of recent mini-batches), a new top-K hot set,
+        and the hot cache migrated to it (hl_hot_migrate: rows that leave go
+        back to the host table, rows that stay keep their trained values, rows
+        that enter come from the host table).  Waits for the steps enqueued
+        before it; refused while look-ahead plans are pending (they were made
+        with the current hot set).  Without write-back the host table holds no
+        cold-row updates, so rows that enter carry none either.  Returns the
+        new hot-set size."""
+        if self._pending:
+            raise RuntimeError("look-ahead plans made with the current hot set are pending: step them first")
+        self.sync()
+        n_old = self.n_hot
+        old = self.hot_ids[:n_old].clone()
+        w_old = self.w_hot[:n_old].clone()
+        for b in batches:
+            hl.hl_lookup_gids(self.h, b.rows, b.bag_ptr, b.n_bags, self.gids)
+            hl.hl_profile_count(self.h, self.gids, b.n_lookups)
+        self.n_hot = hl.hl_profile_topk(self.h, self.k_cap if k is None else k, self.hot_ids, reset_counts=True)
+        hl.hl_hot_migrate(self.h, old, n_old, self.hot_ids, w_old, self.w_hot, self.table.dev)
+        return self.n_hot
+
     def set_hot(self, hot_ids: torch.Tensor):
         n = int(hot_ids.numel())
         self.hot_ids[:n].copy_(hot_ids)

@@ -52,8 +52,10 @@ def table_rows(w: Workload) -> np.ndarray:
     return rows.astype(np.uint32)
 
 
-def _affine(w: Workload, t: int, n: int):
-    r = _rng(w.seed, _P_PERM, t)
+def _affine(w: Workload, t: int, n: int, phase: int = 0):
+    # phase > 0: another bijection, as if user behaviour had shifted (the skew
+    # evolves, Sec. III challenge 3); phase 0 is the stream's own
+    r = _rng(w.seed, _P_PERM, t) if phase == 0 else _rng(w.seed, _P_PERM, t, phase)
     if n == 1:
         return 1, 0
     while True:
@@ -114,8 +116,8 @@ def zipf_ranks(rng: np.random.Generator, n: int, N: int, alpha: float) -> np.nda
     return out
 
 
-def zipf_rows(w: Workload, t: int, N: int, ranks: np.ndarray) -> np.ndarray:
-    a, c = _affine(w, t, N)
+def zipf_rows(w: Workload, t: int, N: int, ranks: np.ndarray, phase: int = 0) -> np.ndarray:
+    a, c = _affine(w, t, N, phase)
     r = (np.uint64(a) * (ranks.astype(np.uint64) - np.uint64(1)) + np.uint64(c)) % np.uint64(N)
     return r.astype(np.uint32)
 
@@ -138,8 +140,10 @@ class Batch:
         return len(self.bag_ptr) - 1
 
 
-def make_batch(w: Workload, rows_per_table: np.ndarray, index: int) -> Batch:
-    """Mini-batch number `index` of the seeded stream (independent of other batches)."""
+def make_batch(w: Workload, rows_per_table: np.ndarray, index: int, phase: int = 0) -> Batch:
+    """Mini-batch number `index` of the seeded stream (independent of other
+    batches); phase > 0 maps the same Zipf ranks to other rows (a drifted
+    popularity)."""
     B, T, S = w.batch, w.n_tables, w.steps
     n_bags = B * S * T
     if w.bag_len_poisson > 0:
@@ -158,14 +162,14 @@ def make_batch(w: Workload, rows_per_table: np.ndarray, index: int) -> Batch:
             starts = bag_ptr[np.arange(B) * T + t]
             excl = np.concatenate([[0], np.cumsum(lt)[:-1]])
             pos = np.repeat(starts - excl, lt) + np.arange(tot)
-            rows[pos] = zipf_rows(w, t, N, ranks)
+            rows[pos] = zipf_rows(w, t, N, ranks, phase)
         return Batch(index, rows, bag_ptr.astype(np.int32), B, T)
 
     rows = np.empty((B, S, T), dtype=np.uint32)
     for t in range(T):
         N = int(rows_per_table[t])
         r = _rng(w.seed, _P_IDX, t, index)
-        fresh = zipf_rows(w, t, N, zipf_ranks(r, B * S, N, w.alpha)).reshape(B, S)
+        fresh = zipf_rows(w, t, N, zipf_ranks(r, B * S, N, w.alpha), phase).reshape(B, S)
         if S > 1 and w.repeat_prob > 0:
             coin = r.random((B, S)) < w.repeat_prob
             idx = fresh.copy()

@@ -26,7 +26,7 @@ def test_header_declares_the_path():
               "hl_cold_gather", "hl_cold_plan", "hl_cold_fetch", "hl_cold_scatter", "hl_embbag_fwd",
               "hl_embbag_bwd_sgd", "hl_embbag_bwd_plan", "hl_embbag_bwd_apply", "hl_dispatch", "hl_embbag_fwd_part",
               "hl_embbag_bwd_apply_part", "hl_cold_reserve", "hl_pipeline_step", "hl_pipeline_plan",
-              "hl_stream_create",
+              "hl_stream_create", "hl_hot_migrate",
               "hl_last_device_error"]:
         assert n in names
 
@@ -64,6 +64,7 @@ def test_host_side_validation():
     assert L.hl_embbag_bwd_apply(None, None, None, 0, 1, 1, 1, None, 0.1, None, 0, None) == 1
     assert L.hl_pipeline_step(None, None, None) == 1
     assert L.hl_pipeline_plan(None, None, None) == 1
+    assert L.hl_hot_migrate(None, None, 0, None, None, None, None, None) == 1
     assert hl.hl_status_string(3) == "capacity exceeded"
 
 

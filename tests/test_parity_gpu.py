@@ -646,3 +646,72 @@ def test_lookahead_chain(name, writeback):
     if writeback:
         check_close(as_f64(finals["lookahead"][1], w.dtype), as_f64(tab, w.dtype),
                     np.maximum(np.abs(as_f64(tab0, w.dtype)), 1e-3), rtol, "host table after the chain")
+
+
+@pytest.mark.parametrize("name", ["dlrm-large", "multi-hot"])
+def test_relearn_migration(name):
+    """Re-learning after training steps (with write-back): the new hot set is
+    the oracle's top-K over drifted sample batches (another rank-to-row map);
+    the hot cache and the host table after the migration equal the oracle's
+    migration of the GPU's state before it, bit for bit (so the table the path
+    reads is unchanged); a step on the new hot set matches the oracle run from
+    that state (flags, codes, cold ids, pooled output)."""
+    import oracle as O
+    from parity_lib import check_close
+    w = configs.scaled(configs.WORKLOADS[name], batch=600, row_scale=0.004, name=name + "-relearn")
+    rows = W.table_rows(w)
+    n_rows = int(rows.sum())
+    k_cap = w.k_cap(n_rows)
+    table = make_table(w, n_rows)
+    prof = [W.make_batch(w, rows, i) for i in range(4)]
+    steps = [W.make_batch(w, rows, 4 + s) for s in range(2)]
+    drift = [W.make_batch(w, rows, 8 + i, phase=1) for i in range(4)]
+    mb = W.make_batch(w, rows, 12, phase=1)
+    hp = HotPath(w, rows, table, max(b.n_lookups for b in prof + steps + drift + [mb]), w.batch, writeback=True)
+    try:
+        hp.learn([to_device(p, "cuda") for p in prof])
+        for si, sb in enumerate(steps):
+            hp.step(to_device(sb, "cuda", W.make_dy(w, 4 + si, sb.n_bags)))
+        torch.cuda.synchronize()
+        assert hp.device_error() == 0
+        n_old = hp.n_hot
+        old = hp.hot_ids[:n_old].cpu().numpy().view(np.uint32).copy()
+        w_old = hp.w_hot[:n_old].cpu().numpy().copy()
+        host0 = table.array.copy()
+        n_new = hp.relearn([to_device(b, "cuda") for b in drift])
+        torch.cuda.synchronize()
+        assert hp.device_error() == 0
+        counts = np.zeros(n_rows, np.uint32)
+        for b in drift:
+            O.count(n_rows, [O.gids(rows, b.rows, b.bag_ptr)[0]], counts)
+        new = O.topk(counts, k_cap)
+        assert np.array_equal(hp.hot_ids[:n_new].cpu().numpy().view(np.uint32), new)
+        leave, enter = np.setdiff1d(old, new), np.setdiff1d(new, old)
+        log(f"[relearn] {name}: {n_old} -> {n_new} hot rows, {len(leave)} leave, {len(enter)} enter")
+        assert len(leave) > 0 and len(enter) > 0
+        host_ref = host0.copy()
+        w_ref, n_wb = O.migrate(old, w_old, new, host_ref)
+        assert n_wb == len(leave)
+        assert np.array_equal(hp.w_hot[:n_new].cpu().numpy().view(np.uint8), w_ref.view(np.uint8)), "hot cache"
+        assert np.array_equal(table.array.view(np.uint8), host_ref.view(np.uint8)), "host table"
+        # a step on the new hot set
+        dY = W.make_dy(w, 12, mb.n_bags)
+        hp.step(to_device(mb, "cuda", dY))
+        torch.cuda.synchronize()
+        assert hp.device_error() == 0
+        B, bps, L = mb.n_samples, mb.bags_per_sample, mb.n_lookups
+        g, _ = O.gids(rows, mb.rows, mb.bag_ptr)
+        flags = O.classify(new, g, mb.bag_ptr, B, bps)
+        pop, nonpop = O.partition(flags)
+        cold, codes = O.cold_plan(g, O.remap(new, g), mb.bag_ptr, nonpop, len(nonpop), bps, k_cap)
+        stg = O.gather(host_ref, cold)
+        out, sc, _ = O.embbag_fwd(w.dtype, w_ref, k_cap, stg, codes, mb.bag_ptr, None, B, bps, B * bps,
+                                  want_scale=True)
+        assert np.array_equal(hp.flags[:B].cpu().numpy(), flags)
+        assert np.array_equal(hp.codes[:L].cpu().numpy(), codes)
+        n_cold = int(hp.n_cold.item())
+        assert np.array_equal(hp.cold_ids[:n_cold].cpu().numpy().view(np.uint32), cold)
+        check_close(hp.out[:B * bps].cpu().numpy(), out, sc, 1e-5, "pooled output after re-learning")
+    finally:
+        hp.close()
+        table.close()
