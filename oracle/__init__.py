@@ -55,6 +55,10 @@ def lib():
             "ho_embbag_bwd_sgd_flat": (None, [i32, i32, P, P, P, i64, P, f32]),
             "ho_round_bf16": (C.c_uint16, [C.c_double]),
             "ho_migrate": (i64, [u64, P, i64, P, P, i64, P, P]),
+            "ho_mix32": (u32, [u32]),
+            "ho_eal_init": (None, [i64, i32, P, P]),
+            "ho_eal_access": (None, [i64, i32, P, P, P, i64]),
+            "ho_eal_hot": (i64, [i64, i32, P, P]),
         }
         for name, (res, args) in sig.items():
             fn = getattr(L, name)
@@ -173,6 +177,29 @@ def migrate(old_ids, w_hot_old, new_ids, host):
     n = lib().ho_migrate(host.strides[0], _p(old_ids), len(old_ids), _p(w_hot_old), _p(new_ids), len(new_ids),
                          _p(out), _p(host))
     return out, int(n)
+
+
+class EAL:
+    """The SRRIP access logger (oracle): n_sets x ways (id, RRPV) entries."""
+
+    def __init__(self, n_sets: int, ways: int):
+        self.n_sets, self.ways = int(n_sets), int(ways)
+        self.tag = np.empty(self.n_sets * self.ways, np.uint32)
+        self.rrpv = np.empty(self.n_sets * self.ways, np.uint8)
+        lib().ho_eal_init(self.n_sets, self.ways, _p(self.tag), _p(self.rrpv))
+
+    def access(self, gids_):
+        g = _c(gids_, np.uint32)
+        lib().ho_eal_access(self.n_sets, self.ways, _p(self.tag), _p(self.rrpv), _p(g), len(g))
+
+    def hot(self):
+        out = np.empty(max(1, self.tag.size), np.uint32)
+        n = lib().ho_eal_hot(self.n_sets, self.ways, _p(self.tag), _p(out))
+        return out[:n].copy()
+
+
+def mix32(x: int) -> int:
+    return int(lib().ho_mix32(int(x) & 0xFFFFFFFF))
 
 
 def gather_ptr(table_ptr: int, row_bytes: int, ids, dim: int, np_dtype):

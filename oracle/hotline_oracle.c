@@ -476,5 +476,68 @@ int64_t ho_migrate(uint64_t row_bytes, const uint32_t* old_ids, int64_t n_old, c
     return wb;
 }
 
+/* ------------------------------------------------------------------ 12. SRRIP tracker */
+/* The Embedding Access Logger of Sec. V-B: a cache of embedding indices with
+ * SRRIP replacement and a 2-bit re-reference prediction value (RRPV) instead
+ * of per-row counters.  Readings (the paper gives no geometry that fits its own
+ * numbers): n_sets sets of `ways` ways; id g lives in set mix(g) % n_sets,
+ * where mix is the 32-bit finalizer of MurmurHash3 (Appleby, public domain);
+ * accesses are taken in stream order (batch by batch, lookup order); a hit
+ * sets the way's RRPV to 0; a miss takes the first way whose RRPV is 3, ageing
+ * every way of the set by one until one is, and inserts the id with RRPV 2
+ * (SRRIP's long re-reference insertion, one below the maximum).  An empty way
+ * holds the id 0xFFFFFFFF and RRPV 3.  The hot set the tracker yields is every
+ * id held at the end, ascending. */
+uint32_t ho_mix32(uint32_t x) {
+    x ^= x >> 16;
+    x *= 0x85EBCA6Bu;
+    x ^= x >> 13;
+    x *= 0xC2B2AE35u;
+    x ^= x >> 16;
+    return x;
+}
+
+void ho_eal_init(int64_t n_sets, int32_t ways, uint32_t* tag, uint8_t* rrpv) {
+    for (int64_t i = 0; i < n_sets * ways; ++i) {
+        tag[i] = 0xFFFFFFFFu;
+        rrpv[i] = 3;
+    }
+}
+
+void ho_eal_access(int64_t n_sets, int32_t ways, uint32_t* tag, uint8_t* rrpv, const uint32_t* gids, int64_t n) {
+    for (int64_t i = 0; i < n; ++i) {
+        const uint32_t g = gids[i];
+        const int64_t set = (int64_t)(ho_mix32(g) % (uint32_t)n_sets);
+        uint32_t* t = tag + set * ways;
+        uint8_t* r = rrpv + set * ways;
+        int32_t hit = -1;
+        for (int32_t w = 0; w < ways; ++w)
+            if (t[w] == g) hit = w;
+        if (hit >= 0) {
+            r[hit] = 0;
+            continue;
+        }
+        for (;;) {
+            int32_t v = -1;
+            for (int32_t w = 0; w < ways && v < 0; ++w)
+                if (r[w] == 3) v = w;
+            if (v >= 0) {
+                t[v] = g;
+                r[v] = 2;
+                break;
+            }
+            for (int32_t w = 0; w < ways; ++w) ++r[w];
+        }
+    }
+}
+
+int64_t ho_eal_hot(int64_t n_sets, int32_t ways, const uint32_t* tag, uint32_t* out) {
+    int64_t n = 0;
+    for (int64_t i = 0; i < n_sets * ways; ++i)
+        if (tag[i] != 0xFFFFFFFFu) out[n++] = tag[i];
+    qsort(out, (size_t)n, sizeof(uint32_t), cmp_u32);
+    return n;
+}
+
 /* bf16 rounding exposed for its own pin (ties-to-even cases). */
 uint16_t ho_round_bf16(double x) { return round_bf16(x); }

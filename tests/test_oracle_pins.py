@@ -422,3 +422,68 @@ def test_migrate_same_and_disjoint_sets():
     other = np.array([0, 5, 41], np.uint32)       # disjoint: every old row leaves, every new one enters
     w_new, n = O.migrate(ids, w_old, other, host)
     assert n == 4 and np.array_equal(host[ids], w_old) and np.array_equal(w_new, h0[other])
+
+
+# ---------------------------------------------------------------------------- SRRIP access logger
+def _mix32_np(x):
+    """MurmurHash3's 32-bit finalizer, written from its published definition with numpy."""
+    x = np.asarray(x, np.uint64) & np.uint64(0xFFFFFFFF)
+    x ^= x >> np.uint64(16)
+    x = (x * np.uint64(0x85EBCA6B)) & np.uint64(0xFFFFFFFF)
+    x ^= x >> np.uint64(13)
+    x = (x * np.uint64(0xC2B2AE35)) & np.uint64(0xFFFFFFFF)
+    x ^= x >> np.uint64(16)
+    return x.astype(np.uint32)
+
+
+def test_eal_hash():
+    assert O.mix32(0) == 0 and O.mix32(1) == 0x514E28B7  # published values of the finalizer
+    xs = np.random.default_rng(3).integers(0, 1 << 32, size=2000, dtype=np.uint64)
+    assert [O.mix32(int(v)) for v in xs] == _mix32_np(xs).tolist()
+
+
+# Worked by hand, one set of two ways (empty ways: RRPV 3):
+#   5: miss, way 0 (RRPV 3) -> [5:2, -:3];   7: miss, way 1 -> [5:2, 7:2]
+#   5: hit -> [5:0, 7:2];   9: miss, no 3: age -> [5:1, 7:3], way 1 -> [5:1, 9:2]
+#   7: miss, no 3: age -> [5:2, 9:3], way 1 -> [5:2, 7:2]
+#   11: miss, no 3: age -> [5:3, 7:3], first 3 is way 0 -> [11:2, 7:3];  hot = [7, 11]
+# Scan resistance, one set of four ways: A B C D fill it (RRPV 2), A B hit (0);
+# a scan X1..X4 of ids seen once: X1 ages the set (A B at 1, C D at 3) and takes
+# C, X2 takes D, X3 ages again (A B at 2, X1 X2 at 3) and takes X1, X4 takes X2:
+# A and B stay (LRU would have evicted them).
+def test_eal_hand_examples():
+    e = O.EAL(1, 2)
+    e.access([5, 7, 5, 9, 7, 11])
+    assert e.tag.tolist() == [11, 7] and e.rrpv.tolist() == [2, 3] and e.hot().tolist() == [7, 11]
+    e = O.EAL(1, 4)
+    e.access([1, 2, 3, 4, 1, 2, 11, 12, 13, 14])
+    assert e.tag.tolist() == [1, 2, 13, 14] and e.rrpv.tolist() == [2, 2, 2, 2]
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_eal_invariants(seed):
+    """Random Zipf-like streams: every held id sits in its own set, at most once;
+    RRPVs are in 0..3 and empty ways hold 3; the last id accessed in each set is
+    held (RRPV 0 or 2); with at least as many ways as distinct ids per set
+    nothing is evicted, so the hot set is every id seen."""
+    rng = np.random.default_rng(seed)
+    n_sets, ways = int(rng.integers(1, 40)), int(rng.integers(1, 9))
+    ids = (rng.zipf(1.3, size=int(rng.integers(1, 3000))) * 7919 % 100003).astype(np.uint32)
+    e = O.EAL(n_sets, ways)
+    for chunk in np.array_split(ids, 3):
+        e.access(chunk)
+    tag, rr = e.tag.reshape(n_sets, ways), e.rrpv.reshape(n_sets, ways)
+    assert (rr <= 3).all()
+    assert (rr[tag == 0xFFFFFFFF] == 3).all()
+    for s in range(n_sets):
+        held = tag[s][tag[s] != 0xFFFFFFFF]
+        assert len(set(held.tolist())) == len(held)
+        assert ((_mix32_np(held) % np.uint32(n_sets)) == s).all()
+    sets = _mix32_np(ids) % np.uint32(n_sets)
+    for s in np.unique(sets):
+        last = ids[np.flatnonzero(sets == s)[-1]]
+        w = np.flatnonzero(tag[s] == last)
+        assert len(w) == 1 and rr[s, w[0]] in (0, 2)
+    big = O.EAL(n_sets, max(len(np.unique(ids[sets == s])) for s in np.unique(sets)))
+    big.access(ids)
+    assert np.array_equal(big.hot(), np.unique(ids))
