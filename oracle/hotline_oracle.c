@@ -486,8 +486,9 @@ int64_t ho_migrate(uint64_t row_bytes, const uint32_t* old_ids, int64_t n_old, c
  * sets the way's RRPV to 0; a miss takes the first way whose RRPV is 3, ageing
  * every way of the set by one until one is, and inserts the id with RRPV 2
  * (SRRIP's long re-reference insertion, one below the maximum).  An empty way
- * holds the id 0xFFFFFFFF and RRPV 3.  The hot set the tracker yields is every
- * id held at the end, ascending. */
+ * holds the id 0xFFFFFFFF and RRPV 3, and an access with that id (the id of a
+ * row out of range) is not logged.  The hot set the tracker yields is every id
+ * held at the end, ascending. */
 uint32_t ho_mix32(uint32_t x) {
     x ^= x >> 16;
     x *= 0x85EBCA6Bu;
@@ -507,6 +508,7 @@ void ho_eal_init(int64_t n_sets, int32_t ways, uint32_t* tag, uint8_t* rrpv) {
 void ho_eal_access(int64_t n_sets, int32_t ways, uint32_t* tag, uint8_t* rrpv, const uint32_t* gids, int64_t n) {
     for (int64_t i = 0; i < n; ++i) {
         const uint32_t g = gids[i];
+        if (g == 0xFFFFFFFFu) continue;
         const int64_t set = (int64_t)(ho_mix32(g) % (uint32_t)n_sets);
         uint32_t* t = tag + set * ways;
         uint8_t* r = rrpv + set * ways;

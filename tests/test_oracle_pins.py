@@ -458,6 +458,8 @@ def test_eal_hand_examples():
     e = O.EAL(1, 4)
     e.access([1, 2, 3, 4, 1, 2, 11, 12, 13, 14])
     assert e.tag.tolist() == [1, 2, 13, 14] and e.rrpv.tolist() == [2, 2, 2, 2]
+    e.access([0xFFFFFFFF] * 5)  # the id of a row out of range is not logged
+    assert e.tag.tolist() == [1, 2, 13, 14] and e.rrpv.tolist() == [2, 2, 2, 2]
 
 
 @pytest.mark.parametrize("seed", range(8))
