@@ -128,6 +128,30 @@ hl_status hl_set_hot(hl_handle* h, const uint32_t* hot_ids, uint32_t n_hot, hl_s
  * rows are copied to GPU memory after learning, Sec. IV). */
 hl_status hl_hot_fill(const hl_handle* h, const uint32_t* hot_ids, const void* w_host, void* w_hot,
                       hl_stream stream);
+/* The Embedding Access Logger with SRRIP replacement (Sec. V-B: a cache of
+ * row ids with a 2-bit re-reference prediction value per entry, in place of a
+ * counter per row; compared with exact counting, the "Oracle LFU", in the
+ * paper's tracker figure).  n_sets sets of `ways` ways (1..16); row id g lives
+ * in set mix(g) % n_sets, mix being the 32-bit finalizer of MurmurHash3; a hit
+ * sets the entry's value to 0; a miss takes the first way whose value is 3,
+ * ageing every way of the set by one until one is, and enters with 2; empty
+ * ways hold 3.  hl_eal_access feeds one batch of row ids (device, in lookup
+ * order; an id 0xFFFFFFFF is skipped) in stream order, asynchronously on
+ * `stream`; batches take effect in call order.  hl_eal_hot writes every id the
+ * logger holds, ascending, to hot_ids_out (device, n_sets * ways entries) and
+ * their number to *n_hot_out (host; synchronous): a hot set for hl_set_hot.
+ * hl_eal_state copies the entries (ids, values; set-major, n_sets * ways each,
+ * device) for inspection.  hl_eal_create allocates the logger (empty) and its
+ * workspace for up to max_lookups ids per call; HL_ERR_CAPACITY: more ids in
+ * one call; HL_ERR_INVALID_ARG: ways outside 1..16, n_sets 0, NULL. */
+typedef struct hl_eal hl_eal;
+hl_status hl_eal_create(hl_handle* h, uint32_t n_sets, int32_t ways, int64_t max_lookups, hl_eal** out);
+hl_status hl_eal_destroy(hl_eal* e);
+hl_status hl_eal_reset(hl_eal* e, hl_stream stream);
+hl_status hl_eal_access(hl_eal* e, const uint32_t* gids, int64_t n, hl_stream stream);
+hl_status hl_eal_hot(hl_eal* e, uint32_t* hot_ids_out, uint32_t* n_hot_out, hl_stream stream);
+hl_status hl_eal_state(const hl_eal* e, uint32_t* tags_out, uint8_t* rrpv_out, hl_stream stream);
+
 /* Hot-set migration of the recurring learning phase (Sec. V-B: the EAL
  * switches back to learning from time to time; Sec. VI: twice per epoch;
  * Sec. IV: hot rows are trained on the GPU, the others in CPU memory).  Call

@@ -57,6 +57,12 @@ _SIGS = {
     "hl_set_hot": (C.c_int, [P, P, U32, P]),
     "hl_hot_fill": (C.c_int, [P, P, P, P, P]),
     "hl_hot_migrate": (C.c_int, [P, P, U32, P, P, P, P, P]),
+    "hl_eal_create": (C.c_int, [P, U32, I32, I64, C.POINTER(P)]),
+    "hl_eal_destroy": (C.c_int, [P]),
+    "hl_eal_reset": (C.c_int, [P, P]),
+    "hl_eal_access": (C.c_int, [P, P, I64, P]),
+    "hl_eal_hot": (C.c_int, [P, P, C.POINTER(U32), P]),
+    "hl_eal_state": (C.c_int, [P, P, P, P]),
     "hl_classify": (C.c_int, [P, P, P, I32, I32, I64, P, P]),
     "hl_partition": (C.c_int, [P, P, I32, P, P, P, P, SZ, P]),
     "hl_remap": (C.c_int, [P, P, I64, P, P]),
@@ -221,6 +227,47 @@ def hl_hot_fill(h, hot_ids, w_host_dev, w_hot, stream=None):
 def hl_hot_migrate(h, old_ids, n_old, new_ids, w_hot_old, w_hot_new, w_host_dev, stream=None):
     _ck("hl_hot_migrate", lib().hl_hot_migrate(h.ptr, _p(old_ids), int(n_old), _p(new_ids), _p(w_hot_old),
                                                _p(w_hot_new), _p(w_host_dev), _s(stream)))
+
+
+class EAL:
+    """An SRRIP access logger (hl_eal_*)."""
+
+    def __init__(self, h, n_sets, ways, max_lookups):
+        self.ptr = P()
+        _ck("hl_eal_create", lib().hl_eal_create(h.ptr, int(n_sets), int(ways), int(max_lookups),
+                                                 C.byref(self.ptr)))
+        self.n_sets, self.ways = int(n_sets), int(ways)
+
+    def close(self):
+        if self.ptr:
+            _ck("hl_eal_destroy", lib().hl_eal_destroy(self.ptr))
+            self.ptr = P()
+
+
+def hl_eal_create(h, n_sets, ways, max_lookups):
+    return EAL(h, n_sets, ways, max_lookups)
+
+
+def hl_eal_destroy(e):
+    e.close()
+
+
+def hl_eal_reset(e, stream=None):
+    _ck("hl_eal_reset", lib().hl_eal_reset(e.ptr, _s(stream)))
+
+
+def hl_eal_access(e, gids, n, stream=None):
+    _ck("hl_eal_access", lib().hl_eal_access(e.ptr, _p(gids), int(n), _s(stream)))
+
+
+def hl_eal_hot(e, hot_ids_out, stream=None):
+    n = U32()
+    _ck("hl_eal_hot", lib().hl_eal_hot(e.ptr, _p(hot_ids_out), C.byref(n), _s(stream)))
+    return int(n.value)
+
+
+def hl_eal_state(e, tags_out, rrpv_out, stream=None):
+    _ck("hl_eal_state", lib().hl_eal_state(e.ptr, _p(tags_out), _p(rrpv_out), _s(stream)))
 
 
 def hl_classify(h, gids, bag_ptr, n_samples, bags_per_sample, n_lookups, flags, stream=None):

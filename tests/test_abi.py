@@ -26,7 +26,7 @@ def test_header_declares_the_path():
               "hl_cold_gather", "hl_cold_plan", "hl_cold_fetch", "hl_cold_scatter", "hl_embbag_fwd",
               "hl_embbag_bwd_sgd", "hl_embbag_bwd_plan", "hl_embbag_bwd_apply", "hl_dispatch", "hl_embbag_fwd_part",
               "hl_embbag_bwd_apply_part", "hl_cold_reserve", "hl_pipeline_step", "hl_pipeline_plan",
-              "hl_stream_create", "hl_hot_migrate",
+              "hl_stream_create", "hl_hot_migrate", "hl_eal_create", "hl_eal_access", "hl_eal_hot",
               "hl_last_device_error"]:
         assert n in names
 
@@ -65,6 +65,10 @@ def test_host_side_validation():
     assert L.hl_pipeline_step(None, None, None) == 1
     assert L.hl_pipeline_plan(None, None, None) == 1
     assert L.hl_hot_migrate(None, None, 0, None, None, None, None, None) == 1
+    e = C.c_void_p()
+    assert L.hl_eal_create(None, 4, 2, 10, C.byref(e)) == 1
+    assert L.hl_eal_access(None, None, 0, None) == 1
+    assert L.hl_eal_hot(None, None, None, None) == 1
     assert hl.hl_status_string(3) == "capacity exceeded"
 
 

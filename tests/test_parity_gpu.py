@@ -715,3 +715,47 @@ def test_relearn_migration(name):
     finally:
         hp.close()
         table.close()
+
+
+@pytest.mark.parametrize("name,geom", [("tiny", None), ("tbsm", None), ("multi-hot", None), ("dlrm-small", (7, 3)),
+                                       ("dlrm-large", (4096, 16))])
+def test_eal_srrip(name, geom):
+    """The SRRIP access logger against the oracle's, bit for bit: every entry
+    (id and 2-bit value) after each profiling batch, fed through the GPU's own
+    gids (with a few rows out of range), and the hot set it yields.  Default
+    geometry: 16 ways and K / 16 sets (as many entries as the hot cache); the
+    others force evictions in every set."""
+    import oracle as O
+    w0 = configs.WORKLOADS[name]
+    w = configs.scaled(w0, batch=min(w0.batch, 1024), row_scale=0.02, name=name + "-eal") \
+        if name in ("dlrm-small", "dlrm-large", "multi-hot") else w0
+    rows = W.table_rows(w)
+    n_rows = int(rows.sum())
+    k_cap = w.k_cap(n_rows)
+    n_sets, ways = geom if geom else (max(1, k_cap // 16), 16)
+    batches = [W.make_batch(w, rows, i) for i in range(6)]
+    batches[2].rows[::97] = np.uint32(0xFFFFFFFF)  # rows out of range: ids 0xFFFFFFFF, not logged
+    h = hl.hl_create(rows, w.dim, w.dtype, k_cap)
+    e = hl.EAL(h, n_sets, ways, max(b.n_lookups for b in batches))
+    oe = O.EAL(n_sets, ways)
+    try:
+        gids = torch.zeros(max(b.n_lookups for b in batches), dtype=torch.int32, device="cuda")
+        tags = torch.zeros(n_sets * ways, dtype=torch.int32, device="cuda")
+        rr = torch.zeros(n_sets * ways, dtype=torch.uint8, device="cuda")
+        for bi, b in enumerate(batches):
+            db = to_device(b, "cuda")
+            hl.hl_lookup_gids(h, db.rows, db.bag_ptr, db.n_bags, gids)
+            hl.hl_eal_access(e, gids, b.n_lookups)
+            g, _ = O.gids(rows, b.rows, b.bag_ptr)
+            oe.access(g)
+            hl.hl_eal_state(e, tags, rr)
+            torch.cuda.synchronize()
+            assert np.array_equal(tags.cpu().numpy().view(np.uint32), oe.tag), f"batch {bi}: ids"
+            assert np.array_equal(rr.cpu().numpy(), oe.rrpv), f"batch {bi}: values"
+        hot = torch.zeros(n_sets * ways, dtype=torch.int32, device="cuda")
+        n = hl.hl_eal_hot(e, hot)
+        assert np.array_equal(hot[:n].cpu().numpy().view(np.uint32), oe.hot())
+        log(f"[eal] {name}: {n_sets}x{ways}: holds {n} ids")
+    finally:
+        e.close()
+        hl.hl_destroy(h)
