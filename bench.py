@@ -126,6 +126,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--breakdown", action="store_true", help="also time reference schedules and the stages")
     ap.add_argument("--no-relearn", action="store_true", help="skip the timed re-learning (hot-set migration)")
+    ap.add_argument("--eal-study", action="store_true", help="compare the SRRIP logger with exact top-K on every workload")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build measures one GPU only (asked for --gpus {args.gpus}); the path shards "
@@ -300,6 +301,16 @@ def main():
     # the learning phase again (after the measured steps, so it changes nothing
     # above): counts over a sample of batches whose popularity has drifted (the
     # same Zipf ranks on other rows), the new top-K, and the hot-cache migration
+    # the SRRIP access logger against the exact hot set learnt above, at its size
+    eal = eal_compare(hp.h, dprof, dmeas[:8], hp.hot_ids[:hp.n_hot].clone(), hp.n_hot)
+    log(f"[bench] SRRIP logger ({eal['sets']} sets x {eal['ways']} ways): holds {eal['captured_frac']:.3f} of the "
+        f"exact hot set; lookups hot {eal['lookups_hot_frac']['srrip']:.3f} vs {eal['lookups_hot_frac']['exact']:.3f}; "
+        f"{eal['us_per_batch']:.1f} us per batch")
+    eal_all = None
+    if args.eal_study:
+        eal_all = {}
+        eal_study(eal_all)
+
     relearn = None
     if not args.no_relearn:
         drift = [to_device(W.make_batch(w, rows, 1000 + i, phase=1), dev) for i in range(w.profile_batches)]
@@ -346,10 +357,95 @@ def main():
         "unique_rows_per_batch": avg["U"], "cold_rows_per_batch": avg["n_cold"],
         "learning_phase_ms": learn_ms, "kernels": kernels,
         "roofline": roof, "link_roofline": link, "cpu_baseline": cpu, "breakdown": breakdown, "relearn": relearn,
+        "srrip_logger": eal, "srrip_logger_all_workloads": eal_all,
     }
     print(json.dumps(res), flush=True)
     hp.close()
     table.close()
+
+
+def eal_compare(h, prof, meas, exact, capacity, ways=16):
+    """The SRRIP access logger (hl_eal_*) against exact counting at the same
+    capacity: the logger gets floor(capacity / ways) sets and the profiling
+    batches (device batches), and its hot set is compared with the exact one
+    (device ids): the share of the exact set it holds, and the share of the
+    measured batches' lookups, and of their samples (popular: every lookup hot),
+    each set covers.  Also the logger's time per batch (HIP events)."""
+    import torch
+    from paper_2204_05436_amd import hotline as hl
+    n_sets = max(1, capacity // ways)
+    max_l = max(b.n_lookups for b in prof + meas)
+    e = hl.EAL(h, n_sets, ways, max_l)
+    gids = torch.zeros(max_l, dtype=torch.int32, device="cuda")
+    try:
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        ms = 0.0
+        for b in prof:
+            hl.hl_lookup_gids(h, b.rows, b.bag_ptr, b.n_samples * b.bps, gids)
+            e0.record()
+            hl.hl_eal_access(e, gids, b.n_lookups)
+            e1.record()
+            torch.cuda.synchronize()
+            ms += e0.elapsed_time(e1)
+        held = torch.zeros(n_sets * ways, dtype=torch.int32, device="cuda")
+        n = hl.hl_eal_hot(e, held)
+        held = held[:n]
+        sets = {"srrip": held, "exact": exact}
+        cov = {k: [0, 0] for k in sets}
+        pop = {k: [0, 0] for k in sets}
+        for b in meas:
+            L = b.n_lookups
+            hl.hl_lookup_gids(h, b.rows, b.bag_ptr, b.n_samples * b.bps, gids)
+            ptr = b.bag_ptr.long()
+            starts, ends = ptr[0:-1:b.bps][:b.n_samples], ptr[b.bps::b.bps][:b.n_samples]
+            for k, ids in sets.items():
+                hot = torch.isin(gids[:L], ids)
+                cov[k][0] += int(hot.sum())
+                cov[k][1] += L
+                cs = torch.cat([torch.zeros(1, dtype=torch.long, device="cuda"), torch.cumsum((~hot).long(), 0)])
+                pop[k][0] += int(((cs[ends] - cs[starts]) == 0).sum())
+                pop[k][1] += b.n_samples
+        inter = int(torch.isin(held, exact).sum())
+        return {"capacity": n_sets * ways, "sets": n_sets, "ways": ways, "exact_hot": int(exact.numel()),
+                "srrip_hot": int(n), "captured_frac": inter / max(1, int(exact.numel())),
+                "lookups_hot_frac": {k: v[0] / max(1, v[1]) for k, v in cov.items()},
+                "popular_samples_frac": {k: v[0] / max(1, v[1]) for k, v in pop.items()},
+                "us_per_batch": ms * 1e3 / max(1, len(prof)),
+                "lookups_per_s": sum(b.n_lookups for b in prof) / max(1e-9, ms * 1e-3)}
+    finally:
+        e.close()
+
+
+def eal_study(out):
+    """The comparison on every workload (full size, 16 profiling batches, 8
+    measured ones), capacity = the hot-set size K, 16 ways."""
+    import torch
+    from paper_2204_05436_amd import configs, hotline as hl, workload as W
+    from paper_2204_05436_amd.runner import to_device
+    for name in configs.ORDER:
+        w = configs.WORKLOADS[name]
+        rows = W.table_rows(w)
+        n_rows = int(rows.sum(dtype=np.int64))
+        k_cap = w.k_cap(n_rows)
+        prof = [to_device(W.make_batch(w, rows, i), "cuda") for i in range(w.profile_batches)]
+        meas = [to_device(W.make_batch(w, rows, w.profile_batches + i), "cuda") for i in range(8)]
+        h = hl.hl_create(rows, w.dim, w.dtype, k_cap)
+        try:
+            gids = torch.zeros(max(b.n_lookups for b in prof), dtype=torch.int32, device="cuda")
+            for b in prof:
+                hl.hl_lookup_gids(h, b.rows, b.bag_ptr, b.n_samples * b.bps, gids)
+                hl.hl_profile_count(h, gids, b.n_lookups)
+            exact = torch.zeros(min(k_cap, n_rows), dtype=torch.int32, device="cuda")
+            n_hot = hl.hl_profile_topk(h, k_cap, exact, reset_counts=True)
+            r = eal_compare(h, prof, meas, exact[:n_hot], min(k_cap, n_hot))
+        finally:
+            hl.hl_destroy(h)
+        r["k_cap"] = k_cap
+        out[name] = r
+        log(f"[bench] SRRIP logger on {name}: holds {r['captured_frac']:.3f} of the exact hot set "
+            f"({r['exact_hot']} ids, capacity {r['capacity']}); lookups hot {r['lookups_hot_frac']['srrip']:.3f} vs "
+            f"{r['lookups_hot_frac']['exact']:.3f}; popular samples {r['popular_samples_frac']['srrip']:.3f} vs "
+            f"{r['popular_samples_frac']['exact']:.3f}")
 
 
 def cpu_baseline(w, rows, prof, meas, meas_idx, table, k_cap, budget_s):
