@@ -127,6 +127,10 @@ def main():
     ap.add_argument("--breakdown", action="store_true", help="also time reference schedules and the stages")
     ap.add_argument("--no-relearn", action="store_true", help="skip the timed re-learning (hot-set migration)")
     ap.add_argument("--eal-study", action="store_true", help="compare the SRRIP logger with exact top-K on every workload")
+    ap.add_argument("--pmc", action="store_true",
+                    help="for a counter run under rocprofv3 --pmc: warmup + --steps steps of the same kernels on one "
+                         "stream, then one device copy of known size (the counters' calibration); prints that size "
+                         "and exits")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build measures one GPU only (asked for --gpus {args.gpus}); the path shards "
@@ -170,6 +174,26 @@ def main():
     torch.cuda.synchronize()
     learn_ms = e0.elapsed_time(e1)
     log(f"[bench] learning phase {learn_ms:.2f} ms, n_hot {n_hot}")
+
+    if args.pmc:
+        # the same kernels one at a time on one stream: a counter run
+        # serializes dispatches, which the pipelined schedule's cross-stream
+        # waits would stall on
+        for i in range(args.warmup + args.steps):
+            hp.step(dmeas[i % len(dmeas)], mode="sequential")
+        torch.cuda.synchronize()
+        n_cal = 256 << 20
+        src = torch.ones(n_cal // 4, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        err = hp.device_error()
+        print(json.dumps({"mode": "pmc", "workload": w.name, "steps": args.warmup + args.steps, "device_error": err,
+                          "calibration_copy_bytes": n_cal}), flush=True)
+        hp.close()
+        table.close()
+        return
 
     # per-batch statistics (untimed pass over every measured batch)
     # steps are issued from a stream of their own (work on the default stream
@@ -285,8 +309,12 @@ def main():
         raise SystemExit(f"no byte model for the dominant kernel {dom}")
     kd = kernels[dom]
     ach = kernel_bytes(dom, avg) / (kd["avg_us"] * 1e-6)
+    # measured HBM bytes per launch (counters, same kernel source), as a rate
+    # over the same launch duration as `achieved`
+    tb = counter_traffic(dom, w.name)
     roof = {"kernel": dom, "bound": "hbm", "achieved": ach / 1e9, "peak": HBM_PEAK / 1e9, "unit": "GB/s",
-            "frac": ach / HBM_PEAK, "traffic": None, "avg_us": kd["avg_us"],
+            "frac": ach / HBM_PEAK, "traffic": None if tb is None else tb / (kd["avg_us"] * 1e-6) / 1e9,
+            "traffic_bytes_per_launch": tb, "avg_us": kd["avg_us"],
             "algorithmic_bytes_per_launch": kernel_bytes(dom, avg)}
     link = None
     if "cg_fetch" in kernels:
@@ -362,6 +390,29 @@ def main():
     print(json.dumps(res), flush=True)
     hp.close()
     table.close()
+
+
+def counter_traffic(kernel, workload):
+    """HBM bytes per launch of `kernel` from the committed counter summary
+    (profiles/<workload>_kernel_traffic.md: FETCH_SIZE and WRITE_SIZE runs,
+    calibrated with a copy of known size), or None when there is none or the
+    kernel's source file has changed since the counters were taken."""
+    import hashlib
+    here = os.path.dirname(os.path.abspath(__file__))
+    path = os.path.join(here, "profiles", f"{workload}_kernel_traffic.md")
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    m = __import__("re").search(r"```traffic\n(.*?)```", text, __import__("re").S)
+    if not m:
+        return None
+    for line in m.group(1).splitlines():
+        f = line.split()
+        if len(f) == 4 and f[0] == kernel:
+            src = os.path.join(here, f[2])
+            if os.path.exists(src) and hashlib.sha1(open(src, "rb").read()).hexdigest() == f[3]:
+                return int(f[1])
+    return None
 
 
 def eal_compare(h, prof, meas, exact, capacity, ways=16):
