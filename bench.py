@@ -20,8 +20,10 @@ schedules and a per-stage breakdown.
 
 Prints one JSON line on stdout; progress goes to stderr."""
 import argparse
+import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -371,9 +373,9 @@ def main():
                    "zipf_alpha": w.alpha, "hot_cache_rows": k_cap, "n_hot": n_hot,
                    "profile_batches": w.profile_batches, "measured_batches": w.measured_batches,
                    "parallelism": "single-gpu"},
-        "schedule": "pipelined by the native scheduler: the host-link fetch on 32 compute units, the look-ahead "
+        "schedule": "pipelined by the native scheduler: the host-link fetch on 8 compute units, the look-ahead "
                     "plans (dispatch, cold plan, grouping of the next mini-batch, during the step before) on 64, "
-                    "the forwards and the backward on the other 160",
+                    "the forwards and the backward on the other 184",
         "host_enqueue_ms_per_step": host_ms / K,
         "fwd_bwd_kernel_us": t_fb * 1e3,
         "fwd_bwd_lookups_per_s": avg["L"] / (t_fb / 1e3),
@@ -397,13 +399,12 @@ def counter_traffic(kernel, workload):
     (profiles/<workload>_kernel_traffic.md: FETCH_SIZE and WRITE_SIZE runs,
     calibrated with a copy of known size), or None when there is none or the
     kernel's source file has changed since the counters were taken."""
-    import hashlib
     here = os.path.dirname(os.path.abspath(__file__))
     path = os.path.join(here, "profiles", f"{workload}_kernel_traffic.md")
     if not os.path.exists(path):
         return None
     text = open(path).read()
-    m = __import__("re").search(r"```traffic\n(.*?)```", text, __import__("re").S)
+    m = re.search(r"```traffic\n(.*?)```", text, re.S)
     if not m:
         return None
     for line in m.group(1).splitlines():

@@ -422,9 +422,10 @@ typedef struct hl_step_io {
 #define HL_STEP_PLANNED 2u
 /* fetch_cus compute units [0, fetch_cus) run the host-link copy (0: no masks
  * at all); plan_cus > 0 gives the look-ahead plans the next plan_cus units of
- * their own (0: they share main's).  Masks in multiples of 32 units keep every
- * shader engine of every XCD equally loaded (others measured up to 30% slower);
- * fetch 32, plan 64, main the other 160 measured fastest here. */
+ * their own (0: they share main's).  Masks in multiples of 8 units keep every
+ * XCD equally loaded (plans on 56 or 48 units measured 35% slower steps); fetch
+ * 8, plan 64, main the other 184 measured fastest here.  The runtime refuses
+ * masks of fewer than 8 units. */
 hl_status hl_pipeline_create(hl_handle* h, int32_t fetch_cus, int32_t plan_cus, hl_pipeline** out);
 hl_status hl_pipeline_destroy(hl_pipeline* p);
 hl_status hl_pipeline_step(hl_pipeline* p, const hl_step_io* io, hl_stream stream);

@@ -196,15 +196,16 @@ eb_fwd(const void* w_hot_, const void* stg_, int32_t stg_rows, uint32_t n_hot, u
        const int32_t* __restrict__ codes, const int32_t* __restrict__ bag_ptr, int32_t bps,
        const int32_t* __restrict__ sample_ids, const int32_t* n_sel_dev, int32_t n_sel_max,
        float* __restrict__ out, eb_geom g, int64_t n_lookups, int64_t n_bags_total, int32_t n_samples,
-       uint32_t* err) {
+       uint32_t* err, hl_hook hk) {
   typedef typename RowIO<VEC, BF>::T T;
   const T* w_hot = (const T*)w_hot_;
   const T* stg = (const T*)stg_;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int gi = lane / g.G, gl = lane - gi * g.G;
+  hl_hook_head(hk);
   if (blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0 && bag_ptr[n_bags_total] != n_lookups)
     hl_flag(err, HL_DEVERR_SHAPE);
-  if (gi >= g.NG) return;
+  if (gi >= g.NG) return;  // (never thread 0, which carries the handover)
   const int32_t colv = blockIdx.y * 64 + gl;
   const bool cact = colv < g.vpr;
   const int64_t col = (int64_t)colv * VEC;
@@ -297,6 +298,7 @@ eb_fwd(const void* w_hot_, const void* stg_, int32_t stg_rows, uint32_t n_hot, u
       if (cact) st_f32<VEC>(out + bag[u] * g.D + col, acc);
     }
   }
+  hl_hook_tail(hk);
 }
 
 // ----------------------------------------------------------------------------- backward
@@ -506,9 +508,11 @@ __global__ void __launch_bounds__(RB_BLOCK)
 bw_reduce1(const uint32_t* __restrict__ keys, const uint32_t* __restrict__ vals, uint32_t n,
            const float* __restrict__ dY, eb_geom g, void* w_hot, void* stg, uint32_t n_hot, float lr,
            float* __restrict__ tfirst, float* __restrict__ tlast, uint32_t* __restrict__ tflag,
-           uint32_t* __restrict__ tkey, float* __restrict__ gc, uint32_t gc_rows, uint32_t* __restrict__ bnd) {
+           uint32_t* __restrict__ tkey, float* __restrict__ gc, uint32_t gc_rows, uint32_t* __restrict__ bnd,
+           hl_hook hk) {
   typedef typename RowIO<VEC, BF>::T T;
   __shared__ float pf[RB_WAVES * 64 * VEC], pl[RB_WAVES * 64 * VEC];
+  hl_hook_head(hk);
   __shared__ uint32_t gflag[RB_WAVES * 64], gkey[RB_WAVES * 64];
   __shared__ uint32_t s_tflag;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
@@ -672,6 +676,7 @@ bw_reduce1(const uint32_t* __restrict__ keys, const uint32_t* __restrict__ vals,
   }
   __syncthreads();
   if (threadIdx.x == 0 && blockIdx.y == 0) tflag[tile] = s_tflag;
+  hl_hook_tail(hk);
 }
 
 // Segments spanning tiles: the tile where a segment starts (flag L) sums its
@@ -762,8 +767,9 @@ bw_reduce2(uint32_t n_tiles, eb_geom g, void* w_hot, void* stg, uint32_t n_hot, 
 template <int VEC, bool BF>
 __global__ void __launch_bounds__(256)
 bw_cold(const uint32_t* __restrict__ keys, uint32_t n, eb_geom g, void* stg, uint32_t n_hot, float lr,
-        const float* __restrict__ gc, uint32_t gc_rows, const uint32_t* __restrict__ bnd) {
+        const float* __restrict__ gc, uint32_t gc_rows, const uint32_t* __restrict__ bnd, hl_hook hk) {
   typedef typename RowIO<VEC, BF>::T T;
+  hl_hook_head(hk);
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int gi = lane / g.G, gl = lane - gi * g.G;
   const int32_t colv = blockIdx.y * 64 + gl;
@@ -807,6 +813,7 @@ bw_cold(const uint32_t* __restrict__ keys, uint32_t n, eb_geom g, void* stg, uin
       for (int q = 0; q < 4 * g.NG && m; ++q) m &= m - 1;
     }
   }
+  hl_hook_tail(hk);
 }
 
 // The cold half of the forward from the backward's grouping: the sorted tail
@@ -943,10 +950,11 @@ static void launch_fwd(const hl_handle* h, dim3 grid, hipStream_t s, const void*
                        int32_t stg_rows, const int32_t* codes, const int32_t* bag_ptr, int32_t bps,
                        const int32_t* ids, const int32_t* n_dev, int32_t n_max, float* out, eb_geom g,
                        int64_t n_lookups, int64_t n_bags, int part) {
+  const hl_hook hk = hl_hook_take(h);
 #define EBF(P)                                                                                                   \
   HL_KERNEL(h, s, P == 0 ? "eb_fwd" : (P == 1 ? "eb_fwd_hot" : "eb_fwd_cold"), (eb_fwd<VEC, BF, P>), grid,       \
             dim3(256), 0, s, w_hot, stg, stg_rows, h->n_hot, h->k_cap, codes, bag_ptr, bps, ids, n_dev, n_max, out, \
-            g, n_lookups, n_bags, (int32_t)(n_bags / bps), h->d_err);
+            g, n_lookups, n_bags, (int32_t)(n_bags / bps), h->d_err, hk);
   if (part == 0) { EBF(0) }
   else if (part == 1) { EBF(1) }
   else { EBF(2) }
@@ -1002,12 +1010,13 @@ static void launch_bwd(const hl_handle* h, uint32_t tiles, hipStream_t s, const 
   const dim3 grid(tiles, g.cchunks);
   if (part == 0) {
     HL_KERNEL(h, s, "bw_reduce1", (bw_reduce1<VEC, BF, false>), grid, dim3(RB_BLOCK), 0, s, sk, sv, n, dY, g, w_hot,
-              stg, n_hot, lr, ws.tfirst, ws.tlast, ws.tflag, ws.tkey, ws.gc, ws.gc_rows, ws.bnd);
+              stg, n_hot, lr, ws.tfirst, ws.tlast, ws.tflag, ws.tkey, ws.gc, ws.gc_rows, ws.bnd, hl_hook{});
     HL_KERNEL(h, s, "bw_reduce2", (bw_reduce2<VEC, BF, false>), grid, dim3(RB_BLOCK), 0, s, tiles, g, w_hot, stg,
               n_hot, lr, ws.tfirst, ws.tlast, ws.tflag, ws.tkey, ws.gc, ws.gc_rows);
   } else if (part == 1 || part == 3) {
     HL_KERNEL(h, s, "bw_reduce1", (bw_reduce1<VEC, BF, true>), grid, dim3(RB_BLOCK), 0, s, sk, sv, n, dY, g, w_hot,
-              stg, n_hot, lr, ws.tfirst, ws.tlast, ws.tflag, ws.tkey, ws.gc, ws.gc_rows, ws.bnd);
+              stg, n_hot, lr, ws.tfirst, ws.tlast, ws.tflag, ws.tkey, ws.gc, ws.gc_rows, ws.bnd,
+              part == 3 ? hl_hook_take(h) : hl_hook{});
     if (part == 1)
       HL_KERNEL(h, s, "bw_reduce2", (bw_reduce2<VEC, BF, true>), grid, dim3(RB_BLOCK), 0, s, tiles, g, w_hot, stg,
                 n_hot, lr, ws.tfirst, ws.tlast, ws.tflag, ws.tkey, ws.gc, ws.gc_rows);
@@ -1017,7 +1026,7 @@ static void launch_bwd(const hl_handle* h, uint32_t tiles, hipStream_t s, const 
     uint32_t b = hl_div_up(n, 256);
     if (b > 128) b = 128;
     HL_KERNEL(h, s, "bw_cold", (bw_cold<VEC, BF>), dim3(b, g.cchunks), dim3(256), 0, s, sk, n, g, stg, n_hot, lr,
-              ws.gc, ws.gc_rows, ws.bnd);
+              ws.gc, ws.gc_rows, ws.bnd, hl_hook{});
   }
 }
 
@@ -1218,7 +1227,7 @@ hl_status hl_embbag_finish_cold(hl_handle* h, void* w_hot, void* staging, int32_
               w_hot, h->n_hot, lr, ws.tfirst, ws.tlast, ws.tflag, ws.tkey, ws.gc, ws.gc_rows, sk, sv, n, ws.bnd, g, \
               staging, stg_rows, h->k_cap, codes, bag_ptr, out, h->d_err);                                         \
     HL_KERNEL(h, s, "bw_cold", (bw_cold<V, B>), dim3(cb, g.cchunks), dim3(256), 0, s, sk, n, g, staging, h->n_hot, \
-              lr, ws.gc, ws.gc_rows, ws.bnd);                                                                      \
+              lr, ws.gc, ws.gc_rows, ws.bnd, hl_hook_take(h));                                                     \
   } while (0)
   if (vec == 4) { if (bf) FIN(4, true); else FIN(4, false); }
   else if (vec == 2) { if (bf) FIN(2, true); else FIN(2, false); }

@@ -62,7 +62,21 @@ struct hl_handle {
   int ws_next;           // next record to reuse when all are taken
   uint64_t* cg_table;    // cold-gather hash table (kept clean between calls)
   uint32_t cg_slots;     // its slots
+  mutable struct hl_hook {  // a handover for the next kernel that takes one (hl_hook_take)
+    uint32_t* sflag;
+    uint32_t sv;
+    const uint32_t* wflag;
+    uint32_t wv;
+    uint32_t* err;
+  } hook;
 };
+typedef hl_handle::hl_hook hl_hook;
+// The pending handover, cleared: the kernel about to launch carries it.
+static inline hl_hook hl_hook_take(const hl_handle* h) {
+  const hl_hook k = h->hook;
+  h->hook = hl_hook{};
+  return k;
+}
 #define HL_WSK_OTHER 1
 #define HL_WSK_BWD_PLAN 2
 static inline void hl_ws_note(hl_handle* h, const void* ws, int kind, int64_t n = 0, int64_t bags = 0,
@@ -250,6 +264,31 @@ hl_status hl_sort_passes(hl_handle* h, hl_sort_ws& ws, const uint32_t* n_dev, ui
 #define HL_ST_AGG 1ull
 #define HL_ST_PRE 2ull
 #define HL_SPIN_LIMIT (1u << 24)
+
+// A handover between streams carried by a kernel of the path instead of a
+// launch of its own.  Block 0 stores sv into *sflag as the kernel starts: the
+// kernels before it on its stream are complete, and their writes were made
+// visible when they ended, so a relaxed store publishes them.  Block 0 waits
+// at its end until *wflag reaches wv: the kernel, and so its stream, ends only
+// then, and the next kernel's start orders its reads after the wait (the
+// relaxed loads need no acquire).  Bounded: past the limit the wait sets
+// HL_DEVERR_STALL and returns.
+__device__ __forceinline__ void hl_hook_head(const hl_hook& k) {
+  if (k.sflag && blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0)
+    __hip_atomic_store(k.sflag, k.sv, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void hl_hook_tail(const hl_hook& k) {
+  if (!k.wflag || blockIdx.x != 0 || blockIdx.y != 0 || threadIdx.x != 0) return;
+  uint32_t spins = 0;
+  // (int32_t)(x - v) >= 0: x has reached v (sequence numbers wrap)
+  while ((int32_t)(__hip_atomic_load(k.wflag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) - k.wv) < 0) {
+    if (++spins > HL_SPIN_LIMIT) {
+      hl_flag(k.err, HL_DEVERR_STALL);
+      return;
+    }
+    __builtin_amdgcn_s_sleep(8);
+  }
+}
 #ifndef HL_LB_WIN
 #define HL_LB_WIN 32
 #endif

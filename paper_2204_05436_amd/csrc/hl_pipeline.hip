@@ -23,6 +23,12 @@
 // each) instead of an event dependency between streams (~17 us measured).
 // Handovers that meet at one point of a stream share one launch (pl_hand): the
 // fetch's two waits, and a plan's grouping signal with the next plan's waits.
+// On the main stream of a planned step they ride on the kernels themselves
+// (hl_hook): the forward signals the previous step's end as it starts and
+// waits for the grouping as it ends, the reduction waits for the fetch, and
+// the step's last kernel waits for the next plan's cold list, so main runs its
+// kernels back to back (each handover launch measured ~2-3 us of main's time
+// per step).
 // Flags need streams that progress independently: a stream with a compute-unit
 // mask has a hardware queue of its own.  Without masks (fetch_cus = 0) streams
 // may share a hardware queue, where a wait ahead of its signal would stall, so
@@ -98,6 +104,7 @@ __global__ void pl_hand(uint32_t* sflag, uint32_t sv, const uint32_t* w1, uint32
 struct pl_plan {
   hl_step_io io;      // the inputs and per-step buffers it ran with
   uint32_t seq;       // its PF_LOOK value
+  uint32_t need;      // the step whose end it waits for (0: none)
   bool pending;       // enqueued, not yet consumed by a step
 };
 
@@ -126,6 +133,7 @@ struct hl_pipeline {
   uint32_t use_seq[32];
   int use_next;
   uint32_t np_last;       // last step that ran its own dispatch and cold plan (cold-gather hash table)
+  uint32_t look_seen;     // the plan whose "cold list" the last step's last kernel waited for (0: none)
 };
 
 static hl_status pl_flush(hl_pipeline* p);
@@ -227,6 +235,37 @@ static hl_status pl_hw(hl_pipeline* p, hipStream_t s, int sf, uint32_t sv, int w
                      w2 >= 0 ? F + w2 : nullptr, v2, w3 >= 0 ? F + w3 : nullptr, v3, p->h->d_err);
   return hipGetLastError() == hipSuccess ? HL_OK : HL_ERR_HIP;
 }
+// Flag mode: the next kernel of the path launched on the stream signals sf = sv
+// as it starts and waits for wf >= wv as it ends (hl_hook_head, hl_hook_tail),
+// which spares the handover launch and its kernel boundary.  A call that
+// launched no such kernel leaves the handover to pl_unhook, which enqueues it
+// alone (the same order: nothing ran in between).
+static void pl_hook(hl_pipeline* p, int sf, uint32_t sv, int wf, uint32_t wv) {
+  hl_hook& k = p->h->hook;
+  k.sflag = sf >= 0 ? p->flags + sf : nullptr;
+  k.sv = sv;
+  k.wflag = wf >= 0 ? p->flags + wf : nullptr;
+  k.wv = wv;
+  k.err = p->h->d_err;
+}
+static hl_status pl_unhook(hl_pipeline* p, hipStream_t s) {
+  const hl_hook k = hl_hook_take(p->h);
+  if (!k.sflag && !k.wflag) return HL_OK;
+  hipLaunchKernelGGL(pl_hand, dim3(1), dim3(64), 0, s, k.sflag, k.sv, k.wflag, k.wv, nullptr, 0u, nullptr, 0u,
+                     p->h->d_err);
+  return hipGetLastError() == hipSuccess ? HL_OK : HL_ERR_HIP;
+}
+// a call on stream s with the handover set by pl_hook (dropped if the call fails)
+#define PL_HOOKED(s, call)              \
+  do {                                  \
+    const hl_status _st = (call);       \
+    if (_st != HL_OK) {                 \
+      (void)hl_hook_take(p->h);         \
+      return _st;                       \
+    }                                   \
+    HL_TRY(pl_unhook(p, (s)));          \
+  } while (0)
+
 // the pending signals, enqueued alone
 static hl_status pl_flush_sort(hl_pipeline* p) {
   if (!p->sort_pend) return HL_OK;
@@ -400,6 +439,7 @@ extern "C" hl_status hl_pipeline_plan(hl_pipeline* p, const hl_step_io* io, hl_s
   p->sort_v = v;
   e->io = *io;
   e->seq = v;
+  e->need = need;
   e->pending = true;
   return HL_OK;
 }
@@ -436,35 +476,51 @@ extern "C" hl_status hl_pipeline_step(hl_pipeline* p, const hl_step_io* io, hl_s
     HL_TRY(pl_hw(p, f, -1, 0, PF_LOOK, e->seq, last ? PF_DONE : -1, last));
     HL_TRY(hl_cold_fetch(h, io->cold_ids, io->n_cold, cap, io->w_host, io->staging, F));
     HL_TRY(pl_sig(p, f, PF_FETCH, q));
-    // main: the previous step's end signal and the wait for the plan in one
-    // launch; the grouping is awaited after the hot forward (the plan stream
-    // carries as much work per step as main: awaiting the grouping before the
-    // forward measured slower, also with plans two steps ahead)
+    // main: the previous step's end signal and the wait for the plan (in the
+    // previous step's last kernel when it waited for this plan already, else
+    // one launch); the grouping is awaited after the hot forward (the plan
+    // stream carries as much work per step as main: awaiting the grouping
+    // before the forward measured slower, also with plans two steps ahead).
+    // The waits between main's kernels ride on the kernels before them.
     if (io->dY && p->sort_pend && p->sort_v == e->seq) HL_TRY(pl_flush_sort(p));
     const bool dp = p->done_pend;
     p->done_pend = false;
-    HL_TRY(pl_hw(p, m, dp ? PF_DONE : -1, p->done_v, PF_LOOK, e->seq, -1, 0));
-    HL_TRY(pl_fwd_hot(h, io, M));
-    if (io->dY) {
-      HL_TRY(pl_wt(p, m, PF_SORT, e->seq));
-      // the reduction of the hot runs and of the staging runs inside a tile
-      HL_TRY(hl_embbag_bwd_apply_any(h, io->w_hot, io->staging, cap, B, bps, L, io->dY, io->lr, 3, io->workspace,
-                                     io->ws_bytes, M));
+    const bool bwd = io->dY != nullptr;
+    if (p->look_seen == e->seq) {
+      pl_hook(p, dp ? PF_DONE : -1, p->done_v, bwd ? PF_SORT : PF_FETCH, bwd ? e->seq : q);
+    } else {
+      HL_TRY(pl_hw(p, m, dp ? PF_DONE : -1, p->done_v, PF_LOOK, e->seq, -1, 0));
+      pl_hook(p, -1, 0, bwd ? PF_SORT : PF_FETCH, bwd ? e->seq : q);
     }
-    HL_TRY(pl_wt(p, m, PF_FETCH, q));
-    if (io->dY) {
+    p->look_seen = 0;
+    PL_HOOKED(m, pl_fwd_hot(h, io, M));
+    // the step's last kernel waits for the next pending plan's cold list (the
+    // oldest; it waits only for steps before this one, so it ends without it)
+    pl_plan* nx = nullptr;
+    for (pl_plan& c : p->plans)
+      if (c.pending && (!nx || pl_before(c.seq, nx->seq))) nx = &c;
+    if (nx && nx->need && !pl_before(nx->need, q)) nx = nullptr;
+    if (bwd) {
+      // the reduction of the hot runs and of the staging runs inside a tile
+      pl_hook(p, -1, 0, PF_FETCH, q);
+      PL_HOOKED(m, hl_embbag_bwd_apply_any(h, io->w_hot, io->staging, cap, B, bps, L, io->dY, io->lr, 3,
+                                           io->workspace, io->ws_bytes, M));
       // the cold half of the forward from the grouping's tail (cold lookups
       // only) with the runs that span tiles, then the staging-row updates
-      HL_TRY(hl_embbag_finish_cold(h, io->w_hot, io->staging, cap, io->codes, io->bag_ptr, B, bps, L, io->lr, io->out,
-                                   io->workspace, io->ws_bytes, M));
+      pl_hook(p, -1, 0, nx ? PF_LOOK : -1, nx ? nx->seq : 0);
+      PL_HOOKED(m, hl_embbag_finish_cold(h, io->w_hot, io->staging, cap, io->codes, io->bag_ptr, B, bps, L, io->lr,
+                                         io->out, io->workspace, io->ws_bytes, M));
     } else {
-      HL_TRY(hl_embbag_fwd_part(h, io->w_hot, io->staging, cap, io->codes, io->bag_ptr, B, bps, L, io->nonpop_ids,
-                                io->counts + 1, B, io->out, 2, M));
+      pl_hook(p, -1, 0, nx ? PF_LOOK : -1, nx ? nx->seq : 0);
+      PL_HOOKED(m, hl_embbag_fwd_part(h, io->w_hot, io->staging, cap, io->codes, io->bag_ptr, B, bps, L,
+                                      io->nonpop_ids, io->counts + 1, B, io->out, 2, M));
     }
+    if (nx) p->look_seen = nx->seq;
   } else {
     // the look-ahead plans use the same cold-gather hash table
     const bool dp = p->done_pend;
     p->done_pend = false;
+    p->look_seen = 0;
     HL_TRY(pl_hw(p, m, dp ? PF_DONE : -1, p->done_v, p->plan_seq ? PF_LOOK : -1, p->plan_seq, -1, 0));
     p->np_last = q;
     HL_TRY(hl_dispatch(h, io->rows, io->bag_ptr, B, bps, L, io->gids, io->codes, io->flags, io->pop_ids,

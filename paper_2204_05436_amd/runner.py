@@ -61,7 +61,7 @@ MODES = ("pipelined", "sequential", "fwdbwd")
 class HotPath:
     def __init__(self, w: Workload, rows_per_table, table: hl.HostTable, max_lookups: int, max_samples: int,
                  device="cuda", k_cap: int | None = None, staging_cap: int | None = None, writeback: bool = False,
-                 fetch_cus: int = 32, plan_cus: int = 64, n_sets: int = 3):
+                 fetch_cus: int = 8, plan_cus: int = 64, n_sets: int = 3):
         self.w = w
         self.device = device
         self.rows_per_table = np.asarray(rows_per_table, dtype=np.uint32)
