@@ -237,13 +237,16 @@ ds_kernel(const uint32_t* __restrict__ rows, const int32_t* __restrict__ bag_ptr
           int32_t spb, const uint32_t* __restrict__ base, const uint32_t* __restrict__ nrow, int32_t n_tables,
           const uint64_t* __restrict__ bitmap, const uint32_t* __restrict__ rank, uint64_t n_rows,
           uint32_t* __restrict__ gids, int32_t* __restrict__ codes, uint8_t* __restrict__ flags, int32_t* pop,
-          int32_t* nonpop, int32_t* counts, int64_t n_lookups, uint32_t* hdr, uint64_t* st, uint32_t* err) {
+          int32_t* nonpop, int32_t* counts, int64_t n_lookups, uint32_t* hdr, uint64_t* st, uint32_t* err,
+          hl_hook hk) {
   __shared__ int32_t off[DS_MAX_BAGS + 1];
   __shared__ uint32_t tb_base[DS_MAX_TABLES], tb_rows[DS_MAX_TABLES];
   __shared__ uint8_t fl[DS_MAX_SPB];
   __shared__ uint16_t bmap[DS_MAP];  // lookup - lo -> bag within the block
   __shared__ uint32_t s_tile, s_epoch, wsum[DS_THREADS / 64];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  hl_hook_head(hk);
+  hl_hook_gate(hk);
   if (tid == 0) {
     s_tile = atomicInc(hdr + DS_TILE, gridDim.x - 1);
     // status words of earlier calls carry older epochs; zeroed words carry no flag
@@ -363,6 +366,28 @@ ds_kernel(const uint32_t* __restrict__ rows, const int32_t* __restrict__ bag_ptr
     __hip_atomic_store(hdr + DS_EPOCH, epoch + 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// the samples per block of the fused dispatch, or 0 when it takes the step by
+// step calls
+static int64_t ds_spb(const hl_handle* h, int32_t n_samples, int32_t bps, int64_t n_lookups, const void* workspace,
+                      size_t ws_bytes) {
+  // about 2048 lookups per block, at most DS_MAX_BAGS bags
+  int64_t spb = n_lookups > 0 ? (2048ll * n_samples + n_lookups - 1) / n_lookups : DS_MAX_SPB;
+  const int64_t bag_cap = DS_MAX_BAGS / bps;
+  if (spb > bag_cap) spb = bag_cap;
+  if (spb > DS_MAX_SPB) spb = DS_MAX_SPB;
+  if (spb < 1) spb = 1;
+  const int64_t tiles = n_samples > 0 ? (n_samples + spb - 1) / spb : 0;
+  if (tiles == 0 || bps > DS_MAX_BAGS || tiles > HL_DISP_MAX_TILES || h->n_tables > DS_MAX_TABLES || !workspace ||
+      ws_bytes < HL_WS_HEADER)
+    return 0;
+  return spb;
+}
+
+bool hl_dispatch_fused(const hl_handle* h, int32_t n_samples, int32_t bps, int64_t n_lookups, const void* workspace,
+                       size_t ws_bytes) {
+  return h && bps >= 1 && n_samples >= 0 && ds_spb(h, n_samples, bps, n_lookups, workspace, ws_bytes) > 0;
+}
+
 extern "C" hl_status hl_dispatch(hl_handle* h, const uint32_t* rows, const int32_t* bag_ptr, int32_t n_samples,
                                  int32_t bps, int64_t n_lookups, uint32_t* gids, int32_t* codes, uint8_t* flags,
                                  int32_t* pop_ids, int32_t* nonpop_ids, int32_t* counts_dev, void* workspace,
@@ -372,15 +397,9 @@ extern "C" hl_status hl_dispatch(hl_handle* h, const uint32_t* rows, const int32
   if (n_lookups > 0 && (!rows || !gids || !codes)) return HL_ERR_INVALID_ARG;
   if ((int64_t)n_samples * bps >= (1ll << 31) || n_lookups >= (1ll << 31)) return HL_ERR_UNSUPPORTED;
   hipStream_t s = (hipStream_t)stream;
-  // about 2048 lookups per block, at most DS_MAX_BAGS bags
-  int64_t spb = n_lookups > 0 ? (2048ll * n_samples + n_lookups - 1) / n_lookups : DS_MAX_SPB;
-  const int64_t bag_cap = DS_MAX_BAGS / bps;
-  if (spb > bag_cap) spb = bag_cap;
-  if (spb > DS_MAX_SPB) spb = DS_MAX_SPB;
-  if (spb < 1) spb = 1;
-  const int64_t tiles = n_samples > 0 ? (n_samples + spb - 1) / spb : 0;
-  if (tiles == 0 || bps > DS_MAX_BAGS || tiles > HL_DISP_MAX_TILES || h->n_tables > DS_MAX_TABLES || !workspace ||
-      ws_bytes < HL_WS_HEADER) {
+  const int64_t spb = ds_spb(h, n_samples, bps, n_lookups, workspace, ws_bytes);
+  const int64_t tiles = spb ? (n_samples + spb - 1) / spb : 0;
+  if (!spb) {
     // the step by step calls (also for an empty batch)
     hl_status st = hl_lookup_gids(h, rows, bag_ptr, (int64_t)n_samples * bps, gids, stream);
     if (st == HL_OK) st = hl_classify(h, gids, bag_ptr, n_samples, bps, n_lookups, flags, stream);
@@ -392,7 +411,7 @@ extern "C" hl_status hl_dispatch(hl_handle* h, const uint32_t* rows, const int32
   uint64_t* stw = (uint64_t*)((uint32_t*)workspace + HL_HDR_DSTAT);
   HL_KERNEL(h, s, "ds_kernel", ds_kernel, dim3((uint32_t)tiles), dim3(DS_THREADS), 0, s, rows, bag_ptr, n_samples, bps,
             (int32_t)spb, h->d_base, h->d_rows, h->n_tables, h->d_bitmap, h->d_rank, h->n_rows, gids, codes, flags,
-            pop_ids, nonpop_ids, counts_dev, n_lookups, hdr, stw, h->d_err);
+            pop_ids, nonpop_ids, counts_dev, n_lookups, hdr, stw, h->d_err, hl_hook_take(h));
   HL_LAUNCHED();
   return HL_OK;
 }

@@ -65,8 +65,11 @@ struct hl_handle {
   mutable struct hl_hook {  // a handover for the next kernel that takes one (hl_hook_take)
     uint32_t* sflag;
     uint32_t sv;
-    const uint32_t* wflag;
+    const uint32_t* wflag;   // waits: wflag >= wv, then w2flag >= w2v
     uint32_t wv;
+    const uint32_t* w2flag;
+    uint32_t w2v;
+    uint32_t gate;           // the waits are every block's, at the kernel's start (hl_hook_gate)
     uint32_t* err;
   } hook;
 };
@@ -200,6 +203,9 @@ hl_status hl_embbag_bwd_apply_any(hl_handle* h, void* w_hot, void* staging, int3
 hl_status hl_embbag_finish_cold(hl_handle* h, void* w_hot, void* staging, int32_t stg_rows, const int32_t* codes,
                                 const int32_t* bag_ptr, int32_t n_samples, int32_t bps, int64_t n_lookups, float lr,
                                 float* out, void* workspace, size_t ws_bytes, hl_stream stream);
+// hl_dispatch takes the fused single-kernel path (its kernel takes a hook)
+bool hl_dispatch_fused(const hl_handle* h, int32_t n_samples, int32_t bps, int64_t n_lookups, const void* workspace,
+                       size_t ws_bytes);
 // hl_embbag_bwd_plan whose first kernel, when it launches one (*sent), also
 // stores sv into *sflag as it starts: a handover signal for the kernels
 // enqueued before it on the stream.
@@ -277,17 +283,32 @@ __device__ __forceinline__ void hl_hook_head(const hl_hook& k) {
   if (k.sflag && blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0)
     __hip_atomic_store(k.sflag, k.sv, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-__device__ __forceinline__ void hl_hook_tail(const hl_hook& k) {
-  if (!k.wflag || blockIdx.x != 0 || blockIdx.y != 0 || threadIdx.x != 0) return;
+__device__ __forceinline__ void hl_hook_spin(const uint32_t* f, uint32_t v, uint32_t* err) {
+  if (!f) return;
   uint32_t spins = 0;
   // (int32_t)(x - v) >= 0: x has reached v (sequence numbers wrap)
-  while ((int32_t)(__hip_atomic_load(k.wflag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) - k.wv) < 0) {
+  while ((int32_t)(__hip_atomic_load(f, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) - v) < 0) {
     if (++spins > HL_SPIN_LIMIT) {
-      hl_flag(k.err, HL_DEVERR_STALL);
+      hl_flag(err, HL_DEVERR_STALL);
       return;
     }
     __builtin_amdgcn_s_sleep(8);
   }
+}
+__device__ __forceinline__ void hl_hook_tail(const hl_hook& k) {
+  if (k.gate || blockIdx.x != 0 || blockIdx.y != 0 || threadIdx.x != 0) return;
+  hl_hook_spin(k.wflag, k.wv, k.err);
+  hl_hook_spin(k.w2flag, k.w2v, k.err);
+}
+// A gate: thread 0 of every block waits before the block starts (the caller
+// synchronizes the block after it).  Only for handovers that order this
+// kernel's writes after other kernels' reads and writes (nothing this kernel
+// reads comes through them): the waits end inside the kernel, after its start
+// made earlier writes visible.
+__device__ __forceinline__ void hl_hook_gate(const hl_hook& k) {
+  if (!k.gate || threadIdx.x != 0) return;
+  hl_hook_spin(k.wflag, k.wv, k.err);
+  hl_hook_spin(k.w2flag, k.w2v, k.err);
 }
 #ifndef HL_LB_WIN
 #define HL_LB_WIN 32

@@ -133,6 +133,7 @@ struct hl_pipeline {
   uint32_t use_seq[32];
   int use_next;
   uint32_t np_last;       // last step that ran its own dispatch and cold plan (cold-gather hash table)
+  uint32_t np_synced;     // the np_last a plan has waited for with a launch of its own
   uint32_t look_seen;     // the plan whose "cold list" the last step's last kernel waited for (0: none)
 };
 
@@ -242,6 +243,7 @@ static hl_status pl_hw(hl_pipeline* p, hipStream_t s, int sf, uint32_t sv, int w
 // alone (the same order: nothing ran in between).
 static void pl_hook(hl_pipeline* p, int sf, uint32_t sv, int wf, uint32_t wv) {
   hl_hook& k = p->h->hook;
+  k = hl_hook{};
   k.sflag = sf >= 0 ? p->flags + sf : nullptr;
   k.sv = sv;
   k.wflag = wf >= 0 ? p->flags + wf : nullptr;
@@ -250,8 +252,9 @@ static void pl_hook(hl_pipeline* p, int sf, uint32_t sv, int wf, uint32_t wv) {
 }
 static hl_status pl_unhook(hl_pipeline* p, hipStream_t s) {
   const hl_hook k = hl_hook_take(p->h);
-  if (!k.sflag && !k.wflag) return HL_OK;
-  hipLaunchKernelGGL(pl_hand, dim3(1), dim3(64), 0, s, k.sflag, k.sv, k.wflag, k.wv, nullptr, 0u, nullptr, 0u,
+  if (!k.sflag && !k.wflag && !k.w2flag) return HL_OK;
+  if (k.gate) return HL_ERR_UNSUPPORTED;  // unreachable: a gate is set only for a call whose first kernel takes it
+  hipLaunchKernelGGL(pl_hand, dim3(1), dim3(64), 0, s, k.sflag, k.sv, k.wflag, k.wv, k.w2flag, k.w2v, nullptr, 0u,
                      p->h->d_err);
   return hipGetLastError() == hipSuccess ? HL_OK : HL_ERR_HIP;
 }
@@ -421,10 +424,24 @@ extern "C" hl_status hl_pipeline_plan(hl_pipeline* p, const hl_step_io* io, hl_s
   const uint32_t wb = pl_wb_last(p, io->cold_ids);
   const bool sp = p->sort_pend;
   p->sort_pend = false;
-  HL_TRY(pl_hw(p, P, sp ? PF_SORT : -1, p->sort_v, need ? PF_DONE : -1, need, wb ? PF_WB : -1, wb));
   const int32_t B = io->n_samples, bps = io->bags_per_sample;
-  HL_TRY(hl_dispatch(h, io->rows, io->bag_ptr, B, bps, io->n_lookups, io->gids, io->codes, io->flags, io->pop_ids,
-                     io->nonpop_ids, io->counts, io->workspace, io->ws_bytes, PS));
+  // The waits order the plan's writes after the reads of the steps that used
+  // its buffers, and it reads nothing they wrote, except the cold-gather hash
+  // table after a step that ran its own cold plan: then one launch waits
+  // (its end makes that step's writes visible to the plan); otherwise the
+  // dispatch kernel's blocks wait as they start, and its block 0 gives the
+  // previous plan's grouping signal.
+  if (p->np_last == p->np_synced && hl_dispatch_fused(h, B, bps, io->n_lookups, io->workspace, io->ws_bytes)) {
+    pl_hook(p, sp ? PF_SORT : -1, p->sort_v, need ? PF_DONE : -1, need);
+    h->hook.w2flag = wb ? p->flags + PF_WB : nullptr;
+    h->hook.w2v = wb;
+    h->hook.gate = 1;
+  } else {
+    HL_TRY(pl_hw(p, P, sp ? PF_SORT : -1, p->sort_v, need ? PF_DONE : -1, need, wb ? PF_WB : -1, wb));
+    p->np_synced = p->np_last;
+  }
+  PL_HOOKED(P, hl_dispatch(h, io->rows, io->bag_ptr, B, bps, io->n_lookups, io->gids, io->codes, io->flags,
+                           io->pop_ids, io->nonpop_ids, io->counts, io->workspace, io->ws_bytes, PS));
   HL_TRY(hl_cold_plan(h, io->gids, io->codes, io->bag_ptr, B, bps, io->n_lookups, nullptr, nullptr, B,
                       io->staging_cap, io->cold_ids, io->n_cold, io->workspace, io->ws_bytes, PS));
   // the cold list is ready: the fetch may start while the grouping runs (the
