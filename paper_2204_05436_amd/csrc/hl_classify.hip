@@ -238,7 +238,7 @@ ds_kernel(const uint32_t* __restrict__ rows, const int32_t* __restrict__ bag_ptr
           const uint64_t* __restrict__ bitmap, const uint32_t* __restrict__ rank, uint64_t n_rows,
           uint32_t* __restrict__ gids, int32_t* __restrict__ codes, uint8_t* __restrict__ flags, int32_t* pop,
           int32_t* nonpop, int32_t* counts, int64_t n_lookups, uint32_t* hdr, uint64_t* st, uint32_t* err,
-          hl_hook hk) {
+          hl_hook hk, hl_cg_fused cf) {
   __shared__ int32_t off[DS_MAX_BAGS + 1];
   __shared__ uint32_t tb_base[DS_MAX_TABLES], tb_rows[DS_MAX_TABLES];
   __shared__ uint8_t fl[DS_MAX_SPB];
@@ -265,6 +265,8 @@ ds_kernel(const uint32_t* __restrict__ rows, const int32_t* __restrict__ bag_ptr
     tb_rows[j] = nrow[j];
   }
   if (tile == 0 && tid == 0 && bag_ptr[(int64_t)n_samples * bps] != n_lookups) hl_flag(err, HL_DEVERR_SHAPE);
+  if (cf.table)  // the fused plan's rank scan status, cleared for the scan that follows
+    for (uint32_t j = blockIdx.x * DS_THREADS + tid; j < cf.rtiles; j += gridDim.x * DS_THREADS) cf.rstat[j] = 0;
   __syncthreads();
   const int32_t lo = off[0], hi = (int32_t)min((int64_t)off[nbg], n_lookups);
   // each lookup's bag from an LDS map built bag by bag (a binary search over the
@@ -319,7 +321,11 @@ ds_kernel(const uint32_t* __restrict__ rows, const int32_t* __restrict__ bag_ptr
       gids[i] = g[k];
       codes[i] = c;
       uint32_t rm;
-      if (c < 0) fl[hl_fdiv((uint32_t)a[k], (uint32_t)bps, inv_b, &rm)] = 0;
+      if (c < 0) {
+        fl[hl_fdiv((uint32_t)a[k], (uint32_t)bps, inv_b, &rm)] = 0;
+        // the fused plan: the cold plan's insert (an id out of range takes no slot)
+        if (cf.table) cf.slotof[i] = g[k] < n_rows ? hl_cg_insert(cf.table, cf.S - 1, g[k], (uint32_t)i) : 0xFFFFFFFFu;
+      }
     }
   }
   __syncthreads();
@@ -392,6 +398,14 @@ extern "C" hl_status hl_dispatch(hl_handle* h, const uint32_t* rows, const int32
                                  int32_t bps, int64_t n_lookups, uint32_t* gids, int32_t* codes, uint8_t* flags,
                                  int32_t* pop_ids, int32_t* nonpop_ids, int32_t* counts_dev, void* workspace,
                                  size_t ws_bytes, hl_stream stream) {
+  return hl_dispatch_ex(h, rows, bag_ptr, n_samples, bps, n_lookups, gids, codes, flags, pop_ids, nonpop_ids,
+                        counts_dev, workspace, ws_bytes, stream, nullptr);
+}
+
+hl_status hl_dispatch_ex(hl_handle* h, const uint32_t* rows, const int32_t* bag_ptr, int32_t n_samples, int32_t bps,
+                         int64_t n_lookups, uint32_t* gids, int32_t* codes, uint8_t* flags, int32_t* pop_ids,
+                         int32_t* nonpop_ids, int32_t* counts_dev, void* workspace, size_t ws_bytes,
+                         hl_stream stream, const hl_cg_fused* cf) {
   if (!h || n_samples < 0 || bps < 1 || n_lookups < 0 || !counts_dev || !bag_ptr) return HL_ERR_INVALID_ARG;
   if (n_samples > 0 && (!flags || !pop_ids || !nonpop_ids)) return HL_ERR_INVALID_ARG;
   if (n_lookups > 0 && (!rows || !gids || !codes)) return HL_ERR_INVALID_ARG;
@@ -399,6 +413,7 @@ extern "C" hl_status hl_dispatch(hl_handle* h, const uint32_t* rows, const int32
   hipStream_t s = (hipStream_t)stream;
   const int64_t spb = ds_spb(h, n_samples, bps, n_lookups, workspace, ws_bytes);
   const int64_t tiles = spb ? (n_samples + spb - 1) / spb : 0;
+  if (!spb && cf && cf->table) return HL_ERR_INVALID_ARG;  // the fused plan needs the fused dispatch
   if (!spb) {
     // the step by step calls (also for an empty batch)
     hl_status st = hl_lookup_gids(h, rows, bag_ptr, (int64_t)n_samples * bps, gids, stream);
@@ -411,7 +426,7 @@ extern "C" hl_status hl_dispatch(hl_handle* h, const uint32_t* rows, const int32
   uint64_t* stw = (uint64_t*)((uint32_t*)workspace + HL_HDR_DSTAT);
   HL_KERNEL(h, s, "ds_kernel", ds_kernel, dim3((uint32_t)tiles), dim3(DS_THREADS), 0, s, rows, bag_ptr, n_samples, bps,
             (int32_t)spb, h->d_base, h->d_rows, h->n_tables, h->d_bitmap, h->d_rank, h->n_rows, gids, codes, flags,
-            pop_ids, nonpop_ids, counts_dev, n_lookups, hdr, stw, h->d_err, hl_hook_take(h));
+            pop_ids, nonpop_ids, counts_dev, n_lookups, hdr, stw, h->d_err, hl_hook_take(h), cf ? *cf : hl_cg_fused{});
   HL_LAUNCHED();
   return HL_OK;
 }

@@ -90,15 +90,6 @@ static hl_status cg_table(hl_handle* h, uint32_t S, hipStream_t s, uint64_t** ou
   return HL_OK;
 }
 
-__device__ __forceinline__ uint32_t cg_hash(uint32_t x) {  // 32-bit finalising mix
-  x ^= x >> 16;
-  x *= 0x85EBCA6Bu;
-  x ^= x >> 13;
-  x *= 0xC2B2AE35u;
-  x ^= x >> 16;
-  return x;
-}
-
 __global__ void cg_mask(uint8_t* mask, int32_t n_samples, const int32_t* __restrict__ ids, const int32_t* n_dev,
                         int32_t n_max, int phase, uint32_t* err) {
   if (phase == 0) {
@@ -189,18 +180,7 @@ cg_insert(const uint32_t* __restrict__ gids, const int32_t* __restrict__ codes, 
         ws.slotof[i] = 0xFFFFFFFFu;
         continue;
       }
-      const uint64_t want = ((uint64_t)(g + 1) << 32) | i;
-      uint32_t slot = cg_hash(g) & smask;
-      for (uint32_t probe = 0; probe <= smask; ++probe) {
-        const uint64_t prev = atomicCAS((unsigned long long*)(table + slot), 0ull, (unsigned long long)want);
-        if (prev == 0) break;
-        if ((uint32_t)(prev >> 32) == g + 1) {
-          atomicMin((unsigned long long*)(table + slot), (unsigned long long)want);
-          break;
-        }
-        slot = (slot + 1) & smask;
-      }
-      ws.slotof[i] = slot;
+      ws.slotof[i] = hl_cg_insert(table, smask, g, i);
       ws.blist[lo + listed + e] = i;
     }
     listed += tot;
@@ -211,10 +191,12 @@ cg_insert(const uint32_t* __restrict__ gids, const int32_t* __restrict__ codes, 
 
 // Lookup i is a first occurrence iff it is a cold lookup of this call whose
 // slot holds (its id, i); the running count of first occurrences numbers the
-// staging rows.
+// staging rows.  In the fused plan (fused = 1) the ids of staging rows below
+// cap go straight to the cold id list.
 __global__ void __launch_bounds__(CG_RT_THREADS)
 cg_rank(const uint32_t* __restrict__ gids, const int32_t* __restrict__ codes, uint32_t n_lookups,
-        const uint64_t* __restrict__ table, cg_ws ws, int32_t* n_cold_dev, uint32_t epoch, uint32_t* err) {
+        const uint64_t* __restrict__ table, cg_ws ws, int32_t* n_cold_dev, uint32_t epoch, uint32_t* cold_ids,
+        int32_t cap, int fused, uint32_t* err) {
   __shared__ uint32_t s_tile, wt[CG_RT_THREADS / 64];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   if (tid == 0) s_tile = atomicInc(ws.ctr + CG_C_RTILE, gridDim.x - 1);
@@ -273,7 +255,8 @@ cg_rank(const uint32_t* __restrict__ gids, const int32_t* __restrict__ codes, ui
     if (first[k]) {
       const uint32_t u = run + (uint32_t)__popcll(m & lt);
       ws.uidx[slot[k]] = u;
-      ws.fst[u] = g[k];
+      if (!fused) ws.fst[u] = g[k];
+      else if (u < (uint32_t)cap) cold_ids[u] = g[k];
     }
     run += (uint32_t)__popcll(m);
     if (i == (uint64_t)n_lookups - 1) {
@@ -419,10 +402,70 @@ extern "C" hl_status hl_cold_plan(hl_handle* h, const uint32_t* gids, int32_t* c
   // call (and every replay of a captured graph)
   const uint32_t epoch = 1;
   HL_KERNEL(h, s, "cg_rank", cg_rank, dim3(ws.rtiles), dim3(CG_RT_THREADS), 0, s, gids, codes, ib > 0 ? n : 0u, table, ws,
-            n_cold_dev, epoch, h->d_err);
+            n_cold_dev, epoch, nullptr, 0, 0, h->d_err);
   if (ib > 0)
     HL_KERNEL(h, s, "cg_codes", cg_codes, dim3(ib), dim3(256), 0, s, bag_ptr, table, ws, cap, h->k_cap, codes,
               cold_ids_out, h->d_err);
+  HL_LAUNCHED();
+  return HL_OK;
+}
+
+// The fused plan's cold state: the cold regions carved after the grouping's
+// region of the workspace.
+static hl_carver cg_fused_carver(const hl_handle* h, void* workspace, size_t ws_bytes, int64_t n_lookups,
+                                 int64_t n_bags) {
+  hl_carver c = hl_carver::after_header(workspace, ws_bytes);
+  c.off = hl_bwd_ws_bytes(h, n_lookups, n_bags);
+  return c;
+}
+
+size_t hl_plan_ws_bytes(const hl_handle* h, int64_t max_lookups, int64_t max_bags, int32_t max_samples) {
+  hl_carver c = cg_fused_carver(h, nullptr, 0, max_lookups, max_bags);
+  cg_ws ws;
+  cg_carve(c, ws, (uint32_t)max_lookups, max_bags, max_samples);
+  return c.off;
+}
+
+hl_status hl_cold_fused_begin(hl_handle* h, int64_t n_lookups, int64_t n_bags, int32_t n_samples, int32_t cap,
+                              void* workspace, size_t ws_bytes, hipStream_t s, hl_cg_fused* out) {
+  *out = hl_cg_fused{};
+  if (!h || !workspace || n_lookups <= 0 || n_bags <= 0 || n_samples <= 0 || cap < 0) return HL_ERR_INVALID_ARG;
+  if (n_lookups >= (1ll << 30) || (uint64_t)h->k_cap + (uint64_t)cap >= (1ull << 31)) return HL_ERR_UNSUPPORTED;
+  if (ws_bytes < hl_plan_ws_bytes(h, n_lookups, n_bags, n_samples)) return HL_ERR_CAPACITY;
+  hl_carver c = cg_fused_carver(h, workspace, ws_bytes, n_lookups, n_bags);
+  cg_ws ws;
+  cg_carve(c, ws, (uint32_t)n_lookups, n_bags, n_samples);
+  // no growth here: a larger table is allocated by a plain cold plan, after
+  // its waits (the table is shared with the steps still in flight)
+  if (h->cg_slots < ws.S || !h->cg_table) return HL_ERR_CAPACITY;
+  (void)s;
+  out->table = h->cg_table;
+  out->S = ws.S;
+  out->slotof = ws.slotof;
+  out->uidx = ws.uidx;
+  out->rstat = ws.rstat;
+  out->rtiles = ws.rtiles;
+  out->ncold = ws.ctr + CG_C_NCOLD;
+  out->cap = cap;
+  return HL_OK;
+}
+
+hl_status hl_cold_rank_fused(hl_handle* h, const uint32_t* gids, const int32_t* codes, int64_t n_lookups,
+                             uint32_t* cold_ids, int32_t* n_cold_dev, void* workspace, const hl_cg_fused& cf,
+                             hipStream_t s) {
+  if (!h || !gids || !codes || !n_cold_dev || !workspace || !cf.table || n_lookups <= 0) return HL_ERR_INVALID_ARG;
+  if (cf.cap > 0 && !cold_ids) return HL_ERR_INVALID_ARG;
+  cg_ws ws{};
+  ws.ctr = reinterpret_cast<uint32_t*>(workspace) + HL_HDR_COLD;
+  ws.S = cf.S;
+  ws.uidx = cf.uidx;
+  ws.slotof = cf.slotof;
+  ws.rstat = cf.rstat;
+  ws.rtiles = cf.rtiles;
+  // the dispatch kernel cleared the status words
+  const uint32_t epoch = 1;
+  HL_KERNEL(h, s, "cg_rank", cg_rank, dim3(cf.rtiles), dim3(CG_RT_THREADS), 0, s, gids, codes, (uint32_t)n_lookups,
+            cf.table, ws, n_cold_dev, epoch, cold_ids, cf.cap, 1, h->d_err);
   HL_LAUNCHED();
   return HL_OK;
 }

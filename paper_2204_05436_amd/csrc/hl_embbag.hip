@@ -374,12 +374,24 @@ __device__ __forceinline__ void bw_uncovered(const int32_t* bag_ptr, int64_t n_b
   *covered = max(min((int64_t)max(bag_ptr[n_bags], 0), n_lookups), *first);
 }
 
-// the bags [b0, b0 + nb) of one block: off[] holds their offsets
+// The fused plan: a cold lookup's code (-1) points at its staging row once the
+// rank scan numbered the rows, if they fit; any other code is returned as is.
+__device__ __forceinline__ int32_t bw_fused_code(int32_t c, uint32_t i, const hl_cg_fused& cf, uint32_t k_cap,
+                                                 bool fits) {
+  if (c != -1 || !cf.table) return c;
+  const uint32_t sl = cf.slotof[i];
+  return sl < cf.S && fits ? (int32_t)(k_cap + cf.uidx[sl]) : -1;
+}
+
+// the bags [b0, b0 + nb) of one block: off[] holds their offsets.  The fused
+// plan (cf.table) also writes the cold lookups' codes and frees their slots,
+// as the cold plan's last kernel does.
 template <int NT>
-__device__ __forceinline__ void bw_prep_bags(const int32_t* __restrict__ codes, const int32_t* off, int64_t b0,
-                                             int nb, int32_t bps, const uint8_t* __restrict__ mask, uint32_t n_hot,
-                                             uint32_t k_cap, int32_t stg_rows, uint32_t* __restrict__ keys,
-                                             uint32_t* __restrict__ vals, int64_t n_lookups, uint32_t* err) {
+__device__ __forceinline__ void bw_prep_bags(int32_t* codes, const int32_t* off, int64_t b0, int nb, int32_t bps,
+                                             const uint8_t* __restrict__ mask, uint32_t n_hot, uint32_t k_cap,
+                                             int32_t stg_rows, uint32_t* __restrict__ keys,
+                                             uint32_t* __restrict__ vals, int64_t n_lookups, uint32_t* err,
+                                             const hl_cg_fused& cf, bool fits) {
   const int32_t lo = off[0], hi = min((int64_t)off[nb], n_lookups);
   for (int32_t i = lo + threadIdx.x; i < hi; i += NT) {
     int a = 0, b = nb;
@@ -390,7 +402,14 @@ __device__ __forceinline__ void bw_prep_bags(const int32_t* __restrict__ codes, 
     const int64_t bag = b0 + a;
     uint32_t key = EB_SENT;
     if (!mask || mask[bag / bps]) {
-      key = bw_key((uint32_t)codes[i], n_hot, k_cap, stg_rows);
+      int32_t c = codes[i];
+      if (cf.table && c == -1) {
+        const uint32_t sl = cf.slotof[i];
+        c = bw_fused_code(c, (uint32_t)i, cf, k_cap, fits);
+        if (c != -1) codes[i] = c;
+        if (sl < cf.S) cf.table[sl] = 0;
+      }
+      key = bw_key((uint32_t)c, n_hot, k_cap, stg_rows);
       if (key == EB_SENT) hl_flag(err, HL_DEVERR_BAD_CODE);
     }
     keys[i] = key;
@@ -424,27 +443,33 @@ bw_prep(const int32_t* __restrict__ codes, const int32_t* __restrict__ bag_ptr, 
   const int64_t gs = (int64_t)gridDim.x * blockDim.x, t0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   for (int64_t i = t0; i < first; i += gs) keys[i] = EB_SENT;
   for (int64_t i = covered + t0; i < n_lookups; i += gs) keys[i] = EB_SENT;
-  bw_prep_bags<256>(codes, off, b0, nb, bps, mask, n_hot, k_cap, stg_rows, keys, vals, n_lookups, err);
+  bw_prep_bags<256>(const_cast<int32_t*>(codes), off, b0, nb, bps, mask, n_hot, k_cap, stg_rows, keys, vals,
+                    n_lookups, err, hl_cg_fused{}, false);
 }
 
 // bw_prep and the sort's digit histogram in one launch (no sample selection):
 // blocks [0, hb) count the digits of every key, taking the keys from the codes
 // by the same rule as the writers, and clear the first pass's status words;
-// the other blocks write the (key, bag) pairs, BPH_BAGS bags each.
+// the other blocks write the (key, bag) pairs, BPH_BAGS bags each.  In the
+// fused plan (cf.table) both roles take a cold lookup's code from the cold
+// plan's state (the writers also store it; a reader that meets the stored
+// code derives the same key), and the first writer block reports rows that do
+// not fit the staging buffer.
 #define BPH_THREADS 1024
 #define BPH_BAGS 1024
 template <int NB>
 __global__ void __launch_bounds__(BPH_THREADS)
-bw_prep_hist(const int32_t* __restrict__ codes, const int32_t* __restrict__ bag_ptr, int64_t n_bags, int32_t bps,
-             uint32_t n_hot, uint32_t k_cap, int32_t stg_rows, uint32_t* __restrict__ keys,
-             uint32_t* __restrict__ vals, int64_t n_lookups, uint32_t hb, int passes, int b,
-             uint32_t* __restrict__ part, uint32_t* __restrict__ zero, uint64_t n_zero, uint32_t* sflag, uint32_t sv,
-             uint32_t* err) {
+bw_prep_hist(int32_t* codes, const int32_t* __restrict__ bag_ptr, int64_t n_bags, int32_t bps, uint32_t n_hot,
+             uint32_t k_cap, int32_t stg_rows, uint32_t* __restrict__ keys, uint32_t* __restrict__ vals,
+             int64_t n_lookups, uint32_t hb, int passes, int b, uint32_t* __restrict__ part,
+             uint32_t* __restrict__ zero, uint64_t n_zero, uint32_t* sflag, uint32_t sv, uint32_t* err,
+             hl_cg_fused cf) {
   __shared__ uint32_t hst[HL_SORT_MAXPASS][NB];
   __shared__ int32_t off[BPH_BAGS + 1];
   bw_start_signal(sflag, sv);
   int64_t first, covered;
   bw_uncovered(bag_ptr, n_bags, n_lookups, &first, &covered);
+  const bool fits = cf.table && *cf.ncold <= (uint32_t)cf.cap;
   if (blockIdx.x < hb) {
     const uint32_t gs = hb * BPH_THREADS;
     for (uint64_t i = (uint64_t)blockIdx.x * BPH_THREADS + threadIdx.x; i < n_zero; i += gs) zero[i] = 0;
@@ -463,7 +488,8 @@ bw_prep_hist(const int32_t* __restrict__ codes, const int32_t* __restrict__ bag_
       for (int u = 0; u < 8; ++u) {
         const uint32_t i = i0 + u * gs;
         if (i >= n) continue;
-        const uint32_t key = (int64_t)i < first || (int64_t)i >= covered ? EB_SENT : bw_key(k[u], n_hot, k_cap, stg_rows);
+        const uint32_t c = (uint32_t)bw_fused_code((int32_t)k[u], i, cf, k_cap, fits);
+        const uint32_t key = (int64_t)i < first || (int64_t)i >= covered ? EB_SENT : bw_key(c, n_hot, k_cap, stg_rows);
         for (int p = 0; p < passes; ++p) atomicAdd(&hst[p][(key >> (b * p)) & mask], 1u);
       }
     }
@@ -478,11 +504,13 @@ bw_prep_hist(const int32_t* __restrict__ codes, const int32_t* __restrict__ bag_
   const int nb = (int)min((int64_t)BPH_BAGS, n_bags - b0);
   for (int j = threadIdx.x; j <= nb; j += BPH_THREADS) off[j] = bag_ptr[b0 + j];
   if (blk == 0 && threadIdx.x == 0 && bag_ptr[n_bags] != n_lookups) hl_flag(err, HL_DEVERR_SHAPE);
+  if (blk == 0 && threadIdx.x == 0 && cf.table && !fits) hl_flag(err, HL_DEVERR_CAPACITY);
   __syncthreads();
   const int64_t gs = (int64_t)(gridDim.x - hb) * BPH_THREADS, t0 = (int64_t)blk * BPH_THREADS + threadIdx.x;
   for (int64_t i = t0; i < first; i += gs) keys[i] = EB_SENT;
   for (int64_t i = covered + t0; i < n_lookups; i += gs) keys[i] = EB_SENT;
-  bw_prep_bags<BPH_THREADS>(codes, off, b0, nb, bps, nullptr, n_hot, k_cap, stg_rows, keys, vals, n_lookups, err);
+  bw_prep_bags<BPH_THREADS>(codes, off, b0, nb, bps, nullptr, n_hot, k_cap, stg_rows, keys, vals, n_lookups, err, cf,
+                            fits);
 }
 
 template <int VEC, bool BF>
@@ -1035,15 +1063,18 @@ extern "C" hl_status hl_embbag_bwd_plan(hl_handle* h, int32_t stg_rows, const in
                                         const int32_t* n_sel_dev, int32_t n_sel_max, void* workspace, size_t ws_bytes,
                                         hl_stream stream) {
   bool sent = false;
-  return hl_embbag_bwd_plan_signal(h, stg_rows, codes, bag_ptr, n_samples, bps, n_lookups, sample_ids, n_sel_dev,
-                                   n_sel_max, workspace, ws_bytes, stream, nullptr, 0, &sent);
+  return hl_embbag_bwd_plan_signal(h, stg_rows, const_cast<int32_t*>(codes), bag_ptr, n_samples, bps, n_lookups,
+                                   sample_ids, n_sel_dev, n_sel_max, workspace, ws_bytes, stream, nullptr, 0, &sent,
+                                   nullptr);
 }
 
-hl_status hl_embbag_bwd_plan_signal(hl_handle* h, int32_t stg_rows, const int32_t* codes, const int32_t* bag_ptr,
+hl_status hl_embbag_bwd_plan_signal(hl_handle* h, int32_t stg_rows, int32_t* codes, const int32_t* bag_ptr,
                                     int32_t n_samples, int32_t bps, int64_t n_lookups, const int32_t* sample_ids,
                                     const int32_t* n_sel_dev, int32_t n_sel_max, void* workspace, size_t ws_bytes,
-                                    hl_stream stream, uint32_t* sflag, uint32_t sval, bool* sent) {
+                                    hl_stream stream, uint32_t* sflag, uint32_t sval, bool* sent,
+                                    const hl_cg_fused* cf) {
   *sent = false;
+  if (cf && cf->table && sample_ids) return HL_ERR_INVALID_ARG;  // the fused plan selects every sample
   hl_status st = check_common(h, codes, bag_ptr, n_samples, bps, n_lookups, sample_ids, n_sel_max, stg_rows);
   if (st != HL_OK) return st;
   if (!workspace) return HL_ERR_INVALID_ARG;
@@ -1081,7 +1112,7 @@ hl_status hl_embbag_bwd_plan_signal(hl_handle* h, int32_t stg_rows, const int32_
 #define BPH(NB)                                                                                                  \
   HL_KERNEL(h, s, "bw_prep_hist", bw_prep_hist<NB>, grid, dim3(BPH_THREADS), 0, s, codes, bag_ptr, n_bags, bps, h->n_hot, \
             h->k_cap, stg_rows, ws.sort.k0, ws.sort.v0, n_lookups, sg.hist_blocks, sg.passes, sg.b, ws.sort.part,   \
-            ws.sort.st[0], sg.n_zero, sflag, sval, h->d_err)
+            ws.sort.st[0], sg.n_zero, sflag, sval, h->d_err, cf ? *cf : hl_cg_fused{})
     if (sg.nb == 256) BPH(256);
     else if (sg.nb == 1024) BPH(1024);
     else BPH(2048);

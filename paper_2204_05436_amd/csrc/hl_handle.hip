@@ -13,6 +13,7 @@ size_t hl_topk_scratch_bytes(uint64_t n_rows);
 size_t hl_partition_ws_bytes(int32_t max_samples);
 size_t hl_cold_ws_bytes(const hl_handle* h, int64_t max_lookups, int64_t max_bags, int32_t max_samples);
 size_t hl_bwd_ws_bytes(const hl_handle* h, int64_t max_lookups, int64_t max_bags);
+size_t hl_plan_ws_bytes(const hl_handle* h, int64_t max_lookups, int64_t max_bags, int32_t max_samples);
 
 extern "C" const char* hl_status_string(hl_status s) {
   switch (s) {
@@ -194,8 +195,10 @@ extern "C" size_t hl_workspace_bytes(const hl_handle* h, int64_t max_lookups, in
   size_t a = hl_partition_ws_bytes(max_samples);
   size_t b = hl_cold_ws_bytes(h, max_lookups, max_bags, max_samples);
   size_t c = hl_bwd_ws_bytes(h, max_lookups, max_bags);
+  size_t d = hl_plan_ws_bytes(h, max_lookups, max_bags, max_samples);
   size_t m = a > b ? a : b;
   m = m > c ? m : c;
+  m = m > d ? m : d;
   return (m + 4095) & ~(size_t)4095;
 }
 

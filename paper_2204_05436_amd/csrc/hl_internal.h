@@ -206,13 +206,77 @@ hl_status hl_embbag_finish_cold(hl_handle* h, void* w_hot, void* staging, int32_
 // hl_dispatch takes the fused single-kernel path (its kernel takes a hook)
 bool hl_dispatch_fused(const hl_handle* h, int32_t n_samples, int32_t bps, int64_t n_lookups, const void* workspace,
                        size_t ws_bytes);
+
+// ---------------------------------------------------------- the fused plan
+// A look-ahead plan over every sample in five launches instead of seven: the
+// dispatch kernel also enters its cold lookups into the cold-gather hash table
+// (the cold plan's insert), the rank scan writes the cold id list itself, and
+// the grouping's first kernel also points the cold lookups' codes at their
+// staging rows and frees their table slots (the cold plan's last kernel).  The
+// cold plan's state lies after the grouping's region of the workspace, so the
+// grouping can read it.
+struct hl_cg_fused {
+  uint64_t* table;        // the handle's hash table (NULL: no fused cold plan)
+  uint32_t S;             // its slots (a power of two)
+  uint32_t* slotof;       // [n] slot of a cold lookup
+  uint32_t* uidx;         // [S] staging row of the id in a slot
+  uint64_t* rstat;        // [rtiles] the rank scan's look-back status (cleared by the dispatch)
+  uint32_t rtiles;
+  const uint32_t* ncold;  // distinct cold ids (written by the rank scan)
+  int32_t cap;            // staging rows
+};
+// workspace bytes of the backward's plan and apply
+size_t hl_bwd_ws_bytes(const hl_handle* h, int64_t max_lookups, int64_t max_bags);
+// workspace bytes of the fused plan (hl_workspace_bytes covers them)
+size_t hl_plan_ws_bytes(const hl_handle* h, int64_t max_lookups, int64_t max_bags, int32_t max_samples);
+// carves the fused plan's cold state; HL_ERR_CAPACITY if the workspace or the
+// handle's hash table is too small (a plain cold plan grows the table)
+hl_status hl_cold_fused_begin(hl_handle* h, int64_t n_lookups, int64_t n_bags, int32_t n_samples, int32_t cap,
+                              void* workspace, size_t ws_bytes, hipStream_t s, hl_cg_fused* out);
+// hl_dispatch whose kernel also inserts the cold lookups (cf: from hl_cold_fused_begin)
+hl_status hl_dispatch_ex(hl_handle* h, const uint32_t* rows, const int32_t* bag_ptr, int32_t n_samples, int32_t bps,
+                         int64_t n_lookups, uint32_t* gids, int32_t* codes, uint8_t* flags, int32_t* pop_ids,
+                         int32_t* nonpop_ids, int32_t* counts_dev, void* workspace, size_t ws_bytes,
+                         hl_stream stream, const hl_cg_fused* cf);
+// the rank scan of the fused plan: staging rows by first occurrence, the cold
+// id list (ids of staging rows below cap) and its count
+hl_status hl_cold_rank_fused(hl_handle* h, const uint32_t* gids, const int32_t* codes, int64_t n_lookups,
+                             uint32_t* cold_ids, int32_t* n_cold_dev, void* workspace, const hl_cg_fused& cf,
+                             hipStream_t s);
+
+// the cold-gather hash table: open addressing keyed by row id, a slot holds
+// (id + 1) << 32 | the smallest lookup index of that id (0 = empty)
+__device__ __forceinline__ uint32_t hl_cg_hash(uint32_t x) {  // 32-bit finalising mix
+  x ^= x >> 16;
+  x *= 0x85EBCA6Bu;
+  x ^= x >> 13;
+  x *= 0xC2B2AE35u;
+  x ^= x >> 16;
+  return x;
+}
+// enters id g of lookup i; returns its slot
+__device__ __forceinline__ uint32_t hl_cg_insert(uint64_t* table, uint32_t smask, uint32_t g, uint32_t i) {
+  const uint64_t want = ((uint64_t)(g + 1) << 32) | i;
+  uint32_t slot = hl_cg_hash(g) & smask;
+  for (uint32_t probe = 0; probe <= smask; ++probe) {
+    const uint64_t prev = atomicCAS((unsigned long long*)(table + slot), 0ull, (unsigned long long)want);
+    if (prev == 0) break;
+    if ((uint32_t)(prev >> 32) == g + 1) {
+      atomicMin((unsigned long long*)(table + slot), (unsigned long long)want);
+      break;
+    }
+    slot = (slot + 1) & smask;
+  }
+  return slot;
+}
 // hl_embbag_bwd_plan whose first kernel, when it launches one (*sent), also
 // stores sv into *sflag as it starts: a handover signal for the kernels
 // enqueued before it on the stream.
-hl_status hl_embbag_bwd_plan_signal(hl_handle* h, int32_t stg_rows, const int32_t* codes, const int32_t* bag_ptr,
+hl_status hl_embbag_bwd_plan_signal(hl_handle* h, int32_t stg_rows, int32_t* codes, const int32_t* bag_ptr,
                                     int32_t n_samples, int32_t bps, int64_t n_lookups, const int32_t* sample_ids,
                                     const int32_t* n_sel_dev, int32_t n_sel_max, void* workspace, size_t ws_bytes,
-                                    hl_stream stream, uint32_t* sflag, uint32_t sv, bool* sent);
+                                    hl_stream stream, uint32_t* sflag, uint32_t sv, bool* sent,
+                                    const hl_cg_fused* cf);
 
 // ----------------------------------------------------------------------------- sort
 // Stable LSD radix sort of (key, value) uint32 pairs with digits of up to 11

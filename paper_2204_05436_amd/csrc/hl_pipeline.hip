@@ -59,6 +59,7 @@
 #define PF_LOOK 7 // a look-ahead plan: its own sequence
 #define PF_DONE 8 // the end of a step on the main stream
 #define PF_SORT 9 // a look-ahead plan's grouping (plan sequence)
+#define PF_COLD 10 // a fused look-ahead plan's cold list (plan sequence; codes follow with PF_LOOK)
 #define PF_N 16
 #define PL_PLANS 4 // look-ahead plans not yet stepped
 
@@ -105,6 +106,7 @@ struct pl_plan {
   hl_step_io io;      // the inputs and per-step buffers it ran with
   uint32_t seq;       // its PF_LOOK value
   uint32_t need;      // the step whose end it waits for (0: none)
+  int cold_flag;      // the flag that tells its cold list is ready (PF_COLD, or PF_LOOK with the codes)
   bool pending;       // enqueued, not yet consumed by a step
 };
 
@@ -425,6 +427,14 @@ extern "C" hl_status hl_pipeline_plan(hl_pipeline* p, const hl_step_io* io, hl_s
   const bool sp = p->sort_pend;
   p->sort_pend = false;
   const int32_t B = io->n_samples, bps = io->bags_per_sample;
+  // the fused plan (five launches) with the grouping, when the workspace and
+  // the hash table allow it
+  hl_cg_fused cf{};
+  bool fuse = io->dY && io->n_lookups > 0 && B > 0 &&
+              hl_dispatch_fused(h, B, bps, io->n_lookups, io->workspace, io->ws_bytes);
+  if (fuse)
+    fuse = hl_cold_fused_begin(h, io->n_lookups, (int64_t)B * bps, B, io->staging_cap, io->workspace, io->ws_bytes, P,
+                               &cf) == HL_OK;
   // The waits order the plan's writes after the reads of the steps that used
   // its buffers, and it reads nothing they wrote, except the cold-gather hash
   // table after a step that ran its own cold plan: then one launch waits
@@ -440,23 +450,38 @@ extern "C" hl_status hl_pipeline_plan(hl_pipeline* p, const hl_step_io* io, hl_s
     HL_TRY(pl_hw(p, P, sp ? PF_SORT : -1, p->sort_v, need ? PF_DONE : -1, need, wb ? PF_WB : -1, wb));
     p->np_synced = p->np_last;
   }
-  PL_HOOKED(P, hl_dispatch(h, io->rows, io->bag_ptr, B, bps, io->n_lookups, io->gids, io->codes, io->flags,
-                           io->pop_ids, io->nonpop_ids, io->counts, io->workspace, io->ws_bytes, PS));
-  HL_TRY(hl_cold_plan(h, io->gids, io->codes, io->bag_ptr, B, bps, io->n_lookups, nullptr, nullptr, B,
-                      io->staging_cap, io->cold_ids, io->n_cold, io->workspace, io->ws_bytes, PS));
-  // the cold list is ready: the fetch may start while the grouping runs (the
-  // grouping's first kernel gives the signal as it starts)
+  PL_HOOKED(P, hl_dispatch_ex(h, io->rows, io->bag_ptr, B, bps, io->n_lookups, io->gids, io->codes, io->flags,
+                              io->pop_ids, io->nonpop_ids, io->counts, io->workspace, io->ws_bytes, PS,
+                              fuse ? &cf : nullptr));
   const uint32_t v = ++p->plan_seq;
   bool sent = false;
-  if (io->dY)
-    HL_TRY(hl_embbag_bwd_plan_signal(h, io->staging_cap, io->codes, io->bag_ptr, B, bps, io->n_lookups, nullptr,
-                                     nullptr, B, io->workspace, io->ws_bytes, PS, p->flags + PF_LOOK, v, &sent));
-  if (!sent) HL_TRY(pl_sig(p, P, PF_LOOK, v));
+  if (fuse) {
+    // the rank scan writes the cold list: the fetch may start once it ends
+    // (the grouping's first kernel signals it as it starts); that kernel also
+    // completes the codes, which the first sort pass then signals as it starts
+    HL_TRY(hl_cold_rank_fused(h, io->gids, io->codes, io->n_lookups, io->cold_ids, io->n_cold, io->workspace, cf, P));
+    pl_hook(p, PF_LOOK, v, -1, 0);
+    PL_HOOKED(P, hl_embbag_bwd_plan_signal(h, io->staging_cap, io->codes, io->bag_ptr, B, bps, io->n_lookups, nullptr,
+                                           nullptr, B, io->workspace, io->ws_bytes, PS, p->flags + PF_COLD, v, &sent,
+                                           &cf));
+    if (!sent) HL_TRY(pl_sig(p, P, PF_COLD, v));
+  } else {
+    HL_TRY(hl_cold_plan(h, io->gids, io->codes, io->bag_ptr, B, bps, io->n_lookups, nullptr, nullptr, B,
+                        io->staging_cap, io->cold_ids, io->n_cold, io->workspace, io->ws_bytes, PS));
+    // the cold list and the codes are ready: the fetch may start while the
+    // grouping runs (the grouping's first kernel gives the signal as it starts)
+    if (io->dY)
+      HL_TRY(hl_embbag_bwd_plan_signal(h, io->staging_cap, io->codes, io->bag_ptr, B, bps, io->n_lookups, nullptr,
+                                       nullptr, B, io->workspace, io->ws_bytes, PS, p->flags + PF_LOOK, v, &sent,
+                                       nullptr));
+    if (!sent) HL_TRY(pl_sig(p, P, PF_LOOK, v));
+  }
   p->sort_pend = true;
   p->sort_v = v;
   e->io = *io;
   e->seq = v;
   e->need = need;
+  e->cold_flag = fuse ? PF_COLD : PF_LOOK;
   e->pending = true;
   return HL_OK;
 }
@@ -490,7 +515,7 @@ extern "C" hl_status hl_pipeline_step(hl_pipeline* p, const hl_step_io* io, hl_s
     // (a pending end signal of the previous step is given by this step's
     // first main-stream launch, enqueued below)
     const uint32_t last = pl_stg_last(p, io->staging);
-    HL_TRY(pl_hw(p, f, -1, 0, PF_LOOK, e->seq, last ? PF_DONE : -1, last));
+    HL_TRY(pl_hw(p, f, -1, 0, e->cold_flag, e->seq, last ? PF_DONE : -1, last));
     HL_TRY(hl_cold_fetch(h, io->cold_ids, io->n_cold, cap, io->w_host, io->staging, F));
     HL_TRY(pl_sig(p, f, PF_FETCH, q));
     // main: the previous step's end signal and the wait for the plan (in the

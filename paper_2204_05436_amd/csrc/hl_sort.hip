@@ -132,7 +132,7 @@ __global__ void __launch_bounds__(HL_SORT_THREADS)
 srt_pass(const uint32_t* __restrict__ kin, const uint32_t* __restrict__ vin, uint32_t* __restrict__ kout,
          uint32_t* __restrict__ vout, const uint32_t* n_dev, uint32_t n_host, int shift, int b,
          const uint32_t* __restrict__ part, uint32_t n_part, uint32_t* st, uint32_t* st_next, uint32_t* tile_ctr,
-         uint32_t* err) {
+         uint32_t* err, hl_hook hk) {
   constexpr int PER = NB >= HL_SORT_THREADS ? NB / HL_SORT_THREADS : 1;
   constexpr int OWNERS = NB / PER;         // threads that own digits
   // look-back window per digit; every predecessor read costs a load per digit
@@ -147,6 +147,7 @@ srt_pass(const uint32_t* __restrict__ kin, const uint32_t* __restrict__ vin, uin
   __shared__ uint32_t lk[HL_SORT_TILE], lv[HL_SORT_TILE];
   const uint32_t n = srt_n(n_dev, n_host);
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  hl_hook_head(hk);
   if (tid == 0) s_tile = atomicInc(tile_ctr, gridDim.x - 1);
   for (int j = tid; j < HL_SORT_WAVES * NB; j += HL_SORT_THREADS) (&wcnt[0][0])[j] = 0;
   __syncthreads();
@@ -349,7 +350,8 @@ static hl_status srt_launch(hl_handle* h, hl_sort_ws& ws, const uint32_t* n_dev,
   for (int p = 0; p < g.passes; ++p) {
     HL_KERNEL(h, s, "srt_pass", srt_pass<NB>, dim3(tiles), dim3(HL_SORT_THREADS), 0, s, ki, vi, ko, vo, n_dev,
               n_host, g.b * p, g.b, ws.part + (size_t)p * HL_SORT_HIST_BLOCKS * NB, g.hist_blocks, ws.st[p & 1],
-              p + 1 < g.passes ? ws.st[(p + 1) & 1] : nullptr, ws.ctr + 1 + p, h->d_err);
+              p + 1 < g.passes ? ws.st[(p + 1) & 1] : nullptr, ws.ctr + 1 + p, h->d_err,
+              p == 0 ? hl_hook_take(h) : hl_hook{});
     uint32_t* t = ki;
     ki = ko;
     ko = t;

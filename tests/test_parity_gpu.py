@@ -534,6 +534,8 @@ def test_multi_step(name, mode, writeback):
         w_hot = O.gather(table.array, hot)
         dYs = [W.make_dy(w, 4 + si, mb.n_bags) for si, mb in enumerate(steps)]
         dbs = [to_device(mb, "cuda", dY) for mb, dY in zip(steps, dYs)]
+        if mode == "lookahead":
+            hl.hl_trace_enable(hp.h, 4096)
         for si, mb in enumerate(steps):
             pre = hp.w_hot[:len(hot)].cpu().numpy().copy()
             assert si > 0 or np.array_equal(pre.view(np.uint8), w_hot.view(np.uint8))
@@ -577,6 +579,14 @@ def test_multi_step(name, mode, writeback):
                 assert np.array_equal(tab.view(np.uint8), ref_tab.view(np.uint8)), f"step {si} write-back"
             else:
                 assert np.array_equal(tab.view(np.uint8), tab_pre.view(np.uint8)), f"step {si} host table changed"
+        if mode == "lookahead":
+            # every step is planned ahead, and the plans take the fused form: the
+            # dispatch kernel inserts the cold lookups and the grouping's first
+            # kernel writes their codes (no cold-plan insert or codes kernel)
+            names = [hl.hl_trace_read(hp.h, i)[0] for i in range(hl.hl_trace_count(hp.h))]
+            hl.hl_trace_enable(hp.h, 0)
+            assert names.count("cg_insert") == 0 and names.count("cg_codes") == 0, names
+            assert names.count("cg_rank") == len(steps) and names.count("ds_kernel") == len(steps), names
     finally:
         hp.close()
         table.close()
