@@ -3,15 +3,17 @@
 // A sort of `bits` bits takes P = ceil(bits / 11) passes of b = ceil(bits / P)
 // bits (two passes of 10 bits for the backward's 20-bit keys).  One histogram
 // kernel counts every digit position in a single read of the keys (per-block
-// counts) and clears the first pass's look-back status.  Then one kernel per
+// counts) and clears the first pass's status words.  Then one kernel per
 // digit: a block takes the next tile (dynamic tile ids, so every lower tile is
 // already running), ranks its items by digit with per-wave LDS counters (the
-// counters' totals are the tile's digit counts), publishes the counts, obtains
-// those of all earlier tiles by decoupled look-back, reorders the tile in LDS
-// so that each digit's run is contiguous and writes it out.  Only tile 0 adds
-// up the histogram: its published prefix starts from each digit's global
-// offset, so the look-back hands the offsets to every later tile.  Each pass block also
-// clears its tile's status words for the next pass.  Item order inside a tile
+// counters' totals are the tile's digit counts), publishes the counts, adds up
+// the counts of all earlier tiles (read together, 64 words in flight per
+// thread: at these sizes every tile runs at once, so one round of loads
+// replaces a chain of inclusive prefixes), adds each digit's global offset
+// (the histogram's exclusive scan, which every tile forms), and writes out the
+// tile, which it has reordered in LDS (before reading the earlier tiles'
+// counts) so that each digit's run is contiguous.  Each pass
+// block also clears its tile's status words for the next pass.  Item order inside a tile
 // is wave-major, then item, then lane, which is index order, so the sort is
 // stable.
 #include "hl_internal.h"
@@ -29,17 +31,26 @@ void hl_sort_ws_carve(hl_carver& c, hl_sort_ws& ws, uint32_t n_max) {
   ws.ctr = c.base ? c.header() + HL_HDR_SORT : nullptr;
 }
 
-// Status word of (tile, digit): flag in the top two bits (0 = not yet
-// published), count below.  Relaxed agent-scope atomics: the word carries its
-// own value and no other data is published through it.
+// Status of (tile, digit): a flag bit (0 = not yet published) over the
+// tile's count of the digit.  With one digit per owning thread a 32-bit word
+// per digit (SRT_AGG); with two or more, two digits share a word, 16 bits
+// each (SRT_AGG2 per half: a tile's count stays below 2^15), so a thread
+// reads its digits' counts of a tile in one load.  Relaxed agent-scope
+// atomics: a word carries its own value and no other data is published
+// through it.
 #define SRT_AGG 0x40000000u
-#define SRT_PRE 0x80000000u
 #define SRT_VAL 0x3FFFFFFFu
+#define SRT_AGG2 0x80008000u
+static_assert(HL_SORT_TILE < 0x8000, "a tile's digit count must fit 15 bits");
 __device__ __forceinline__ void srt_st_store(uint32_t* p, uint32_t w) {
   __hip_atomic_store(p, w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 __device__ __forceinline__ uint32_t srt_st_load(const uint32_t* p) {
   return __hip_atomic_load(const_cast<uint32_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint64_t srt_st_load2(const uint32_t* p) {  // two words (8-byte aligned)
+  return __hip_atomic_load(reinterpret_cast<uint64_t*>(const_cast<uint32_t*>(p)), __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
 }
 
 __device__ __forceinline__ uint32_t srt_n(const uint32_t* n_dev, uint32_t n_host) {
@@ -135,11 +146,11 @@ srt_pass(const uint32_t* __restrict__ kin, const uint32_t* __restrict__ vin, uin
          uint32_t* err, hl_hook hk) {
   constexpr int PER = NB >= HL_SORT_THREADS ? NB / HL_SORT_THREADS : 1;
   constexpr int OWNERS = NB / PER;         // threads that own digits
-  // look-back window per digit; every predecessor read costs a load per digit
-  // (NB x tiles^2 / 2 loads when no inclusive prefix is found early), so the
-  // window stays short and the walk stops at the first inclusive prefix
-  constexpr int WIN = PER >= 4 ? 8 : 16;
-  constexpr int WIN0 = 4;
+  // status words of a tile per digit owner, and the earlier tiles whose
+  // counts one round reads (48 words in flight per thread)
+  constexpr int PW = PER >= 2 ? PER / 2 : 1;
+  constexpr int CHUNK = 48 / PW;
+  constexpr size_t TW = PER >= 2 ? NB / 2 : NB;  // words per tile
   __shared__ uint32_t s_tile;
   __shared__ uint32_t wcnt[HL_SORT_WAVES][NB];
   __shared__ uint32_t tdex[NB], gbase[NB];
@@ -153,7 +164,7 @@ srt_pass(const uint32_t* __restrict__ kin, const uint32_t* __restrict__ vin, uin
   __syncthreads();
   const uint32_t tile = s_tile;
   if (st_next)  // this tile's status words of the next pass
-    for (int j = tid; j < NB; j += HL_SORT_THREADS) st_next[(size_t)tile * NB + j] = 0;
+    for (int j = tid; j < (int)TW; j += HL_SORT_THREADS) st_next[(size_t)tile * TW + j] = 0;
   const uint64_t tb = (uint64_t)tile * HL_SORT_TILE;
   if (tb >= n) return;
   const uint32_t mask = (1u << b) - 1u;
@@ -165,25 +176,23 @@ srt_pass(const uint32_t* __restrict__ kin, const uint32_t* __restrict__ vin, uin
     key[k] = ok ? kin[idx] : 0xFFFFFFFFu;
     val[k] = ok ? vin[idx] : 0u;
   }
-  // global counts of the owned digits (loads issued together), read by tile 0
-  // only: its published prefix carries the digits' global offsets, so every
-  // later tile obtains them through the look-back
+  // global counts of the owned digits: loads issued with the keys', summed
+  // after the ranking (which waits only for the keys)
   const int d0 = tid * PER;
   const bool owner = tid < OWNERS;
-  uint32_t dtot[PER];
-  {
-    const uint32_t np = tile == 0 ? n_part : 0u;
-    uint32_t pv[PER][HL_SORT_HIST_BLOCKS];
+  uint32_t pv[PER][HL_SORT_HIST_BLOCKS];
 #pragma unroll
-    for (int j = 0; j < PER; ++j)
+  for (int q = 0; q < HL_SORT_HIST_BLOCKS; ++q) {
+    const bool in = owner && (uint32_t)q < n_part;
+    if constexpr (PER >= 2) {  // two digits per load
 #pragma unroll
-      for (int q = 0; q < HL_SORT_HIST_BLOCKS; ++q)
-        pv[j][q] = (owner && (uint32_t)q < np) ? part[(size_t)q * NB + d0 + j] : 0u;
-#pragma unroll
-    for (int j = 0; j < PER; ++j) {
-      dtot[j] = 0;
-#pragma unroll
-      for (int q = 0; q < HL_SORT_HIST_BLOCKS; ++q) dtot[j] += pv[j][q];
+      for (int j = 0; j < PER; j += 2) {
+        const uint2 x = in ? *reinterpret_cast<const uint2*>(part + (size_t)q * NB + d0 + j) : make_uint2(0u, 0u);
+        pv[j][q] = x.x;
+        pv[j + 1][q] = x.y;
+      }
+    } else {
+      pv[0][q] = in ? part[(size_t)q * NB + d0] : 0u;
     }
   }
   // ranking: every item adds 1 to its digit's counter of the wave; the old
@@ -199,8 +208,16 @@ srt_pass(const uint32_t* __restrict__ kin, const uint32_t* __restrict__ vin, uin
     dg[k] = (key[k] >> shift) & mask;
     lr[k] = idx < n ? atomicAdd(&wcnt[w][dg[k]], 1u) : 0u;
   }
+  uint32_t dtot[PER];
+#pragma unroll
+  for (int j = 0; j < PER; ++j) {
+    dtot[j] = 0;
+#pragma unroll
+    for (int q = 0; q < HL_SORT_HIST_BLOCKS; ++q) dtot[j] += pv[j][q];
+  }
   __syncthreads();
-  // wave-exclusive offsets of each owned digit; the totals are the tile's counts
+  // wave-exclusive offsets of each owned digit; the totals are the tile's
+  // counts, published at once for the later tiles
   uint32_t tc[PER], tx[PER];
 #pragma unroll
   for (int j = 0; j < PER; ++j) {
@@ -214,84 +231,26 @@ srt_pass(const uint32_t* __restrict__ kin, const uint32_t* __restrict__ vin, uin
       }
     tc[j] = run;
     tx[j] = run;
-    if (owner && tile > 0) srt_st_store(st + (size_t)tile * NB + d0 + j, SRT_AGG | run);
+  }
+  if (owner) {
+    if constexpr (PER >= 2) {
+#pragma unroll
+      for (int j = 0; j < PER; j += 2)
+        srt_st_store(st + (size_t)tile * TW + (d0 + j) / 2, SRT_AGG2 | tc[j] | (tc[j + 1] << 16));
+    } else {
+      srt_st_store(st + (size_t)tile * TW + d0, SRT_AGG | tc[0]);
+    }
   }
   uint32_t gx[PER];
 #pragma unroll
   for (int j = 0; j < PER; ++j) gx[j] = dtot[j];
   srt_scan2<NB, PER>(tx, gx, scan_ws);
-  // tile 0: inclusive prefix = the digit's global offset + its own count
-  if (owner && tile == 0)
+  if (owner)
 #pragma unroll
-    for (int j = 0; j < PER; ++j) srt_st_store(st + d0 + j, SRT_PRE | (gx[j] + tc[j]));
-  // decoupled look-back: counts of this digit in all earlier tiles
-  uint32_t excl[PER];
-  int64_t jj[PER];
-#pragma unroll
-  for (int j = 0; j < PER; ++j) {
-    excl[j] = 0;
-    jj[j] = owner ? (int64_t)tile - 1 : -1;
-  }
-  uint32_t spins = 0;
-  // the first window is short: the nearest tiles have most likely published
-  // their inclusive prefix by then, and each word read costs bandwidth
-  int win = WIN0;
-  while (true) {
-    uint32_t wv[PER][WIN];
-#pragma unroll
-    for (int j = 0; j < PER; ++j)
-#pragma unroll
-      for (int q = 0; q < WIN; ++q)
-        wv[j][q] = q < win && jj[j] - q >= 0 ? srt_st_load(st + (size_t)(jj[j] - q) * NB + d0 + j) : SRT_PRE;
-    bool any = false, stall = false;
-#pragma unroll
-    for (int j = 0; j < PER; ++j) {
-      if (jj[j] < 0) continue;
-      int used = 0;
-      bool stop = false;
-#pragma unroll
-      for (int q = 0; q < WIN; ++q) {
-        if (stop) continue;
-        if (q >= win) {  // beyond this round's window
-          stop = true;
-          continue;
-        }
-        const uint32_t x = wv[j][q];
-        if ((x & (SRT_AGG | SRT_PRE)) == 0) {  // not yet published
-          stop = true;
-          stall = true;
-          continue;
-        }
-        if (jj[j] - q >= 0) excl[j] += x & SRT_VAL;
-        if (x & SRT_PRE) {
-          used = -1;
-          stop = true;
-          continue;
-        }
-        used = q + 1;
-      }
-      jj[j] = used < 0 ? -1 : jj[j] - used;
-      any |= jj[j] >= 0;
-    }
-    if (!any) break;
-    win = WIN;
-    if (stall) {
-      if (++spins > HL_SPIN_LIMIT) {
-        hl_flag(err, HL_DEVERR_STALL);
-        break;
-      }
-      __builtin_amdgcn_s_sleep(1);
-    }
-  }
-  if (owner) {
-#pragma unroll
-    for (int j = 0; j < PER; ++j) {
-      if (tile > 0) srt_st_store(st + (size_t)tile * NB + d0 + j, SRT_PRE | (excl[j] + tc[j]));
-      tdex[d0 + j] = tx[j];
-      gbase[d0 + j] = tile == 0 ? gx[j] : excl[j];
-    }
-  }
+    for (int j = 0; j < PER; ++j) tdex[d0 + j] = tx[j];
   __syncthreads();
+  // the tile in digit order in LDS (its own offsets are known now; the
+  // earlier tiles' counts are read below)
 #pragma unroll
   for (int k = 0; k < HL_SORT_ITEMS; ++k) {
     const uint64_t idx = tb + (uint64_t)w * (HL_SORT_ITEMS * 64) + k * 64 + lane;
@@ -301,6 +260,61 @@ srt_pass(const uint32_t* __restrict__ kin, const uint32_t* __restrict__ vin, uin
       lv[p] = val[k];
     }
   }
+  // counts of each owned digit in all earlier tiles: their published counts,
+  // read CHUNK tiles at a time with every load in flight (no chain through
+  // inclusive prefixes); a round with an unpublished word is read again
+  uint32_t excl[PER];
+#pragma unroll
+  for (int j = 0; j < PER; ++j) excl[j] = 0;
+  uint32_t spins = 0;
+  for (uint32_t q0 = 0; owner && q0 < tile; q0 += CHUNK) {
+    for (;;) {
+      uint32_t wv[CHUNK][PW];
+#pragma unroll
+      for (int q = 0; q < CHUNK; ++q) {
+        const bool in = q0 + q < tile;
+        const uint32_t* a = st + (size_t)(q0 + q) * TW + (PER >= 2 ? d0 / 2 : d0);
+        if constexpr (PW == 2) {
+          const uint64_t x = in ? srt_st_load2(a) : ((uint64_t)SRT_AGG2 << 32 | SRT_AGG2);
+          wv[q][0] = (uint32_t)x;
+          wv[q][1] = (uint32_t)(x >> 32);
+        } else {
+          wv[q][0] = in ? srt_st_load(a) : (PER >= 2 ? SRT_AGG2 : SRT_AGG);
+        }
+      }
+      bool ready = true;
+      uint32_t sum[PER];
+#pragma unroll
+      for (int j = 0; j < PER; ++j) sum[j] = 0;
+#pragma unroll
+      for (int q = 0; q < CHUNK; ++q)
+#pragma unroll
+        for (int x = 0; x < PW; ++x) {
+          const uint32_t v = wv[q][x];
+          if constexpr (PER >= 2) {
+            ready = ready && (v & SRT_AGG2) == SRT_AGG2;
+            sum[2 * x] += v & 0x7FFFu;
+            sum[2 * x + 1] += (v >> 16) & 0x7FFFu;
+          } else {
+            ready = ready && (v & SRT_AGG) != 0;
+            sum[0] += v & SRT_VAL;
+          }
+        }
+      if (ready) {
+#pragma unroll
+        for (int j = 0; j < PER; ++j) excl[j] += sum[j];
+        break;
+      }
+      if (++spins > HL_SPIN_LIMIT) {
+        hl_flag(err, HL_DEVERR_STALL);
+        break;
+      }
+      __builtin_amdgcn_s_sleep(1);
+    }
+  }
+  if (owner)
+#pragma unroll
+    for (int j = 0; j < PER; ++j) gbase[d0 + j] = gx[j] + excl[j];
   __syncthreads();
   const uint32_t nv = (uint32_t)min((uint64_t)HL_SORT_TILE, (uint64_t)n - tb);
 #pragma unroll 4
