@@ -178,11 +178,28 @@ def main():
     log(f"[bench] learning phase {learn_ms:.2f} ms, n_hot {n_hot}")
 
     if args.pmc:
-        # the same kernels one at a time on one stream: a counter run
+        # the step's kernels one at a time on one stream (a counter run
         # serializes dispatches, which the pipelined schedule's cross-stream
-        # waits would stall on
+        # waits would stall on), through the calls that launch the same kernel
+        # variants as the pipelined step where the library has them: the hot
+        # half of the forward over every sample, the grouping's sort passes,
+        # the split reduction, the staging-row updates and the host-link copy
+        h = hp.h
         for i in range(args.warmup + args.steps):
-            hp.step(dmeas[i % len(dmeas)], mode="sequential")
+            b = dmeas[i % len(dmeas)]
+            B, bps, L, cap = b.n_samples, b.bps, b.n_lookups, hp.staging_cap
+            hl.hl_dispatch(h, b.rows, b.bag_ptr, B, bps, L, hp.gids, hp.codes, hp.flags, hp.pop, hp.nonpop,
+                           hp.counts, hp.ws)
+            hl.hl_cold_plan(h, hp.gids, hp.codes, b.bag_ptr, B, bps, L, None, None, B, cap, hp.cold_ids, hp.n_cold,
+                            hp.ws)
+            hl.hl_cold_fetch(h, hp.cold_ids, hp.n_cold, cap, table.dev, hp.staging)
+            hl.hl_embbag_bwd_plan(h, cap, hp.codes, b.bag_ptr, B, bps, L, None, None, B, hp.ws)
+            hl.hl_embbag_fwd_part(h, hp.w_hot, hp.staging, cap, hp.codes, b.bag_ptr, B, bps, L, None, None, B,
+                                  hp.out, 1)
+            hl.hl_embbag_bwd_apply_part(h, hp.w_hot, hp.staging, cap, B, bps, L, b.dY, w.lr, 1, hp.ws)
+            hl.hl_embbag_fwd_part(h, hp.w_hot, hp.staging, cap, hp.codes, b.bag_ptr, B, bps, L, hp.nonpop,
+                                  hp.counts[1:], B, hp.out, 2)
+            hl.hl_embbag_bwd_apply_part(h, hp.w_hot, hp.staging, cap, B, bps, L, b.dY, w.lr, 2, hp.ws)
         torch.cuda.synchronize()
         n_cal = 256 << 20
         src = torch.ones(n_cal // 4, dtype=torch.float32, device=dev)
