@@ -658,6 +658,46 @@ def test_lookahead_chain(name, writeback):
                     np.maximum(np.abs(as_f64(tab0, w.dtype)), 1e-3), rtol, "host table after the chain")
 
 
+@pytest.mark.parametrize("writeback", [False, True])
+def test_mixed_plain_and_planned(writeback):
+    """Plain steps (their own dispatch and cold plan on the main stream) and
+    planned ones (look-ahead plans on the plan stream) interleaved in one untied
+    chain: a plan after a plain step waits for it with a launch of its own (the
+    plain step's cold plan leaves the shared hash table, which the plan reads),
+    the others wait inside the dispatch kernel.  The hot cache and the host
+    table end bit for bit where plain steps alone leave them."""
+    w = configs.scaled(configs.WORKLOADS["dlrm-large"], batch=640, row_scale=0.004, name="dlrm-large-mixed")
+    rows = W.table_rows(w)
+    n_rows = int(rows.sum())
+    prof = [W.make_batch(w, rows, i) for i in range(4)]
+    steps = [W.make_batch(w, rows, 4 + s) for s in range(8)]
+    dYs = [W.make_dy(w, 4 + si, mb.n_bags) for si, mb in enumerate(steps)]
+    # which steps plan ahead: step i plans batch i + 1 when ahead[i]
+    ahead = [False, True, True, False, False, True, False, False]
+    finals = {}
+    for variant in ("plain", "mixed"):
+        table = make_table(w, n_rows)
+        hp = HotPath(w, rows, table, max(b.n_lookups for b in prof + steps), w.batch, writeback=writeback)
+        try:
+            hp.learn([to_device(p, "cuda") for p in prof])
+            dbs = [to_device(mb, "cuda", dY) for mb, dY in zip(steps, dYs)]
+            side = torch.cuda.Stream()
+            side.wait_stream(torch.cuda.current_stream())
+            with torch.cuda.stream(side):
+                for si in range(len(dbs)):
+                    nxt = dbs[si + 1] if variant == "mixed" and ahead[si] and si + 1 < len(dbs) else None
+                    hp.step(dbs[si], untied=True, next=nxt)
+                hp.sync()
+            torch.cuda.synchronize()
+            assert hp.device_error() == 0, variant
+            finals[variant] = (hp.w_hot[:hp.n_hot].cpu().numpy().copy(), table.array.copy())
+        finally:
+            hp.close()
+            table.close()
+    assert np.array_equal(finals["plain"][0].view(np.uint8), finals["mixed"][0].view(np.uint8)), "hot cache"
+    assert np.array_equal(finals["plain"][1].view(np.uint8), finals["mixed"][1].view(np.uint8)), "host table"
+
+
 @pytest.mark.parametrize("name", ["dlrm-large", "multi-hot"])
 def test_relearn_migration(name):
     """Re-learning after training steps (with write-back): the new hot set is
