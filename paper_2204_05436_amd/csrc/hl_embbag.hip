@@ -20,8 +20,12 @@
 #include "hl_internal.h"
 
 #define EB_SENT 0xFFFFFFFFu
-#define RB_E 8
-#define RB_WAVES 8
+#ifndef RB_E
+#define RB_E 8      // sorted entries per row group of the reduction
+#endif
+#ifndef RB_WAVES
+#define RB_WAVES 2  // waves per reduction block (2 measured fastest: a block waits for its slowest wave)
+#endif
 #define RB_BLOCK (RB_WAVES * 64)
 
 // ----------------------------------------------------------------------------- row I/O
