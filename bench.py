@@ -107,7 +107,7 @@ def reference_regions(hp, dmeas, side, K):
     out["fwd_bwd_section_us_mean"], out["fwd_bwd_section_us_median"] = 1e3 * np.mean(fb), 1e3 * np.median(fb)
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(len(STAGES) + 1)] for _ in range(K)]
     for i in range(K):
-        hp.step(dmeas[i % len(dmeas)], events=ev[i], mode="sequential")
+        hp.step(dmeas[i % len(dmeas)], events=ev[i], mode="sequential", split_fwd=False)
     torch.cuda.synchronize()
     st = {s: 0.0 for s in STAGES}
     for i in range(K):
@@ -321,9 +321,12 @@ def main():
     bwd_b = 4 * avg["L"] + 4 * (avg["n_bags"] + 1) + avg["n_bags"] * avg["O"] + 2 * avg["U"] * avg["R"]
     fb_frac = (fwd_b + bwd_b) / (t_fb / 1e3) / HBM_PEAK
 
-    # roofline of the dominant kernel by time per step (the host-link-bound row
-    # copy excluded: it is reported against the link)
-    dom = next(n for n in kernels if n not in ("cg_fetch", "cg_scatter"))
+    # roofline of the dominant kernel of the forward and backward (the HBM-bound
+    # part of the path) by time per step.  The host-link copy is reported against
+    # the link; the plan stream's kernels run a mini-batch ahead, and the dispatch
+    # kernel's blocks start by waiting for the steps that last used its buffers,
+    # so its launch duration is not its own work.
+    dom = next(n for n in kernels if n in fb_kernels)
     if kernel_bytes(dom, avg) is None:
         raise SystemExit(f"no byte model for the dominant kernel {dom}")
     kd = kernels[dom]
@@ -340,6 +343,26 @@ def main():
         gb = avg["n_cold"] * avg["R"]
         link = {"kernel": "cg_fetch", "bytes_per_launch": gb, "avg_us": kernels["cg_fetch"]["avg_us"],
                 "achieved_GBps": gb / (kernels["cg_fetch"]["avg_us"] * 1e-6) / 1e9, "peak_GBps": LINK_PEAK / 1e9}
+
+    # the same batches through the library's calls in order on one stream, each
+    # stage alone on the whole GPU (events between the stages): the forward and
+    # backward without the host-link copy and the plans running beside them
+    from paper_2204_05436_amd.runner import STAGES
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(len(STAGES) + 1)] for _ in range(K)]
+    with torch.cuda.stream(side):
+        for i in range(K):
+            hp.step(dmeas[i % len(dmeas)], events=ev[i], mode="sequential", split_fwd=False)
+    torch.cuda.synchronize()
+    err = hp.device_error()
+    if err:
+        raise SystemExit(f"device error word {err:#x} in the sequential steps")
+    st = {s: sum(ev[i][j].elapsed_time(ev[i][j + 1]) for i in range(K)) / K for j, s in enumerate(STAGES)}
+    t_fb1 = st["fwd_pop"] + st["fwd_nonpop"] + st["bwd"]
+    alone = {"stage_ms": st, "fwd_bwd_us": t_fb1 * 1e3, "fwd_bwd_lookups_per_s": avg["L"] / (t_fb1 / 1e3),
+             "fwd_bwd_hbm_frac": (fwd_b + bwd_b) / (t_fb1 / 1e3) / HBM_PEAK,
+             "classify_samples_per_s": avg["B"] / ((st["classify"] + st["partition"]) / 1e3)}
+    log(f"[bench] stages alone: " + ", ".join(f"{s} {v * 1e3:.1f}us" for s, v in st.items()) +
+        f"; fwd+bwd {alone['fwd_bwd_hbm_frac']:.3f} of the HBM peak")
 
     breakdown = None
     if args.breakdown:
@@ -398,6 +421,7 @@ def main():
         "fwd_bwd_lookups_per_s": avg["L"] / (t_fb / 1e3),
         "fwd_bwd_hbm_frac": fb_frac,
         "fwd_bwd_algorithmic_bytes": fwd_b + bwd_b,
+        "alone_on_gpu": alone,
         # the dispatch kernel classifies, partitions and remaps a mini-batch
         "classify_samples_per_s": avg["B"] / (kernels["ds_kernel"]["avg_us"] * 1e-6),
         "popular_fraction": avg["n_pop"] / avg["B"],
