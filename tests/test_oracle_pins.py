@@ -12,6 +12,8 @@
   equals unsplit (Eq. 5), linearity of the update, untouched rows unchanged.
 """
 import collections
+import json
+import pathlib
 
 import numpy as np
 import pytest
@@ -37,11 +39,20 @@ import oracle as O
 #   G(id6) = (2,0)               -> (2,2) - (1,0)    = (1, 2)
 #   K = 1: the tie id1/id4 at count 2 goes to the smaller id -> hot = {1}; no
 #   sample is all-hot; cold ids by first occurrence = [4, 6, 3].
-HAND_ROWS_PER_TABLE = np.array([4, 3], np.uint32)
-HAND_TABLE = np.array([[1, 2], [3, 4], [5, 6], [7, 8], [-1, 0], [0, -1], [2, 2]], np.float32)
-HAND_ROWS = np.array([1, 0, 1, 2, 3, 0], np.uint32)
-HAND_PTR = np.arange(7, dtype=np.int32)
-HAND_DY = np.array([[1, 0], [0, 1], [1, 1], [2, 0], [0, -1], [1, 1]], np.float32)
+GOLD = pathlib.Path(__file__).parent / "golden"
+
+
+def _gold(name):
+    return json.loads((GOLD / name).read_text())
+
+
+HAND = _gold("hand_two_tables.json")
+HAND_ROWS_PER_TABLE = np.array(HAND["rows_per_table"], np.uint32)
+HAND_TABLE = np.array(HAND["table"], np.float32)
+HAND_ROWS = np.array(HAND["rows"], np.uint32)
+HAND_PTR = np.array(HAND["bag_ptr"], np.int32)
+HAND_DY = np.array(HAND["dY"], np.float32)
+HAND_B, HAND_BPS, HAND_LR = HAND["n_samples"], HAND["bags_per_sample"], HAND["lr"]
 
 
 def _table(dtype):
@@ -57,33 +68,34 @@ def _as_f64(a, dtype):
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_hand_example_k2(dtype):
+    x = HAND["k2"]
     g, rc = O.gids(HAND_ROWS_PER_TABLE, HAND_ROWS, HAND_PTR)
-    assert rc == 0 and g.tolist() == [1, 4, 1, 6, 3, 4]
-    counts, _ = O.count(7, [g])
-    assert counts.tolist() == [0, 2, 0, 1, 2, 0, 1]
-    hot = O.topk(counts, 2)
-    assert hot.tolist() == [1, 4]
-    flags = O.classify(hot, g, HAND_PTR, 3, 2)
-    assert flags.tolist() == [1, 0, 0]
+    assert rc == 0 and g.tolist() == HAND["gids"]
+    counts, _ = O.count(len(HAND_TABLE), [g])
+    assert counts.tolist() == HAND["counts"]
+    hot = O.topk(counts, len(x["hot"]))
+    assert hot.tolist() == x["hot"]
+    flags = O.classify(hot, g, HAND_PTR, HAND_B, HAND_BPS)
+    assert flags.tolist() == x["flags"]
     pop, nonpop = O.partition(flags)
-    assert pop.tolist() == [0] and nonpop.tolist() == [1, 2]
+    assert pop.tolist() == x["pop"] and nonpop.tolist() == x["nonpop"]
     codes0 = O.remap(hot, g)
-    assert codes0.tolist() == [0, 1, 0, -1, -1, 1]
-    cold, codes = O.cold_plan(g, codes0, HAND_PTR, nonpop, 2, 2, 2)
-    assert cold.tolist() == [6, 3] and codes.tolist() == [0, 1, 0, 2, 3, 1]
+    assert codes0.tolist() == x["codes_remap"]
+    cold, codes = O.cold_plan(g, codes0, HAND_PTR, nonpop, len(nonpop), HAND_BPS, len(hot))
+    assert cold.tolist() == x["cold_ids"] and codes.tolist() == x["codes"]
     table = _table(dtype)
     w_hot, stg = O.gather(table, hot), O.gather(table, cold)
-    assert _as_f64(stg, dtype).tolist() == [[2, 2], [7, 8]]
-    out, _, rc = O.embbag_fwd(dtype, w_hot, 2, stg, codes, HAND_PTR, None, 3, 2, 6)
+    assert _as_f64(stg, dtype).tolist() == x["staging"]
+    out, _, rc = O.embbag_fwd(dtype, w_hot, len(hot), stg, codes, HAND_PTR, None, HAND_B, HAND_BPS, len(g))
     assert rc == 0
-    assert out.tolist() == [[3, 4], [-1, 0], [3, 4], [2, 2], [7, 8], [-1, 0]]
-    uniq, scale, rc = O.embbag_bwd_sgd(dtype, w_hot, 2, stg, codes, HAND_PTR, None, 3, 2, HAND_DY, 0.5,
-                                       want_scale=True)
-    assert rc == 0 and uniq.tolist() == [0, 1, 2, 3]
-    assert _as_f64(w_hot, dtype).tolist() == [[2, 3.5], [-1.5, -1]]
-    assert _as_f64(stg, dtype).tolist() == [[1, 2], [7, 8.5]]
+    assert out.tolist() == x["out"]
+    uniq, scale, rc = O.embbag_bwd_sgd(dtype, w_hot, len(hot), stg, codes, HAND_PTR, None, HAND_B, HAND_BPS, HAND_DY,
+                                       HAND_LR, want_scale=True)
+    assert rc == 0 and uniq.tolist() == x["unique_codes"]
+    assert _as_f64(w_hot, dtype).tolist() == x["w_hot_after"]
+    assert _as_f64(stg, dtype).tolist() == x["staging_after"]
     # error scale |row| + lr * sum|dY| for code 0 (id 1): (3 + 0.5*2, 4 + 0.5*1)
-    assert scale[0].tolist() == [4.0, 4.5]
+    assert scale[0].tolist() == x["error_scale_code0"]
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
@@ -91,36 +103,41 @@ def test_hand_example_writeback(dtype):
     """After the K=2 step, writing the updated cold rows back and taking the hot
     rows from the cache gives the whole table updated by one SGD step (hand
     values above); rows no lookup names keep their bits."""
+    x = HAND["k2"]
     g, _ = O.gids(HAND_ROWS_PER_TABLE, HAND_ROWS, HAND_PTR)
-    hot = np.array([1, 4], np.uint32)
-    _, nonpop = O.partition(O.classify(hot, g, HAND_PTR, 3, 2))
-    cold, codes = O.cold_plan(g, O.remap(hot, g), HAND_PTR, nonpop, 2, 2, 2)
+    hot = np.array(x["hot"], np.uint32)
+    _, nonpop = O.partition(O.classify(hot, g, HAND_PTR, HAND_B, HAND_BPS))
+    cold, codes = O.cold_plan(g, O.remap(hot, g), HAND_PTR, nonpop, len(nonpop), HAND_BPS, len(hot))
     table = _table(dtype)
     w_hot, stg = O.gather(table, hot), O.gather(table, cold)
-    O.embbag_bwd_sgd(dtype, w_hot, 2, stg, codes, HAND_PTR, None, 3, 2, HAND_DY, 0.5)
+    O.embbag_bwd_sgd(dtype, w_hot, len(hot), stg, codes, HAND_PTR, None, HAND_B, HAND_BPS, HAND_DY, HAND_LR)
     host = table.copy()
     O.scatter(host, cold, stg)
-    assert _as_f64(host[[6, 3]], dtype).tolist() == [[1, 2], [7, 8.5]]
-    for r in (0, 1, 2, 4, 5):
-        assert (host[r] == table[r]).all()
+    assert _as_f64(host[cold.astype(np.int64)], dtype).tolist() == x["staging_after"]
+    named = set(hot.tolist()) | set(cold.tolist())
+    for r in range(len(table)):
+        if r not in named:
+            assert (host[r] == table[r]).all()
     host[hot] = w_hot
-    assert _as_f64(host, dtype).tolist() == [[1, 2], [2, 3.5], [5, 6], [7, 8.5], [-1.5, -1], [0, -1], [1, 2]]
+    assert _as_f64(host, dtype).tolist() == x["table_after_writeback"]
 
 
 def test_hand_example_k1_tie_and_multihot():
+    x = HAND["k1"]
     g, _ = O.gids(HAND_ROWS_PER_TABLE, HAND_ROWS, HAND_PTR)
-    counts, _ = O.count(7, [g])
+    counts, _ = O.count(len(HAND_TABLE), [g])
     hot = O.topk(counts, 1)
-    assert hot.tolist() == [1]
-    flags = O.classify(hot, g, HAND_PTR, 3, 2)
+    assert hot.tolist() == x["hot"]
+    flags = O.classify(hot, g, HAND_PTR, HAND_B, HAND_BPS)
     pop, nonpop = O.partition(flags)
-    assert pop.tolist() == [] and nonpop.tolist() == [0, 1, 2]
-    cold, codes = O.cold_plan(g, O.remap(hot, g), HAND_PTR, nonpop, 3, 2, 1)
-    assert cold.tolist() == [4, 6, 3]
-    assert codes.tolist() == [0, 1, 0, 2, 3, 1]
+    assert pop.tolist() == x["pop"] and nonpop.tolist() == x["nonpop"]
+    cold, codes = O.cold_plan(g, O.remap(hot, g), HAND_PTR, nonpop, len(nonpop), HAND_BPS, len(hot))
+    assert cold.tolist() == x["cold_ids"]
+    assert codes.tolist() == x["codes"]
     # multi-hot bag {id1, id1, id2} pools to (3+3+5, 4+4+6)
-    out = O.embbag_fwd_flat("f32", HAND_TABLE, np.array([1, 1, 2], np.uint32), np.array([0, 3], np.int32))
-    assert out.tolist() == [[11, 14]]
+    m = HAND["multi_hot_bag"]
+    out = O.embbag_fwd_flat("f32", HAND_TABLE, np.array(m["ids"], np.uint32), np.array([0, len(m["ids"])], np.int32))
+    assert out.tolist() == [m["out"]]
 
 
 def test_out_of_range_row_is_reported():
@@ -368,14 +385,12 @@ def test_empty_inputs():
 # moves to slot 0 with (30, 30), and its stale host copy (3, 3) is left alone.
 # Row 4 enters from the host: (4, 4) in slot 1.  One row written back.
 def test_migrate_hand_example():
-    host = np.repeat(np.arange(6, dtype=np.float32)[:, None], 2, axis=1).copy()
-    w_old = np.array([[10, 10], [30, 30]], np.float32)
-    w_new, n = O.migrate([1, 3], w_old, [3, 4], host)
-    assert n == 1
-    assert np.array_equal(w_new, np.array([[30, 30], [4, 4]], np.float32))
-    expect = np.repeat(np.arange(6, dtype=np.float32)[:, None], 2, axis=1)
-    expect[1] = 10
-    assert np.array_equal(host, expect)
+    x = _gold("migrate_hand.json")
+    host = np.repeat(np.arange(x["n_rows"], dtype=np.float32)[:, None], 2, axis=1).copy()
+    w_new, n = O.migrate(x["old_ids"], np.array(x["w_old"], np.float32), x["new_ids"], host)
+    assert n == x["written_back"]
+    assert np.array_equal(w_new, np.array(x["w_new"], np.float32))
+    assert np.array_equal(host, np.array(x["host_after"], np.float32))
 
 
 def _logical(host, ids, w_hot):
@@ -437,7 +452,8 @@ def _mix32_np(x):
 
 
 def test_eal_hash():
-    assert O.mix32(0) == 0 and O.mix32(1) == 0x514E28B7  # published values of the finalizer
+    pub = _gold("srrip_hand.json")["mix32"]
+    assert O.mix32(0) == pub["0"] and O.mix32(1) == pub["1"]  # published values of the finalizer
     xs = np.random.default_rng(3).integers(0, 1 << 32, size=2000, dtype=np.uint64)
     assert [O.mix32(int(v)) for v in xs] == _mix32_np(xs).tolist()
 
@@ -452,14 +468,17 @@ def test_eal_hash():
 # C, X2 takes D, X3 ages again (A B at 2, X1 X2 at 3) and takes X1, X4 takes X2:
 # A and B stay (LRU would have evicted them).
 def test_eal_hand_examples():
-    e = O.EAL(1, 2)
-    e.access([5, 7, 5, 9, 7, 11])
-    assert e.tag.tolist() == [11, 7] and e.rrpv.tolist() == [2, 3] and e.hot().tolist() == [7, 11]
-    e = O.EAL(1, 4)
-    e.access([1, 2, 3, 4, 1, 2, 11, 12, 13, 14])
-    assert e.tag.tolist() == [1, 2, 13, 14] and e.rrpv.tolist() == [2, 2, 2, 2]
-    e.access([0xFFFFFFFF] * 5)  # the id of a row out of range is not logged
-    assert e.tag.tolist() == [1, 2, 13, 14] and e.rrpv.tolist() == [2, 2, 2, 2]
+    x = _gold("srrip_hand.json")
+    t = x["two_ways"]
+    e = O.EAL(t["sets"], t["ways"])
+    e.access(t["stream"])
+    assert e.tag.tolist() == t["tag"] and e.rrpv.tolist() == t["rrpv"] and e.hot().tolist() == t["hot"]
+    t = x["scan"]
+    e = O.EAL(t["sets"], t["ways"])
+    e.access(t["stream"])
+    assert e.tag.tolist() == t["tag"] and e.rrpv.tolist() == t["rrpv"]
+    e.access([0xFFFFFFFF] * t["then_invalid"])  # the id of a row out of range is not logged
+    assert e.tag.tolist() == t["tag"] and e.rrpv.tolist() == t["rrpv"]
 
 
 @pytest.mark.parametrize("seed", range(8))
