@@ -22,7 +22,9 @@
 // HL_DEVERR_STALL and returns).  A handover costs two small kernels (~3 us
 // each) instead of an event dependency between streams (~17 us measured).
 // Handovers that meet at one point of a stream share one launch (pl_hand): the
-// fetch's two waits, and a plan's grouping signal with the next plan's waits.
+// fetch's two waits, the fetch's end signal with the next plan's fetch waits
+// (the copies follow one another with one launch between them), and a plan's
+// grouping signal with the next plan's waits.
 // On the main stream of a planned step they ride on the kernels themselves
 // (hl_hook): the forward signals the previous step's end as it starts and
 // waits for the grouping as it ends, the reduction waits for the fetch, and
@@ -137,6 +139,8 @@ struct hl_pipeline {
   uint32_t np_last;       // last step that ran its own dispatch and cold plan (cold-gather hash table)
   uint32_t np_synced;     // the np_last a plan has waited for with a launch of its own
   uint32_t look_seen;     // the plan whose "cold list" the last step's last kernel waited for (0: none)
+  uint32_t fetch_seen;    // the plan whose fetch waits the fetch stream's last signal launch also took
+  uint32_t fetch_last;    // (0: none), and the step whose end it awaited for that plan's staging rows
 };
 
 static hl_status pl_flush(hl_pipeline* p);
@@ -515,9 +519,28 @@ extern "C" hl_status hl_pipeline_step(hl_pipeline* p, const hl_step_io* io, hl_s
     // (a pending end signal of the previous step is given by this step's
     // first main-stream launch, enqueued below)
     const uint32_t last = pl_stg_last(p, io->staging);
-    HL_TRY(pl_hw(p, f, -1, 0, e->cold_flag, e->seq, last ? PF_DONE : -1, last));
+    if (p->fetch_seen != e->seq || p->fetch_last != last)
+      HL_TRY(pl_hw(p, f, -1, 0, e->cold_flag, e->seq, last ? PF_DONE : -1, last));
+    p->fetch_seen = 0;
     HL_TRY(hl_cold_fetch(h, io->cold_ids, io->n_cold, cap, io->w_host, io->staging, F));
-    HL_TRY(pl_sig(p, f, PF_FETCH, q));
+    // the signal launch also takes the next pending plan's fetch waits (its
+    // cold list, and the end of the last step that used its staging rows), so
+    // that plan's copy follows this one with no launch between them.  Only for
+    // a plan that waits for no step from this one on and has staging rows of its
+    // own: every signal it awaits is then enqueued by the end of this call.
+    pl_plan* fx = nullptr;
+    if (p->use_flags && !io->write_back)
+      for (pl_plan& c : p->plans)
+        if (c.pending && (!fx || pl_before(c.seq, fx->seq))) fx = &c;
+    if (fx && ((fx->need && !pl_before(fx->need, q)) || fx->io.staging == io->staging)) fx = nullptr;
+    if (fx) {
+      const uint32_t lx = pl_stg_last(p, fx->io.staging);
+      HL_TRY(pl_hw(p, f, PF_FETCH, q, fx->cold_flag, fx->seq, lx ? PF_DONE : -1, lx));
+      p->fetch_seen = fx->seq;
+      p->fetch_last = lx;
+    } else {
+      HL_TRY(pl_sig(p, f, PF_FETCH, q));
+    }
     // main: the previous step's end signal and the wait for the plan (in the
     // previous step's last kernel when it waited for this plan already, else
     // one launch); the grouping is awaited after the hot forward (the plan
@@ -574,6 +597,7 @@ extern "C" hl_status hl_pipeline_step(hl_pipeline* p, const hl_step_io* io, hl_s
                         io->n_cold, io->workspace, io->ws_bytes, M));
     HL_TRY(pl_sig(p, m, PF_PLAN, q));
     // the working parameters of the non-popular mu-batch over the host link
+    p->fetch_seen = 0;
     HL_TRY(pl_wt(p, f, PF_PLAN, q));
     HL_TRY(hl_cold_fetch(h, io->cold_ids, io->n_cold, cap, io->w_host, io->staging, F));
     HL_TRY(pl_sig(p, f, PF_FETCH, q));
