@@ -321,12 +321,15 @@ def main():
     bwd_b = 4 * avg["L"] + 4 * (avg["n_bags"] + 1) + avg["n_bags"] * avg["O"] + 2 * avg["U"] * avg["R"]
     fb_frac = (fwd_b + bwd_b) / (t_fb / 1e3) / HBM_PEAK
 
-    # roofline of the dominant kernel of the forward and backward (the HBM-bound
-    # part of the path) by time per step.  The host-link copy is reported against
-    # the link; the plan stream's kernels run a mini-batch ahead, and the dispatch
-    # kernel's blocks start by waiting for the steps that last used its buffers,
-    # so its launch duration is not its own work.
-    dom = next(n for n in kernels if n in fb_kernels)
+    # roofline of the dominant HBM-bound kernel by time per step: the forward's
+    # hot half and the backward's reduction move the path's bytes; the host-link
+    # copy is reported against the link, and the grouping's sort passes, the
+    # cold-row kernels and the dispatch are latency-bound at these sizes (the
+    # dispatch kernel's blocks also start by waiting for the steps that last
+    # used its buffers).  The dominant kernel overall is named beside it.
+    hbm_kernels = ("eb_fwd_hot", "bw_reduce1", "bw_reduce2")
+    dom = next(n for n in kernels if n in hbm_kernels)
+    dom_all = next(n for n in kernels if n not in ("cg_fetch", "cg_scatter"))
     if kernel_bytes(dom, avg) is None:
         raise SystemExit(f"no byte model for the dominant kernel {dom}")
     kd = kernels[dom]
@@ -337,7 +340,9 @@ def main():
     roof = {"kernel": dom, "bound": "hbm", "achieved": ach / 1e9, "peak": HBM_PEAK / 1e9, "unit": "GB/s",
             "frac": ach / HBM_PEAK, "traffic": None if tb is None else tb / (kd["avg_us"] * 1e-6) / 1e9,
             "traffic_bytes_per_launch": tb, "avg_us": kd["avg_us"],
-            "algorithmic_bytes_per_launch": kernel_bytes(dom, avg)}
+            "algorithmic_bytes_per_launch": kernel_bytes(dom, avg),
+            "dominant_kernel_overall": {"kernel": dom_all, "ms_per_step": kernels[dom_all]["ms_per_step"],
+                                        "bound": "hbm" if dom_all in hbm_kernels else "latency"}}
     link = None
     if "cg_fetch" in kernels:
         gb = avg["n_cold"] * avg["R"]
@@ -347,22 +352,42 @@ def main():
     # the same batches through the library's calls in order on one stream, each
     # stage alone on the whole GPU (events between the stages): the forward and
     # backward without the host-link copy and the plans running beside them
+    # Events only at the edges of the spans timed (a pair of events adds a few
+    # microseconds of its own: the stages' pass below has an empty span), then
+    # one pass with events between every stage.
     from paper_2204_05436_amd.runner import STAGES
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(len(STAGES) + 1)] for _ in range(K)]
-    with torch.cuda.stream(side):
-        for i in range(K):
-            hp.step(dmeas[i % len(dmeas)], events=ev[i], mode="sequential", split_fwd=False)
-    torch.cuda.synchronize()
-    err = hp.device_error()
-    if err:
-        raise SystemExit(f"device error word {err:#x} in the sequential steps")
+    ix = {s: j for j, s in enumerate(STAGES)}
+    edges = (ix["classify"], ix["remap"], ix["fwd_pop"], len(STAGES))  # classify+partition, fwd+bwd
+
+    class _NoEvent:
+        def record(self, *a):
+            pass
+
+    def seq_pass(marks):
+        ev = [[torch.cuda.Event(enable_timing=True) if j in marks else _NoEvent() for j in range(len(STAGES) + 1)]
+              for _ in range(K)]
+        with torch.cuda.stream(side):
+            for i in range(K):
+                hp.step(dmeas[i % len(dmeas)], events=ev[i], mode="sequential", split_fwd=False)
+        torch.cuda.synchronize()
+        err = hp.device_error()
+        if err:
+            raise SystemExit(f"device error word {err:#x} in the sequential steps")
+        return ev
+
+    ev = seq_pass(edges)
+    t_cp = sum(e[edges[0]].elapsed_time(e[edges[1]]) for e in ev) / K
+    t_fb1 = sum(e[edges[2]].elapsed_time(e[edges[3]]) for e in ev) / K
+    ev = seq_pass(range(len(STAGES) + 1))
     st = {s: sum(ev[i][j].elapsed_time(ev[i][j + 1]) for i in range(K)) / K for j, s in enumerate(STAGES)}
-    t_fb1 = st["fwd_pop"] + st["fwd_nonpop"] + st["bwd"]
-    alone = {"stage_ms": st, "fwd_bwd_us": t_fb1 * 1e3, "fwd_bwd_lookups_per_s": avg["L"] / (t_fb1 / 1e3),
+    alone = {"fwd_bwd_us": t_fb1 * 1e3, "fwd_bwd_lookups_per_s": avg["L"] / (t_fb1 / 1e3),
              "fwd_bwd_hbm_frac": (fwd_b + bwd_b) / (t_fb1 / 1e3) / HBM_PEAK,
-             "classify_samples_per_s": avg["B"] / ((st["classify"] + st["partition"]) / 1e3)}
-    log(f"[bench] stages alone: " + ", ".join(f"{s} {v * 1e3:.1f}us" for s, v in st.items()) +
-        f"; fwd+bwd {alone['fwd_bwd_hbm_frac']:.3f} of the HBM peak")
+             "classify_partition_us": t_cp * 1e3, "classify_samples_per_s": avg["B"] / (t_cp / 1e3),
+             "stage_ms_events_between_every_stage": st,
+             "empty_span_us": st["fwd_nonpop"] * 1e3}
+    log(f"[bench] alone on the GPU: fwd+bwd {t_fb1 * 1e3:.1f} us ({alone['fwd_bwd_hbm_frac']:.3f} of the HBM "
+        f"peak), classify+partition {t_cp * 1e3:.1f} us; stages " +
+        ", ".join(f"{s} {v * 1e3:.1f}us" for s, v in st.items()))
 
     breakdown = None
     if args.breakdown:
