@@ -46,7 +46,7 @@ typedef enum {
   HL_ERR_OUT_OF_RANGE = 2, /* a value outside its table or capacity (host-checked) */
   HL_ERR_CAPACITY = 3,     /* a buffer or workspace is too small */
   HL_ERR_HIP = 4,          /* the HIP runtime reported an error */
-  HL_ERR_UNSUPPORTED = 5,  /* shape or dtype this build does not handle */
+  HL_ERR_UNSUPPORTED = 5,  /* shape or dtype the library does not handle */
   HL_ERR_DEVICE = 6        /* hl_last_device_error: the device error word is set */
 } hl_status;
 

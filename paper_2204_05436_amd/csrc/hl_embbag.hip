@@ -102,6 +102,22 @@ __device__ __forceinline__ void ld_f32(const float* p, float* v) { RowIO<VEC, fa
 template <int VEC>
 __device__ __forceinline__ void st_f32(float* p, const float* v) { RowIO<VEC, false>::store(p, v); }
 
+// Pooled outputs are written once per launch and not read again by it: the
+// non-temporal hint marks their lines for early eviction, so they do not push
+// the hot rows out of the caches (the forward's hot half measured ~20% faster
+// alone on the GPU; the same hint on the backward's gradient-row loads was
+// slower, and they keep plain loads).
+typedef float hl_f4 __attribute__((ext_vector_type(4)));
+template <int VEC>
+__device__ __forceinline__ void st_f32_nt(float* p, const float* v) {
+  if constexpr (VEC == 4) {
+    const hl_f4 x = {v[0], v[1], v[2], v[3]};
+    __builtin_nontemporal_store(x, reinterpret_cast<hl_f4*>(p));
+  } else {
+    RowIO<VEC, false>::store(p, v);
+  }
+}
+
 struct eb_geom {
   int32_t D, vpr, G, NG, cchunks, VEC;
 };
@@ -277,7 +293,7 @@ eb_fwd(const void* w_hot_, const void* stg_, int32_t stg_rows, uint32_t n_hot, u
             for (int e = 0; e < VEC; ++e) o[e] = 0.f;
 #pragma unroll
           for (int e = 0; e < VEC; ++e) o[e] += v[u][e];
-          st_f32<VEC>(out + bag[u] * g.D + col, o);
+          st_f32_nt<VEC>(out + bag[u] * g.D + col, o);
         }
       continue;
     }
@@ -299,7 +315,7 @@ eb_fwd(const void* w_hot_, const void* stg_, int32_t stg_rows, uint32_t n_hot, u
         eb_pass<VEC, BF, false>(acc, w_hot, stg, stg_rows, n_hot, k_cap, codes, lo[u], hi[u], g, col, cact, gl, err);
       if (PART != 1)
         eb_pass<VEC, BF, true>(acc, w_hot, stg, stg_rows, n_hot, k_cap, codes, lo[u], hi[u], g, col, cact, gl, err);
-      if (cact) st_f32<VEC>(out + bag[u] * g.D + col, acc);
+      if (cact) st_f32_nt<VEC>(out + bag[u] * g.D + col, acc);
     }
   }
   hl_hook_tail(hk);
