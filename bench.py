@@ -608,8 +608,11 @@ def eal_study(out):
 
 
 def cpu_baseline(w, rows, prof, meas, meas_idx, table, k_cap, budget_s):
-    """The oracle (single-threaded C, fp64) on the same batches: learning phase once
-    (untimed), then the per-batch steps timed batch by batch until the budget is spent."""
+    """The oracle (single-threaded C, fp64) on the same batches, pinned to one
+    host core (the calling thread's affinity, restored after): learning phase
+    once (untimed), then the per-batch steps timed batch by batch until the
+    budget is spent, with the time of each stage beside the total.  The times
+    include the binding's numpy marshalling around each oracle call."""
     import oracle as O
     from paper_2204_05436_amd import workload as W
 
@@ -620,34 +623,47 @@ def cpu_baseline(w, rows, prof, meas, meas_idx, table, k_cap, budget_s):
         O.count(n_rows, [g], counts)
     hot = O.topk(counts, k_cap)
     w_hot = O.gather(table.array, hot)
-    done, L, B, t_all, t_cls = 0, 0, 0, 0.0, 0.0
-    log("[bench] cpu baseline (oracle) ...")
-    for i, mb in zip(meas_idx, meas):
-        dY = W.make_dy(w, i, mb.n_bags)
-        bps = mb.bags_per_sample
-        t0 = time.perf_counter()
-        g, _ = O.gids(rows, mb.rows, mb.bag_ptr)
-        flags = O.classify(hot, g, mb.bag_ptr, mb.n_samples, bps)
-        pop, nonpop = O.partition(flags)
-        t1 = time.perf_counter()
-        codes = O.remap(hot, g)
-        cold, codes = O.cold_plan(g, codes, mb.bag_ptr, nonpop, len(nonpop), bps, k_cap)
-        stg = O.gather(table.array, cold)
-        O.embbag_fwd(w.dtype, w_hot, k_cap, stg, codes, mb.bag_ptr, pop, len(pop), bps, mb.n_bags)
-        O.embbag_fwd(w.dtype, w_hot, k_cap, stg, codes, mb.bag_ptr, nonpop, len(nonpop), bps, mb.n_bags)
-        O.embbag_bwd_sgd(w.dtype, w_hot, k_cap, stg, codes, mb.bag_ptr, None, mb.n_samples, bps, dY, w.lr)
-        t2 = time.perf_counter()
-        t_all += t2 - t0
-        t_cls += t1 - t0
-        L += mb.n_lookups
-        B += mb.n_samples
-        done += 1
-        if t_all >= budget_s:
-            break
+    done, L, B, t_all = 0, 0, 0, 0.0
+    stage = {"classify_partition": 0.0, "remap_coldplan_gather": 0.0, "fwd": 0.0, "bwd": 0.0}
+    aff = os.sched_getaffinity(0)
+    core = min(aff)
+    os.sched_setaffinity(0, {core})
+    log(f"[bench] cpu baseline (oracle) on core {core} ...")
+    try:
+        for i, mb in zip(meas_idx, meas):
+            dY = W.make_dy(w, i, mb.n_bags)
+            bps = mb.bags_per_sample
+            t0 = time.perf_counter()
+            g, _ = O.gids(rows, mb.rows, mb.bag_ptr)
+            flags = O.classify(hot, g, mb.bag_ptr, mb.n_samples, bps)
+            pop, nonpop = O.partition(flags)
+            t1 = time.perf_counter()
+            codes = O.remap(hot, g)
+            cold, codes = O.cold_plan(g, codes, mb.bag_ptr, nonpop, len(nonpop), bps, k_cap)
+            stg = O.gather(table.array, cold)
+            t2 = time.perf_counter()
+            O.embbag_fwd(w.dtype, w_hot, k_cap, stg, codes, mb.bag_ptr, pop, len(pop), bps, mb.n_bags)
+            O.embbag_fwd(w.dtype, w_hot, k_cap, stg, codes, mb.bag_ptr, nonpop, len(nonpop), bps, mb.n_bags)
+            t3 = time.perf_counter()
+            O.embbag_bwd_sgd(w.dtype, w_hot, k_cap, stg, codes, mb.bag_ptr, None, mb.n_samples, bps, dY, w.lr)
+            t4 = time.perf_counter()
+            t_all += t4 - t0
+            for k, dt in zip(stage, (t1 - t0, t2 - t1, t3 - t2, t4 - t3)):
+                stage[k] += dt
+            L += mb.n_lookups
+            B += mb.n_samples
+            done += 1
+            if t_all >= budget_s:
+                break
+    finally:
+        os.sched_setaffinity(0, aff)
     log(f"[bench] cpu baseline: {done} batches in {t_all:.1f}s")
     return {"value": L / t_all, "unit": "lookups/s", "cores": 1, "kind": "oracle",
-            "classify_samples_per_s": B / t_cls,
-            "sample": f"{done} measured batches of {w.name}, every per-batch step, single-threaded fp64 oracle",
+            "classify_samples_per_s": B / stage["classify_partition"],
+            "fwd_bwd_lookups_per_s": L / (stage["fwd"] + stage["bwd"]),
+            "stage_ms_per_batch": {k: 1e3 * v / done for k, v in stage.items()},
+            "sample": f"{done} measured batches of {w.name}, every per-batch step, single-threaded fp64 oracle "
+                      f"pinned to host core {core}",
             "host_cpu": _cpu_model(), "host_nproc": os.cpu_count()}
 
 

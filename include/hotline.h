@@ -195,7 +195,12 @@ hl_status hl_partition(hl_handle* h, const uint8_t* flags, int32_t n_samples, in
                        int32_t* nonpop_ids, int32_t* counts_dev, void* workspace, size_t ws_bytes,
                        hl_stream stream);
 
-/* codes[i] = hot slot of gids[i], or -1 when the row is not hot. */
+/* Address generation of the Data Dispatcher (Sec. V-A: each lookup is turned
+ * into the address of its row; Sec. IV: the hot rows live in GPU memory, the
+ * others in CPU memory): codes[i] = hot-cache slot of gids[i] (the rank of
+ * gids[i] among the ascending hot ids), or -1 when the row is not hot (its
+ * address is resolved by the cold gather).  gids and codes hold n entries
+ * (device); an id >= n_rows gives -1 and sets HL_DEVERR_OUT_OF_RANGE. */
 hl_status hl_remap(const hl_handle* h, const uint32_t* gids, int64_t n, int32_t* codes,
                    hl_stream stream);
 

@@ -4,8 +4,11 @@ torch tensors (their data_ptr is passed); streams are torch streams.  Raises
 ImportError when the HIP library has not been built: there is no fallback."""
 from __future__ import annotations
 
+import atexit
 import ctypes as C
+import itertools
 import os
+import sys
 
 import numpy as np
 
@@ -112,6 +115,41 @@ def lib():
     return _lib
 
 
+# Library objects still alive when the interpreter exits are destroyed here,
+# newest first, after the device has finished their work: the HIP runtime's
+# own teardown (and a profiler's, which runs before it) must not find
+# compute-unit-masked streams, events, pinned host memory or handles of this
+# library still registered with it.
+_live = {}
+_seq = itertools.count()
+
+
+def _track(key, destroy):
+    _live[key] = (next(_seq), destroy)
+
+
+def _untrack(key):
+    _live.pop(key, None)
+
+
+@atexit.register
+def _destroy_live():
+    if not _live:
+        return
+    torch = sys.modules.get("torch")
+    try:
+        if torch is not None and torch.cuda.is_initialized():
+            torch.cuda.synchronize()
+    except Exception:
+        pass
+    for key, (_, destroy) in sorted(_live.items(), key=lambda kv: -kv[1][0]):
+        try:
+            destroy()
+        except Exception:
+            pass
+    _live.clear()
+
+
 def _ck(fn, st):
     if st != 0:
         raise HotlineError(fn, st)
@@ -142,6 +180,7 @@ def _nbytes(t):
 class Handle:
     def __init__(self, ptr):
         self.ptr = ptr
+        _track(("handle", ptr), self.close)
 
     @property
     def n_rows(self):
@@ -157,6 +196,7 @@ class Handle:
 
     def close(self):
         if self.ptr:
+            _untrack(("handle", self.ptr))
             _ck("hl_destroy", lib().hl_destroy(self.ptr))
             self.ptr = None
 
@@ -237,9 +277,12 @@ class EAL:
         _ck("hl_eal_create", lib().hl_eal_create(h.ptr, int(n_sets), int(ways), int(max_lookups),
                                                  C.byref(self.ptr)))
         self.n_sets, self.ways = int(n_sets), int(ways)
+        self._key = ("eal", self.ptr.value)
+        _track(self._key, self.close)
 
     def close(self):
         if self.ptr:
+            _untrack(self._key)
             _ck("hl_eal_destroy", lib().hl_eal_destroy(self.ptr))
             self.ptr = P()
 
@@ -400,20 +443,24 @@ def hl_stream_create(first_cu, n_cu, complement=False):
     """Returns the raw stream handle (wrap it with torch.cuda.ExternalStream)."""
     s = P()
     _ck("hl_stream_create", lib().hl_stream_create(int(first_cu), int(n_cu), int(bool(complement)), C.byref(s)))
+    _track(("stream", s.value), lambda v=s.value: lib().hl_stream_destroy(v))
     return s.value
 
 
 def hl_stream_destroy(stream):
+    _untrack(("stream", stream))
     _ck("hl_stream_destroy", lib().hl_stream_destroy(stream))
 
 
 def hl_pipeline_create(h, fetch_cus, plan_cus=0):
     p = P()
     _ck("hl_pipeline_create", lib().hl_pipeline_create(h.ptr, int(fetch_cus), int(plan_cus), C.byref(p)))
+    _track(("pipeline", p.value), lambda v=p.value: lib().hl_pipeline_destroy(v))
     return p.value
 
 
 def hl_pipeline_destroy(p):
+    _untrack(("pipeline", p))
     _ck("hl_pipeline_destroy", lib().hl_pipeline_destroy(p))
 
 
@@ -460,6 +507,7 @@ class HostTable:
         self.host, self.dev = hl_host_alloc(self.nbytes)
         buf = (C.c_char * self.nbytes).from_address(self.host)
         self.array = np.frombuffer(buf, dtype=self.np_dtype).reshape(self.shape)
+        _track(("host", self.host), self.close)
 
     def torch_view(self):
         import torch
@@ -467,6 +515,7 @@ class HostTable:
 
     def close(self):
         if self.host:
+            _untrack(("host", self.host))
             self.array = None
             hl_host_free(self.host)
             self.host = None
