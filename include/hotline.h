@@ -327,6 +327,18 @@ hl_status hl_embbag_bwd_apply(hl_handle* h, void* w_hot, void* staging, int32_t 
                               const float* dY, float lr, void* workspace, size_t ws_bytes,
                               hl_stream stream);
 
+/* The grouping the last hl_embbag_bwd_plan left in `workspace` (with the same
+ * staging_rows, n_samples, bags_per_sample and n_lookups; else
+ * HL_ERR_INVALID_ARG), copied for inspection to keys_out and bags_out (device,
+ * n_lookups entries each): one (key, bag) pair per lookup in the order the
+ * reduction takes them, key = hot slot, or n_hot + staging row, or 0xFFFFFFFF
+ * for a lookup the plan skipped.  The pairs of one key are contiguous and in
+ * ascending lookup (CSR) order, hot keys come first, and the summation order of
+ * the update (Sec. IV-A, Eq. 5: one coalesced step) follows this order. */
+hl_status hl_embbag_bwd_grouping(hl_handle* h, int32_t staging_rows, int32_t n_samples, int32_t bags_per_sample,
+                                 int64_t n_lookups, const void* workspace, size_t ws_bytes, uint32_t* keys_out,
+                                 uint32_t* bags_out, hl_stream stream);
+
 /* hl_embbag_bwd_apply in halves, bit for bit the same updates: part 1 reduces
  * dY for every group, updates the hot rows and keeps the sums of the staging
  * rows below n_lookups in the workspace without reading those rows (so it can

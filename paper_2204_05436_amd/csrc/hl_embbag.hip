@@ -1312,3 +1312,27 @@ extern "C" hl_status hl_embbag_bwd_sgd(hl_handle* h, void* w_hot, void* staging,
   return hl_embbag_bwd_apply(h, w_hot, staging, stg_rows, n_samples, bps, n_lookups, dY, lr, workspace, ws_bytes,
                              stream);
 }
+
+// The grouping that the last hl_embbag_bwd_plan on this workspace left (for
+// inspection): the (key, bag) pairs in the order the reduction takes them.
+extern "C" hl_status hl_embbag_bwd_grouping(hl_handle* h, int32_t stg_rows, int32_t n_samples, int32_t bps,
+                                            int64_t n_lookups, const void* workspace, size_t ws_bytes,
+                                            uint32_t* keys_out, uint32_t* bags_out, hl_stream stream) {
+  if (!h || !workspace || n_samples < 0 || bps < 1 || n_lookups < 0 || stg_rows < 0) return HL_ERR_INVALID_ARG;
+  if (n_lookups > 0 && (!keys_out || !bags_out)) return HL_ERR_INVALID_ARG;
+  const int64_t n_bags = (int64_t)n_samples * bps;
+  hl_ws_rec* rec = hl_ws_find(h, workspace);
+  if (!rec || rec->n != n_lookups || rec->bags != n_bags || rec->stg != stg_rows) return HL_ERR_INVALID_ARG;
+  if (n_lookups == 0) return HL_OK;
+  if (ws_bytes < hl_bwd_ws_bytes(h, n_lookups, n_bags)) return HL_ERR_CAPACITY;
+  hl_carver c = hl_carver::after_header(const_cast<void*>(workspace), ws_bytes);
+  bw_ws ws;
+  bw_carve(c, ws, (uint32_t)n_lookups, n_bags, h->dim);
+  uint32_t *sk, *sv;
+  hl_sort_result(ws.sort, bw_key_bits(h, stg_rows), &sk, &sv);
+  hipStream_t s = (hipStream_t)stream;
+  if (hipMemcpyAsync(keys_out, sk, (size_t)n_lookups * 4, hipMemcpyDeviceToDevice, s) != hipSuccess ||
+      hipMemcpyAsync(bags_out, sv, (size_t)n_lookups * 4, hipMemcpyDeviceToDevice, s) != hipSuccess)
+    return HL_ERR_HIP;
+  return HL_OK;
+}

@@ -133,6 +133,19 @@ __device__ __forceinline__ uint32_t hl_fdiv(uint32_t n, uint32_t d, float inv, u
 
 __device__ __forceinline__ void hl_flag(uint32_t* err, uint32_t bit) { atomicOr(err, bit); }
 
+// The lanes of the wave whose `bits`-bit digit equals this lane's, among the
+// lanes where `valid` holds (0 on a lane where it does not): one ballot per
+// digit bit, each keeping the lanes that agree on that bit.
+__device__ __forceinline__ uint64_t hl_match_digit(uint32_t digit, int bits, bool valid) {
+  uint64_t m = __ballot(valid);
+  for (int b = 0; b < bits; ++b) {
+    const bool one = (digit >> b) & 1u;
+    const uint64_t ones = __ballot(one);
+    m &= one ? ones : ~ones;
+  }
+  return valid ? m : 0ull;
+}
+
 // ----------------------------------------------------------------------------- hot set probes
 // Membership: bit (g & 63) of word g >> 6.  Rank: rank[g >> 8] counts hot ids
 // below the 256-id block; the block's 4 words before g's word and the bits of

@@ -5,8 +5,9 @@
 // kernel counts every digit position in a single read of the keys (per-block
 // counts) and clears the first pass's status words.  Then one kernel per
 // digit: a block takes the next tile (dynamic tile ids, so every lower tile is
-// already running), ranks its items by digit with per-wave LDS counters (the
-// counters' totals are the tile's digit counts), publishes the counts, adds up
+// already running), ranks its items by digit with per-wave LDS counters that
+// the lanes of one digit advance together (their peer mask found by ballots;
+// the counters' totals are the tile's digit counts), publishes the counts, adds up
 // the counts of all earlier tiles (read together, 64 words in flight per
 // thread: at these sizes every tile runs at once, so one round of loads
 // replaces a chain of inclusive prefixes), adds each digit's global offset
@@ -195,18 +196,27 @@ srt_pass(const uint32_t* __restrict__ kin, const uint32_t* __restrict__ vin, uin
       pv[0][q] = in ? part[(size_t)q * NB + d0] : 0u;
     }
   }
-  // ranking: every item adds 1 to its digit's counter of the wave; the old
-  // value is its rank among the wave's earlier items of that digit.  One
-  // wave's LDS atomics are applied in instruction order, and the lanes of one
-  // instruction that hit the same counter in lane order (a property of the LDS
-  // unit, checked on this GPU over 49M random lane patterns with partial masks,
-  // none out of order), so ranks follow (item, lane) order: the sort is stable.
+  // ranking, stable by construction: for each item slot the lanes holding the
+  // same digit find one another with one ballot per digit bit (their peer
+  // mask); the lowest peer adds the group's size to the wave's counter of that
+  // digit (one atomic per distinct digit, so no two lanes of an instruction
+  // touch one counter) and the others take its old value by a lane shuffle;
+  // a lane's rank is that value plus its peers on lower lanes.  A wave's LDS
+  // instructions execute in issue order, so the counters advance in item
+  // order: ranks follow (item, lane) order, which is index order.
   uint32_t dg[HL_SORT_ITEMS], lr[HL_SORT_ITEMS];
+  const uint64_t lt = (1ull << lane) - 1ull;
 #pragma unroll
   for (int k = 0; k < HL_SORT_ITEMS; ++k) {
     const uint64_t idx = tb + (uint64_t)w * (HL_SORT_ITEMS * 64) + k * 64 + lane;
+    const bool valid = idx < n;
     dg[k] = (key[k] >> shift) & mask;
-    lr[k] = idx < n ? atomicAdd(&wcnt[w][dg[k]], 1u) : 0u;
+    const uint64_t peers = hl_match_digit(dg[k], b, valid);
+    const int leader = __ffsll((unsigned long long)peers) - 1;
+    uint32_t base = 0;
+    if (valid && lane == leader) base = atomicAdd(&wcnt[w][dg[k]], (uint32_t)__popcll(peers));
+    base = __shfl(base, leader < 0 ? 0 : leader);
+    lr[k] = valid ? base + (uint32_t)__popcll(peers & lt) : 0u;
   }
   uint32_t dtot[PER];
 #pragma unroll

@@ -81,6 +81,7 @@ _SIGS = {
     "hl_embbag_bwd_plan": (C.c_int, [P, I32, P, P, I32, I32, I64, P, P, I32, P, SZ, P]),
     "hl_embbag_bwd_apply": (C.c_int, [P, P, P, I32, I32, I32, I64, P, F32, P, SZ, P]),
     "hl_embbag_bwd_apply_part": (C.c_int, [P, P, P, I32, I32, I32, I64, P, F32, I32, P, SZ, P]),
+    "hl_embbag_bwd_grouping": (C.c_int, [P, I32, I32, I32, I64, P, SZ, P, P, P]),
     "hl_last_device_error": (C.c_int, [P, C.POINTER(U32)]),
     "hl_trace_enable": (C.c_int, [P, I32]),
     "hl_trace_count": (I32, [P]),
@@ -407,6 +408,13 @@ def hl_embbag_bwd_apply_part(h, w_hot, staging, staging_rows, n_samples, bags_pe
     _ck("hl_embbag_bwd_apply_part", lib().hl_embbag_bwd_apply_part(
         h.ptr, _p(w_hot), _p(staging), int(staging_rows), int(n_samples), int(bags_per_sample), int(n_lookups),
         _p(dY), float(lr), int(part), _p(ws), _nbytes(ws), _s(stream)))
+
+
+def hl_embbag_bwd_grouping(h, staging_rows, n_samples, bags_per_sample, n_lookups, ws, keys_out, bags_out,
+                           stream=None):
+    _ck("hl_embbag_bwd_grouping", lib().hl_embbag_bwd_grouping(
+        h.ptr, int(staging_rows), int(n_samples), int(bags_per_sample), int(n_lookups), _p(ws), _nbytes(ws),
+        _p(keys_out), _p(bags_out), _s(stream)))
 
 
 def hl_last_device_error(h):

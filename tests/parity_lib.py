@@ -54,6 +54,35 @@ def check_close(got, ref, scale, rtol, what):
                              f"got {got[tuple(i)]!r} ref {ref[tuple(i)]!r} tol {tol[tuple(i)]!r}")
 
 
+def check_grouping(keys, bags, codes, bag_of, n_hot, k_cap, what):
+    """The backward's grouping of one mini-batch (hl_embbag_bwd_grouping)
+    against the lookups' codes: the pairs of a key contiguous, its bags in
+    ascending lookup order (the stable order of numpy's argsort of the keys),
+    hot keys before the others.  Returns the number of repeated (key, bag)
+    pairs (a row twice in one bag) and how many of them are of staging rows."""
+    c = np.asarray(codes).astype(np.int64)
+    want_k = np.where((c >= 0) & (c < n_hot), c, np.where(c >= k_cap, n_hot + (c - k_cap), 0xFFFFFFFF))
+    want_k = want_k.astype(np.uint32)
+    order = np.argsort(want_k, kind="stable")
+    got_order = np.argsort(keys, kind="stable")
+    assert np.array_equal(keys[got_order], want_k[order]), f"{what}: keys differ as multisets"
+    assert np.array_equal(bags[got_order], bag_of[order]), f"{what}: a key's bags are not in lookup order"
+    runs = 1 + int(np.count_nonzero(keys[1:] != keys[:-1])) if keys.size else 0
+    assert runs == np.unique(keys).size, f"{what}: a key's pairs are not contiguous"
+    hot = keys < n_hot
+    assert not (hot[1:] & ~hot[:-1]).any(), f"{what}: a hot key after a non-hot one"
+    dup = (keys[1:] == keys[:-1]) & (bags[1:] == bags[:-1])
+    return int(dup.sum()), int((dup & ~hot[1:]).sum())
+
+
+def grouping_of(hp, B, bps, L):
+    """The grouping the last backward plan left in hp's workspace, as numpy."""
+    keys = torch.zeros(max(1, L), dtype=torch.int32, device=hp.device)
+    bags = torch.zeros(max(1, L), dtype=torch.int32, device=hp.device)
+    hl.hl_embbag_bwd_grouping(hp.h, hp.staging_cap, B, bps, L, hp.ws, keys, bags)
+    return keys[:L].cpu().numpy().view(np.uint32).copy(), bags[:L].cpu().numpy().view(np.uint32).copy()
+
+
 def _on_side(fn):
     """Run fn(stream) on a fresh side stream ordered after the current stream's
     work; the current stream then waits for it."""
@@ -92,6 +121,7 @@ def run_gpu_stages(hp: HotPath, prof, mb, dY, k=None, hot_ids=None, split=False)
     r["w_hot_pre"] = hp.w_hot[:n_hot].cpu().numpy().copy()
     b = to_device(mb, hp.device, dY)
     B, bps, L = b.n_samples, b.bps, b.n_lookups
+    r["bag_ptr"] = np.asarray(mb.bag_ptr)
     if split:  # the dispatch kernel, as the pipelined step calls it
         hl.hl_dispatch(h, b.rows, b.bag_ptr, B, bps, L, hp.gids, hp.codes, hp.flags, hp.pop, hp.nonpop, hp.counts,
                        hp.ws)
@@ -151,6 +181,8 @@ def run_gpu_stages(hp: HotPath, prof, mb, dY, k=None, hot_ids=None, split=False)
                              B, b.dY, hp.w.lr, hp.ws)
     r["w_hot_new"] = hp.w_hot[:n_hot].cpu().numpy().copy()
     r["staging_new"] = hp.staging[:min(n_cold, hp.staging_cap)].cpu().numpy().copy()
+    r["grouping"] = grouping_of(hp, B, bps, L) if b.dY is not None else None
+    r["n_hot"] = n_hot
     r["deverr"] = hp.device_error()
     return r
 
@@ -219,3 +251,7 @@ def compare(w, g, o, k_cap, check_counts=True):
     assert np.array_equal(g["w_hot_new"][untouched].view(np.uint8), g["w_hot_pre"][untouched].view(np.uint8)), \
         "untouched hot rows changed"
     assert g["deverr"] == 0, f"device error word {g['deverr']:#x}"
+    if g.get("grouping") is not None:
+        ptr = np.asarray(g["bag_ptr"], np.int64)
+        bag_of = np.repeat(np.arange(len(ptr) - 1, dtype=np.uint32), np.diff(ptr))
+        check_grouping(*g["grouping"], g["codes"], bag_of, g["n_hot"], k_cap, "grouping")
