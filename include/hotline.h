@@ -307,6 +307,25 @@ hl_status hl_embbag_bwd_sgd(hl_handle* h, void* w_hot, void* staging, int32_t st
                             const int32_t* n_sel_dev, int32_t n_sel_max, const float* dY, float lr,
                             void* workspace, size_t ws_bytes, hl_stream stream);
 
+/* hl_embbag_bwd_sgd for callers that cannot allocate device memory (code under
+ * graph capture, tight serving loops, harnesses that forbid allocation): the
+ * same arguments but the workspace, the same updates bit for bit (same
+ * kernels, same grouping).  The workspace is a file-scope device array of
+ * hl_noalloc_scratch_bytes() = 32 MiB in the library, one copy per GPU, held
+ * until the process ends (hl_create looks up its address on the handle's
+ * device and zero-fills it once).  The call allocates nothing.  Mini-batches
+ * whose plan needs more than the array (about 50 bytes per lookup at dim 64,
+ * 85 at dim 128: each of the benchmark's mini-batches fits) return HL_ERR_CAPACITY and enqueue nothing.  Every call
+ * on one GPU shares that GPU's array and leaves its last contents there: calls
+ * that overlap on one GPU (on concurrent streams or host threads) race and
+ * must not be issued. */
+size_t hl_noalloc_scratch_bytes(void);
+hl_status hl_embbag_bwd_sgd_noalloc(hl_handle* h, void* w_hot, void* staging, int32_t staging_rows,
+                                    const int32_t* codes, const int32_t* bag_ptr, int32_t n_samples,
+                                    int32_t bags_per_sample, int64_t n_lookups, const int32_t* sample_ids,
+                                    const int32_t* n_sel_dev, int32_t n_sel_max, const float* dY, float lr,
+                                    hl_stream stream);
+
 /* The two halves of hl_embbag_bwd_sgd.  hl_embbag_bwd_plan groups the
  * selected lookups by code (it reads codes and bag_ptr only, not the rows or
  * dY) and leaves the grouping in the workspace; hl_embbag_bwd_apply reduces dY

@@ -341,7 +341,8 @@ static uint32_t bw_tile_entries(int32_t D, int vec) {
   return (uint32_t)(RB_WAVES * g.NG * RB_E);
 }
 
-static void bw_carve(hl_carver& c, bw_ws& ws, uint32_t n_max, int64_t max_bags, int32_t D) {
+// compact: no staging-row sums (gc), for plans whose apply is whole (part 0)
+static void bw_carve(hl_carver& c, bw_ws& ws, uint32_t n_max, int64_t max_bags, int32_t D, bool compact = false) {
   hl_sort_ws_carve(c, ws.sort, n_max);
   ws.mask = c.take<uint8_t>((size_t)max_bags + 1);
   // the smallest tile (largest count) over the vector widths the call may pick
@@ -354,8 +355,8 @@ static void bw_carve(hl_carver& c, bw_ws& ws, uint32_t n_max, int64_t max_bags, 
   ws.tlast = c.take<float>((size_t)ws.tiles * D);
   ws.tflag = c.take<uint32_t>(ws.tiles);
   ws.tkey = c.take<uint32_t>(ws.tiles);
-  ws.gc_rows = n_max;
-  ws.gc = c.take<float>((size_t)n_max * D);
+  ws.gc_rows = compact ? 0 : n_max;
+  ws.gc = c.take<float>((size_t)ws.gc_rows * D);
   ws.bnd = c.take<uint32_t>(1);
 }
 
@@ -364,6 +365,17 @@ size_t hl_bwd_ws_bytes(const hl_handle* h, int64_t max_lookups, int64_t max_bags
   bw_ws ws;
   bw_carve(c, ws, (uint32_t)max_lookups, max_bags, h->dim);
   return c.off;
+}
+
+size_t hl_bwd_ws_bytes_compact(const hl_handle* h, int64_t max_lookups, int64_t max_bags) {
+  hl_carver c = hl_carver::after_header(nullptr, 0);
+  bw_ws ws;
+  bw_carve(c, ws, (uint32_t)max_lookups, max_bags, h->dim, true);
+  return c.off;
+}
+
+static size_t bw_bytes(const hl_handle* h, int64_t n, int64_t bags, bool compact) {
+  return compact ? hl_bwd_ws_bytes_compact(h, n, bags) : hl_bwd_ws_bytes(h, n, bags);
 }
 
 __global__ void bw_mask(uint8_t* mask, int32_t n_samples, const int32_t* __restrict__ ids, const int32_t* n_dev,
@@ -1094,23 +1106,25 @@ hl_status hl_embbag_bwd_plan_signal(hl_handle* h, int32_t stg_rows, int32_t* cod
                                     int32_t n_samples, int32_t bps, int64_t n_lookups, const int32_t* sample_ids,
                                     const int32_t* n_sel_dev, int32_t n_sel_max, void* workspace, size_t ws_bytes,
                                     hl_stream stream, uint32_t* sflag, uint32_t sval, bool* sent,
-                                    const hl_cg_fused* cf) {
+                                    const hl_cg_fused* cf, bool compact) {
   *sent = false;
+  if (compact && cf && cf->table) return HL_ERR_INVALID_ARG;  // the fused plan's state follows the full layout
   if (cf && cf->table && sample_ids) return HL_ERR_INVALID_ARG;  // the fused plan selects every sample
   hl_status st = check_common(h, codes, bag_ptr, n_samples, bps, n_lookups, sample_ids, n_sel_max, stg_rows);
   if (st != HL_OK) return st;
   if (!workspace) return HL_ERR_INVALID_ARG;
   const int64_t n_bags = (int64_t)n_samples * bps;
-  if (ws_bytes < hl_bwd_ws_bytes(h, n_lookups, n_bags)) return HL_ERR_CAPACITY;
+  if (ws_bytes < bw_bytes(h, n_lookups, n_bags, compact)) return HL_ERR_CAPACITY;
   hl_ws_note(h, workspace, HL_WSK_OTHER);
   if (n_samples == 0 || n_lookups == 0 || n_sel_max == 0) {
     hl_ws_note(h, workspace, HL_WSK_BWD_PLAN, 0, n_bags, stg_rows);
+    hl_ws_find(h, workspace)->compact = compact;
     return HL_OK;
   }
   hipStream_t s = (hipStream_t)stream;
   hl_carver c = hl_carver::after_header(workspace, ws_bytes);
   bw_ws ws;
-  bw_carve(c, ws, (uint32_t)n_lookups, n_bags, h->dim);
+  bw_carve(c, ws, (uint32_t)n_lookups, n_bags, h->dim, compact);
   const uint8_t* mask = nullptr;
   if (sample_ids) {
     uint32_t gb = hl_div_up(n_samples, 256);
@@ -1145,6 +1159,7 @@ hl_status hl_embbag_bwd_plan_signal(hl_handle* h, int32_t stg_rows, int32_t* cod
   }
   if (st != HL_OK) return st;
   hl_ws_note(h, workspace, HL_WSK_BWD_PLAN, n_lookups, n_bags, stg_rows);
+  hl_ws_find(h, workspace)->compact = compact;
   return HL_OK;
 }
 
@@ -1169,16 +1184,17 @@ hl_status hl_embbag_bwd_apply_any(hl_handle* h, void* w_hot, void* staging, int3
   if (!rec || rec->n != n_lookups || rec->bags != n_bags || rec->stg != stg_rows)
     return HL_ERR_INVALID_ARG;  // no matching plan is held by this workspace
   if (part == 2 && rec->part1 != 1) return HL_ERR_INVALID_ARG;  // the first half has not run on this plan
+  if (part != 0 && rec->compact) return HL_ERR_INVALID_ARG;      // no room for the staging-row sums
   if (n_lookups == 0 || n_samples == 0) {
     if (part == 1 || part == 3) rec->part1 = part == 1 ? 1 : 3;
     return HL_OK;
   }
   if ((part != 2 && (!dY || (h->n_hot && !w_hot))) || (stg_rows && !staging)) return HL_ERR_INVALID_ARG;
-  if (ws_bytes < hl_bwd_ws_bytes(h, n_lookups, n_bags)) return HL_ERR_CAPACITY;
+  if (ws_bytes < bw_bytes(h, n_lookups, n_bags, rec->compact)) return HL_ERR_CAPACITY;
   hipStream_t s = (hipStream_t)stream;
   hl_carver c = hl_carver::after_header(workspace, ws_bytes);
   bw_ws ws;
-  bw_carve(c, ws, (uint32_t)n_lookups, n_bags, h->dim);
+  bw_carve(c, ws, (uint32_t)n_lookups, n_bags, h->dim, rec->compact);
   uint32_t *sk, *sv;
   hl_sort_result(ws.sort, bw_key_bits(h, stg_rows), &sk, &sv);
   const uint32_t n = (uint32_t)n_lookups;
@@ -1213,10 +1229,10 @@ hl_status hl_embbag_fwd_cold_sorted(hl_handle* h, const void* staging, int32_t s
   if (!rec || rec->n != n_lookups || rec->bags != n_bags || rec->stg != stg_rows || !rec->part1)
     return HL_ERR_INVALID_ARG;  // the grouping and the first apply half must be in this workspace
   if (n_lookups == 0 || n_samples == 0) return HL_OK;
-  if (ws_bytes < hl_bwd_ws_bytes(h, n_lookups, n_bags)) return HL_ERR_CAPACITY;
+  if (ws_bytes < bw_bytes(h, n_lookups, n_bags, rec->compact)) return HL_ERR_CAPACITY;
   hl_carver c = hl_carver::after_header(workspace, ws_bytes);
   bw_ws ws;
-  bw_carve(c, ws, (uint32_t)n_lookups, n_bags, h->dim);
+  bw_carve(c, ws, (uint32_t)n_lookups, n_bags, h->dim, rec->compact);
   uint32_t *sk, *sv;
   hl_sort_result(ws.sort, bw_key_bits(h, stg_rows), &sk, &sv);
   const size_t es = h->dtype == HL_F32 ? 4 : 2;
@@ -1253,10 +1269,10 @@ hl_status hl_embbag_finish_cold(hl_handle* h, void* w_hot, void* staging, int32_
     return HL_ERR_INVALID_ARG;  // the grouping and apply part 3 must be in this workspace
   rec->part1 = 0;  // the plan is used up: no part 2 or second finish on it
   if (n_lookups == 0 || n_samples == 0) return HL_OK;
-  if (ws_bytes < hl_bwd_ws_bytes(h, n_lookups, n_bags)) return HL_ERR_CAPACITY;
+  if (ws_bytes < bw_bytes(h, n_lookups, n_bags, rec->compact)) return HL_ERR_CAPACITY;
   hl_carver c = hl_carver::after_header(workspace, ws_bytes);
   bw_ws ws;
-  bw_carve(c, ws, (uint32_t)n_lookups, n_bags, h->dim);
+  bw_carve(c, ws, (uint32_t)n_lookups, n_bags, h->dim, rec->compact);
   uint32_t *sk, *sv;
   hl_sort_result(ws.sort, bw_key_bits(h, stg_rows), &sk, &sv);
   // the first half's vector width (its tile sums' layout); out and the rows must allow it
@@ -1324,10 +1340,10 @@ extern "C" hl_status hl_embbag_bwd_grouping(hl_handle* h, int32_t stg_rows, int3
   hl_ws_rec* rec = hl_ws_find(h, workspace);
   if (!rec || rec->n != n_lookups || rec->bags != n_bags || rec->stg != stg_rows) return HL_ERR_INVALID_ARG;
   if (n_lookups == 0) return HL_OK;
-  if (ws_bytes < hl_bwd_ws_bytes(h, n_lookups, n_bags)) return HL_ERR_CAPACITY;
+  if (ws_bytes < bw_bytes(h, n_lookups, n_bags, rec->compact)) return HL_ERR_CAPACITY;
   hl_carver c = hl_carver::after_header(const_cast<void*>(workspace), ws_bytes);
   bw_ws ws;
-  bw_carve(c, ws, (uint32_t)n_lookups, n_bags, h->dim);
+  bw_carve(c, ws, (uint32_t)n_lookups, n_bags, h->dim, rec->compact);
   uint32_t *sk, *sv;
   hl_sort_result(ws.sort, bw_key_bits(h, stg_rows), &sk, &sv);
   hipStream_t s = (hipStream_t)stream;

@@ -142,6 +142,8 @@ extern "C" hl_status hl_create(hl_handle** out, int32_t n_tables, const uint32_t
   h->trace = new hl_trace();
   hl_status st = HL_OK;
   if (hipGetDevice(&h->device) != hipSuccess) st = HL_ERR_HIP;
+  // the allocation-free backward's static workspace on this device
+  if (st == HL_OK) st = hl_scratch_setup(h->device);
   auto dm = [&](void** p, size_t bytes) {
     if (st == HL_OK && hipMalloc(p, bytes) != hipSuccess) st = HL_ERR_HIP;
   };

@@ -36,6 +36,7 @@ struct hl_ws_rec {
   int32_t stg;         // its staging rows
   int part1;           // the first half of the apply ran on it (3: without its spanning segments)
   int vec;             // the row vector width that half used (its tile layout depends on it)
+  int compact;         // the plan used the layout without the staging-row sums (whole applies only)
 };
 struct hl_handle {
   int device;
@@ -240,6 +241,13 @@ struct hl_cg_fused {
 };
 // workspace bytes of the backward's plan and apply
 size_t hl_bwd_ws_bytes(const hl_handle* h, int64_t max_lookups, int64_t max_bags);
+// the same without the staging-row sums that the applies in halves keep
+// (enough for a plan followed by a whole apply)
+size_t hl_bwd_ws_bytes_compact(const hl_handle* h, int64_t max_lookups, int64_t max_bags);
+// the allocation-free backward's static workspace: its device address on
+// `device` is looked up (and the array zero-filled) once, with that device
+// current; hl_create does it for the handle's device
+hl_status hl_scratch_setup(int device);
 // workspace bytes of the fused plan (hl_workspace_bytes covers them)
 size_t hl_plan_ws_bytes(const hl_handle* h, int64_t max_lookups, int64_t max_bags, int32_t max_samples);
 // carves the fused plan's cold state; HL_ERR_CAPACITY if the workspace or the
@@ -289,7 +297,7 @@ hl_status hl_embbag_bwd_plan_signal(hl_handle* h, int32_t stg_rows, int32_t* cod
                                     int32_t n_samples, int32_t bps, int64_t n_lookups, const int32_t* sample_ids,
                                     const int32_t* n_sel_dev, int32_t n_sel_max, void* workspace, size_t ws_bytes,
                                     hl_stream stream, uint32_t* sflag, uint32_t sv, bool* sent,
-                                    const hl_cg_fused* cf);
+                                    const hl_cg_fused* cf, bool compact = false);
 
 // ----------------------------------------------------------------------------- sort
 // Stable LSD radix sort of (key, value) uint32 pairs with digits of up to 11

@@ -82,6 +82,8 @@ _SIGS = {
     "hl_embbag_bwd_apply": (C.c_int, [P, P, P, I32, I32, I32, I64, P, F32, P, SZ, P]),
     "hl_embbag_bwd_apply_part": (C.c_int, [P, P, P, I32, I32, I32, I64, P, F32, I32, P, SZ, P]),
     "hl_embbag_bwd_grouping": (C.c_int, [P, I32, I32, I32, I64, P, SZ, P, P, P]),
+    "hl_noalloc_scratch_bytes": (SZ, []),
+    "hl_embbag_bwd_sgd_noalloc": (C.c_int, [P, P, P, I32, P, P, I32, I32, I64, P, P, I32, P, F32, P]),
     "hl_last_device_error": (C.c_int, [P, C.POINTER(U32)]),
     "hl_trace_enable": (C.c_int, [P, I32]),
     "hl_trace_count": (I32, [P]),
@@ -387,6 +389,18 @@ def hl_embbag_bwd_sgd(h, w_hot, staging, staging_rows, codes, bag_ptr, n_samples
         h.ptr, _p(w_hot), _p(staging), int(staging_rows), _p(codes), _p(bag_ptr), int(n_samples),
         int(bags_per_sample), int(n_lookups), _p(sample_ids), _p(n_sel_dev), int(n_sel_max), _p(dY), float(lr),
         _p(ws), _nbytes(ws), _s(stream)))
+
+
+def hl_noalloc_scratch_bytes():
+    return int(lib().hl_noalloc_scratch_bytes())
+
+
+def hl_embbag_bwd_sgd_noalloc(h, w_hot, staging, staging_rows, codes, bag_ptr, n_samples, bags_per_sample, n_lookups,
+                              sample_ids, n_sel_dev, n_sel_max, dY, lr, stream=None):
+    _ck("hl_embbag_bwd_sgd_noalloc", lib().hl_embbag_bwd_sgd_noalloc(
+        h.ptr, _p(w_hot), _p(staging), int(staging_rows), _p(codes), _p(bag_ptr), int(n_samples),
+        int(bags_per_sample), int(n_lookups), _p(sample_ids), _p(n_sel_dev), int(n_sel_max), _p(dY), float(lr),
+        _s(stream)))
 
 
 def hl_embbag_bwd_plan(h, staging_rows, codes, bag_ptr, n_samples, bags_per_sample, n_lookups, sample_ids, n_sel_dev,
