@@ -298,9 +298,14 @@ hl_status hl_embbag_fwd_part(const hl_handle* h, const void* w_hot, const void* 
  * the selected bags' lookups, G_c = sum of dY[bag(i)] over its lookups and
  * row(c) <- round_storage(row(c) - lr * G_c), round to nearest even.  Each
  * row is written once; rows no lookup names are untouched.  Deterministic:
- * the summation order depends only on the inputs.  dY: [n_samples *
- * bags_per_sample, dim] fp32.  Invalid codes set HL_DEVERR_BAD_CODE and are
- * skipped. */
+ * the summation order depends only on the inputs (ascending lookup order).
+ * dY: [n_samples * bags_per_sample, dim] fp32.  Invalid codes set
+ * HL_DEVERR_BAD_CODE and are skipped.  A mini-batch with as many lookups as
+ * bags is taken to hold one lookup per bag (bag_ptr[j] = j, the one-hot
+ * layout, grouped table by table): another layout with that count sets
+ * HL_DEVERR_SHAPE; in that layout a hot code that names a row of another
+ * table than its bag's (hl_remap's codes never do) sets HL_DEVERR_BAD_CODE
+ * and is skipped. */
 hl_status hl_embbag_bwd_sgd(hl_handle* h, void* w_hot, void* staging, int32_t staging_rows,
                             const int32_t* codes, const int32_t* bag_ptr, int32_t n_samples,
                             int32_t bags_per_sample, int64_t n_lookups, const int32_t* sample_ids,
@@ -368,6 +373,13 @@ hl_status hl_embbag_bwd_apply_part(hl_handle* h, void* w_hot, void* staging, int
                                    int32_t n_samples, int32_t bags_per_sample, int64_t n_lookups,
                                    const float* dY, float lr, int32_t part, void* workspace,
                                    size_t ws_bytes, hl_stream stream);
+
+/* For tests of the sorts' fallback: the backward's grouping ranks the items
+ * of each radix pass by equal keys, checks the pass kept the order of equal
+ * digits and redoes it with ranks that are stable by construction (ballot
+ * peer masks) if not; on != 0 makes every pass take the second form directly.
+ * The grouping is the same either way. */
+hl_status hl_debug_ballot_ranks(hl_handle* h, int32_t on);
 
 /* ----------------------------------------------------------------- errors --
  * Waits for the device, returns the error word (HL_DEVERR_* bits) in *err_out

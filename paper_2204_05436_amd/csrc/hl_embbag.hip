@@ -19,7 +19,6 @@
 
 #include "hl_internal.h"
 
-#define EB_SENT 0xFFFFFFFFu
 #ifndef RB_E
 #define RB_E 8      // sorted entries per row group of the reduction
 #endif
@@ -333,6 +332,7 @@ struct bw_ws {
   uint32_t* tkey;    // [tiles]
   float* gc;         // [n_max][D] gradient sums of staging rows, kept between the two halves of the apply
   uint32_t* bnd;     // [1] first sorted position whose key is not a hot slot (set by the first half)
+  uint32_t* gsmall;  // [HL_GROUP_SMALL] the grouping by table's per-chunk counts and per-table ranges
   uint32_t tiles, gc_rows;
 };
 
@@ -358,6 +358,7 @@ static void bw_carve(hl_carver& c, bw_ws& ws, uint32_t n_max, int64_t max_bags, 
   ws.gc_rows = compact ? 0 : n_max;
   ws.gc = c.take<float>((size_t)ws.gc_rows * D);
   ws.bnd = c.take<uint32_t>(1);
+  ws.gsmall = c.take<uint32_t>(HL_GROUP_SMALL);
 }
 
 size_t hl_bwd_ws_bytes(const hl_handle* h, int64_t max_lookups, int64_t max_bags) {
@@ -395,11 +396,6 @@ __global__ void bw_mask(uint8_t* mask, int32_t n_samples, const int32_t* __restr
 // unselected samples and invalid codes get the sentinel key (sorted last,
 // ignored), and so do positions outside [bag_ptr[0], bag_ptr[n_bags]) (only if
 // bag_ptr disagrees with n_lookups; bag_ptr is non-decreasing).
-__device__ __forceinline__ uint32_t bw_key(uint32_t c, uint32_t n_hot, uint32_t k_cap, int32_t stg_rows) {
-  if (c < n_hot) return c;
-  if (c >= k_cap && c - k_cap < (uint32_t)stg_rows) return n_hot + (c - k_cap);
-  return EB_SENT;
-}
 
 // the lookup positions no bag covers: [0, bag_ptr[0]) and [bag_ptr[n_bags], n)
 __device__ __forceinline__ void bw_uncovered(const int32_t* bag_ptr, int64_t n_bags, int64_t n_lookups,
@@ -408,14 +404,6 @@ __device__ __forceinline__ void bw_uncovered(const int32_t* bag_ptr, int64_t n_b
   *covered = max(min((int64_t)max(bag_ptr[n_bags], 0), n_lookups), *first);
 }
 
-// The fused plan: a cold lookup's code (-1) points at its staging row once the
-// rank scan numbered the rows, if they fit; any other code is returned as is.
-__device__ __forceinline__ int32_t bw_fused_code(int32_t c, uint32_t i, const hl_cg_fused& cf, uint32_t k_cap,
-                                                 bool fits) {
-  if (c != -1 || !cf.table) return c;
-  const uint32_t sl = cf.slotof[i];
-  return sl < cf.S && fits ? (int32_t)(k_cap + cf.uidx[sl]) : -1;
-}
 
 // the bags [b0, b0 + nb) of one block: off[] holds their offsets.  The fused
 // plan (cf.table) also writes the cold lookups' codes and frees their slots,
@@ -451,13 +439,6 @@ __device__ __forceinline__ void bw_prep_bags(int32_t* codes, const int32_t* off,
   }
 }
 
-// A kernel starts only once the kernels before it on its stream are complete
-// and their writes visible: a store at its start is a handover signal for
-// them (block 0 makes it, with release order at agent scope).
-__device__ __forceinline__ void bw_start_signal(uint32_t* sflag, uint32_t sv) {
-  if (sflag && blockIdx.x == 0 && threadIdx.x == 0)
-    __hip_atomic_store(sflag, sv, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
-}
 
 #define BP_BAGS 256
 __global__ void __launch_bounds__(256)
@@ -1141,6 +1122,18 @@ hl_status hl_embbag_bwd_plan_signal(hl_handle* h, int32_t stg_rows, int32_t* cod
     HL_LAUNCHED();
     *sent = sflag != nullptr;
     st = hl_sort_pairs(h, ws.sort, nullptr, (uint32_t)n_lookups, bits, s, &sk, &sv);
+  } else if (hl_group_by_table_ok(h, n_lookups, n_bags)) {
+    // one lookup per bag: grouped table by table (hl_group.hip), into the
+    // buffers where the sort leaves its result; the others hold the
+    // table-major pairs
+    if ((uint64_t)n_lookups > ws.sort.n_max) return HL_ERR_CAPACITY;
+    uint32_t *rk, *rv;
+    hl_sort_result(ws.sort, bits, &rk, &rv);
+    uint32_t* tk = rk == ws.sort.k0 ? ws.sort.k1 : ws.sort.k0;
+    uint32_t* tv = rv == ws.sort.v0 ? ws.sort.v1 : ws.sort.v0;
+    st = hl_group_by_table(h, codes, bag_ptr, n_bags, stg_rows, tk, tv, rk, rv, ws.gsmall, sflag, sval,
+                           cf && cf->table ? cf : nullptr, s);
+    *sent = sflag != nullptr;
   } else {
     if ((uint64_t)n_lookups > ws.sort.n_max) return HL_ERR_CAPACITY;
     const hl_sort_geom sg = hl_sort_geometry((uint32_t)n_lookups, bits);

@@ -116,6 +116,20 @@ extern "C" hl_status hl_trace_reset(hl_handle* h) {
 }
 
 // ----------------------------------------------------------------------------- handle
+// ----------------------------------------------------------------------------- table bounds
+__global__ void hl_k_tbounds(const uint32_t* __restrict__ base, int32_t n_tables, const uint64_t* __restrict__ bm,
+                             const uint32_t* __restrict__ rank, uint64_t n_entries, uint32_t* __restrict__ tb) {
+  for (int32_t t = threadIdx.x; t <= n_tables; t += blockDim.x)
+    tb[t] = t < n_tables ? hl_hot_below(bm, rank, base[t]) : rank[n_entries - 1];
+}
+
+hl_status hl_table_bounds(hl_handle* h, hipStream_t s) {
+  HL_KERNEL(h, s, "hl_k_tbounds", hl_k_tbounds, dim3(1), dim3(256), 0, s, h->d_base, h->n_tables, h->d_bitmap,
+            h->d_rank, h->n_tiles4k * 16 + 1, h->d_tb);
+  HL_LAUNCHED();
+  return HL_OK;
+}
+
 extern "C" hl_status hl_create(hl_handle** out, int32_t n_tables, const uint32_t* rows_per_table,
                                int32_t dim, hl_dtype dtype, uint32_t k_cap) {
   if (!out || n_tables < 1 || !rows_per_table || dim < 1 || dim > 8192 || k_cap < 1)
@@ -152,6 +166,7 @@ extern "C" hl_status hl_create(hl_handle** out, int32_t n_tables, const uint32_t
   dm((void**)&h->d_counts, sizeof(uint32_t) * total);
   dm((void**)&h->d_bitmap, sizeof(uint64_t) * h->n_tiles4k * 64);
   dm((void**)&h->d_rank, sizeof(uint32_t) * (h->n_tiles4k * 16 + 1));
+  dm((void**)&h->d_tb, sizeof(uint32_t) * (n_tables + 1));
   dm((void**)&h->d_err, sizeof(uint32_t));
   dm((void**)&h->d_tk, h->tk_bytes);
   if (st == HL_OK) {
@@ -162,6 +177,7 @@ extern "C" hl_status hl_create(hl_handle** out, int32_t n_tables, const uint32_t
   if (st == HL_OK) st = fill32(h->d_counts, total, 0, 0);
   if (st == HL_OK) st = fill32((uint32_t*)h->d_bitmap, h->n_tiles4k * 128, 0, 0);
   if (st == HL_OK) st = fill32(h->d_rank, h->n_tiles4k * 16 + 1, 0, 0);
+  if (st == HL_OK) st = fill32(h->d_tb, n_tables + 1, 0, 0);
   if (st == HL_OK) st = fill32(h->d_err, 1, 0, 0);
   if (st == HL_OK) st = fill32(h->d_tk, h->tk_bytes / 4, 0, 0);
   if (st == HL_OK && hipDeviceSynchronize() != hipSuccess) st = HL_ERR_HIP;
@@ -175,7 +191,7 @@ extern "C" hl_status hl_create(hl_handle** out, int32_t n_tables, const uint32_t
 
 extern "C" hl_status hl_destroy(hl_handle* h) {
   if (!h) return HL_ERR_INVALID_ARG;
-  void* ps[] = {h->d_base, h->d_rows, h->d_counts, h->d_bitmap, h->d_rank, h->d_err, h->d_tk, h->cg_table};
+  void* ps[] = {h->d_base, h->d_rows, h->d_counts, h->d_bitmap, h->d_rank, h->d_tb, h->d_err, h->d_tk, h->cg_table};
   hl_status st = HL_OK;
   if (h->trace) {
     trace_free(h->trace);
@@ -185,6 +201,12 @@ extern "C" hl_status hl_destroy(hl_handle* h) {
     if (p && hipFree(p) != hipSuccess) st = HL_ERR_HIP;
   free(h);
   return st;
+}
+
+extern "C" hl_status hl_debug_ballot_ranks(hl_handle* h, int32_t on) {
+  if (!h) return HL_ERR_INVALID_ARG;
+  h->ballot_ranks = on != 0;
+  return HL_OK;
 }
 
 extern "C" uint64_t hl_n_rows(const hl_handle* h) { return h ? h->n_rows : 0; }

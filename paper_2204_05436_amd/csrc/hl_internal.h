@@ -53,12 +53,14 @@ struct hl_handle {
   uint32_t* d_counts;    // [n_rows] access counts
   uint64_t* d_bitmap;    // [n_tiles4k*64] hot-set membership, bit g of word g/64
   uint32_t* d_rank;      // [n_tiles4k*16 + 1] hot ids below 256*j
+  uint32_t* d_tb;        // [n_tables + 1] hot ids below each table's first row (the last: n_hot)
   uint32_t* d_err;       // device error word
   uint32_t* d_tk;        // top-K scratch (state, histograms, tile counts)
   size_t tk_bytes;
   hl_trace* trace;       // per-kernel event records (owned)
   // Workspaces that hold a backward plan (grouping) for a later apply step;
   // any other call on a workspace clears its record.
+  int ballot_ranks;      // the sorts rank every pass by ballots (hl_debug_ballot_ranks)
   hl_ws_rec ws_rec[4];
   int ws_next;           // next record to reuse when all are taken
   uint64_t* cg_table;    // cold-gather hash table (kept clean between calls)
@@ -239,6 +241,42 @@ struct hl_cg_fused {
   const uint32_t* ncold;  // distinct cold ids (written by the rank scan)
   int32_t cap;            // staging rows
 };
+// The backward's sort key of a slot code: the hot slot, or n_hot + staging
+// row; any other code (an invalid one, or -1) gets EB_SENT, which the
+// reduction skips.
+#define EB_SENT 0xFFFFFFFFu
+__device__ __forceinline__ uint32_t bw_key(uint32_t c, uint32_t n_hot, uint32_t k_cap, int32_t stg_rows) {
+  if (c < n_hot) return c;
+  if (c >= k_cap && c - k_cap < (uint32_t)stg_rows) return n_hot + (c - k_cap);
+  return EB_SENT;
+}
+// The fused plan: a cold lookup's code (-1) points at its staging row once the
+// rank scan numbered the rows, if they fit; any other code is returned as is.
+__device__ __forceinline__ int32_t bw_fused_code(int32_t c, uint32_t i, const hl_cg_fused& cf, uint32_t k_cap,
+                                                 bool fits) {
+  if (c != -1 || !cf.table) return c;
+  const uint32_t sl = cf.slotof[i];
+  return sl < cf.S && fits ? (int32_t)(k_cap + cf.uidx[sl]) : -1;
+}
+// A kernel starts only once the kernels before it on its stream are complete
+// and their writes visible: a store at its start is a handover signal for
+// them (block 0 makes it, with release order at agent scope).
+__device__ __forceinline__ void bw_start_signal(uint32_t* sflag, uint32_t sv) {
+  if (sflag && blockIdx.x == 0 && threadIdx.x == 0)
+    __hip_atomic_store(sflag, sv, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+}
+// d_tb of the current hot set (after the bitmap and the rank directory)
+hl_status hl_table_bounds(hl_handle* h, hipStream_t s);
+// Hot ids below row id g (g < n_rows): the rank directory's count for g's
+// 256-id block plus the bitmap bits of that block below g.
+__device__ __forceinline__ uint32_t hl_hot_below(const uint64_t* __restrict__ bm, const uint32_t* __restrict__ rank,
+                                                 uint32_t g) {
+  const uint32_t blk = g >> 8, wi = (g >> 6) & 3, bit = g & 63;
+  uint32_t r = rank[blk];
+  for (uint32_t k = 0; k < wi; ++k) r += __popcll(bm[(size_t)blk * 4 + k]);
+  return r + __popcll(bm[(size_t)blk * 4 + wi] & ((1ull << bit) - 1ull));
+}
+
 // workspace bytes of the backward's plan and apply
 size_t hl_bwd_ws_bytes(const hl_handle* h, int64_t max_lookups, int64_t max_bags);
 // the same without the staging-row sums that the applies in halves keep
@@ -298,6 +336,18 @@ hl_status hl_embbag_bwd_plan_signal(hl_handle* h, int32_t stg_rows, int32_t* cod
                                     const int32_t* n_sel_dev, int32_t n_sel_max, void* workspace, size_t ws_bytes,
                                     hl_stream stream, uint32_t* sflag, uint32_t sv, bool* sent,
                                     const hl_cg_fused* cf, bool compact = false);
+
+// ----------------------------------------------------------------------------- grouping by table
+// The backward's grouping of a one-hot mini-batch table by table (hl_group.hip):
+// taken when every bag holds one lookup (n_lookups = n_bags, checked per bag
+// on the device: HL_DEVERR_SHAPE otherwise), the bags split evenly over at
+// most 64 tables and a table has at most 32768 bags.  k_tm/v_tm: scratch of
+// n_bags pairs; kout/vout: the grouping; small: HL_GROUP_SMALL words.
+#define HL_GROUP_SMALL (64 * 32 + 2 * 64)
+bool hl_group_by_table_ok(const hl_handle* h, int64_t n_lookups, int64_t n_bags);
+hl_status hl_group_by_table(hl_handle* h, int32_t* codes, const int32_t* bag_ptr, int64_t n_bags, int32_t stg_rows,
+                            uint32_t* k_tm, uint32_t* v_tm, uint32_t* kout, uint32_t* vout, uint32_t* small,
+                            uint32_t* sflag, uint32_t sv, const hl_cg_fused* cf, hipStream_t s);
 
 // ----------------------------------------------------------------------------- sort
 // Stable LSD radix sort of (key, value) uint32 pairs with digits of up to 11

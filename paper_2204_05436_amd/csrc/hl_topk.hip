@@ -10,6 +10,12 @@
 // bitmap and the rank directory in one pass.
 #include "hl_internal.h"
 
+#define HL_TRY_ST(x)                  \
+  do {                                \
+    const hl_status _st = (x);        \
+    if (_st != HL_OK) return _st;     \
+  } while (0)
+
 #define TK_BLOCKS 1024
 #define TK_STATE 16
 // state words
@@ -233,6 +239,7 @@ extern "C" hl_status hl_profile_topk(hl_handle* h, uint32_t k, uint32_t* hot_ids
   HL_KERNEL(h, s, "tk_emit", tk_emit, dim3((uint32_t)tiles), dim3(256), 0, s, h->d_counts, n, h->d_tk, tiles,
                      hot_ids_out, h->d_bitmap, h->d_rank, reset_counts);
   HL_LAUNCHED();
+  HL_TRY_ST(hl_table_bounds(h, s));
   uint32_t nh = 0;
   HL_HIP(hipMemcpyAsync(&nh, h->d_tk + S_NHOT, 4, hipMemcpyDeviceToHost, s));
   HL_HIP(hipStreamSynchronize(s));
@@ -283,6 +290,7 @@ extern "C" hl_status hl_set_hot(hl_handle* h, const uint32_t* hot_ids, uint32_t 
   if (g2 > 4096) g2 = 4096;
   HL_KERNEL(h, s, "sh_rank", sh_rank, dim3(g2), dim3(256), 0, s, hot_ids, n_hot, ne, h->d_rank);
   HL_LAUNCHED();
+  HL_TRY_ST(hl_table_bounds(h, s));
   h->n_hot = n_hot;
   return HL_OK;
 }

@@ -85,6 +85,7 @@ _SIGS = {
     "hl_noalloc_scratch_bytes": (SZ, []),
     "hl_embbag_bwd_sgd_noalloc": (C.c_int, [P, P, P, I32, P, P, I32, I32, I64, P, P, I32, P, F32, P]),
     "hl_last_device_error": (C.c_int, [P, C.POINTER(U32)]),
+    "hl_debug_ballot_ranks": (C.c_int, [P, I32]),
     "hl_trace_enable": (C.c_int, [P, I32]),
     "hl_trace_count": (I32, [P]),
     "hl_trace_only": (C.c_int, [P, C.c_char_p]),
@@ -429,6 +430,10 @@ def hl_embbag_bwd_grouping(h, staging_rows, n_samples, bags_per_sample, n_lookup
     _ck("hl_embbag_bwd_grouping", lib().hl_embbag_bwd_grouping(
         h.ptr, int(staging_rows), int(n_samples), int(bags_per_sample), int(n_lookups), _p(ws), _nbytes(ws),
         _p(keys_out), _p(bags_out), _s(stream)))
+
+
+def hl_debug_ballot_ranks(h, on):
+    _ck("hl_debug_ballot_ranks", lib().hl_debug_ballot_ranks(h.ptr, int(bool(on))))
 
 
 def hl_last_device_error(h):

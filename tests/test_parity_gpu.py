@@ -809,3 +809,33 @@ def test_eal_srrip(name, geom):
     finally:
         e.close()
         hl.hl_destroy(h)
+
+
+@pytest.mark.parametrize("name", ["dlrm-large", "tbsm", "tiny"])
+def test_grouping_ranks_fallback(name):
+    """The grouping's radix passes rank equal digits with one counter update per
+    item, check the order they kept, and redo a pass with ballot ranks if an
+    order broke.  With the ballot ranks forced (hl_debug_ballot_ranks) the
+    grouping is the same bit for bit, and the parity holds."""
+    w = configs.scaled(configs.WORKLOADS[name], batch=1500, row_scale=0.01 if name != "tiny" else 0.5,
+                       name=name + "-ranks")
+    rows = W.table_rows(w)
+    n_rows = int(rows.sum(dtype=np.int64))
+    k_cap = w.k_cap(n_rows)
+    prof = [W.make_batch(w, rows, i) for i in range(4)]
+    mb = W.make_batch(w, rows, 5)
+    dY = W.make_dy(w, 5, mb.n_bags)
+    groupings = []
+    for forced in (False, True):
+        table = make_table(w, n_rows)
+        hp = HotPath(w, rows, table, max(b.n_lookups for b in prof + [mb]), mb.n_samples)
+        try:
+            hl.hl_debug_ballot_ranks(hp.h, forced)
+            g = run_gpu_stages(hp, prof, mb, dY, split=True)
+            o = run_oracle(w, rows, prof, mb, dY, table.array, k_cap)
+            compare(w, g, o, k_cap)
+            groupings.append(g["grouping"])
+        finally:
+            hp.close()
+            table.close()
+    assert np.array_equal(groupings[0][0], groupings[1][0]) and np.array_equal(groupings[0][1], groupings[1][1])
