@@ -322,6 +322,132 @@ eb_fwd(const void* w_hot_, const void* stg_, int32_t stg_rows, uint32_t n_hot, u
   hl_hook_tail(hk);
 }
 
+// The same for a one-hot mini-batch over every sample (as many lookups as
+// bags: bag j is expected to hold lookup j alone), PART 0 or 1: the codes are
+// loaded with the bag offsets that confirm them, one chunk ahead, and the rows
+// of the next chunk are in flight while a chunk is stored, so each row group
+// keeps two chunks' rows loading.  A chunk with a bag that is not one-hot is
+// pooled bag by bag as eb_fwd does.  Same sums, same outputs.
+template <int VEC, bool BF>
+struct oh_meta {
+  uint32_t code[FC];
+  bool oh;  // every bag of the chunk holds exactly its own lookup
+};
+
+template <int VEC, bool BF>
+__device__ __forceinline__ void oh_load_meta(int64_t ch, int64_t chunks, int64_t n_bags,
+                                             const int32_t* __restrict__ bag_ptr, const int32_t* __restrict__ codes,
+                                             oh_meta<VEC, BF>& m) {
+  int32_t lo[FC], hi[FC];
+#pragma unroll
+  for (int u = 0; u < FC; ++u) {
+    const int64_t b = ch * FC + u;
+    const bool v = ch < chunks && b < n_bags;
+    lo[u] = v ? bag_ptr[b] : (int32_t)b;
+    hi[u] = v ? bag_ptr[b + 1] : (int32_t)b + 1;
+    m.code[u] = v ? (uint32_t)codes[b] : 0u;
+  }
+  m.oh = true;
+#pragma unroll
+  for (int u = 0; u < FC; ++u) m.oh = m.oh && lo[u] == (int32_t)(ch * FC + u) && hi[u] == lo[u] + 1;
+}
+
+// a chunk's rows (PART 1: its hot rows only), zero for a code that names no row
+template <int VEC, bool BF, int PART>
+__device__ __forceinline__ void oh_load_rows(int64_t ch, int64_t n_bags, const oh_meta<VEC, BF>& m,
+                                             const typename RowIO<VEC, BF>::T* w_hot,
+                                             const typename RowIO<VEC, BF>::T* stg, int32_t stg_rows, uint32_t n_hot,
+                                             uint32_t k_cap, int64_t D, int64_t col, bool cact, float (&v)[FC][VEC]) {
+#pragma unroll
+  for (int u = 0; u < FC; ++u) {
+    const uint32_t cu = m.code[u];
+    const bool in = ch * FC + u < n_bags && cact;
+    const bool hot = cu < n_hot;
+    const bool cold = PART == 0 && cu >= k_cap && cu - k_cap < (uint32_t)stg_rows;
+    if (in && (hot || cold)) {
+      const typename RowIO<VEC, BF>::T* p = hot ? w_hot + (int64_t)cu * D : stg + (int64_t)(cu - k_cap) * D;
+      RowIO<VEC, BF>::load(p + col, v[u]);
+    } else {
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) v[u][e] = 0.f;
+    }
+  }
+}
+
+// The same for a one-hot mini-batch over every sample (as many lookups as
+// bags: bag j is expected to hold lookup j alone), PART 0 or 1: the codes are
+// loaded with the bag offsets that confirm them, one chunk ahead, and the rows
+// of the next chunk are in flight while a chunk is stored, so each row group
+// keeps two chunks' rows loading.  A chunk with a bag that is not one-hot is
+// pooled bag by bag as eb_fwd does.  Same sums, same outputs.
+template <int VEC, bool BF, int PART>
+__global__ void __launch_bounds__(256)
+eb_fwd_oh(const void* w_hot_, const void* stg_, int32_t stg_rows, uint32_t n_hot, uint32_t k_cap,
+          const int32_t* __restrict__ codes, const int32_t* __restrict__ bag_ptr, float* __restrict__ out, eb_geom g,
+          int64_t n_lookups, int64_t n_bags, uint32_t* err, hl_hook hk) {
+  static_assert(PART == 0 || PART == 1, "whole forward or its hot half");
+  typedef typename RowIO<VEC, BF>::T T;
+  const T* w_hot = (const T*)w_hot_;
+  const T* stg = (const T*)stg_;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int gi = lane / g.G, gl = lane - gi * g.G;
+  hl_hook_head(hk);
+  if (blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0 && bag_ptr[n_bags] != n_lookups)
+    hl_flag(err, HL_DEVERR_SHAPE);
+  if (gi >= g.NG) return;  // (never thread 0, which carries the handover)
+  const int32_t colv = blockIdx.y * 64 + gl;
+  const bool cact = colv < g.vpr;
+  const int64_t col = (int64_t)colv * VEC;
+  const int64_t chunks = (n_bags + FC - 1) / FC;
+  const int64_t stride = (int64_t)gridDim.x * 4 * g.NG;
+  int64_t c = ((int64_t)blockIdx.x * 4 + w) * g.NG + gi;
+  oh_meta<VEC, BF> m0, m1;
+  float v0[FC][VEC];
+  oh_load_meta<VEC, BF>(c, chunks, n_bags, bag_ptr, codes, m0);
+  oh_load_rows<VEC, BF, PART>(c, n_bags, m0, w_hot, stg, stg_rows, n_hot, k_cap, g.D, col, cact && m0.oh, v0);
+  oh_load_meta<VEC, BF>(c + stride, chunks, n_bags, bag_ptr, codes, m1);
+  for (; c < chunks; c += stride) {
+    float v1[FC][VEC];
+    oh_load_rows<VEC, BF, PART>(c + stride, n_bags, m1, w_hot, stg, stg_rows, n_hot, k_cap, g.D, col,
+                                cact && m1.oh && c + stride < chunks, v1);
+    oh_meta<VEC, BF> m2;
+    oh_load_meta<VEC, BF>(c + 2 * stride, chunks, n_bags, bag_ptr, codes, m2);
+    if (m0.oh) {
+#pragma unroll
+      for (int u = 0; u < FC; ++u) {
+        const int64_t b = c * FC + u;
+        if (b >= n_bags) continue;
+        const uint32_t cu = m0.code[u];
+        const bool named = cu < n_hot || (cu >= k_cap && cu - k_cap < (uint32_t)stg_rows);
+        if (!named && gl == 0) hl_flag(err, HL_DEVERR_BAD_CODE);
+        if (cact) st_f32_nt<VEC>(out + b * g.D + col, v0[u]);
+      }
+    } else {
+      // some bag of this chunk is not one-hot: bag by bag, its hot rows then
+      // (PART 0) its staging rows, in CSR order
+      for (int u = 0; u < FC; ++u) {
+        const int64_t b = c * FC + u;
+        if (b >= n_bags) break;
+        const int32_t lo = bag_ptr[b], hi = bag_ptr[b + 1];
+        float acc[VEC];
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) acc[e] = 0.f;
+        eb_pass<VEC, BF, false>(acc, w_hot, stg, stg_rows, n_hot, k_cap, codes, lo, hi, g, col, cact, gl, err);
+        if (PART == 0)
+          eb_pass<VEC, BF, true>(acc, w_hot, stg, stg_rows, n_hot, k_cap, codes, lo, hi, g, col, cact, gl, err);
+        if (cact) st_f32_nt<VEC>(out + b * g.D + col, acc);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < FC; ++u)
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) v0[u][e] = v1[u][e];
+    m0 = m1;
+    m1 = m2;
+  }
+  hl_hook_tail(hk);
+}
+
 // ----------------------------------------------------------------------------- backward
 struct bw_ws {
   hl_sort_ws sort;
@@ -1004,6 +1130,26 @@ static void launch_fwd(const hl_handle* h, dim3 grid, hipStream_t s, const void*
 #undef EBF
 }
 
+// grid of the one-hot forward: about 8 resident blocks per compute unit, each
+// row group taking several chunks in turn
+#define EB_OH_BLOCKS 1024
+template <int VEC, bool BF>
+static void launch_fwd_oh(const hl_handle* h, hipStream_t s, const void* w_hot, const void* stg, int32_t stg_rows,
+                          const int32_t* codes, const int32_t* bag_ptr, float* out, eb_geom g, int64_t n_lookups,
+                          int64_t n_bags, int part) {
+  const hl_hook hk = hl_hook_take(h);
+  const int64_t chunks = (n_bags + FC - 1) / FC;
+  int64_t blocks = (chunks + 4 * g.NG - 1) / (4 * g.NG);
+  if (blocks > EB_OH_BLOCKS) blocks = EB_OH_BLOCKS;
+  const dim3 grid((uint32_t)blocks, g.cchunks);
+  if (part == 0)
+    HL_KERNEL(h, s, "eb_fwd", (eb_fwd_oh<VEC, BF, 0>), grid, dim3(256), 0, s, w_hot, stg, stg_rows, h->n_hot,
+              h->k_cap, codes, bag_ptr, out, g, n_lookups, n_bags, h->d_err, hk);
+  else
+    HL_KERNEL(h, s, "eb_fwd_hot", (eb_fwd_oh<VEC, BF, 1>), grid, dim3(256), 0, s, w_hot, stg, stg_rows, h->n_hot,
+              h->k_cap, codes, bag_ptr, out, g, n_lookups, n_bags, h->d_err, hk);
+}
+
 extern "C" hl_status hl_embbag_fwd_part(const hl_handle* h, const void* w_hot, const void* staging, int32_t stg_rows,
                                         const int32_t* codes, const int32_t* bag_ptr, int32_t n_samples, int32_t bps,
                                         int64_t n_lookups, const int32_t* sample_ids, const int32_t* n_sel_dev,
@@ -1023,6 +1169,16 @@ extern "C" hl_status hl_embbag_fwd_part(const hl_handle* h, const void* w_hot, c
   hipStream_t s = (hipStream_t)stream;
   const int64_t nb = (int64_t)n_samples * bps;
   const bool bf = h->dtype == HL_BF16;
+  if (part != 2 && !sample_ids && n_sel_max == n_samples && n_lookups == nb) {
+    // every sample of a one-hot mini-batch
+#define FOH(V, B) launch_fwd_oh<V, B>(h, s, w_hot, staging, stg_rows, codes, bag_ptr, out, g, n_lookups, nb, part)
+    if (vec == 4) { if (bf) FOH(4, true); else FOH(4, false); }
+    else if (vec == 2) { if (bf) FOH(2, true); else FOH(2, false); }
+    else { if (bf) FOH(1, true); else FOH(1, false); }
+#undef FOH
+    HL_LAUNCHED();
+    return HL_OK;
+  }
 #define FWD(V, B) launch_fwd<V, B>(h, grid, s, w_hot, staging, stg_rows, codes, bag_ptr, bps, sample_ids, n_sel_dev, \
                                    n_sel_max, out, g, n_lookups, nb, part)
   if (vec == 4) { if (bf) FWD(4, true); else FWD(4, false); }

@@ -1,5 +1,5 @@
 // The backward's grouping of a one-hot mini-batch (one lookup per bag, the
-// layout of the DLRM- and TBSM-shaped workloads) table by table.
+// layout of the DLRM-shaped workloads) table by table.
 //
 // The reduction needs the (key, bag) pairs of every distinct key contiguous,
 // in ascending lookup order, hot keys first.  Hot slots are ranks of the
@@ -8,33 +8,111 @@
 // table.  Sorting each table's lookups by key, and placing the tables' hot
 // pairs one after another at the front and their other pairs one before
 // another at the back, gives such an order without a sort over the whole
-// mini-batch.  A table's E = n_bags / T lookups (bag j = s T + t is its s-th)
-// are cut into chunks of GC; two launches, every block independent:
+// mini-batch.  Two launches:
 //
-//  gt_chunk -- a block per (table, chunk): reads its lookups' codes (strided
-//              by T), forms the keys (the fused plan's cold-code rewrite
-//              included), compresses them to [0, R_t) for hot slots (R_t =
-//              hi_t - lo_t) and above for staging rows, sorts the chunk by
-//              key in LDS (LSD radix of as many 9-bit digits as its largest
-//              key needs; each pass checked for stability and redone with
-//              ballot ranks if it broke an order), and writes the sorted
-//              chunk and its count of hot keys.
-//  gt_merge -- a block per (table, chunk): the table's sorted chunks into
-//              LDS; each pair's rank in its table is its rank in its chunk
-//              plus, in every other chunk, the keys below it (and the equal
-//              ones of earlier chunks: lookup order) by binary search; the
-//              tables' offsets from the chunks' hot counts.
+//  gt_prep  -- the pairs in table-major order (bag j = s T + t goes to
+//              position t E + s, E = bags per table): a block takes 64
+//              consecutive bag rows s, reads their offsets and codes
+//              (coalesced), forms the keys (the fused plan's cold-code
+//              rewrite included), and writes each table's 64 pairs through
+//              LDS.  It also clears gt_sort's status words.
+//  gt_sort  -- one block per table:
+//              the table's E pairs, keys compressed to [0, R_t) for hot slots
+//              (R_t = hi_t - lo_t) and above for staging rows, sorted in LDS
+//              by an LSD radix of as many 9-bit digits as the largest key
+//              needs; then the table's hot pairs go to the front of the
+//              output after those of the earlier tables, its others to the
+//              back before those of the earlier tables (offsets by a
+//              look-back over the earlier tables' counts).
+//
+// Ranks inside a wave: the lanes that hold the wave's first lane's digit
+// advance its counter once, together (stable by construction); every other
+// lane adds 1 to its digit's counter and takes the old value, an order among
+// same-digit lanes of one instruction that nothing specifies.  So the sorted
+// table is checked (keys ascending, bags ascending among equal keys: the
+// stable order, and the only one that passes) and, if the check fails, sorted
+// again with every rank formed from ballot peer masks.
 #include "hl_internal.h"
 
-#define GC 1024           // lookups per chunk (gt_merge's searches take 11 halving steps)
-#define GC_THREADS 256
-#define GC_ITEMS (GC / GC_THREADS)
-#define GC_WAVES (GC_THREADS / 64)
+#define GT_S 32           // bag rows per gt_prep block
+#define GT_PI ((GT_S * GT_TMAX + 255) / 256)  // bags per gt_prep thread (at most)
 #define GT_TMAX 64        // tables the path takes
-#define GT_CMAX 32        // chunks per table
-#define GT_DBITS 9        // largest digit of the chunk sort
+#define GT_THREADS 1024
+#define GT_WAVES (GT_THREADS / 64)
+#define GT_IMAX 8         // items per thread: at most GT_IMAX * GT_THREADS bags per table (no spills)
+#define GT_DBITS 9        // largest digit of the sort
 #define GT_NB (1 << GT_DBITS)
+#define GT_FLAG (1ull << 63)
 
+// ----------------------------------------------------------------------------- prep
+__global__ void __launch_bounds__(256)
+gt_prep(int32_t* codes, const int32_t* __restrict__ bag_ptr, int64_t n_bags, int32_t T, uint32_t E, uint32_t n_hot,
+        uint32_t k_cap, int32_t stg_rows, uint32_t* __restrict__ keys_tm, uint32_t* __restrict__ vals_tm,
+        uint64_t* __restrict__ tstat, int64_t n_lookups, uint32_t* sflag, uint32_t sv, uint32_t* err,
+        hl_cg_fused cf) {
+  __shared__ uint32_t lk[GT_TMAX][GT_S];
+  __shared__ uint32_t s_bad;
+  bw_start_signal(sflag, sv);
+  const int tid = threadIdx.x;
+  if (tid == 0) s_bad = 0;
+  if (blockIdx.x == 0)
+    for (int t = tid; t < T; t += blockDim.x) tstat[t] = 0;
+  const bool fits = cf.table && *cf.ncold <= (uint32_t)cf.cap;
+  if (blockIdx.x == 0 && tid == 0) {
+    if (bag_ptr[n_bags] != n_lookups) hl_flag(err, HL_DEVERR_SHAPE);
+    if (cf.table && !fits) hl_flag(err, HL_DEVERR_CAPACITY);
+  }
+  __syncthreads();
+  const uint32_t s0 = blockIdx.x * GT_S;
+  const uint32_t ns = min((uint32_t)GT_S, E - s0);
+  const int64_t j0 = (int64_t)s0 * T;
+  const uint32_t nb = ns * (uint32_t)T;
+  bool bad = false, badc = false;
+  // every load of the thread's bags in flight before any is used
+  int32_t lo[GT_PI], hi[GT_PI], cc[GT_PI];
+#pragma unroll
+  for (int i = 0; i < GT_PI; ++i) {
+    const uint32_t q = tid + i * 256;
+    const int64_t j = j0 + min(q, nb - 1);
+    lo[i] = bag_ptr[j];
+    hi[i] = bag_ptr[j + 1];
+    cc[i] = codes[j];
+  }
+#pragma unroll
+  for (int i = 0; i < GT_PI; ++i) {
+    const uint32_t q = tid + i * 256;
+    if (q >= nb) continue;
+    const int64_t j = j0 + q;
+    uint32_t key = EB_SENT;
+    // one lookup per bag: bag j holds lookup j
+    if (lo[i] != j || hi[i] != j + 1) {
+      bad = true;
+    } else {
+      int32_t c = cc[i];
+      if (cf.table && c == -1) {
+        const uint32_t sl = cf.slotof[j];
+        c = bw_fused_code(c, (uint32_t)j, cf, k_cap, fits);
+        if (c != -1) codes[j] = c;
+        if (sl < cf.S) cf.table[sl] = 0;
+      }
+      key = bw_key((uint32_t)c, n_hot, k_cap, stg_rows);
+      badc = badc || key == EB_SENT;
+    }
+    lk[q % (uint32_t)T][q / (uint32_t)T] = key;
+  }
+  if (bad) s_bad = 1;  // (every writer stores 1)
+  if (badc) hl_flag(err, HL_DEVERR_BAD_CODE);
+  __syncthreads();
+  if (tid == 0 && s_bad) hl_flag(err, HL_DEVERR_SHAPE);
+  for (uint32_t q = tid; q < nb; q += blockDim.x) {
+    const uint32_t t = q / ns, s = q - t * ns;
+    const uint64_t p = (uint64_t)t * E + s0 + s;
+    keys_tm[p] = lk[t][s];  // (a row of GT_S pairs of one table)
+    vals_tm[p] = (s0 + s) * (uint32_t)T + t;
+  }
+}
+
+// ----------------------------------------------------------------------------- sort
 // Exclusive scan of one value per thread over the block; *total receives the sum.
 __device__ __forceinline__ uint32_t gt_scan(uint32_t v, uint32_t* ws, uint32_t* total) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
@@ -47,7 +125,7 @@ __device__ __forceinline__ uint32_t gt_scan(uint32_t v, uint32_t* ws, uint32_t* 
   if (lane == 63) ws[w] = x;
   __syncthreads();
   uint32_t off = 0, tot = 0;
-  for (int q = 0; q < (int)(blockDim.x >> 6); ++q) {
+  for (int q = 0; q < GT_WAVES; ++q) {
     const uint32_t c = ws[q];
     off += q < w ? c : 0u;
     tot += c;
@@ -57,310 +135,203 @@ __device__ __forceinline__ uint32_t gt_scan(uint32_t v, uint32_t* ws, uint32_t* 
   return x - v + off;
 }
 
-// ----------------------------------------------------------------------------- chunk sort
-__global__ void __launch_bounds__(GC_THREADS)
-gt_chunk(int32_t* codes, const int32_t* __restrict__ bag_ptr, int64_t n_bags, int32_t T, uint32_t E, uint32_t C,
-         uint32_t n_hot, uint32_t k_cap, int32_t stg_rows, const uint32_t* __restrict__ tb, uint32_t* __restrict__ ck,
-         uint32_t* __restrict__ cv, uint32_t* __restrict__ hcnt, uint32_t* __restrict__ lor, int64_t n_lookups,
-         uint32_t* sflag, uint32_t sv, uint32_t* err, hl_cg_fused cf, int ballot_only) {
-  __shared__ uint32_t sk[GC], sval[GC], spos[GC];
-  __shared__ uint32_t wcnt[GC_WAVES][GT_NB];
+template <int ITEMS>
+__global__ void __launch_bounds__(GT_THREADS)
+gt_sort(const uint32_t* __restrict__ keys_tm, const uint32_t* __restrict__ vals_tm, uint32_t E, int32_t T,
+        uint32_t n, const uint32_t* __restrict__ tb, uint32_t n_hot, uint32_t* __restrict__ kout,
+        uint32_t* __restrict__ vout, uint64_t* tstat, uint32_t* err, int ballot_only, hl_hook hk) {
+  __shared__ uint32_t sk[ITEMS * GT_THREADS], sv[ITEMS * GT_THREADS];
+  __shared__ uint32_t wcnt[GT_WAVES][GT_NB];
   __shared__ uint32_t dofs[GT_NB];
-  __shared__ uint32_t scan_ws[GC_WAVES];
-  __shared__ uint32_t s_lo, s_hi, s_max, s_bad;
-  bw_start_signal(sflag, sv);
+  __shared__ uint32_t scan_ws[GT_WAVES];
+  __shared__ uint32_t s_lo, s_hi, s_max, s_sent;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const uint32_t t = blockIdx.x / C, c = blockIdx.x - t * C;
-  const uint32_t s0 = c * GC;
-  const uint32_t ns = min((uint32_t)GC, E - s0);
-  const bool fits = cf.table && *cf.ncold <= (uint32_t)cf.cap;
+  hl_hook_head(hk);  // a handover signal: the codes are complete (gt_prep has ended)
+  const uint32_t t = blockIdx.x;
   if (tid == 0) {
     s_lo = tb[t];  // the table's hot slots
     s_hi = tb[t + 1];
     s_max = 0;
-    s_bad = 0;
-    if (blockIdx.x == 0 && bag_ptr[n_bags] != n_lookups) hl_flag(err, HL_DEVERR_SHAPE);
-    if (blockIdx.x == 0 && cf.table && !fits) hl_flag(err, HL_DEVERR_CAPACITY);
+    s_sent = 0;
   }
-  for (int j = tid; j < GC_WAVES * GT_NB; j += GC_THREADS) (&wcnt[0][0])[j] = 0;
-  // the chunk's lookups: item k of thread (w, lane) is the chunk's lookup
-  // r = w * 64 ITEMS + 64 k + lane (lookup order)
-  uint32_t key[GC_ITEMS], val[GC_ITEMS];
-  bool bad = false, badc = false;
-#pragma unroll
-  for (int k = 0; k < GC_ITEMS; ++k) {
-    const uint32_t r = (uint32_t)w * (GC_ITEMS * 64) + k * 64 + lane;
-    key[k] = EB_SENT;
-    val[k] = 0;
-    if (r >= ns) continue;
-    const int64_t j = (int64_t)(s0 + r) * T + t;
-    val[k] = (uint32_t)j;
-    if (bag_ptr[j] != j || bag_ptr[j + 1] != j + 1) {  // one lookup per bag: bag j holds lookup j
-      bad = true;
-      continue;
-    }
-    int32_t cc = codes[j];
-    if (cf.table && cc == -1) {
-      const uint32_t sl = cf.slotof[j];
-      cc = bw_fused_code(cc, (uint32_t)j, cf, k_cap, fits);
-      if (cc != -1) codes[j] = cc;
-      if (sl < cf.S) cf.table[sl] = 0;
-    }
-    key[k] = bw_key((uint32_t)cc, n_hot, k_cap, stg_rows);
-    badc = badc || key[k] == EB_SENT;
-  }
-  if (bad) s_bad = 1;  // (every writer stores 1)
+  for (int j = tid; j < GT_WAVES * GT_NB; j += GT_THREADS) (&wcnt[0][0])[j] = 0;
   __syncthreads();
-  if (tid == 0 && s_bad) hl_flag(err, HL_DEVERR_SHAPE);
   const uint32_t lo = s_lo, R = s_hi - s_lo;
-  // compressed keys: hot slot - lo, R + staging row; skipped lookups (an
-  // invalid code, or a hot slot of another table's row) R + stg_rows, after
-  // every other
-  const uint32_t sent = R + (uint32_t)stg_rows;
-  uint32_t kmax = 0;
-  bool foreign = false;
-#pragma unroll
-  for (int k = 0; k < GC_ITEMS; ++k) {
-    const uint32_t r = (uint32_t)w * (GC_ITEMS * 64) + k * 64 + lane;
-    uint32_t x = sent;
-    if (key[k] < n_hot) {
-      if (key[k] - lo < R) x = key[k] - lo;
-      else foreign = true;
-    } else if (key[k] != EB_SENT) {
-      x = R + (key[k] - n_hot);
-    }
-    key[k] = x;
-    if (r < ns) kmax = max(kmax, x);
-  }
-  if (badc || foreign) hl_flag(err, HL_DEVERR_BAD_CODE);
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) kmax = max(kmax, (uint32_t)__shfl_xor(kmax, o));
-  if (lane == 0) atomicMax(&s_max, kmax);
-  __syncthreads();
-  const int bits = 32 - __clz(s_max);
-  const int passes = (bits + GT_DBITS - 1) / GT_DBITS;  // 0: every key is 0, already in order
-  const int b = passes ? (bits + passes - 1) / passes : 1;
-  const uint32_t mask = (1u << b) - 1u;
   const uint64_t lt = (1ull << lane) - 1ull;
-  for (int p = 0; p < passes; ++p) {
-    const int shift = p * b;
-    uint32_t dg[GC_ITEMS];
+  uint32_t key[ITEMS], val[ITEMS];
+  for (int stable = ballot_only ? 1 : 0; stable < 2; ++stable) {
+    // the table's pairs: position w * 64 ITEMS + 64 k + lane (lookup order);
+    // compressed keys: hot slot - lo, or R + staging row, or (skipped: an
+    // invalid code, or a hot slot of another table's row) one past the largest
+    uint32_t kmax = 0;
+    bool foreign = false, anysent = false;
 #pragma unroll
-    for (int k = 0; k < GC_ITEMS; ++k) dg[k] = (key[k] >> shift) & mask;
-    // The pass is stable iff the items of one digit keep their order.  First
-    // try: every item adds 1 to its digit's counter of the wave and takes the
-    // old value as its rank inside the wave; the order that gives to lanes of
-    // one instruction with the same digit is not specified, so the pass is
-    // checked after its scatter (equal digits next to each other must come
-    // from increasing positions) and, if an order was broken, done again with
-    // ranks that are stable by construction (ballot peer masks).
-    for (int stable = ballot_only ? 1 : 0; stable < 2; ++stable) {
-      uint32_t rk[GC_ITEMS];
+    for (int k = 0; k < ITEMS; ++k) {
+      const uint32_t pos = (uint32_t)w * (ITEMS * 64) + k * 64 + lane;
+      const bool valid = pos < E;
+      const uint32_t kk = keys_tm[(uint64_t)t * E + min(pos, E - 1)];
+      val[k] = vals_tm[(uint64_t)t * E + min(pos, E - 1)];
+      uint32_t c = EB_SENT;
+      if (kk < n_hot) {
+        if (kk - lo < R) c = kk - lo;
+        else foreign = true;
+      } else if (kk != EB_SENT) {
+        c = R + (kk - n_hot);
+      }
+      key[k] = c;
+      if (valid && c != EB_SENT) kmax = max(kmax, c);
+      anysent = anysent || (valid && c == EB_SENT);
+    }
+    if (foreign && !stable) hl_flag(err, HL_DEVERR_BAD_CODE);
 #pragma unroll
-      for (int k = 0; k < GC_ITEMS; ++k) {
-        const uint32_t r = (uint32_t)w * (GC_ITEMS * 64) + k * 64 + lane;
-        const bool valid = r < ns;
-        if (!stable) {
-          rk[k] = valid ? atomicAdd(&wcnt[w][dg[k]], 1u) : 0u;
-        } else {
+    for (int o = 32; o > 0; o >>= 1) kmax = max(kmax, (uint32_t)__shfl_xor(kmax, o));
+    if (lane == 0) atomicMax(&s_max, kmax);
+    if (anysent) s_sent = 1;
+    __syncthreads();
+    const uint32_t sent = max(s_max + 1, R);  // after every valid key, never below R (not hot)
+#pragma unroll
+    for (int k = 0; k < ITEMS; ++k)
+      if (key[k] == EB_SENT) key[k] = sent;
+    const uint32_t top = s_sent ? sent : s_max;
+    const int bits = 32 - __clz(top);
+    const int passes = (bits + GT_DBITS - 1) / GT_DBITS;  // 0: every key is 0, already in order
+    const int b = passes ? (bits + passes - 1) / passes : 1;
+    const uint32_t mask = (1u << b) - 1u;
+    for (int p = 0; p < passes; ++p) {
+      const int shift = p * b;
+      uint32_t dg[ITEMS], rk[ITEMS];
+#pragma unroll
+      for (int k = 0; k < ITEMS; ++k) {
+        const uint32_t pos = (uint32_t)w * (ITEMS * 64) + k * 64 + lane;
+        const bool valid = pos < E;
+        dg[k] = (key[k] >> shift) & mask;
+        if (stable) {
           const uint64_t peers = hl_match_digit(dg[k], b, valid);
           const int leader = __ffsll((unsigned long long)peers) - 1;
           uint32_t bs = 0;
           if (valid && lane == leader) bs = atomicAdd(&wcnt[w][dg[k]], (uint32_t)__popcll(peers));
           bs = __shfl(bs, leader < 0 ? 0 : leader);
           rk[k] = bs + (uint32_t)__popcll(peers & lt);
+        } else {
+          // the lanes of the first lane's digit together, the others one by one
+          const uint32_t d0 = __builtin_amdgcn_readfirstlane(dg[k]);
+          const uint64_t m0 = __ballot(valid && dg[k] == d0);
+          const bool in0 = (m0 >> lane) & 1ull;
+          const int l0 = m0 ? __ffsll((unsigned long long)m0) - 1 : 0;
+          uint32_t b0 = 0;
+          if (m0 && lane == l0) b0 = atomicAdd(&wcnt[w][d0], (uint32_t)__popcll(m0));
+          b0 = __shfl(b0, l0);
+          uint32_t r1 = 0;
+          if (valid && !in0) r1 = atomicAdd(&wcnt[w][dg[k]], 1u);
+          rk[k] = in0 ? b0 + (uint32_t)__popcll(m0 & lt) : r1;
         }
       }
       __syncthreads();
       // per digit: offsets of the waves, then of the digits
-      for (uint32_t d = tid; d <= mask; d += GC_THREADS) {
-        uint32_t run = 0;
-        for (int q = 0; q < GC_WAVES; ++q) {
-          const uint32_t x = wcnt[q][d];
-          wcnt[q][d] = run;
-          run += x;
+      uint32_t tot = 0;
+      if (tid <= (int)mask) {
+        for (int q = 0; q < GT_WAVES; ++q) {
+          const uint32_t x = wcnt[q][tid];
+          wcnt[q][tid] = tot;
+          tot += x;
         }
-        dofs[d] = run;
-      }
-      __syncthreads();
-      // exclusive scan of the digit totals (GT_NB / GC_THREADS per thread)
-      constexpr int PD = GT_NB / GC_THREADS;
-      uint32_t loc[PD], sum = 0;
-#pragma unroll
-      for (int q = 0; q < PD; ++q) {
-        const uint32_t d = tid * PD + q;
-        loc[q] = d <= mask ? dofs[d] : 0u;
-        sum += loc[q];
       }
       uint32_t all;
-      uint32_t ex = gt_scan(sum, scan_ws, &all);
-#pragma unroll
-      for (int q = 0; q < PD; ++q) {
-        const uint32_t d = tid * PD + q;
-        if (d <= mask) dofs[d] = ex;
-        ex += loc[q];
-      }
+      const uint32_t ex = gt_scan(tid <= (int)mask ? tot : 0u, scan_ws, &all);
+      if (tid <= (int)mask) dofs[tid] = ex;
       __syncthreads();
 #pragma unroll
-      for (int k = 0; k < GC_ITEMS; ++k) {
-        const uint32_t r = (uint32_t)w * (GC_ITEMS * 64) + k * 64 + lane;
-        if (r < ns) {
+      for (int k = 0; k < ITEMS; ++k) {
+        const uint32_t pos = (uint32_t)w * (ITEMS * 64) + k * 64 + lane;
+        if (pos < E) {
           const uint32_t q = dofs[dg[k]] + wcnt[w][dg[k]] + rk[k];
           sk[q] = key[k];
-          sval[q] = val[k];
-          spos[q] = r;
+          sv[q] = val[k];
         }
       }
       __syncthreads();
-      for (int j = tid; j < GC_WAVES * GT_NB; j += GC_THREADS) (&wcnt[0][0])[j] = 0;
-      if (stable) break;
-      bool broken = false;
 #pragma unroll
-      for (int k = 0; k < GC_ITEMS; ++k) {
-        const uint32_t q = (uint32_t)w * (GC_ITEMS * 64) + k * 64 + lane;
-        if (q > 0 && q < ns && ((sk[q] >> shift) & mask) == ((sk[q - 1] >> shift) & mask) && spos[q] < spos[q - 1])
-          broken = true;
+      for (int k = 0; k < ITEMS; ++k) {
+        const uint32_t pos = (uint32_t)w * (ITEMS * 64) + k * 64 + lane;
+        if (pos < E) {
+          key[k] = sk[pos];
+          val[k] = sv[pos];
+        }
       }
-      if (!__syncthreads_or(broken)) break;  // (also orders the counters' clearing before the next ranks)
+      for (int j = tid; j < GT_WAVES * GT_NB; j += GT_THREADS) (&wcnt[0][0])[j] = 0;
+      __syncthreads();
     }
+    if (stable) break;
+    // the check: keys ascending, bags ascending among equal keys
+    bool broken = false;
 #pragma unroll
-    for (int k = 0; k < GC_ITEMS; ++k) {
-      const uint32_t r = (uint32_t)w * (GC_ITEMS * 64) + k * 64 + lane;
-      if (r < ns) {
-        key[k] = sk[r];
-        val[k] = sval[r];
+    for (int k = 0; k < ITEMS; ++k) {
+      const uint32_t pos = (uint32_t)w * (ITEMS * 64) + k * 64 + lane;
+      if (pos > 0 && pos < E && passes > 0) {
+        const uint32_t kp = sk[pos - 1], vp = sv[pos - 1];
+        broken = broken || kp > key[k] || (kp == key[k] && vp > val[k]);
       }
+    }
+    if (!__syncthreads_or(broken)) break;
+    if (tid == 0) {
+      s_max = 0;
+      s_sent = 0;
     }
     __syncthreads();
   }
+  // hot pairs of this table (keys below R, sorted first)
   uint32_t hc = 0;
-  const uint64_t o = (uint64_t)t * E + s0;
 #pragma unroll
-  for (int k = 0; k < GC_ITEMS; ++k) {
-    const uint32_t r = (uint32_t)w * (GC_ITEMS * 64) + k * 64 + lane;
-    if (r < ns) {
-      ck[o + r] = key[k];
-      cv[o + r] = val[k];
-      hc += key[k] < R ? 1u : 0u;
-    }
+  for (int k = 0; k < ITEMS; ++k) {
+    const uint32_t pos = (uint32_t)w * (ITEMS * 64) + k * 64 + lane;
+    hc += (pos < E && key[k] < R) ? 1u : 0u;
   }
   uint32_t h;
   (void)gt_scan(hc, scan_ws, &h);
-  if (tid == 0) {
-    hcnt[blockIdx.x] = h;
-    if (c == 0) {
-      lor[2 * t] = lo;
-      lor[2 * t + 1] = R;
-    }
-  }
-}
-
-// ----------------------------------------------------------------------------- merge
-__global__ void __launch_bounds__(GC_THREADS)
-gt_merge(const uint32_t* __restrict__ ck, const uint32_t* __restrict__ cv, int32_t T, uint32_t E, uint32_t C,
-         uint32_t n, uint32_t n_hot, int32_t stg_rows, const uint32_t* __restrict__ hcnt,
-         const uint32_t* __restrict__ lor, uint32_t* __restrict__ kout, uint32_t* __restrict__ vout, uint32_t* err,
-         hl_hook hk) {
-  extern __shared__ uint32_t lk[];  // the table's E sorted keys, chunk by chunk
-  __shared__ uint32_t scan_ws[GC_WAVES];
-  hl_hook_head(hk);  // a handover signal: the codes are complete (gt_chunk has ended)
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const uint32_t t = blockIdx.x / C, c = blockIdx.x - t * C;
-  const uint64_t tb = (uint64_t)t * E;
-  // the table's keys into LDS, 8 loads in flight per thread (tb is a multiple
-  // of 4 when E is: 16-byte loads then)
-  if ((E & 3) == 0) {
-    const uint4* src = reinterpret_cast<const uint4*>(ck + tb);
-    uint4* dst = reinterpret_cast<uint4*>(lk);
-    const uint32_t n4 = E >> 2;
-    for (uint32_t i0 = tid; i0 < n4; i0 += 8 * GC_THREADS) {
-      uint4 v[8];
-#pragma unroll
-      for (int u = 0; u < 8; ++u) v[u] = src[min(i0 + u * GC_THREADS, n4 - 1)];  // (all in flight)
-#pragma unroll
-      for (int u = 0; u < 8; ++u)
-        if (i0 + u * GC_THREADS < n4) dst[i0 + u * GC_THREADS] = v[u];
-    }
-  } else {
-    for (uint32_t i0 = tid; i0 < E; i0 += 8 * GC_THREADS) {
-      uint32_t v[8];
-#pragma unroll
-      for (int u = 0; u < 8; ++u) v[u] = ck[tb + min(i0 + u * GC_THREADS, E - 1)];
-#pragma unroll
-      for (int u = 0; u < 8; ++u)
-        if (i0 + u * GC_THREADS < E) lk[i0 + u * GC_THREADS] = v[u];
-    }
-  }
-  // the hot pairs of the earlier tables and of this one
-  uint32_t eh = 0, th = 0;
-  for (uint32_t q = tid; q < (t + 1) * C; q += GC_THREADS) {
-    const uint32_t x = hcnt[q];
-    if (q < t * C) eh += x;
-    else th += x;
-  }
-  uint32_t H, h;
-  (void)gt_scan(eh, scan_ws, &H);
-  (void)gt_scan(th, scan_ws, &h);  // (its barriers also order the LDS fill above)
-  const uint32_t lo = lor[2 * t], R = lor[2 * t + 1];
-  const uint32_t sent = R + (uint32_t)stg_rows;
-  const uint64_t NH = (uint64_t)t * E - H;          // the earlier tables' other pairs
-  const uint64_t nb0 = (uint64_t)n - NH - (E - h);  // this table's other pairs, before theirs
-  const uint32_t s0 = c * GC;
-  const uint32_t ns = min((uint32_t)GC, E - s0);
-  // rank in the table: the chunk's own, plus the other chunks' keys before it
-  uint32_t x[GC_ITEMS], g[GC_ITEMS];
-#pragma unroll
-  for (int k = 0; k < GC_ITEMS; ++k) {
-    const uint32_t r = (uint32_t)w * (GC_ITEMS * 64) + k * 64 + lane;
-    x[k] = r < ns ? lk[s0 + r] : 0u;
-    g[k] = r;
-  }
-  // a chunk's keys not above x if it precedes this one (lookup order), below
-  // x if it follows (keys are far below 2^32 - 1, so "not above x" is "below
-  // x + 1"): a fixed number of halving steps written without branches, the
-  // searches of the GC_ITEMS pairs interleaved
-  const uint32_t cu = __builtin_amdgcn_readfirstlane(c);
-  for (uint32_t c2 = 0; c2 < C; ++c2) {
-    if (c2 == cu) continue;
-    const uint32_t b0 = c2 * GC, n2 = min((uint32_t)GC, E - b0);
-    const uint32_t inc = c2 < cu ? 1u : 0u;
-    uint32_t pos[GC_ITEMS], xb[GC_ITEMS];
-#pragma unroll
-    for (int k = 0; k < GC_ITEMS; ++k) {
-      pos[k] = 0;
-      xb[k] = x[k] + inc;
-    }
-#pragma unroll
-    for (int e = 10; e >= 0; --e) {  // steps 1024 .. 1 (GC = 1024)
-      const uint32_t step = 1u << e;
-#pragma unroll
-      for (int k = 0; k < GC_ITEMS; ++k) {
-        const uint32_t m = pos[k] + step;
-        const uint32_t v = lk[b0 + min(m, n2) - 1];
-        const uint32_t take = (uint32_t)(m <= n2) & (uint32_t)(v < xb[k]);
-        pos[k] += take * step;
+  const uint32_t nh = E - h;
+  if (tid == 0)
+    __hip_atomic_store(tstat + t, GT_FLAG | ((uint64_t)nh << 32) | h, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  // the earlier tables' counts (each block publishes before it waits; the
+  // blocks of a grid start in index order and the grid fits the device, so
+  // the earlier tables' blocks run)
+  uint32_t eh = 0, enh = 0;
+  if (tid < (int)t) {
+    uint32_t spins = 0;
+    for (;;) {
+      const uint64_t x = __hip_atomic_load(tstat + tid, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if (x & GT_FLAG) {
+        eh = (uint32_t)x;
+        enh = (uint32_t)(x >> 32) & 0x7FFFFFFFu;
+        break;
       }
+      if (++spins > HL_SPIN_LIMIT) {
+        hl_flag(err, HL_DEVERR_STALL);
+        break;
+      }
+      __builtin_amdgcn_s_sleep(1);
     }
-#pragma unroll
-    for (int k = 0; k < GC_ITEMS; ++k) g[k] += pos[k];
   }
+  uint32_t H, NH;
+  (void)gt_scan(eh, scan_ws, &H);
+  (void)gt_scan(enh, scan_ws, &NH);
+  const uint64_t nb0 = (uint64_t)n - NH - nh;  // this table's non-hot pairs, before the earlier tables'
+  const uint32_t sent_key = max(s_max + 1, R);
 #pragma unroll
-  for (int k = 0; k < GC_ITEMS; ++k) {
-    const uint32_t r = (uint32_t)w * (GC_ITEMS * 64) + k * 64 + lane;
-    if (r >= ns) continue;
-    const uint32_t v = cv[tb + s0 + r];
-    uint64_t p;
+  for (int k = 0; k < ITEMS; ++k) {
+    const uint32_t pos = (uint32_t)w * (ITEMS * 64) + k * 64 + lane;
+    if (pos >= E) continue;
+    uint64_t o;
     uint32_t kk;
-    if (x[k] < R) {
-      p = (uint64_t)H + g[k];
-      kk = x[k] + lo;
+    if (pos < h) {
+      o = (uint64_t)H + pos;
+      kk = key[k] + lo;
     } else {
-      p = nb0 + (g[k] - h);
-      kk = x[k] >= sent ? EB_SENT : n_hot + (x[k] - R);
+      o = nb0 + (pos - h);
+      kk = key[k] >= sent_key ? EB_SENT : n_hot + (key[k] - R);
     }
-    if (p < n) {
-      kout[p] = kk;
-      vout[p] = v;
+    if (o < n) {
+      kout[o] = kk;
+      vout[o] = val[k];
     } else {
       hl_flag(err, HL_DEVERR_INTERNAL);
     }
@@ -371,7 +342,7 @@ gt_merge(const uint32_t* __restrict__ ck, const uint32_t* __restrict__ cv, int32
 bool hl_group_by_table_ok(const hl_handle* h, int64_t n_lookups, int64_t n_bags) {
   const int32_t T = h->n_tables;
   if (n_lookups != n_bags || n_bags == 0 || T > GT_TMAX || n_bags % T != 0) return false;
-  return n_bags / T <= (int64_t)GT_CMAX * GC;
+  return n_bags / T <= (int64_t)GT_IMAX * GT_THREADS;
 }
 
 hl_status hl_group_by_table(hl_handle* h, int32_t* codes, const int32_t* bag_ptr, int64_t n_bags, int32_t stg_rows,
@@ -379,20 +350,17 @@ hl_status hl_group_by_table(hl_handle* h, int32_t* codes, const int32_t* bag_ptr
                             uint32_t* sflag, uint32_t sv, const hl_cg_fused* cf, hipStream_t s) {
   const int32_t T = h->n_tables;
   const uint32_t E = (uint32_t)(n_bags / T);
-  const uint32_t C = hl_div_up(E, GC);
-  static_assert(HL_GROUP_SMALL >= GT_TMAX * GT_CMAX + 2 * GT_TMAX, "grouping counters");
-  uint32_t* hcnt = small;                     // [T * C]
-  uint32_t* lor = small + GT_TMAX * GT_CMAX;  // [2 T]
-  const size_t lds = (size_t)E * sizeof(uint32_t);
-  if (lds > 64 * 1024 &&
-      hipFuncSetAttribute((const void*)gt_merge, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess)
-    return HL_ERR_HIP;
-  const hl_hook hk = hl_hook_take(h);  // carried by gt_merge (the first sort pass takes it on the other path)
-  HL_KERNEL(h, s, "gt_chunk", gt_chunk, dim3(T * C), dim3(GC_THREADS), 0, s, codes, bag_ptr, n_bags, T, E, C,
-            h->n_hot, h->k_cap, stg_rows, h->d_tb, k_tm, v_tm, hcnt, lor,
-            n_bags, sflag, sv, h->d_err, cf ? *cf : hl_cg_fused{}, h->ballot_ranks);
-  HL_KERNEL(h, s, "gt_merge", gt_merge, dim3(T * C), dim3(GC_THREADS), lds, s, k_tm, v_tm, T, E,
-            C, (uint32_t)n_bags, h->n_hot, stg_rows, hcnt, lor, kout, vout, h->d_err, hk);
+  static_assert(HL_GROUP_SMALL >= 2 * GT_TMAX, "grouping words");
+  uint64_t* tstat = reinterpret_cast<uint64_t*>(small);  // [T], cleared by gt_prep
+  const hl_hook hk = hl_hook_take(h);  // carried by gt_sort (the first sort pass takes it on the other path)
+  HL_KERNEL(h, s, "gt_prep", gt_prep, dim3(hl_div_up(E, GT_S)), dim3(256), 0, s, codes, bag_ptr, n_bags, T, E,
+            h->n_hot, h->k_cap, stg_rows, k_tm, v_tm, tstat, n_bags, sflag, sv, h->d_err, cf ? *cf : hl_cg_fused{});
+#define GTS(I)                                                                                                    \
+  HL_KERNEL(h, s, "gt_sort", gt_sort<I>, dim3(T), dim3(GT_THREADS), 0, s, k_tm, v_tm, E, T, (uint32_t)n_bags,     \
+            h->d_tb, h->n_hot, kout, vout, tstat, h->d_err, h->ballot_ranks, hk)
+  if (E <= 4 * GT_THREADS) GTS(4);
+  else GTS(8);
+#undef GTS
   HL_LAUNCHED();
   return HL_OK;
 }
