@@ -41,13 +41,29 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def kernel_bytes(name, st):
-    """Algorithmic bytes of one launch of kernel `name` in the pipelined step
-    (per-step statistics st): each input read once, each output written once.
-    L lookups, nb bags, B samples, U distinct rows, C distinct cold rows, Lc
-    cold lookups, R bytes per stored row, O bytes per pooled output row."""
+def kernel_bytes(name, st, alone=False):
+    """Algorithmic bytes of one launch of kernel `name` (per-step statistics
+    st): each input read once, each output written once.  L lookups, nb bags,
+    B samples, U distinct rows, C distinct cold rows, Lc cold lookups, R bytes
+    per stored row, O bytes per pooled output row.  alone: the kernels of the
+    calls in order on one stream (the forward over every bag, the whole
+    backward: every distinct row read and written by the reduction), else
+    those of the pipelined step (hot and cold halves apart)."""
     L, nb, B, U, R, O = st["L"], st["n_bags"], st["B"], st["U"], st["R"], st["O"]
     C, Lc = st["n_cold"], st["Lc"]
+    if alone:
+        return {
+            # the forward over every bag: codes, offsets, each referenced row once, outputs
+            "eb_fwd": 4 * L + 4 * (nb + 1) + U * R + nb * O,
+            # grouping: codes and offsets in, table-major pairs out; the pairs in and out once more
+            "gt_prep": 4 * L + 4 * (nb + 1) + 8 * L,
+            "gt_sort": 16 * L,
+            "bw_prep_hist": 4 * L + 4 * (nb + 1) + 8 * L,
+            "srt_hist": 4 * L,
+            "srt_pass": 16 * L,
+            # reduction: sorted keys and bags, dY, each updated row read and written
+            "bw_reduce1": 8 * L + nb * O + 2 * U * R,
+        }.get(name)
     return {
         # rows, offsets, a bitmap word per lookup; gids, codes, flags, the two lists
         "ds_kernel": 4 * L + 4 * (nb + 1) + 8 * L + 8 * L + 5 * B,
@@ -57,11 +73,15 @@ def kernel_bytes(name, st):
         "cg_codes": 8 * Lc + 4 * C,
         # the host-link copy (also reported against the link's peak)
         "cg_fetch": 4 * C + 2 * C * R,
-        # grouping: keys and bags out, a histogram read, two passes of keys and bags in and out
+        # grouping: keys and bags out (with the fused plan's cold codes: a slot
+        # read and a code written per cold lookup), a histogram read, the
+        # pairs in and out per pass
         "bw_prep": 4 * L + 4 * (nb + 1) + 8 * L,
         "srt_hist": 4 * L,
-        "bw_prep_hist": 4 * L + 4 * (nb + 1) + 8 * L,
+        "bw_prep_hist": 4 * L + 4 * (nb + 1) + 8 * L + 8 * Lc,
         "srt_pass": 16 * L,
+        "gt_prep": 4 * L + 4 * (nb + 1) + 8 * L + 8 * Lc,
+        "gt_sort": 16 * L,
         # hot half of the forward over every bag: codes, offsets, each referenced row once, outputs
         "eb_fwd_hot": 4 * L + 4 * (nb + 1) + (U - C) * R + nb * O,
         # cold half: tail keys and bags, offsets, staging rows, outputs read and written
@@ -69,7 +89,8 @@ def kernel_bytes(name, st):
         # the same with the reduction's spanning segments (their partial sums are
         # workspace, not algorithmic bytes)
         "eb_tail_r2": 8 * Lc + 8 * Lc + C * R + 2 * Lc * O,
-        # reduction: sorted keys and bags, dY, each updated row read and written
+        # reduction: sorted keys and bags, dY, each updated hot row read and
+        # written, the staging rows' sums written
         "bw_reduce1": 8 * L + nb * O + 2 * (U - C) * R + C * O,
         "bw_cold": 4 * Lc + 2 * C * R + C * O,
     }.get(name)
@@ -129,6 +150,12 @@ def main():
     ap.add_argument("--repeats", type=int, default=20, help="more timed regions, for the spread of the step time")
     ap.add_argument("--breakdown", action="store_true", help="also time reference schedules and the stages")
     ap.add_argument("--no-relearn", action="store_true", help="skip the timed re-learning (hot-set migration)")
+    ap.add_argument("--fetch-study", action="store_true",
+                    help="sweep the hot-set size: popular share, cold rows, step time with and without write-back, "
+                         "and the share of the host-link fetch hidden under the forward and backward kernels")
+    ap.add_argument("--handover-kernels", action="store_true",
+                    help="time the steps with the handovers between streams as kernels of their own instead of "
+                         "inside the path's kernels (whose first block signals at the start and waits at the end)")
     ap.add_argument("--eal-study", action="store_true", help="compare the SRRIP logger with exact top-K on every workload")
     ap.add_argument("--pmc", action="store_true",
                     help="for a counter run under rocprofv3 --pmc: warmup + --steps steps of the same kernels on one "
@@ -166,7 +193,8 @@ def main():
     for i, b in zip(meas_idx, meas):
         dmeas.append(to_device(b, dev, W.make_dy(w, i, b.n_bags)))
     max_l = max(b.n_lookups for b in prof + meas)
-    hp = HotPath(w, rows, table, max_l, w.batch, device=dev)
+    # (the study's smaller hot sets leave up to every row of a mini-batch cold)
+    hp = HotPath(w, rows, table, max_l, w.batch, device=dev, staging_cap=max_l if args.fetch_study else None)
     log(f"[bench] inputs resident; workspace {hp.ws.numel() / 2**20:.1f} MiB, hot cache {k_cap} rows")
 
     # learning phase
@@ -183,8 +211,9 @@ def main():
         # serializes dispatches, which the pipelined schedule's cross-stream
         # waits would stall on), through the calls that launch the same kernel
         # variants as the pipelined step where the library has them: the hot
-        # half of the forward over every sample, the grouping's sort passes,
-        # the split reduction, the staging-row updates and the host-link copy
+        # half of the forward over every sample, the grouping, the split
+        # reduction, the staging-row updates and the host-link copy; then the
+        # forward and backward of the calls in order
         h = hp.h
         for i in range(args.warmup + args.steps):
             b = dmeas[i % len(dmeas)]
@@ -201,6 +230,11 @@ def main():
             hl.hl_embbag_fwd_part(h, hp.w_hot, hp.staging, cap, hp.codes, b.bag_ptr, B, bps, L, hp.nonpop,
                                   hp.counts[1:], B, hp.out, 2)
             hl.hl_embbag_bwd_apply_part(h, hp.w_hot, hp.staging, cap, B, bps, L, b.dY, w.lr, 2, hp.ws)
+            # the variants of the calls in order on one stream: the forward over
+            # every bag, the whole backward
+            hl.hl_embbag_fwd(h, hp.w_hot, hp.staging, cap, hp.codes, b.bag_ptr, B, bps, L, None, None, B, hp.out)
+            hl.hl_embbag_bwd_sgd(h, hp.w_hot, hp.staging, cap, hp.codes, b.bag_ptr, B, bps, L, None, None, B, b.dY,
+                                 w.lr, hp.ws)
         torch.cuda.synchronize()
         n_cal = 256 << 20
         src = torch.ones(n_cal // 4, dtype=torch.float32, device=dev)
@@ -238,9 +272,10 @@ def main():
     if err:
         raise SystemExit(f"device error word {err:#x} after the statistics pass")
     log("[bench] statistics pass done")
+    hk = args.handover_kernels
     with torch.cuda.stream(side):
         for i in range(args.warmup):
-            hp.step(dmeas[i % len(dmeas)], untied=True, next=ahead(i, args.warmup))
+            hp.step(dmeas[i % len(dmeas)], untied=True, next=ahead(i, args.warmup), handover_kernels=hk)
         hp.sync()
     torch.cuda.synchronize()
     log(f"[bench] warmup {args.warmup} steps done")
@@ -257,7 +292,7 @@ def main():
         t_start = time.perf_counter()
         start.record()  # the side stream is idle: the event completes before the first step is issued
         for i in range(K):
-            hp.step(dmeas[i % len(dmeas)], untied=True, next=ahead(i, K))
+            hp.step(dmeas[i % len(dmeas)], untied=True, next=ahead(i, K), handover_kernels=hk)
         host_ms = (time.perf_counter() - t_start) * 1e3
         hp.sync()
         stop.record()
@@ -275,7 +310,7 @@ def main():
         with torch.cuda.stream(side):
             start.record()
             for i in range(K):
-                hp.step(dmeas[i % len(dmeas)], untied=True, next=ahead(i, K))
+                hp.step(dmeas[i % len(dmeas)], untied=True, next=ahead(i, K), handover_kernels=hk)
             hp.sync()
             stop.record()
         torch.cuda.synchronize()
@@ -305,26 +340,48 @@ def main():
     torch.cuda.synchronize()
     copy_GBps = 10 * 2 * src.numel() * 4 / (e0.elapsed_time(e1) / 1e3) / 1e9
     del src, dst
+    # achievable host-link rate: a pinned host buffer copied to the device, of
+    # the cold rows' size per step and of 64 MiB
+    h2d_GBps = {}
+    for nbytes in (max(4096, int(np.mean([s["n_cold"] * s["R"] for s in stats]))), 64 << 20):
+        hsrc = torch.empty(nbytes, dtype=torch.uint8, pin_memory=True)
+        ddst = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+        ddst.copy_(hsrc, non_blocking=True)
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(10):
+            ddst.copy_(hsrc, non_blocking=True)
+        e1.record()
+        torch.cuda.synchronize()
+        h2d_GBps[str(nbytes)] = 10 * nbytes / (e0.elapsed_time(e1) / 1e3) / 1e9
+        del hsrc, ddst
+    log(f"[bench] pinned host-to-device copies: " + ", ".join(f"{k} B {v:.1f} GB/s" for k, v in h2d_GBps.items()))
 
     steps_stats = [stats[i % len(stats)] for i in range(K)]
     avg = {k: float(np.mean([s[k] for s in steps_stats])) for k in steps_stats[0]}
     L_tot = sum(s["L"] for s in steps_stats)
     value = L_tot / (total_ms / 1e3)
 
-    def look_ahead_steps():
+    def look_ahead_steps(hk):
         with torch.cuda.stream(side):
             for i in range(K):
-                hp.step(dmeas[i % len(dmeas)], untied=True, next=ahead(i, K))
+                hp.step(dmeas[i % len(dmeas)], untied=True, next=ahead(i, K), handover_kernels=hk)
             hp.sync()
         torch.cuda.synchronize()
 
-    def traced(only):
-        """K look-ahead steps with HIP events around every kernel named `only`
-        (None: every kernel) on the stream it is launched on; per name: launches
-        and total ms."""
+    def sequential_steps():
+        with torch.cuda.stream(side):
+            for i in range(K):
+                hp.step(dmeas[i % len(dmeas)], mode="sequential", split_fwd=False)
+        torch.cuda.synchronize()
+
+    def traced(run, only):
+        """K steps of `run` with every kernel named `only` (None: every kernel)
+        timed by its own dispatch (events that the launch itself records);
+        per name: launches and total ms."""
         hl.hl_trace_enable(hp.h, 64 * K + 64)
         hl.hl_trace_only(hp.h, only)
-        look_ahead_steps()
+        run()
         kern = {}
         for i in range(hl.hl_trace_count(hp.h)):
             name, ms = hl.hl_trace_read(hp.h, i)
@@ -333,66 +390,88 @@ def main():
             k[1] += ms
         hl.hl_trace_only(hp.h, None)
         hl.hl_trace_enable(hp.h, 0)
+        err = hp.device_error()
+        if err:
+            raise SystemExit(f"device error word {err:#x} in a traced pass")
         return kern
 
-    # per-kernel durations in the timed configuration: which kernels run (events
-    # around all of them), then each kernel timed alone (events around its
-    # launches only, so the others run as in the timed region)
-    names = list(traced(None))
-    kernels = {}
-    for n in names:
-        c, t = traced(n)[n]
-        kernels[n] = {"launches_per_step": c / K, "ms_per_step": t / K, "avg_us": 1e3 * t / c}
-        kb = kernel_bytes(n, avg)
-        if kb is not None:
-            kernels[n]["algorithmic_GBps"] = kb / (kernels[n]["avg_us"] * 1e-6) / 1e9
-    kernels = dict(sorted(kernels.items(), key=lambda x: -x[1]["ms_per_step"]))
-    log("[bench] per-kernel times: " + ", ".join(f"{n} {k['avg_us']:.1f}us x{k['launches_per_step']:.0f}"
-                                               for n, k in kernels.items()))
+    def per_kernel(run, alone):
+        """which kernels run (all traced), then each name traced alone"""
+        kern = {}
+        for n in traced(run, None):
+            c, t = traced(run, n)[n]
+            kern[n] = {"launches_per_step": c / K, "ms_per_step": t / K, "avg_us": 1e3 * t / c}
+            kb = kernel_bytes(n, avg, alone)
+            if kb is not None:
+                kern[n]["algorithmic_GBps"] = kb / (kern[n]["avg_us"] * 1e-6) / 1e9
+        return dict(sorted(kern.items(), key=lambda x: -x[1]["ms_per_step"]))
+
+    def fmt(kern):
+        return ", ".join(f"{n} {k['avg_us']:.1f}us x{k['launches_per_step']:.0f}" for n, k in kern.items())
+
+    # per-kernel durations: in the timed schedule (with the handovers inside
+    # the kernels, a kernel's duration includes its waits for the other
+    # streams), in the same schedule with the handovers as kernels of their
+    # own (each kernel's own work, beside the other streams' kernels), and in
+    # the calls in order on one stream (each kernel alone on the whole GPU)
+    kernels_timed = per_kernel(lambda: look_ahead_steps(hk), False)
+    log("[bench] per-kernel times, timed schedule: " + fmt(kernels_timed))
+    kernels = kernels_timed if hk else per_kernel(lambda: look_ahead_steps(True), False)
+    if not hk:
+        log("[bench] per-kernel times, handovers as kernels: " + fmt(kernels))
+    kernels_alone = per_kernel(sequential_steps, True)
+    log("[bench] per-kernel times, alone: " + fmt(kernels_alone))
 
     # the embedding forward and backward: their kernels' time per step (the
     # grouping included), against the algorithmic bytes of both passes
-    fb_kernels = ("eb_fwd_hot", "eb_fwd_tail", "eb_tail_r2", "bw_prep", "bw_prep_hist", "srt_hist", "srt_pass",
-                  "bw_reduce1", "bw_reduce2", "bw_cold")
+    fb_kernels = ("eb_fwd", "eb_fwd_hot", "eb_fwd_tail", "eb_tail_r2", "bw_prep", "bw_prep_hist", "srt_hist",
+                  "srt_pass", "gt_prep", "gt_sort", "bw_reduce1", "bw_reduce2", "bw_cold")
     t_fb = sum(kernels[n]["ms_per_step"] for n in fb_kernels if n in kernels)
+    t_fb_alone = sum(kernels_alone[n]["ms_per_step"] for n in fb_kernels if n in kernels_alone)
     fwd_b = 4 * avg["L"] + 4 * (avg["n_bags"] + 1) + avg["U"] * avg["R"] + avg["n_bags"] * avg["O"]
     bwd_b = 4 * avg["L"] + 4 * (avg["n_bags"] + 1) + avg["n_bags"] * avg["O"] + 2 * avg["U"] * avg["R"]
     fb_frac = (fwd_b + bwd_b) / (t_fb / 1e3) / HBM_PEAK
+    fb_frac_alone = (fwd_b + bwd_b) / (t_fb_alone / 1e3) / HBM_PEAK
 
-    # roofline of the dominant HBM-bound kernel by time per step: the forward's
-    # hot half and the backward's reduction move the path's bytes; the host-link
-    # copy is reported against the link, and the grouping's sort passes, the
-    # cold-row kernels and the dispatch are latency-bound at these sizes (the
-    # dispatch kernel's blocks also start by waiting for the steps that last
-    # used its buffers).  The dominant kernel overall is named beside it.
-    hbm_kernels = ("eb_fwd_hot", "bw_reduce1", "bw_reduce2")
-    dom = next(n for n in kernels if n in hbm_kernels)
+    # roofline of the dominant HBM-bound kernel of the forward and backward,
+    # by time per step alone on the GPU (its own work, no wait for another
+    # stream inside it; rocprofv3 sees these launches under their own kernel
+    # names, apart from the pipelined step's variants): the forward and the
+    # backward's reduction move the path's bytes; the grouping is
+    # latency-bound at these sizes.  Then the same for the timed schedule's
+    # dominant HBM-bound kernel, from the pass with its handovers as kernels
+    # of their own (beside the other streams' kernels, on the main stream's
+    # compute units), and the dominant kernel overall.
+    def roofline(kern, names, alone):
+        dom = next(n for n in kern if n in names)
+        kd = kern[dom]
+        ab = kernel_bytes(dom, avg, alone)
+        if ab is None:
+            raise SystemExit(f"no byte model for the dominant kernel {dom}")
+        ach = ab / (kd["avg_us"] * 1e-6)
+        # measured HBM bytes per launch (counters, same kernel source), as a
+        # rate over the same launch duration as `achieved`
+        tb = counter_traffic(dom, w.name, alone)
+        return {"kernel": dom, "bound": "hbm", "achieved": ach / 1e9, "peak": HBM_PEAK / 1e9, "unit": "GB/s",
+                "frac": ach / HBM_PEAK, "traffic": None if tb is None else tb / (kd["avg_us"] * 1e-6) / 1e9,
+                "traffic_bytes_per_launch": tb, "avg_us": kd["avg_us"], "algorithmic_bytes_per_launch": ab,
+                "schedule": "alone" if alone else "timed, handovers as kernels"}
+    roof = roofline(kernels_alone, ("eb_fwd", "bw_reduce1", "bw_reduce2"), True)
+    roof_timed = roofline(kernels, ("eb_fwd_hot", "bw_reduce1", "bw_reduce2"), False)
     dom_all = next(n for n in kernels if n not in ("cg_fetch", "cg_scatter"))
-    if kernel_bytes(dom, avg) is None:
-        raise SystemExit(f"no byte model for the dominant kernel {dom}")
-    kd = kernels[dom]
-    ach = kernel_bytes(dom, avg) / (kd["avg_us"] * 1e-6)
-    # measured HBM bytes per launch (counters, same kernel source), as a rate
-    # over the same launch duration as `achieved`
-    tb = counter_traffic(dom, w.name)
-    roof = {"kernel": dom, "bound": "hbm", "achieved": ach / 1e9, "peak": HBM_PEAK / 1e9, "unit": "GB/s",
-            "frac": ach / HBM_PEAK, "traffic": None if tb is None else tb / (kd["avg_us"] * 1e-6) / 1e9,
-            "traffic_bytes_per_launch": tb, "avg_us": kd["avg_us"],
-            "algorithmic_bytes_per_launch": kernel_bytes(dom, avg),
-            "dominant_kernel_overall": {"kernel": dom_all, "ms_per_step": kernels[dom_all]["ms_per_step"],
-                                        "bound": "hbm" if dom_all in hbm_kernels else "latency"}}
+    roof_timed["dominant_kernel_overall"] = {"kernel": dom_all, "ms_per_step": kernels[dom_all]["ms_per_step"]}
     link = None
     if "cg_fetch" in kernels:
         gb = avg["n_cold"] * avg["R"]
         link = {"kernel": "cg_fetch", "bytes_per_launch": gb, "avg_us": kernels["cg_fetch"]["avg_us"],
-                "achieved_GBps": gb / (kernels["cg_fetch"]["avg_us"] * 1e-6) / 1e9, "peak_GBps": LINK_PEAK / 1e9}
+                "achieved_GBps": gb / (kernels["cg_fetch"]["avg_us"] * 1e-6) / 1e9, "peak_GBps": LINK_PEAK / 1e9,
+                "measured_pinned_copy_GBps": h2d_GBps}
 
-    # the same batches through the library's calls in order on one stream, each
-    # stage alone on the whole GPU (events between the stages): the forward and
-    # backward without the host-link copy and the plans running beside them
-    # Events only at the edges of the spans timed (a pair of events adds a few
-    # microseconds of its own: the stages' pass below has an empty span), then
-    # one pass with events between every stage.
+    # the same batches through the library's calls in order on one stream: the
+    # spans of classify+partition and of fwd+bwd between events (launch gaps
+    # included), then one pass with events between every stage.  Events only
+    # at the edges of the spans timed (a pair of events adds a few
+    # microseconds of its own: the stages' pass below has an empty span).
     from paper_2204_05436_amd.runner import STAGES
     ix = {s: j for j, s in enumerate(STAGES)}
     edges = (ix["classify"], ix["remap"], ix["fwd_pop"], len(STAGES))  # classify+partition, fwd+bwd
@@ -418,16 +497,23 @@ def main():
     t_fb1 = sum(e[edges[2]].elapsed_time(e[edges[3]]) for e in ev) / K
     ev = seq_pass(range(len(STAGES) + 1))
     st = {s: sum(ev[i][j].elapsed_time(ev[i][j + 1]) for i in range(K)) / K for j, s in enumerate(STAGES)}
-    alone = {"fwd_bwd_us": t_fb1 * 1e3, "fwd_bwd_lookups_per_s": avg["L"] / (t_fb1 / 1e3),
-             "fwd_bwd_hbm_frac": (fwd_b + bwd_b) / (t_fb1 / 1e3) / HBM_PEAK,
+    cl_kern = ("hl_k_gids", "cl_kernel", "pt_count", "pt_scan", "pt_emit")
+    t_cl_alone = sum(kernels_alone[n]["ms_per_step"] for n in cl_kern if n in kernels_alone)
+    alone = {"fwd_bwd_kernel_us": t_fb_alone * 1e3, "fwd_bwd_lookups_per_s": avg["L"] / (t_fb_alone / 1e3),
+             "fwd_bwd_hbm_frac": fb_frac_alone,
+             "fwd_bwd_span_us": t_fb1 * 1e3, "fwd_bwd_span_hbm_frac": (fwd_b + bwd_b) / (t_fb1 / 1e3) / HBM_PEAK,
              # every lookup's row counted (no coalescing): fwd L R + n O, bwd n O + 2 L R
-             "lookup_equivalent_GBps": (3 * avg["L"] * avg["R"] + 2 * avg["n_bags"] * avg["O"]) / (t_fb1 / 1e3) / 1e9,
+             "lookup_equivalent_GBps": (3 * avg["L"] * avg["R"] + 2 * avg["n_bags"] * avg["O"]) / (t_fb_alone / 1e3)
+             / 1e9,
              "achievable_copy_GBps": copy_GBps,
-             "classify_partition_us": t_cp * 1e3, "classify_samples_per_s": avg["B"] / (t_cp / 1e3),
+             "classify_partition_kernel_us": t_cl_alone * 1e3,
+             "classify_samples_per_s": avg["B"] / (t_cl_alone / 1e3) if t_cl_alone else None,
+             "classify_partition_span_us": t_cp * 1e3,
              "stage_ms_events_between_every_stage": st,
-             "empty_span_us": st["fwd_nonpop"] * 1e3}
-    log(f"[bench] alone on the GPU: fwd+bwd {t_fb1 * 1e3:.1f} us ({alone['fwd_bwd_hbm_frac']:.3f} of the HBM "
-        f"peak), classify+partition {t_cp * 1e3:.1f} us; stages " +
+             "empty_span_us": st["fwd_nonpop"] * 1e3,
+             "kernels": kernels_alone}
+    log(f"[bench] alone on the GPU: fwd+bwd kernels {t_fb_alone * 1e3:.1f} us ({fb_frac_alone:.3f} of the HBM "
+        f"peak; span {t_fb1 * 1e3:.1f} us), classify+partition kernels {t_cl_alone * 1e3:.1f} us; stages " +
         ", ".join(f"{s} {v * 1e3:.1f}us" for s, v in st.items()))
 
     breakdown = None
@@ -446,6 +532,35 @@ def main():
     if args.eal_study:
         eal_all = {}
         eal_study(eal_all)
+
+    # the timed region again with the write-back of the updated cold rows to
+    # the host table (on the fetch stream after each step; the next plans and
+    # fetches of those rows wait for it)
+    def timed_steps(n):
+        with torch.cuda.stream(side):
+            start.record()
+            for i in range(n):
+                hp.step(dmeas[i % len(dmeas)], untied=True, next=ahead(i, n), handover_kernels=hk)
+            hp.sync()
+            stop.record()
+        torch.cuda.synchronize()
+        err = hp.device_error()
+        if err:
+            raise SystemExit(f"device error word {err:#x} in a timed region")
+        return start.elapsed_time(stop) / n
+
+    hp.writeback = True
+    timed_steps(args.warmup)
+    wb_ms = float(np.median([timed_steps(K) for _ in range(5)]))
+    wb_kern = traced(lambda: look_ahead_steps(hk), "cg_scatter").get("cg_scatter", [0, 0.0])
+    hp.writeback = False
+    write_back = {"ms_per_step": wb_ms, "lookups_per_s": L_tot / K / (wb_ms / 1e3),
+                  "cg_scatter_avg_us": 1e3 * wb_kern[1] / max(1, wb_kern[0]),
+                  "bytes_per_step": avg["n_cold"] * avg["R"]}
+    log(f"[bench] with write-back: {wb_ms:.4f} ms per step (without {total_ms / K:.4f}), write-back copy "
+        f"{write_back['cg_scatter_avg_us']:.1f} us")
+
+    study = fetch_study(hp, w, dprof, dmeas, side, K, ahead, traced, look_ahead_steps) if args.fetch_study else None
 
     relearn = None
     if not args.no_relearn:
@@ -483,35 +598,127 @@ def main():
                     "plans (dispatch, cold plan, grouping of the next mini-batch, during the step before) on 64, "
                     "the forwards and the backward on the other 184",
         "host_enqueue_ms_per_step": host_ms / K,
+        "handovers": "kernels" if hk else "inline",
+        # the forward and backward kernels' own work per step in the timed
+        # schedule (handovers as kernels), and against their time alone
         "fwd_bwd_kernel_us": t_fb * 1e3,
+        "fwd_bwd_timed_over_alone": t_fb / t_fb_alone,
         "fwd_bwd_lookups_per_s": avg["L"] / (t_fb / 1e3),
         "fwd_bwd_hbm_frac": fb_frac,
         "fwd_bwd_algorithmic_bytes": fwd_b + bwd_b,
         "alone_on_gpu": alone,
         # the dispatch kernel classifies, partitions and remaps a mini-batch
+        # the dispatch kernel's own work (classify, partition, remap of a mini-batch)
         "classify_samples_per_s": avg["B"] / (kernels["ds_kernel"]["avg_us"] * 1e-6),
+        "classify_kernel_us": kernels["ds_kernel"]["avg_us"],
         "popular_fraction": avg["n_pop"] / avg["B"],
         "unique_rows_per_batch": avg["U"], "cold_rows_per_batch": avg["n_cold"],
-        "learning_phase_ms": learn_ms, "kernels": kernels,
-        "roofline": roof, "link_roofline": link, "cpu_baseline": cpu, "breakdown": breakdown, "relearn": relearn,
+        "learning_phase_ms": learn_ms, "kernels": kernels, "kernels_timed_schedule": kernels_timed,
+        "roofline": roof, "roofline_timed_schedule": roof_timed, "link_roofline": link, "cpu_baseline": cpu, "breakdown": breakdown, "relearn": relearn,
         "srrip_logger": eal, "srrip_logger_all_workloads": eal_all,
+        "write_back": write_back, "fetch_study": study,
     }
     print(json.dumps(res), flush=True)
     hp.close()
     table.close()
 
 
-def counter_traffic(kernel, workload):
-    """HBM bytes per launch of `kernel` from the committed counter summary
-    (profiles/<workload>_kernel_traffic.md: FETCH_SIZE and WRITE_SIZE runs,
-    calibrated with a copy of known size), or None when there is none or the
-    kernel's source file has changed since the counters were taken."""
+# the main stream's kernels of a planned step: the forwards and the backward
+MAIN_KERNELS = ("eb_fwd_hot", "eb_fwd_cold", "eb_fwd_tail", "eb_tail_r2", "bw_reduce1", "bw_reduce2", "bw_cold")
+
+
+def fetch_overlap(hp, run):
+    """One traced run (every kernel, start and end on one time line): the
+    host-link fetch's time per launch and the shares of it during which a
+    main-stream kernel (the forwards and the backward), or any other kernel,
+    ran."""
+    from paper_2204_05436_amd import hotline as hl
+    hl.hl_trace_enable(hp.h, 1 << 16)
+    hl.hl_trace_only(hp.h, None)
+    run()
+    recs = [hl.hl_trace_read_at(hp.h, i) for i in range(hl.hl_trace_count(hp.h))]
+    hl.hl_trace_enable(hp.h, 0)
+
+    def union(iv):
+        out = []
+        for a, b in sorted(iv):
+            if out and a <= out[-1][1]:
+                out[-1][1] = max(out[-1][1], b)
+            else:
+                out.append([a, b])
+        return out
+
+    def covered(f, u):
+        return sum(max(0.0, min(f[1], b) - max(f[0], a)) for a, b in u)
+    fetch = [(t0, t0 + d) for n, t0, d in recs if n == "cg_fetch"]
+    main = union([(t0, t0 + d) for n, t0, d in recs if n in MAIN_KERNELS])
+    other = union([(t0, t0 + d) for n, t0, d in recs if n not in ("cg_fetch", "cg_scatter")])
+    tf = sum(b - a for a, b in fetch)
+    return {"fetch_us": 1e3 * tf / max(1, len(fetch)),
+            "hidden_under_fwd_bwd": sum(covered(f, main) for f in fetch) / tf if tf else None,
+            "hidden_under_any_kernel": sum(covered(f, other) for f in fetch) / tf if tf else None}
+
+
+def fetch_study(hp, w, dprof, dmeas, side, K, ahead, traced, look_ahead_steps):
+    """Hot sets of 1/32 ... all of the rows the profiling batches touched
+    (up to the cache's capacity): per size the popular share of samples, the
+    cold rows per mini-batch, the step time without and with write-back, and
+    the share of the fetch hidden under the forward and backward kernels
+    (Sec. VII-F: the popular share decides how much of the gather the
+    pipeline hides)."""
+    import torch
+    n_full = hp.learn(dprof)
+    out = []
+    for frac in (1 / 32, 1 / 8, 1 / 4, 1 / 2, 1):
+        k = max(1, int(n_full * frac))
+        n_hot = hp.learn(dprof, k=k)
+        pops, colds = [], []
+        for j, b in enumerate(dmeas[:8]):
+            with torch.cuda.stream(side):
+                hp.step(b)
+            torch.cuda.synchronize()
+            c = hp.counts.cpu().numpy()
+            pops.append(c[0] / b.n_samples)
+            colds.append(int(hp.n_cold.item()))
+        ms = {}
+        for wb in (False, True):
+            hp.writeback = wb
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            look_ahead_steps(False)
+            with torch.cuda.stream(side):
+                e0.record()
+                for i in range(K):
+                    hp.step(dmeas[i % len(dmeas)], untied=True, next=ahead(i, K))
+                hp.sync()
+                e1.record()
+            torch.cuda.synchronize()
+            ms["with_write_back" if wb else "no_write_back"] = e0.elapsed_time(e1) / K
+        hp.writeback = False
+        ov = fetch_overlap(hp, lambda: look_ahead_steps(False))
+        err = hp.device_error()
+        if err:
+            raise SystemExit(f"device error word {err:#x} in the fetch study")
+        row = {"hot_rows": n_hot, "popular_share": float(np.mean(pops)), "cold_rows_per_batch": float(np.mean(colds)),
+               "ms_per_step": ms, **ov}
+        log(f"[bench] fetch study: {row}")
+        out.append(row)
+    hp.learn(dprof)
+    return out
+
+
+def counter_traffic(kernel, workload, alone=False):
+    """HBM bytes per launch of `kernel` (alone: its variant in the calls in
+    order on one stream, else the pipelined step's) from the committed
+    counter summary (profiles/<workload>_kernel_traffic.md: FETCH_SIZE and
+    WRITE_SIZE runs, calibrated with a copy of known size), or None when there
+    is none or the kernel's source file has changed since the counters were
+    taken."""
     here = os.path.dirname(os.path.abspath(__file__))
     path = os.path.join(here, "profiles", f"{workload}_kernel_traffic.md")
     if not os.path.exists(path):
         return None
     text = open(path).read()
-    m = re.search(r"```traffic\n(.*?)```", text, re.S)
+    m = re.search(r"```traffic_alone\n(.*?)```" if alone else r"```traffic\n(.*?)```", text, re.S)
     if not m:
         return None
     for line in m.group(1).splitlines():

@@ -388,16 +388,19 @@ hl_status hl_last_device_error(hl_handle* h, uint32_t* err_out);
 
 /* ---------------------------------------------------------------- tracing --
  * Per-kernel timing with HIP events.  hl_trace_enable(h, cap) creates cap
- * event pairs and records one pair around every kernel the handle's calls
- * launch (until cap records exist); cap = 0 turns tracing off.  hl_trace_read
- * waits for record i and returns its kernel name (static string) and
- * duration in ms.  hl_trace_reset forgets the records.  hl_trace_only(h,
- * name) records only kernels of that name (NULL: all again), so one kernel
- * can be timed without events around all the others. */
+ * event pairs, and every kernel the handle's calls launch (until cap records
+ * exist) is launched so that its dispatch records the pair at its own start
+ * and end (no marker packets on the stream); cap = 0 turns tracing off.
+ * hl_trace_read waits for record i and returns its kernel name (static
+ * string) and duration in ms; hl_trace_read_at also gives its start in ms
+ * after record 0's start (records on several streams on one time line).
+ * hl_trace_reset forgets the records.  hl_trace_only(h, name) records only
+ * kernels of that name (NULL: all again). */
 hl_status hl_trace_enable(hl_handle* h, int32_t cap);
 hl_status hl_trace_only(hl_handle* h, const char* name);
 int32_t hl_trace_count(const hl_handle* h);
 hl_status hl_trace_read(const hl_handle* h, int32_t i, const char** name, float* ms);
+hl_status hl_trace_read_at(const hl_handle* h, int32_t i, const char** name, float* start_ms, float* ms);
 hl_status hl_trace_reset(hl_handle* h);
 
 /* ---------------------------------------------------------------- streams --
@@ -468,6 +471,14 @@ typedef struct hl_step_io {
  * codes, flags, pop_ids, nonpop_ids, counts, cold_ids, n_cold, workspace);
  * the step skips them.  HL_ERR_INVALID_ARG if no such plan is pending. */
 #define HL_STEP_PLANNED 2u
+/* Step flag (also read by hl_pipeline_plan): the waits of the handovers
+ * between the pipeline's streams run in kernels of their own, launched around
+ * the calls, instead of inside the path's kernels (whose first block otherwise
+ * waits as the kernel ends, or every block as it starts).  Same order, same
+ * results, a few more launches; the path's kernels then hold no waits, so
+ * their durations are their own work (for timing them in the pipelined
+ * schedule). */
+#define HL_STEP_HANDOVER_KERNELS 4u
 /* fetch_cus compute units [0, fetch_cus) run the host-link copy (0: no masks
  * at all); plan_cus > 0 gives the look-ahead plans the next plan_cus units of
  * their own (0: they share main's).  Masks in multiples of 8 units keep every

@@ -47,18 +47,15 @@ static hl_status fill32(uint32_t* p, uint64_t n, uint32_t v, hipStream_t s) {
 hl_status hl_fill32(uint32_t* p, uint64_t n, uint32_t v, hipStream_t s) { return fill32(p, n, v, s); }
 
 // ----------------------------------------------------------------------------- tracing
-int hl_trace_begin(const hl_handle* h, hipStream_t s, const char* name) {
+int hl_trace_take(const hl_handle* h, const char* name, hipEvent_t* a, hipEvent_t* b) {
   hl_trace* t = h ? h->trace : nullptr;
   if (!t || t->n >= t->cap) return -1;
   if (t->only[0] && strcmp(t->only, name) != 0) return -1;
   const int i = t->n++;
   t->rec[i].name = name;
-  if (hipEventRecord(t->rec[i].a, s) != hipSuccess) return -1;
+  *a = t->rec[i].a;
+  *b = t->rec[i].b;
   return i;
-}
-
-void hl_trace_end(const hl_handle* h, hipStream_t s, int idx) {
-  if (idx >= 0) (void)hipEventRecord(h->trace->rec[idx].b, s);
 }
 
 static void trace_free(hl_trace* t) {
@@ -105,6 +102,16 @@ extern "C" hl_status hl_trace_read(const hl_handle* h, int32_t i, const char** n
   HL_HIP(hipEventSynchronize(h->trace->rec[i].b));
   HL_HIP(hipEventElapsedTime(ms, h->trace->rec[i].a, h->trace->rec[i].b));
   *name = h->trace->rec[i].name;
+  return HL_OK;
+}
+
+extern "C" hl_status hl_trace_read_at(const hl_handle* h, int32_t i, const char** name, float* start_ms,
+                                      float* ms) {
+  if (!h || i < 0 || i >= h->trace->n || !name || !start_ms || !ms) return HL_ERR_INVALID_ARG;
+  const hl_status st = hl_trace_read(h, i, name, ms);
+  if (st != HL_OK) return st;
+  HL_HIP(hipEventSynchronize(h->trace->rec[0].a));
+  HL_HIP(hipEventElapsedTime(start_ms, h->trace->rec[0].a, h->trace->rec[i].a));
   return HL_OK;
 }
 

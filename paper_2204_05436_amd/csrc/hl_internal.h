@@ -1,6 +1,7 @@
 // Internal declarations shared by the HIP sources of libhotline (not installed).
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -18,15 +19,22 @@ struct hl_trace {
   hl_trace_rec* rec = nullptr;
   char only[64] = {0};  // record only kernels of this name (empty: all)
 };
-// Index of the record opened for kernel `name` on stream s, or -1.
-int hl_trace_begin(const struct hl_handle* h, hipStream_t s, const char* name);
-void hl_trace_end(const struct hl_handle* h, hipStream_t s, int idx);
-#define HL_KERNEL(h, s, name, ...)                  \
-  do {                                              \
-    int _ti = hl_trace_begin((h), (s), (name));     \
-    hipLaunchKernelGGL(__VA_ARGS__);                \
-    hl_trace_end((h), (s), _ti);                    \
-  } while (0)
+// A record for kernel `name` (its two events in *a, *b), or -1 when none is
+// taken (tracing off, full, or another name selected).
+int hl_trace_take(const struct hl_handle* h, const char* name, hipEvent_t* a, hipEvent_t* b);
+// A kernel launch; when traced, through the launch that has the dispatch
+// itself record its start and end in the record's events (the kernel's own
+// duration: no marker packets before and after it on the stream).
+template <typename F, typename... A>
+static inline void hl_launch(const struct hl_handle* h, const char* name, F kernel, dim3 grid, dim3 block,
+                             uint32_t shmem, hipStream_t s, A... args) {
+  hipEvent_t a, b;
+  if (hl_trace_take(h, name, &a, &b) >= 0)
+    hipExtLaunchKernelGGL(kernel, grid, block, shmem, s, a, b, 0u, args...);
+  else
+    hipLaunchKernelGGL(kernel, grid, block, shmem, s, args...);
+}
+#define HL_KERNEL(h, s, name, ...) hl_launch((h), (name), __VA_ARGS__)
 
 // ----------------------------------------------------------------------------- handle
 // A workspace holding a backward plan (grouping) for a later apply step.

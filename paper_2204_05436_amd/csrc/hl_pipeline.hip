@@ -124,6 +124,7 @@ struct hl_pipeline {
   uint32_t wb_seq[8];     // (a list not among them was last written back before all of these)
   int wb_next;
   bool use_flags;         // handovers through device flags (masked streams)
+  bool sep_hand;          // this call's handovers as kernels of their own (HL_STEP_HANDOVER_KERNELS)
   hipEvent_t ev[PF_N];    // the same handovers as events (pipelines without masks)
   hipEvent_t ev_in, ev_out, ev_pin, ev_plan, ev_f, ev_g;
   const void* stg_ptr[4]; // staging buffers of recent steps, and the last step that used each
@@ -264,15 +265,47 @@ static hl_status pl_unhook(hl_pipeline* p, hipStream_t s) {
                      p->h->d_err);
   return hipGetLastError() == hipSuccess ? HL_OK : HL_ERR_HIP;
 }
-// a call on stream s with the handover set by pl_hook (dropped if the call fails)
-#define PL_HOOKED(s, call)              \
-  do {                                  \
-    const hl_status _st = (call);       \
-    if (_st != HL_OK) {                 \
-      (void)hl_hook_take(p->h);         \
-      return _st;                       \
-    }                                   \
-    HL_TRY(pl_unhook(p, (s)));          \
+// HL_STEP_HANDOVER_KERNELS: the waits of the handover set by pl_hook taken
+// out of the call on stream s.  A gate's waits (and its signal) go into a
+// pl_hand launched now, before the call; otherwise the signal stays with the
+// kernel that takes the handover (not always the call's first: the grouping's
+// sort gives the plan's signal once its first kernel has completed the codes)
+// and the waits go into *rest, for pl_unhook after the call.
+static hl_status pl_hand_split(hl_pipeline* p, hipStream_t s, hl_hook* rest) {
+  hl_hook& k = p->h->hook;
+  *rest = hl_hook{};
+  if (!k.gate) {
+    rest->wflag = k.wflag;
+    rest->wv = k.wv;
+    rest->w2flag = k.w2flag;
+    rest->w2v = k.w2v;
+    rest->err = k.err;
+    k.wflag = k.w2flag = nullptr;
+    return HL_OK;
+  }
+  const hl_hook g = hl_hook_take(p->h);
+  if (!g.sflag && !g.wflag && !g.w2flag) return HL_OK;
+  hipLaunchKernelGGL(pl_hand, dim3(1), dim3(64), 0, s, g.sflag, g.sv, g.wflag, g.wv, g.w2flag, g.w2v, nullptr, 0u,
+                     p->h->d_err);
+  return hipGetLastError() == hipSuccess ? HL_OK : HL_ERR_HIP;
+}
+// a call on stream s with the handover set by pl_hook (dropped if the call
+// fails); what no kernel of the call took is enqueued after it
+#define PL_HOOKED(s, call)                                    \
+  do {                                                        \
+    hl_hook _rest{};                                          \
+    if (p->sep_hand) HL_TRY(pl_hand_split(p, (s), &_rest));   \
+    const hl_status _st = (call);                             \
+    if (_st != HL_OK) {                                       \
+      (void)hl_hook_take(p->h);                               \
+      return _st;                                             \
+    }                                                         \
+    if (p->sep_hand) {                                        \
+      _rest.sflag = p->h->hook.sflag; /* (a signal not taken) */ \
+      _rest.sv = p->h->hook.sv;                               \
+      p->h->hook = _rest;                                     \
+    }                                                         \
+    HL_TRY(pl_unhook(p, (s)));                                \
   } while (0)
 
 // the pending signals, enqueued alone
@@ -403,6 +436,7 @@ extern "C" hl_status hl_pipeline_plan(hl_pipeline* p, const hl_step_io* io, hl_s
   if (!p->use_flags) return HL_ERR_UNSUPPORTED;
   HL_TRY(pl_not_capturing((hipStream_t)stream));
   if (pl_pending(p, io->workspace)) return HL_ERR_INVALID_ARG;  // that plan has not been stepped yet
+  p->sep_hand = io->step_flags & HL_STEP_HANDOVER_KERNELS;
   pl_plan* e = nullptr;
   for (pl_plan& c : p->plans)
     if (!c.pending) e = &c;
@@ -494,6 +528,7 @@ extern "C" hl_status hl_pipeline_step(hl_pipeline* p, const hl_step_io* io, hl_s
   if (!p || !io) return HL_ERR_INVALID_ARG;
   hl_handle* h = p->h;
   HL_TRY(pl_not_capturing((hipStream_t)stream));
+  p->sep_hand = io->step_flags & HL_STEP_HANDOVER_KERNELS;
   const bool planned = io->step_flags & HL_STEP_PLANNED;
   pl_plan* e = pl_pending(p, io->workspace);
   if (planned ? !e || !pl_same_plan(e->io, *io) : e != nullptr) return HL_ERR_INVALID_ARG;

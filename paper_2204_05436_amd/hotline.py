@@ -44,6 +44,7 @@ class StepIO(C.Structure):
 
 HL_STEP_UNTIED = 1
 HL_STEP_PLANNED = 2
+HL_STEP_HANDOVER_KERNELS = 4
 _SIGS = {
     "hl_status_string": (C.c_char_p, [C.c_int]),
     "hl_create": (C.c_int, [C.POINTER(P), I32, P, I32, C.c_int, U32]),
@@ -90,6 +91,7 @@ _SIGS = {
     "hl_trace_count": (I32, [P]),
     "hl_trace_only": (C.c_int, [P, C.c_char_p]),
     "hl_trace_read": (C.c_int, [P, I32, C.POINTER(C.c_char_p), C.POINTER(C.c_float)]),
+    "hl_trace_read_at": (C.c_int, [P, I32, C.POINTER(C.c_char_p), C.POINTER(C.c_float), C.POINTER(C.c_float)]),
     "hl_trace_reset": (C.c_int, [P]),
     "hl_host_alloc": (C.c_int, [SZ, C.POINTER(P), C.POINTER(P)]),
     "hl_stream_create": (C.c_int, [I32, I32, I32, C.POINTER(P)]),
@@ -460,6 +462,13 @@ def hl_trace_read(h, i):
     name, ms = C.c_char_p(), C.c_float()
     _ck("hl_trace_read", lib().hl_trace_read(h.ptr, int(i), C.byref(name), C.byref(ms)))
     return name.value.decode(), float(ms.value)
+
+
+def hl_trace_read_at(h, i):
+    """(name, start ms after record 0's start, duration ms) of record i"""
+    name, t0, ms = C.c_char_p(), C.c_float(), C.c_float()
+    _ck("hl_trace_read_at", lib().hl_trace_read_at(h.ptr, int(i), C.byref(name), C.byref(t0), C.byref(ms)))
+    return name.value.decode(), float(t0.value), float(ms.value)
 
 
 def hl_trace_reset(h):

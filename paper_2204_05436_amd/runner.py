@@ -146,16 +146,17 @@ class HotPath:
         io.step_flags = flags
         return io
 
-    def plan(self, b: DevBatch, untied=False):
+    def plan(self, b: DevBatch, untied=False, handover_kernels=False):
         """Look-ahead segregation of batch b (hl_pipeline_plan): its dispatch,
         cold plan and grouping run on the pipeline's plan stream while the steps
         enqueued before it train; the step of b skips them.  Up to n_sets - 1
-        plans ahead of the steps."""
+        plans ahead of the steps.  handover_kernels: as in step()."""
         if len(self._pending) >= self.n_sets - 1:
             raise RuntimeError(f"{len(self._pending)} look-ahead plans are already pending")
         p = self._par
         self._par = (p + 1) % self.n_sets
-        io = self._fill_io(hl.StepIO(), b, self._sets[p], 0.0, hl.HL_STEP_UNTIED if untied else 0)
+        flags = (hl.HL_STEP_UNTIED if untied else 0) | (hl.HL_STEP_HANDOVER_KERNELS if handover_kernels else 0)
+        io = self._fill_io(hl.StepIO(), b, self._sets[p], 0.0, flags)
         hl.hl_pipeline_plan(self.pipe, io, torch.cuda.current_stream(self.device))
         self._pending.append((b, p))
 
@@ -201,7 +202,7 @@ class HotPath:
 
     # ------------------------------------------------------------------ one mini-batch
     def step(self, b: DevBatch, lr: float | None = None, events=None, mode: str = "pipelined", split_fwd=True,
-             untied=False, next=None):
+             untied=False, next=None, handover_kernels=False):
         """classify -> partition -> remap -> cold gather (non-popular) -> forward of
         both mu-batches -> one coalesced SGD step [-> write-back of the cold rows].
 
@@ -211,7 +212,9 @@ class HotPath:
           sync() before using the results).  next: the following batch, or
           a list of the following batches, planned ahead (plan()) up to
           n_sets - 1 of them, to run while this step trains; their own steps
-          find them done.
+          find them done.  handover_kernels: the handovers between the
+          streams as kernels of their own (HL_STEP_HANDOVER_KERNELS), so that
+          the path's kernels hold no waits.
         mode "sequential": the fused calls in order on the current stream;
           `events`: optional list of len(STAGES)+1 torch.cuda.Event recorded
           around the stages.
@@ -231,10 +234,10 @@ class HotPath:
             if next is not None:
                 raise ValueError("no look-ahead under capture")
             return self._step_pipelined(b, lr, events, mode, caller, capturing)
-        flags = hl.HL_STEP_UNTIED if untied else 0
+        flags = (hl.HL_STEP_UNTIED if untied else 0) | (hl.HL_STEP_HANDOVER_KERNELS if handover_kernels else 0)
         nexts = [] if next is None else (list(next) if isinstance(next, (list, tuple)) else [next])
         if nexts and not self._pending:
-            self.plan(b, untied)
+            self.plan(b, untied, handover_kernels)
         if self._pending:
             if self._pending[0][0] is not b:
                 raise RuntimeError("steps must take the batches in the order they were planned")
@@ -250,7 +253,7 @@ class HotPath:
             if len(self._pending) >= self.n_sets - 1:
                 break
             if not any(nb is pb for pb, _ in self._pending):
-                self.plan(nb, untied)
+                self.plan(nb, untied, handover_kernels)
 
     def sync(self, stream=None):
         """The stream (default: current) waits for every step enqueued so far."""

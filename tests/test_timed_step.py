@@ -24,12 +24,17 @@ pytestmark = pytest.mark.gpu
 N_STEPS = 3
 
 
-@pytest.mark.parametrize("name,k", [("dlrm-large", None), ("multi-hot", None), ("multi-hot", 2000)])
-def test_timed_step_full_size(name, k):
+@pytest.mark.parametrize("name,k,hk,wb", [("dlrm-large", None, False, False), ("multi-hot", None, False, False),
+                                          ("multi-hot", 2000, False, False), ("dlrm-large", None, True, False),
+                                          ("dlrm-large", None, False, True)])
+def test_timed_step_full_size(name, k, hk, wb):
     """k: the hot-set size (None: the workload's).  Multi-hot with the 2000
     most accessed rows hot leaves popular rows cold, so bags repeat cold rows:
     the grouping's order inside a key, which the cold forward's adjacency test
-    reads, is then exercised."""
+    reads, is then exercised.  hk: the handovers between the streams as
+    kernels of their own (the schedule the benchmark times its kernels in).
+    wb: the updated cold rows written back to the host table after each step
+    (the next steps gather from the updated table)."""
     w = configs.WORKLOADS[name]
     rows = W.table_rows(w)
     n_rows = int(rows.sum(dtype=np.int64))
@@ -41,7 +46,7 @@ def test_timed_step_full_size(name, k):
     dYs = [W.make_dy(w, i, mb.n_bags) for i, mb in zip(idx, steps)]
     log(f"[timed-step] {name}: rows={n_rows} B={w.batch} L={steps[0].n_lookups} k_cap={k_cap}")
     table = make_table(w, n_rows)
-    hp = HotPath(w, rows, table, max(b.n_lookups for b in prof + steps), w.batch, device="cuda")
+    hp = HotPath(w, rows, table, max(b.n_lookups for b in prof + steps), w.batch, device="cuda", writeback=wb)
     try:
         assert hp.n_sets == 3 and hp.fetch_cus == 8 and hp.plan_cus == 64
         hp.learn([to_device(p, "cuda") for p in prof], k=k)
@@ -60,20 +65,26 @@ def test_timed_step_full_size(name, k):
         for si in range(N_STEPS):
             mb, dY = steps[si], dYs[si]
             w_pre = hp.w_hot[:n_hot].cpu().numpy().copy()
-            tab_pre = table.array  # no write-back: the host table does not change
-            log(f"[timed-step] {name}: step {si}")
-            with torch.cuda.stream(side):
-                # the benchmark's call: plans for the next n_sets - 1 batches
-                hp.step(dbs[si], untied=True, next=[dbs[j] for j in range(si + 1, si + hp.n_sets)])
-                hp.sync()
-            torch.cuda.synchronize()
-            assert hp.device_error() == 0, f"step {si}"
+            # the oracle's plan needs the hot set and the batch only
             B, bps, L = mb.n_samples, mb.bags_per_sample, mb.n_lookups
             g, _ = O.gids(rows, mb.rows, mb.bag_ptr)
             flags = O.classify(hot, g, mb.bag_ptr, B, bps)
             pop, nonpop = O.partition(flags)
             cold, codes = O.cold_plan(g, O.remap(hot, g), mb.bag_ptr, nonpop, len(nonpop), bps, k_cap)
-            stg = O.gather(tab_pre, cold)
+            # the host table's cold rows before the step (after the last
+            # write-back), and a sample of its other rows
+            stg = O.gather(table.array, cold)
+            if wb:
+                samp = np.setdiff1d(np.random.default_rng(si).integers(0, n_rows, 100000), cold)
+                samp_pre = table.array[samp].copy()
+            log(f"[timed-step] {name}: step {si}")
+            with torch.cuda.stream(side):
+                # the benchmark's call: plans for the next n_sets - 1 batches
+                hp.step(dbs[si], untied=True, next=[dbs[j] for j in range(si + 1, si + hp.n_sets)],
+                        handover_kernels=hk)
+                hp.sync()
+            torch.cuda.synchronize()
+            assert hp.device_error() == 0, f"step {si}"
             assert np.array_equal(hp.flags[:B].cpu().numpy(), flags), f"step {si} flags"
             cnt = hp.counts.cpu().numpy()
             assert cnt[0] == len(pop) and cnt[1] == len(nonpop), f"step {si} mu-batch sizes"
@@ -98,6 +109,10 @@ def test_timed_step_full_size(name, k):
             ts = uniq[~hu] - k_cap
             check_close(as_f64(gst[ts], w.dtype), as_f64(stg_ref[ts], w.dtype), usc[~hu], rtol,
                         f"step {si} staging rows")
+            if wb:  # the host table: the cold rows updated, the others as before
+                tab = table.array
+                assert np.array_equal(tab[cold].view(np.uint8), gst.view(np.uint8)), f"step {si} written back"
+                assert np.array_equal(tab[samp].view(np.uint8), samp_pre.view(np.uint8)), f"step {si} other rows"
             untouched = np.setdiff1d(np.arange(n_hot), uniq[hu])
             assert np.array_equal(gw[untouched].view(np.uint8), w_pre[untouched].view(np.uint8)), f"step {si}"
             keys = torch.zeros(L, dtype=torch.int32, device="cuda")
