@@ -2,7 +2,8 @@
 // the hot cache (HBM) and the staging buffer of gathered cold rows.
 //
 // Lane layout: a row is covered by G lanes holding VEC consecutive elements
-// each (fp32: 16-byte loads for VEC = 4; bf16: 8-byte loads widened to fp32),
+// each (fp32: 16-byte loads for VEC = 4; bf16: 16-byte loads for VEC = 8,
+// widened to fp32),
 // G = min(dim/VEC, 64); a wave holds NG = 64/G row groups; rows wider than 64
 // vectors are split into column chunks over blockIdx.y.
 //
@@ -54,6 +55,18 @@ struct RowIO<2, false> {
   }
 };
 template <>
+struct RowIO<8, false> {
+  typedef float T;
+  static __device__ __forceinline__ void load(const T* p, float* v) {
+    RowIO<4, false>::load(p, v);
+    RowIO<4, false>::load(p + 4, v + 4);
+  }
+  static __device__ __forceinline__ void store(T* p, const float* v) {
+    RowIO<4, false>::store(p, v);
+    RowIO<4, false>::store(p + 4, v + 4);
+  }
+};
+template <>
 struct RowIO<1, false> {
   typedef float T;
   static __device__ __forceinline__ void load(const T* p, float* v) { v[0] = *p; }
@@ -76,6 +89,23 @@ struct RowIO<4, true> {
   }
   static __device__ __forceinline__ void store(T* p, const float* v) {
     *reinterpret_cast<uint2*>(p) = make_uint2(f2bf(v[0]) | (f2bf(v[1]) << 16), f2bf(v[2]) | (f2bf(v[3]) << 16));
+  }
+};
+template <>
+struct RowIO<8, true> {
+  typedef uint16_t T;
+  static __device__ __forceinline__ void load(const T* p, float* v) {
+    uint4 x = *reinterpret_cast<const uint4*>(p);
+    const uint32_t w[4] = {x.x, x.y, x.z, x.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      v[2 * i] = bf2f(w[i] & 0xFFFFu);
+      v[2 * i + 1] = bf2f(w[i] >> 16);
+    }
+  }
+  static __device__ __forceinline__ void store(T* p, const float* v) {
+    *reinterpret_cast<uint4*>(p) = make_uint4(f2bf(v[0]) | (f2bf(v[1]) << 16), f2bf(v[2]) | (f2bf(v[3]) << 16),
+                                              f2bf(v[4]) | (f2bf(v[5]) << 16), f2bf(v[6]) | (f2bf(v[7]) << 16));
   }
 };
 template <>
@@ -109,9 +139,12 @@ __device__ __forceinline__ void st_f32(float* p, const float* v) { RowIO<VEC, fa
 typedef float hl_f4 __attribute__((ext_vector_type(4)));
 template <int VEC>
 __device__ __forceinline__ void st_f32_nt(float* p, const float* v) {
-  if constexpr (VEC == 4) {
-    const hl_f4 x = {v[0], v[1], v[2], v[3]};
-    __builtin_nontemporal_store(x, reinterpret_cast<hl_f4*>(p));
+  if constexpr (VEC == 4 || VEC == 8) {
+#pragma unroll
+    for (int i = 0; i < VEC; i += 4) {
+      const hl_f4 x = {v[i], v[i + 1], v[i + 2], v[i + 3]};
+      __builtin_nontemporal_store(x, reinterpret_cast<hl_f4*>(p + i));
+    }
   } else {
     RowIO<VEC, false>::store(p, v);
   }
@@ -132,8 +165,10 @@ static eb_geom eb_make_geom(int32_t D, int vec) {
   return g;
 }
 
+// bf16 rows take 8 elements per lane (16-byte loads), fp32 rows 4; fewer
+// when the dimension or a pointer's alignment does not allow them
 static int eb_pick_vec(int32_t D, size_t esize, std::initializer_list<const void*> ptrs) {
-  int vec = D % 4 == 0 ? 4 : (D % 2 == 0 ? 2 : 1);
+  int vec = (esize == 2 && D % 8 == 0) ? 8 : (D % 4 == 0 ? 4 : (D % 2 == 0 ? 2 : 1));
   for (;;) {
     bool ok = true;
     for (const void* p : ptrs)
@@ -150,18 +185,19 @@ __device__ __forceinline__ int32_t eb_nsel(const int32_t* ids, const int32_t* n_
 }
 
 // ----------------------------------------------------------------------------- forward
-// A row group takes FC consecutive bag slots of the selection (slot q = bag j of
-// selected sample q / bps) and issues the loads of all of them before using
-// any: offsets, then codes, then rows, so FC rows per lane are in flight.  When
-// every bag of the chunk holds one lookup (one-hot features) that is the whole
-// work; otherwise bags are pooled one by one with 4 rows in flight.
+// A row group takes FC (bags of about one lookup) or 1 (multi-hot bags)
+// consecutive bag slots of the selection (slot q = bag j of selected sample
+// q / bps) and issues the loads of all of them before using any: offsets,
+// then codes, then rows, so FC rows per lane are in flight.  When every bag of
+// the chunk holds one lookup (one-hot features) that is the whole work;
+// otherwise bags are pooled one by one (eb_bag).
 //
-// A bag's sum takes its hot rows first, then its staging (cold) rows, each in
-// CSR order, so that the two halves can run apart with identical results:
-// PART 0 does both, PART 1 only the hot rows (writing the partial sum), PART 2
-// adds the cold rows onto the stored partial sum (bags without cold rows are
-// left alone).  The hot half needs no fetched row, so it runs while the
-// working parameters still travel over the host link.
+// A bag's sum is the sum of its hot rows plus the sum of its staging (cold)
+// rows, each in CSR order, so that the two halves can run apart with
+// identical results: PART 0 does both, PART 1 only the hot rows (writing the
+// partial sum), PART 2 adds the cold rows' sum onto the stored partial sum
+// (bags without cold rows are left alone).  The hot half needs no fetched row,
+// so it runs while the working parameters still travel over the host link.
 #ifndef FC
 #define FC 4  // bag slots per row group of the forward (4 measured fastest of 4, 6, 8, 12, 16)
 #endif
@@ -180,13 +216,18 @@ __device__ __forceinline__ bool eb_code_row(uint32_t cu, uint32_t n_hot, uint32_
   return false;
 }
 
-// acc += the bag's rows of one kind (hot, or staging when COLD), in CSR order,
-// 4 rows in flight.  Invalid codes are flagged by the hot pass only.
+// acc += the bag's rows of one kind (hot, or staging when COLD), in CSR order.
+// Invalid codes are flagged by the hot pass only.  Called by a whole row
+// group at once (its G lanes in the same control flow).  Row groups of 8 lanes
+// or more load the codes of G lookups at once, one per lane, and take the row
+// indices from each other by shuffles, 8 rows in flight; narrower groups load
+// 4 codes, then 4 rows, at a time.  Either way each lane adds the rows in CSR
+// order.
 template <int VEC, bool BF, bool COLD>
-__device__ __forceinline__ void eb_pass(float* acc, const typename RowIO<VEC, BF>::T* w_hot,
-                                        const typename RowIO<VEC, BF>::T* stg, int32_t stg_rows, uint32_t n_hot,
-                                        uint32_t k_cap, const int32_t* __restrict__ codes, int32_t lo, int32_t hi,
-                                        eb_geom g, int64_t col, bool cact, int gl, uint32_t* err) {
+__device__ __forceinline__ void eb_pass4(float* acc, const typename RowIO<VEC, BF>::T* w_hot,
+                                         const typename RowIO<VEC, BF>::T* stg, int32_t stg_rows, uint32_t n_hot,
+                                         uint32_t k_cap, const int32_t* __restrict__ codes, int32_t lo, int32_t hi,
+                                         eb_geom g, int64_t col, bool cact, int gl, uint32_t* err, bool* any) {
   for (int32_t i = lo; i < hi; i += 4) {
     uint32_t cc[4];
 #pragma unroll
@@ -200,6 +241,7 @@ __device__ __forceinline__ void eb_pass(float* acc, const typename RowIO<VEC, BF
       const bool in = i + k < hi;
       const bool ok = in && eb_code_row(cc[k], n_hot, k_cap, stg_rows, &r, &st);
       use[k] = ok && st == COLD;
+      *any = *any || use[k];
       if (use[k] && cact) RowIO<VEC, BF>::load((COLD ? stg : w_hot) + r * g.D + col, v[k]);
       if (!COLD && in && !ok && gl == 0) hl_flag(err, HL_DEVERR_BAD_CODE);
     }
@@ -211,13 +253,149 @@ __device__ __forceinline__ void eb_pass(float* acc, const typename RowIO<VEC, BF
   }
 }
 
+#define EB_SEG_ROWS 8  // rows in flight per lane in the passes' wide form
+
+// The wide form's segment: the codes of lookups b0 .. b0 + G - 1 of [b0, hi),
+// one per lane of the group (an invalid code past hi; a lane's own code that
+// names no row is flagged when `flag`).
+__device__ __forceinline__ uint32_t eb_seg_code(const int32_t* __restrict__ codes, int32_t b0, int32_t hi, int gl,
+                                                uint32_t n_hot, uint32_t k_cap, int32_t stg_rows, bool flag,
+                                                uint32_t* err) {
+  const int32_t i = b0 + gl;
+  if (i >= hi) return ~0u;
+  const uint32_t c = (uint32_t)codes[i];
+  int64_t r;
+  bool st;
+  if (flag && !eb_code_row(c, n_hot, k_cap, stg_rows, &r, &st)) hl_flag(err, HL_DEVERR_BAD_CODE);
+  return c;
+}
+
+// acc += the bag's rows of one kind (hot, or staging when COLD), in CSR order;
+// *any: some row of that kind was found.  Invalid codes are flagged by the hot
+// pass only.  Called by a whole row group at once (its G lanes in the same
+// control flow).  Row groups of 8 lanes or more load the codes of G lookups at
+// once, one per lane, and take them from each other by shuffles, 8 rows in
+// flight; narrower groups load 4 codes, then 4 rows, at a time.  Either way
+// each lane adds the rows in CSR order.
+template <int VEC, bool BF, bool COLD>
+__device__ __forceinline__ void eb_pass(float* acc, const typename RowIO<VEC, BF>::T* w_hot,
+                                        const typename RowIO<VEC, BF>::T* stg, int32_t stg_rows, uint32_t n_hot,
+                                        uint32_t k_cap, const int32_t* __restrict__ codes, int32_t lo, int32_t hi,
+                                        eb_geom g, int64_t col, bool cact, int gl, uint32_t* err, bool* any) {
+  if (g.G < EB_SEG_ROWS) {
+    eb_pass4<VEC, BF, COLD>(acc, w_hot, stg, stg_rows, n_hot, k_cap, codes, lo, hi, g, col, cact, gl, err, any);
+    return;
+  }
+  const int g0 = (int)(threadIdx.x & 63) - gl;  // the group's first lane
+  for (int32_t b0 = lo; b0 < hi; b0 += g.G) {
+    const uint32_t mine = eb_seg_code(codes, b0, hi, gl, n_hot, k_cap, stg_rows, !COLD, err);
+    const int n = min(g.G, hi - b0);
+    for (int k0 = 0; k0 < n; k0 += EB_SEG_ROWS) {
+      bool use[EB_SEG_ROWS];
+      float v[EB_SEG_ROWS][VEC];
+#pragma unroll
+      for (int k = 0; k < EB_SEG_ROWS; ++k) {
+        const uint32_t c = (uint32_t)__shfl((int)mine, g0 + min(k0 + k, n - 1));
+        int64_t r = 0;
+        bool st = false;
+        use[k] = k0 + k < n && eb_code_row(c, n_hot, k_cap, stg_rows, &r, &st) && st == COLD;
+        *any = *any || use[k];
+        if (use[k] && cact) RowIO<VEC, BF>::load((COLD ? stg : w_hot) + r * g.D + col, v[k]);
+      }
+#pragma unroll
+      for (int k = 0; k < EB_SEG_ROWS; ++k)
+        if (use[k] && cact)
+#pragma unroll
+          for (int e = 0; e < VEC; ++e) acc[e] += v[k][e];
+    }
+  }
+}
+
+// Both kinds at once, into separate sums (hot into acc_h, staging into acc_c,
+// each in CSR order: the sums the two single-kind passes give), with one code
+// load per segment.  *anyc: some staging row was found.
+template <int VEC, bool BF>
+__device__ __forceinline__ void eb_pass_both(float* acc_h, float* acc_c, bool* anyc,
+                                             const typename RowIO<VEC, BF>::T* w_hot,
+                                             const typename RowIO<VEC, BF>::T* stg, int32_t stg_rows, uint32_t n_hot,
+                                             uint32_t k_cap, const int32_t* __restrict__ codes, int32_t lo, int32_t hi,
+                                             eb_geom g, int64_t col, bool cact, int gl, uint32_t* err) {
+  if (g.G < EB_SEG_ROWS) {
+    bool anyh = false;
+    eb_pass4<VEC, BF, false>(acc_h, w_hot, stg, stg_rows, n_hot, k_cap, codes, lo, hi, g, col, cact, gl, err, &anyh);
+    eb_pass4<VEC, BF, true>(acc_c, w_hot, stg, stg_rows, n_hot, k_cap, codes, lo, hi, g, col, cact, gl, err, anyc);
+    return;
+  }
+  const int g0 = (int)(threadIdx.x & 63) - gl;
+  for (int32_t b0 = lo; b0 < hi; b0 += g.G) {
+    const uint32_t mine = eb_seg_code(codes, b0, hi, gl, n_hot, k_cap, stg_rows, true, err);
+    const int n = min(g.G, hi - b0);
+    for (int k0 = 0; k0 < n; k0 += EB_SEG_ROWS) {
+      bool use[EB_SEG_ROWS], cold[EB_SEG_ROWS];
+      float v[EB_SEG_ROWS][VEC];
+#pragma unroll
+      for (int k = 0; k < EB_SEG_ROWS; ++k) {
+        const uint32_t c = (uint32_t)__shfl((int)mine, g0 + min(k0 + k, n - 1));
+        int64_t r = 0;
+        bool st = false;
+        use[k] = k0 + k < n && eb_code_row(c, n_hot, k_cap, stg_rows, &r, &st);
+        cold[k] = st;
+        *anyc = *anyc || (use[k] && st);
+        if (use[k] && cact) RowIO<VEC, BF>::load((st ? stg : w_hot) + r * g.D + col, v[k]);
+      }
+#pragma unroll
+      for (int k = 0; k < EB_SEG_ROWS; ++k)
+        if (use[k] && cact) {
+          float* a = cold[k] ? acc_c : acc_h;
+#pragma unroll
+          for (int e = 0; e < VEC; ++e) a[e] += v[k][e];
+        }
+    }
+  }
+}
+
+// One bag pooled into *o (the row group's slice of the bag's output row):
+// PART 0 sums the hot rows and the staging rows apart (each in CSR order) and
+// stores their sum (the hot sum alone when no staging row is in the bag);
+// PART 1 stores the hot sum; PART 2 adds the staging rows' sum onto the stored
+// hot sum (bags without staging rows are left alone).  So PART 1 then PART 2
+// store what PART 0 does.
+template <int VEC, bool BF, int PART>
+__device__ __forceinline__ void eb_bag(float* o, const typename RowIO<VEC, BF>::T* w_hot,
+                                       const typename RowIO<VEC, BF>::T* stg, int32_t stg_rows, uint32_t n_hot,
+                                       uint32_t k_cap, const int32_t* __restrict__ codes, int32_t lo, int32_t hi,
+                                       eb_geom g, int64_t col, bool cact, int gl, uint32_t* err) {
+  float acc[VEC], accc[VEC];
+#pragma unroll
+  for (int e = 0; e < VEC; ++e) {
+    acc[e] = 0.f;
+    accc[e] = 0.f;
+  }
+  bool anyc = false;
+  if (PART == 0) {
+    eb_pass_both<VEC, BF>(acc, accc, &anyc, w_hot, stg, stg_rows, n_hot, k_cap, codes, lo, hi, g, col, cact, gl,
+                          err);
+  } else if (PART == 1) {
+    bool anyh = false;
+    eb_pass<VEC, BF, false>(acc, w_hot, stg, stg_rows, n_hot, k_cap, codes, lo, hi, g, col, cact, gl, err, &anyh);
+  } else {
+    eb_pass<VEC, BF, true>(accc, w_hot, stg, stg_rows, n_hot, k_cap, codes, lo, hi, g, col, cact, gl, err, &anyc);
+    if (!anyc) return;
+    if (cact) ld_f32<VEC>(o, acc);
+  }
+  if (anyc)
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) acc[e] += accc[e];
+  if (cact) st_f32_nt<VEC>(o, acc);
+}
+
 template <int VEC, bool BF, int PART>
 __global__ void __launch_bounds__(256)
 eb_fwd(const void* w_hot_, const void* stg_, int32_t stg_rows, uint32_t n_hot, uint32_t k_cap,
        const int32_t* __restrict__ codes, const int32_t* __restrict__ bag_ptr, int32_t bps,
        const int32_t* __restrict__ sample_ids, const int32_t* n_sel_dev, int32_t n_sel_max,
        float* __restrict__ out, eb_geom g, int64_t n_lookups, int64_t n_bags_total, int32_t n_samples,
-       uint32_t* err, hl_hook hk) {
+       int32_t nbg, uint32_t* err, hl_hook hk) {
   typedef typename RowIO<VEC, BF>::T T;
   const T* w_hot = (const T*)w_hot_;
   const T* stg = (const T*)stg_;
@@ -231,16 +409,16 @@ eb_fwd(const void* w_hot_, const void* stg_, int32_t stg_rows, uint32_t n_hot, u
   const bool cact = colv < g.vpr;
   const int64_t col = (int64_t)colv * VEC;
   const int64_t total = (int64_t)eb_nsel(sample_ids, n_sel_dev, n_sel_max) * bps;
-  const int64_t chunks = (total + FC - 1) / FC;
+  const int64_t chunks = (total + nbg - 1) / nbg;
   const int64_t stride = (int64_t)gridDim.x * 4 * g.NG;
   for (int64_t c = ((int64_t)blockIdx.x * 4 + w) * g.NG + gi; c < chunks; c += stride) {
-    const int64_t q0 = c * FC;
+    const int64_t q0 = c * nbg;
     int64_t si = q0 / bps, j = q0 - si * bps;
     int64_t bag[FC];
     bool val[FC];
 #pragma unroll
     for (int u = 0; u < FC; ++u) {
-      val[u] = q0 + u < total;
+      val[u] = u < nbg && q0 + u < total;
       int64_t smp = si;
       if (val[u] && sample_ids) smp = sample_ids[si];
       if (val[u] && (smp < 0 || smp >= n_samples)) {
@@ -300,23 +478,8 @@ eb_fwd(const void* w_hot_, const void* stg_, int32_t stg_rows, uint32_t n_hot, u
     }
     for (int u = 0; u < FC; ++u) {
       if (!val[u]) continue;
-      float acc[VEC];
-#pragma unroll
-      for (int e = 0; e < VEC; ++e) acc[e] = 0.f;
-      if (PART == 2) {
-        bool any = false;
-        for (int32_t i = lo[u]; i < hi[u] && !any; ++i) {
-          const uint32_t cc = (uint32_t)codes[i];
-          any = cc >= k_cap && cc - k_cap < (uint32_t)stg_rows;
-        }
-        if (!any) continue;
-        if (cact) ld_f32<VEC>(out + bag[u] * g.D + col, acc);
-      }
-      if (PART != 2)
-        eb_pass<VEC, BF, false>(acc, w_hot, stg, stg_rows, n_hot, k_cap, codes, lo[u], hi[u], g, col, cact, gl, err);
-      if (PART != 1)
-        eb_pass<VEC, BF, true>(acc, w_hot, stg, stg_rows, n_hot, k_cap, codes, lo[u], hi[u], g, col, cact, gl, err);
-      if (cact) st_f32_nt<VEC>(out + bag[u] * g.D + col, acc);
+      eb_bag<VEC, BF, PART>(out + bag[u] * g.D + col, w_hot, stg, stg_rows, n_hot, k_cap, codes, lo[u], hi[u], g,
+                            col, cact, gl, err);
     }
   }
   hl_hook_tail(hk);
@@ -429,13 +592,8 @@ eb_fwd_oh(const void* w_hot_, const void* stg_, int32_t stg_rows, uint32_t n_hot
         const int64_t b = c * FC + u;
         if (b >= n_bags) break;
         const int32_t lo = bag_ptr[b], hi = bag_ptr[b + 1];
-        float acc[VEC];
-#pragma unroll
-        for (int e = 0; e < VEC; ++e) acc[e] = 0.f;
-        eb_pass<VEC, BF, false>(acc, w_hot, stg, stg_rows, n_hot, k_cap, codes, lo, hi, g, col, cact, gl, err);
-        if (PART == 0)
-          eb_pass<VEC, BF, true>(acc, w_hot, stg, stg_rows, n_hot, k_cap, codes, lo, hi, g, col, cact, gl, err);
-        if (cact) st_f32_nt<VEC>(out + b * g.D + col, acc);
+        eb_bag<VEC, BF, PART>(out + b * g.D + col, w_hot, stg, stg_rows, n_hot, k_cap, codes, lo, hi, g, col, cact, gl,
+                              err);
       }
     }
 #pragma unroll
@@ -1034,13 +1192,31 @@ __device__ __forceinline__ void eb_tail_body(uint32_t bid, uint32_t nblk, const 
       if (!take[j]) continue;
       const uint32_t u = key[j] - n_hot;
       if (hi[j] - lo[j] != 1) {
-        // the bag's first cold lookup in CSR order names the pair that completes it
+        // the bag's first cold lookup in CSR order names the pair that completes
+        // it (row groups of 8 lanes or more search G codes at a time: a code
+        // per lane, the first cold one by a ballot)
         bool mine = false;
-        for (int32_t i = lo[j]; i < hi[j]; ++i) {
-          const uint32_t c = (uint32_t)codes[i];
-          if (c >= k_cap && c - k_cap < (uint32_t)stg_rows) {
-            mine = c - k_cap == u;
-            break;
+        if (g.G >= EB_SEG_ROWS) {
+          const int g0 = lane - gl;
+          const uint64_t gm = g.G == 64 ? ~0ull : ((1ull << g.G) - 1ull);
+          for (int32_t b0 = lo[j]; b0 < hi[j]; b0 += g.G) {
+            const int32_t i = b0 + gl;
+            const uint32_t c = i < hi[j] ? (uint32_t)codes[i] : ~0u;
+            const bool cold = i < hi[j] && c >= k_cap && c - k_cap < (uint32_t)stg_rows;
+            const uint64_t m = (__ballot(cold) >> g0) & gm;
+            if (m) {
+              const uint32_t cf = (uint32_t)__shfl((int)c, g0 + __ffsll((unsigned long long)m) - 1);
+              mine = cf - k_cap == u;
+              break;
+            }
+          }
+        } else {
+          for (int32_t i = lo[j]; i < hi[j]; ++i) {
+            const uint32_t c = (uint32_t)codes[i];
+            if (c >= k_cap && c - k_cap < (uint32_t)stg_rows) {
+              mine = c - k_cap == u;
+              break;
+            }
           }
         }
         if (!mine) take[j] = false;
@@ -1062,8 +1238,15 @@ __device__ __forceinline__ void eb_tail_body(uint32_t bid, uint32_t nblk, const 
           for (int e = 0; e < VEC; ++e) o[j][e] += v[j][e];
         }
       } else {
-        eb_pass<VEC, BF, true>(o[j], nullptr, stg, stg_rows, n_hot, k_cap, codes, lo[j], hi[j], g, col, cact, gl,
-                               err);
+        // the staging rows' sum, onto the stored hot sum (as PART 2 of the forward adds it)
+        float c[VEC];
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) c[e] = 0.f;
+        bool anyc = false;
+        eb_pass<VEC, BF, true>(c, nullptr, stg, stg_rows, n_hot, k_cap, codes, lo[j], hi[j], g, col, cact, gl, err,
+                               &anyc);
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) o[j][e] += c[e];
       }
       if (cact) st_f32<VEC>(out + (int64_t)bag[j] * g.D + col, o[j]);
     }
@@ -1118,12 +1301,12 @@ template <int VEC, bool BF>
 static void launch_fwd(const hl_handle* h, dim3 grid, hipStream_t s, const void* w_hot, const void* stg,
                        int32_t stg_rows, const int32_t* codes, const int32_t* bag_ptr, int32_t bps,
                        const int32_t* ids, const int32_t* n_dev, int32_t n_max, float* out, eb_geom g,
-                       int64_t n_lookups, int64_t n_bags, int part) {
+                       int64_t n_lookups, int64_t n_bags, int part, int32_t nbg) {
   const hl_hook hk = hl_hook_take(h);
 #define EBF(P)                                                                                                   \
   HL_KERNEL(h, s, P == 0 ? "eb_fwd" : (P == 1 ? "eb_fwd_hot" : "eb_fwd_cold"), (eb_fwd<VEC, BF, P>), grid,       \
             dim3(256), 0, s, w_hot, stg, stg_rows, h->n_hot, h->k_cap, codes, bag_ptr, bps, ids, n_dev, n_max, out, \
-            g, n_lookups, n_bags, (int32_t)(n_bags / bps), h->d_err, hk);
+            g, n_lookups, n_bags, (int32_t)(n_bags / bps), nbg, h->d_err, hk);
   if (part == 0) { EBF(0) }
   else if (part == 1) { EBF(1) }
   else { EBF(2) }
@@ -1162,17 +1345,21 @@ extern "C" hl_status hl_embbag_fwd_part(const hl_handle* h, const void* w_hot, c
   const size_t es = h->dtype == HL_F32 ? 4 : 2;
   const int vec = eb_pick_vec(h->dim, es, {w_hot, staging, out});
   eb_geom g = eb_make_geom(h->dim, vec);
-  const int64_t chunks = ((int64_t)n_sel_max * bps + FC - 1) / FC;
+  const int64_t nb = (int64_t)n_samples * bps;
+  // bags of several lookups each (multi-hot): one bag per row group, so that
+  // more groups pool at once; bags of about one lookup: FC per group
+  const int32_t nbg = n_lookups > 2 * nb ? 1 : FC;
+  const int64_t chunks = ((int64_t)n_sel_max * bps + nbg - 1) / nbg;
   int64_t blocks = (chunks + 4 * g.NG - 1) / (4 * g.NG);
   if (blocks > (1 << 20)) blocks = 1 << 20;
   dim3 grid((uint32_t)blocks, g.cchunks);
   hipStream_t s = (hipStream_t)stream;
-  const int64_t nb = (int64_t)n_samples * bps;
   const bool bf = h->dtype == HL_BF16;
   if (part != 2 && !sample_ids && n_sel_max == n_samples && n_lookups == nb) {
     // every sample of a one-hot mini-batch
 #define FOH(V, B) launch_fwd_oh<V, B>(h, s, w_hot, staging, stg_rows, codes, bag_ptr, out, g, n_lookups, nb, part)
-    if (vec == 4) { if (bf) FOH(4, true); else FOH(4, false); }
+    if (vec == 8) FOH(8, true);  // (bf16 only)
+    else if (vec == 4) { if (bf) FOH(4, true); else FOH(4, false); }
     else if (vec == 2) { if (bf) FOH(2, true); else FOH(2, false); }
     else { if (bf) FOH(1, true); else FOH(1, false); }
 #undef FOH
@@ -1180,8 +1367,9 @@ extern "C" hl_status hl_embbag_fwd_part(const hl_handle* h, const void* w_hot, c
     return HL_OK;
   }
 #define FWD(V, B) launch_fwd<V, B>(h, grid, s, w_hot, staging, stg_rows, codes, bag_ptr, bps, sample_ids, n_sel_dev, \
-                                   n_sel_max, out, g, n_lookups, nb, part)
-  if (vec == 4) { if (bf) FWD(4, true); else FWD(4, false); }
+                                   n_sel_max, out, g, n_lookups, nb, part, nbg)
+  if (vec == 8) FWD(8, true);  // (bf16 only)
+  else if (vec == 4) { if (bf) FWD(4, true); else FWD(4, false); }
   else if (vec == 2) { if (bf) FWD(2, true); else FWD(2, false); }
   else { if (bf) FWD(1, true); else FWD(1, false); }
 #undef FWD
@@ -1355,7 +1543,8 @@ hl_status hl_embbag_bwd_apply_any(hl_handle* h, void* w_hot, void* staging, int3
   if (tiles > ws.tiles) return HL_ERR_CAPACITY;
   const bool bf = h->dtype == HL_BF16;
 #define BWD(V, B) launch_bwd<V, B>(h, tiles, s, sk, sv, n, dY, g, w_hot, staging, h->n_hot, lr, ws, part)
-  if (vec == 4) { if (bf) BWD(4, true); else BWD(4, false); }
+  if (vec == 8) BWD(8, true);  // (bf16 only)
+  else if (vec == 4) { if (bf) BWD(4, true); else BWD(4, false); }
   else if (vec == 2) { if (bf) BWD(2, true); else BWD(2, false); }
   else { if (bf) BWD(1, true); else BWD(1, false); }
 #undef BWD
@@ -1395,7 +1584,8 @@ hl_status hl_embbag_fwd_cold_sorted(hl_handle* h, const void* staging, int32_t s
 #define TAIL(V, B)                                                                                                  \
   HL_KERNEL(h, s, "eb_fwd_tail", (eb_fwd_tail<V, B>), dim3(b, g.cchunks), dim3(256), 0, s, sk, sv, n, ws.bnd, g, \
             staging, stg_rows, h->n_hot, h->k_cap, codes, bag_ptr, out, h->d_err)
-  if (vec == 4) { if (bf) TAIL(4, true); else TAIL(4, false); }
+  if (vec == 8) TAIL(8, true);  // (bf16 only)
+  else if (vec == 4) { if (bf) TAIL(4, true); else TAIL(4, false); }
   else if (vec == 2) { if (bf) TAIL(2, true); else TAIL(2, false); }
   else { if (bf) TAIL(1, true); else TAIL(1, false); }
 #undef TAIL
@@ -1434,7 +1624,7 @@ hl_status hl_embbag_finish_cold(hl_handle* h, void* w_hot, void* staging, int32_
   const uint32_t tiles = hl_div_up(n, te);
   if (tiles > ws.tiles) return HL_ERR_CAPACITY;
   uint32_t tb = hl_div_up(n, RB_WAVES * g.NG * FT);
-  if (tb > 256) tb = 256;
+  if (tb > 1024) tb = 1024;  // (the tail, cold lookups only, is a part of n the device knows)
   uint32_t cb = hl_div_up(n, 256);  // (as part 2: the tail is short, a small grid strides over it)
   if (cb > 128) cb = 128;
   hipStream_t s = (hipStream_t)stream;
@@ -1447,7 +1637,8 @@ hl_status hl_embbag_finish_cold(hl_handle* h, void* w_hot, void* staging, int32_
     HL_KERNEL(h, s, "bw_cold", (bw_cold<V, B>), dim3(cb, g.cchunks), dim3(256), 0, s, sk, n, g, staging, h->n_hot, \
               lr, ws.gc, ws.gc_rows, ws.bnd, hl_hook_take(h));                                                     \
   } while (0)
-  if (vec == 4) { if (bf) FIN(4, true); else FIN(4, false); }
+  if (vec == 8) FIN(8, true);  // (bf16 only)
+  else if (vec == 4) { if (bf) FIN(4, true); else FIN(4, false); }
   else if (vec == 2) { if (bf) FIN(2, true); else FIN(2, false); }
   else { if (bf) FIN(1, true); else FIN(1, false); }
 #undef FIN
