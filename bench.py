@@ -89,6 +89,9 @@ def kernel_bytes(name, st, alone=False):
         # the same with the reduction's spanning segments (their partial sums are
         # workspace, not algorithmic bytes)
         "eb_tail_r2": 8 * Lc + 8 * Lc + C * R + 2 * Lc * O,
+        # the cold half bag by bag (multi-hot): codes and offsets of every bag,
+        # staging rows, outputs read and written
+        "eb_bags_r2": 4 * L + 4 * (nb + 1) + C * R + 2 * nb * O,
         # reduction: sorted keys and bags, dY, each updated hot row read and
         # written, the staging rows' sums written
         "bw_reduce1": 8 * L + nb * O + 2 * (U - C) * R + C * O,
@@ -424,8 +427,8 @@ def main():
 
     # the embedding forward and backward: their kernels' time per step (the
     # grouping included), against the algorithmic bytes of both passes
-    fb_kernels = ("eb_fwd", "eb_fwd_hot", "eb_fwd_tail", "eb_tail_r2", "bw_prep", "bw_prep_hist", "srt_hist",
-                  "srt_pass", "gt_prep", "gt_sort", "bw_reduce1", "bw_reduce2", "bw_cold")
+    fb_kernels = ("eb_fwd", "eb_fwd_hot", "eb_fwd_tail", "eb_tail_r2", "eb_bags_r2", "bw_prep", "bw_prep_hist",
+                  "srt_hist", "srt_pass", "gt_prep", "gt_sort", "bw_reduce1", "bw_reduce2", "bw_cold")
     t_fb = sum(kernels[n]["ms_per_step"] for n in fb_kernels if n in kernels)
     t_fb_alone = sum(kernels_alone[n]["ms_per_step"] for n in fb_kernels if n in kernels_alone)
     fwd_b = 4 * avg["L"] + 4 * (avg["n_bags"] + 1) + avg["U"] * avg["R"] + avg["n_bags"] * avg["O"]
@@ -624,7 +627,8 @@ def main():
 
 
 # the main stream's kernels of a planned step: the forwards and the backward
-MAIN_KERNELS = ("eb_fwd_hot", "eb_fwd_cold", "eb_fwd_tail", "eb_tail_r2", "bw_reduce1", "bw_reduce2", "bw_cold")
+MAIN_KERNELS = ("eb_fwd_hot", "eb_fwd_cold", "eb_fwd_tail", "eb_tail_r2", "eb_bags_r2", "bw_reduce1", "bw_reduce2",
+                "bw_cold")
 
 
 def fetch_overlap(hp, run):

@@ -16,6 +16,7 @@
 // second kernel in tile order.  Every row is read and written once and the
 // summation order depends only on the sorted order, so results are
 // deterministic.
+#include <algorithm>
 #include <initializer_list>
 
 #include "hl_internal.h"
@@ -389,29 +390,27 @@ __device__ __forceinline__ void eb_bag(float* o, const typename RowIO<VEC, BF>::
   if (cact) st_f32_nt<VEC>(o, acc);
 }
 
+// The forward's work of block bid of nblk (each of blockDim.x / 64 waves).
 template <int VEC, bool BF, int PART>
-__global__ void __launch_bounds__(256)
-eb_fwd(const void* w_hot_, const void* stg_, int32_t stg_rows, uint32_t n_hot, uint32_t k_cap,
-       const int32_t* __restrict__ codes, const int32_t* __restrict__ bag_ptr, int32_t bps,
-       const int32_t* __restrict__ sample_ids, const int32_t* n_sel_dev, int32_t n_sel_max,
-       float* __restrict__ out, eb_geom g, int64_t n_lookups, int64_t n_bags_total, int32_t n_samples,
-       int32_t nbg, uint32_t* err, hl_hook hk) {
+__device__ __forceinline__ void eb_fwd_body(uint32_t bid, uint32_t nblk, const void* w_hot_, const void* stg_,
+                                            int32_t stg_rows, uint32_t n_hot, uint32_t k_cap,
+                                            const int32_t* __restrict__ codes, const int32_t* __restrict__ bag_ptr,
+                                            int32_t bps, const int32_t* __restrict__ sample_ids,
+                                            const int32_t* n_sel_dev, int32_t n_sel_max, float* __restrict__ out,
+                                            eb_geom g, int32_t n_samples, int32_t nbg, uint32_t* err) {
   typedef typename RowIO<VEC, BF>::T T;
   const T* w_hot = (const T*)w_hot_;
   const T* stg = (const T*)stg_;
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, nw = blockDim.x >> 6;
   const int gi = lane / g.G, gl = lane - gi * g.G;
-  hl_hook_head(hk);
-  if (blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0 && bag_ptr[n_bags_total] != n_lookups)
-    hl_flag(err, HL_DEVERR_SHAPE);
-  if (gi >= g.NG) return;  // (never thread 0, which carries the handover)
+  if (gi >= g.NG) return;
   const int32_t colv = blockIdx.y * 64 + gl;
   const bool cact = colv < g.vpr;
   const int64_t col = (int64_t)colv * VEC;
   const int64_t total = (int64_t)eb_nsel(sample_ids, n_sel_dev, n_sel_max) * bps;
   const int64_t chunks = (total + nbg - 1) / nbg;
-  const int64_t stride = (int64_t)gridDim.x * 4 * g.NG;
-  for (int64_t c = ((int64_t)blockIdx.x * 4 + w) * g.NG + gi; c < chunks; c += stride) {
+  const int64_t stride = (int64_t)nblk * nw * g.NG;
+  for (int64_t c = ((int64_t)bid * nw + w) * g.NG + gi; c < chunks; c += stride) {
     const int64_t q0 = c * nbg;
     int64_t si = q0 / bps, j = q0 - si * bps;
     int64_t bag[FC];
@@ -482,6 +481,21 @@ eb_fwd(const void* w_hot_, const void* stg_, int32_t stg_rows, uint32_t n_hot, u
                             col, cact, gl, err);
     }
   }
+}
+
+template <int VEC, bool BF, int PART>
+__global__ void __launch_bounds__(256)
+eb_fwd(const void* w_hot, const void* stg, int32_t stg_rows, uint32_t n_hot, uint32_t k_cap,
+       const int32_t* __restrict__ codes, const int32_t* __restrict__ bag_ptr, int32_t bps,
+       const int32_t* __restrict__ sample_ids, const int32_t* n_sel_dev, int32_t n_sel_max,
+       float* __restrict__ out, eb_geom g, int64_t n_lookups, int64_t n_bags_total, int32_t n_samples,
+       int32_t nbg, uint32_t* err, hl_hook hk) {
+  hl_hook_head(hk);
+  if (blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0 && bag_ptr[n_bags_total] != n_lookups)
+    hl_flag(err, HL_DEVERR_SHAPE);
+  // (thread 0, which carries the handover, is in the first row group of every block)
+  eb_fwd_body<VEC, BF, PART>(blockIdx.x, gridDim.x, w_hot, stg, stg_rows, n_hot, k_cap, codes, bag_ptr, bps,
+                             sample_ids, n_sel_dev, n_sel_max, out, g, n_samples, nbg, err);
   hl_hook_tail(hk);
 }
 
@@ -1285,6 +1299,26 @@ eb_tail_r2(uint32_t n_tiles, void* w_hot, uint32_t n_hot, float lr, const float*
                                   n_hot, k_cap, codes, bag_ptr, out, err);
 }
 
+// The same launch for bags of several lookups (multi-hot), where nearly every
+// bag holds a staging row: the cold half of the forward bag by bag (part 2 of
+// the forward over every bag, one bag per row group) in place of the sorted
+// tail.
+template <int VEC, bool BF>
+__global__ void __launch_bounds__(RB_BLOCK)
+eb_bags_r2(uint32_t n_tiles, void* w_hot, uint32_t n_hot, float lr, const float* __restrict__ tfirst,
+           const float* __restrict__ tlast, const uint32_t* __restrict__ tflag, const uint32_t* __restrict__ tkey,
+           float* __restrict__ gc, uint32_t gc_rows, eb_geom g, void* stg, int32_t stg_rows, uint32_t k_cap,
+           const int32_t* __restrict__ codes, const int32_t* __restrict__ bag_ptr, int32_t bps, int32_t n_samples,
+           float* __restrict__ out, uint32_t* err) {
+  if (blockIdx.x < n_tiles) {
+    bw_reduce2_body<VEC, BF, true>(blockIdx.x, n_tiles, g, w_hot, stg, n_hot, lr, tfirst, tlast, tflag, tkey, gc,
+                                   gc_rows);
+    return;
+  }
+  eb_fwd_body<VEC, BF, 2>(blockIdx.x - n_tiles, gridDim.x - n_tiles, w_hot, stg, stg_rows, n_hot, k_cap, codes,
+                          bag_ptr, bps, nullptr, nullptr, n_samples, out, g, n_samples, 1, err);
+}
+
 // ----------------------------------------------------------------------------- host side
 static hl_status check_common(const hl_handle* h, const int32_t* codes, const int32_t* bag_ptr, int32_t n_samples,
                               int32_t bps, int64_t n_lookups, const int32_t* sample_ids, int32_t n_sel_max,
@@ -1629,11 +1663,19 @@ hl_status hl_embbag_finish_cold(hl_handle* h, void* w_hot, void* staging, int32_
   if (cb > 128) cb = 128;
   hipStream_t s = (hipStream_t)stream;
   const bool bf = h->dtype == HL_BF16;
+  // bags of several lookups: the cold half bag by bag, one bag per row group
+  const bool multi = n_lookups > 2 * n_bags;
+  const uint32_t fb = (uint32_t)std::min<int64_t>((n_bags + RB_WAVES * g.NG - 1) / (RB_WAVES * g.NG), 1 << 16);
 #define FIN(V, B)                                                                                                   \
   do {                                                                                                             \
-    HL_KERNEL(h, s, "eb_tail_r2", (eb_tail_r2<V, B>), dim3(tiles + tb, g.cchunks), dim3(RB_BLOCK), 0, s, tiles,    \
-              w_hot, h->n_hot, lr, ws.tfirst, ws.tlast, ws.tflag, ws.tkey, ws.gc, ws.gc_rows, sk, sv, n, ws.bnd, g, \
-              staging, stg_rows, h->k_cap, codes, bag_ptr, out, h->d_err);                                         \
+    if (multi)                                                                                                     \
+      HL_KERNEL(h, s, "eb_bags_r2", (eb_bags_r2<V, B>), dim3(tiles + fb, g.cchunks), dim3(RB_BLOCK), 0, s, tiles,  \
+                w_hot, h->n_hot, lr, ws.tfirst, ws.tlast, ws.tflag, ws.tkey, ws.gc, ws.gc_rows, g, staging,        \
+                stg_rows, h->k_cap, codes, bag_ptr, bps, n_samples, out, h->d_err);                                \
+    else                                                                                                           \
+      HL_KERNEL(h, s, "eb_tail_r2", (eb_tail_r2<V, B>), dim3(tiles + tb, g.cchunks), dim3(RB_BLOCK), 0, s, tiles,  \
+                w_hot, h->n_hot, lr, ws.tfirst, ws.tlast, ws.tflag, ws.tkey, ws.gc, ws.gc_rows, sk, sv, n, ws.bnd, \
+                g, staging, stg_rows, h->k_cap, codes, bag_ptr, out, h->d_err);                                    \
     HL_KERNEL(h, s, "bw_cold", (bw_cold<V, B>), dim3(cb, g.cchunks), dim3(256), 0, s, sk, n, g, staging, h->n_hot, \
               lr, ws.gc, ws.gc_rows, ws.bnd, hl_hook_take(h));                                                     \
   } while (0)
