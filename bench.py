@@ -631,16 +631,23 @@ MAIN_KERNELS = ("eb_fwd_hot", "eb_fwd_cold", "eb_fwd_tail", "eb_tail_r2", "eb_ba
                 "bw_cold")
 
 
-def fetch_overlap(hp, run):
-    """One traced run (every kernel, start and end on one time line): the
-    host-link fetch's time per launch and the shares of it during which a
-    main-stream kernel (the forwards and the backward), or any other kernel,
-    ran."""
+def fetch_overlap(hp, run, K):
+    """One run with the host-link copy and the main stream's kernels (the
+    forwards and the backward) traced, start and end on one time line (the
+    other kernels untraced: tracing every kernel changes the schedule): the
+    copy's time per launch, the share of it during which a main-stream kernel
+    ran, and the run's time per step (to compare with the untraced steps)."""
+    import torch
     from paper_2204_05436_amd import hotline as hl
     hl.hl_trace_enable(hp.h, 1 << 16)
-    hl.hl_trace_only(hp.h, None)
+    hl.hl_trace_only(hp.h, ",".join(("cg_fetch",) + MAIN_KERNELS))
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
     run()
+    e1.record()
+    torch.cuda.synchronize()
     recs = [hl.hl_trace_read_at(hp.h, i) for i in range(hl.hl_trace_count(hp.h))]
+    hl.hl_trace_only(hp.h, None)
     hl.hl_trace_enable(hp.h, 0)
 
     def union(iv):
@@ -656,11 +663,10 @@ def fetch_overlap(hp, run):
         return sum(max(0.0, min(f[1], b) - max(f[0], a)) for a, b in u)
     fetch = [(t0, t0 + d) for n, t0, d in recs if n == "cg_fetch"]
     main = union([(t0, t0 + d) for n, t0, d in recs if n in MAIN_KERNELS])
-    other = union([(t0, t0 + d) for n, t0, d in recs if n not in ("cg_fetch", "cg_scatter")])
     tf = sum(b - a for a, b in fetch)
     return {"fetch_us": 1e3 * tf / max(1, len(fetch)),
             "hidden_under_fwd_bwd": sum(covered(f, main) for f in fetch) / tf if tf else None,
-            "hidden_under_any_kernel": sum(covered(f, other) for f in fetch) / tf if tf else None}
+            "traced_ms_per_step": e0.elapsed_time(e1) / K}
 
 
 def fetch_study(hp, w, dprof, dmeas, side, K, ahead, traced, look_ahead_steps):
@@ -698,7 +704,7 @@ def fetch_study(hp, w, dprof, dmeas, side, K, ahead, traced, look_ahead_steps):
             torch.cuda.synchronize()
             ms["with_write_back" if wb else "no_write_back"] = e0.elapsed_time(e1) / K
         hp.writeback = False
-        ov = fetch_overlap(hp, lambda: look_ahead_steps(False))
+        ov = fetch_overlap(hp, lambda: look_ahead_steps(False), K)
         err = hp.device_error()
         if err:
             raise SystemExit(f"device error word {err:#x} in the fetch study")

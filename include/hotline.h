@@ -394,8 +394,10 @@ hl_status hl_last_device_error(hl_handle* h, uint32_t* err_out);
  * hl_trace_read waits for record i and returns its kernel name (static
  * string) and duration in ms; hl_trace_read_at also gives its start in ms
  * after record 0's start (records on several streams on one time line).
- * hl_trace_reset forgets the records.  hl_trace_only(h, name) records only
- * kernels of that name (NULL: all again). */
+ * hl_trace_reset forgets the records.  hl_trace_only(h, names) records only
+ * kernels of those comma-separated names, at most 255 characters (NULL: all
+ * again); tracing every kernel of a pipelined step changes its schedule (the
+ * traced launches take longer to issue), so a few names at a time. */
 hl_status hl_trace_enable(hl_handle* h, int32_t cap);
 hl_status hl_trace_only(hl_handle* h, const char* name);
 int32_t hl_trace_count(const hl_handle* h);

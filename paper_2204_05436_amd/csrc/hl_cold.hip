@@ -301,7 +301,12 @@ cg_codes(const int32_t* __restrict__ bag_ptr, uint64_t* table, cg_ws ws, int32_t
 template <typename V, bool TO_HOST>
 __global__ void __launch_bounds__(256)
 cg_copy(const uint32_t* __restrict__ ids, const int32_t* n_dev, int32_t cap, uint64_t n_rows, V* host, V* stg,
-        uint32_t upr, uint32_t* err) {
+        uint32_t upr, uint32_t* err, hl_hook hk) {
+  // a handover: block 0 signals as the copy starts (the copy before it on the
+  // stream is complete), and every block waits for its inputs first
+  hl_hook_head(hk);
+  hl_hook_gate(hk);
+  if (hk.gate) __syncthreads();
   const int32_t nd = *n_dev;
   if (nd < 0 || nd > cap) {
     if (blockIdx.x == 0 && threadIdx.x == 0) hl_flag(err, nd < 0 ? HL_DEVERR_OUT_OF_RANGE : HL_DEVERR_CAPACITY);
@@ -343,13 +348,14 @@ static hl_status cg_launch_copy(hl_handle* h, const uint32_t* ids, const int32_t
   uint64_t units = (uint64_t)(cap > 0 ? cap : 1) * (rb / 4);
   uint32_t g = (uint32_t)((units + 1023) / 1024);
   g = g < 1 ? 1 : (g > 64 ? 64 : g);
+  const hl_hook hk = to_host ? hl_hook{} : hl_hook_take(h);  // (the fetch carries the pipeline's handover)
 #define CG_COPY(V)                                                                                             \
   if (to_host)                                                                                                 \
     HL_KERNEL(h, s, "cg_scatter", (cg_copy<V, true>), dim3(g), dim3(256), 0, s, ids, n_dev, cap, h->n_rows,     \
-              (V*)host, (V*)stg, (uint32_t)(rb / sizeof(V)), h->d_err);                                        \
+              (V*)host, (V*)stg, (uint32_t)(rb / sizeof(V)), h->d_err, hl_hook{});                             \
   else                                                                                                         \
     HL_KERNEL(h, s, "cg_fetch", (cg_copy<V, false>), dim3(g), dim3(256), 0, s, ids, n_dev, cap, h->n_rows,      \
-              (V*)host, (V*)stg, (uint32_t)(rb / sizeof(V)), h->d_err);
+              (V*)host, (V*)stg, (uint32_t)(rb / sizeof(V)), h->d_err, hk);
   if (rb % 16 == 0 && ((uintptr_t)host | (uintptr_t)stg) % 16 == 0) { CG_COPY(uint4) }
   else if (rb % 8 == 0 && ((uintptr_t)host | (uintptr_t)stg) % 8 == 0) { CG_COPY(uint2) }
   else if (rb % 4 == 0 && ((uintptr_t)host | (uintptr_t)stg) % 4 == 0) { CG_COPY(uint32_t) }

@@ -47,10 +47,23 @@ static hl_status fill32(uint32_t* p, uint64_t n, uint32_t v, hipStream_t s) {
 hl_status hl_fill32(uint32_t* p, uint64_t n, uint32_t v, hipStream_t s) { return fill32(p, n, v, s); }
 
 // ----------------------------------------------------------------------------- tracing
+// name is one of the comma-separated names of list
+static bool trace_listed(const char* list, const char* name) {
+  const size_t n = strlen(name);
+  for (const char* p = list; *p;) {
+    const char* e = strchr(p, ',');
+    const size_t m = e ? (size_t)(e - p) : strlen(p);
+    if (m == n && strncmp(p, name, n) == 0) return true;
+    if (!e) break;
+    p = e + 1;
+  }
+  return false;
+}
+
 int hl_trace_take(const hl_handle* h, const char* name, hipEvent_t* a, hipEvent_t* b) {
   hl_trace* t = h ? h->trace : nullptr;
   if (!t || t->n >= t->cap) return -1;
-  if (t->only[0] && strcmp(t->only, name) != 0) return -1;
+  if (t->only[0] && !trace_listed(t->only, name)) return -1;
   const int i = t->n++;
   t->rec[i].name = name;
   *a = t->rec[i].a;

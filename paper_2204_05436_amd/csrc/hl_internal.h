@@ -17,7 +17,7 @@ struct hl_trace_rec {
 struct hl_trace {
   int32_t cap = 0, n = 0;
   hl_trace_rec* rec = nullptr;
-  char only[64] = {0};  // record only kernels of this name (empty: all)
+  char only[256] = {0};  // record only kernels of these comma-separated names (empty: all)
 };
 // A record for kernel `name` (its two events in *a, *b), or -1 when none is
 // taken (tracing off, full, or another name selected).

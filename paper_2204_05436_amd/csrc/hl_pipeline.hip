@@ -140,6 +140,9 @@ struct hl_pipeline {
   uint32_t np_last;       // last step that ran its own dispatch and cold plan (cold-gather hash table)
   uint32_t np_synced;     // the np_last a plan has waited for with a launch of its own
   uint32_t look_seen;     // the plan whose "cold list" the last step's last kernel waited for (0: none)
+  bool fetch_pend;        // the last copy's end signal (value fetch_pv) rides on the next copy, that of
+  uint32_t fetch_pv;      // plan fetch_plan (its kernel signals as it starts, and waits for its inputs)
+  uint32_t fetch_plan;
   uint32_t fetch_seen;    // the plan whose fetch waits the fetch stream's last signal launch also took
   uint32_t fetch_last;    // (0: none), and the step whose end it awaited for that plan's staging rows
 };
@@ -319,8 +322,14 @@ static hl_status pl_flush_done(hl_pipeline* p) {
   p->done_pend = false;
   return pl_sig(p, p->main, PF_DONE, p->done_v);
 }
+static hl_status pl_flush_fetch(hl_pipeline* p) {
+  if (!p->fetch_pend) return HL_OK;
+  p->fetch_pend = false;
+  return pl_sig(p, p->fetch, PF_FETCH, p->fetch_pv);
+}
 static hl_status pl_flush(hl_pipeline* p) {
   HL_TRY(pl_flush_sort(p));
+  HL_TRY(pl_flush_fetch(p));
   return pl_flush_done(p);
 }
 // a before b in sequence order (sequence numbers wrap)
@@ -533,6 +542,9 @@ extern "C" hl_status hl_pipeline_step(hl_pipeline* p, const hl_step_io* io, hl_s
   pl_plan* e = pl_pending(p, io->workspace);
   if (planned ? !e || !pl_same_plan(e->io, *io) : e != nullptr) return HL_ERR_INVALID_ARG;
   if (!planned) HL_TRY(pl_group(p));
+  // the last copy's end signal rides on this step's copy only if this is the
+  // plan it was kept for
+  if (p->fetch_pend && (!planned || e->seq != p->fetch_plan || io->staging_cap <= 0)) HL_TRY(pl_flush_fetch(p));
   const int32_t B = io->n_samples, bps = io->bags_per_sample, cap = io->staging_cap;
   const int64_t L = io->n_lookups;
   hipStream_t caller = (hipStream_t)stream, m = p->main, f = p->fetch, g = p->group;
@@ -554,21 +566,39 @@ extern "C" hl_status hl_pipeline_step(hl_pipeline* p, const hl_step_io* io, hl_s
     // (a pending end signal of the previous step is given by this step's
     // first main-stream launch, enqueued below)
     const uint32_t last = pl_stg_last(p, io->staging);
-    if (p->fetch_seen != e->seq || p->fetch_last != last)
-      HL_TRY(pl_hw(p, f, -1, 0, e->cold_flag, e->seq, last ? PF_DONE : -1, last));
-    p->fetch_seen = 0;
-    HL_TRY(hl_cold_fetch(h, io->cold_ids, io->n_cold, cap, io->w_host, io->staging, F));
-    // the signal launch also takes the next pending plan's fetch waits (its
-    // cold list, and the end of the last step that used its staging rows), so
-    // that plan's copy follows this one with no launch between them.  Only for
-    // a plan that waits for no step from this one on and has staging rows of its
-    // own: every signal it awaits is then enqueued by the end of this call.
+    if (p->fetch_pend) {
+      // the copy itself gives the last copy's end signal as it starts and
+      // waits for its inputs (every block, before it reads)
+      pl_hook(p, PF_FETCH, p->fetch_pv, e->cold_flag, e->seq);
+      h->hook.w2flag = last ? p->flags + PF_DONE : nullptr;
+      h->hook.w2v = last;
+      h->hook.gate = 1;
+      p->fetch_pend = false;
+      p->fetch_seen = 0;
+      PL_HOOKED(f, hl_cold_fetch(h, io->cold_ids, io->n_cold, cap, io->w_host, io->staging, F));
+    } else {
+      if (p->fetch_seen != e->seq || p->fetch_last != last)
+        HL_TRY(pl_hw(p, f, -1, 0, e->cold_flag, e->seq, last ? PF_DONE : -1, last));
+      p->fetch_seen = 0;
+      HL_TRY(hl_cold_fetch(h, io->cold_ids, io->n_cold, cap, io->w_host, io->staging, F));
+    }
+    // the end signal rides on the next pending plan's copy, which also waits
+    // for its own inputs (its cold list, and the end of the last step that
+    // used its staging rows), so the copies follow one another with no launch
+    // between them.  Only for a plan that waits for no step from this one on
+    // and has staging rows of its own: every signal it awaits is then enqueued
+    // by the end of this call (the signal is enqueued alone if anything else
+    // comes first, or at a sync).
     pl_plan* fx = nullptr;
     if (p->use_flags && !io->write_back)
       for (pl_plan& c : p->plans)
         if (c.pending && (!fx || pl_before(c.seq, fx->seq))) fx = &c;
     if (fx && ((fx->need && !pl_before(fx->need, q)) || fx->io.staging == io->staging)) fx = nullptr;
-    if (fx) {
+    if (fx && fx->io.staging_cap > 0) {
+      p->fetch_pend = true;
+      p->fetch_pv = q;
+      p->fetch_plan = fx->seq;
+    } else if (fx) {
       const uint32_t lx = pl_stg_last(p, fx->io.staging);
       HL_TRY(pl_hw(p, f, PF_FETCH, q, fx->cold_flag, fx->seq, lx ? PF_DONE : -1, lx));
       p->fetch_seen = fx->seq;
@@ -680,6 +710,9 @@ extern "C" hl_status hl_pipeline_step(hl_pipeline* p, const hl_step_io* io, hl_s
     HL_TRY(pl_sig(p, f, PF_WB, q));
   }
   if (tie) {
+    // (the step's end waits for its copy's end signal, which would otherwise
+    // ride on the next step's copy)
+    HL_TRY(pl_flush_fetch(p));
     HL_HIPTRY(hipEventRecord(p->ev_out, m));
     HL_HIPTRY(hipStreamWaitEvent(caller, p->ev_out, 0));
   }
