@@ -630,7 +630,6 @@ struct bw_ws {
   uint32_t* tkey;    // [tiles]
   float* gc;         // [n_max][D] gradient sums of staging rows, kept between the two halves of the apply
   uint32_t* bnd;     // [1] first sorted position whose key is not a hot slot (set by the first half)
-  uint32_t* gsmall;  // [HL_GROUP_SMALL] the grouping by table's per-chunk counts and per-table ranges
   uint32_t tiles, gc_rows;
 };
 
@@ -656,7 +655,6 @@ static void bw_carve(hl_carver& c, bw_ws& ws, uint32_t n_max, int64_t max_bags, 
   ws.gc_rows = compact ? 0 : n_max;
   ws.gc = c.take<float>((size_t)ws.gc_rows * D);
   ws.bnd = c.take<uint32_t>(1);
-  ws.gsmall = c.take<uint32_t>(HL_GROUP_SMALL);
 }
 
 size_t hl_bwd_ws_bytes(const hl_handle* h, int64_t max_lookups, int64_t max_bags) {
@@ -1023,7 +1021,10 @@ bw_reduce1(const uint32_t* __restrict__ keys, const uint32_t* __restrict__ vals,
 // Segments spanning tiles: the tile where a segment starts (flag L) sums its
 // own piece and the next tiles' first pieces up to the first tile that is not
 // wholly inside the segment.  Piece p is summed by group p % groups in
-// ascending p, then groups are added in order.
+// ascending p, then groups are added in order.  The loads that need nothing
+// but the tile index (its flag, key and piece, the next tiles' flags) are
+// issued together, and the row with the pieces of the later tiles, so a
+// segment takes two dependent rounds of loads.
 template <int VEC, bool BF, bool SPLIT>
 __device__ __forceinline__ void bw_reduce2_body(uint32_t t, uint32_t n_tiles, eb_geom g, void* w_hot, void* stg,
                                                 uint32_t n_hot, float lr, const float* __restrict__ tfirst,
@@ -1031,20 +1032,8 @@ __device__ __forceinline__ void bw_reduce2_body(uint32_t t, uint32_t n_tiles, eb
                                                 const uint32_t* __restrict__ tkey, float* __restrict__ gc,
                                                 uint32_t gc_rows) {
   typedef typename RowIO<VEC, BF>::T T;
-  if (!(tflag[t] & GF_L)) return;
   __shared__ uint32_t s_end;
   __shared__ float part[RB_WAVES * 64 * VEC];
-  if (threadIdx.x == 0) s_end = n_tiles;
-  __syncthreads();
-  for (uint32_t t2 = t + 1 + threadIdx.x; t2 < n_tiles; t2 += RB_BLOCK) {
-    if (!(tflag[t2] & GF_W)) {
-      atomicMin(&s_end, t2);
-      break;
-    }
-    if (t2 >= s_end) break;
-  }
-  __syncthreads();
-  const uint32_t tend = s_end;  // last tile holding a piece (not whole)
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int gi = lane / g.G, gl = lane - gi * g.G;
   const bool gact = gi < g.NG;
@@ -1052,16 +1041,45 @@ __device__ __forceinline__ void bw_reduce2_body(uint32_t t, uint32_t n_tiles, eb
   const int32_t colv = blockIdx.y * 64 + gl;
   const bool cact = gact && colv < g.vpr;
   const int64_t col = (int64_t)colv * VEC;
+  const uint32_t f = tflag[t];
+  const uint32_t key = tkey[t];
+  const uint32_t t2 = t + 1 + threadIdx.x;
+  const uint32_t f2 = t2 < n_tiles ? tflag[t2] : GF_W;
+  float v0[VEC];  // piece 0 (this tile's), summed by group 0
+#pragma unroll
+  for (int e = 0; e < VEC; ++e) v0[e] = 0.f;
+  if (grp == 0 && cact) ld_f32<VEC>(tlast + (int64_t)t * g.D + col, v0);
+  if (threadIdx.x == 0) s_end = n_tiles;
+  __syncthreads();
+  if (!(f & GF_L)) return;  // (the same for every thread of the block)
+  // the row, for group 0 (its address needs only the key)
+  const bool defer = SPLIT && bw_deferred(key, n_hot, gc_rows);
+  float wv[VEC];
+  T* rp = bw_row<VEC, BF>(w_hot, stg, n_hot, g.D, key) + col;
+  if (grp == 0 && cact && !defer) RowIO<VEC, BF>::load(rp, wv);
+  // the first tile after t that is not wholly inside the segment holds its
+  // last piece (a window of RB_BLOCK tiles at a time)
+  if (!(f2 & GF_W)) atomicMin(&s_end, t2);
+  __syncthreads();
+  uint32_t tend = s_end;
+  for (uint32_t base = t + 1 + RB_BLOCK; tend == n_tiles && base < n_tiles; base += RB_BLOCK) {
+    const uint32_t t3 = base + threadIdx.x;
+    if (t3 < n_tiles && !(tflag[t3] & GF_W)) atomicMin(&s_end, t3);
+    __syncthreads();
+    tend = s_end;
+  }
   const uint32_t npieces = (tend < n_tiles ? tend : n_tiles - 1) - t + 1;
   if (gact) {
     float acc[VEC];
 #pragma unroll
     for (int e = 0; e < VEC; ++e) acc[e] = 0.f;
+    if (grp == 0)
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) acc[e] += v0[e];
     if (cact) {
-      for (uint32_t p = grp; p < npieces; p += ngb) {
+      for (uint32_t p = grp == 0 ? ngb : grp; p < npieces; p += ngb) {
         float v[VEC];
-        const float* src = p == 0 ? tlast + (int64_t)t * g.D : tfirst + (int64_t)(t + p) * g.D;
-        ld_f32<VEC>(src + col, v);
+        ld_f32<VEC>(tfirst + (int64_t)(t + p) * g.D + col, v);
 #pragma unroll
         for (int e = 0; e < VEC; ++e) acc[e] += v[e];
       }
@@ -1077,17 +1095,13 @@ __device__ __forceinline__ void bw_reduce2_body(uint32_t t, uint32_t n_tiles, eb
     for (int q = 0; q < ngb; ++q)
 #pragma unroll
       for (int e = 0; e < VEC; ++e) acc[e] += part[(q * g.G + gl) * VEC + e];
-    const uint32_t key = tkey[t];
-    if (SPLIT && bw_deferred(key, n_hot, gc_rows)) {
+    if (defer) {
       st_f32<VEC>(gc + (int64_t)(key - n_hot) * g.D + col, acc);
       return;
     }
-    T* p = bw_row<VEC, BF>(w_hot, stg, n_hot, g.D, key) + col;
-    float wv[VEC];
-    RowIO<VEC, BF>::load(p, wv);
 #pragma unroll
     for (int e = 0; e < VEC; ++e) wv[e] -= lr * acc[e];
-    RowIO<VEC, BF>::store(p, wv);
+    RowIO<VEC, BF>::store(rp, wv);
   }
 }
 
@@ -1424,19 +1438,21 @@ static int bw_key_bits(const hl_handle* h, int32_t stg_rows) {
   return hl_bit_width((uint64_t)h->n_hot + (uint64_t)stg_rows);
 }
 
+// The reduction's grid: the blocks resident at once on the compute units the
+// launch may use (h->grid_cus), at most one per tile.
 template <int VEC, bool BF>
 static void launch_bwd(const hl_handle* h, uint32_t tiles, hipStream_t s, const uint32_t* sk, const uint32_t* sv,
                        uint32_t n, const float* dY, eb_geom g, void* w_hot, void* stg, uint32_t n_hot, float lr,
                        bw_ws& ws, int part) {
   const dim3 grid(tiles, g.cchunks);
   if (part == 0) {
-    HL_KERNEL(h, s, "bw_reduce1", (bw_reduce1<VEC, BF, false>), grid, dim3(RB_BLOCK), 0, s, sk, sv, n, dY, g, w_hot,
-              stg, n_hot, lr, ws.tfirst, ws.tlast, ws.tflag, ws.tkey, ws.gc, ws.gc_rows, ws.bnd, hl_hook{});
+    HL_KERNEL(h, s, "bw_reduce1", (bw_reduce1<VEC, BF, false>), grid, dim3(RB_BLOCK), 0, s, sk, sv, n, dY, g,
+              w_hot, stg, n_hot, lr, ws.tfirst, ws.tlast, ws.tflag, ws.tkey, ws.gc, ws.gc_rows, ws.bnd, hl_hook{});
     HL_KERNEL(h, s, "bw_reduce2", (bw_reduce2<VEC, BF, false>), grid, dim3(RB_BLOCK), 0, s, tiles, g, w_hot, stg,
               n_hot, lr, ws.tfirst, ws.tlast, ws.tflag, ws.tkey, ws.gc, ws.gc_rows);
   } else if (part == 1 || part == 3) {
-    HL_KERNEL(h, s, "bw_reduce1", (bw_reduce1<VEC, BF, true>), grid, dim3(RB_BLOCK), 0, s, sk, sv, n, dY, g, w_hot,
-              stg, n_hot, lr, ws.tfirst, ws.tlast, ws.tflag, ws.tkey, ws.gc, ws.gc_rows, ws.bnd,
+    HL_KERNEL(h, s, "bw_reduce1", (bw_reduce1<VEC, BF, true>), grid, dim3(RB_BLOCK), 0, s, sk, sv, n, dY, g,
+              w_hot, stg, n_hot, lr, ws.tfirst, ws.tlast, ws.tflag, ws.tkey, ws.gc, ws.gc_rows, ws.bnd,
               part == 3 ? hl_hook_take(h) : hl_hook{});
     if (part == 1)
       HL_KERNEL(h, s, "bw_reduce2", (bw_reduce2<VEC, BF, true>), grid, dim3(RB_BLOCK), 0, s, tiles, g, w_hot, stg,
@@ -1509,7 +1525,7 @@ hl_status hl_embbag_bwd_plan_signal(hl_handle* h, int32_t stg_rows, int32_t* cod
     hl_sort_result(ws.sort, bits, &rk, &rv);
     uint32_t* tk = rk == ws.sort.k0 ? ws.sort.k1 : ws.sort.k0;
     uint32_t* tv = rv == ws.sort.v0 ? ws.sort.v1 : ws.sort.v0;
-    st = hl_group_by_table(h, codes, bag_ptr, n_bags, stg_rows, tk, tv, rk, rv, ws.gsmall, sflag, sval,
+    st = hl_group_by_table(h, codes, bag_ptr, n_bags, stg_rows, tk, tv, rk, rv, sflag, sval,
                            cf && cf->table ? cf : nullptr, s);
     *sent = sflag != nullptr;
   } else {

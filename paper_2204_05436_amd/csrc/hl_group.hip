@@ -10,28 +10,29 @@
 // another at the back, gives such an order without a sort over the whole
 // mini-batch.  Two launches:
 //
-//  gt_prep  -- the pairs in table-major order (bag j = s T + t goes to
-//              position t E + s, E = bags per table): a block takes 64
-//              consecutive bag rows s, reads their offsets and codes
-//              (coalesced), forms the keys (the fused plan's cold-code
-//              rewrite included), and writes each table's 64 pairs through
-//              LDS.  It also clears gt_sort's status words.
+//  gt_prep  -- the keys in table-major order (bag j = s T + t goes to
+//              position t E + s, E = bags per table; the bag is implied by
+//              the position): a block takes GT_S consecutive bag rows s,
+//              reads their offsets and codes (coalesced), forms the keys (the
+//              fused plan's cold-code rewrite included), and writes each
+//              table's GT_S keys through LDS; it also stores, for its rows,
+//              the number of hot keys of the tables before each table.
 //  gt_sort  -- one block per table:
-//              the table's E pairs, keys compressed to [0, R_t) for hot slots
-//              (R_t = hi_t - lo_t) and above for staging rows, sorted in LDS
-//              by an LSD radix of as many 9-bit digits as the largest key
-//              needs; then the table's hot pairs go to the front of the
-//              output after those of the earlier tables, its others to the
-//              back before those of the earlier tables (offsets by a
-//              look-back over the earlier tables' counts).
+//              the table's E keys, compressed to [0, R_t) for hot slots
+//              (R_t = hi_t - lo_t) and above for staging rows, sorted with
+//              their positions in LDS by an LSD radix of as many 9-bit digits
+//              as the largest key needs; then the table's hot pairs go to the
+//              front of the output after those of the earlier tables, its
+//              others to the back before those of the earlier tables (both
+//              offsets from the prep blocks' counts).
 //
 // Ranks inside a wave: the lanes that hold the wave's first lane's digit
 // advance its counter once, together (stable by construction); every other
 // lane adds 1 to its digit's counter and takes the old value, an order among
 // same-digit lanes of one instruction that nothing specifies.  So the sorted
-// table is checked (keys ascending, bags ascending among equal keys: the
-// stable order, and the only one that passes) and, if the check fails, sorted
-// again with every rank formed from ballot peer masks.
+// table is checked (keys ascending, positions ascending among equal keys:
+// the stable order, and the only one that passes) and, if the check fails,
+// sorted again with every rank formed from ballot peer masks.
 #include "hl_internal.h"
 
 #define GT_S 32           // bag rows per gt_prep block
@@ -42,21 +43,19 @@
 #define GT_IMAX 8         // items per thread: at most GT_IMAX * GT_THREADS bags per table (no spills)
 #define GT_DBITS 9        // largest digit of the sort
 #define GT_NB (1 << GT_DBITS)
-#define GT_FLAG (1ull << 63)
 
 // ----------------------------------------------------------------------------- prep
 __global__ void __launch_bounds__(256)
 gt_prep(int32_t* codes, const int32_t* __restrict__ bag_ptr, int64_t n_bags, int32_t T, uint32_t E, uint32_t n_hot,
-        uint32_t k_cap, int32_t stg_rows, uint32_t* __restrict__ keys_tm, uint32_t* __restrict__ vals_tm,
-        uint64_t* __restrict__ tstat, int64_t n_lookups, uint32_t* sflag, uint32_t sv, uint32_t* err,
+        uint32_t k_cap, int32_t stg_rows, const uint32_t* __restrict__ tb, uint32_t* __restrict__ keys_tm,
+        uint32_t* __restrict__ cum, int64_t n_lookups, uint32_t* sflag, uint32_t sv, uint32_t* err,
         hl_cg_fused cf) {
   __shared__ uint32_t lk[GT_TMAX][GT_S];
+  __shared__ uint32_t hcnt[GT_TMAX];
   __shared__ uint32_t s_bad;
   bw_start_signal(sflag, sv);
   const int tid = threadIdx.x;
   if (tid == 0) s_bad = 0;
-  if (blockIdx.x == 0)
-    for (int t = tid; t < T; t += blockDim.x) tstat[t] = 0;
   const bool fits = cf.table && *cf.ncold <= (uint32_t)cf.cap;
   if (blockIdx.x == 0 && tid == 0) {
     if (bag_ptr[n_bags] != n_lookups) hl_flag(err, HL_DEVERR_SHAPE);
@@ -107,8 +106,21 @@ gt_prep(int32_t* codes, const int32_t* __restrict__ bag_ptr, int64_t n_bags, int
   for (uint32_t q = tid; q < nb; q += blockDim.x) {
     const uint32_t t = q / ns, s = q - t * ns;
     const uint64_t p = (uint64_t)t * E + s0 + s;
-    keys_tm[p] = lk[t][s];  // (a row of GT_S pairs of one table)
-    vals_tm[p] = (s0 + s) * (uint32_t)T + t;
+    keys_tm[p] = lk[t][s];  // (a row of GT_S keys of one table)
+  }
+  // hot keys per table (those gt_sort places at the front: a hot slot of the
+  // table's own range), then for each table those of the tables before it
+  if (tid < T) {
+    const uint32_t lo = tb[tid], R = tb[tid + 1] - lo;
+    uint32_t c = 0;
+    for (uint32_t s = 0; s < ns; ++s) c += (lk[tid][s] < n_hot && lk[tid][s] - lo < R) ? 1u : 0u;
+    hcnt[tid] = c;
+  }
+  __syncthreads();
+  if (tid <= T) {
+    uint32_t c = 0;
+    for (int t = 0; t < tid; ++t) c += hcnt[t];
+    cum[(uint64_t)blockIdx.x * (T + 1) + tid] = c;
   }
 }
 
@@ -137,14 +149,16 @@ __device__ __forceinline__ uint32_t gt_scan(uint32_t v, uint32_t* ws, uint32_t* 
 
 template <int ITEMS>
 __global__ void __launch_bounds__(GT_THREADS)
-gt_sort(const uint32_t* __restrict__ keys_tm, const uint32_t* __restrict__ vals_tm, uint32_t E, int32_t T,
-        uint32_t n, const uint32_t* __restrict__ tb, uint32_t n_hot, uint32_t* __restrict__ kout,
-        uint32_t* __restrict__ vout, uint64_t* tstat, uint32_t* err, int ballot_only, hl_hook hk) {
-  __shared__ uint32_t sk[ITEMS * GT_THREADS], sv[ITEMS * GT_THREADS];
+gt_sort(const uint32_t* __restrict__ keys_tm, const uint32_t* __restrict__ cum, uint32_t nblk, uint32_t E,
+        int32_t T, uint32_t n, const uint32_t* __restrict__ tb, uint32_t n_hot, uint32_t* __restrict__ kout,
+        uint32_t* __restrict__ vout, uint32_t* err, int ballot_only, hl_hook hk) {
+  // a sorted item in LDS: compressed key in the high word, table-major
+  // position in the low word (one 8-byte store and load per item and pass)
+  __shared__ uint64_t sx[ITEMS * GT_THREADS];
   __shared__ uint32_t wcnt[GT_WAVES][GT_NB];
   __shared__ uint32_t dofs[GT_NB];
   __shared__ uint32_t scan_ws[GT_WAVES];
-  __shared__ uint32_t s_lo, s_hi, s_max, s_sent;
+  __shared__ uint32_t s_lo, s_hi, s_max, s_sent, s_hb, s_ht;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   hl_hook_head(hk);  // a handover signal: the codes are complete (gt_prep has ended)
   const uint32_t t = blockIdx.x;
@@ -153,24 +167,33 @@ gt_sort(const uint32_t* __restrict__ keys_tm, const uint32_t* __restrict__ vals_
     s_hi = tb[t + 1];
     s_max = 0;
     s_sent = 0;
+    s_hb = 0;
+    s_ht = 0;
+  }
+  // hot keys of the earlier tables (hb) and up to this one (ht), summed over
+  // the prep blocks (loads issued with the keys')
+  uint32_t hb = 0, ht = 0;
+  for (uint32_t b = tid; b < nblk; b += GT_THREADS) {
+    hb += cum[(uint64_t)b * (T + 1) + t];
+    ht += cum[(uint64_t)b * (T + 1) + t + 1];
   }
   for (int j = tid; j < GT_WAVES * GT_NB; j += GT_THREADS) (&wcnt[0][0])[j] = 0;
   __syncthreads();
   const uint32_t lo = s_lo, R = s_hi - s_lo;
   const uint64_t lt = (1ull << lane) - 1ull;
-  uint32_t key[ITEMS], val[ITEMS];
+  uint32_t key[ITEMS], pos[ITEMS];
   for (int stable = ballot_only ? 1 : 0; stable < 2; ++stable) {
-    // the table's pairs: position w * 64 ITEMS + 64 k + lane (lookup order);
-    // compressed keys: hot slot - lo, or R + staging row, or (skipped: an
-    // invalid code, or a hot slot of another table's row) one past the largest
+    // the table's keys: position w * 64 ITEMS + 64 k + lane (lookup order);
+    // compressed: hot slot - lo, or R + staging row, or (skipped: an invalid
+    // code, or a hot slot of another table's row) one past the largest
     uint32_t kmax = 0;
     bool foreign = false, anysent = false;
 #pragma unroll
     for (int k = 0; k < ITEMS; ++k) {
-      const uint32_t pos = (uint32_t)w * (ITEMS * 64) + k * 64 + lane;
-      const bool valid = pos < E;
-      const uint32_t kk = keys_tm[(uint64_t)t * E + min(pos, E - 1)];
-      val[k] = vals_tm[(uint64_t)t * E + min(pos, E - 1)];
+      const uint32_t ps = (uint32_t)w * (ITEMS * 64) + k * 64 + lane;
+      const bool valid = ps < E;
+      const uint32_t kk = keys_tm[(uint64_t)t * E + min(ps, E - 1)];
+      pos[k] = ps;
       uint32_t c = EB_SENT;
       if (kk < n_hot) {
         if (kk - lo < R) c = kk - lo;
@@ -187,6 +210,17 @@ gt_sort(const uint32_t* __restrict__ keys_tm, const uint32_t* __restrict__ vals_
     for (int o = 32; o > 0; o >>= 1) kmax = max(kmax, (uint32_t)__shfl_xor(kmax, o));
     if (lane == 0) atomicMax(&s_max, kmax);
     if (anysent) s_sent = 1;
+    if (!stable || ballot_only) {
+#pragma unroll
+      for (int o = 32; o > 0; o >>= 1) {
+        hb += __shfl_xor(hb, o);
+        ht += __shfl_xor(ht, o);
+      }
+      if (lane == 0) {
+        atomicAdd(&s_hb, hb);
+        atomicAdd(&s_ht, ht);
+      }
+    }
     __syncthreads();
     const uint32_t sent = max(s_max + 1, R);  // after every valid key, never below R (not hot)
 #pragma unroll
@@ -200,30 +234,43 @@ gt_sort(const uint32_t* __restrict__ keys_tm, const uint32_t* __restrict__ vals_
     for (int p = 0; p < passes; ++p) {
       const int shift = p * b;
       uint32_t dg[ITEMS], rk[ITEMS];
+      if (stable) {
 #pragma unroll
-      for (int k = 0; k < ITEMS; ++k) {
-        const uint32_t pos = (uint32_t)w * (ITEMS * 64) + k * 64 + lane;
-        const bool valid = pos < E;
-        dg[k] = (key[k] >> shift) & mask;
-        if (stable) {
+        for (int k = 0; k < ITEMS; ++k) {
+          const bool valid = (uint32_t)w * (ITEMS * 64) + k * 64 + lane < E;
+          dg[k] = (key[k] >> shift) & mask;
           const uint64_t peers = hl_match_digit(dg[k], b, valid);
           const int leader = __ffsll((unsigned long long)peers) - 1;
           uint32_t bs = 0;
           if (valid && lane == leader) bs = atomicAdd(&wcnt[w][dg[k]], (uint32_t)__popcll(peers));
           bs = __shfl(bs, leader < 0 ? 0 : leader);
           rk[k] = bs + (uint32_t)__popcll(peers & lt);
-        } else {
-          // the lanes of the first lane's digit together, the others one by one
+        }
+      } else {
+        // the lanes of the first lane's digit together (their base read from
+        // the leading lane's register), the others one by one; every counter
+        // update of the items is issued before any old value is used (a
+        // wave's LDS operations execute in the order issued)
+        uint64_t m0[ITEMS];
+        uint32_t b0[ITEMS];
+#pragma unroll
+        for (int k = 0; k < ITEMS; ++k) {
+          const bool valid = (uint32_t)w * (ITEMS * 64) + k * 64 + lane < E;
+          dg[k] = (key[k] >> shift) & mask;
           const uint32_t d0 = __builtin_amdgcn_readfirstlane(dg[k]);
-          const uint64_t m0 = __ballot(valid && dg[k] == d0);
-          const bool in0 = (m0 >> lane) & 1ull;
-          const int l0 = m0 ? __ffsll((unsigned long long)m0) - 1 : 0;
-          uint32_t b0 = 0;
-          if (m0 && lane == l0) b0 = atomicAdd(&wcnt[w][d0], (uint32_t)__popcll(m0));
-          b0 = __shfl(b0, l0);
-          uint32_t r1 = 0;
-          if (valid && !in0) r1 = atomicAdd(&wcnt[w][dg[k]], 1u);
-          rk[k] = in0 ? b0 + (uint32_t)__popcll(m0 & lt) : r1;
+          m0[k] = __ballot(valid && dg[k] == d0);
+          const bool in0 = (m0[k] >> lane) & 1ull;
+          const int l0 = m0[k] ? __ffsll((unsigned long long)m0[k]) - 1 : 0;
+          b0[k] = 0;
+          rk[k] = 0;
+          if (m0[k] && lane == l0) b0[k] = atomicAdd(&wcnt[w][d0], (uint32_t)__popcll(m0[k]));
+          if (valid && !in0) rk[k] = atomicAdd(&wcnt[w][dg[k]], 1u);
+        }
+#pragma unroll
+        for (int k = 0; k < ITEMS; ++k) {
+          const int l0 = m0[k] ? __ffsll((unsigned long long)m0[k]) - 1 : 0;
+          const uint32_t base = __builtin_amdgcn_readlane(b0[k], l0);
+          if ((m0[k] >> lane) & 1ull) rk[k] = base + (uint32_t)__popcll(m0[k] & lt);
         }
       }
       __syncthreads();
@@ -242,35 +289,31 @@ gt_sort(const uint32_t* __restrict__ keys_tm, const uint32_t* __restrict__ vals_
       __syncthreads();
 #pragma unroll
       for (int k = 0; k < ITEMS; ++k) {
-        const uint32_t pos = (uint32_t)w * (ITEMS * 64) + k * 64 + lane;
-        if (pos < E) {
+        if ((uint32_t)w * (ITEMS * 64) + k * 64 + lane < E) {
           const uint32_t q = dofs[dg[k]] + wcnt[w][dg[k]] + rk[k];
-          sk[q] = key[k];
-          sv[q] = val[k];
+          sx[q] = ((uint64_t)key[k] << 32) | pos[k];
         }
       }
       __syncthreads();
 #pragma unroll
       for (int k = 0; k < ITEMS; ++k) {
-        const uint32_t pos = (uint32_t)w * (ITEMS * 64) + k * 64 + lane;
-        if (pos < E) {
-          key[k] = sk[pos];
-          val[k] = sv[pos];
+        const uint32_t ps = (uint32_t)w * (ITEMS * 64) + k * 64 + lane;
+        if (ps < E) {
+          const uint64_t x = sx[ps];
+          key[k] = (uint32_t)(x >> 32);
+          pos[k] = (uint32_t)x;
         }
       }
       for (int j = tid; j < GT_WAVES * GT_NB; j += GT_THREADS) (&wcnt[0][0])[j] = 0;
       __syncthreads();
     }
     if (stable) break;
-    // the check: keys ascending, bags ascending among equal keys
+    // the check: (key, position) strictly ascending (positions are distinct)
     bool broken = false;
 #pragma unroll
     for (int k = 0; k < ITEMS; ++k) {
-      const uint32_t pos = (uint32_t)w * (ITEMS * 64) + k * 64 + lane;
-      if (pos > 0 && pos < E && passes > 0) {
-        const uint32_t kp = sk[pos - 1], vp = sv[pos - 1];
-        broken = broken || kp > key[k] || (kp == key[k] && vp > val[k]);
-      }
+      const uint32_t ps = (uint32_t)w * (ITEMS * 64) + k * 64 + lane;
+      if (ps > 0 && ps < E && passes > 0) broken = broken || sx[ps - 1] >= (((uint64_t)key[k] << 32) | pos[k]);
     }
     if (!__syncthreads_or(broken)) break;
     if (tid == 0) {
@@ -279,59 +322,28 @@ gt_sort(const uint32_t* __restrict__ keys_tm, const uint32_t* __restrict__ vals_
     }
     __syncthreads();
   }
-  // hot pairs of this table (keys below R, sorted first)
-  uint32_t hc = 0;
-#pragma unroll
-  for (int k = 0; k < ITEMS; ++k) {
-    const uint32_t pos = (uint32_t)w * (ITEMS * 64) + k * 64 + lane;
-    hc += (pos < E && key[k] < R) ? 1u : 0u;
-  }
-  uint32_t h;
-  (void)gt_scan(hc, scan_ws, &h);
-  const uint32_t nh = E - h;
-  if (tid == 0)
-    __hip_atomic_store(tstat + t, GT_FLAG | ((uint64_t)nh << 32) | h, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  // the earlier tables' counts (each block publishes before it waits; the
-  // blocks of a grid start in index order and the grid fits the device, so
-  // the earlier tables' blocks run)
-  uint32_t eh = 0, enh = 0;
-  if (tid < (int)t) {
-    uint32_t spins = 0;
-    for (;;) {
-      const uint64_t x = __hip_atomic_load(tstat + tid, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      if (x & GT_FLAG) {
-        eh = (uint32_t)x;
-        enh = (uint32_t)(x >> 32) & 0x7FFFFFFFu;
-        break;
-      }
-      if (++spins > HL_SPIN_LIMIT) {
-        hl_flag(err, HL_DEVERR_STALL);
-        break;
-      }
-      __builtin_amdgcn_s_sleep(1);
-    }
-  }
-  uint32_t H, NH;
-  (void)gt_scan(eh, scan_ws, &H);
-  (void)gt_scan(enh, scan_ws, &NH);
-  const uint64_t nb0 = (uint64_t)n - NH - nh;  // this table's non-hot pairs, before the earlier tables'
+  // hot pairs of this table (keys below R, sorted first): h of them, after
+  // the earlier tables' H; the others before the earlier tables' E t - H
+  const uint32_t H = s_hb, h = s_ht - s_hb;
+  const uint64_t nb0 = (uint64_t)n - ((uint64_t)E * t - H) - (E - h);
   const uint32_t sent_key = max(s_max + 1, R);
 #pragma unroll
   for (int k = 0; k < ITEMS; ++k) {
-    const uint32_t pos = (uint32_t)w * (ITEMS * 64) + k * 64 + lane;
-    if (pos >= E) continue;
+    const uint32_t ps = (uint32_t)w * (ITEMS * 64) + k * 64 + lane;
+    if (ps >= E) continue;
+    if ((ps + 1 == h && key[k] >= R) || (ps == h && key[k] < R)) hl_flag(err, HL_DEVERR_INTERNAL);
     uint64_t o;
     uint32_t kk;
-    if (pos < h) {
-      o = (uint64_t)H + pos;
+    if (ps < h) {
+      o = (uint64_t)H + ps;
       kk = key[k] + lo;
     } else {
-      o = nb0 + (pos - h);
+      o = nb0 + (ps - h);
       kk = key[k] >= sent_key ? EB_SENT : n_hot + (key[k] - R);
     }
     if (o < n) {
       kout[o] = kk;
-      vout[o] = val[k];
+      vout[o] = pos[k] * (uint32_t)T + t;  // the bag of table-major position pos
     } else {
       hl_flag(err, HL_DEVERR_INTERNAL);
     }
@@ -342,22 +354,23 @@ gt_sort(const uint32_t* __restrict__ keys_tm, const uint32_t* __restrict__ vals_
 bool hl_group_by_table_ok(const hl_handle* h, int64_t n_lookups, int64_t n_bags) {
   const int32_t T = h->n_tables;
   if (n_lookups != n_bags || n_bags == 0 || T > GT_TMAX || n_bags % T != 0) return false;
-  return n_bags / T <= (int64_t)GT_IMAX * GT_THREADS;
+  const int64_t E = n_bags / T;
+  // the prep blocks' counts go where the table-major bags would
+  return E <= (int64_t)GT_IMAX * GT_THREADS && hl_div_up(E, GT_S) * (T + 1) <= n_lookups;
 }
 
 hl_status hl_group_by_table(hl_handle* h, int32_t* codes, const int32_t* bag_ptr, int64_t n_bags, int32_t stg_rows,
-                            uint32_t* k_tm, uint32_t* v_tm, uint32_t* kout, uint32_t* vout, uint32_t* small,
-                            uint32_t* sflag, uint32_t sv, const hl_cg_fused* cf, hipStream_t s) {
+                            uint32_t* k_tm, uint32_t* cum, uint32_t* kout, uint32_t* vout, uint32_t* sflag,
+                            uint32_t sv, const hl_cg_fused* cf, hipStream_t s) {
   const int32_t T = h->n_tables;
   const uint32_t E = (uint32_t)(n_bags / T);
-  static_assert(HL_GROUP_SMALL >= 2 * GT_TMAX, "grouping words");
-  uint64_t* tstat = reinterpret_cast<uint64_t*>(small);  // [T], cleared by gt_prep
+  const uint32_t nblk = hl_div_up(E, GT_S);
   const hl_hook hk = hl_hook_take(h);  // carried by gt_sort (the first sort pass takes it on the other path)
-  HL_KERNEL(h, s, "gt_prep", gt_prep, dim3(hl_div_up(E, GT_S)), dim3(256), 0, s, codes, bag_ptr, n_bags, T, E,
-            h->n_hot, h->k_cap, stg_rows, k_tm, v_tm, tstat, n_bags, sflag, sv, h->d_err, cf ? *cf : hl_cg_fused{});
+  HL_KERNEL(h, s, "gt_prep", gt_prep, dim3(nblk), dim3(256), 0, s, codes, bag_ptr, n_bags, T, E, h->n_hot, h->k_cap,
+            stg_rows, h->d_tb, k_tm, cum, n_bags, sflag, sv, h->d_err, cf ? *cf : hl_cg_fused{});
 #define GTS(I)                                                                                                    \
-  HL_KERNEL(h, s, "gt_sort", gt_sort<I>, dim3(T), dim3(GT_THREADS), 0, s, k_tm, v_tm, E, T, (uint32_t)n_bags,     \
-            h->d_tb, h->n_hot, kout, vout, tstat, h->d_err, h->ballot_ranks, hk)
+  HL_KERNEL(h, s, "gt_sort", gt_sort<I>, dim3(T), dim3(GT_THREADS), 0, s, k_tm, cum, nblk, E, T, (uint32_t)n_bags, \
+            h->d_tb, h->n_hot, kout, vout, h->d_err, h->ballot_ranks, hk)
   if (E <= 4 * GT_THREADS) GTS(4);
   else GTS(8);
 #undef GTS

@@ -349,14 +349,13 @@ hl_status hl_embbag_bwd_plan_signal(hl_handle* h, int32_t stg_rows, int32_t* cod
 // The backward's grouping of a one-hot mini-batch table by table (hl_group.hip):
 // taken when every bag holds one lookup (n_lookups = n_bags, checked per bag
 // on the device: HL_DEVERR_SHAPE otherwise), the bags split evenly over at
-// most 64 tables and a table has at most 8192 bags.  k_tm/v_tm: scratch of
-// n_bags pairs; kout/vout: the grouping; small: HL_GROUP_SMALL words (any
-// contents: the carved regions are shared with other calls).
-#define HL_GROUP_SMALL 128
+// most 64 tables and a table has at most 8192 bags.  k_tm: scratch of n_bags
+// keys; cum: scratch of n_bags words (the prep blocks' hot counts, at most
+// ceil(E / 32) (T + 1) of them); kout/vout: the grouping.
 bool hl_group_by_table_ok(const hl_handle* h, int64_t n_lookups, int64_t n_bags);
 hl_status hl_group_by_table(hl_handle* h, int32_t* codes, const int32_t* bag_ptr, int64_t n_bags, int32_t stg_rows,
-                            uint32_t* k_tm, uint32_t* v_tm, uint32_t* kout, uint32_t* vout, uint32_t* small,
-                            uint32_t* sflag, uint32_t sv, const hl_cg_fused* cf, hipStream_t s);
+                            uint32_t* k_tm, uint32_t* cum, uint32_t* kout, uint32_t* vout, uint32_t* sflag,
+                            uint32_t sv, const hl_cg_fused* cf, hipStream_t s);
 
 // ----------------------------------------------------------------------------- sort
 // Stable LSD radix sort of (key, value) uint32 pairs with digits of up to 11
