@@ -351,6 +351,19 @@ hl_status hl_embbag_bwd_apply(hl_handle* h, void* w_hot, void* staging, int32_t 
                               const float* dY, float lr, void* workspace, size_t ws_bytes,
                               hl_stream stream);
 
+/* hl_embbag_fwd over every sample followed by hl_embbag_bwd_plan over every
+ * sample, with the same results (out bit for bit, the same grouping left in
+ * the workspace for hl_embbag_bwd_apply).  The backward's grouping reads only
+ * the codes (Sec. IV: hot rows are updated on the GPU after both forwards),
+ * so for a one-hot mini-batch (one lookup per bag, grouped table by table)
+ * the sorts of the tables run in the forward's launch, on compute units the
+ * forward leaves free; other mini-batches take the two calls in turn.
+ * Arguments as those two calls; the workspace as hl_embbag_bwd_plan's. */
+hl_status hl_embbag_fwd_plan(hl_handle* h, const void* w_hot, const void* staging, int32_t staging_rows,
+                             const int32_t* codes, const int32_t* bag_ptr, int32_t n_samples,
+                             int32_t bags_per_sample, int64_t n_lookups, float* out, void* workspace,
+                             size_t ws_bytes, hl_stream stream);
+
 /* The grouping the last hl_embbag_bwd_plan left in `workspace` (with the same
  * staging_rows, n_samples, bags_per_sample and n_lookups; else
  * HL_ERR_INVALID_ARG), copied for inspection to keys_out and bags_out (device,

@@ -19,6 +19,7 @@
 #include <algorithm>
 #include <initializer_list>
 
+#include "hl_group_sort.h"
 #include "hl_internal.h"
 
 #ifndef RB_E
@@ -557,27 +558,28 @@ __device__ __forceinline__ void oh_load_rows(int64_t ch, int64_t n_bags, const o
 // of the next chunk are in flight while a chunk is stored, so each row group
 // keeps two chunks' rows loading.  A chunk with a bag that is not one-hot is
 // pooled bag by bag as eb_fwd does.  Same sums, same outputs.
+// The work of block bid of nblk (each of blockDim.x / 64 waves).
 template <int VEC, bool BF, int PART>
-__global__ void __launch_bounds__(256)
-eb_fwd_oh(const void* w_hot_, const void* stg_, int32_t stg_rows, uint32_t n_hot, uint32_t k_cap,
-          const int32_t* __restrict__ codes, const int32_t* __restrict__ bag_ptr, float* __restrict__ out, eb_geom g,
-          int64_t n_lookups, int64_t n_bags, uint32_t* err, hl_hook hk) {
+__device__ __forceinline__ void eb_fwd_oh_body(uint32_t bid, uint32_t nblk, const void* w_hot_, const void* stg_,
+                                               int32_t stg_rows, uint32_t n_hot, uint32_t k_cap,
+                                               const int32_t* __restrict__ codes,
+                                               const int32_t* __restrict__ bag_ptr, float* __restrict__ out,
+                                               eb_geom g, int64_t n_lookups, int64_t n_bags, uint32_t* err) {
   static_assert(PART == 0 || PART == 1, "whole forward or its hot half");
   typedef typename RowIO<VEC, BF>::T T;
   const T* w_hot = (const T*)w_hot_;
   const T* stg = (const T*)stg_;
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, nw = blockDim.x >> 6;
   const int gi = lane / g.G, gl = lane - gi * g.G;
-  hl_hook_head(hk);
-  if (blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0 && bag_ptr[n_bags] != n_lookups)
+  if (bid == 0 && blockIdx.y == 0 && threadIdx.x == 0 && bag_ptr[n_bags] != n_lookups)
     hl_flag(err, HL_DEVERR_SHAPE);
-  if (gi >= g.NG) return;  // (never thread 0, which carries the handover)
+  if (gi >= g.NG) return;
   const int32_t colv = blockIdx.y * 64 + gl;
   const bool cact = colv < g.vpr;
   const int64_t col = (int64_t)colv * VEC;
   const int64_t chunks = (n_bags + FC - 1) / FC;
-  const int64_t stride = (int64_t)gridDim.x * 4 * g.NG;
-  int64_t c = ((int64_t)blockIdx.x * 4 + w) * g.NG + gi;
+  const int64_t stride = (int64_t)nblk * nw * g.NG;
+  int64_t c = ((int64_t)bid * nw + w) * g.NG + gi;
   oh_meta<VEC, BF> m0, m1;
   float v0[FC][VEC];
   oh_load_meta<VEC, BF>(c, chunks, n_bags, bag_ptr, codes, m0);
@@ -617,7 +619,42 @@ eb_fwd_oh(const void* w_hot_, const void* stg_, int32_t stg_rows, uint32_t n_hot
     m0 = m1;
     m1 = m2;
   }
+}
+
+template <int VEC, bool BF, int PART>
+__global__ void __launch_bounds__(256)
+eb_fwd_oh(const void* w_hot, const void* stg, int32_t stg_rows, uint32_t n_hot, uint32_t k_cap,
+          const int32_t* __restrict__ codes, const int32_t* __restrict__ bag_ptr, float* __restrict__ out, eb_geom g,
+          int64_t n_lookups, int64_t n_bags, uint32_t* err, hl_hook hk) {
+  hl_hook_head(hk);
+  // (thread 0, which carries the handover, is in the first row group of every block)
+  eb_fwd_oh_body<VEC, BF, PART>(blockIdx.x, gridDim.x, w_hot, stg, stg_rows, n_hot, k_cap, codes, bag_ptr, out, g,
+                                n_lookups, n_bags, err);
   hl_hook_tail(hk);
+}
+
+// The forward over every bag of a one-hot mini-batch and the backward's
+// grouping in one launch: blocks [0, T) each sort a table (the grouping's
+// second step, after gt_prep: gt_sort_body), the others pool the bags.  The
+// sort reads the prep's keys and writes the grouping, the forward reads the
+// codes and rows and writes the pooled outputs: nothing one writes is read by
+// the other, so they run side by side (the sort on a few compute units at LDS
+// and latency speed, the HBM-bound forward on the rest).
+template <int VEC, bool BF, int ITEMS>
+__global__ void __launch_bounds__(GT_THREADS)
+eb_fwd_gt(const void* w_hot, const void* stg, int32_t stg_rows, uint32_t n_hot, uint32_t k_cap,
+          const int32_t* __restrict__ codes, const int32_t* __restrict__ bag_ptr, float* __restrict__ out, eb_geom g,
+          int64_t n_lookups, int64_t n_bags, const uint32_t* __restrict__ keys_tm, const uint32_t* __restrict__ cum,
+          uint32_t nblk, uint32_t E, int32_t T, const uint32_t* __restrict__ tb, uint32_t* __restrict__ kout,
+          uint32_t* __restrict__ vout, uint32_t* err, int ballot_only, hl_hook hk) {
+  hl_hook_head(hk);
+  if (blockIdx.x < (uint32_t)T) {
+    gt_sort_body<ITEMS>(blockIdx.x, keys_tm, cum, nblk, E, T, (uint32_t)n_bags, tb, n_hot, kout, vout, err,
+                        ballot_only);
+    return;
+  }
+  eb_fwd_oh_body<VEC, BF, 0>(blockIdx.x - T, gridDim.x - T, w_hot, stg, stg_rows, n_hot, k_cap, codes, bag_ptr, out,
+                             g, n_lookups, n_bags, err);
 }
 
 // ----------------------------------------------------------------------------- backward
@@ -1547,6 +1584,87 @@ hl_status hl_embbag_bwd_plan_signal(hl_handle* h, int32_t stg_rows, int32_t* cod
   if (st != HL_OK) return st;
   hl_ws_note(h, workspace, HL_WSK_BWD_PLAN, n_lookups, n_bags, stg_rows);
   hl_ws_find(h, workspace)->compact = compact;
+  return HL_OK;
+}
+
+// Compute units of the handle's device.
+static int eb_device_cus(const hl_handle* h) {
+  static int cus[64];
+  const int d = h->device >= 0 && h->device < 64 ? h->device : 0;
+  if (cus[d] <= 0) {
+    int v = 0;
+    if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, h->device) != hipSuccess || v <= 0) v = 1;
+    cus[d] = v;
+  }
+  return cus[d];
+}
+
+template <int VEC, bool BF>
+static void launch_fwd_gt(hl_handle* h, hipStream_t s, const void* w_hot, const void* stg, int32_t stg_rows,
+                          const int32_t* codes, const int32_t* bag_ptr, float* out, eb_geom g, int64_t n_lookups,
+                          int64_t n_bags, const uint32_t* k_tm, const uint32_t* cum, uint32_t nblk, uint32_t* kout,
+                          uint32_t* vout) {
+  const int32_t T = h->n_tables;
+  const uint32_t E = (uint32_t)(n_bags / T);
+  // one block per compute unit (each holds the sort's LDS): the tables' sorts
+  // and, on the other units, the forward
+  const int cus = eb_device_cus(h);
+  const uint32_t nf = (uint32_t)(cus > 2 * T ? cus - T : cus);
+  const hl_hook hk = hl_hook_take(h);
+#define FGT(I)                                                                                                    \
+  HL_KERNEL(h, s, "eb_fwd_gt", (eb_fwd_gt<VEC, BF, I>), dim3(T + nf), dim3(GT_THREADS), 0, s, w_hot, stg, stg_rows, \
+            h->n_hot, h->k_cap, codes, bag_ptr, out, g, n_lookups, n_bags, k_tm, cum, nblk, E, T, h->d_tb, kout,     \
+            vout, h->d_err, h->ballot_ranks, hk)
+  if (E <= 4 * GT_THREADS) FGT(4);
+  else FGT(8);
+#undef FGT
+}
+
+extern "C" hl_status hl_embbag_fwd_plan(hl_handle* h, const void* w_hot, const void* staging, int32_t stg_rows,
+                                        const int32_t* codes, const int32_t* bag_ptr, int32_t n_samples, int32_t bps,
+                                        int64_t n_lookups, float* out, void* workspace, size_t ws_bytes,
+                                        hl_stream stream) {
+  hl_status st = check_common(h, codes, bag_ptr, n_samples, bps, n_lookups, nullptr, n_samples, stg_rows);
+  if (st != HL_OK) return st;
+  if (!workspace) return HL_ERR_INVALID_ARG;
+  const int64_t n_bags = (int64_t)n_samples * bps;
+  const size_t es = h->dtype == HL_F32 ? 4 : 2;
+  const int vec = eb_pick_vec(h->dim, es, {w_hot, staging, out});
+  const eb_geom g = eb_make_geom(h->dim, vec);
+  const bool bf = h->dtype == HL_BF16;
+  // (rows of 4 elements per lane: wider rows would spill in blocks of GT_THREADS)
+  const bool fused = n_samples > 0 && n_lookups > 0 && n_lookups == n_bags && g.cchunks == 1 && vec == 4 &&
+                     hl_group_by_table_ok(h, n_lookups, n_bags);
+  if (!fused) {
+    // the two calls one after the other
+    st = hl_embbag_fwd(h, w_hot, staging, stg_rows, codes, bag_ptr, n_samples, bps, n_lookups, nullptr, nullptr,
+                       n_samples, out, stream);
+    if (st != HL_OK) return st;
+    return hl_embbag_bwd_plan(h, stg_rows, codes, bag_ptr, n_samples, bps, n_lookups, nullptr, nullptr, n_samples,
+                              workspace, ws_bytes, stream);
+  }
+  if (!out || (h->n_hot && !w_hot) || (stg_rows && !staging)) return HL_ERR_INVALID_ARG;
+  if (ws_bytes < bw_bytes(h, n_lookups, n_bags, false)) return HL_ERR_CAPACITY;
+  hl_ws_note(h, workspace, HL_WSK_OTHER);
+  hipStream_t s = (hipStream_t)stream;
+  hl_carver c = hl_carver::after_header(workspace, ws_bytes);
+  bw_ws ws;
+  bw_carve(c, ws, (uint32_t)n_lookups, n_bags, h->dim, false);
+  if ((uint64_t)n_lookups > ws.sort.n_max) return HL_ERR_CAPACITY;
+  uint32_t *rk, *rv;
+  hl_sort_result(ws.sort, bw_key_bits(h, stg_rows), &rk, &rv);
+  uint32_t* tk = rk == ws.sort.k0 ? ws.sort.k1 : ws.sort.k0;
+  uint32_t* tv = rv == ws.sort.v0 ? ws.sort.v1 : ws.sort.v0;
+  const uint32_t nblk = hl_group_prep(h, const_cast<int32_t*>(codes), bag_ptr, n_bags, stg_rows, tk, tv, nullptr, 0,
+                                      nullptr, s);
+#define FG(V, B) launch_fwd_gt<V, B>(h, s, w_hot, staging, stg_rows, codes, bag_ptr, out, g, n_lookups, n_bags, tk, tv, \
+                                     nblk, rk, rv)
+  if (bf) FG(4, true);
+  else FG(4, false);
+#undef FG
+  HL_LAUNCHED();
+  hl_ws_note(h, workspace, HL_WSK_BWD_PLAN, n_lookups, n_bags, stg_rows);
+  hl_ws_find(h, workspace)->compact = false;
   return HL_OK;
 }
 

@@ -353,6 +353,11 @@ hl_status hl_embbag_bwd_plan_signal(hl_handle* h, int32_t stg_rows, int32_t* cod
 // keys; cum: scratch of n_bags words (the prep blocks' hot counts, at most
 // ceil(E / 32) (T + 1) of them); kout/vout: the grouping.
 bool hl_group_by_table_ok(const hl_handle* h, int64_t n_lookups, int64_t n_bags);
+// The grouping's first launch alone (gt_prep); returns its block count, which
+// the sort takes (hl_group_sort.h: gt_sort_body).
+uint32_t hl_group_prep(hl_handle* h, int32_t* codes, const int32_t* bag_ptr, int64_t n_bags, int32_t stg_rows,
+                       uint32_t* k_tm, uint32_t* cum, uint32_t* sflag, uint32_t sv, const hl_cg_fused* cf,
+                       hipStream_t s);
 hl_status hl_group_by_table(hl_handle* h, int32_t* codes, const int32_t* bag_ptr, int64_t n_bags, int32_t stg_rows,
                             uint32_t* k_tm, uint32_t* cum, uint32_t* kout, uint32_t* vout, uint32_t* sflag,
                             uint32_t sv, const hl_cg_fused* cf, hipStream_t s);

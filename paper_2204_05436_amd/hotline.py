@@ -80,6 +80,7 @@ _SIGS = {
     "hl_embbag_fwd_part": (C.c_int, [P, P, P, I32, P, P, I32, I32, I64, P, P, I32, P, I32, P]),
     "hl_embbag_bwd_sgd": (C.c_int, [P, P, P, I32, P, P, I32, I32, I64, P, P, I32, P, F32, P, SZ, P]),
     "hl_embbag_bwd_plan": (C.c_int, [P, I32, P, P, I32, I32, I64, P, P, I32, P, SZ, P]),
+    "hl_embbag_fwd_plan": (C.c_int, [P, P, P, I32, P, P, I32, I32, I64, P, P, SZ, P]),
     "hl_embbag_bwd_apply": (C.c_int, [P, P, P, I32, I32, I32, I64, P, F32, P, SZ, P]),
     "hl_embbag_bwd_apply_part": (C.c_int, [P, P, P, I32, I32, I32, I64, P, F32, I32, P, SZ, P]),
     "hl_embbag_bwd_grouping": (C.c_int, [P, I32, I32, I32, I64, P, SZ, P, P, P]),
@@ -411,6 +412,13 @@ def hl_embbag_bwd_plan(h, staging_rows, codes, bag_ptr, n_samples, bags_per_samp
     _ck("hl_embbag_bwd_plan", lib().hl_embbag_bwd_plan(
         h.ptr, int(staging_rows), _p(codes), _p(bag_ptr), int(n_samples), int(bags_per_sample), int(n_lookups),
         _p(sample_ids), _p(n_sel_dev), int(n_sel_max), _p(ws), _nbytes(ws), _s(stream)))
+
+
+def hl_embbag_fwd_plan(h, w_hot, staging, staging_rows, codes, bag_ptr, n_samples, bags_per_sample, n_lookups, out, ws,
+                       stream=None):
+    _ck("hl_embbag_fwd_plan", lib().hl_embbag_fwd_plan(
+        h.ptr, _p(w_hot), _p(staging), int(staging_rows), _p(codes), _p(bag_ptr), int(n_samples),
+        int(bags_per_sample), int(n_lookups), _p(out), _p(ws), _nbytes(ws), _s(stream)))
 
 
 def hl_embbag_bwd_apply(h, w_hot, staging, staging_rows, n_samples, bags_per_sample, n_lookups, dY, lr, ws,

@@ -359,14 +359,23 @@ class HotPath:
             mark(6)
             hl.hl_embbag_fwd(self.h, self.w_hot, self.staging, self.staging_cap, self.codes, b.bag_ptr, B, bps, L,
                              self.nonpop, self.counts[1:], B, self.out)
+        elif b.dY is not None:
+            # the forward with the backward's grouping beside it, then the update
+            hl.hl_embbag_fwd_plan(self.h, self.w_hot, self.staging, self.staging_cap, self.codes, b.bag_ptr, B, bps, L,
+                                  self.out, self.ws)
+            mark(6)
         else:
             hl.hl_embbag_fwd(self.h, self.w_hot, self.staging, self.staging_cap, self.codes, b.bag_ptr, B, bps, L,
                              None, None, B, self.out)
             mark(6)
         mark(7)
         if b.dY is not None:
-            hl.hl_embbag_bwd_sgd(self.h, self.w_hot, self.staging, self.staging_cap, self.codes, b.bag_ptr, B, bps, L,
-                                 None, None, B, b.dY, lr, self.ws)
+            if split_fwd:
+                hl.hl_embbag_bwd_sgd(self.h, self.w_hot, self.staging, self.staging_cap, self.codes, b.bag_ptr, B,
+                                     bps, L, None, None, B, b.dY, lr, self.ws)
+            else:
+                hl.hl_embbag_bwd_apply(self.h, self.w_hot, self.staging, self.staging_cap, B, bps, L, b.dY, lr,
+                                       self.ws)
         mark(8)
         if self.writeback:
             hl.hl_cold_scatter(self.h, self.cold_ids, self.n_cold, self.staging_cap, self.staging, self.table.dev)

@@ -96,12 +96,13 @@ def _on_side(fn):
     main.wait_event(e1)
 
 
-def run_gpu_stages(hp: HotPath, prof, mb, dY, k=None, hot_ids=None, split=False):
+def run_gpu_stages(hp: HotPath, prof, mb, dY, k=None, hot_ids=None, split=False, fwd_plan=False):
     """All stages on the GPU, with snapshots.  Either profiles (k) or installs hot_ids.
     split: the dispatch kernel for ids, classify, partition and remap, the cold
     gather as plan + fetch and the backward as plan + apply, the fetch and the
     backward's plan each on a side stream (the pipelined schedule's entry
-    points)."""
+    points).  fwd_plan (not split): the forward over every sample with the
+    backward's plan (hl_embbag_fwd_plan), then the apply."""
     h = hp.h
     r = {}
     dprof = [to_device(p, hp.device) for p in prof]
@@ -171,6 +172,10 @@ def run_gpu_stages(hp: HotPath, prof, mb, dY, k=None, hot_ids=None, split=False)
                               hp.counts[1:], B, hp.out, 2)
         r["out"] = hp.out[:B * bps].cpu().numpy().copy()
         hl.hl_embbag_bwd_apply_part(h, hp.w_hot, hp.staging, hp.staging_cap, B, bps, L, b.dY, hp.w.lr, 2, hp.ws)
+    elif fwd_plan:
+        hl.hl_embbag_fwd_plan(h, hp.w_hot, hp.staging, hp.staging_cap, hp.codes, b.bag_ptr, B, bps, L, hp.out, hp.ws)
+        r["out"] = hp.out[:B * bps].cpu().numpy().copy()
+        hl.hl_embbag_bwd_apply(h, hp.w_hot, hp.staging, hp.staging_cap, B, bps, L, b.dY, hp.w.lr, hp.ws)
     else:
         hl.hl_embbag_fwd(h, hp.w_hot, hp.staging, hp.staging_cap, hp.codes, b.bag_ptr, B, bps, L, hp.pop,
                          hp.counts[0:], B, hp.out)

@@ -839,3 +839,41 @@ def test_grouping_ranks_fallback(name):
             hp.close()
             table.close()
     assert np.array_equal(groupings[0][0], groupings[1][0]) and np.array_equal(groupings[0][1], groupings[1][1])
+
+
+@pytest.mark.parametrize("name,full", [("dlrm-large", True), ("dlrm-large", False), ("dlrm-small", False),
+                                       ("tbsm", False), ("tiny", False), ("multi-hot", False)])
+def test_fwd_plan(name, full):
+    """hl_embbag_fwd_plan (the forward over every sample with the backward's
+    plan; for one-hot mini-batches the tables' sorts run in the forward's
+    launch) then the apply: pooled outputs, the grouping and the updated rows
+    bit for bit those of hl_embbag_fwd then hl_embbag_bwd_sgd, and within
+    tolerance of the oracle."""
+    w = configs.WORKLOADS[name]
+    if not full:
+        w = configs.scaled(w, batch=700 if name != "tiny" else 1024, row_scale=0.004 if name != "tiny" else 1.0,
+                           name=name + "-fp")
+    rows = W.table_rows(w)
+    n_rows = int(rows.sum(dtype=np.int64))
+    k_cap = w.k_cap(n_rows)
+    prof = [W.make_batch(w, rows, i) for i in range(4 if not full else w.profile_batches)]
+    mb = W.make_batch(w, rows, w.profile_batches)
+    dY = W.make_dy(w, w.profile_batches, mb.n_bags)
+    table = make_table(w, n_rows)
+    res = []
+    try:
+        for fp in (False, True):
+            hp = HotPath(w, rows, table, max(b.n_lookups for b in prof + [mb]), mb.n_samples)
+            try:
+                res.append(run_gpu_stages(hp, prof, mb, dY, fwd_plan=fp))
+            finally:
+                hp.close()
+        o = run_oracle(w, rows, prof, mb, dY, table.array, k_cap)
+    finally:
+        table.close()
+    a, b = res
+    assert a["deverr"] == 0 and b["deverr"] == 0
+    for key in ("codes", "cold", "out", "w_hot_new", "staging_new"):
+        assert np.array_equal(np.asarray(a[key]).view(np.uint8), np.asarray(b[key]).view(np.uint8)), key
+    assert np.array_equal(a["grouping"][0], b["grouping"][0]) and np.array_equal(a["grouping"][1], b["grouping"][1])
+    compare(w, b, o, k_cap)
