@@ -500,64 +500,20 @@ eb_fwd(const void* w_hot, const void* stg, int32_t stg_rows, uint32_t n_hot, uin
   hl_hook_tail(hk);
 }
 
-// The same for a one-hot mini-batch over every sample (as many lookups as
-// bags: bag j is expected to hold lookup j alone), PART 0 or 1: the codes are
-// loaded with the bag offsets that confirm them, one chunk ahead, and the rows
-// of the next chunk are in flight while a chunk is stored, so each row group
-// keeps two chunks' rows loading.  A chunk with a bag that is not one-hot is
-// pooled bag by bag as eb_fwd does.  Same sums, same outputs.
-template <int VEC, bool BF>
-struct oh_meta {
-  uint32_t code[FC];
-  bool oh;  // every bag of the chunk holds exactly its own lookup
-};
+// The forward of a one-hot mini-batch over every sample (as many lookups as
+// bags: bag j is expected to hold lookup j alone), PART 0 or 1, wave by wave:
+// a wave takes a unit of NG * OH_RPG consecutive bags (OH_RPG per row group,
+// at most 256 bags), loads their offsets and codes one bag per lane and
+// passes the codes to the row groups through LDS; when every bag of the unit
+// holds exactly its own lookup, each row group issues its rows' loads all at
+// once, then stores them, so a unit costs two dependent rounds of loads.  A
+// unit with a bag that is not one-hot is pooled bag by bag as eb_fwd does.
+// Same sums, same outputs: the row itself (PART 1: its hot rows only, zero
+// for a staging row; zero for a code that names no row).
+#define OH_RPG(VEC) ((VEC) >= 8 ? 8 : 16)  // rows per row group per unit (at most): up to 64 floats per lane in flight
+#define OH_UNIT 256                // bags per unit (at most)
+#define OH_MAXW (GT_THREADS / 64)
 
-template <int VEC, bool BF>
-__device__ __forceinline__ void oh_load_meta(int64_t ch, int64_t chunks, int64_t n_bags,
-                                             const int32_t* __restrict__ bag_ptr, const int32_t* __restrict__ codes,
-                                             oh_meta<VEC, BF>& m) {
-  int32_t lo[FC], hi[FC];
-#pragma unroll
-  for (int u = 0; u < FC; ++u) {
-    const int64_t b = ch * FC + u;
-    const bool v = ch < chunks && b < n_bags;
-    lo[u] = v ? bag_ptr[b] : (int32_t)b;
-    hi[u] = v ? bag_ptr[b + 1] : (int32_t)b + 1;
-    m.code[u] = v ? (uint32_t)codes[b] : 0u;
-  }
-  m.oh = true;
-#pragma unroll
-  for (int u = 0; u < FC; ++u) m.oh = m.oh && lo[u] == (int32_t)(ch * FC + u) && hi[u] == lo[u] + 1;
-}
-
-// a chunk's rows (PART 1: its hot rows only), zero for a code that names no row
-template <int VEC, bool BF, int PART>
-__device__ __forceinline__ void oh_load_rows(int64_t ch, int64_t n_bags, const oh_meta<VEC, BF>& m,
-                                             const typename RowIO<VEC, BF>::T* w_hot,
-                                             const typename RowIO<VEC, BF>::T* stg, int32_t stg_rows, uint32_t n_hot,
-                                             uint32_t k_cap, int64_t D, int64_t col, bool cact, float (&v)[FC][VEC]) {
-#pragma unroll
-  for (int u = 0; u < FC; ++u) {
-    const uint32_t cu = m.code[u];
-    const bool in = ch * FC + u < n_bags && cact;
-    const bool hot = cu < n_hot;
-    const bool cold = PART == 0 && cu >= k_cap && cu - k_cap < (uint32_t)stg_rows;
-    if (in && (hot || cold)) {
-      const typename RowIO<VEC, BF>::T* p = hot ? w_hot + (int64_t)cu * D : stg + (int64_t)(cu - k_cap) * D;
-      RowIO<VEC, BF>::load(p + col, v[u]);
-    } else {
-#pragma unroll
-      for (int e = 0; e < VEC; ++e) v[u][e] = 0.f;
-    }
-  }
-}
-
-// The same for a one-hot mini-batch over every sample (as many lookups as
-// bags: bag j is expected to hold lookup j alone), PART 0 or 1: the codes are
-// loaded with the bag offsets that confirm them, one chunk ahead, and the rows
-// of the next chunk are in flight while a chunk is stored, so each row group
-// keeps two chunks' rows loading.  A chunk with a bag that is not one-hot is
-// pooled bag by bag as eb_fwd does.  Same sums, same outputs.
 // The work of block bid of nblk (each of blockDim.x / 64 waves).
 template <int VEC, bool BF, int PART>
 __device__ __forceinline__ void eb_fwd_oh_body(uint32_t bid, uint32_t nblk, const void* w_hot_, const void* stg_,
@@ -567,57 +523,77 @@ __device__ __forceinline__ void eb_fwd_oh_body(uint32_t bid, uint32_t nblk, cons
                                                eb_geom g, int64_t n_lookups, int64_t n_bags, uint32_t* err) {
   static_assert(PART == 0 || PART == 1, "whole forward or its hot half");
   typedef typename RowIO<VEC, BF>::T T;
+  __shared__ uint32_t s_code[OH_MAXW][OH_UNIT];
   const T* w_hot = (const T*)w_hot_;
   const T* stg = (const T*)stg_;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, nw = blockDim.x >> 6;
   const int gi = lane / g.G, gl = lane - gi * g.G;
   if (bid == 0 && blockIdx.y == 0 && threadIdx.x == 0 && bag_ptr[n_bags] != n_lookups)
     hl_flag(err, HL_DEVERR_SHAPE);
-  if (gi >= g.NG) return;
+  const bool gact = gi < g.NG;
   const int32_t colv = blockIdx.y * 64 + gl;
-  const bool cact = colv < g.vpr;
+  const bool cact = gact && colv < g.vpr;
   const int64_t col = (int64_t)colv * VEC;
-  const int64_t chunks = (n_bags + FC - 1) / FC;
-  const int64_t stride = (int64_t)nblk * nw * g.NG;
-  int64_t c = ((int64_t)bid * nw + w) * g.NG + gi;
-  oh_meta<VEC, BF> m0, m1;
-  float v0[FC][VEC];
-  oh_load_meta<VEC, BF>(c, chunks, n_bags, bag_ptr, codes, m0);
-  oh_load_rows<VEC, BF, PART>(c, n_bags, m0, w_hot, stg, stg_rows, n_hot, k_cap, g.D, col, cact && m0.oh, v0);
-  oh_load_meta<VEC, BF>(c + stride, chunks, n_bags, bag_ptr, codes, m1);
-  for (; c < chunks; c += stride) {
-    float v1[FC][VEC];
-    oh_load_rows<VEC, BF, PART>(c + stride, n_bags, m1, w_hot, stg, stg_rows, n_hot, k_cap, g.D, col,
-                                cact && m1.oh && c + stride < chunks, v1);
-    oh_meta<VEC, BF> m2;
-    oh_load_meta<VEC, BF>(c + 2 * stride, chunks, n_bags, bag_ptr, codes, m2);
-    if (m0.oh) {
+  constexpr int RPG = OH_RPG(VEC);
+  const int rpg = g.NG * RPG <= OH_UNIT ? RPG : OH_UNIT / g.NG;
+  const int64_t ub = (int64_t)g.NG * rpg;  // bags per unit
+  const int64_t units = (n_bags + ub - 1) / ub;
+  uint32_t* sc = s_code[w];
+  for (int64_t u = (int64_t)bid * nw + w; u < units; u += (int64_t)nblk * nw) {
+    const int64_t b0 = u * ub;
+    // offsets and codes, one bag per lane
+    bool bad = false;
 #pragma unroll
-      for (int u = 0; u < FC; ++u) {
-        const int64_t b = c * FC + u;
-        if (b >= n_bags) continue;
-        const uint32_t cu = m0.code[u];
-        const bool named = cu < n_hot || (cu >= k_cap && cu - k_cap < (uint32_t)stg_rows);
-        if (!named && gl == 0) hl_flag(err, HL_DEVERR_BAD_CODE);
-        if (cact) st_f32_nt<VEC>(out + b * g.D + col, v0[u]);
-      }
-    } else {
-      // some bag of this chunk is not one-hot: bag by bag, its hot rows then
-      // (PART 0) its staging rows, in CSR order
-      for (int u = 0; u < FC; ++u) {
-        const int64_t b = c * FC + u;
-        if (b >= n_bags) break;
+    for (int k = 0; k < OH_UNIT / 64; ++k) {
+      const int64_t q = (int64_t)k * 64 + lane, b = b0 + q;
+      if (q < ub && b < n_bags) {
         const int32_t lo = bag_ptr[b], hi = bag_ptr[b + 1];
-        eb_bag<VEC, BF, PART>(out + b * g.D + col, w_hot, stg, stg_rows, n_hot, k_cap, codes, lo, hi, g, col, cact, gl,
-                              err);
+        const uint32_t cu = (uint32_t)codes[b];
+        sc[q] = cu;
+        bad = bad || lo != b || hi != b + 1;
+        if (!bad && !(cu < n_hot || (cu >= k_cap && cu - k_cap < (uint32_t)stg_rows))) hl_flag(err, HL_DEVERR_BAD_CODE);
       }
     }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    if (__ballot(bad)) {
+      // some bag of the unit is not one-hot: bag by bag, its hot rows then
+      // (PART 0) its staging rows, in CSR order
+      if (gact)
+        for (int i = 0; i < rpg; ++i) {
+          const int64_t b = b0 + (int64_t)gi * rpg + i;
+          if (b >= n_bags) break;
+          eb_bag<VEC, BF, PART>(out + b * g.D + col, w_hot, stg, stg_rows, n_hot, k_cap, codes, bag_ptr[b],
+                                bag_ptr[b + 1], g, col, cact, gl, err);
+        }
+    } else if (gact) {
+      float v[RPG][VEC];
 #pragma unroll
-    for (int u = 0; u < FC; ++u)
+      for (int i = 0; i < RPG; ++i) {
+        const int64_t b = b0 + (int64_t)gi * rpg + i;
+        const uint32_t cu = i < rpg ? sc[gi * rpg + i] : 0u;
+        const bool in = i < rpg && b < n_bags && cact;
+        const bool hot = cu < n_hot;
+        const bool cold = PART == 0 && cu >= k_cap && cu - k_cap < (uint32_t)stg_rows;
+        if (in && (hot || cold)) {
+          const T* p = hot ? w_hot + (int64_t)cu * g.D : stg + (int64_t)(cu - k_cap) * g.D;
+          RowIO<VEC, BF>::load(p + col, v[i]);
+        } else {
 #pragma unroll
-      for (int e = 0; e < VEC; ++e) v0[u][e] = v1[u][e];
-    m0 = m1;
-    m1 = m2;
+          for (int e = 0; e < VEC; ++e) v[i][e] = 0.f;
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < RPG; ++i) {
+        const int64_t b = b0 + (int64_t)gi * rpg + i;
+        if (i < rpg && b < n_bags && cact) st_f32_nt<VEC>(out + b * g.D + col, v[i]);
+      }
+    }
+    // (the next unit's codes overwrite sc: every lane has read this one's)
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
   }
 }
 
@@ -640,6 +616,12 @@ eb_fwd_oh(const void* w_hot, const void* stg, int32_t stg_rows, uint32_t n_hot, 
 // codes and rows and writes the pooled outputs: nothing one writes is read by
 // the other, so they run side by side (the sort on a few compute units at LDS
 // and latency speed, the HBM-bound forward on the rest).
+#ifdef HL_FG_PROBE
+__device__ uint64_t fg_probe[1024][2];
+extern "C" int hl_probe_read_fg(uint64_t* host) {
+  return (int)hipMemcpyFromSymbol(host, HIP_SYMBOL(fg_probe), sizeof(fg_probe));
+}
+#endif
 template <int VEC, bool BF, int ITEMS>
 __global__ void __launch_bounds__(GT_THREADS)
 eb_fwd_gt(const void* w_hot, const void* stg, int32_t stg_rows, uint32_t n_hot, uint32_t k_cap,
@@ -648,13 +630,20 @@ eb_fwd_gt(const void* w_hot, const void* stg, int32_t stg_rows, uint32_t n_hot, 
           uint32_t nblk, uint32_t E, int32_t T, const uint32_t* __restrict__ tb, uint32_t* __restrict__ kout,
           uint32_t* __restrict__ vout, uint32_t* err, int ballot_only, hl_hook hk) {
   hl_hook_head(hk);
+#ifdef HL_FG_PROBE
+  if (threadIdx.x == 0 && blockIdx.x < 1024) fg_probe[blockIdx.x][0] = wall_clock64();
+#endif
   if (blockIdx.x < (uint32_t)T) {
     gt_sort_body<ITEMS>(blockIdx.x, keys_tm, cum, nblk, E, T, (uint32_t)n_bags, tb, n_hot, kout, vout, err,
                         ballot_only);
-    return;
-  }
+  } else {
   eb_fwd_oh_body<VEC, BF, 0>(blockIdx.x - T, gridDim.x - T, w_hot, stg, stg_rows, n_hot, k_cap, codes, bag_ptr, out,
                              g, n_lookups, n_bags, err);
+  }
+#ifdef HL_FG_PROBE
+  __syncthreads();
+  if (threadIdx.x == 0 && blockIdx.x < 1024) fg_probe[blockIdx.x][1] = wall_clock64();
+#endif
 }
 
 // ----------------------------------------------------------------------------- backward
