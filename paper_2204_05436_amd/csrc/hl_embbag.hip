@@ -1464,8 +1464,6 @@ static int bw_key_bits(const hl_handle* h, int32_t stg_rows) {
   return hl_bit_width((uint64_t)h->n_hot + (uint64_t)stg_rows);
 }
 
-// The reduction's grid: the blocks resident at once on the compute units the
-// launch may use (h->grid_cus), at most one per tile.
 template <int VEC, bool BF>
 static void launch_bwd(const hl_handle* h, uint32_t tiles, hipStream_t s, const uint32_t* sk, const uint32_t* sv,
                        uint32_t n, const float* dY, eb_geom g, void* w_hot, void* stg, uint32_t n_hot, float lr,
