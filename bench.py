@@ -237,10 +237,9 @@ def main():
                                   hp.counts[1:], B, hp.out, 2)
             hl.hl_embbag_bwd_apply_part(h, hp.w_hot, hp.staging, cap, B, bps, L, b.dY, w.lr, 2, hp.ws)
             # the variants of the calls in order on one stream: the forward over
-            # every bag, the whole backward
-            hl.hl_embbag_fwd(h, hp.w_hot, hp.staging, cap, hp.codes, b.bag_ptr, B, bps, L, None, None, B, hp.out)
-            hl.hl_embbag_bwd_sgd(h, hp.w_hot, hp.staging, cap, hp.codes, b.bag_ptr, B, bps, L, None, None, B, b.dY,
-                                 w.lr, hp.ws)
+            # every bag with the backward's plan, then the apply
+            hl.hl_embbag_fwd_plan(h, hp.w_hot, hp.staging, cap, hp.codes, b.bag_ptr, B, bps, L, hp.out, hp.ws)
+            hl.hl_embbag_bwd_apply(h, hp.w_hot, hp.staging, cap, B, bps, L, b.dY, w.lr, hp.ws)
         torch.cuda.synchronize()
         n_cal = 256 << 20
         src = torch.ones(n_cal // 4, dtype=torch.float32, device=dev)
@@ -734,11 +733,13 @@ def counter_traffic(kernel, workload, alone=False):
     m = re.search(r"```traffic_alone\n(.*?)```" if alone else r"```traffic\n(.*?)```", text, re.S)
     if not m:
         return None
+    # a line: kernel, bytes per launch, then (source file, sha1) pairs of the
+    # files its code comes from
     for line in m.group(1).splitlines():
         f = line.split()
-        if len(f) == 4 and f[0] == kernel:
-            src = os.path.join(here, f[2])
-            if os.path.exists(src) and hashlib.sha1(open(src, "rb").read()).hexdigest() == f[3]:
+        if len(f) >= 4 and len(f) % 2 == 0 and f[0] == kernel:
+            srcs = [(os.path.join(here, f[i]), f[i + 1]) for i in range(2, len(f), 2)]
+            if all(os.path.exists(p) and hashlib.sha1(open(p, "rb").read()).hexdigest() == h for p, h in srcs):
                 return int(f[1])
     return None
 
