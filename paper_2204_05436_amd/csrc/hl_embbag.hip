@@ -1143,8 +1143,12 @@ bw_reduce2(uint32_t n_tiles, eb_geom g, void* w_hot, void* stg, uint32_t n_hot, 
 // The deferred staging-row updates: every run end in the sorted keys whose key
 // is a staging row below gc_rows applies row <- round(row - lr * gc[u]), the
 // same arithmetic as the one-pass update.  Only the sorted tail from *bnd (the
-// end of the hot slots, found by the first half) is scanned.  A wave tests 64
-// positions, then its row groups take the run ends it found, a group per row.
+// end of the hot slots, found by the first half) is scanned.  A wave tests
+// CW_POS positions at a time (one per lane), then its row groups take the run
+// ends found, each group its share at once (at most CW_POS / NG rows per
+// group, all loads in flight together), so a wave's positions cost one round
+// of row loads.
+#define CW_POS 16
 template <int VEC, bool BF>
 __global__ void __launch_bounds__(256)
 bw_cold(const uint32_t* __restrict__ keys, uint32_t n, eb_geom g, void* stg, uint32_t n_hot, float lr,
@@ -1157,27 +1161,30 @@ bw_cold(const uint32_t* __restrict__ keys, uint32_t n, eb_geom g, void* stg, uin
   const bool cact = gi < g.NG && colv < g.vpr;
   const int64_t col = (int64_t)colv * VEC;
   const uint32_t b0 = min(*bnd, n);
-  for (uint64_t base = b0 + ((uint64_t)blockIdx.x * 4 + w) * 64; base < n; base += (uint64_t)gridDim.x * 256) {
+  constexpr int RPG = CW_POS / 4 > 0 ? CW_POS / 4 : 1;  // rows per group for groups of 16 lanes or wider
+  for (uint64_t base = b0 + ((uint64_t)blockIdx.x * 4 + w) * CW_POS; base < n;
+       base += (uint64_t)gridDim.x * 4 * CW_POS) {
     const uint64_t p = base + lane;
-    const uint32_t k = p < n ? keys[p] : EB_SENT;
-    const uint32_t kn = p + 1 < n ? keys[p + 1] : EB_SENT;
-    uint64_t m = __ballot(k != kn && bw_deferred(k, n_hot, gc_rows));
+    const bool in = lane < CW_POS && p < n;
+    const uint32_t k = in ? keys[p] : EB_SENT;
+    const uint32_t kn = in && p + 1 < n ? keys[p + 1] : EB_SENT;
+    uint64_t m = __ballot(in && k != kn && bw_deferred(k, n_hot, gc_rows));
     while (m) {
-      // run end gi + NG j of the remaining ones goes to group gi, 4 per group in flight
+      // run end gi + NG j of the remaining ones goes to group gi
       uint64_t mm = m;
       for (int q = 0; q < gi; ++q) mm &= mm - 1;
-      int src[4];
-      bool has[4];
+      int src[RPG];
+      bool has[RPG];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
+      for (int j = 0; j < RPG; ++j) {
         has[j] = mm != 0;
         src[j] = has[j] ? __ffsll((unsigned long long)mm) - 1 : 0;
         for (int q = 0; q < g.NG && mm; ++q) mm &= mm - 1;
       }
-      int64_t u[4];
-      float wv[4][VEC], gv[4][VEC];
+      int64_t u[RPG];
+      float wv[RPG][VEC], gv[RPG][VEC];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
+      for (int j = 0; j < RPG; ++j) {
         u[j] = (int64_t)__shfl(k, src[j]) - n_hot;
         if (has[j] && cact) {
           RowIO<VEC, BF>::load((T*)stg + u[j] * g.D + col, wv[j]);
@@ -1185,13 +1192,13 @@ bw_cold(const uint32_t* __restrict__ keys, uint32_t n, eb_geom g, void* stg, uin
         }
       }
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
+      for (int j = 0; j < RPG; ++j)
         if (has[j] && cact) {
 #pragma unroll
           for (int e = 0; e < VEC; ++e) wv[j][e] = wv[j][e] - lr * gv[j][e];
           RowIO<VEC, BF>::store((T*)stg + u[j] * g.D + col, wv[j]);
         }
-      for (int q = 0; q < 4 * g.NG && m; ++q) m &= m - 1;
+      for (int q = 0; q < RPG * g.NG && m; ++q) m &= m - 1;
     }
   }
   hl_hook_tail(hk);
@@ -1482,10 +1489,10 @@ static void launch_bwd(const hl_handle* h, uint32_t tiles, hipStream_t s, const 
       HL_KERNEL(h, s, "bw_reduce2", (bw_reduce2<VEC, BF, true>), grid, dim3(RB_BLOCK), 0, s, tiles, g, w_hot, stg,
                 n_hot, lr, ws.tfirst, ws.tlast, ws.tflag, ws.tkey, ws.gc, ws.gc_rows);
   } else {
-    // the tail (cold lookups: about a tenth of a mini-batch here) is short; a
-    // small grid strides over it
-    uint32_t b = hl_div_up(n, 256);
-    if (b > 128) b = 128;
+    // the tail (cold lookups: about a tenth of a mini-batch here) is a part of
+    // n the device knows; a grid of a few thousand waves strides over it
+    uint32_t b = hl_div_up(n, 4 * CW_POS);
+    if (b > 1024) b = 1024;
     HL_KERNEL(h, s, "bw_cold", (bw_cold<VEC, BF>), dim3(b, g.cchunks), dim3(256), 0, s, sk, n, g, stg, n_hot, lr,
               ws.gc, ws.gc_rows, ws.bnd, hl_hook{});
   }
@@ -1780,8 +1787,10 @@ hl_status hl_embbag_finish_cold(hl_handle* h, void* w_hot, void* staging, int32_
   if (tiles > ws.tiles) return HL_ERR_CAPACITY;
   uint32_t tb = hl_div_up(n, RB_WAVES * g.NG * FT);
   if (tb > 1024) tb = 1024;  // (the tail, cold lookups only, is a part of n the device knows)
-  uint32_t cb = hl_div_up(n, 256);  // (as part 2: the tail is short, a small grid strides over it)
-  if (cb > 128) cb = 128;
+  // (as part 2: the tail, cold lookups only, is a part of n the device knows; a
+  // grid of a few thousand waves strides over it)
+  uint32_t cb = hl_div_up(n, 4 * CW_POS);
+  if (cb > 1024) cb = 1024;
   hipStream_t s = (hipStream_t)stream;
   const bool bf = h->dtype == HL_BF16;
   // bags of several lookups: the cold half bag by bag, one bag per row group
