@@ -22,9 +22,9 @@
 #include "hl_group_sort.h"
 #include "hl_internal.h"
 
-#ifndef RB_E
-#define RB_E 8      // sorted entries per row group of the reduction
-#endif
+// sorted entries per row group of the reduction: 6 for rows of 4 or more
+// elements per lane (the register budget of 7 waves per SIMD), else 8
+#define RB_EN(V) ((V) >= 4 ? 6 : 8)
 #ifndef RB_WAVES
 #define RB_WAVES 2  // waves per reduction block (2 measured fastest: a block waits for its slowest wave)
 #endif
@@ -616,12 +616,6 @@ eb_fwd_oh(const void* w_hot, const void* stg, int32_t stg_rows, uint32_t n_hot, 
 // codes and rows and writes the pooled outputs: nothing one writes is read by
 // the other, so they run side by side (the sort on a few compute units at LDS
 // and latency speed, the HBM-bound forward on the rest).
-#ifdef HL_FG_PROBE
-__device__ uint64_t fg_probe[1024][2];
-extern "C" int hl_probe_read_fg(uint64_t* host) {
-  return (int)hipMemcpyFromSymbol(host, HIP_SYMBOL(fg_probe), sizeof(fg_probe));
-}
-#endif
 template <int VEC, bool BF, int ITEMS>
 __global__ void __launch_bounds__(GT_THREADS)
 eb_fwd_gt(const void* w_hot, const void* stg, int32_t stg_rows, uint32_t n_hot, uint32_t k_cap,
@@ -630,20 +624,13 @@ eb_fwd_gt(const void* w_hot, const void* stg, int32_t stg_rows, uint32_t n_hot, 
           uint32_t nblk, uint32_t E, int32_t T, const uint32_t* __restrict__ tb, uint32_t* __restrict__ kout,
           uint32_t* __restrict__ vout, uint32_t* err, int ballot_only, hl_hook hk) {
   hl_hook_head(hk);
-#ifdef HL_FG_PROBE
-  if (threadIdx.x == 0 && blockIdx.x < 1024) fg_probe[blockIdx.x][0] = wall_clock64();
-#endif
   if (blockIdx.x < (uint32_t)T) {
     gt_sort_body<ITEMS>(blockIdx.x, keys_tm, cum, nblk, E, T, (uint32_t)n_bags, tb, n_hot, kout, vout, err,
                         ballot_only);
   } else {
-  eb_fwd_oh_body<VEC, BF, 0>(blockIdx.x - T, gridDim.x - T, w_hot, stg, stg_rows, n_hot, k_cap, codes, bag_ptr, out,
-                             g, n_lookups, n_bags, err);
+    eb_fwd_oh_body<VEC, BF, 0>(blockIdx.x - T, gridDim.x - T, w_hot, stg, stg_rows, n_hot, k_cap, codes, bag_ptr,
+                               out, g, n_lookups, n_bags, err);
   }
-#ifdef HL_FG_PROBE
-  __syncthreads();
-  if (threadIdx.x == 0 && blockIdx.x < 1024) fg_probe[blockIdx.x][1] = wall_clock64();
-#endif
 }
 
 // ----------------------------------------------------------------------------- backward
@@ -661,7 +648,7 @@ struct bw_ws {
 
 static uint32_t bw_tile_entries(int32_t D, int vec) {
   eb_geom g = eb_make_geom(D, vec);
-  return (uint32_t)(RB_WAVES * g.NG * RB_E);
+  return (uint32_t)(RB_WAVES * g.NG * RB_EN(vec));
 }
 
 // compact: no staging-row sums (gc), for plans whose apply is whole (part 0)
@@ -876,6 +863,7 @@ bw_reduce1(const uint32_t* __restrict__ keys, const uint32_t* __restrict__ vals,
            uint32_t* __restrict__ tkey, float* __restrict__ gc, uint32_t gc_rows, uint32_t* __restrict__ bnd,
            hl_hook hk) {
   typedef typename RowIO<VEC, BF>::T T;
+  constexpr int RB_E = RB_EN(VEC);
   __shared__ float pf[RB_WAVES * 64 * VEC], pl[RB_WAVES * 64 * VEC];
   hl_hook_head(hk);
   __shared__ uint32_t gflag[RB_WAVES * 64], gkey[RB_WAVES * 64];
@@ -1700,7 +1688,7 @@ hl_status hl_embbag_bwd_apply_any(hl_handle* h, void* w_hot, void* staging, int3
   const size_t es = h->dtype == HL_F32 ? 4 : 2;
   const int vec = eb_pick_vec(h->dim, es, {w_hot, staging, part == 2 ? nullptr : dY});
   eb_geom g = eb_make_geom(h->dim, vec);
-  const uint32_t te = (uint32_t)(RB_WAVES * g.NG * RB_E);
+  const uint32_t te = (uint32_t)(RB_WAVES * g.NG * RB_EN(vec));
   const uint32_t tiles = hl_div_up(n, te);
   if (tiles > ws.tiles) return HL_ERR_CAPACITY;
   const bool bf = h->dtype == HL_BF16;
@@ -1782,7 +1770,7 @@ hl_status hl_embbag_finish_cold(hl_handle* h, void* w_hot, void* staging, int32_
   if (eb_pick_vec(h->dim, es, {w_hot, staging, out}) < vec) return HL_ERR_INVALID_ARG;
   eb_geom g = eb_make_geom(h->dim, vec);
   const uint32_t n = (uint32_t)n_lookups;
-  const uint32_t te = (uint32_t)(RB_WAVES * g.NG * RB_E);
+  const uint32_t te = (uint32_t)(RB_WAVES * g.NG * RB_EN(vec));
   const uint32_t tiles = hl_div_up(n, te);
   if (tiles > ws.tiles) return HL_ERR_CAPACITY;
   uint32_t tb = hl_div_up(n, RB_WAVES * g.NG * FT);

@@ -49,30 +49,43 @@ __device__ __forceinline__ void gt_sort_body(uint32_t t, const uint32_t* __restr
   __shared__ uint32_t wcnt[GT_WAVES][GT_NB];
   __shared__ uint32_t dofs[GT_NB];
   __shared__ uint32_t scan_ws[GT_WAVES];
-  __shared__ uint32_t s_lo, s_hi, s_max, s_sent, s_hb, s_ht;
+  __shared__ uint32_t s_max, s_sent, s_hb, s_ht;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  if (tid == 0) {
-    s_lo = tb[t];  // the table's hot slots
-    s_hi = tb[t + 1];
-    s_max = 0;
-    s_sent = 0;
-    s_hb = 0;
-    s_ht = 0;
+  const uint32_t lo = tb[t], R = tb[t + 1] - lo;  // the table's hot slots
+  // the table's keys, position w * 64 ITEMS + 64 k + lane (lookup order), and
+  // the hot keys of the earlier tables (hb) and up to this one (ht) summed
+  // over the prep blocks: all loads issued before any is waited for
+  uint32_t key[ITEMS], pos[ITEMS];
+#pragma unroll
+  for (int k = 0; k < ITEMS; ++k) {
+    const uint32_t ps = (uint32_t)w * (ITEMS * 64) + k * 64 + lane;
+    key[k] = keys_tm[(uint64_t)t * E + min(ps, E - 1)];
+    pos[k] = ps;
   }
-  // hot keys of the earlier tables (hb) and up to this one (ht), summed over
-  // the prep blocks (loads issued with the keys')
   uint32_t hb = 0, ht = 0;
   for (uint32_t b = tid; b < nblk; b += GT_THREADS) {
     hb += cum[(uint64_t)b * (T + 1) + t];
     ht += cum[(uint64_t)b * (T + 1) + t + 1];
   }
+  if (tid == 0) {
+    s_max = 0;
+    s_sent = 0;
+    s_hb = 0;
+    s_ht = 0;
+  }
   for (int j = tid; j < GT_WAVES * GT_NB; j += GT_THREADS) (&wcnt[0][0])[j] = 0;
   __syncthreads();
-  const uint32_t lo = s_lo, R = s_hi - s_lo;
   const uint64_t lt = (1ull << lane) - 1ull;
-  uint32_t key[ITEMS], pos[ITEMS];
-  for (int stable = ballot_only ? 1 : 0; stable < 2; ++stable) {
-    // the table's keys: position w * 64 ITEMS + 64 k + lane (lookup order);
+  for (int stable = ballot_only ? 1 : 0, fresh = 1; stable < 2; ++stable, fresh = 0) {
+    if (!fresh) {
+      // (sorting again: the keys as loaded)
+#pragma unroll
+      for (int k = 0; k < ITEMS; ++k) {
+        const uint32_t ps = (uint32_t)w * (ITEMS * 64) + k * 64 + lane;
+        key[k] = keys_tm[(uint64_t)t * E + min(ps, E - 1)];
+        pos[k] = ps;
+      }
+    }
     // compressed: hot slot - lo, or R + staging row, or (skipped: an invalid
     // code, or a hot slot of another table's row) one past the largest
     uint32_t kmax = 0;
@@ -81,8 +94,7 @@ __device__ __forceinline__ void gt_sort_body(uint32_t t, const uint32_t* __restr
     for (int k = 0; k < ITEMS; ++k) {
       const uint32_t ps = (uint32_t)w * (ITEMS * 64) + k * 64 + lane;
       const bool valid = ps < E;
-      const uint32_t kk = keys_tm[(uint64_t)t * E + min(ps, E - 1)];
-      pos[k] = ps;
+      const uint32_t kk = key[k];
       uint32_t c = EB_SENT;
       if (kk < n_hot) {
         if (kk - lo < R) c = kk - lo;
@@ -94,12 +106,12 @@ __device__ __forceinline__ void gt_sort_body(uint32_t t, const uint32_t* __restr
       if (valid && c != EB_SENT) kmax = max(kmax, c);
       anysent = anysent || (valid && c == EB_SENT);
     }
-    if (foreign && !stable) hl_flag(err, HL_DEVERR_BAD_CODE);
+    if (foreign && fresh) hl_flag(err, HL_DEVERR_BAD_CODE);
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) kmax = max(kmax, (uint32_t)__shfl_xor(kmax, o));
     if (lane == 0) atomicMax(&s_max, kmax);
     if (anysent) s_sent = 1;
-    if (!stable || ballot_only) {
+    if (fresh) {
 #pragma unroll
       for (int o = 32; o > 0; o >>= 1) {
         hb += __shfl_xor(hb, o);
@@ -120,6 +132,7 @@ __device__ __forceinline__ void gt_sort_body(uint32_t t, const uint32_t* __restr
     const int passes = (bits + GT_DBITS - 1) / GT_DBITS;  // 0: every key is 0, already in order
     const int b = passes ? (bits + passes - 1) / passes : 1;
     const uint32_t mask = (1u << b) - 1u;
+    bool broken = false;  // the check, on the last pass of the fast ranks
     for (int p = 0; p < passes; ++p) {
       const int shift = p * b;
       uint32_t dg[ITEMS], rk[ITEMS];
@@ -136,40 +149,47 @@ __device__ __forceinline__ void gt_sort_body(uint32_t t, const uint32_t* __restr
           rk[k] = bs + (uint32_t)__popcll(peers & lt);
         }
       } else {
-        // the lanes of the first lane's digit together (their base read from
-        // the leading lane's register), the others one by one; every counter
-        // update of the items is issued before any old value is used (a
-        // wave's LDS operations execute in the order issued)
-        uint64_t m0[ITEMS];
-        uint32_t b0[ITEMS];
+        // the lanes of the first lane's digit together (their lowest lane
+        // adds their count, the others add its old value to their rank among
+        // them), every other lane adds 1 and takes the old value: one counter
+        // update per item, all issued before any old value is used (a wave's
+        // LDS operations execute in the order issued)
+        uint32_t later = 0;  // items whose rank waits for the lowest lane's old value
+        int l0[ITEMS];       // (uniform)
 #pragma unroll
         for (int k = 0; k < ITEMS; ++k) {
           const bool valid = (uint32_t)w * (ITEMS * 64) + k * 64 + lane < E;
           dg[k] = (key[k] >> shift) & mask;
           const uint32_t d0 = __builtin_amdgcn_readfirstlane(dg[k]);
-          m0[k] = __ballot(valid && dg[k] == d0);
-          const bool in0 = (m0[k] >> lane) & 1ull;
-          const int l0 = m0[k] ? __ffsll((unsigned long long)m0[k]) - 1 : 0;
-          b0[k] = 0;
-          rk[k] = 0;
-          if (m0[k] && lane == l0) b0[k] = atomicAdd(&wcnt[w][d0], (uint32_t)__popcll(m0[k]));
-          if (valid && !in0) rk[k] = atomicAdd(&wcnt[w][dg[k]], 1u);
+          const uint64_t m0 = __ballot(valid && dg[k] == d0);
+          const bool in0 = (m0 >> lane) & 1ull;
+          const uint32_t pr = (uint32_t)__popcll(m0 & lt);
+          l0[k] = m0 ? __ffsll((unsigned long long)m0) - 1 : 0;
+          rk[k] = pr;
+          if ((valid && !in0) || (in0 && pr == 0))
+            rk[k] = atomicAdd(&wcnt[w][dg[k]], in0 ? (uint32_t)__popcll(m0) : 1u);
+          if (in0 && pr != 0) later |= 1u << k;
         }
 #pragma unroll
         for (int k = 0; k < ITEMS; ++k) {
-          const int l0 = m0[k] ? __ffsll((unsigned long long)m0[k]) - 1 : 0;
-          const uint32_t base = __builtin_amdgcn_readlane(b0[k], l0);
-          if ((m0[k] >> lane) & 1ull) rk[k] = base + (uint32_t)__popcll(m0[k] & lt);
+          const uint32_t base = __builtin_amdgcn_readlane(rk[k], l0[k]);
+          if ((later >> k) & 1u) rk[k] += base;
         }
       }
       __syncthreads();
       // per digit: offsets of the waves, then of the digits
       uint32_t tot = 0;
       if (tid <= (int)mask) {
-        for (int q = 0; q < GT_WAVES; ++q) {
-          const uint32_t x = wcnt[q][tid];
-          wcnt[q][tid] = tot;
-          tot += x;
+#pragma unroll
+        for (int q0 = 0; q0 < GT_WAVES; q0 += 8) {
+          uint32_t x[8];
+#pragma unroll
+          for (int q = 0; q < 8; ++q) x[q] = wcnt[q0 + q][tid];
+#pragma unroll
+          for (int q = 0; q < 8; ++q) {
+            wcnt[q0 + q][tid] = tot;
+            tot += x[q];
+          }
         }
       }
       uint32_t all;
@@ -184,6 +204,7 @@ __device__ __forceinline__ void gt_sort_body(uint32_t t, const uint32_t* __restr
         }
       }
       __syncthreads();
+      const bool last = p + 1 == passes;
 #pragma unroll
       for (int k = 0; k < ITEMS; ++k) {
         const uint32_t ps = (uint32_t)w * (ITEMS * 64) + k * 64 + lane;
@@ -191,20 +212,15 @@ __device__ __forceinline__ void gt_sort_body(uint32_t t, const uint32_t* __restr
           const uint64_t x = sx[ps];
           key[k] = (uint32_t)(x >> 32);
           pos[k] = (uint32_t)x;
+          // (key, position) strictly ascending (positions are distinct)
+          if (last && !stable && ps > 0) broken = broken || sx[ps - 1] >= x;
         }
       }
       for (int j = tid; j < GT_WAVES * GT_NB; j += GT_THREADS) (&wcnt[0][0])[j] = 0;
-      __syncthreads();
+      if (last) broken = __syncthreads_or(broken);
+      else __syncthreads();
     }
-    if (stable) break;
-    // the check: (key, position) strictly ascending (positions are distinct)
-    bool broken = false;
-#pragma unroll
-    for (int k = 0; k < ITEMS; ++k) {
-      const uint32_t ps = (uint32_t)w * (ITEMS * 64) + k * 64 + lane;
-      if (ps > 0 && ps < E && passes > 0) broken = broken || sx[ps - 1] >= (((uint64_t)key[k] << 32) | pos[k]);
-    }
-    if (!__syncthreads_or(broken)) break;
+    if (stable || !broken) break;
     if (tid == 0) {
       s_max = 0;
       s_sent = 0;
@@ -238,4 +254,3 @@ __device__ __forceinline__ void gt_sort_body(uint32_t t, const uint32_t* __restr
     }
   }
 }
-
