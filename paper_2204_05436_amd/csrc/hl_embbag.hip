@@ -774,7 +774,9 @@ bw_prep(const int32_t* __restrict__ codes, const int32_t* __restrict__ bag_ptr, 
 // bw_prep and the sort's digit histogram in one launch (no sample selection):
 // blocks [0, hb) count the digits of every key, taking the keys from the codes
 // by the same rule as the writers, and clear the first pass's status words;
-// the other blocks write the (key, bag) pairs, BPH_BAGS bags each.  In the
+// the other blocks write the (key, bag) pairs, bpb bags each (at most
+// BPH_BAGS: fewer when bags hold many lookups, so the writers spread over
+// the chip).  In the
 // fused plan (cf.table) both roles take a cold lookup's code from the cold
 // plan's state (the writers also store it; a reader that meets the stored
 // code derives the same key), and the first writer block reports rows that do
@@ -786,7 +788,7 @@ __global__ void __launch_bounds__(BPH_THREADS)
 bw_prep_hist(int32_t* codes, const int32_t* __restrict__ bag_ptr, int64_t n_bags, int32_t bps, uint32_t n_hot,
              uint32_t k_cap, int32_t stg_rows, uint32_t* __restrict__ keys, uint32_t* __restrict__ vals,
              int64_t n_lookups, uint32_t hb, int passes, int b, uint32_t* __restrict__ part,
-             uint32_t* __restrict__ zero, uint64_t n_zero, uint32_t* sflag, uint32_t sv, uint32_t* err,
+             uint32_t* __restrict__ zero, uint64_t n_zero, int32_t bpb, uint32_t* sflag, uint32_t sv, uint32_t* err,
              hl_cg_fused cf) {
   __shared__ uint32_t hst[HL_SORT_MAXPASS][NB];
   __shared__ int32_t off[BPH_BAGS + 1];
@@ -824,8 +826,8 @@ bw_prep_hist(int32_t* codes, const int32_t* __restrict__ bag_ptr, int64_t n_bags
     return;
   }
   const uint32_t blk = blockIdx.x - hb;
-  const int64_t b0 = (int64_t)blk * BPH_BAGS;
-  const int nb = (int)min((int64_t)BPH_BAGS, n_bags - b0);
+  const int64_t b0 = (int64_t)blk * bpb;
+  const int nb = (int)min((int64_t)bpb, n_bags - b0);
   for (int j = threadIdx.x; j <= nb; j += BPH_THREADS) off[j] = bag_ptr[b0 + j];
   if (blk == 0 && threadIdx.x == 0 && bag_ptr[n_bags] != n_lookups) hl_flag(err, HL_DEVERR_SHAPE);
   if (blk == 0 && threadIdx.x == 0 && cf.table && !fits) hl_flag(err, HL_DEVERR_CAPACITY);
@@ -1550,11 +1552,14 @@ hl_status hl_embbag_bwd_plan_signal(hl_handle* h, int32_t stg_rows, int32_t* cod
   } else {
     if ((uint64_t)n_lookups > ws.sort.n_max) return HL_ERR_CAPACITY;
     const hl_sort_geom sg = hl_sort_geometry((uint32_t)n_lookups, bits);
-    const dim3 grid(sg.hist_blocks + (uint32_t)hl_div_up(n_bags, BPH_BAGS));
+    // bags per writer block: up to about 8192 lookups each, 64 to BPH_BAGS bags
+    int32_t bpb = BPH_BAGS;
+    while (bpb > 64 && (int64_t)bpb * n_lookups > 8192 * n_bags) bpb >>= 1;
+    const dim3 grid(sg.hist_blocks + (uint32_t)hl_div_up(n_bags, bpb));
 #define BPH(NB)                                                                                                  \
   HL_KERNEL(h, s, "bw_prep_hist", bw_prep_hist<NB>, grid, dim3(BPH_THREADS), 0, s, codes, bag_ptr, n_bags, bps, h->n_hot, \
             h->k_cap, stg_rows, ws.sort.k0, ws.sort.v0, n_lookups, sg.hist_blocks, sg.passes, sg.b, ws.sort.part,   \
-            ws.sort.st[0], sg.n_zero, sflag, sval, h->d_err, cf ? *cf : hl_cg_fused{})
+            ws.sort.st[0], sg.n_zero, bpb, sflag, sval, h->d_err, cf ? *cf : hl_cg_fused{})
     if (sg.nb == 256) BPH(256);
     else if (sg.nb == 1024) BPH(1024);
     else BPH(2048);

@@ -368,10 +368,11 @@ hl_status hl_group_by_table(hl_handle* h, int32_t* codes, const int32_t* bag_ptr
 // for the cross-tile digit offsets.  See hl_sort.hip.
 #define HL_SORT_THREADS 512
 #define HL_SORT_WAVES (HL_SORT_THREADS / 64)
-#ifndef HL_SORT_ITEMS
-#define HL_SORT_ITEMS 12
-#endif
-#define HL_SORT_TILE (HL_SORT_THREADS * HL_SORT_ITEMS)
+// items per thread of a pass block: 4, 6 or 12 (the fewest that keep the
+// tiles to HL_SORT_TILES_AIM, so a small sort still spreads over the chip)
+#define HL_SORT_TILE_MIN (HL_SORT_THREADS * 4)
+#define HL_SORT_TILE_MAX (HL_SORT_THREADS * 12)
+#define HL_SORT_TILES_AIM 128
 #define HL_SORT_MAXNB 2048        // bins of an 11-bit digit
 #define HL_SORT_MAXPASS 3
 #define HL_SORT_HIST_BLOCKS 16
@@ -403,6 +404,8 @@ void hl_sort_result(const hl_sort_ws& ws, int bits, uint32_t** out_k, uint32_t**
 // first pass's status words ws.st[0][0 .. n_zero) to clear.
 struct hl_sort_geom {
   int passes, b, nb;
+  int items;      // per thread of a pass block
+  uint32_t tile;  // items per pass block
   uint32_t hist_blocks;
   uint64_t n_zero;
 };

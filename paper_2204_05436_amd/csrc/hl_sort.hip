@@ -21,7 +21,7 @@
 
 void hl_sort_ws_carve(hl_carver& c, hl_sort_ws& ws, uint32_t n_max) {
   ws.n_max = n_max;
-  ws.tiles_max = n_max ? hl_div_up(n_max, HL_SORT_TILE) : 1;
+  ws.tiles_max = n_max ? hl_div_up(n_max, HL_SORT_TILE_MIN) : 1;
   ws.k0 = c.take<uint32_t>(n_max);
   ws.v0 = c.take<uint32_t>(n_max);
   ws.k1 = c.take<uint32_t>(n_max);
@@ -42,7 +42,7 @@ void hl_sort_ws_carve(hl_carver& c, hl_sort_ws& ws, uint32_t n_max) {
 #define SRT_AGG 0x40000000u
 #define SRT_VAL 0x3FFFFFFFu
 #define SRT_AGG2 0x80008000u
-static_assert(HL_SORT_TILE < 0x8000, "a tile's digit count must fit 15 bits");
+static_assert(HL_SORT_TILE_MAX < 0x8000, "a tile's digit count must fit 15 bits");
 __device__ __forceinline__ void srt_st_store(uint32_t* p, uint32_t w) {
   __hip_atomic_store(p, w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
@@ -139,12 +139,13 @@ __device__ __forceinline__ void srt_scan2(uint32_t (&a)[PER], uint32_t (&c)[PER]
   }
 }
 
-template <int NB>
+template <int NB, int ITEMS>
 __global__ void __launch_bounds__(HL_SORT_THREADS)
 srt_pass(const uint32_t* __restrict__ kin, const uint32_t* __restrict__ vin, uint32_t* __restrict__ kout,
          uint32_t* __restrict__ vout, const uint32_t* n_dev, uint32_t n_host, int shift, int b,
          const uint32_t* __restrict__ part, uint32_t n_part, uint32_t* st, uint32_t* st_next, uint32_t* tile_ctr,
          uint32_t* err, hl_hook hk) {
+  constexpr uint32_t TILE = HL_SORT_THREADS * ITEMS;
   constexpr int PER = NB >= HL_SORT_THREADS ? NB / HL_SORT_THREADS : 1;
   constexpr int OWNERS = NB / PER;         // threads that own digits
   // status words of a tile per digit owner, and the earlier tiles whose
@@ -156,7 +157,7 @@ srt_pass(const uint32_t* __restrict__ kin, const uint32_t* __restrict__ vin, uin
   __shared__ uint32_t wcnt[HL_SORT_WAVES][NB];
   __shared__ uint32_t tdex[NB], gbase[NB];
   __shared__ uint32_t scan_ws[HL_SORT_WAVES][2];
-  __shared__ uint32_t lk[HL_SORT_TILE], lv[HL_SORT_TILE];
+  __shared__ uint32_t lk[TILE], lv[TILE];
   const uint32_t n = srt_n(n_dev, n_host);
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   hl_hook_head(hk);
@@ -166,13 +167,13 @@ srt_pass(const uint32_t* __restrict__ kin, const uint32_t* __restrict__ vin, uin
   const uint32_t tile = s_tile;
   if (st_next)  // this tile's status words of the next pass
     for (int j = tid; j < (int)TW; j += HL_SORT_THREADS) st_next[(size_t)tile * TW + j] = 0;
-  const uint64_t tb = (uint64_t)tile * HL_SORT_TILE;
+  const uint64_t tb = (uint64_t)tile * TILE;
   if (tb >= n) return;
   const uint32_t mask = (1u << b) - 1u;
-  uint32_t key[HL_SORT_ITEMS], val[HL_SORT_ITEMS];
+  uint32_t key[ITEMS], val[ITEMS];
 #pragma unroll
-  for (int k = 0; k < HL_SORT_ITEMS; ++k) {
-    const uint64_t idx = tb + (uint64_t)w * (HL_SORT_ITEMS * 64) + k * 64 + lane;
+  for (int k = 0; k < ITEMS; ++k) {
+    const uint64_t idx = tb + (uint64_t)w * (ITEMS * 64) + k * 64 + lane;
     const bool ok = idx < n;
     key[k] = ok ? kin[idx] : 0xFFFFFFFFu;
     val[k] = ok ? vin[idx] : 0u;
@@ -204,11 +205,11 @@ srt_pass(const uint32_t* __restrict__ kin, const uint32_t* __restrict__ vin, uin
   // a lane's rank is that value plus its peers on lower lanes.  A wave's LDS
   // instructions execute in issue order, so the counters advance in item
   // order: ranks follow (item, lane) order, which is index order.
-  uint32_t dg[HL_SORT_ITEMS], lr[HL_SORT_ITEMS];
+  uint32_t dg[ITEMS], lr[ITEMS];
   const uint64_t lt = (1ull << lane) - 1ull;
 #pragma unroll
-  for (int k = 0; k < HL_SORT_ITEMS; ++k) {
-    const uint64_t idx = tb + (uint64_t)w * (HL_SORT_ITEMS * 64) + k * 64 + lane;
+  for (int k = 0; k < ITEMS; ++k) {
+    const uint64_t idx = tb + (uint64_t)w * (ITEMS * 64) + k * 64 + lane;
     const bool valid = idx < n;
     dg[k] = (key[k] >> shift) & mask;
     const uint64_t peers = hl_match_digit(dg[k], b, valid);
@@ -262,8 +263,8 @@ srt_pass(const uint32_t* __restrict__ kin, const uint32_t* __restrict__ vin, uin
   // the tile in digit order in LDS (its own offsets are known now; the
   // earlier tiles' counts are read below)
 #pragma unroll
-  for (int k = 0; k < HL_SORT_ITEMS; ++k) {
-    const uint64_t idx = tb + (uint64_t)w * (HL_SORT_ITEMS * 64) + k * 64 + lane;
+  for (int k = 0; k < ITEMS; ++k) {
+    const uint64_t idx = tb + (uint64_t)w * (ITEMS * 64) + k * 64 + lane;
     if (idx < n) {
       const uint32_t p = tdex[dg[k]] + wcnt[w][dg[k]] + lr[k];
       lk[p] = key[k];
@@ -326,7 +327,7 @@ srt_pass(const uint32_t* __restrict__ kin, const uint32_t* __restrict__ vin, uin
 #pragma unroll
     for (int j = 0; j < PER; ++j) gbase[d0 + j] = gx[j] + excl[j];
   __syncthreads();
-  const uint32_t nv = (uint32_t)min((uint64_t)HL_SORT_TILE, (uint64_t)n - tb);
+  const uint32_t nv = (uint32_t)min((uint64_t)TILE, (uint64_t)n - tb);
 #pragma unroll 4
   for (uint32_t i = tid; i < nv; i += HL_SORT_THREADS) {
     const uint32_t kk = lk[i];
@@ -351,7 +352,14 @@ hl_sort_geom hl_sort_geometry(uint32_t n_host, int bits) {
   g.nb = pl.nb;
   const uint32_t hb = hl_div_up(n_host, HL_SORT_HIST_THREADS * 8);
   g.hist_blocks = hb < 1 ? 1 : (hb > HL_SORT_HIST_BLOCKS ? HL_SORT_HIST_BLOCKS : hb);
-  g.n_zero = (uint64_t)hl_div_up(n_host, HL_SORT_TILE) * pl.nb;
+  g.items = 12;
+  for (int it : {4, 6})
+    if (hl_div_up(n_host, HL_SORT_THREADS * it) <= HL_SORT_TILES_AIM) {
+      g.items = it;
+      break;
+    }
+  g.tile = HL_SORT_THREADS * g.items;
+  g.n_zero = (uint64_t)hl_div_up(n_host, g.tile) * pl.nb;
   return g;
 }
 
@@ -365,14 +373,14 @@ static hl_status srt_hist_launch(hl_handle* h, hl_sort_ws& ws, const uint32_t* n
   return HL_OK;
 }
 
-template <int NB>
+template <int NB, int ITEMS>
 static hl_status srt_launch(hl_handle* h, hl_sort_ws& ws, const uint32_t* n_dev, uint32_t n_host, int bits,
                             hipStream_t s) {
-  const uint32_t tiles = hl_div_up(n_host, HL_SORT_TILE);
   const hl_sort_geom g = hl_sort_geometry(n_host, bits);
+  const uint32_t tiles = hl_div_up(n_host, g.tile);
   uint32_t *ki = ws.k0, *vi = ws.v0, *ko = ws.k1, *vo = ws.v1;
   for (int p = 0; p < g.passes; ++p) {
-    HL_KERNEL(h, s, "srt_pass", srt_pass<NB>, dim3(tiles), dim3(HL_SORT_THREADS), 0, s, ki, vi, ko, vo, n_dev,
+    HL_KERNEL(h, s, "srt_pass", (srt_pass<NB, ITEMS>), dim3(tiles), dim3(HL_SORT_THREADS), 0, s, ki, vi, ko, vo, n_dev,
               n_host, g.b * p, g.b, ws.part + (size_t)p * HL_SORT_HIST_BLOCKS * NB, g.hist_blocks, ws.st[p & 1],
               p + 1 < g.passes ? ws.st[(p + 1) & 1] : nullptr, ws.ctr + 1 + p, h->d_err,
               p == 0 ? hl_hook_take(h) : hl_hook{});
@@ -400,10 +408,15 @@ hl_status hl_sort_passes(hl_handle* h, hl_sort_ws& ws, const uint32_t* n_dev, ui
   if (n_host == 0) return HL_OK;
   hl_status st = srt_check(ws, n_host, bits);
   if (st != HL_OK) return st;
-  const srt_plan pl = srt_make_plan(bits);
-  if (pl.nb == 256) st = srt_launch<256>(h, ws, n_dev, n_host, bits, s);
-  else if (pl.nb == 1024) st = srt_launch<1024>(h, ws, n_dev, n_host, bits, s);
-  else st = srt_launch<2048>(h, ws, n_dev, n_host, bits, s);
+  const hl_sort_geom g = hl_sort_geometry(n_host, bits);
+#define SRT(NB)                                                                       \
+  (g.items == 4 ? srt_launch<NB, 4>(h, ws, n_dev, n_host, bits, s)                    \
+                : g.items == 6 ? srt_launch<NB, 6>(h, ws, n_dev, n_host, bits, s)     \
+                               : srt_launch<NB, 12>(h, ws, n_dev, n_host, bits, s))
+  if (g.nb == 256) st = SRT(256);
+  else if (g.nb == 1024) st = SRT(1024);
+  else st = SRT(2048);
+#undef SRT
   if (st != HL_OK) return st;
   hl_sort_result(ws, bits, out_k, out_v);
   return HL_OK;
