@@ -43,10 +43,13 @@ gt_prep(int32_t* codes, const int32_t* __restrict__ bag_ptr, int64_t n_bags, int
         hl_cg_fused cf) {
   __shared__ uint32_t lk[GT_TMAX][GT_S];
   __shared__ uint32_t hcnt[GT_TMAX];
+  __shared__ uint32_t stb[GT_TMAX + 1];
   __shared__ uint32_t s_bad;
   bw_start_signal(sflag, sv);
   const int tid = threadIdx.x;
   if (tid == 0) s_bad = 0;
+  if (tid <= T) stb[tid] = tb[tid];
+  if (tid < T) hcnt[tid] = 0;
   const bool fits = cf.table && *cf.ncold <= (uint32_t)cf.cap;
   if (blockIdx.x == 0 && tid == 0) {
     if (bag_ptr[n_bags] != n_lookups) hl_flag(err, HL_DEVERR_SHAPE);
@@ -88,7 +91,11 @@ gt_prep(int32_t* codes, const int32_t* __restrict__ bag_ptr, int64_t n_bags, int
       key = bw_key((uint32_t)c, n_hot, k_cap, stg_rows);
       badc = badc || key == EB_SENT;
     }
-    lk[q % (uint32_t)T][q / (uint32_t)T] = key;
+    const uint32_t t = q % (uint32_t)T;
+    lk[t][q / (uint32_t)T] = key;
+    // hot keys per table: those gt_sort places at the front (a hot slot of
+    // the table's own range)
+    if (key < n_hot && key - stb[t] < stb[t + 1] - stb[t]) atomicAdd(&hcnt[t], 1u);
   }
   if (bad) s_bad = 1;  // (every writer stores 1)
   if (badc) hl_flag(err, HL_DEVERR_BAD_CODE);
@@ -99,19 +106,19 @@ gt_prep(int32_t* codes, const int32_t* __restrict__ bag_ptr, int64_t n_bags, int
     const uint64_t p = (uint64_t)t * E + s0 + s;
     keys_tm[p] = lk[t][s];  // (a row of GT_S keys of one table)
   }
-  // hot keys per table (those gt_sort places at the front: a hot slot of the
-  // table's own range), then for each table those of the tables before it
-  if (tid < T) {
-    const uint32_t lo = tb[tid], R = tb[tid + 1] - lo;
-    uint32_t c = 0;
-    for (uint32_t s = 0; s < ns; ++s) c += (lk[tid][s] < n_hot && lk[tid][s] - lo < R) ? 1u : 0u;
-    hcnt[tid] = c;
-  }
-  __syncthreads();
-  if (tid <= T) {
-    uint32_t c = 0;
-    for (int t = 0; t < tid; ++t) c += hcnt[t];
-    cum[(uint64_t)blockIdx.x * (T + 1) + tid] = c;
+  // for each table the hot keys of the tables before it (T <= 64: one wave's
+  // scan; the last entry, T, is the total)
+  if (tid < 64) {
+    const uint32_t v = tid < T ? hcnt[tid] : 0u;
+    uint32_t x = v;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const uint32_t y = __shfl_up(x, o);
+      if (tid >= o) x += y;
+    }
+    uint32_t* c = cum + (uint64_t)blockIdx.x * (T + 1);
+    if (tid <= T) c[tid] = x - v;
+    if (T == 64 && tid == 63) c[64] = x;
   }
 }
 
