@@ -127,6 +127,30 @@ def test_backward_key_widths(bits):
     parity_case(w, batches=([], mb), hot_ids=hot, split=bits % 2 == 0, staging_cap=cap)
 
 
+@pytest.mark.parametrize("n", [2048 * 128, 2048 * 128 + 1, 3072 * 128, 3072 * 128 + 1])
+def test_sort_tile_sizes(n):
+    """The general radix sort takes 4, 6 or 12 items per thread of its
+    512-thread tiles, the fewest that keep a sort to 128 tiles: mini-batches of
+    exactly n lookups on either side of each switch, in multi-hot bags (so the
+    grouping by table does not apply), against the oracle (the grouping
+    against the stable order of the keys)."""
+    rng = np.random.default_rng(n)
+    rows = np.array([5000, 3000], np.uint32)
+    T, B = len(rows), 2048
+    nb = B * T
+    lens = 1 + rng.multinomial(n - nb, np.full(nb, 1.0 / nb))
+    ptr = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    assert int(ptr[-1]) == n
+    ids = np.empty(n, np.uint32)
+    for j in range(nb):
+        ids[ptr[j]:ptr[j + 1]] = (rng.zipf(1.2, lens[j]) - 1) % rows[j % T]
+    mb = W.Batch(0, ids, ptr, B, T)
+    w = configs.Workload(name=f"tiles{n}", n_tables=T, dim=16, dtype="f32", batch=B, steps=1,
+                         rows_fixed=tuple(int(r) for r in rows), hot_frac=0.05, seed=n % 997, lr=0.05)
+    hot = np.arange(0, 400, 3, dtype=np.uint32)
+    parity_case(w, batches=([], mb), hot_ids=hot, split=n % 2 == 1)
+
+
 def test_determinism_and_split_equals_unsplit():
     w = configs.scaled(configs.WORKLOADS["multi-hot"], batch=300, row_scale=0.002, name="mh-det")
     rows = W.table_rows(w)
