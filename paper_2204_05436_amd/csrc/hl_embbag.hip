@@ -34,13 +34,18 @@
 template <int VEC, bool BF>
 struct RowIO;
 
+// A row slice of VEC elements: load() gives it as floats; load_raw() keeps the
+// loaded bytes (Raw) and unpack() converts them when they are used, so a row
+// in flight holds only its bytes' registers (bf16: half of the floats').
 template <>
 struct RowIO<4, false> {
   typedef float T;
-  static __device__ __forceinline__ void load(const T* p, float* v) {
-    float4 x = *reinterpret_cast<const float4*>(p);
+  typedef float4 Raw;
+  static __device__ __forceinline__ Raw load_raw(const T* p) { return *reinterpret_cast<const float4*>(p); }
+  static __device__ __forceinline__ void unpack(const Raw& x, float* v) {
     v[0] = x.x; v[1] = x.y; v[2] = x.z; v[3] = x.w;
   }
+  static __device__ __forceinline__ void load(const T* p, float* v) { unpack(load_raw(p), v); }
   static __device__ __forceinline__ void store(T* p, const float* v) {
     *reinterpret_cast<float4*>(p) = make_float4(v[0], v[1], v[2], v[3]);
   }
@@ -48,10 +53,12 @@ struct RowIO<4, false> {
 template <>
 struct RowIO<2, false> {
   typedef float T;
-  static __device__ __forceinline__ void load(const T* p, float* v) {
-    float2 x = *reinterpret_cast<const float2*>(p);
+  typedef float2 Raw;
+  static __device__ __forceinline__ Raw load_raw(const T* p) { return *reinterpret_cast<const float2*>(p); }
+  static __device__ __forceinline__ void unpack(const Raw& x, float* v) {
     v[0] = x.x; v[1] = x.y;
   }
+  static __device__ __forceinline__ void load(const T* p, float* v) { unpack(load_raw(p), v); }
   static __device__ __forceinline__ void store(T* p, const float* v) {
     *reinterpret_cast<float2*>(p) = make_float2(v[0], v[1]);
   }
@@ -59,10 +66,17 @@ struct RowIO<2, false> {
 template <>
 struct RowIO<8, false> {
   typedef float T;
-  static __device__ __forceinline__ void load(const T* p, float* v) {
-    RowIO<4, false>::load(p, v);
-    RowIO<4, false>::load(p + 4, v + 4);
+  struct Raw {
+    float4 a, b;
+  };
+  static __device__ __forceinline__ Raw load_raw(const T* p) {
+    return Raw{*reinterpret_cast<const float4*>(p), *reinterpret_cast<const float4*>(p + 4)};
   }
+  static __device__ __forceinline__ void unpack(const Raw& x, float* v) {
+    RowIO<4, false>::unpack(x.a, v);
+    RowIO<4, false>::unpack(x.b, v + 4);
+  }
+  static __device__ __forceinline__ void load(const T* p, float* v) { unpack(load_raw(p), v); }
   static __device__ __forceinline__ void store(T* p, const float* v) {
     RowIO<4, false>::store(p, v);
     RowIO<4, false>::store(p + 4, v + 4);
@@ -71,6 +85,9 @@ struct RowIO<8, false> {
 template <>
 struct RowIO<1, false> {
   typedef float T;
+  typedef float Raw;
+  static __device__ __forceinline__ Raw load_raw(const T* p) { return *p; }
+  static __device__ __forceinline__ void unpack(const Raw& x, float* v) { v[0] = x; }
   static __device__ __forceinline__ void load(const T* p, float* v) { v[0] = *p; }
   static __device__ __forceinline__ void store(T* p, const float* v) { *p = v[0]; }
 };
@@ -85,10 +102,12 @@ __device__ __forceinline__ uint32_t f2bf(float f) {  // round to nearest even (f
 template <>
 struct RowIO<4, true> {
   typedef uint16_t T;
-  static __device__ __forceinline__ void load(const T* p, float* v) {
-    uint2 x = *reinterpret_cast<const uint2*>(p);
+  typedef uint2 Raw;
+  static __device__ __forceinline__ Raw load_raw(const T* p) { return *reinterpret_cast<const uint2*>(p); }
+  static __device__ __forceinline__ void unpack(const Raw& x, float* v) {
     v[0] = bf2f(x.x & 0xFFFFu); v[1] = bf2f(x.x >> 16); v[2] = bf2f(x.y & 0xFFFFu); v[3] = bf2f(x.y >> 16);
   }
+  static __device__ __forceinline__ void load(const T* p, float* v) { unpack(load_raw(p), v); }
   static __device__ __forceinline__ void store(T* p, const float* v) {
     *reinterpret_cast<uint2*>(p) = make_uint2(f2bf(v[0]) | (f2bf(v[1]) << 16), f2bf(v[2]) | (f2bf(v[3]) << 16));
   }
@@ -96,8 +115,9 @@ struct RowIO<4, true> {
 template <>
 struct RowIO<8, true> {
   typedef uint16_t T;
-  static __device__ __forceinline__ void load(const T* p, float* v) {
-    uint4 x = *reinterpret_cast<const uint4*>(p);
+  typedef uint4 Raw;
+  static __device__ __forceinline__ Raw load_raw(const T* p) { return *reinterpret_cast<const uint4*>(p); }
+  static __device__ __forceinline__ void unpack(const Raw& x, float* v) {
     const uint32_t w[4] = {x.x, x.y, x.z, x.w};
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
@@ -105,6 +125,7 @@ struct RowIO<8, true> {
       v[2 * i + 1] = bf2f(w[i] >> 16);
     }
   }
+  static __device__ __forceinline__ void load(const T* p, float* v) { unpack(load_raw(p), v); }
   static __device__ __forceinline__ void store(T* p, const float* v) {
     *reinterpret_cast<uint4*>(p) = make_uint4(f2bf(v[0]) | (f2bf(v[1]) << 16), f2bf(v[2]) | (f2bf(v[3]) << 16),
                                               f2bf(v[4]) | (f2bf(v[5]) << 16), f2bf(v[6]) | (f2bf(v[7]) << 16));
@@ -113,10 +134,12 @@ struct RowIO<8, true> {
 template <>
 struct RowIO<2, true> {
   typedef uint16_t T;
-  static __device__ __forceinline__ void load(const T* p, float* v) {
-    uint32_t x = *reinterpret_cast<const uint32_t*>(p);
+  typedef uint32_t Raw;
+  static __device__ __forceinline__ Raw load_raw(const T* p) { return *reinterpret_cast<const uint32_t*>(p); }
+  static __device__ __forceinline__ void unpack(const Raw& x, float* v) {
     v[0] = bf2f(x & 0xFFFFu); v[1] = bf2f(x >> 16);
   }
+  static __device__ __forceinline__ void load(const T* p, float* v) { unpack(load_raw(p), v); }
   static __device__ __forceinline__ void store(T* p, const float* v) {
     *reinterpret_cast<uint32_t*>(p) = f2bf(v[0]) | (f2bf(v[1]) << 16);
   }
@@ -124,6 +147,9 @@ struct RowIO<2, true> {
 template <>
 struct RowIO<1, true> {
   typedef uint16_t T;
+  typedef uint16_t Raw;
+  static __device__ __forceinline__ Raw load_raw(const T* p) { return *p; }
+  static __device__ __forceinline__ void unpack(const Raw& x, float* v) { v[0] = bf2f(x); }
   static __device__ __forceinline__ void load(const T* p, float* v) { v[0] = bf2f(*p); }
   static __device__ __forceinline__ void store(T* p, const float* v) { *p = (uint16_t)f2bf(v[0]); }
 };
@@ -255,7 +281,9 @@ __device__ __forceinline__ void eb_pass4(float* acc, const typename RowIO<VEC, B
   }
 }
 
+#ifndef EB_SEG_ROWS
 #define EB_SEG_ROWS 8  // rows in flight per lane in the passes' wide form
+#endif
 
 // The wide form's segment: the codes of lookups b0 .. b0 + G - 1 of [b0, hi),
 // one per lane of the group (an invalid code past hi; a lane's own code that
@@ -294,7 +322,7 @@ __device__ __forceinline__ void eb_pass(float* acc, const typename RowIO<VEC, BF
     const int n = min(g.G, hi - b0);
     for (int k0 = 0; k0 < n; k0 += EB_SEG_ROWS) {
       bool use[EB_SEG_ROWS];
-      float v[EB_SEG_ROWS][VEC];
+      typename RowIO<VEC, BF>::Raw rv[EB_SEG_ROWS];
 #pragma unroll
       for (int k = 0; k < EB_SEG_ROWS; ++k) {
         const uint32_t c = (uint32_t)__shfl((int)mine, g0 + min(k0 + k, n - 1));
@@ -302,13 +330,16 @@ __device__ __forceinline__ void eb_pass(float* acc, const typename RowIO<VEC, BF
         bool st = false;
         use[k] = k0 + k < n && eb_code_row(c, n_hot, k_cap, stg_rows, &r, &st) && st == COLD;
         *any = *any || use[k];
-        if (use[k] && cact) RowIO<VEC, BF>::load((COLD ? stg : w_hot) + r * g.D + col, v[k]);
+        if (use[k] && cact) rv[k] = RowIO<VEC, BF>::load_raw((COLD ? stg : w_hot) + r * g.D + col);
       }
 #pragma unroll
       for (int k = 0; k < EB_SEG_ROWS; ++k)
-        if (use[k] && cact)
+        if (use[k] && cact) {
+          float v[VEC];
+          RowIO<VEC, BF>::unpack(rv[k], v);
 #pragma unroll
-          for (int e = 0; e < VEC; ++e) acc[e] += v[k][e];
+          for (int e = 0; e < VEC; ++e) acc[e] += v[e];
+        }
     }
   }
 }
@@ -334,7 +365,7 @@ __device__ __forceinline__ void eb_pass_both(float* acc_h, float* acc_c, bool* a
     const int n = min(g.G, hi - b0);
     for (int k0 = 0; k0 < n; k0 += EB_SEG_ROWS) {
       bool use[EB_SEG_ROWS], cold[EB_SEG_ROWS];
-      float v[EB_SEG_ROWS][VEC];
+      typename RowIO<VEC, BF>::Raw rv[EB_SEG_ROWS];
 #pragma unroll
       for (int k = 0; k < EB_SEG_ROWS; ++k) {
         const uint32_t c = (uint32_t)__shfl((int)mine, g0 + min(k0 + k, n - 1));
@@ -343,14 +374,16 @@ __device__ __forceinline__ void eb_pass_both(float* acc_h, float* acc_c, bool* a
         use[k] = k0 + k < n && eb_code_row(c, n_hot, k_cap, stg_rows, &r, &st);
         cold[k] = st;
         *anyc = *anyc || (use[k] && st);
-        if (use[k] && cact) RowIO<VEC, BF>::load((st ? stg : w_hot) + r * g.D + col, v[k]);
+        if (use[k] && cact) rv[k] = RowIO<VEC, BF>::load_raw((st ? stg : w_hot) + r * g.D + col);
       }
 #pragma unroll
       for (int k = 0; k < EB_SEG_ROWS; ++k)
         if (use[k] && cact) {
+          float v[VEC];
+          RowIO<VEC, BF>::unpack(rv[k], v);
           float* a = cold[k] ? acc_c : acc_h;
 #pragma unroll
-          for (int e = 0; e < VEC; ++e) a[e] += v[k][e];
+          for (int e = 0; e < VEC; ++e) a[e] += v[e];
         }
     }
   }
@@ -917,7 +950,7 @@ bw_reduce1(const uint32_t* __restrict__ keys, const uint32_t* __restrict__ vals,
       }
     }
     // rows of complete runs (issued before the sums are formed)
-    float wr[RB_E][VEC];
+    typename RowIO<VEC, BF>::Raw wr[RB_E];
     bool cpl[RB_E];
     bool from0 = true;
 #pragma unroll
@@ -927,7 +960,7 @@ bw_reduce1(const uint32_t* __restrict__ keys, const uint32_t* __restrict__ vals,
       const bool end = valid && (j == RB_E - 1 || kk[j + 1] != kk[j]);
       cpl[j] = end && !(from0 && cprev) && !(j == RB_E - 1 && cnext);
       if (cpl[j] && cact && !(SPLIT && bw_deferred(kk[j], n_hot, gc_rows)))
-        RowIO<VEC, BF>::load(bw_row<VEC, BF>(w_hot, stg, n_hot, g.D, kk[j]) + col, wr[j]);
+        wr[j] = RowIO<VEC, BF>::load_raw(bw_row<VEC, BF>(w_hot, stg, n_hot, g.D, kk[j]) + col);
     }
     float acc[VEC];
 #pragma unroll
@@ -949,9 +982,10 @@ bw_reduce1(const uint32_t* __restrict__ keys, const uint32_t* __restrict__ vals,
             if (SPLIT && bw_deferred(kk[j], n_hot, gc_rows)) {
               st_f32<VEC>(gc + (int64_t)(kk[j] - n_hot) * g.D + col, acc);
             } else {
-              float nw[VEC];
+              float wv[VEC], nw[VEC];
+              RowIO<VEC, BF>::unpack(wr[j], wv);
 #pragma unroll
-              for (int e = 0; e < VEC; ++e) nw[e] = wr[j][e] - lr * acc[e];
+              for (int e = 0; e < VEC; ++e) nw[e] = wv[e] - lr * acc[e];
               RowIO<VEC, BF>::store(bw_row<VEC, BF>(w_hot, stg, n_hot, g.D, kk[j]) + col, nw);
             }
           }
