@@ -1127,11 +1127,17 @@ __device__ __forceinline__ void bw_reduce2_body(uint32_t t, uint32_t n_tiles, eb
 #pragma unroll
       for (int e = 0; e < VEC; ++e) acc[e] += v0[e];
     if (cact) {
-      for (uint32_t p = grp == 0 ? ngb : grp; p < npieces; p += ngb) {
-        float v[VEC];
-        ld_f32<VEC>(tfirst + (int64_t)(t + p) * g.D + col, v);
+      // (four pieces in flight, added in ascending order)
+      for (uint32_t p = grp == 0 ? ngb : grp; p < npieces; p += 4 * ngb) {
+        float v[4][VEC];
 #pragma unroll
-        for (int e = 0; e < VEC; ++e) acc[e] += v[e];
+        for (int i = 0; i < 4; ++i)
+          if (p + i * ngb < npieces) ld_f32<VEC>(tfirst + (int64_t)(t + p + i * ngb) * g.D + col, v[i]);
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          if (p + i * ngb < npieces)
+#pragma unroll
+            for (int e = 0; e < VEC; ++e) acc[e] += v[i][e];
       }
     }
 #pragma unroll
