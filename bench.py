@@ -502,7 +502,7 @@ def main():
     t_fb1 = sum(e[edges[2]].elapsed_time(e[edges[3]]) for e in ev) / K
     ev = seq_pass(range(len(STAGES) + 1))
     st = {s: sum(ev[i][j].elapsed_time(ev[i][j + 1]) for i in range(K)) / K for j, s in enumerate(STAGES)}
-    cl_kern = ("hl_k_gids", "cl_kernel", "pt_count", "pt_scan", "pt_emit")
+    cl_kern = ("hl_k_gids", "cl_kernel", "pt_count", "pt_scan", "pt_emit", "pt_one")
     t_cl_alone = sum(kernels_alone[n]["ms_per_step"] for n in cl_kern if n in kernels_alone)
     alone = {"fwd_bwd_kernel_us": t_fb_alone * 1e3, "fwd_bwd_lookups_per_s": avg["L"] / (t_fb_alone / 1e3),
              "fwd_bwd_hbm_frac": fb_frac_alone,

@@ -155,6 +155,69 @@ pt_emit(const uint8_t* __restrict__ flags, int32_t n, int32_t tile, const uint32
   }
 }
 
+// Up to PT_ONE samples: one block, every flag loaded at once (PT_ONE / 1024 per
+// thread); the popular counts of every (chunk of 1024, wave) go to LDS, one
+// wave scans them in (chunk, wave) order, which is index order, and every
+// sample is then placed: one launch, two barriers.
+#define PT_ONE 16384
+__global__ void __launch_bounds__(1024)
+pt_one(const uint8_t* __restrict__ flags, int32_t n, int32_t* __restrict__ pop, int32_t* __restrict__ nonpop,
+       int32_t* counts) {
+  constexpr int K = PT_ONE / 1024;  // chunks; K * 16 = 4 counts per lane of one wave
+  __shared__ uint32_t wt[K * 16];
+  __shared__ uint32_t s_total;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const uint64_t lt = (1ull << lane) - 1ull;
+  bool f[K];
+#pragma unroll
+  for (int k = 0; k < K; ++k) {
+    const int32_t i = k * 1024 + threadIdx.x;
+    f[k] = i < n && flags[i] != 0;
+  }
+#pragma unroll
+  for (int k = 0; k < K; ++k) {
+    const uint64_t b = __ballot(f[k]);
+    if (lane == 0) wt[k * 16 + w] = (uint32_t)__popcll(b);
+  }
+  __syncthreads();
+  if (w == 0) {
+    uint32_t v[4], sum = 0;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      v[j] = wt[lane * 4 + j];
+      sum += v[j];
+    }
+    uint32_t x = sum;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const uint32_t y = __shfl_up(x, o);
+      if (lane >= o) x += y;
+    }
+    uint32_t run = x - sum;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      wt[lane * 4 + j] = run;
+      run += v[j];
+    }
+    if (lane == 63) s_total = x;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int k = 0; k < K; ++k) {
+    const int32_t i = k * 1024 + threadIdx.x;
+    const uint64_t b = __ballot(f[k]);
+    if (i < n) {
+      const uint32_t before = wt[k * 16 + w] + (uint32_t)__popcll(b & lt);
+      if (f[k]) pop[before] = i;
+      else nonpop[i - before] = i;
+    }
+  }
+  if (threadIdx.x == 0) {
+    counts[0] = (int32_t)s_total;
+    counts[1] = n - (int32_t)s_total;
+  }
+}
+
 size_t hl_partition_ws_bytes(int32_t max_samples) {
   return HL_WS_HEADER + 4 * ((size_t)(max_samples + PT_SMALL - 1) / PT_SMALL + 64);
 }
@@ -164,6 +227,11 @@ extern "C" hl_status hl_partition(hl_handle* h, const uint8_t* flags, int32_t n,
                                   hl_stream stream) {
   if (!h || n < 0 || !counts || (n > 0 && (!flags || !pop || !nonpop))) return HL_ERR_INVALID_ARG;
   hipStream_t s = (hipStream_t)stream;
+  if (n <= PT_ONE) {
+    HL_KERNEL(h, s, "pt_one", pt_one, dim3(1), dim3(1024), 0, s, flags, n, pop, nonpop, counts);
+    HL_LAUNCHED();
+    return HL_OK;
+  }
   const bool small = n <= PT_SMALL * 1024;
   const int32_t tile = small ? PT_SMALL : PT_BIG;
   const int32_t tiles = n == 0 ? 1 : (int32_t)hl_div_up(n, tile);

@@ -452,9 +452,10 @@ def test_empty_batch():
         table.close()
 
 
-@pytest.mark.parametrize("n", [1, 1023, 1025, 200_003, 1_300_007])
+@pytest.mark.parametrize("n", [1, 1023, 1025, 8192, 16384, 16385, 200_003, 1_300_007])
 def test_partition_sizes(n):
-    """One tile, several 1K tiles, and more than 1M samples (64K tiles)."""
+    """One block for up to 16K samples (the flags in registers), then 1K
+    tiles, and more than 1M samples (64K tiles)."""
     w = configs.scaled(configs.WORKLOADS["tiny"], batch=1, row_scale=0.1, name="tiny-part")
     rows = W.table_rows(w)
     table = make_table(w, int(rows.sum()))
