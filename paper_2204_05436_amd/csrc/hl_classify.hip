@@ -9,6 +9,7 @@
 // lookup clears its sample's flag in LDS, the sample found by binary search
 // over the block's sample offsets.
 #define CL_MAX_SPB 1024
+#define CL_U 4
 __global__ void __launch_bounds__(256)
 cl_kernel(const uint32_t* __restrict__ gids, const int32_t* __restrict__ bag_ptr, int32_t n_samples,
           int32_t bps, int32_t spb, const uint64_t* __restrict__ bitmap, uint64_t n_rows,
@@ -23,12 +24,22 @@ cl_kernel(const uint32_t* __restrict__ gids, const int32_t* __restrict__ bag_ptr
     hl_flag(err, HL_DEVERR_SHAPE);
   __syncthreads();
   const int32_t lo = off[0], hi = off[ns];
-  for (int32_t i = lo + threadIdx.x; i < hi; i += blockDim.x) {
-    const uint32_t g = gids[i];
-    bool hot = false;
-    if (g < n_rows) hot = hl_is_hot(bitmap, g);
-    else hl_flag(err, HL_DEVERR_OUT_OF_RANGE);
-    if (!hot) {
+  // CL_U lookups per thread at a time: their ids, then their bitmap words, in flight together
+  for (int32_t i0 = lo + threadIdx.x; i0 < hi; i0 += CL_U * blockDim.x) {
+    uint32_t g[CL_U];
+#pragma unroll
+    for (int u = 0; u < CL_U; ++u) {
+      const int32_t i = i0 + u * (int32_t)blockDim.x;
+      g[u] = i < hi ? gids[i] : 0u;
+    }
+    bool hot[CL_U];
+#pragma unroll
+    for (int u = 0; u < CL_U; ++u) hot[u] = g[u] < n_rows && hl_is_hot(bitmap, g[u]);
+#pragma unroll
+    for (int u = 0; u < CL_U; ++u) {
+      const int32_t i = i0 + u * (int32_t)blockDim.x;
+      if (i >= hi || hot[u]) continue;
+      if (g[u] >= n_rows) hl_flag(err, HL_DEVERR_OUT_OF_RANGE);
       int a = 0, b = ns;
       while (b - a > 1) {
         int m = (a + b) >> 1;
