@@ -499,7 +499,10 @@ typedef struct hl_step_io {
  * their own (0: they share main's).  Masks in multiples of 8 units keep every
  * XCD equally loaded (plans on 56 or 48 units measured 35% slower steps); fetch
  * 8, plan 64, main the other 184 measured fastest here.  The runtime refuses
- * masks of fewer than 8 units. */
+ * masks of fewer than 8 units.  With masks the streams hand over through
+ * device flags, which needs each stream on a hardware queue of its own: the
+ * call checks every pair that hands over (a bounded wait enqueued ahead of its
+ * signal, ~10 ms at most) and returns HL_ERR_UNSUPPORTED if one ran out. */
 hl_status hl_pipeline_create(hl_handle* h, int32_t fetch_cus, int32_t plan_cus, hl_pipeline** out);
 hl_status hl_pipeline_destroy(hl_pipeline* p);
 hl_status hl_pipeline_step(hl_pipeline* p, const hl_step_io* io, hl_stream stream);

@@ -34,7 +34,11 @@
 // Flags need streams that progress independently: a stream with a compute-unit
 // mask has a hardware queue of its own.  Without masks (fetch_cus = 0) streams
 // may share a hardware queue, where a wait ahead of its signal would stall, so
-// the handovers are events then.
+// the handovers are events then.  hl_pipeline_create checks it: for each pair
+// of streams that hand over, a bounded wait is enqueued on one stream before
+// the signal on the other; a wait that runs out (the two shared a queue)
+// makes the creation fail (HL_ERR_UNSUPPORTED) instead of a later step
+// stalling.
 //
 // Look-ahead (hl_pipeline_plan): the dispatch, the cold plan and the
 // backward's grouping of the next mini-batch, which read only its inputs and
@@ -67,6 +71,20 @@
 
 __global__ void pl_signal(uint32_t* flag, uint32_t v) {
   if (threadIdx.x == 0) __hip_atomic_store(flag, v, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// The creation's check of a pair of streams: waits up to `limit` sleeps for
+// *flag to reach v; *stalled = 1 if it did not.
+__global__ void pl_probe_wait(const uint32_t* flag, uint32_t v, uint32_t limit, uint32_t* stalled) {
+  if (threadIdx.x != 0) return;
+  uint32_t spins = 0;
+  while ((int32_t)(__hip_atomic_load(flag, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT) - v) < 0) {
+    if (++spins > limit) {
+      __hip_atomic_store(stalled, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      return;
+    }
+    __builtin_amdgcn_s_sleep(8);
+  }
 }
 
 __global__ void pl_wait(const uint32_t* flag, uint32_t v, uint32_t* err) {
@@ -191,8 +209,29 @@ extern "C" hl_status hl_pipeline_create(hl_handle* h, int32_t fetch_cus, int32_t
     if (st == HL_OK && hipEventCreateWithFlags(e, hipEventDisableTiming | hipEventReleaseToDevice) != hipSuccess)
       st = HL_ERR_HIP;
   }
-  if (st == HL_OK && hipMalloc(&p->flags, PF_N * sizeof(uint32_t)) != hipSuccess) st = HL_ERR_HIP;
-  if (st == HL_OK && hipMemset(p->flags, 0, PF_N * sizeof(uint32_t)) != hipSuccess) st = HL_ERR_HIP;
+  // PF_N handover flags, then two words for the creation's check
+  if (st == HL_OK && hipMalloc(&p->flags, (PF_N + 2) * sizeof(uint32_t)) != hipSuccess) st = HL_ERR_HIP;
+  if (st == HL_OK && hipMemset(p->flags, 0, (PF_N + 2) * sizeof(uint32_t)) != hipSuccess) st = HL_ERR_HIP;
+  if (st == HL_OK && p->use_flags) {
+    // each pair of streams that hand over: the wait enqueued first (~10 ms at
+    // most if it runs out), the signal second; sequence numbers 1, 2, ...
+    uint32_t* pf = p->flags + PF_N;
+    const hipStream_t pairs[][2] = {{p->fetch, p->main}, {p->main, p->fetch}, {p->plan, p->main}, {p->main, p->plan},
+                                    {p->fetch, p->plan}};
+    uint32_t seq = 0;
+    for (const auto& pr : pairs) {
+      if (st != HL_OK || pr[0] == pr[1]) continue;
+      ++seq;
+      hipLaunchKernelGGL(pl_probe_wait, dim3(1), dim3(64), 0, pr[0], pf, seq, 50000u, pf + 1);
+      hipLaunchKernelGGL(pl_signal, dim3(1), dim3(64), 0, pr[1], pf, seq);
+      if (hipGetLastError() != hipSuccess || hipStreamSynchronize(pr[0]) != hipSuccess ||
+          hipStreamSynchronize(pr[1]) != hipSuccess)
+        st = HL_ERR_HIP;
+    }
+    uint32_t stalled = 0;
+    if (st == HL_OK && hipMemcpy(&stalled, pf + 1, sizeof(stalled), hipMemcpyDeviceToHost) != hipSuccess) st = HL_ERR_HIP;
+    if (st == HL_OK && stalled) st = HL_ERR_UNSUPPORTED;  // two of the streams share a hardware queue
+  }
   if (st != HL_OK) {
     hl_pipeline_destroy(p);
     return st;
