@@ -200,7 +200,10 @@ def main():
         dmeas.append(to_device(b, dev, W.make_dy(w, i, b.n_bags)))
     max_l = max(b.n_lookups for b in prof + meas)
     # (the study's smaller hot sets leave up to every row of a mini-batch cold)
-    hp = HotPath(w, rows, table, max_l, w.batch, device=dev, staging_cap=max_l if args.fetch_study else None)
+    # (a counter run serializes dispatches, so its path takes no masked streams:
+    # their flag handovers, and the pipeline's check of them, would stall)
+    hp = HotPath(w, rows, table, max_l, w.batch, device=dev, staging_cap=max_l if args.fetch_study else None,
+                 fetch_cus=0 if args.pmc else 8)
     log(f"[bench] inputs resident; workspace {hp.ws.numel() / 2**20:.1f} MiB, hot cache {k_cap} rows")
 
     # learning phase

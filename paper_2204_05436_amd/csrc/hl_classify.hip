@@ -166,16 +166,17 @@ pt_emit(const uint8_t* __restrict__ flags, int32_t n, int32_t tile, const uint32
   }
 }
 
-// Up to PT_ONE samples: one block, every flag loaded at once (PT_ONE / 1024 per
-// thread); the popular counts of every (chunk of 1024, wave) go to LDS, one
+// Up to PT_ONE samples: one block, every flag loaded at once (up to PT_ONE / 1024
+// per thread); the popular counts of every (chunk of 1024, wave) go to LDS, one
 // wave scans them in (chunk, wave) order, which is index order, and every
 // sample is then placed: one launch, two barriers.
 #define PT_ONE 16384
+template <int K>  // chunks of 1024 (1, 4 or 16: at most 4 counts per lane of one wave)
 __global__ void __launch_bounds__(1024)
 pt_one(const uint8_t* __restrict__ flags, int32_t n, int32_t* __restrict__ pop, int32_t* __restrict__ nonpop,
        int32_t* counts) {
-  constexpr int K = PT_ONE / 1024;  // chunks; K * 16 = 4 counts per lane of one wave
-  __shared__ uint32_t wt[K * 16];
+  constexpr int PL = (K * 16 + 63) / 64;  // counts per lane of the scanning wave
+  __shared__ uint32_t wt[PL * 64];
   __shared__ uint32_t s_total;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const uint64_t lt = (1ull << lane) - 1ull;
@@ -192,10 +193,10 @@ pt_one(const uint8_t* __restrict__ flags, int32_t n, int32_t* __restrict__ pop, 
   }
   __syncthreads();
   if (w == 0) {
-    uint32_t v[4], sum = 0;
+    uint32_t v[PL], sum = 0;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      v[j] = wt[lane * 4 + j];
+    for (int j = 0; j < PL; ++j) {
+      v[j] = lane * PL + j < K * 16 ? wt[lane * PL + j] : 0u;
       sum += v[j];
     }
     uint32_t x = sum;
@@ -206,8 +207,8 @@ pt_one(const uint8_t* __restrict__ flags, int32_t n, int32_t* __restrict__ pop, 
     }
     uint32_t run = x - sum;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      wt[lane * 4 + j] = run;
+    for (int j = 0; j < PL; ++j) {
+      if (lane * PL + j < K * 16) wt[lane * PL + j] = run;
       run += v[j];
     }
     if (lane == 63) s_total = x;
@@ -239,7 +240,9 @@ extern "C" hl_status hl_partition(hl_handle* h, const uint8_t* flags, int32_t n,
   if (!h || n < 0 || !counts || (n > 0 && (!flags || !pop || !nonpop))) return HL_ERR_INVALID_ARG;
   hipStream_t s = (hipStream_t)stream;
   if (n <= PT_ONE) {
-    HL_KERNEL(h, s, "pt_one", pt_one, dim3(1), dim3(1024), 0, s, flags, n, pop, nonpop, counts);
+    if (n <= 1024) HL_KERNEL(h, s, "pt_one", pt_one<1>, dim3(1), dim3(1024), 0, s, flags, n, pop, nonpop, counts);
+    else if (n <= 4096) HL_KERNEL(h, s, "pt_one", pt_one<4>, dim3(1), dim3(1024), 0, s, flags, n, pop, nonpop, counts);
+    else HL_KERNEL(h, s, "pt_one", pt_one<16>, dim3(1), dim3(1024), 0, s, flags, n, pop, nonpop, counts);
     HL_LAUNCHED();
     return HL_OK;
   }

@@ -452,7 +452,7 @@ def test_empty_batch():
         table.close()
 
 
-@pytest.mark.parametrize("n", [1, 1023, 1025, 8192, 16384, 16385, 200_003, 1_300_007])
+@pytest.mark.parametrize("n", [1, 1023, 1024, 1025, 4096, 4097, 8192, 16384, 16385, 200_003, 1_300_007])
 def test_partition_sizes(n):
     """One block for up to 16K samples (the flags in registers), then 1K
     tiles, and more than 1M samples (64K tiles)."""
