@@ -341,6 +341,15 @@ ds_kernel(const uint32_t* __restrict__ rows, const int32_t* __restrict__ bag_ptr
   const int64_t bg0 = s0 * bps;
   const int nbg = ns * bps;
   for (int j = tid; j <= nbg; j += DS_THREADS) off[j] = bag_ptr[bg0 + j];
+  // the first round's rows, loaded before the offsets reach LDS (their range
+  // needs only the block's first and last offsets)
+  const int32_t lo0 = bag_ptr[bg0], hi0 = (int32_t)min((int64_t)bag_ptr[bg0 + nbg], n_lookups);
+  uint32_t r0[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int32_t i = lo0 + tid + k * DS_THREADS;
+    r0[k] = i < hi0 ? rows[i] : 0u;
+  }
   for (int j = tid; j < ns; j += DS_THREADS) fl[j] = 1;
   for (int j = tid; j < n_tables; j += DS_THREADS) {
     tb_base[j] = base[j];
@@ -366,6 +375,7 @@ ds_kernel(const uint32_t* __restrict__ rows, const int32_t* __restrict__ bag_ptr
   const float inv_t = 1.0f / (float)n_tables, inv_b = 1.0f / (float)bps;
   // 4 lookups per thread per round, their loads issued together
   for (int32_t i0 = lo + tid; i0 < hi; i0 += 4 * DS_THREADS) {
+    const bool first = i0 == lo + tid;
     int a[4];
     uint32_t r[4];
 #pragma unroll
@@ -381,7 +391,7 @@ ds_kernel(const uint32_t* __restrict__ rows, const int32_t* __restrict__ bag_ptr
           }
       }
       a[k] = x;
-      r[k] = i < hi ? rows[i] : 0u;
+      r[k] = first ? r0[k] : (i < hi ? rows[i] : 0u);
     }
     uint32_t g[4];
 #pragma unroll
