@@ -285,9 +285,11 @@ extern "C" hl_status hl_host_free(void* host) {
 }
 
 // ----------------------------------------------------------------------------- gids
-// Block = 256 bags; their lookups are contiguous.  Threads walk the lookups and
-// find their bag by binary search over the block's bag offsets in LDS.
-#define GIDS_BAGS 256
+// Block = GIDS_BAGS bags; their lookups are contiguous.  Threads walk the
+// lookups, four at a time with their row loads issued together, and find each
+// one's bag by binary search over the block's bag offsets in LDS.  (The call
+// knows bags, not lookups: 64 bags keep multi-hot blocks at ~1300 lookups.)
+#define GIDS_BAGS 64
 __global__ void __launch_bounds__(256)
 hl_k_gids(const uint32_t* __restrict__ rows, const int32_t* __restrict__ bag_ptr, int64_t n_bags,
           const uint32_t* __restrict__ base, const uint32_t* __restrict__ nrow, int32_t n_tables,
@@ -298,19 +300,30 @@ hl_k_gids(const uint32_t* __restrict__ rows, const int32_t* __restrict__ bag_ptr
   for (int j = threadIdx.x; j <= nb; j += blockDim.x) off[j] = bag_ptr[b0 + j];
   __syncthreads();
   const int32_t lo = off[0], hi = off[nb];
-  for (int32_t i = lo + threadIdx.x; i < hi; i += blockDim.x) {
-    int a = 0, b = nb;  // off[a] <= i < off[b]
-    while (b - a > 1) {
-      int m = (a + b) >> 1;
-      if (off[m] <= i) a = m; else b = m;
+  // 4 lookups per thread at a time, their row loads issued together
+  for (int32_t i0 = lo + threadIdx.x; i0 < hi; i0 += 4 * (int32_t)blockDim.x) {
+    uint32_t r[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int32_t i = i0 + k * (int32_t)blockDim.x;
+      r[k] = i < hi ? rows[i] : 0u;
     }
-    const int32_t t = (int32_t)((b0 + a) % n_tables);
-    const uint32_t r = rows[i];
-    if (r < nrow[t]) {
-      gids[i] = base[t] + r;
-    } else {
-      gids[i] = 0xFFFFFFFFu;
-      hl_flag(err, HL_DEVERR_OUT_OF_RANGE);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int32_t i = i0 + k * (int32_t)blockDim.x;
+      if (i >= hi) continue;
+      int a = 0, b = nb;  // off[a] <= i < off[b]
+      while (b - a > 1) {
+        int m = (a + b) >> 1;
+        if (off[m] <= i) a = m; else b = m;
+      }
+      const int32_t t = (int32_t)((b0 + a) % n_tables);
+      if (r[k] < nrow[t]) {
+        gids[i] = base[t] + r[k];
+      } else {
+        gids[i] = 0xFFFFFFFFu;
+        hl_flag(err, HL_DEVERR_OUT_OF_RANGE);
+      }
     }
   }
 }
