@@ -25,7 +25,8 @@
 
 #define CG_C_NCOLD 1
 #define CG_C_RTILE 2
-#define CG_BAGS 256      // bags per insert block
+#define CG_BAGS 256      // bags per insert block (at most; fewer for bags of many lookups)
+#define CG_BAGS_MIN 64
 #define CG_IR 1024       // lookup positions per insert round (256 threads x 4)
 #define CG_RT_THREADS 512
 #define CG_RT (CG_RT_THREADS * 4)  // lookups per rank tile
@@ -34,7 +35,7 @@ struct cg_ws {
   uint32_t* ctr;      // header counters
   uint32_t* uidx;     // [S] staging row of the id in the slot
   uint32_t* slotof;   // [n_max] slot of a cold lookup
-  uint32_t* blist;    // [n_max] cold lookups of insert block b at [bag_ptr[b * CG_BAGS], ...)
+  uint32_t* blist;    // [n_max] cold lookups of insert block b at [bag_ptr[b * bpb], ...)
   uint32_t* bcnt;     // [iblocks] their number
   uint32_t* fst;      // [n_max] id of staging row u
   uint64_t* rstat;    // [rtiles] look-back status of the rank scan
@@ -51,7 +52,7 @@ static uint32_t cg_table_slots(uint32_t n_max) {
 static void cg_carve(hl_carver& c, cg_ws& ws, uint32_t n_max, int64_t n_bags, int32_t n_samples) {
   ws.S = cg_table_slots(n_max);
   ws.rtiles = n_max ? hl_div_up(n_max, CG_RT) : 1;
-  ws.iblocks = n_bags > 0 ? hl_div_up((uint64_t)n_bags, CG_BAGS) : 1;
+  ws.iblocks = n_bags > 0 ? hl_div_up((uint64_t)n_bags, CG_BAGS_MIN) : 1;
   ws.ctr = c.base ? c.header() + HL_HDR_COLD : nullptr;
   ws.uidx = c.take<uint32_t>(ws.S);
   ws.slotof = c.take<uint32_t>(n_max);
@@ -107,14 +108,14 @@ __global__ void cg_mask(uint8_t* mask, int32_t n_samples, const int32_t* __restr
 
 __global__ void __launch_bounds__(256)
 cg_insert(const uint32_t* __restrict__ gids, const int32_t* __restrict__ codes, const int32_t* __restrict__ bag_ptr,
-          int64_t n_bags, int32_t bps, const uint8_t* __restrict__ mask, uint32_t n_lookups, uint64_t n_rows,
-          uint64_t* table, cg_ws ws, uint32_t* err) {
+          int64_t n_bags, int32_t bps, int32_t bpb, const uint8_t* __restrict__ mask, uint32_t n_lookups,
+          uint64_t n_rows, uint64_t* table, cg_ws ws, uint32_t* err) {
   __shared__ int32_t off[CG_BAGS + 1];
   __shared__ uint32_t cl[CG_IR], cg_[CG_IR];
   __shared__ uint32_t wn[4];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int64_t b0 = (int64_t)blockIdx.x * CG_BAGS;
-  const int nb = (int)min((int64_t)CG_BAGS, n_bags - b0);
+  const int64_t b0 = (int64_t)blockIdx.x * bpb;
+  const int nb = (int)min((int64_t)bpb, n_bags - b0);
   for (int j = tid; j <= nb; j += 256) off[j] = bag_ptr[b0 + j];
   __syncthreads();
   const int32_t lo = off[0], hi = (int32_t)min((int64_t)off[nb], (int64_t)n_lookups);
@@ -270,13 +271,13 @@ cg_rank(const uint32_t* __restrict__ gids, const int32_t* __restrict__ codes, ui
 // rows and free their table slots; cold_ids[u] = id of staging row u.  When
 // the rows do not fit: only the capacity bit and the slot clearing.
 __global__ void __launch_bounds__(256)
-cg_codes(const int32_t* __restrict__ bag_ptr, uint64_t* table, cg_ws ws, int32_t cap, uint32_t k_cap,
+cg_codes(const int32_t* __restrict__ bag_ptr, int32_t bpb, uint64_t* table, cg_ws ws, int32_t cap, uint32_t k_cap,
          int32_t* __restrict__ codes, uint32_t* __restrict__ cold_ids, uint32_t* err) {
   const uint32_t ncold = ws.ctr[CG_C_NCOLD];
   const bool fits = ncold <= (uint32_t)cap;
   if (blockIdx.x == 0 && threadIdx.x == 0 && !fits) hl_flag(err, HL_DEVERR_CAPACITY);
   const uint32_t cnt = ws.bcnt[blockIdx.x];
-  const int32_t lo = bag_ptr[(int64_t)blockIdx.x * CG_BAGS];
+  const int32_t lo = bag_ptr[(int64_t)blockIdx.x * bpb];
   for (uint32_t e = threadIdx.x; e < cnt; e += 256) {
     const uint32_t i = ws.blist[lo + e];
     const uint32_t sl = ws.slotof[i];
@@ -400,17 +401,20 @@ extern "C" hl_status hl_cold_plan(hl_handle* h, const uint32_t* gids, int32_t* c
   }
   // without a list the first n_sel_max samples are selected: their bags come first
   const int64_t sel_bags = sample_ids ? n_bags : (int64_t)n_sel_max * bps;
-  const uint32_t ib = sel_bags > 0 ? hl_div_up((uint64_t)sel_bags, CG_BAGS) : 0;
+  // bags per insert block: about 2048 lookups, CG_BAGS_MIN to CG_BAGS bags
+  int32_t bpb = CG_BAGS;
+  while (bpb > CG_BAGS_MIN && (int64_t)bpb * n > 2048 * n_bags) bpb >>= 1;
+  const uint32_t ib = sel_bags > 0 ? hl_div_up((uint64_t)sel_bags, bpb) : 0;
   if (ib > 0)
-    HL_KERNEL(h, s, "cg_insert", cg_insert, dim3(ib), dim3(256), 0, s, gids, codes, bag_ptr, sel_bags, bps, mask, n,
-              h->n_rows, table, ws, h->d_err);
+    HL_KERNEL(h, s, "cg_insert", cg_insert, dim3(ib), dim3(256), 0, s, gids, codes, bag_ptr, sel_bags, bps, bpb, mask,
+              n, h->n_rows, table, ws, h->d_err);
   // the insert kernel cleared the status words, so one fixed tag serves every
   // call (and every replay of a captured graph)
   const uint32_t epoch = 1;
   HL_KERNEL(h, s, "cg_rank", cg_rank, dim3(ws.rtiles), dim3(CG_RT_THREADS), 0, s, gids, codes, ib > 0 ? n : 0u, table, ws,
             n_cold_dev, epoch, nullptr, 0, 0, h->d_err);
   if (ib > 0)
-    HL_KERNEL(h, s, "cg_codes", cg_codes, dim3(ib), dim3(256), 0, s, bag_ptr, table, ws, cap, h->k_cap, codes,
+    HL_KERNEL(h, s, "cg_codes", cg_codes, dim3(ib), dim3(256), 0, s, bag_ptr, bpb, table, ws, cap, h->k_cap, codes,
               cold_ids_out, h->d_err);
   HL_LAUNCHED();
   return HL_OK;
