@@ -1591,7 +1591,7 @@ hl_status hl_embbag_bwd_plan_signal(hl_handle* h, int32_t stg_rows, int32_t* cod
     *sent = sflag != nullptr;
   } else {
     if ((uint64_t)n_lookups > ws.sort.n_max) return HL_ERR_CAPACITY;
-    const hl_sort_geom sg = hl_sort_geometry((uint32_t)n_lookups, bits);
+    const hl_sort_geom sg = hl_sort_geometry((uint32_t)n_lookups, bits, hl_stream_cus(s));
     // bags per writer block: up to about 8192 lookups each, 64 to BPH_BAGS bags
     int32_t bpb = BPH_BAGS;
     while (bpb > 64 && (int64_t)bpb * n_lookups > 8192 * n_bags) bpb >>= 1;

@@ -369,7 +369,8 @@ hl_status hl_group_by_table(hl_handle* h, int32_t* codes, const int32_t* bag_ptr
 #define HL_SORT_THREADS 512
 #define HL_SORT_WAVES (HL_SORT_THREADS / 64)
 // items per thread of a pass block: 4, 6 or 12 (the fewest that keep the
-// tiles to HL_SORT_TILES_AIM, so a small sort still spreads over the chip)
+// tiles to HL_SORT_TILES_AIM and to the stream's compute units, so a small
+// sort still spreads over the units it has, in one round of blocks)
 #define HL_SORT_TILE_MIN (HL_SORT_THREADS * 4)
 #define HL_SORT_TILE_MAX (HL_SORT_THREADS * 12)
 #define HL_SORT_TILES_AIM 128
@@ -409,7 +410,11 @@ struct hl_sort_geom {
   uint32_t hist_blocks;
   uint64_t n_zero;
 };
-hl_sort_geom hl_sort_geometry(uint32_t n_host, int bits);
+// cus: compute units of the stream the sort runs on (its mask; 0: unknown),
+// which cap the tiles (one pass block per unit)
+hl_sort_geom hl_sort_geometry(uint32_t n_host, int bits, int cus);
+// Compute units in a stream's mask (0 if it cannot be read).
+int hl_stream_cus(hipStream_t s);
 // The digit passes of hl_sort_pairs, once the counts and the cleared status
 // words are in place (hl_sort_geometry); same contract otherwise.
 hl_status hl_sort_passes(hl_handle* h, hl_sort_ws& ws, const uint32_t* n_dev, uint32_t n_host, int bits,

@@ -344,7 +344,15 @@ void hl_sort_result(const hl_sort_ws& ws, int bits, uint32_t** out_k, uint32_t**
   *out_v = odd ? ws.v1 : ws.v0;
 }
 
-hl_sort_geom hl_sort_geometry(uint32_t n_host, int bits) {
+int hl_stream_cus(hipStream_t s) {
+  uint32_t m[16] = {0};
+  if (hipExtStreamGetCUMask(s, 16, m) != hipSuccess) return 0;
+  int c = 0;
+  for (uint32_t w : m) c += __builtin_popcount(w);
+  return c;
+}
+
+hl_sort_geom hl_sort_geometry(uint32_t n_host, int bits, int cus) {
   const srt_plan pl = srt_make_plan(bits);
   hl_sort_geom g;
   g.passes = pl.passes;
@@ -352,9 +360,10 @@ hl_sort_geom hl_sort_geometry(uint32_t n_host, int bits) {
   g.nb = pl.nb;
   const uint32_t hb = hl_div_up(n_host, HL_SORT_HIST_THREADS * 8);
   g.hist_blocks = hb < 1 ? 1 : (hb > HL_SORT_HIST_BLOCKS ? HL_SORT_HIST_BLOCKS : hb);
+  const uint32_t aim = cus > 0 && cus < HL_SORT_TILES_AIM ? (uint32_t)cus : HL_SORT_TILES_AIM;
   g.items = 12;
   for (int it : {4, 6})
-    if (hl_div_up(n_host, HL_SORT_THREADS * it) <= HL_SORT_TILES_AIM) {
+    if (hl_div_up(n_host, HL_SORT_THREADS * it) <= aim) {
       g.items = it;
       break;
     }
@@ -366,7 +375,7 @@ hl_sort_geom hl_sort_geometry(uint32_t n_host, int bits) {
 template <int NB>
 static hl_status srt_hist_launch(hl_handle* h, hl_sort_ws& ws, const uint32_t* n_dev, uint32_t n_host, int bits,
                                  hipStream_t s) {
-  const hl_sort_geom g = hl_sort_geometry(n_host, bits);
+  const hl_sort_geom g = hl_sort_geometry(n_host, bits, hl_stream_cus(s));
   HL_KERNEL(h, s, "srt_hist", srt_hist<NB>, dim3(g.hist_blocks), dim3(HL_SORT_HIST_THREADS), 0, s, ws.k0, n_dev,
             n_host, g.passes, g.b, ws.part, ws.st[0], g.n_zero);
   HL_LAUNCHED();
@@ -376,7 +385,7 @@ static hl_status srt_hist_launch(hl_handle* h, hl_sort_ws& ws, const uint32_t* n
 template <int NB, int ITEMS>
 static hl_status srt_launch(hl_handle* h, hl_sort_ws& ws, const uint32_t* n_dev, uint32_t n_host, int bits,
                             hipStream_t s) {
-  const hl_sort_geom g = hl_sort_geometry(n_host, bits);
+  const hl_sort_geom g = hl_sort_geometry(n_host, bits, hl_stream_cus(s));
   const uint32_t tiles = hl_div_up(n_host, g.tile);
   uint32_t *ki = ws.k0, *vi = ws.v0, *ko = ws.k1, *vo = ws.v1;
   for (int p = 0; p < g.passes; ++p) {
@@ -408,7 +417,7 @@ hl_status hl_sort_passes(hl_handle* h, hl_sort_ws& ws, const uint32_t* n_dev, ui
   if (n_host == 0) return HL_OK;
   hl_status st = srt_check(ws, n_host, bits);
   if (st != HL_OK) return st;
-  const hl_sort_geom g = hl_sort_geometry(n_host, bits);
+  const hl_sort_geom g = hl_sort_geometry(n_host, bits, hl_stream_cus(s));
 #define SRT(NB)                                                                       \
   (g.items == 4 ? srt_launch<NB, 4>(h, ws, n_dev, n_host, bits, s)                    \
                 : g.items == 6 ? srt_launch<NB, 6>(h, ws, n_dev, n_host, bits, s)     \
