@@ -64,18 +64,22 @@ typedef enum { HL_F32 = 0, HL_BF16 = 1 } hl_dtype;
 typedef struct hl_handle hl_handle;
 typedef void* hl_stream; /* hipStream_t */
 
-const char* hl_status_string(hl_status s);
+/* A static string naming status s; any int32 value is accepted (an unknown
+ * one gives "unknown status"). */
+const char* hl_status_string(int32_t s);
 
 /* ---------------------------------------------------------------- handle --
  * Tables and their base registers: the accelerator's Address Registers hold
  * each table's base (Sec. V-A "Data Dispatcher"; s_wr of the ISA table).
  * rows_per_table (host, n_tables entries) fixes gid = base[t] + row; total
  * rows must be < 2^32-1.  k_cap is the hot-cache capacity in rows (>= 1).
+ * dtype is one of hl_dtype's values, passed as a plain int32 so that any value
+ * a caller hands over is defined: any other value gives HL_ERR_INVALID_ARG.
  * Allocates the handle's device state on the current device: access counts
  * (4 B/row), hot-set bitmap (1 bit/row) and rank directory (4 B per 256 rows).
  * Synchronous. */
 hl_status hl_create(hl_handle** out, int32_t n_tables, const uint32_t* rows_per_table, int32_t dim,
-                    hl_dtype dtype, uint32_t k_cap);
+                    int32_t dtype, uint32_t k_cap);
 hl_status hl_destroy(hl_handle* h);
 uint64_t hl_n_rows(const hl_handle* h);
 uint32_t hl_n_hot(const hl_handle* h);   /* size of the current hot set (host copy) */

@@ -21,21 +21,29 @@ F32, BF16 = 0, 1
 _lib = None
 
 
-def build(force: bool = False) -> str:
-    """Compile the oracle with gcc (single-threaded, fp64, no FMA contraction)."""
-    if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
-        tmp = _LIB + ".tmp%d" % os.getpid()
+# gcc's AddressSanitizer and UndefinedBehaviorSanitizer, any finding fatal
+SAN_FLAGS = ["-g", "-fno-omit-frame-pointer", "-fsanitize=address,undefined",
+             "-fno-sanitize-recover=all"]
+
+
+def build(force: bool = False, out: str | None = None, sanitize: bool = False) -> str:
+    """Compile the oracle with gcc (single-threaded, fp64, no FMA contraction).
+    With ``sanitize`` the copy at ``out`` carries gcc's ASan and UBSan checks; a
+    process that loads it preloads gcc's libasan (``gcc -print-file-name=libasan.so``)."""
+    lib_path = out or _LIB
+    if force or sanitize or not os.path.exists(lib_path) or os.path.getmtime(lib_path) < os.path.getmtime(_SRC):
+        tmp = lib_path + ".tmp%d" % os.getpid()
         subprocess.check_call(["gcc", "-O2", "-ffp-contract=off", "-fno-fast-math", "-std=c99",
-                               "-Wall", "-Wextra", "-shared", "-fPIC", _SRC, "-o", tmp, "-lm"])
-        os.replace(tmp, _LIB)
-    return _LIB
+                               "-Wall", "-Wextra", *(SAN_FLAGS if sanitize else ()),
+                               "-shared", "-fPIC", _SRC, "-o", tmp, "-lm"])
+        os.replace(tmp, lib_path)
+    return lib_path
 
 
 def lib():
     global _lib
     if _lib is None:
-        build()
-        L = C.CDLL(_LIB)
+        L = C.CDLL(build())
         P = C.c_void_p
         i32, i64, u32, u64, f32 = C.c_int32, C.c_int64, C.c_uint32, C.c_uint64, C.c_float
         sig = {

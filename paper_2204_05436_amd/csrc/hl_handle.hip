@@ -15,7 +15,7 @@ size_t hl_cold_ws_bytes(const hl_handle* h, int64_t max_lookups, int64_t max_bag
 size_t hl_bwd_ws_bytes(const hl_handle* h, int64_t max_lookups, int64_t max_bags);
 size_t hl_plan_ws_bytes(const hl_handle* h, int64_t max_lookups, int64_t max_bags, int32_t max_samples);
 
-extern "C" const char* hl_status_string(hl_status s) {
+extern "C" const char* hl_status_string(int32_t s) {
   switch (s) {
     case HL_OK: return "ok";
     case HL_ERR_INVALID_ARG: return "invalid argument";
@@ -151,7 +151,7 @@ hl_status hl_table_bounds(hl_handle* h, hipStream_t s) {
 }
 
 extern "C" hl_status hl_create(hl_handle** out, int32_t n_tables, const uint32_t* rows_per_table,
-                               int32_t dim, hl_dtype dtype, uint32_t k_cap) {
+                               int32_t dim, int32_t dtype, uint32_t k_cap) {
   if (!out || n_tables < 1 || !rows_per_table || dim < 1 || dim > 8192 || k_cap < 1)
     return HL_ERR_INVALID_ARG;
   if (dtype != HL_F32 && dtype != HL_BF16) return HL_ERR_INVALID_ARG;
@@ -168,7 +168,7 @@ extern "C" hl_status hl_create(hl_handle** out, int32_t n_tables, const uint32_t
   h->n_tables = n_tables;
   h->n_rows = total;
   h->dim = dim;
-  h->dtype = dtype;
+  h->dtype = (hl_dtype)dtype;
   h->k_cap = k_cap;
   h->row_bytes = (uint32_t)dim * (dtype == HL_F32 ? 4u : 2u);
   h->n_tiles4k = (total + 4095) / 4096;

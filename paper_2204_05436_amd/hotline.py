@@ -13,7 +13,8 @@ import sys
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libhotline.so")
+# HOTLINE_LIB names another build of the same library (a host-sanitized copy)
+LIB_PATH = os.environ.get("HOTLINE_LIB") or os.path.join(_HERE, "libhotline.so")
 
 HL_F32, HL_BF16 = 0, 1
 STATUS = {0: "ok", 1: "invalid argument", 2: "out of range", 3: "capacity exceeded", 4: "HIP runtime error",

@@ -70,6 +70,9 @@ def test_host_side_validation():
     assert L.hl_eal_access(None, None, 0, None) == 1
     assert L.hl_eal_hot(None, None, None, None) == 1
     assert hl.hl_status_string(3) == "capacity exceeded"
+    assert hl.hl_status_string(99) == "unknown status"
+    assert hl.hl_status_string(-5) == "unknown status"
+    assert L.hl_create(C.byref(h), 2, rows, 4, -1, 1) == 1         # negative dtype
 
 
 def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
