@@ -882,13 +882,58 @@ def cpu_baseline(w, rows, prof, meas, meas_idx, table, k_cap, budget_s):
     finally:
         os.sched_setaffinity(0, aff)
     log(f"[bench] cpu baseline: {done} batch steps in {t_all:.1f}s")
+    mc = cpu_multicore_segregation(rows, hot, meas, min(3.0, budget_s))
     return {"value": L / t_all, "unit": "lookups/s", "cores": 1, "kind": "oracle",
+            "multicore_segregation": mc,
             "classify_samples_per_s": B / stage["classify_partition"],
             "fwd_bwd_lookups_per_s": L / (stage["fwd"] + stage["bwd"]),
             "stage_ms_per_batch": {k: 1e3 * v / done for k, v in stage.items()},
             "sample": f"{done} batch steps of {w.name} (its {len(meas)} measured batches in turn), every per-batch "
                       f"step, single-threaded fp64 oracle pinned to host core {core}",
             "host_cpu": _cpu_model(), "host_nproc": os.cpu_count()}
+
+
+def cpu_multicore_segregation(rows, hot, meas, budget_s):
+    """Labelled multi-core CPU baseline, not the oracle: classify + partition of
+    the same measured batches on the host's cores (OpenMP, at most 16 threads),
+    the CPU-side segregation whose cost Sec. III measures.  The hot-set bitmap
+    is built once, untimed (a learning phase's work); each batch is timed around
+    the C call alone."""
+    import ctypes as C
+    import oracle as O
+
+    n_rows = int(rows.sum(dtype=np.int64))
+    bm, _ = O.mc_hot_bitmap(hot, n_rows)
+    threads = max(1, min(16, len(os.sched_getaffinity(0))))
+    L = O.mc_lib()
+    rpt = np.ascontiguousarray(rows, dtype=np.uint32)
+    nmax = max(mb.n_samples for mb in meas)
+    flags = np.empty(nmax, dtype=np.uint8)
+    pop = np.empty(nmax, dtype=np.int32)
+    nonpop = np.empty(nmax, dtype=np.int32)
+    ptr = lambda a: a.ctypes.data_as(C.c_void_p)
+    calls = []
+    for mb in meas:
+        r = np.ascontiguousarray(mb.rows, dtype=np.uint32)
+        bp = np.ascontiguousarray(mb.bag_ptr, dtype=np.int32)
+        calls.append((r, bp, (len(rpt), ptr(rpt), ptr(r), ptr(bp), mb.n_samples, mb.bags_per_sample, ptr(bm),
+                              threads, ptr(flags), ptr(pop), ptr(nonpop))))
+    for _, _, a in calls[:2]:                       # thread team start-up, untimed
+        L.mc_segregate(*a)
+    t, done, S = 0.0, 0, 0
+    while t < budget_s:
+        _, _, a = calls[done % len(calls)]
+        t0 = time.perf_counter()
+        npop = L.mc_segregate(*a)
+        t += time.perf_counter() - t0
+        if npop < 0:
+            raise SystemExit("multi-core segregation: bad argument")
+        S += a[4]
+        done += 1
+    log(f"[bench] multi-core segregation: {done} batches on {threads} threads in {t:.2f}s")
+    return {"value": S / t, "unit": "samples/s", "cores": threads, "kind": "openmp classify+partition, not the oracle",
+            "us_per_batch": 1e6 * t / done,
+            "sample": f"{done} classify+partition calls over the measured batches in turn, {threads} OpenMP threads"}
 
 
 def _cpu_model():

@@ -4,6 +4,10 @@ Only the test-suite, the smoke check and the benchmark's CPU-baseline leg may
 import this package.  It shares no code with the HIP library and never calls
 it.  Every function takes and returns numpy arrays; the arithmetic is all in
 the C file.
+
+``mc_*`` wrap cpu_segregation_mc.c, which is not the oracle: a multi-core
+(OpenMP) classify + partition that the benchmark reports as a labelled CPU
+baseline, checked bit for bit against the oracle by the tests.
 """
 from __future__ import annotations
 
@@ -16,6 +20,8 @@ import numpy as np
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "hotline_oracle.c")
 _LIB = os.path.join(_HERE, "liboracle.so")
+_MC_SRC = os.path.join(_HERE, "cpu_segregation_mc.c")
+_MC_LIB = os.path.join(_HERE, "libcpuseg_mc.so")
 F32, BF16 = 0, 1
 
 _lib = None
@@ -37,7 +43,19 @@ def build(force: bool = False, out: str | None = None, sanitize: bool = False) -
                                "-Wall", "-Wextra", *(SAN_FLAGS if sanitize else ()),
                                "-shared", "-fPIC", _SRC, "-o", tmp, "-lm"])
         os.replace(tmp, lib_path)
+    if out is None and not sanitize:
+        build_mc(force)
     return lib_path
+
+
+def build_mc(force: bool = False) -> str:
+    """Compile the multi-core CPU segregation baseline (OpenMP; not the oracle)."""
+    if force or not os.path.exists(_MC_LIB) or os.path.getmtime(_MC_LIB) < os.path.getmtime(_MC_SRC):
+        tmp = _MC_LIB + ".tmp%d" % os.getpid()
+        subprocess.check_call(["gcc", "-O2", "-fopenmp", "-std=c99", "-Wall", "-Wextra", "-shared", "-fPIC",
+                               _MC_SRC, "-o", tmp])
+        os.replace(tmp, _MC_LIB)
+    return _MC_LIB
 
 
 def lib():
@@ -74,6 +92,47 @@ def lib():
             fn.argtypes = args
         _lib = L
     return _lib
+
+
+_mc = None
+
+
+def mc_lib():
+    """The multi-core segregation baseline (cpu_segregation_mc.c)."""
+    global _mc
+    if _mc is None:
+        L = C.CDLL(build_mc())
+        P = C.c_void_p
+        L.mc_hot_bitmap.restype = C.c_int
+        L.mc_hot_bitmap.argtypes = [P, C.c_int64, C.c_uint64, P]
+        L.mc_segregate.restype = C.c_int32
+        L.mc_segregate.argtypes = [C.c_int32, P, P, P, C.c_int32, C.c_int32, P, C.c_int32, P, P, P]
+        _mc = L
+    return _mc
+
+
+def mc_hot_bitmap(hot_ids, n_rows):
+    hot_ids = _c(hot_ids, np.uint32)
+    bm = np.empty((int(n_rows) + 63) // 64, dtype=np.uint64)
+    rc = mc_lib().mc_hot_bitmap(_p(hot_ids), len(hot_ids), int(n_rows), _p(bm))
+    return bm, rc
+
+
+def mc_segregate(rows_per_table, rows, bag_ptr, n_samples, bps, bm, n_threads, out=None):
+    """(flags, pop, nonpop) of the multi-core segregation; ``out`` may hold
+    preallocated (flags, pop, nonpop) arrays of n_samples entries."""
+    rpt = _c(rows_per_table, np.uint32)
+    rows = _c(rows, np.uint32)
+    bag_ptr = _c(bag_ptr, np.int32)
+    if out is None:
+        out = (np.empty(n_samples, dtype=np.uint8), np.empty(n_samples, dtype=np.int32),
+               np.empty(n_samples, dtype=np.int32))
+    flags, pop, nonpop = out
+    npop = mc_lib().mc_segregate(len(rpt), _p(rpt), _p(rows), _p(bag_ptr), n_samples, bps, _p(bm),
+                                 n_threads, _p(flags), _p(pop), _p(nonpop))
+    if npop < 0:
+        raise ValueError("mc_segregate: bad argument")
+    return flags[:n_samples], pop[:npop], nonpop[: n_samples - npop]
 
 
 def _p(a):
