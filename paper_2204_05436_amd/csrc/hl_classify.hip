@@ -310,6 +310,9 @@ extern "C" hl_status hl_remap(const hl_handle* h, const uint32_t* gids, int64_t 
 #define DS_MAX_TABLES 1024  // table bases and sizes in LDS up to this many tables
 #define DS_MAX_BAGS 4096
 #define DS_MAX_SPB 2048
+#define DS_LOOKUPS_MIN 512  // lookups per block: n_lookups / DS_BLOCKS_AIM within these bounds
+#define DS_LOOKUPS_MAX 2048
+#define DS_BLOCKS_AIM 64
 #define DS_MAP 8192         // lookups per block mapped to their bag in LDS
 #define DS_EPOCH 0
 #define DS_DONE 1
@@ -468,8 +471,11 @@ ds_kernel(const uint32_t* __restrict__ rows, const int32_t* __restrict__ bag_ptr
 // step calls
 static int64_t ds_spb(const hl_handle* h, int32_t n_samples, int32_t bps, int64_t n_lookups, const void* workspace,
                       size_t ws_bytes) {
-  // about 2048 lookups per block, at most DS_MAX_BAGS bags
-  int64_t spb = n_lookups > 0 ? (2048ll * n_samples + n_lookups - 1) / n_lookups : DS_MAX_SPB;
+  // About 64 blocks: fewer leave a small mini-batch's dependent loads to a few
+  // CUs, more lengthen the look-back chain and the cold inserts' contention.
+  int64_t lpb = n_lookups / DS_BLOCKS_AIM;
+  lpb = lpb < DS_LOOKUPS_MIN ? DS_LOOKUPS_MIN : (lpb > DS_LOOKUPS_MAX ? DS_LOOKUPS_MAX : lpb);
+  int64_t spb = n_lookups > 0 ? (lpb * n_samples + n_lookups - 1) / n_lookups : DS_MAX_SPB;
   const int64_t bag_cap = DS_MAX_BAGS / bps;
   if (spb > bag_cap) spb = bag_cap;
   if (spb > DS_MAX_SPB) spb = DS_MAX_SPB;
