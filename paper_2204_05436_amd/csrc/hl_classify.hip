@@ -23,7 +23,8 @@ cl_kernel(const uint32_t* __restrict__ gids, const int32_t* __restrict__ bag_ptr
   if (blockIdx.x == 0 && threadIdx.x == 0 && bag_ptr[(int64_t)n_samples * bps] != n_lookups)
     hl_flag(err, HL_DEVERR_SHAPE);
   __syncthreads();
-  const int32_t lo = off[0], hi = off[ns];
+  // a bag_ptr that overruns n_lookups is flagged above; no id past n_lookups is read
+  const int32_t lo = (int32_t)min((int64_t)off[0], n_lookups), hi = (int32_t)min((int64_t)off[ns], n_lookups);
   // CL_U lookups per thread at a time: their ids, then their bitmap words, in flight together
   for (int32_t i0 = lo + threadIdx.x; i0 < hi; i0 += CL_U * blockDim.x) {
     uint32_t g[CL_U];
@@ -52,6 +53,12 @@ cl_kernel(const uint32_t* __restrict__ gids, const int32_t* __restrict__ bag_ptr
   for (int j = threadIdx.x; j < ns; j += blockDim.x) flags[s0 + j] = fl[j];
 }
 
+// samples per classify block: about 512 lookups
+static int64_t cl_spb(int32_t n_samples, int64_t n_lookups) {
+  int64_t spb = n_lookups > 0 ? (512ll * n_samples + n_lookups - 1) / n_lookups : CL_MAX_SPB;
+  return spb < 1 ? 1 : (spb > CL_MAX_SPB ? CL_MAX_SPB : spb);
+}
+
 extern "C" hl_status hl_classify(const hl_handle* h, const uint32_t* gids, const int32_t* bag_ptr,
                                  int32_t n_samples, int32_t bps, int64_t n_lookups, uint8_t* flags,
                                  hl_stream stream) {
@@ -59,9 +66,7 @@ extern "C" hl_status hl_classify(const hl_handle* h, const uint32_t* gids, const
   if (n_samples == 0) return HL_OK;
   if (!bag_ptr || !flags || (n_lookups > 0 && !gids)) return HL_ERR_INVALID_ARG;
   if ((int64_t)n_samples * bps >= (1ll << 31)) return HL_ERR_UNSUPPORTED;
-  // about 512 lookups per block
-  int64_t spb = n_lookups > 0 ? (512ll * n_samples + n_lookups - 1) / n_lookups : CL_MAX_SPB;
-  spb = spb < 1 ? 1 : (spb > CL_MAX_SPB ? CL_MAX_SPB : spb);
+  const int64_t spb = cl_spb(n_samples, n_lookups);
   hipStream_t s = (hipStream_t)stream;
   HL_KERNEL(h, s, "cl_kernel", cl_kernel, dim3(hl_div_up(n_samples, spb)), dim3(256), 0, s, gids,
                      bag_ptr, n_samples, bps, (int32_t)spb, h->d_bitmap, h->n_rows, flags, n_lookups,
