@@ -171,62 +171,70 @@ pt_emit(const uint8_t* __restrict__ flags, int32_t n, int32_t tile, const uint32
   }
 }
 
-// Up to PT_ONE samples: one block, every flag loaded at once (up to PT_ONE / 1024
-// per thread); the popular counts of every (chunk of 1024, wave) go to LDS, one
-// wave scans them in (chunk, wave) order, which is index order, and every
-// sample is then placed: one launch, two barriers.
+// Up to PT_ONE samples: one block; a thread holds 4 consecutive flags of each
+// chunk of 4096 (one 4-byte load when the flags are 4-byte aligned), a wave
+// scan gives each thread the popular samples before its 4 within the wave,
+// the totals of every (chunk, wave) go to LDS, one wave scans them in (chunk,
+// wave) order, which is index order, and every sample is then placed: one
+// launch, two barriers.
 #define PT_ONE 16384
-template <int K>  // chunks of 1024 (1, 4 or 16: at most 4 counts per lane of one wave)
+template <int C>  // chunks of 4096 samples (1, 2 or 4): each thread holds 4 consecutive samples of a chunk
 __global__ void __launch_bounds__(1024)
-pt_one(const uint8_t* __restrict__ flags, int32_t n, int32_t* __restrict__ pop, int32_t* __restrict__ nonpop,
-       int32_t* counts) {
-  constexpr int PL = (K * 16 + 63) / 64;  // counts per lane of the scanning wave
-  __shared__ uint32_t wt[PL * 64];
+pt_one(const uint8_t* __restrict__ flags, int32_t n, int aligned, int32_t* __restrict__ pop,
+       int32_t* __restrict__ nonpop, int32_t* counts) {
+  __shared__ uint32_t wt[C * 16];
   __shared__ uint32_t s_total;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const uint64_t lt = (1ull << lane) - 1ull;
-  bool f[K];
+  uint32_t f[C], ex[C];  // f: the 4 samples' flags as bits 0..3; ex: popular samples before them in the wave
 #pragma unroll
-  for (int k = 0; k < K; ++k) {
-    const int32_t i = k * 1024 + threadIdx.x;
-    f[k] = i < n && flags[i] != 0;
-  }
+  for (int c = 0; c < C; ++c) {
+    const int32_t b = c * 4096 + 4 * (int32_t)threadIdx.x;
+    uint32_t v = 0;
+    if (aligned && b + 3 < n) {
+      const uint32_t x = *reinterpret_cast<const uint32_t*>(flags + b);
 #pragma unroll
-  for (int k = 0; k < K; ++k) {
-    const uint64_t b = __ballot(f[k]);
-    if (lane == 0) wt[k * 16 + w] = (uint32_t)__popcll(b);
-  }
-  __syncthreads();
-  if (w == 0) {
-    uint32_t v[PL], sum = 0;
+      for (int q = 0; q < 4; ++q) v |= (((x >> (8 * q)) & 0xFFu) != 0u ? 1u : 0u) << q;
+    } else {
 #pragma unroll
-    for (int j = 0; j < PL; ++j) {
-      v[j] = lane * PL + j < K * 16 ? wt[lane * PL + j] : 0u;
-      sum += v[j];
+      for (int q = 0; q < 4; ++q) v |= (b + q < n && flags[b + q] != 0 ? 1u : 0u) << q;
     }
-    uint32_t x = sum;
+    f[c] = v;
+  }
+#pragma unroll
+  for (int c = 0; c < C; ++c) {
+    const uint32_t cnt = (uint32_t)__popc(f[c]);
+    uint32_t x = cnt;
 #pragma unroll
     for (int o = 1; o < 64; o <<= 1) {
       const uint32_t y = __shfl_up(x, o);
       if (lane >= o) x += y;
     }
-    uint32_t run = x - sum;
+    ex[c] = x - cnt;
+    if (lane == 63) wt[c * 16 + w] = x;
+  }
+  __syncthreads();
+  if (w == 0) {  // the C*16 wave totals (at most 64, one per lane), scanned in order
+    const uint32_t v = lane < C * 16 ? wt[lane] : 0u;
+    uint32_t x = v;
 #pragma unroll
-    for (int j = 0; j < PL; ++j) {
-      if (lane * PL + j < K * 16) wt[lane * PL + j] = run;
-      run += v[j];
+    for (int o = 1; o < 64; o <<= 1) {
+      const uint32_t y = __shfl_up(x, o);
+      if (lane >= o) x += y;
     }
+    if (lane < C * 16) wt[lane] = x - v;
     if (lane == 63) s_total = x;
   }
   __syncthreads();
 #pragma unroll
-  for (int k = 0; k < K; ++k) {
-    const int32_t i = k * 1024 + threadIdx.x;
-    const uint64_t b = __ballot(f[k]);
-    if (i < n) {
-      const uint32_t before = wt[k * 16 + w] + (uint32_t)__popcll(b & lt);
-      if (f[k]) pop[before] = i;
-      else nonpop[i - before] = i;
+  for (int c = 0; c < C; ++c) {
+    const int32_t b = c * 4096 + 4 * (int32_t)threadIdx.x;
+    uint32_t before = wt[c * 16 + w] + ex[c];  // popular samples before sample b
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int32_t i = b + q;
+      if (i >= n) break;
+      if ((f[c] >> q) & 1u) pop[before++] = i;
+      else nonpop[i - (int32_t)before] = i;
     }
   }
   if (threadIdx.x == 0) {
@@ -245,9 +253,10 @@ extern "C" hl_status hl_partition(hl_handle* h, const uint8_t* flags, int32_t n,
   if (!h || n < 0 || !counts || (n > 0 && (!flags || !pop || !nonpop))) return HL_ERR_INVALID_ARG;
   hipStream_t s = (hipStream_t)stream;
   if (n <= PT_ONE) {
-    if (n <= 1024) HL_KERNEL(h, s, "pt_one", pt_one<1>, dim3(1), dim3(1024), 0, s, flags, n, pop, nonpop, counts);
-    else if (n <= 4096) HL_KERNEL(h, s, "pt_one", pt_one<4>, dim3(1), dim3(1024), 0, s, flags, n, pop, nonpop, counts);
-    else HL_KERNEL(h, s, "pt_one", pt_one<16>, dim3(1), dim3(1024), 0, s, flags, n, pop, nonpop, counts);
+    const int al = ((uintptr_t)flags & 3u) == 0;
+    if (n <= 4096) HL_KERNEL(h, s, "pt_one", pt_one<1>, dim3(1), dim3(1024), 0, s, flags, n, al, pop, nonpop, counts);
+    else if (n <= 8192) HL_KERNEL(h, s, "pt_one", pt_one<2>, dim3(1), dim3(1024), 0, s, flags, n, al, pop, nonpop, counts);
+    else HL_KERNEL(h, s, "pt_one", pt_one<4>, dim3(1), dim3(1024), 0, s, flags, n, al, pop, nonpop, counts);
     HL_LAUNCHED();
     return HL_OK;
   }
